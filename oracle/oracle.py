@@ -1,0 +1,133 @@
+"""numpy <-> C marshalling for the float64 oracle (test infrastructure only).
+
+Every function takes numpy arrays in the library's layouts:
+  idx [B,L,H] int, pi [H,K,N] int, D/b/c [B,L,H,N] complex, h0 [B,H,N]
+complex or None, dy [B,L,H] real, dh_final [B,H,N] complex or None.
+Inputs are promoted to float64 / complex128 (exact for float32 inputs) and
+the results come back as float64 / complex128 arrays.
+"""
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pdssm_oracle.c")
+_LIB = os.path.join(_HERE, "libpdssm_oracle.so")
+_lib = None
+
+
+def oracle_lib_path():
+    return _LIB
+
+
+def build_oracle(force=True):
+    """Compile the oracle with gcc (-O2, plain C11).  Returns the .so path."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-Wall", "-Werror",
+             "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build_oracle(force=True)
+        lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        lib.pdssm_oracle_fwd.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, I, P]
+        lib.pdssm_oracle_bwd.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P, P]
+        lib.pdssm_oracle_compose.argtypes = [I, I, I, I, I, P, P, P, I, P, P]
+        lib.pdssm_oracle_num_chunks.argtypes = [I, I]
+        for f in (lib.pdssm_oracle_fwd, lib.pdssm_oracle_bwd, lib.pdssm_oracle_compose,
+                  lib.pdssm_oracle_num_chunks):
+            f.restype = I
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _cplx(a):
+    return None if a is None else np.ascontiguousarray(a, dtype=np.complex128)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+def _dims(idx, pi, D):
+    B, L, H = idx.shape
+    H2, K, N = pi.shape
+    assert H2 == H and D.shape == (B, L, H, N), (idx.shape, pi.shape, D.shape)
+    return B, L, H, N, K
+
+
+def _check(rc, what):
+    if rc == -1:
+        raise IndexError("%s: idx or pi out of range" % what)
+    if rc != 0:
+        raise ValueError("%s: oracle returned %d" % (what, rc))
+
+
+def oracle_num_chunks(L, chunk):
+    return _load().pdssm_oracle_num_chunks(int(L), int(chunk))
+
+
+def oracle_fwd(idx, pi, D, b, c, h0=None, chunk=0):
+    """Returns (y [B,L,H] f64, h_final [B,H,N] c128, saved [B,H,C,N] c128 or None)."""
+    idx, pi = _i32(idx), _i32(pi)
+    D, b, c, h0 = _cplx(D), _cplx(b), _cplx(c), _cplx(h0)
+    B, L, H, N, K = _dims(idx, pi, D)
+    y = np.empty((B, L, H), np.float64)
+    hf = np.empty((B, H, N), np.complex128)
+    saved = None
+    if chunk > 0:
+        C = oracle_num_chunks(L, chunk)
+        saved = np.empty((B, H, C, N), np.complex128)
+    rc = _load().pdssm_oracle_fwd(B, L, H, N, K, _ptr(idx), _ptr(pi), _ptr(D), _ptr(b),
+                                  _ptr(c), _ptr(h0), _ptr(y), _ptr(hf), int(chunk),
+                                  _ptr(saved))
+    _check(rc, "oracle_fwd")
+    return y, hf, saved
+
+
+def oracle_bwd(idx, pi, D, b, c, dy, h0=None, dh_final=None):
+    """Returns (dD, db, dc [B,L,H,N] c128, dh0 [B,H,N] c128)."""
+    idx, pi = _i32(idx), _i32(pi)
+    D, b, c, h0, dhf = _cplx(D), _cplx(b), _cplx(c), _cplx(h0), _cplx(dh_final)
+    dy = np.ascontiguousarray(dy, dtype=np.float64)
+    B, L, H, N, K = _dims(idx, pi, D)
+    assert dy.shape == (B, L, H)
+    dD = np.empty((B, L, H, N), np.complex128)
+    db = np.empty_like(dD)
+    dc = np.empty_like(dD)
+    dh0 = np.empty((B, H, N), np.complex128)
+    rc = _load().pdssm_oracle_bwd(B, L, H, N, K, _ptr(idx), _ptr(pi), _ptr(D), _ptr(b),
+                                  _ptr(c), _ptr(h0), _ptr(dy), _ptr(dhf), _ptr(dD),
+                                  _ptr(db), _ptr(dc), _ptr(dh0))
+    _check(rc, "oracle_bwd")
+    return dD, db, dc, dh0
+
+
+def oracle_compose(idx, pi, D, chunk):
+    """Returns (pi_out [B,H,C,N] int32, d_out [B,H,C,N] c128) per chunk."""
+    idx, pi, D = _i32(idx), _i32(pi), _cplx(D)
+    B, L, H, N, K = _dims(idx, pi, D)
+    C = oracle_num_chunks(L, chunk)
+    if C < 1:
+        raise ValueError("bad chunk")
+    pm = np.empty((B, H, C, N), np.int32)
+    dm = np.empty((B, H, C, N), np.complex128)
+    rc = _load().pdssm_oracle_compose(B, L, H, N, K, _ptr(idx), _ptr(pi), _ptr(D),
+                                      int(chunk), _ptr(pm), _ptr(dm))
+    _check(rc, "oracle_compose")
+    return pm, dm
