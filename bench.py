@@ -1,0 +1,185 @@
+"""PD-scan benchmark on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
+
+One step = one forward scan (pdssm_scan_fwd: y, h_final, saved chunk states)
+plus one backward scan (pdssm_scan_bwd: dD, db, dc, dh0) over one batch of
+seeded synthetic inputs already resident in HBM.  Prints ONE JSON line.
+
+value = state updates (B*L*H*N) per second of the whole fwd+bwd step.
+roofline = the dominant call's algorithmic bytes (every input read once,
+every output written once) over its average duration, measured with HIP
+events on the stream the kernels are launched on, against the 8 TB/s HBM peak.
+cpu_baseline = the float64 oracle timed on a bounded sample of the same
+workload on this host.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "PD-scan state-updates/s (B*L*H*N) fwd and fwd+bwd; achieved HBM GB/s vs peak"
+
+
+def alg_bytes(w, C, op):
+    """Algorithmic HBM bytes of one call: inputs read once, outputs written once."""
+    B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
+    steps = B * L * H
+    su = steps * N
+    dict_b = H * K * N * 4
+    if op == "fwd":
+        # idx, D, b, c in; y, h_final, saved out
+        return steps * 4 + 3 * su * 8 + dict_b + steps * 4 + B * H * N * 8 + B * H * C * N * 8
+    # idx, dy, D, b, c, saved in; dD, db, dc, dh0 out
+    return steps * 8 + 3 * su * 8 + dict_b + B * H * C * N * 8 + 3 * su * 8 + B * H * N * 8
+
+
+def cpu_baseline(w, inp, target_s=12.0):
+    """Time the oracle (fwd + bwd, float64, one thread) on whole sequences of
+    the workload until about target_s seconds of CPU work are done."""
+    from oracle import oracle_bwd, oracle_fwd
+    from paper_2605_19150_amd.inputs import sub_sequence
+    done_su, t_used, nseq = 0, 0.0, 0
+    seqs = [(bb, hh) for bb in range(w.B) for hh in range(w.H)]
+    for bb, hh in seqs:
+        sub = sub_sequence(inp, bb, hh)
+        t0 = time.perf_counter()
+        oracle_fwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"])
+        oracle_bwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"], sub["dy"])
+        t_used += time.perf_counter() - t0
+        done_su += w.L * w.N
+        nseq += 1
+        if t_used >= target_s:
+            break
+    return {"value": done_su / t_used, "unit": "state-updates/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d sequences (whole L=%d each), fwd+bwd float64, %.1f s"
+                      % (nseq, len(seqs), w.L, t_used)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", choices=["fwd", "bwd", "both"], default="both",
+                    help="profiling aid: launch only one call per step")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="profiling aid: time a plain 1 GiB device copy instead")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
+              "(the PD scan shards by sequence without communication; see DESIGN.md)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_19150_amd import pdssm
+    from paper_2605_19150_amd.inputs import WORKLOADS, workload_inputs
+
+    dev = torch.device("cuda:0")
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(args.warmup):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        print(json.dumps({"copy_bytes": 2 * n, "ms": ms, "GBps": 2 * n / ms / 1e6}))
+        return
+
+    w = WORKLOADS[args.workload]
+    print("bench: workload %d (%s): generating inputs" % (args.workload, w.name), file=sys.stderr,
+          flush=True)
+    inp = workload_inputs(args.workload, seed=0)
+    T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
+    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        if args.only in ("fwd", "both"):
+            s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+        if ev is not None:
+            ev[1].record(stream)
+        if args.only in ("bwd", "both"):
+            s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
+        if ev is not None:
+            ev[2].record(stream)
+
+    if args.only == "bwd":
+        s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    s.check_status()
+    print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    ms_step = float(np.mean([e[0].elapsed_time(e[2]) for e in evs]))
+    s.check_status()
+
+    su = w.state_updates
+    fwd_b, bwd_b = alg_bytes(w, s.C, "fwd"), alg_bytes(w, s.C, "bwd")
+    dom = "bwd" if (bwd_ms >= fwd_ms and args.only != "fwd") else "fwd"
+    dom_ms, dom_b = (bwd_ms, bwd_b) if dom == "bwd" else (fwd_ms, fwd_b)
+    achieved = dom_b / (dom_ms * 1e-3) / 1e9
+    out = {
+        "metric": METRIC,
+        "value": su / (ms_step * 1e-3),
+        "unit": "state-updates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded, shapes and distributions of the named workload)",
+        "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
+                   "chunk": s.chunk, "step": "fwd+bwd" if args.only == "both" else args.only,
+                   "global_batch": w.B, "seq_len": w.L, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "kernel": "pdssm_scan_%s" % dom,
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
+        "fwd": {"ms": fwd_ms, "state_updates_per_s": su / (fwd_ms * 1e-3),
+                "alg_bytes": fwd_b, "alg_GBps": fwd_b / (fwd_ms * 1e-3) / 1e9},
+        "bwd": {"ms": bwd_ms, "state_updates_per_s": su / (bwd_ms * 1e-3),
+                "alg_bytes": bwd_b, "alg_GBps": bwd_b / (bwd_ms * 1e-3) / 1e9},
+        "fwd_bwd_alg_GBps": (fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9,
+        "wall_s_timed": wall,
+        "device": torch.cuda.get_device_name(dev),
+    }
+    if not args.no_cpu_baseline and args.only == "both":
+        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,159 @@
+/*
+ * pdssm.h -- C ABI of the MI355X (gfx950) PD-scan library, libpdssm.so.
+ *
+ * The library computes the forward and backward pass of the structured sparse
+ * linear recurrence of Flash PD-SSM (arXiv 2605.19150):
+ *
+ *   h_t = P_t D_t h_{t-1} + b_t,      y_t = Re( sum_n c_t[n] h_t[n] ),
+ *
+ * per (batch b, head h) sequence, t = 0..L-1, state size N.
+ *   - P_t is column-one-hot (paper Sec. 2.3 column hardmax; Sec. 3.1 eq. (5);
+ *     App. D): it is stored as an int map pi_t of length N, and column j has
+ *     its one in row pi_t[j].  Source entry j of the state is scaled by D_t[j]
+ *     and moved to entry pi_t[j]; entries mapped to the same row add up.
+ *   - pi_t is row k_t = idx[b,t,h] of the per-head dictionary pi[h,:,:]
+ *     (Sec. 3.1 eqs. (5)-(8), hard selection; App. E.2.1 index arrays).
+ *   - D_t is a per-step complex diagonal, b_t the per-step input term
+ *     (App. E.2 recurrence), c_t the readout vector and Re the real readout
+ *     (Sec. 2.1 eq. (1) with psi = Re).
+ *   - Two PD operators compose in linear time (App. E.2 associative operator,
+ *     App. E.3.1 accumulator update): applying (pi1, d1) then (pi2, d2) gives
+ *     (pi2[pi1[j]], d2[pi1[j]] * d1[j]).
+ *   - The sequence is cut into chunks of `chunk` steps (App. E.1 Algorithm 1,
+ *     chunk c = steps [c*chunk, min((c+1)*chunk, L)), last one may be short).
+ *     Only the states entering each chunk ("saved") ever reach memory; the
+ *     per-step states h_t are never written.
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are dense row-major device memory owned by the caller.  Complex
+ *     numbers are interleaved (re, im) float32 pairs (== torch.complex64).
+ *       idx [B,L,H] int32 in [0,K)   pi [H,K,N] int32 in [0,N)
+ *       D, b, c [B,L,H,N] complex    y, dy [B,L,H] float32
+ *       h0, h_final, dh_final, dh0 [B,H,N] complex
+ *       saved [B,H,C,N] complex, C = pdssm_num_chunks(desc)
+ *   - The library never allocates or frees memory and never synchronises.
+ *     Scratch memory comes from the caller as `ws` (at least
+ *     pdssm_workspace_size(desc, op) bytes, 256-byte aligned).  All work is
+ *     enqueued in order on `stream` (a hipStream_t; NULL = default stream)
+ *     and the call returns once it is enqueued.
+ *   - Outputs are overwritten, never accumulated.  Outputs must not overlap
+ *     inputs or each other.  Optional pointers may be NULL.
+ *   - Return value: PDSSM_OK, or a negative pdssm_status detected on the host
+ *     (bad pointer or size, unsupported N or chunk, workspace too small, HIP
+ *     launch failure).  Nothing is enqueued when a host check fails.
+ *   - Index checking is always on: an idx entry outside [0,K) or a pi entry
+ *     outside [0,N) is replaced by 0 inside the kernels (so every memory access
+ *     stays in bounds) and PDSSM_ERR_INDEX is stored to *dev_status (a device
+ *     int the caller zeroes beforehand and reads after synchronising; it is
+ *     never cleared by the library).  Results of an affected sequence are then
+ *     meaningless.  dev_status may be NULL.
+ *   - Complex gradients follow dX = dl/dRe(X) + i*dl/dIm(X) (torch's
+ *     convention) for the loss l = sum_t dy_t*y_t + Re(sum conj(dh_final)*h_L).
+ *   - Supported sizes: N in {8, 16, 32, 64, 128, 256}; 1 <= K <= 256;
+ *     B, L, H >= 1 with B*L*H*N < 2^31; chunk in {16, 32, 64} or 0 (default,
+ *     32) for scan_fwd / scan_bwd; any chunk >= 1 for pdssm_compose_chunks.
+ *   - Calls on different streams may run concurrently if their outputs and
+ *     workspaces do not overlap; the library keeps no mutable global state.
+ */
+#ifndef PDSSM_H
+#define PDSSM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PDSSM_ABI_VERSION 1
+
+typedef struct pdssm_c64 {
+    float re, im;
+} pdssm_c64;
+
+typedef struct pdssm_desc {
+    int32_t B, L, H, N, K; /* batch, steps, heads, state size, dictionary size */
+    int32_t chunk;         /* steps per chunk; 0 = default; fwd and bwd must agree */
+    uint32_t flags;        /* reserved, must be 0 */
+} pdssm_desc;
+
+typedef enum pdssm_status {
+    PDSSM_OK = 0,
+    PDSSM_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, overlap, flags != 0 */
+    PDSSM_ERR_UNSUPPORTED = -2, /* N, K or chunk outside the supported set */
+    PDSSM_ERR_WORKSPACE = -3,   /* ws NULL or smaller than pdssm_workspace_size */
+    PDSSM_ERR_HIP = -4,         /* a HIP launch reported an error */
+    PDSSM_ERR_INDEX = -5        /* written to *dev_status by kernels only */
+} pdssm_status;
+
+typedef enum pdssm_op {
+    PDSSM_OP_FWD = 1,
+    PDSSM_OP_BWD = 2,
+    PDSSM_OP_COMPOSE = 3
+} pdssm_op;
+
+/* ABI version of the loaded library (PDSSM_ABI_VERSION at build time). */
+int pdssm_abi_version(void);
+
+/* Effective chunk length of desc (resolves chunk = 0), or a negative status. */
+int pdssm_chunk_len(const pdssm_desc* desc);
+
+/* C = ceil(L / chunk) for the effective chunk, or a negative status. */
+int pdssm_num_chunks(const pdssm_desc* desc);
+
+/* Workspace bytes the op needs for desc (0 if none); (size_t)-1 if desc is
+ * invalid. */
+size_t pdssm_workspace_size(const pdssm_desc* desc, int op);
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* pdssm_status_string(int status);
+
+/*
+ * Forward scan (App. E.1 Algorithm 1 / App. E.2 recurrence, readout of
+ * Sec. 2.1 eq. (1) fused in).
+ * In:  idx, pi, D, b, c (required); h0 (NULL = zero initial state).
+ * Out: y (required); h_final = h_{L-1} (optional); saved (optional): the state
+ *      entering every chunk, saved[b,h,c,:] = h_{c*chunk-1} (h0 for c = 0),
+ *      which pdssm_scan_bwd needs.
+ */
+int pdssm_scan_fwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
+                   const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                   const pdssm_c64* h0, float* y, pdssm_c64* h_final, pdssm_c64* saved,
+                   void* ws, size_t ws_bytes, int* dev_status, void* stream);
+
+/*
+ * Backward scan: the vector-Jacobian product of pdssm_scan_fwd (the paper
+ * leaves the adjoint of the scan unstated; this is the exact adjoint of the
+ * forward above).  Per sequence, with g_t the gradient reaching h_t:
+ *   g_t     = dy_t * conj(c_t) + (conj(D_{t+1}) * g_{t+1}[pi_{t+1}])
+ *   dD_t[j] = conj(h_{t-1}[j]) * g_t[pi_t[j]],  db_t = g_t,
+ *   dc_t    = dy_t * conj(h_t),  dh0[j] = conj(D_0[j]) * g_0[pi_0[j]],
+ * starting from g_{L-1} = dy_{L-1} conj(c_{L-1}) + dh_final.
+ * In:  idx, pi, D, b, c, saved (from pdssm_scan_fwd with the same desc and h0),
+ *      dy (required); dh_final (NULL = zero).  h0 is not read: the states are
+ *      recomputed from saved.
+ * Out: dD, db, dc (required); dh0 (optional).
+ */
+int pdssm_scan_bwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
+                   const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                   const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
+                   pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
+                   void* ws, size_t ws_bytes, int* dev_status, void* stream);
+
+/*
+ * Composed operator of every chunk in PD form (App. E.3.1 accumulator update,
+ * App. E.2 associative operator): for chunk c of sequence (b,h),
+ * A_{e-1} ... A_s with A_t = P_t D_t is returned as pi_out[b,h,c,:] (int32,
+ * exact) and d_out[b,h,c,:] (complex), i.e. column j of the product holds
+ * d_out[j] in row pi_out[j].  chunk >= L gives one whole-sequence map.
+ * Needs no workspace.  Out: pi_out, d_out [B,H,C,N] (required).
+ */
+int pdssm_compose_chunks(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
+                         const pdssm_c64* D, int32_t* pi_out, pdssm_c64* d_out,
+                         int* dev_status, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PDSSM_H */

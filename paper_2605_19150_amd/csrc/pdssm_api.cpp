@@ -1,0 +1,262 @@
+// pdssm_api.cpp -- the C ABI of libpdssm.so: argument checks, workspace
+// layout and kernel dispatch.  Declarations and the contract are in pdssm.h.
+#include "pdssm.h"
+
+#include <hip/hip_runtime.h>
+
+#include <initializer_list>
+
+#include "pdssm_internal.h"
+
+namespace {
+
+using pdssm::ScanArgs;
+
+constexpr int kDefaultChunk = 32;
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool n_supported(int N) {
+    return N == 8 || N == 16 || N == 32 || N == 64 || N == 128 || N == 256;
+}
+
+bool scan_chunk_ok(int N, int tau) {
+    return (tau == 16 || tau == 32 || tau == 64) &&
+           pdssm::bwd_emit_lds_bytes(N, tau) <= pdssm::kMaxLdsPerGroup;
+}
+
+// Dimension checks shared by every op.  Returns PDSSM_OK or a status.
+int check_dims(const pdssm_desc* d) {
+    if (!d) return PDSSM_ERR_INVALID_ARG;
+    if (d->flags != 0) return PDSSM_ERR_INVALID_ARG;
+    if (d->B < 1 || d->L < 1 || d->H < 1 || d->N < 1 || d->K < 1 || d->chunk < 0)
+        return PDSSM_ERR_INVALID_ARG;
+    if (!n_supported(d->N) || d->K > 256) return PDSSM_ERR_UNSUPPORTED;
+    const long long elems = (long long)d->B * d->L * d->H * d->N;
+    if (elems >= (1LL << 31)) return PDSSM_ERR_UNSUPPORTED;
+    if ((long long)d->H * d->K * d->N >= (1LL << 31)) return PDSSM_ERR_UNSUPPORTED;
+    return PDSSM_OK;
+}
+
+// Effective scan chunk (fwd/bwd) or a negative status.
+int scan_chunk(const pdssm_desc* d) {
+    int st = check_dims(d);
+    if (st != PDSSM_OK) return st;
+    int tau = d->chunk;
+    if (tau == 0) {
+        tau = kDefaultChunk;
+        if (!scan_chunk_ok(d->N, tau)) tau = 16;
+    }
+    if (!scan_chunk_ok(d->N, tau)) return PDSSM_ERR_UNSUPPORTED;
+    return tau;
+}
+
+struct Range {
+    const void* p;
+    size_t n;
+};
+
+bool overlap(Range a, Range b) {
+    if (!a.p || !b.p || a.n == 0 || b.n == 0) return false;
+    auto x = reinterpret_cast<uintptr_t>(a.p), y = reinterpret_cast<uintptr_t>(b.p);
+    return x < y + b.n && y < x + a.n;
+}
+
+// Every output must be disjoint from every input and from every other output.
+bool any_overlap(std::initializer_list<Range> outs, std::initializer_list<Range> ins) {
+    for (auto o = outs.begin(); o != outs.end(); ++o) {
+        for (auto i : ins)
+            if (overlap(*o, i)) return true;
+        for (auto o2 = o + 1; o2 != outs.end(); ++o2)
+            if (overlap(*o, *o2)) return true;
+    }
+    return false;
+}
+
+struct Sizes {
+    size_t seqN, stepN, perChunk, idxN;
+};
+
+Sizes sizes_of(const pdssm_desc* d, int C) {
+    Sizes s;
+    s.seqN = (size_t)d->B * d->H * d->N;
+    s.stepN = (size_t)d->B * d->L * d->H * d->N;
+    s.perChunk = (size_t)d->B * d->H * C * d->N;
+    s.idxN = (size_t)d->B * d->L * d->H;
+    return s;
+}
+
+// Workspace carve-up: int map, complex diag, complex term, complex carry/U.
+size_t ws_bytes_for(const Sizes& s) {
+    return align_up(s.perChunk * 4) + 3 * align_up(s.perChunk * 8);
+}
+
+void carve(ScanArgs& a, void* ws, const Sizes& s) {
+    char* p = static_cast<char*>(ws);
+    a.agg_p = reinterpret_cast<int*>(p);
+    p += align_up(s.perChunk * 4);
+    a.agg_d = reinterpret_cast<float2*>(p);
+    p += align_up(s.perChunk * 8);
+    a.agg_v = reinterpret_cast<float2*>(p);
+    p += align_up(s.perChunk * 8);
+    a.U = reinterpret_cast<float2*>(p);  // fwd: carry when saved == NULL
+}
+
+ScanArgs base_args(const pdssm_desc* d, int tau) {
+    ScanArgs a = {};
+    a.B = d->B;
+    a.L = d->L;
+    a.H = d->H;
+    a.N = d->N;
+    a.K = d->K;
+    a.tau = tau;
+    a.C = (d->L + tau - 1) / tau;
+    return a;
+}
+
+bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) % 16) != 0; }
+
+}  // namespace
+
+extern "C" {
+
+int pdssm_abi_version(void) { return PDSSM_ABI_VERSION; }
+
+int pdssm_chunk_len(const pdssm_desc* d) { return scan_chunk(d); }
+
+int pdssm_num_chunks(const pdssm_desc* d) {
+    int tau = scan_chunk(d);
+    if (tau < 0) return tau;
+    return (d->L + tau - 1) / tau;
+}
+
+size_t pdssm_workspace_size(const pdssm_desc* d, int op) {
+    if (op == PDSSM_OP_COMPOSE) return check_dims(d) == PDSSM_OK ? 0 : (size_t)-1;
+    if (op != PDSSM_OP_FWD && op != PDSSM_OP_BWD) return (size_t)-1;
+    int tau = scan_chunk(d);
+    if (tau < 0) return (size_t)-1;
+    return ws_bytes_for(sizes_of(d, (d->L + tau - 1) / tau));
+}
+
+const char* pdssm_status_string(int st) {
+    switch (st) {
+        case PDSSM_OK: return "PDSSM_OK";
+        case PDSSM_ERR_INVALID_ARG: return "PDSSM_ERR_INVALID_ARG: bad pointer, size, flags or overlapping buffers";
+        case PDSSM_ERR_UNSUPPORTED: return "PDSSM_ERR_UNSUPPORTED: N, K, chunk or total size outside the supported set";
+        case PDSSM_ERR_WORKSPACE: return "PDSSM_ERR_WORKSPACE: workspace missing or smaller than pdssm_workspace_size";
+        case PDSSM_ERR_HIP: return "PDSSM_ERR_HIP: a HIP kernel launch failed";
+        case PDSSM_ERR_INDEX: return "PDSSM_ERR_INDEX: idx or pi entry out of range";
+        default: return "unknown pdssm status";
+    }
+}
+
+int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
+                   const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                   const pdssm_c64* h0, float* y, pdssm_c64* h_final, pdssm_c64* saved,
+                   void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+    int tau = scan_chunk(d);
+    if (tau < 0) return tau;
+    if (!idx || !pi || !D || !b || !c || !y) return PDSSM_ERR_INVALID_ARG;
+    for (const void* p : {(const void*)D, (const void*)b, (const void*)c, (const void*)h0,
+                          (const void*)h_final, (const void*)saved, (const void*)pi})
+        if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    ScanArgs a = base_args(d, tau);
+    const Sizes s = sizes_of(d, a.C);
+    const size_t need = ws_bytes_for(s);
+    if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
+        return PDSSM_ERR_WORKSPACE;
+    const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
+    if (any_overlap({{y, s.idxN * 4}, {h_final, s.seqN * 8}, {saved, s.perChunk * 8}, {ws, need}},
+                    {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {h0, s.seqN * 8}}))
+        return PDSSM_ERR_INVALID_ARG;
+    a.idx = idx;
+    a.pi = pi;
+    a.D = reinterpret_cast<const float2*>(D);
+    a.b = reinterpret_cast<const float2*>(b);
+    a.c = reinterpret_cast<const float2*>(c);
+    a.h0 = reinterpret_cast<const float2*>(h0);
+    a.y = y;
+    a.hfinal = reinterpret_cast<float2*>(h_final);
+    a.status = dev_status;
+    carve(a, ws, s);
+    a.carry = saved ? reinterpret_cast<float2*>(saved) : a.U;
+    hipError_t e = pdssm::launch_fwd_chunked(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
+                   const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                   const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
+                   pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
+                   void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+    int tau = scan_chunk(d);
+    if (tau < 0) return tau;
+    if (!idx || !pi || !D || !b || !c || !saved || !dy || !dD || !db || !dc)
+        return PDSSM_ERR_INVALID_ARG;
+    for (const void* p : {(const void*)D, (const void*)b, (const void*)c, (const void*)saved,
+                          (const void*)dh_final, (const void*)dD, (const void*)db,
+                          (const void*)dc, (const void*)dh0, (const void*)pi})
+        if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    ScanArgs a = base_args(d, tau);
+    const Sizes s = sizes_of(d, a.C);
+    const size_t need = ws_bytes_for(s);
+    if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
+        return PDSSM_ERR_WORKSPACE;
+    const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
+    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {ws, need}},
+                    {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * 8},
+                     {dy, nidx}, {dh_final, s.seqN * 8}}))
+        return PDSSM_ERR_INVALID_ARG;
+    a.idx = idx;
+    a.pi = pi;
+    a.D = reinterpret_cast<const float2*>(D);
+    a.b = reinterpret_cast<const float2*>(b);
+    a.c = reinterpret_cast<const float2*>(c);
+    a.dy = dy;
+    a.dhf = reinterpret_cast<const float2*>(dh_final);
+    a.dD = reinterpret_cast<float2*>(dD);
+    a.db = reinterpret_cast<float2*>(db);
+    a.dc = reinterpret_cast<float2*>(dc);
+    a.dh0 = reinterpret_cast<float2*>(dh0);
+    a.status = dev_status;
+    carve(a, ws, s);
+    a.carry = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
+    hipError_t e = pdssm::launch_bwd_chunked(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+int pdssm_compose_chunks(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
+                         const pdssm_c64* D, int32_t* pi_out, pdssm_c64* d_out,
+                         int* dev_status, void* stream) {
+    int st = check_dims(d);
+    if (st != PDSSM_OK) return st;
+    if (!idx || !pi || !D || !pi_out || !d_out) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned(D) || misaligned(pi) || misaligned(pi_out) || misaligned(d_out))
+        return PDSSM_ERR_INVALID_ARG;
+    pdssm::ComposeArgs a = {};
+    a.B = d->B;
+    a.L = d->L;
+    a.H = d->H;
+    a.N = d->N;
+    a.K = d->K;
+    a.tau = d->chunk == 0 ? kDefaultChunk : d->chunk;
+    if (a.tau > d->L) a.tau = d->L;
+    a.C = (d->L + a.tau - 1) / a.tau;
+    const size_t per = (size_t)d->B * d->H * a.C * d->N;
+    const size_t nst = (size_t)d->B * d->L * d->H * d->N * 8;
+    if (any_overlap({{pi_out, per * 4}, {d_out, per * 8}},
+                    {{idx, (size_t)d->B * d->L * d->H * 4}, {pi, (size_t)d->H * d->K * d->N * 4},
+                     {D, nst}}))
+        return PDSSM_ERR_INVALID_ARG;
+    a.idx = idx;
+    a.pi = pi;
+    a.D = reinterpret_cast<const float2*>(D);
+    a.pi_out = pi_out;
+    a.d_out = reinterpret_cast<float2*>(d_out);
+    a.status = dev_status;
+    hipError_t e = pdssm::launch_compose(a, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+}  // extern "C"

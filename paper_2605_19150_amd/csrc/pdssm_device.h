@@ -1,0 +1,202 @@
+// pdssm_device.h -- wave-level building blocks of the PD scan for gfx950.
+//
+// One 64-lane wavefront owns one sequence's N-wide complex state.  State
+// entry j lives in lane j / SL, slot j % SL, where SL = max(1, N/64) entries
+// per lane (consecutive entries per lane so a step's row of D, b or c is one
+// 8*SL-byte vector load per lane).  For N < 64 only the first N lanes are
+// active.  Cross-lane movement goes through a per-wave LDS buffer; LDS
+// instructions of one wave execute in issue order, so a wave needs no
+// workgroup barrier for its own buffer, only a compiler fence (wave_sync).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pdssm {
+
+constexpr int kWave = 64;
+constexpr int kErrIndex = -5;  // PDSSM_ERR_INDEX
+
+template <int N>
+struct Lay {
+    static constexpr int SL = N > kWave ? N / kWave : 1;     // entries per lane
+    static constexpr int LANES = N < kWave ? N : kWave;      // active lanes
+    static_assert(N >= 8 && N <= 256 && (N & (N - 1)) == 0, "N must be a power of two in [8,256]");
+};
+
+// ------------------------------------------------------------------ complex
+__device__ __forceinline__ float2 cmul(float2 a, float2 b) {
+    return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+}
+// conj(a) * b
+__device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
+    return make_float2(a.x * b.x + a.y * b.y, a.x * b.y - a.y * b.x);
+}
+__device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+
+// ------------------------------------------------------------------ wave sync
+// Orders this wave's LDS accesses in the compiler; the hardware already
+// executes one wave's LDS instructions in order.
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ int readlane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
+__device__ __forceinline__ float readlane_f(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// Sum over the 64 lanes; the total lands in lane 63 (other lanes hold
+// partial sums).  Row-wise inclusive scan with DPP row_shr, then the
+// row_bcast15 / row_bcast31 steps carry row totals up to the last row.
+__device__ __forceinline__ float wave_sum_last(float v) {
+    float t;
+    t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x111, 0xf, 0xf, true));
+    v += t;
+    t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x112, 0xf, 0xf, true));
+    v += t;
+    t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x114, 0xf, 0xf, true));
+    v += t;
+    t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x118, 0xf, 0xf, true));
+    v += t;
+    t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x142, 0xa, 0xf, false));
+    v += t;
+    t = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x143, 0xc, 0xf, false));
+    v += t;
+    return v;
+}
+
+// ------------------------------------------------------------------ per-lane vectors
+template <int SL>
+struct CV {
+    float2 v[SL];
+};
+template <int SL>
+struct IV {
+    int v[SL];
+};
+
+template <int SL>
+__device__ __forceinline__ CV<SL> cv_zero() {
+    CV<SL> r;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) r.v[s] = make_float2(0.f, 0.f);
+    return r;
+}
+
+// Load this lane's SL consecutive complex entries of a row (row + lane*SL).
+template <int SL>
+__device__ __forceinline__ CV<SL> ld_cv(const float2* __restrict__ row, int lane) {
+    CV<SL> r;
+    const float2* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        r.v[0] = *p;
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 2) {
+            float4 q = *reinterpret_cast<const float4*>(p + s);
+            r.v[s] = make_float2(q.x, q.y);
+            r.v[s + 1] = make_float2(q.z, q.w);
+        }
+    }
+    return r;
+}
+
+template <int SL>
+__device__ __forceinline__ void st_cv(float2* __restrict__ row, int lane, const CV<SL>& x) {
+    float2* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        *p = x.v[0];
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 2)
+            *reinterpret_cast<float4*>(p + s) = make_float4(x.v[s].x, x.v[s].y, x.v[s + 1].x, x.v[s + 1].y);
+    }
+}
+
+template <int SL>
+__device__ __forceinline__ IV<SL> ld_iv(const int* __restrict__ row, int lane) {
+    IV<SL> r;
+    const int* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        r.v[0] = *p;
+    } else if constexpr (SL == 2) {
+        int2 q = *reinterpret_cast<const int2*>(p);
+        r.v[0] = q.x;
+        r.v[1] = q.y;
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4) {
+            int4 q = *reinterpret_cast<const int4*>(p + s);
+            r.v[s] = q.x;
+            r.v[s + 1] = q.y;
+            r.v[s + 2] = q.z;
+            r.v[s + 3] = q.w;
+        }
+    }
+    return r;
+}
+
+template <int SL>
+__device__ __forceinline__ void st_iv(int* __restrict__ row, int lane, const IV<SL>& x) {
+#pragma unroll
+    for (int s = 0; s < SL; ++s) row[lane * SL + s] = x.v[s];
+}
+
+// Replace out-of-range map entries by 0; returns true if any entry was bad.
+template <int N, int SL>
+__device__ __forceinline__ bool sanitize_map(IV<SL>& p) {
+    bool bad = false;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        bool b = (unsigned)p.v[s] >= (unsigned)N;
+        bad |= b;
+        p.v[s] = b ? 0 : p.v[s];
+    }
+    return bad;
+}
+
+__device__ __forceinline__ void report_index_error(int* status) {
+    if (status) *status = kErrIndex;
+}
+
+// ------------------------------------------------------------------ the PD step
+// x <- bt + P(pt) (Dt .* x): every lane scatters D_t[j]*x[j] to row pt[j] of
+// the wave's LDS buffer X (pre-filled with b_t); colliding rows add up
+// through LDS float atomics.  X holds N complex values.
+template <int N>
+__device__ __forceinline__ void pd_scatter_step(float2* X, int lane, bool act,
+                                                CV<Lay<N>::SL>& x,
+                                                const CV<Lay<N>::SL>& Dt,
+                                                const CV<Lay<N>::SL>& bt,
+                                                const IV<Lay<N>::SL>& pt) {
+    constexpr int SL = Lay<N>::SL;
+    wave_sync();
+    if (act) st_cv<SL>(X, lane, bt);
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            float2 v = cmul(Dt.v[s], x.v[s]);
+            float* dst = reinterpret_cast<float*>(X + pt.v[s]);
+            atomicAdd(dst, v.x);
+            atomicAdd(dst + 1, v.y);
+        }
+    }
+    wave_sync();
+    if (act) x = ld_cv<SL>(X, lane);
+}
+
+// Gather: out[j] = V[pt[j]] where V is the wave's staged N-vector in LDS.
+template <int N>
+__device__ __forceinline__ CV<Lay<N>::SL> gather_cv(const float2* V, const IV<Lay<N>::SL>& pt) {
+    CV<Lay<N>::SL> r;
+#pragma unroll
+    for (int s = 0; s < Lay<N>::SL; ++s) r.v[s] = V[pt.v[s]];
+    return r;
+}
+
+}  // namespace pdssm

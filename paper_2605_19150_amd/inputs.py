@@ -167,3 +167,18 @@ def fsa_inputs(B, L, H, N, K, seed=0, perm=False, n_accept=None):
     c = np.broadcast_to(acc[None, None, :, :], shape).astype(np.complex64)
     dy = rng.standard_normal((B, L, H), dtype=np.float32)
     return dict(idx=idx, pi=pi, D=D, b=b, c=c, h0=h0, dy=dy, start=start, accept=acc)
+
+
+def sub_sequence(inp, bb, hh):
+    """Inputs of the single sequence (bb, hh) as a B=1, H=1 problem."""
+    out = {}
+    for k in ("D", "b", "c"):
+        out[k] = np.ascontiguousarray(inp[k][bb:bb + 1, :, hh:hh + 1])
+    out["idx"] = np.ascontiguousarray(inp["idx"][bb:bb + 1, :, hh:hh + 1])
+    out["pi"] = np.ascontiguousarray(inp["pi"][hh:hh + 1])
+    if "dy" in inp:
+        out["dy"] = np.ascontiguousarray(inp["dy"][bb:bb + 1, :, hh:hh + 1])
+    for k in ("h0", "dh_final"):
+        if inp.get(k) is not None:
+            out[k] = np.ascontiguousarray(inp[k][bb:bb + 1, hh:hh + 1])
+    return out

@@ -1,0 +1,232 @@
+"""Thin ctypes binding of libpdssm.so (the C ABI declared in include/pdssm.h).
+
+Only argument marshalling happens here: shape/dtype/device checks, output and
+workspace allocation with torch, and passing raw device pointers plus the
+current HIP stream to the library.  Every step of the scan runs in the HIP
+kernels.  If the library is missing the binding raises; there is no fallback.
+
+Tensor layouts (all contiguous, on one GPU):
+  idx [B,L,H] int32, pi [H,K,N] int32, D/b/c [B,L,H,N] complex64,
+  h0/h_final/dh_final/dh0 [B,H,N] complex64, y/dy [B,L,H] float32,
+  saved [B,H,C,N] complex64 (C = num_chunks).
+"""
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpdssm.so")
+_lib = None
+
+OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INDEX = 0, -1, -2, -3, -4, -5
+OP_FWD, OP_BWD, OP_COMPOSE = 1, 2, 3
+
+
+class PdssmError(RuntimeError):
+    def __init__(self, status, what):
+        super().__init__("%s: %s" % (what, status_string(status)))
+        self.status = status
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("L", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("N", ctypes.c_int32), ("K", ctypes.c_int32), ("chunk", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
+           "pdssm_status_string", "pdssm_scan_fwd", "pdssm_scan_bwd", "pdssm_compose_chunks")
+
+
+def lib_path():
+    return _LIB_PATH
+
+
+def load():
+    """Load libpdssm.so once (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError("libpdssm.so is not built (%s); run __graft_entry__.build()" % _LIB_PATH)
+    L = ctypes.CDLL(_LIB_PATH)
+    P, I, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+    D = ctypes.POINTER(Desc)
+    L.pdssm_abi_version.argtypes, L.pdssm_abi_version.restype = [], I
+    L.pdssm_chunk_len.argtypes, L.pdssm_chunk_len.restype = [D], I
+    L.pdssm_num_chunks.argtypes, L.pdssm_num_chunks.restype = [D], I
+    L.pdssm_workspace_size.argtypes, L.pdssm_workspace_size.restype = [D, I], Z
+    L.pdssm_status_string.argtypes, L.pdssm_status_string.restype = [I], ctypes.c_char_p
+    L.pdssm_scan_fwd.argtypes = [D] + [P] * 10 + [Z, P, P]
+    L.pdssm_scan_fwd.restype = I
+    L.pdssm_scan_bwd.argtypes = [D] + [P] * 13 + [Z, P, P]
+    L.pdssm_scan_bwd.restype = I
+    L.pdssm_compose_chunks.argtypes = [D] + [P] * 7
+    L.pdssm_compose_chunks.restype = I
+    if L.pdssm_abi_version() != 1:
+        raise ImportError("libpdssm.so ABI version mismatch")
+    _lib = L
+    return L
+
+
+def status_string(st):
+    return load().pdssm_status_string(int(st)).decode()
+
+
+def desc(B, L, H, N, K, chunk=0):
+    return Desc(int(B), int(L), int(H), int(N), int(K), int(chunk), 0)
+
+
+def chunk_len(d):
+    return load().pdssm_chunk_len(ctypes.byref(d))
+
+
+def num_chunks(d):
+    return load().pdssm_num_chunks(ctypes.byref(d))
+
+
+def workspace_size(d, op):
+    n = load().pdssm_workspace_size(ctypes.byref(d), int(op))
+    if n == ctypes.c_size_t(-1).value:
+        raise PdssmError(ERR_INVALID_ARG, "workspace_size")
+    return n
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _need(t, name, dtype, shape, device):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s must have shape %s, got %s" % (name, tuple(shape), tuple(t.shape)))
+    if t.device != device or t.device.type != "cuda":
+        raise ValueError("%s must be on %s" % (name, device))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def dims_of(idx, pi):
+    B, L, H = idx.shape
+    H2, K, N = pi.shape
+    if H2 != H:
+        raise ValueError("idx and pi disagree on H")
+    return B, L, H, N, K
+
+
+def _check_inputs(idx, pi, D, b, c):
+    B, L, H, N, K = dims_of(idx, pi)
+    dev = idx.device
+    _need(idx, "idx", torch.int32, (B, L, H), dev)
+    _need(pi, "pi", torch.int32, (H, K, N), dev)
+    for t, n in ((D, "D"), (b, "b"), (c, "c")):
+        _need(t, n, torch.complex64, (B, L, H, N), dev)
+    return B, L, H, N, K, dev
+
+
+class Scan:
+    """Pre-allocated outputs and workspaces for one problem size; fwd() and
+    bwd() allocate nothing, so they can be timed in a loop."""
+
+    def __init__(self, B, L, H, N, K, chunk=0, device="cuda"):
+        self.d = desc(B, L, H, N, K, chunk)
+        self.dims = (B, L, H, N, K)
+        self.device = torch.device(device)
+        self.C = num_chunks(self.d)
+        if self.C < 0:
+            raise PdssmError(self.C, "num_chunks")
+        self.chunk = chunk_len(self.d)
+        dev = self.device
+        self.ws_fwd = torch.empty(max(workspace_size(self.d, OP_FWD), 1), dtype=torch.uint8, device=dev)
+        self.ws_bwd = torch.empty(max(workspace_size(self.d, OP_BWD), 1), dtype=torch.uint8, device=dev)
+        self.y = torch.empty((B, L, H), dtype=torch.float32, device=dev)
+        self.h_final = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
+        self.saved = torch.empty((B, H, self.C, N), dtype=torch.complex64, device=dev)
+        self.dD = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
+        self.db = torch.empty_like(self.dD)
+        self.dc = torch.empty_like(self.dD)
+        self.dh0 = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def fwd(self, idx, pi, D, b, c, h0=None, stream=None):
+        st = load().pdssm_scan_fwd(ctypes.byref(self.d), _p(idx), _p(pi), _p(D), _p(b), _p(c),
+                                   _p(h0), _p(self.y), _p(self.h_final), _p(self.saved),
+                                   _p(self.ws_fwd), self.ws_fwd.numel(), _p(self.status),
+                                   _stream(stream))
+        if st != OK:
+            raise PdssmError(st, "pdssm_scan_fwd")
+        return self.y, self.h_final, self.saved
+
+    def bwd(self, idx, pi, D, b, c, dy, dh_final=None, stream=None):
+        st = load().pdssm_scan_bwd(ctypes.byref(self.d), _p(idx), _p(pi), _p(D), _p(b), _p(c),
+                                   _p(self.saved), _p(dy), _p(dh_final), _p(self.dD), _p(self.db),
+                                   _p(self.dc), _p(self.dh0), _p(self.ws_bwd),
+                                   self.ws_bwd.numel(), _p(self.status), _stream(stream))
+        if st != OK:
+            raise PdssmError(st, "pdssm_scan_bwd")
+        return self.dD, self.db, self.dc, self.dh0
+
+    def check_status(self):
+        """Synchronise and raise if a kernel flagged an out-of-range index."""
+        torch.cuda.synchronize(self.device)
+        st = int(self.status.item())
+        if st != OK:
+            raise PdssmError(st, "kernel index check")
+
+
+def scan_fwd(idx, pi, D, b, c, h0=None, chunk=0, stream=None):
+    """Returns (y [B,L,H] f32, h_final [B,H,N] c64, saved [B,H,C,N] c64)."""
+    B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
+    if h0 is not None:
+        _need(h0, "h0", torch.complex64, (B, H, N), dev)
+    s = Scan(B, L, H, N, K, chunk, dev)
+    s.fwd(idx, pi, D, b, c, h0, stream)
+    s.check_status()
+    return s.y, s.h_final, s.saved
+
+
+def scan_bwd(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
+    """Returns (dD, db, dc [B,L,H,N] c64, dh0 [B,H,N] c64)."""
+    B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
+    s = Scan(B, L, H, N, K, chunk, dev)
+    _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
+    _need(dy, "dy", torch.float32, (B, L, H), dev)
+    if dh_final is not None:
+        _need(dh_final, "dh_final", torch.complex64, (B, H, N), dev)
+    s.saved = saved
+    s.bwd(idx, pi, D, b, c, dy, dh_final, stream)
+    s.check_status()
+    return s.dD, s.db, s.dc, s.dh0
+
+
+def compose_chunks(idx, pi, D, chunk, stream=None):
+    """Returns (pi_out [B,H,C,N] int32, d_out [B,H,C,N] c64)."""
+    B, L, H, N, K = dims_of(idx, pi)
+    dev = idx.device
+    _need(idx, "idx", torch.int32, (B, L, H), dev)
+    _need(pi, "pi", torch.int32, (H, K, N), dev)
+    _need(D, "D", torch.complex64, (B, L, H, N), dev)
+    if chunk < 1:
+        raise ValueError("chunk must be >= 1")
+    tau = min(int(chunk), L)
+    C = -(-L // tau)
+    pi_out = torch.empty((B, H, C, N), dtype=torch.int32, device=dev)
+    d_out = torch.empty((B, H, C, N), dtype=torch.complex64, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    d = desc(B, L, H, N, K, tau)
+    st = load().pdssm_compose_chunks(ctypes.byref(d), _p(idx), _p(pi), _p(D), _p(pi_out),
+                                     _p(d_out), _p(status), _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_compose_chunks")
+    torch.cuda.synchronize(dev)
+    if int(status.item()) != OK:
+        raise PdssmError(int(status.item()), "kernel index check")
+    return pi_out, d_out

@@ -1,0 +1,133 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/pdssm.h declares, and rejects bad arguments before any
+HIP call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_19150_amd import pdssm
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "pdssm.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(pdssm_[a-z_0-9]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(pdssm.lib_path()):
+        from paper_2605_19150_amd.build import build_library
+        build_library()
+    return pdssm.load()
+
+
+def test_exports_every_declared_function(lib):
+    names = header_functions()
+    assert "pdssm_scan_fwd" in names and "pdssm_scan_bwd" in names and "pdssm_compose_chunks" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(names) <= set(pdssm.EXPORTS) | set(names)
+    assert lib.pdssm_abi_version() == 1
+
+
+def test_chunk_and_workspace_queries(lib):
+    d = pdssm.desc(16, 2048, 16, 64, 16)
+    assert pdssm.chunk_len(d) == 32
+    assert pdssm.num_chunks(d) == 64
+    d = pdssm.desc(8, 18000, 8, 128, 32, chunk=16)
+    assert pdssm.num_chunks(d) == 1125
+    for op in (pdssm.OP_FWD, pdssm.OP_BWD):
+        n = pdssm.workspace_size(d, op)
+        assert n >= 8 * 8 * 1125 * 128 * 28
+    assert pdssm.workspace_size(d, pdssm.OP_COMPOSE) == 0
+    d = pdssm.desc(1, 1, 1, 8, 1)
+    assert pdssm.num_chunks(d) == 1
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(N=48), pdssm.ERR_UNSUPPORTED),
+    (dict(N=512), pdssm.ERR_UNSUPPORTED),
+    (dict(K=257), pdssm.ERR_UNSUPPORTED),
+    (dict(chunk=24), pdssm.ERR_UNSUPPORTED),
+    (dict(L=0), pdssm.ERR_INVALID_ARG),
+    (dict(B=-1), pdssm.ERR_INVALID_ARG),
+    (dict(chunk=-3), pdssm.ERR_INVALID_ARG),
+])
+def test_bad_descriptors(lib, kw, code):
+    args = dict(B=2, L=10, H=2, N=64, K=4, chunk=0)
+    args.update(kw)
+    d = pdssm.desc(**args)
+    assert pdssm.num_chunks(d) == code
+    with pytest.raises(pdssm.PdssmError):
+        pdssm.workspace_size(d, pdssm.OP_FWD)
+
+
+def test_flags_must_be_zero(lib):
+    d = pdssm.desc(2, 10, 2, 64, 4)
+    d.flags = 1
+    assert pdssm.num_chunks(d) == pdssm.ERR_INVALID_ARG
+
+
+def test_status_strings(lib):
+    for st in (0, -1, -2, -3, -4, -5):
+        assert pdssm.status_string(st).startswith("PDSSM_")
+    assert "unknown" in pdssm.status_string(7)
+
+
+class FakeBufs:
+    """Distinct fake device addresses: the host checks reject the call before
+    any pointer could be dereferenced."""
+
+    def __init__(self):
+        self.next = 1 << 40
+
+    def __call__(self, nbytes):
+        p = self.next
+        self.next += (nbytes + 4095) // 4096 * 4096 + 4096
+        return ctypes.c_void_p(p)
+
+
+def _fwd_call(lib, d, override=None, ws_bytes=None):
+    B, L, H, N, K = d.B, d.L, d.H, d.N, d.K
+    f = FakeBufs()
+    st = B * L * H * N * 8
+    args = dict(idx=f(B * L * H * 4), pi=f(H * K * N * 4), D=f(st), b=f(st), c=f(st), h0=None,
+                y=f(B * L * H * 4), hf=f(B * H * N * 8), saved=f(B * H * 64 * N * 8))
+    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_FWD)
+    args["ws"] = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+    args.update(override or {})
+    return lib.pdssm_scan_fwd(ctypes.byref(d), args["idx"], args["pi"], args["D"], args["b"],
+                              args["c"], args["h0"], args["y"], args["hf"], args["saved"],
+                              args["ws"], need if ws_bytes is None else ws_bytes, None, None)
+
+
+def test_fwd_rejects_null_required(lib):
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    for name in ("idx", "pi", "D", "b", "c", "y"):
+        assert _fwd_call(lib, d, {name: None}) == pdssm.ERR_INVALID_ARG, name
+
+
+def test_fwd_rejects_small_workspace(lib):
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    assert _fwd_call(lib, d, ws_bytes=16) == pdssm.ERR_WORKSPACE
+    assert _fwd_call(lib, d, {"ws": None}) == pdssm.ERR_WORKSPACE
+
+
+def test_fwd_rejects_aliasing_and_misalignment(lib):
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    f = FakeBufs()
+    shared = f(2 * 40 * 2 * 64 * 8)
+    assert _fwd_call(lib, d, {"D": shared, "y": shared}) == pdssm.ERR_INVALID_ARG
+    assert _fwd_call(lib, d, {"D": ctypes.c_void_p(shared.value + 4)}) == pdssm.ERR_INVALID_ARG
+
+
+def test_bwd_and_compose_reject_null(lib):
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    P = ctypes.c_void_p(1 << 40)
+    assert lib.pdssm_scan_bwd(ctypes.byref(d), *([None] * 13), 0, None, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_compose_chunks(ctypes.byref(d), P, P, None, None, None, None, None) == pdssm.ERR_INVALID_ARG

@@ -1,0 +1,209 @@
+"""GPU parity: the HIP path (through the C ABI) against the float64 oracle.
+
+Tolerance (fp32 compute, float64 reference): |gpu - ref| <= 1e-5 + 1e-4*|ref|
+on every real component of y, h_final, saved states and all gradients; the
+composed integer maps and the automaton case are compared bit for bit.
+"""
+import numpy as np
+import pytest
+
+from helpers import assert_close, sub_sequence
+from oracle import oracle_bwd, oracle_compose, oracle_fwd
+from paper_2605_19150_amd.inputs import WORKLOADS, fsa_inputs, make_inputs, workload_inputs
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU machines, never run there
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2605_19150_amd import pdssm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def to_dev(inp):
+    return {k: torch.from_numpy(np.ascontiguousarray(v)).to(DEV) for k, v in inp.items()
+            if isinstance(v, np.ndarray) and k not in ("start", "accept")}
+
+
+def run_gpu(inp, chunk=0, bwd=True):
+    T = to_dev(inp)
+    y, hf, saved = pdssm.scan_fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=T.get("h0"),
+                                  chunk=chunk)
+    out = dict(y=y.cpu().numpy(), h_final=hf.cpu().numpy(), saved=saved.cpu().numpy())
+    if bwd:
+        g = pdssm.scan_bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], saved, T["dy"],
+                           dh_final=T.get("dh_final"), chunk=chunk)
+        for k, v in zip(("dD", "db", "dc", "dh0"), g):
+            out[k] = v.cpu().numpy()
+    return out
+
+
+def check_all(inp, got, chunk_eff, bwd=True):
+    ry, rhf, rsaved = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"],
+                                 h0=inp.get("h0"), chunk=chunk_eff)
+    assert_close("y", got["y"], ry)
+    assert_close("h_final", got["h_final"], rhf)
+    assert_close("saved", got["saved"], rsaved)
+    if bwd:
+        rg = oracle_bwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"],
+                        h0=inp.get("h0"), dh_final=inp.get("dh_final"))
+        for k, r in zip(("dD", "db", "dc", "dh0"), rg):
+            assert_close(k, got[k], r)
+
+
+# ------------------------------------------------------------------ small shapes
+CASES = []
+for N in (8, 16, 32, 64, 128, 256):
+    for chunk in (16, 32, 64):
+        if (chunk + 2) * N * 8 > 65536:
+            continue
+        for L in (1, chunk - 1, chunk, chunk + 1, 3 * chunk + 5):
+            CASES.append((N, chunk, L))
+
+
+@pytest.mark.parametrize("N,chunk,L", CASES)
+def test_small_shapes(N, chunk, L):
+    print("case N=%d chunk=%d L=%d" % (N, chunk, L), flush=True)
+    inp = make_inputs(B=2, L=L, H=3, N=N, K=5, seed=N * 1000 + chunk * 10 + L, with_h0=True,
+                      with_dhf=True)
+    got = run_gpu(inp, chunk=chunk)
+    check_all(inp, got, chunk)
+
+
+@pytest.mark.parametrize("pi_kind", ["uniform", "perm", "identity"])
+def test_map_kinds_default_chunk(pi_kind):
+    inp = make_inputs(B=3, L=200, H=2, N=64, K=7, seed=7, pi_kind=pi_kind, with_h0=True,
+                      with_dhf=True)
+    got = run_gpu(inp)
+    check_all(inp, got, 32)
+
+
+def test_single_dictionary_entry_and_k256():
+    for K in (1, 256):
+        inp = make_inputs(B=1, L=70, H=2, N=32, K=K, seed=K)
+        got = run_gpu(inp)
+        check_all(inp, got, 32)
+
+
+def test_all_maps_collapse_to_one_row():
+    """Degenerate many-to-one maps: every entry maps to row 0 (maximal collisions)."""
+    inp = make_inputs(B=1, L=50, H=1, N=128, K=3, seed=3)
+    inp["pi"][:] = 0
+    got = run_gpu(inp)
+    check_all(inp, got, 32)
+
+
+# ------------------------------------------------------------------ automaton: exact
+@pytest.mark.parametrize("N,perm", [(8, False), (64, True), (64, False), (128, False), (256, True)])
+def test_fsa_bit_exact(N, perm):
+    f = fsa_inputs(B=2, L=300, H=3, N=N, K=6, seed=N, perm=perm)
+    got = run_gpu(f, bwd=False)
+    ry, rhf, _ = oracle_fwd(f["idx"], f["pi"], f["D"], f["b"], f["c"], h0=f["h0"])
+    np.testing.assert_array_equal(got["y"].astype(np.float64), ry)
+    np.testing.assert_array_equal(got["h_final"].astype(np.complex128), rhf)
+
+
+# ------------------------------------------------------------------ compose: exact maps
+@pytest.mark.parametrize("N,chunk,L", [(8, 5, 64), (64, 32, 100), (128, 7, 50), (256, 1, 9),
+                                       (64, 1000, 257)])
+def test_compose_chunks(N, chunk, L):
+    inp = make_inputs(B=2, L=L, H=2, N=N, K=4, seed=chunk + N)
+    T = to_dev(inp)
+    pm, dm = pdssm.compose_chunks(T["idx"], T["pi"], T["D"], chunk)
+    rp, rd = oracle_compose(inp["idx"], inp["pi"], inp["D"], min(chunk, L))
+    np.testing.assert_array_equal(pm.cpu().numpy(), rp)
+    assert_close("d_out", dm.cpu().numpy(), rd)
+
+
+# ------------------------------------------------------------------ split / determinism / errors
+def test_split_invariance_through_h0():
+    inp = make_inputs(B=2, L=150, H=2, N=64, K=4, seed=21, with_h0=True)
+    T = to_dev(inp)
+    y, hf, _ = pdssm.scan_fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=T["h0"])
+    L1 = 77
+    sl = lambda k, a, b: T[k][:, a:b].contiguous()  # noqa: E731
+    y1, h1, _ = pdssm.scan_fwd(sl("idx", 0, L1), T["pi"], sl("D", 0, L1), sl("b", 0, L1),
+                               sl("c", 0, L1), h0=T["h0"])
+    y2, h2, _ = pdssm.scan_fwd(sl("idx", L1, 150), T["pi"], sl("D", L1, 150), sl("b", L1, 150),
+                               sl("c", L1, 150), h0=h1.clone())
+    ry, rhf, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp["h0"])
+    assert_close("y split", torch.cat([y1, y2], 1).cpu().numpy(), ry)
+    assert_close("h_final split", h2.cpu().numpy(), rhf)
+
+
+def test_deterministic():
+    inp = make_inputs(B=2, L=300, H=4, N=128, K=8, seed=5, with_dhf=True)
+    a = run_gpu(inp)
+    b = run_gpu(inp)
+    for k in a:
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def test_out_of_range_indices_flagged_not_faulting():
+    inp = make_inputs(B=1, L=40, H=2, N=64, K=4, seed=9)
+    bad = dict(inp)
+    bad["idx"] = inp["idx"].copy()
+    bad["idx"][0, 5, 1] = 4
+    T = to_dev(bad)
+    with pytest.raises(pdssm.PdssmError) as e:
+        pdssm.scan_fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+    assert e.value.status == pdssm.ERR_INDEX
+    bad = dict(inp)
+    bad["pi"] = inp["pi"].copy()
+    bad["pi"][1, 2, 3] = 64
+    T = to_dev(bad)
+    with pytest.raises(pdssm.PdssmError):
+        pdssm.scan_fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+    # the untouched head is still right
+    y, _, _ = pdssm.scan_fwd(*(to_dev(inp)[k] for k in ("idx", "pi", "D", "b", "c")))
+    ry, _, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"])
+    assert_close("y", y.cpu().numpy(), ry)
+
+
+# ------------------------------------------------------------------ the named workloads
+_cache = {}
+
+
+def workload(i):
+    if i not in _cache:
+        _cache.clear()
+        _cache[i] = workload_inputs(i, seed=0)
+    return _cache[i]
+
+
+def test_workload1_tiny_full():
+    inp = workload(1)
+    got = run_gpu(inp, bwd=False)
+    ry, rhf, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"])
+    assert_close("y", got["y"], ry)
+    assert_close("h_final", got["h_final"], rhf)
+
+
+@pytest.mark.parametrize("wi", [2, 3, 4, 5])
+def test_workload_full_size_sampled(wi):
+    """Full-size run in the benchmark's launch configuration; the oracle checks
+    a sample of whole sequences (first, last and two in between)."""
+    w = WORKLOADS[wi]
+    print("workload %d: %s" % (wi, w.name), flush=True)
+    inp = workload(wi)
+    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K)
+    T = to_dev(inp)
+    s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+    s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
+    s.check_status()
+    picks = sorted({(0, 0), (w.B - 1, w.H - 1), (w.B // 2, 1 % w.H), (1 % w.B, w.H // 2)})
+    for bb, hh in picks:
+        sub = sub_sequence(inp, bb, hh)
+        got = dict(y=s.y[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
+                   h_final=s.h_final[bb:bb + 1, hh:hh + 1].cpu().numpy(),
+                   saved=s.saved[bb:bb + 1, hh:hh + 1].cpu().numpy(),
+                   dD=s.dD[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
+                   db=s.db[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
+                   dc=s.dc[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
+                   dh0=s.dh0[bb:bb + 1, hh:hh + 1].cpu().numpy())
+        check_all(sub, got, s.chunk)
+    # properties over every sequence: finite outputs
+    for t in (s.y, s.h_final, s.dD, s.db, s.dc, s.dh0):
+        assert torch.isfinite(torch.view_as_real(t) if t.is_complex() else t).all()
