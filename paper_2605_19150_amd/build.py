@@ -10,7 +10,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpdssm.so")
-SOURCES = ["pdssm_chunked.hip", "pdssm_api.cpp"]
+SOURCES = ["pdssm_chunked.hip", "pdssm_fused.hip", "pdssm_api.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

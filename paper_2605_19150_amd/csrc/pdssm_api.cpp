@@ -6,13 +6,14 @@
 
 #include <initializer_list>
 
+#include "pdssm_fused.h"
 #include "pdssm_internal.h"
 
 namespace {
 
 using pdssm::ScanArgs;
 
-constexpr int kDefaultChunk = 32;
+constexpr int kDefaultComposeChunk = 32;
 constexpr size_t kAlign = 256;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
@@ -21,9 +22,12 @@ bool n_supported(int N) {
     return N == 8 || N == 16 || N == 32 || N == 64 || N == 128 || N == 256;
 }
 
+int slots(int N) { return N > 64 ? N / 64 : 1; }
+
+// Scan chunk lengths: 4, 8 or 16 steps with chunk * max(1, N/64) <= 16 (the
+// fused kernels keep a chunk's rows in registers).  Default: the largest.
 bool scan_chunk_ok(int N, int tau) {
-    return (tau == 16 || tau == 32 || tau == 64) &&
-           pdssm::bwd_emit_lds_bytes(N, tau) <= pdssm::kMaxLdsPerGroup;
+    return (tau == 4 || tau == 8 || tau == 16) && tau * slots(N) <= 16;
 }
 
 // Dimension checks shared by every op.  Returns PDSSM_OK or a status.
@@ -44,10 +48,7 @@ int scan_chunk(const pdssm_desc* d) {
     int st = check_dims(d);
     if (st != PDSSM_OK) return st;
     int tau = d->chunk;
-    if (tau == 0) {
-        tau = kDefaultChunk;
-        if (!scan_chunk_ok(d->N, tau)) tau = 16;
-    }
+    if (tau == 0) tau = 16 / slots(d->N);
     if (!scan_chunk_ok(d->N, tau)) return PDSSM_ERR_UNSUPPORTED;
     return tau;
 }
@@ -75,7 +76,7 @@ bool any_overlap(std::initializer_list<Range> outs, std::initializer_list<Range>
 }
 
 struct Sizes {
-    size_t seqN, stepN, perChunk, idxN;
+    size_t seqN, stepN, perChunk, idxN, dictN;
 };
 
 Sizes sizes_of(const pdssm_desc* d, int C) {
@@ -84,15 +85,31 @@ Sizes sizes_of(const pdssm_desc* d, int C) {
     s.stepN = (size_t)d->B * d->L * d->H * d->N;
     s.perChunk = (size_t)d->B * d->H * C * d->N;
     s.idxN = (size_t)d->B * d->L * d->H;
+    s.dictN = (size_t)d->H * d->K * d->N;
     return s;
 }
 
-// Workspace carve-up: int map, complex diag, complex term, complex carry/U.
-size_t ws_bytes_for(const Sizes& s) {
+// The fused single-read kernels stage one head's dictionary tables in LDS;
+// when they do not fit, the chunked three-pass kernels run instead.
+bool use_fused(const pdssm_desc* d) {
+    return pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWaves).total <= pdssm::kMaxLds;
+}
+
+// Fused workspace: byte dictionary, row records, per-entry max in-degree.
+size_t fused_ws_bytes(const Sizes& s, const pdssm_desc* d) {
+    return align_up(s.dictN) + align_up(s.dictN * 8) + align_up((size_t)d->H * d->K);
+}
+
+// Chunked workspace: int map, complex diag, complex term, complex carry/U.
+size_t chunked_ws_bytes(const Sizes& s) {
     return align_up(s.perChunk * 4) + 3 * align_up(s.perChunk * 8);
 }
 
-void carve(ScanArgs& a, void* ws, const Sizes& s) {
+size_t ws_bytes_for(const Sizes& s, const pdssm_desc* d) {
+    return use_fused(d) ? fused_ws_bytes(s, d) : chunked_ws_bytes(s);
+}
+
+void carve_chunked(ScanArgs& a, void* ws, const Sizes& s) {
     char* p = static_cast<char*>(ws);
     a.agg_p = reinterpret_cast<int*>(p);
     p += align_up(s.perChunk * 4);
@@ -101,6 +118,54 @@ void carve(ScanArgs& a, void* ws, const Sizes& s) {
     a.agg_v = reinterpret_cast<float2*>(p);
     p += align_up(s.perChunk * 8);
     a.U = reinterpret_cast<float2*>(p);  // fwd: carry when saved == NULL
+}
+
+// Builds the dictionary tables into ws and fills the fused args.
+hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* pi, void* ws,
+                      const Sizes& s, int* status, hipStream_t st) {
+    char* p = static_cast<char*>(ws);
+    pdssm::PrepArgs pa;
+    pa.H = d->H;
+    pa.K = d->K;
+    pa.N = d->N;
+    pa.pi = pi;
+    pa.dict = reinterpret_cast<uint8_t*>(p);
+    p += align_up(s.dictN);
+    pa.rec = reinterpret_cast<uint64_t*>(p);
+    p += align_up(s.dictN * 8);
+    pa.mtab = reinterpret_cast<uint8_t*>(p);
+    pa.status = status;
+    f.dict = pa.dict;
+    f.rec = pa.rec;
+    f.mtab = pa.mtab;
+    f.lds = pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWaves);
+    return pdssm::launch_prep(pa, st);
+}
+
+pdssm::FusedArgs fused_base(const ScanArgs& a) {
+    pdssm::FusedArgs f = {};
+    f.B = a.B;
+    f.L = a.L;
+    f.H = a.H;
+    f.N = a.N;
+    f.K = a.K;
+    f.tau = a.tau;
+    f.C = a.C;
+    f.idx = a.idx;
+    f.D = a.D;
+    f.b = a.b;
+    f.c = a.c;
+    f.h0 = a.h0;
+    f.dy = a.dy;
+    f.dhf = a.dhf;
+    f.y = a.y;
+    f.hfinal = a.hfinal;
+    f.dD = a.dD;
+    f.db = a.db;
+    f.dc = a.dc;
+    f.dh0 = a.dh0;
+    f.status = a.status;
+    return f;
 }
 
 ScanArgs base_args(const pdssm_desc* d, int tau) {
@@ -136,7 +201,7 @@ size_t pdssm_workspace_size(const pdssm_desc* d, int op) {
     if (op != PDSSM_OP_FWD && op != PDSSM_OP_BWD) return (size_t)-1;
     int tau = scan_chunk(d);
     if (tau < 0) return (size_t)-1;
-    return ws_bytes_for(sizes_of(d, (d->L + tau - 1) / tau));
+    return ws_bytes_for(sizes_of(d, (d->L + tau - 1) / tau), d);
 }
 
 const char* pdssm_status_string(int st) {
@@ -163,7 +228,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
     ScanArgs a = base_args(d, tau);
     const Sizes s = sizes_of(d, a.C);
-    const size_t need = ws_bytes_for(s);
+    const size_t need = ws_bytes_for(s, d);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
@@ -179,9 +244,18 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     a.y = y;
     a.hfinal = reinterpret_cast<float2*>(h_final);
     a.status = dev_status;
-    carve(a, ws, s);
-    a.carry = saved ? reinterpret_cast<float2*>(saved) : a.U;
-    hipError_t e = pdssm::launch_fwd_chunked(a, static_cast<hipStream_t>(stream));
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (use_fused(d)) {
+        pdssm::FusedArgs f = fused_base(a);
+        f.saved = reinterpret_cast<float2*>(saved);
+        e = prep_fused(f, d, pi, ws, s, dev_status, st);
+        if (e == hipSuccess) e = pdssm::launch_fwd_fused(f, st);
+    } else {
+        carve_chunked(a, ws, s);
+        a.carry = saved ? reinterpret_cast<float2*>(saved) : a.U;
+        e = pdssm::launch_fwd_chunked(a, st);
+    }
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
@@ -200,7 +274,7 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
     ScanArgs a = base_args(d, tau);
     const Sizes s = sizes_of(d, a.C);
-    const size_t need = ws_bytes_for(s);
+    const size_t need = ws_bytes_for(s, d);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
@@ -220,9 +294,18 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     a.dc = reinterpret_cast<float2*>(dc);
     a.dh0 = reinterpret_cast<float2*>(dh0);
     a.status = dev_status;
-    carve(a, ws, s);
-    a.carry = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
-    hipError_t e = pdssm::launch_bwd_chunked(a, static_cast<hipStream_t>(stream));
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (use_fused(d)) {
+        pdssm::FusedArgs f = fused_base(a);
+        f.saved = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
+        e = prep_fused(f, d, pi, ws, s, dev_status, st);
+        if (e == hipSuccess) e = pdssm::launch_bwd_fused(f, st);
+    } else {
+        carve_chunked(a, ws, s);
+        a.carry = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
+        e = pdssm::launch_bwd_chunked(a, st);
+    }
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
@@ -240,7 +323,7 @@ int pdssm_compose_chunks(const pdssm_desc* d, const int32_t* idx, const int32_t*
     a.H = d->H;
     a.N = d->N;
     a.K = d->K;
-    a.tau = d->chunk == 0 ? kDefaultChunk : d->chunk;
+    a.tau = d->chunk == 0 ? kDefaultComposeChunk : d->chunk;
     if (a.tau > d->L) a.tau = d->L;
     a.C = (d->L + a.tau - 1) / a.tau;
     const size_t per = (size_t)d->B * d->H * a.C * d->N;

@@ -1,0 +1,79 @@
+// pdssm_fused.h -- launch interface of the fused single-read scan kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pdssm {
+
+// Waves per workgroup of the fused kernels (one workgroup per sequence).
+constexpr int kFusedWaves = 12;
+
+// Byte offsets of the fused kernels' dynamic LDS regions.
+struct LdsLayout {
+    uint32_t rec, dict, mtab, ring, ready, vd, x, pa, total;
+};
+
+inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
+
+// Dictionary tables hold K entries plus one identity entry (index K) that
+// pads the last, partial chunk of a sequence with exact no-op steps.  Each
+// wave's vd row block has N + 1 rows; row N stays zero.
+inline LdsLayout fused_lds_layout(int N, int K, int W) {
+    LdsLayout l;
+    size_t o = 0;
+    const size_t KE = (size_t)K + 1;
+    l.rec = (uint32_t)o;   o += KE * N * 8;
+    l.dict = (uint32_t)o;  o += align16(KE * N);
+    l.mtab = (uint32_t)o;  o += align16(KE);
+    l.ring = (uint32_t)o;  o += (size_t)2 * N * 8;
+    l.ready = (uint32_t)o; o += 16;
+    l.vd = (uint32_t)o;    o += (size_t)W * (N + 1) * 16;
+    l.x = (uint32_t)o;     o += (size_t)W * N * 8;
+    l.pa = (uint32_t)o;    o += align16((size_t)W * N);
+    l.total = (uint32_t)o;
+    return l;
+}
+
+constexpr size_t kMaxLds = 163840;  // gfx950: 160 KiB per workgroup
+
+// Per-call dictionary tables built by the prep kernel (workspace).
+struct PrepArgs {
+    int H, K, N;
+    const int* pi;   // [H][K][N]
+    uint8_t* dict;   // [H][K][N] byte copy of pi (sanitised)
+    uint64_t* rec;   // [H][K][N] per destination row: 7 source bytes + in-degree byte;
+                     // unused source bytes hold N (a zero row) when N <= 128, else 0
+    uint8_t* mtab;   // [H][K] max in-degree of the entry, 255 = needs the atomic scatter
+    int* status;
+};
+
+struct FusedArgs {
+    int B, L, H, N, K;
+    int tau, C;
+    const int* idx;
+    const float2* D;
+    const float2* b;
+    const float2* c;
+    const float2* h0;
+    const float* dy;
+    const float2* dhf;
+    float* y;
+    float2* hfinal;
+    float2* saved;  // [B*H][C][N]
+    float2* dD;
+    float2* db;
+    float2* dc;
+    float2* dh0;
+    const uint8_t* dict;
+    const uint64_t* rec;
+    const uint8_t* mtab;
+    int* status;
+    LdsLayout lds;
+};
+
+hipError_t launch_prep(const PrepArgs& p, hipStream_t s);
+hipError_t launch_fwd_fused(const FusedArgs& a, hipStream_t s);
+hipError_t launch_bwd_fused(const FusedArgs& a, hipStream_t s);
+
+}  // namespace pdssm

@@ -1,0 +1,655 @@
+// pdssm_fused.hip -- single-read fused PD scan for gfx950.
+//
+// Layout of the work.  One workgroup of W waves owns one (batch, head)
+// sequence.  The sequence is cut into chunks of TAU steps (App. E.1
+// Algorithm 1); wave w takes chunks w, w+W, w+2W, ... .  For each chunk the
+// wave
+//   1. loads the chunk's D, b, c rows (and idx) into registers -- the only
+//      time they are read from HBM;
+//   2. folds the chunk into its PD operator (pi_c, d_c) and local state B_c
+//      (the state the chunk reaches from zero), App. E.3.1 accumulator update;
+//   3. waits for the state entering the chunk from the wave that owns the
+//      previous chunk (an LDS hand-off, no workgroup barrier), passes on
+//      carry_{c+1} = B_c + (pi_c, d_c) carry_c at once, and records carry_c as
+//      the saved chunk state;
+//   4. replays the chunk from carry_c out of its registers and reduces the
+//      readout y_t = Re<c_t, h_t> on the fly; h_t never reaches memory.
+// The backward runs the same schedule in reverse time with the adjoint
+// recurrence (a gather: g_{t-1}[j] = conj(D_t[j]) g_t[pi_t[j]] + readout term),
+// recomputing the chunk's states from its saved entering state.
+//
+// Scatter as gathers.  The forward step h'[r] = b[r] + sum_{j: pi(j)=r}
+// D[j] h[j] adds up every source that lands on row r.  For each dictionary
+// entry a prep kernel lists, per destination row, its sources in ascending
+// order (up to 7, plus the in-degree) once per call; the step then writes
+// D .* h to LDS once and every lane gathers its row's sources.  The order of
+// the sum is fixed, so results are deterministic.  The number of gathers per
+// step is fixed per head (1, 3 or 7, the head's largest in-degree rounded
+// up), so the step has no branches: unused record slots point at a row that
+// stays zero.  An entry with a row of in-degree above 7 (rare for random maps,
+// e.g. an all-to-one map) takes an LDS float-atomic scatter instead; heads
+// without such entries never test for it.
+//
+// The last chunk of a sequence may be short; its missing steps run as exact
+// no-ops (D = 1, b = 0, an identity dictionary entry at index K), so no step
+// tests its own index either.
+#include "pdssm_device.h"
+#include "pdssm_fused.h"
+
+namespace pdssm {
+
+namespace {
+
+constexpr int kMaxSrc = 7;          // sources per row record
+constexpr unsigned kFallback = 255; // mtab value: entry needs the atomic scatter
+
+// Unused source slots: row N of the wave's vd block (kept zero) when it fits
+// in a byte; for N = 256 the in-degree byte masks them instead.
+template <int N>
+struct Sentinel {
+    static constexpr bool kZeroRow = N <= 128;
+    static constexpr unsigned kByte = N <= 128 ? (unsigned)N : 0u;
+};
+
+// ------------------------------------------------------------------ prep
+// One wave per dictionary entry (h, k): byte dictionary, per-row source
+// records, per-entry max in-degree.
+template <int N>
+__global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    __shared__ int psh[4][N];
+    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int e = blockIdx.x * 4 + wv;
+    if (e >= a.H * a.K) return;
+    const bool act = lane < LANES;
+    int* P = psh[wv];
+    bool bad = false;
+    if (act) {
+        IV<SL> p = ld_iv<SL>(a.pi + (size_t)e * N, lane);
+        bad = sanitize_map<N, SL>(p);
+        st_iv<SL>(P, lane, p);
+#pragma unroll
+        for (int s = 0; s < SL; ++s) a.dict[(size_t)e * N + lane * SL + s] = (uint8_t)p.v[s];
+    }
+    wave_sync();
+    int maxdeg = 0;
+    if (act) {
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            const int r = lane * SL + s;
+            uint64_t rec = 0;
+#pragma unroll
+            for (int m = 0; m < kMaxSrc; ++m) rec |= (uint64_t)Sentinel<N>::kByte << (8 * m);
+            int cnt = 0;
+            for (int j = 0; j < N; ++j) {
+                if (P[j] == r) {
+                    if (cnt < kMaxSrc) {
+                        rec &= ~((uint64_t)255 << (8 * cnt));
+                        rec |= (uint64_t)j << (8 * cnt);
+                    }
+                    ++cnt;
+                }
+            }
+            rec |= (uint64_t)min(cnt, 255) << 56;
+            a.rec[(size_t)e * N + r] = rec;
+            maxdeg = max(maxdeg, cnt);
+        }
+    }
+    for (int off = 32; off >= 1; off >>= 1) maxdeg = max(maxdeg, __shfl_xor(maxdeg, off));
+    if (lane == 0) a.mtab[e] = (uint8_t)(maxdeg <= kMaxSrc ? maxdeg : kFallback);
+    if (bad) report_index_error(a.status);
+}
+
+// ------------------------------------------------------------------ shared pieces
+struct Smem {
+    uint64_t* rec;  // [K+1][N]
+    uint8_t* dict;  // [K+1][N]
+    uint8_t* mtab;  // [K+1]
+    float2* ring;   // [2][N]
+    int* ready;     // [4]
+    float4* vd;     // [W][N+1]
+    float2* x;      // [W][N]
+    uint8_t* pa;    // [W][N] (backward)
+};
+
+__device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout& l) {
+    Smem s;
+    s.rec = reinterpret_cast<uint64_t*>(base + l.rec);
+    s.dict = base + l.dict;
+    s.mtab = base + l.mtab;
+    s.ring = reinterpret_cast<float2*>(base + l.ring);
+    s.ready = reinterpret_cast<int*>(base + l.ready);
+    s.vd = reinterpret_cast<float4*>(base + l.vd);
+    s.x = reinterpret_cast<float2*>(base + l.x);
+    s.pa = base + l.pa;
+    return s;
+}
+
+// Copy head hh's dictionary tables into LDS, append the identity entry and
+// clear every wave's zero row (all threads; a barrier follows).
+template <int N, int W>
+__device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, int hh) {
+    const int nthr = blockDim.x, tid = threadIdx.x;
+    const int K = a.K;
+    const size_t e0 = (size_t)hh * K;
+    const uint64_t* rsrc = a.rec + e0 * N;
+    for (int i = tid; i < K * N; i += nthr) s.rec[i] = rsrc[i];
+    const uint32_t* dsrc = reinterpret_cast<const uint32_t*>(a.dict + e0 * N);
+    uint32_t* ddst = reinterpret_cast<uint32_t*>(s.dict);
+    for (int i = tid; i < K * N / 4; i += nthr) ddst[i] = dsrc[i];
+    for (int i = tid; i < K; i += nthr) s.mtab[i] = a.mtab[e0 + i];
+    for (int j = tid; j < N; j += nthr) {
+        uint64_t rec = (uint64_t)1 << 56 | (uint64_t)j;
+#pragma unroll
+        for (int m = 1; m < kMaxSrc; ++m) rec |= (uint64_t)Sentinel<N>::kByte << (8 * m);
+        s.rec[(size_t)K * N + j] = rec;
+        s.dict[K * N + j] = (uint8_t)j;
+    }
+    if (tid == 0) s.mtab[K] = 1;
+    for (int w = tid; w < W; w += nthr) s.vd[w * (N + 1) + N] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// Gather variant of a head: the smallest of 1, 3, 7 sources covering every
+// entry's in-degree, and whether some entry needs the atomic scatter.
+__device__ __forceinline__ int head_variant(const Smem& s, int K, bool& fallback) {
+    const int lane = lane_id();
+    int m = 0, fb = 0;
+    for (int i = lane; i < K; i += kWave) {
+        const int v = s.mtab[i];
+        if (v == (int)kFallback) fb = 1;
+        else m = max(m, v);
+    }
+    for (int off = 32; off >= 1; off >>= 1) {
+        m = max(m, __shfl_xor(m, off));
+        fb |= __shfl_xor(fb, off);
+    }
+    fallback = fb != 0;
+    return m <= 1 ? 1 : (m <= 3 ? 3 : 7);
+}
+
+// Sequence handled by this workgroup.  Workgroups are dispatched round-robin
+// over the 8 XCDs; consecutive sequences (neighbouring heads of one batch
+// row, whose rows of D/b/c/y sit next to each other in memory) are kept on
+// one XCD so they share its L2.
+__device__ __forceinline__ int xcd_seq(int nseq) {
+    const int i = blockIdx.x;
+    if (nseq % 8 != 0) return i;
+    return (i % 8) * (nseq / 8) + i / 8;
+}
+
+// Spin on the workgroup hand-off counter until it reaches `want`.  Bounded:
+// after kSpinLimit polls the kernel reports an error and proceeds, so a wave
+// always exits.  The counter only grows (atomic max), so a late or early
+// publish can never hide a value another wave waits for.
+constexpr int kSpinLimit = 1 << 22;
+constexpr int kErrHang = -4;  // PDSSM_ERR_HIP
+
+__device__ __forceinline__ void wait_ready(int* ready, int want, int* status) {
+    int spins = 0;
+    while (__hip_atomic_load(ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < want) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++spins > kSpinLimit) {
+            if (status && lane_id() == 0) *status = kErrHang;
+            return;
+        }
+    }
+}
+
+__device__ __forceinline__ void publish_ready(int* ready, int v) {
+    __hip_atomic_fetch_max(ready, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// acc[j] += sum of V[src] over the G listed sources of destination row j;
+// V = the .xy half of the wave's vd rows.  Straight-line: G reads, no tests.
+template <int N, int G>
+__device__ __forceinline__ void gather_rows(const float4* vd, const uint64_t* recrow, int lane,
+                                            CV<Lay<N>::SL>& acc) {
+    constexpr int SL = Lay<N>::SL;
+    const float2* V = reinterpret_cast<const float2*>(vd);
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        const uint64_t r = recrow[lane * SL + s];
+        const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
+#pragma unroll
+        for (int m = 0; m < G; ++m) {
+            const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
+            float2 v = V[2 * src];
+            if constexpr (!Sentinel<N>::kZeroRow) {
+                const bool use = m < (int)(hi >> 24);
+                v = use ? v : make_float2(0.f, 0.f);
+            }
+            acc.v[s].x += v.x;
+            acc.v[s].y += v.y;
+        }
+    }
+}
+
+// Per-chunk registers of one wave.
+template <int N, int TAU>
+struct Chunk {
+    static constexpr int SL = Lay<N>::SL;
+    CV<SL> D[TAU], b[TAU], c[TAU];
+    int kv, mv, len;
+};
+
+// One step h <- bt + P(k) (Dt .* h).  With STAGE_D the step also leaves D_t
+// in vd.zw for a map composition.  FB: the head has entries that need the
+// atomic scatter, tested per step.
+template <int N, int G, bool FB, bool STAGE_D>
+__device__ __forceinline__ void pd_step(const Smem& s, float4* vd, float2* X, int lane, bool act,
+                                        int k, int M, CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt,
+                                        const CV<Lay<N>::SL>& bt) {
+    constexpr int SL = Lay<N>::SL;
+    if constexpr (FB) {
+        if (M == (int)kFallback) {
+            if constexpr (STAGE_D) {
+                wave_sync();
+                if (act) {
+#pragma unroll
+                    for (int q = 0; q < SL; ++q)
+                        reinterpret_cast<float2*>(vd)[2 * (lane * SL + q) + 1] = Dt.v[q];
+                }
+            }
+            IV<SL> pt;
+            if (act) {
+#pragma unroll
+                for (int q = 0; q < SL; ++q) pt.v[q] = s.dict[k * N + lane * SL + q];
+            }
+            pd_scatter_step<N>(X, lane, act, h, Dt, bt, pt);
+            return;
+        }
+    }
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int q = 0; q < SL; ++q) {
+            const float2 v = cmul(Dt.v[q], h.v[q]);
+            if constexpr (STAGE_D)
+                vd[lane * SL + q] = make_float4(v.x, v.y, Dt.v[q].x, Dt.v[q].y);
+            else
+                reinterpret_cast<float2*>(vd)[2 * (lane * SL + q)] = v;
+        }
+    }
+    wave_sync();
+    if (act) {
+        CV<SL> acc = bt;
+        gather_rows<N, G>(vd, s.rec + (size_t)k * N, lane, acc);
+        h = acc;
+    }
+}
+
+// Loads chunk ch of sequence (bb, hh) into registers; the missing steps of a
+// short last chunk become identity steps.
+template <int N, int TAU, bool LOAD_B, bool LOAD_C>
+__device__ __forceinline__ void load_chunk(const FusedArgs& a, const Smem& s, int bb, int hh, int ch,
+                                           int lane, bool act, Chunk<N, TAU>& q, bool& bad) {
+    constexpr int SL = Lay<N>::SL;
+    const int s0 = ch * TAU;
+    q.len = min(TAU, a.L - s0);
+    const size_t stride = (size_t)a.H * N;
+    const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
+    int kv = a.K;  // identity entry for padded steps
+    if (lane < q.len) {
+        kv = a.idx[((size_t)bb * a.L + s0 + lane) * a.H + hh];
+        const bool bk = (unsigned)kv >= (unsigned)a.K;
+        bad |= bk;
+        kv = bk ? 0 : kv;
+    }
+    q.kv = kv;
+#pragma unroll
+    for (int t = 0; t < TAU; ++t) {
+        const size_t off = base + (size_t)min(t, q.len - 1) * stride;
+        if (act) {
+            q.D[t] = ld_cv<SL>(a.D + off, lane);
+            if constexpr (LOAD_B) q.b[t] = ld_cv<SL>(a.b + off, lane);
+            if constexpr (LOAD_C) q.c[t] = ld_cv<SL>(a.c + off, lane);
+        } else {
+            q.D[t] = cv_zero<SL>();
+            if constexpr (LOAD_B) q.b[t] = cv_zero<SL>();
+            if constexpr (LOAD_C) q.c[t] = cv_zero<SL>();
+        }
+    }
+    q.mv = s.mtab[kv];
+    if (q.len < TAU) {
+#pragma unroll
+        for (int t = 0; t < TAU; ++t) {
+            if (t >= q.len) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    q.D[t].v[r] = make_float2(1.f, 0.f);
+                    if constexpr (LOAD_B) q.b[t].v[r] = make_float2(0.f, 0.f);
+                    if constexpr (LOAD_C) q.c[t].v[r] = make_float2(0.f, 0.f);
+                }
+            }
+        }
+    }
+}
+
+// ================================================================== forward
+template <int N, int TAU, int W, int G, bool FB>
+__device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const bool act = lane < LANES;
+    float4* vd = s.vd + wv * (N + 1);
+    float2* X = s.x + wv * N;
+    bool bad = false;
+
+    for (int ch = wv; ch < a.C; ch += W) {
+        // ---- 1. load the chunk
+        Chunk<N, TAU> q;
+        load_chunk<N, TAU, true, true>(a, s, bb, hh, ch, lane, act, q, bad);
+
+        // ---- 2. chunk operator (pi_c, d_c) and local state B_c
+        IV<SL> pm;
+        CV<SL> dm, Bm = cv_zero<SL>();
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            pm.v[r] = lane * SL + r;
+            dm.v[r] = make_float2(1.f, 0.f);
+        }
+#pragma unroll
+        for (int t = 0; t < TAU; ++t) {
+            const int k = readlane_i(q.kv, t);
+            const int M = FB ? readlane_i(q.mv, t) : 0;
+            pd_step<N, G, FB, true>(s, vd, X, lane, act, k, M, Bm, q.D[t], q.b[t]);
+            // (pi, d) <- (pi_t[pi], D_t[pi] * d), D_t staged in vd.zw
+            if (act) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    const int p = pm.v[r];
+                    dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
+                    pm.v[r] = s.dict[k * N + p];
+                }
+            }
+        }
+
+        // ---- 3. hand-off: carry_{c+1} = B_c + (pi_c, d_c) carry_c
+        wait_ready(s.ready, ch, a.status);
+        CV<SL> carry = cv_zero<SL>();
+        if (act) carry = ld_cv<SL>(s.ring + (ch & 1) * N, lane);
+        CV<SL> nxt = carry;
+        pd_scatter_step<N>(X, lane, act, nxt, dm, Bm, pm);
+        if (act) st_cv<SL>(s.ring + ((ch + 1) & 1) * N, lane, nxt);
+        wave_sync();
+        if (lane == 0) publish_ready(s.ready, ch + 1);
+        if (act) {
+            if (a.saved) st_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane, carry);
+            if (ch == a.C - 1 && a.hfinal) st_cv<SL>(a.hfinal + (size_t)seq * N, lane, nxt);
+        }
+
+        // ---- 4. replay from carry_c with the fused readout
+        CV<SL> h = carry;
+        float yv = 0.f;
+#pragma unroll
+        for (int t = 0; t < TAU; ++t) {
+            const int k = readlane_i(q.kv, t);
+            const int M = FB ? readlane_i(q.mv, t) : 0;
+            pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, h, q.D[t], q.b[t]);
+            float part = 0.f;
+#pragma unroll
+            for (int r = 0; r < SL; ++r) part += q.c[t].v[r].x * h.v[r].x - q.c[t].v[r].y * h.v[r].y;
+            const float tot = readlane_f(wave_sum_last(part), kWave - 1);
+            yv = lane == t ? tot : yv;
+        }
+        if (lane < q.len) a.y[((size_t)bb * a.L + ch * TAU + lane) * a.H + hh] = yv;
+    }
+    if (bad) report_index_error(a.status);
+}
+
+template <int N, int TAU, int W>
+__global__ __launch_bounds__(W * 64) void k_fwd_fused(FusedArgs a) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    extern __shared__ __align__(16) unsigned char lds[];
+    const Smem s = carve_smem(lds, a.lds);
+    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const bool act = lane < LANES;
+    const int seq = xcd_seq(a.B * a.H);
+    const int bb = seq / a.H, hh = seq - bb * a.H;
+
+    stage_tables<N, W>(a, s, hh);
+    if (wv == 0) {
+        CV<SL> h0 = cv_zero<SL>();
+        if (a.h0 && act) h0 = ld_cv<SL>(a.h0 + (size_t)seq * N, lane);
+        if (act) st_cv<SL>(s.ring, lane, h0);
+        if (lane == 0) *s.ready = 0;
+    }
+    __syncthreads();
+    bool fb;
+    const int G = head_variant(s, a.K, fb);
+    if (fb) fwd_body<N, TAU, W, 7, true>(a, s, seq, bb, hh);
+    else if (G == 1) fwd_body<N, TAU, W, 1, false>(a, s, seq, bb, hh);
+    else if (G == 3) fwd_body<N, TAU, W, 3, false>(a, s, seq, bb, hh);
+    else fwd_body<N, TAU, W, 7, false>(a, s, seq, bb, hh);
+}
+
+// ================================================================== backward
+template <int N, int TAU, int W, int G, bool FB>
+__device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const bool act = lane < LANES;
+    float4* vd = s.vd + wv * (N + 1);
+    float2* X = s.x + wv * N;
+    uint8_t* PA = s.pa + wv * N;
+    const size_t stride = (size_t)a.H * N;
+    bool bad = false;
+
+    for (int r = wv; r < a.C; r += W) {
+        const int ch = a.C - 1 - r;
+        const int s0 = ch * TAU;
+        const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
+        Chunk<N, TAU> q;
+        load_chunk<N, TAU, false, true>(a, s, bb, hh, ch, lane, act, q, bad);
+        float dyv = 0.f;
+        if (lane < q.len) dyv = a.dy[((size_t)bb * a.L + s0 + lane) * a.H + hh];
+
+        // ---- local adjoint from zero and the chunk operator, reverse time:
+        // Phi <- Phi A_t: pa(j) <- pa[pi_t(j)], da(j) <- da[pi_t(j)] D_t(j)
+        CV<SL> g = cv_zero<SL>(), da;
+        IV<SL> pa;
+#pragma unroll
+        for (int i = 0; i < SL; ++i) {
+            pa.v[i] = lane * SL + i;
+            da.v[i] = make_float2(1.f, 0.f);
+        }
+#pragma unroll
+        for (int t = TAU - 1; t >= 0; --t) {
+            const int k = readlane_i(q.kv, t);
+            const float dyt = readlane_f(dyv, t);
+            IV<SL> pt;
+            wave_sync();
+            if (act) {
+#pragma unroll
+                for (int i = 0; i < SL; ++i) {
+                    pt.v[i] = s.dict[k * N + lane * SL + i];
+                    g.v[i].x += dyt * q.c[t].v[i].x;
+                    g.v[i].y -= dyt * q.c[t].v[i].y;
+                    vd[lane * SL + i] = make_float4(g.v[i].x, g.v[i].y, da.v[i].x, da.v[i].y);
+                    PA[lane * SL + i] = (uint8_t)pa.v[i];
+                }
+            }
+            wave_sync();
+            if (act) {
+#pragma unroll
+                for (int i = 0; i < SL; ++i) {
+                    const float4 e = vd[pt.v[i]];
+                    pa.v[i] = PA[pt.v[i]];
+                    da.v[i] = cmul(make_float2(e.z, e.w), q.D[t].v[i]);
+                    g.v[i] = cmulc(q.D[t].v[i], make_float2(e.x, e.y));
+                }
+            }
+        }
+
+        // ---- start the loads the recompute needs while the hand-off waits
+#pragma unroll
+        for (int t = 0; t < TAU; ++t) {
+            const size_t off = base + (size_t)min(t, q.len - 1) * stride;
+            q.b[t] = act ? ld_cv<SL>(a.b + off, lane) : cv_zero<SL>();
+        }
+        CV<SL> hs = cv_zero<SL>();
+        if (act) hs = ld_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane);
+
+        // ---- hand-off: U_{c-1} = gamma_c + Phi_c^H U_c (a gather from the ring)
+        wait_ready(s.ready, r, a.status);
+        CV<SL> U = cv_zero<SL>(), Up;
+        if (act) {
+            const float2* ring = s.ring + (r & 1) * N;
+            U = ld_cv<SL>(ring, lane);
+#pragma unroll
+            for (int i = 0; i < SL; ++i) Up.v[i] = cadd(g.v[i], cmulc(da.v[i], ring[pa.v[i]]));
+            st_cv<SL>(s.ring + ((r + 1) & 1) * N, lane, Up);
+        }
+        wave_sync();
+        if (lane == 0) publish_ready(s.ready, r + 1);
+        if (ch == 0 && a.dh0 && act) st_cv<SL>(a.dh0 + (size_t)seq * N, lane, Up);
+
+        // ---- recompute the chunk's states from the saved entering state
+        if (q.len < TAU) {
+#pragma unroll
+            for (int t = 0; t < TAU; ++t)
+                if (t >= q.len) q.b[t] = cv_zero<SL>();
+        }
+        CV<SL> Hs[TAU + 1];
+        Hs[0] = hs;
+#pragma unroll
+        for (int t = 0; t < TAU; ++t) {
+            const int k = readlane_i(q.kv, t);
+            const int M = FB ? readlane_i(q.mv, t) : 0;
+            pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, hs, q.D[t], q.b[t]);
+            Hs[t + 1] = hs;
+        }
+
+        // ---- final reverse walk with the true incoming gradient
+        g = U;
+#pragma unroll
+        for (int t = TAU - 1; t >= 0; --t) {
+            const int k = readlane_i(q.kv, t);
+            const float dyt = readlane_f(dyv, t);
+            const size_t off = base + (size_t)t * stride;
+            IV<SL> pt;
+            CV<SL> dct;
+            wave_sync();
+            if (act) {
+#pragma unroll
+                for (int i = 0; i < SL; ++i) {
+                    pt.v[i] = s.dict[k * N + lane * SL + i];
+                    g.v[i].x += dyt * q.c[t].v[i].x;
+                    g.v[i].y -= dyt * q.c[t].v[i].y;
+                    dct.v[i] = make_float2(dyt * Hs[t + 1].v[i].x, -dyt * Hs[t + 1].v[i].y);
+                    reinterpret_cast<float2*>(vd)[2 * (lane * SL + i)] = g.v[i];
+                }
+            }
+            if (t < q.len && act) {
+                st_cv<SL>(a.db + off, lane, g);
+                st_cv<SL>(a.dc + off, lane, dct);
+            }
+            wave_sync();
+            if (act) {
+                CV<SL> dDt;
+#pragma unroll
+                for (int i = 0; i < SL; ++i) {
+                    const float2 gp = reinterpret_cast<const float2*>(vd)[2 * pt.v[i]];
+                    dDt.v[i] = cmulc(Hs[t].v[i], gp);
+                    g.v[i] = cmulc(q.D[t].v[i], gp);
+                }
+                if (t < q.len) st_cv<SL>(a.dD + off, lane, dDt);
+            }
+        }
+    }
+    if (bad) report_index_error(a.status);
+}
+
+template <int N, int TAU, int W>
+__global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    extern __shared__ __align__(16) unsigned char lds[];
+    const Smem s = carve_smem(lds, a.lds);
+    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const bool act = lane < LANES;
+    const int seq = xcd_seq(a.B * a.H);
+    const int bb = seq / a.H, hh = seq - bb * a.H;
+
+    stage_tables<N, W>(a, s, hh);
+    if (wv == 0) {
+        CV<SL> u = cv_zero<SL>();
+        if (a.dhf && act) u = ld_cv<SL>(a.dhf + (size_t)seq * N, lane);
+        if (act) st_cv<SL>(s.ring, lane, u);
+        if (lane == 0) *s.ready = 0;
+    }
+    __syncthreads();
+    bool fb;
+    const int G = head_variant(s, a.K, fb);
+    if (fb) bwd_body<N, TAU, W, 7, true>(a, s, seq, bb, hh);
+    else if (G == 1) bwd_body<N, TAU, W, 1, false>(a, s, seq, bb, hh);
+    else if (G == 3) bwd_body<N, TAU, W, 3, false>(a, s, seq, bb, hh);
+    else bwd_body<N, TAU, W, 7, false>(a, s, seq, bb, hh);
+}
+
+template <int N, int TAU, int W>
+hipError_t fwd_launch(const FusedArgs& a, hipStream_t st) {
+    auto kern = k_fwd_fused<N, TAU, W>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(W * 64), a.lds.total, st, a);
+    return hipGetLastError();
+}
+
+template <int N, int TAU, int W>
+hipError_t bwd_launch(const FusedArgs& a, hipStream_t st) {
+    auto kern = k_bwd_fused<N, TAU, W>;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(W * 64), a.lds.total, st, a);
+    return hipGetLastError();
+}
+
+template <int N>
+hipError_t prep_launch(const PrepArgs& p, hipStream_t st) {
+    hipLaunchKernelGGL(k_prep<N>, dim3((p.H * p.K + 3) / 4), dim3(256), 0, st, p);
+    return hipGetLastError();
+}
+
+// Chunk lengths compiled per N: TAU * max(1, N/64) <= 16 keeps a chunk's
+// D, b, c rows (and the backward's recomputed states) in registers.
+template <int N, bool FWD>
+hipError_t dispatch_tau(const FusedArgs& a, hipStream_t st) {
+    constexpr int SL = Lay<N>::SL;
+    constexpr int W = kFusedWaves;
+    switch (a.tau) {
+        case 4: return FWD ? fwd_launch<N, 4, W>(a, st) : bwd_launch<N, 4, W>(a, st);
+        case 8:
+            if constexpr (8 * SL <= 16) return FWD ? fwd_launch<N, 8, W>(a, st) : bwd_launch<N, 8, W>(a, st);
+            break;
+        case 16:
+            if constexpr (16 * SL <= 16) return FWD ? fwd_launch<N, 16, W>(a, st) : bwd_launch<N, 16, W>(a, st);
+            break;
+        default: break;
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+#define PDSSM_FUSED_N(N_, EXPR_T)                     \
+    switch (N_) {                                     \
+        case 8: { constexpr int NN = 8; EXPR_T; }     \
+        case 16: { constexpr int NN = 16; EXPR_T; }   \
+        case 32: { constexpr int NN = 32; EXPR_T; }   \
+        case 64: { constexpr int NN = 64; EXPR_T; }   \
+        case 128: { constexpr int NN = 128; EXPR_T; } \
+        case 256: { constexpr int NN = 256; EXPR_T; } \
+        default: return hipErrorInvalidValue;         \
+    }
+
+hipError_t launch_prep(const PrepArgs& p, hipStream_t st) { PDSSM_FUSED_N(p.N, return prep_launch<NN>(p, st)) }
+hipError_t launch_fwd_fused(const FusedArgs& a, hipStream_t st) {
+    PDSSM_FUSED_N(a.N, return (dispatch_tau<NN, true>(a, st)))
+}
+hipError_t launch_bwd_fused(const FusedArgs& a, hipStream_t st) {
+    PDSSM_FUSED_N(a.N, return (dispatch_tau<NN, false>(a, st)))
+}
+
+}  // namespace pdssm

@@ -37,13 +37,16 @@ def test_exports_every_declared_function(lib):
 
 def test_chunk_and_workspace_queries(lib):
     d = pdssm.desc(16, 2048, 16, 64, 16)
-    assert pdssm.chunk_len(d) == 32
-    assert pdssm.num_chunks(d) == 64
-    d = pdssm.desc(8, 18000, 8, 128, 32, chunk=16)
-    assert pdssm.num_chunks(d) == 1125
+    assert pdssm.chunk_len(d) == 16
+    assert pdssm.num_chunks(d) == 128
+    d = pdssm.desc(8, 18000, 8, 128, 32)
+    assert pdssm.chunk_len(d) == 8
+    assert pdssm.num_chunks(d) == 2250
+    assert pdssm.num_chunks(pdssm.desc(8, 18000, 8, 128, 32, chunk=16)) == pdssm.ERR_UNSUPPORTED
+    assert pdssm.chunk_len(pdssm.desc(1, 10, 1, 256, 4)) == 4
     for op in (pdssm.OP_FWD, pdssm.OP_BWD):
         n = pdssm.workspace_size(d, op)
-        assert n >= 8 * 8 * 1125 * 128 * 28
+        assert n >= 8 * 32 * 128 * 9  # dictionary tables of the fused path
     assert pdssm.workspace_size(d, pdssm.OP_COMPOSE) == 0
     d = pdssm.desc(1, 1, 1, 8, 1)
     assert pdssm.num_chunks(d) == 1
@@ -54,6 +57,8 @@ def test_chunk_and_workspace_queries(lib):
     (dict(N=512), pdssm.ERR_UNSUPPORTED),
     (dict(K=257), pdssm.ERR_UNSUPPORTED),
     (dict(chunk=24), pdssm.ERR_UNSUPPORTED),
+    (dict(chunk=32), pdssm.ERR_UNSUPPORTED),
+    (dict(N=128, chunk=16), pdssm.ERR_UNSUPPORTED),
     (dict(L=0), pdssm.ERR_INVALID_ARG),
     (dict(B=-1), pdssm.ERR_INVALID_ARG),
     (dict(chunk=-3), pdssm.ERR_INVALID_ARG),

@@ -56,10 +56,11 @@ def check_all(inp, got, chunk_eff, bwd=True):
 # ------------------------------------------------------------------ small shapes
 CASES = []
 for N in (8, 16, 32, 64, 128, 256):
-    for chunk in (16, 32, 64):
-        if (chunk + 2) * N * 8 > 65536:
+    for chunk in (4, 8, 16):
+        if chunk * max(1, N // 64) > 16:
             continue
-        for L in (1, chunk - 1, chunk, chunk + 1, 3 * chunk + 5):
+        # ragged edges, and enough chunks (> 12 waves) to wrap the round-robin
+        for L in (1, chunk - 1, chunk, chunk + 1, 3 * chunk + 5, 30 * chunk + 7):
             CASES.append((N, chunk, L))
 
 
@@ -77,22 +78,43 @@ def test_map_kinds_default_chunk(pi_kind):
     inp = make_inputs(B=3, L=200, H=2, N=64, K=7, seed=7, pi_kind=pi_kind, with_h0=True,
                       with_dhf=True)
     got = run_gpu(inp)
-    check_all(inp, got, 32)
+    check_all(inp, got, 16)
 
 
 def test_single_dictionary_entry_and_k256():
     for K in (1, 256):
         inp = make_inputs(B=1, L=70, H=2, N=32, K=K, seed=K)
         got = run_gpu(inp)
-        check_all(inp, got, 32)
+        check_all(inp, got, 16)
 
 
-def test_all_maps_collapse_to_one_row():
-    """Degenerate many-to-one maps: every entry maps to row 0 (maximal collisions)."""
-    inp = make_inputs(B=1, L=50, H=1, N=128, K=3, seed=3)
+@pytest.mark.parametrize("N", [64, 128])
+def test_all_maps_collapse_to_one_row(N):
+    """Degenerate many-to-one maps: every entry maps to row 0 (maximal
+    collisions, in-degree N: the atomic-scatter branch)."""
+    inp = make_inputs(B=1, L=250, H=1, N=N, K=3, seed=3)
     inp["pi"][:] = 0
     got = run_gpu(inp)
-    check_all(inp, got, 32)
+    check_all(inp, got, 16 // max(1, N // 64))
+
+
+def test_mixed_degenerate_and_regular_entries():
+    """Some dictionary entries need the atomic branch (a row of in-degree > 7),
+    the others the gather records; steps switch between them."""
+    inp = make_inputs(B=2, L=400, H=2, N=64, K=6, seed=31, with_h0=True, with_dhf=True)
+    inp["pi"][0, 1, :9] = 5
+    inp["pi"][1, 4, :] = 63
+    got = run_gpu(inp)
+    check_all(inp, got, 16)
+
+
+@pytest.mark.parametrize("N,K", [(128, 128), (256, 64)])
+def test_large_dictionary_chunked_path(N, K):
+    """A head's dictionary tables too large for LDS: the chunked three-pass
+    kernels run instead, with the same saved-state layout."""
+    inp = make_inputs(B=2, L=90, H=2, N=N, K=K, seed=N + K, with_h0=True, with_dhf=True)
+    got = run_gpu(inp)
+    check_all(inp, got, 16 // max(1, N // 64))
 
 
 # ------------------------------------------------------------------ automaton: exact
