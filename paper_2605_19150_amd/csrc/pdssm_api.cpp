@@ -48,7 +48,7 @@ int scan_chunk(const pdssm_desc* d) {
     int st = check_dims(d);
     if (st != PDSSM_OK) return st;
     int tau = d->chunk;
-    if (tau == 0) tau = 16 / slots(d->N);
+    if (tau == 0) tau = slots(d->N) >= 2 ? 4 : 8;
     if (!scan_chunk_ok(d->N, tau)) return PDSSM_ERR_UNSUPPORTED;
     return tau;
 }
@@ -92,7 +92,8 @@ Sizes sizes_of(const pdssm_desc* d, int C) {
 // The fused single-read kernels stage one head's dictionary tables in LDS;
 // when they do not fit, the chunked three-pass kernels run instead.
 bool use_fused(const pdssm_desc* d) {
-    return pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWaves).total <= pdssm::kMaxLds;
+    const int tau = scan_chunk(d);
+    return pdssm::fused_lds_layout(d->N, d->K, pdssm::fused_waves(d->N, tau)).total <= pdssm::kMaxLds;
 }
 
 // Fused workspace: byte dictionary, row records, per-entry max in-degree.
@@ -138,7 +139,7 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     f.dict = pa.dict;
     f.rec = pa.rec;
     f.mtab = pa.mtab;
-    f.lds = pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWaves);
+    f.lds = pdssm::fused_lds_layout(d->N, d->K, pdssm::fused_waves(d->N, f.tau));
     return pdssm::launch_prep(pa, st);
 }
 

@@ -35,7 +35,7 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     __shared__ float2 xs[kWavesPerGroup][N];
     __shared__ float2 dsh[kWavesPerGroup][N];
     __shared__ int psh[kWavesPerGroup][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int nseq = a.B * a.H;
     const int task = blockIdx.x * kWavesPerGroup + wv;
     if (task >= nseq * a.C) return;
@@ -117,7 +117,7 @@ template <int N>
 __global__ __launch_bounds__(256) void k_fwd_carry(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 xs[kWavesPerGroup][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int seq = blockIdx.x * kWavesPerGroup + wv;
     if (seq >= a.B * a.H) return;
     const bool act = lane < LANES;
@@ -152,7 +152,7 @@ template <int N>
 __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 xs[kWavesPerGroup][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int nseq = a.B * a.H;
     const int task = blockIdx.x * kWavesPerGroup + wv;
     if (task >= nseq * a.C) return;
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(256) void k_bwd_agg(ScanArgs a) {
     __shared__ float2 gsh[kWavesPerGroup][N];
     __shared__ float2 dsh[kWavesPerGroup][N];
     __shared__ int psh[kWavesPerGroup][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int nseq = a.B * a.H;
     const int task = blockIdx.x * kWavesPerGroup + wv;
     if (task >= nseq * a.C) return;
@@ -306,7 +306,7 @@ template <int N>
 __global__ __launch_bounds__(256) void k_bwd_carry(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 xs[kWavesPerGroup][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int seq = blockIdx.x * kWavesPerGroup + wv;
     if (seq >= a.B * a.H) return;
     const bool act = lane < LANES;
@@ -461,7 +461,7 @@ __global__ __launch_bounds__(256) void k_compose(ComposeArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 dsh[kWavesPerGroup][N];
     __shared__ int psh[kWavesPerGroup][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int nseq = a.B * a.H;
     const int task = blockIdx.x * kWavesPerGroup + wv;
     if (task >= nseq * a.C) return;

@@ -44,6 +44,12 @@ __device__ __forceinline__ void wave_sync() {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
+// Index of this wave in its workgroup, as a wave-uniform (scalar) value: the
+// compiler cannot prove threadIdx.x >> 6 uniform, and everything derived from
+// it (chunk numbers, row addresses, loop bounds) would otherwise live in
+// vector registers and branch per lane.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
 __device__ __forceinline__ int readlane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ __forceinline__ float readlane_f(float v, int l) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
@@ -68,6 +74,15 @@ __device__ __forceinline__ float wave_sum_last(float v) {
     v += t;
     return v;
 }
+
+// Forces a value to be computed before this point: the compiler otherwise
+// sinks work to its first use, which may sit behind a wait on another wave.
+__device__ __forceinline__ void materialize(float v) { asm volatile("" ::"v"(v) : "memory"); }
+__device__ __forceinline__ void materialize(int v) { asm volatile("" ::"v"(v) : "memory"); }
+
+// Keeps memory operations issued before this point from being moved below it
+// (e.g. a prefetch the compiler would otherwise sink to its first use).
+__device__ __forceinline__ void issue_fence() { asm volatile("" ::: "memory"); }
 
 // ------------------------------------------------------------------ per-lane vectors
 template <int SL>
@@ -103,6 +118,38 @@ __device__ __forceinline__ CV<SL> ld_cv(const float2* __restrict__ row, int lane
         }
     }
     return r;
+}
+
+// Raw buffer access to rows of a [.., N] complex tensor: a scalar resource
+// descriptor holds the base of a block of rows, a scalar offset selects the
+// row and one shared 32-bit VGPR holds the lane's byte offset, so a chunk of
+// row loads costs no per-load 64-bit address registers.
+constexpr int kBufferDword3 = 0x00020000;  // raw buffer, gfx9 family
+// Cache-policy operand of a load that streams data read exactly once: the
+// nontemporal hint (nt) of gfx94x/gfx950.
+constexpr int kLoadStream = 2;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_block(const float2* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float2*>(base), 0, bytes, kBufferDword3);
+}
+
+// This lane's SL consecutive complex entries of the row at byte offset soff;
+// AUX is the cache-policy operand (0 or kLoadStream).
+template <int SL, int AUX = 0>
+__device__ __forceinline__ CV<SL> ld_row(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    CV<SL> out;
+    if constexpr (SL == 1) {
+        out.v[0] = __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 2) {
+            const float4 q =
+                __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff + 8 * s, AUX));
+            out.v[s] = make_float2(q.x, q.y);
+            out.v[s + 1] = make_float2(q.z, q.w);
+        }
+    }
+    return out;
 }
 
 template <int SL>

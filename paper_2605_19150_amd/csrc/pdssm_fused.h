@@ -6,19 +6,33 @@
 
 namespace pdssm {
 
-// Waves per workgroup of the fused kernels (one workgroup per sequence).
-constexpr int kFusedWaves = 12;
+// Chunk-computing waves per workgroup of the fused kernels (one workgroup per
+// sequence; the forward adds one frontier wave).
+// Kernels that prefetch the next chunk (two register buffers, when a chunk
+// holds <= 8 rows per lane) run fewer, fatter waves.
+#ifndef PDSSM_PF_WAVES
+#define PDSSM_PF_WAVES 8
+#endif
+#ifndef PDSSM_PF_MAX_ROWS
+#define PDSSM_PF_MAX_ROWS 8
+#endif
+constexpr int kFusedWaves = 11;
+constexpr bool fused_prefetch(int N, int tau) { return tau * (N > 64 ? N / 64 : 1) <= PDSSM_PF_MAX_ROWS; }
+constexpr int fused_waves(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_PF_WAVES : kFusedWaves; }
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
-    uint32_t rec, dict, mtab, ring, ready, vd, x, pa, total;
+    uint32_t rec, dict, mtab, ring, ready, agg, agp, aflag, vd, x, cs, pa, total;
 };
 
 inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
 
 // Dictionary tables hold K entries plus one identity entry (index K) that
 // pads the last, partial chunk of a sequence with exact no-op steps.  Each
-// wave's vd row block has N + 1 rows; row N stays zero.
+// wave's vd row block has N + 1 rows; row N stays zero.  W is the number of
+// chunk-computing waves; one more wave (the frontier wave) carries the state
+// from chunk to chunk.  ring: W + 1 carry slots; agg/agp/aflag: 2W slots of
+// published chunk operators (local state, diagonal, map) and their chunk ids.
 inline LdsLayout fused_lds_layout(int N, int K, int W) {
     LdsLayout l;
     size_t o = 0;
@@ -26,10 +40,15 @@ inline LdsLayout fused_lds_layout(int N, int K, int W) {
     l.rec = (uint32_t)o;   o += KE * N * 8;
     l.dict = (uint32_t)o;  o += align16(KE * N);
     l.mtab = (uint32_t)o;  o += align16(KE);
-    l.ring = (uint32_t)o;  o += (size_t)2 * N * 8;
-    l.ready = (uint32_t)o; o += 16;
+    l.ring = (uint32_t)o;  o += (size_t)(W + 1) * N * 8;
+    l.ready = (uint32_t)o; // followed by the 2W operator-slot flags
+    l.aflag = (uint32_t)(o + 4);
+    o += align16((size_t)(1 + 2 * W) * 4);
+    l.agg = (uint32_t)o;   o += (size_t)2 * W * N * 16;
+    l.agp = (uint32_t)o;   o += align16((size_t)2 * W * N);
     l.vd = (uint32_t)o;    o += (size_t)W * (N + 1) * 16;
-    l.x = (uint32_t)o;     o += (size_t)W * N * 8;
+    l.x = (uint32_t)o;     o += (size_t)(W + 1) * N * 8;
+    l.cs = (uint32_t)o;    o += (size_t)W * N * 8;
     l.pa = (uint32_t)o;    o += align16((size_t)W * N);
     l.total = (uint32_t)o;
     return l;

@@ -58,7 +58,7 @@ template <int N>
 __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ int psh[4][N];
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const int e = blockIdx.x * 4 + wv;
     if (e >= a.H * a.K) return;
     const bool act = lane < LANES;
@@ -105,10 +105,14 @@ struct Smem {
     uint64_t* rec;  // [K+1][N]
     uint8_t* dict;  // [K+1][N]
     uint8_t* mtab;  // [K+1]
-    float2* ring;   // [2][N]
-    int* ready;     // [4]
+    float2* ring;   // [W+1][N] carry slots
+    int* ready;     // carry counter, followed by the operator-slot flags
+    float4* agg;    // [2W][N] published chunk operator: local state (xy), diagonal (zw)
+    uint8_t* agp;   // [2W][N] published chunk map
+    int* aflag;     // [2W] chunk id held by each operator slot
     float4* vd;     // [W][N+1]
     float2* x;      // [W][N]
+    float2* cs;     // [W][N] (forward: staged c_t)
     uint8_t* pa;    // [W][N] (backward)
 };
 
@@ -119,8 +123,12 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
     s.mtab = base + l.mtab;
     s.ring = reinterpret_cast<float2*>(base + l.ring);
     s.ready = reinterpret_cast<int*>(base + l.ready);
+    s.agg = reinterpret_cast<float4*>(base + l.agg);
+    s.agp = base + l.agp;
+    s.aflag = reinterpret_cast<int*>(base + l.aflag);
     s.vd = reinterpret_cast<float4*>(base + l.vd);
     s.x = reinterpret_cast<float2*>(base + l.x);
+    s.cs = reinterpret_cast<float2*>(base + l.cs);
     s.pa = base + l.pa;
     return s;
 }
@@ -177,19 +185,23 @@ __device__ __forceinline__ int xcd_seq(int nseq) {
     return (i % 8) * (nseq / 8) + i / 8;
 }
 
-// Spin on the workgroup hand-off counter until it reaches `want`.  Bounded:
-// after kSpinLimit polls the kernel reports an error and proceeds, so a wave
-// always exits.  The counter only grows (atomic max), so a late or early
-// publish can never hide a value another wave waits for.
+// Spin on a workgroup hand-off flag until it reaches `want`.  Every flag only
+// grows (atomic max), so a late or early publish can never hide a value
+// another wave waits for.  Bounded: after kSpinLimit polls the wave reports an
+// error and raises every flag of the workgroup (the nflags ints at `all`) to
+// INT_MAX, so that all other waiting waves are released at once and the grid
+// drains.
 constexpr int kSpinLimit = 1 << 22;
 constexpr int kErrHang = -4;  // PDSSM_ERR_HIP
 
-__device__ __forceinline__ void wait_ready(int* ready, int want, int* status) {
+__device__ __forceinline__ void wait_ready(int* ready, int want, int* status, int* all, int nflags) {
     int spins = 0;
     while (__hip_atomic_load(ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < want) {
         __builtin_amdgcn_s_sleep(1);
         if (++spins > kSpinLimit) {
             if (status && lane_id() == 0) *status = kErrHang;
+            for (int i = lane_id(); i < nflags; i += kWave)
+                __hip_atomic_fetch_max(all + i, 0x7fffffff, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             return;
         }
     }
@@ -278,156 +290,406 @@ __device__ __forceinline__ void pd_step(const Smem& s, float4* vd, float2* X, in
     }
 }
 
-// Loads chunk ch of sequence (bb, hh) into registers; the missing steps of a
-// short last chunk become identity steps.
-template <int N, int TAU, bool LOAD_B, bool LOAD_C>
-__device__ __forceinline__ void load_chunk(const FusedArgs& a, const Smem& s, int bb, int hh, int ch,
-                                           int lane, bool act, Chunk<N, TAU>& q, bool& bad) {
+// Issues the loads of chunk ch of sequence (bb, hh) into registers and
+// consumes none of them, so a wave can prefetch one chunk while it computes
+// another.  Steps past the end of a short last chunk read through a null
+// buffer descriptor (zero records): out-of-range buffer reads return 0, so
+// their b and c rows are 0; their D row is taken as 1 at use (Dt()).
+//
+// The issue itself never branches (a chunk number >= C issues a chunk with no
+// steps, all through the null descriptor): the compiler can then count the
+// outstanding loads exactly and a wave waits only for the chunk it computes.
+// AUX: cache policy of the row loads (the forward streams them, kLoadStream).
+template <int N, int TAU, bool LOAD_B, bool LOAD_C, int AUX = 0>
+__device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, int ch, int lane, bool act,
+                                            Chunk<N, TAU>& q) {
     constexpr int SL = Lay<N>::SL;
-    const int s0 = ch * TAU;
-    q.len = min(TAU, a.L - s0);
-    const size_t stride = (size_t)a.H * N;
+    const int chc = min(ch, a.C - 1);  // addresses stay inside the tensors
+    const int s0 = chc * TAU;
+    const int lenc = min(TAU, a.L - s0);
+    q.len = ch < a.C ? lenc : 0;
     const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
-    int kv = a.K;  // identity entry for padded steps
-    if (lane < q.len) {
-        kv = a.idx[((size_t)bb * a.L + s0 + lane) * a.H + hh];
-        const bool bk = (unsigned)kv >= (unsigned)a.K;
-        bad |= bk;
-        kv = bk ? 0 : kv;
-    }
-    q.kv = kv;
+    q.kv = a.idx[((size_t)bb * a.L + s0 + min(lane, lenc - 1)) * a.H + hh];
+    const uint32_t rstride = (uint32_t)a.H * N * 8;  // bytes between consecutive steps
+    const uint32_t extent = (uint32_t)(lenc - 1) * rstride + N * 8;
+    const __amdgpu_buffer_rsrc_t rD = row_block(a.D + base, extent);
+    const __amdgpu_buffer_rsrc_t rb = row_block(a.b + base, extent);
+    const __amdgpu_buffer_rsrc_t rc = row_block(a.c + base, extent);
+    const __amdgpu_buffer_rsrc_t rnull = row_block(a.D, 0);
+    const uint32_t voff = (uint32_t)lane * SL * 8;
 #pragma unroll
     for (int t = 0; t < TAU; ++t) {
-        const size_t off = base + (size_t)min(t, q.len - 1) * stride;
+        const bool in = t < q.len;
+        const uint32_t soff = (uint32_t)t * rstride;
         if (act) {
-            q.D[t] = ld_cv<SL>(a.D + off, lane);
-            if constexpr (LOAD_B) q.b[t] = ld_cv<SL>(a.b + off, lane);
-            if constexpr (LOAD_C) q.c[t] = ld_cv<SL>(a.c + off, lane);
+            q.D[t] = ld_row<SL, AUX>(in ? rD : rnull, voff, soff);
+            if constexpr (LOAD_B) q.b[t] = ld_row<SL, AUX>(in ? rb : rnull, voff, soff);
+            if constexpr (LOAD_C) q.c[t] = ld_row<SL, AUX>(in ? rc : rnull, voff, soff);
         } else {
             q.D[t] = cv_zero<SL>();
             if constexpr (LOAD_B) q.b[t] = cv_zero<SL>();
             if constexpr (LOAD_C) q.c[t] = cv_zero<SL>();
         }
     }
-    q.mv = s.mtab[kv];
-    if (q.len < TAU) {
+}
+
+// D row of step t as used by the step: 1 for the padded steps of a short chunk.
+template <int N, int TAU>
+__device__ __forceinline__ CV<Lay<N>::SL> Dt(const Chunk<N, TAU>& q, int t) {
+    CV<Lay<N>::SL> d = q.D[t];
+    const bool in = t < q.len;
 #pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            if (t >= q.len) {
-#pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    q.D[t].v[r] = make_float2(1.f, 0.f);
-                    if constexpr (LOAD_B) q.b[t].v[r] = make_float2(0.f, 0.f);
-                    if constexpr (LOAD_C) q.c[t].v[r] = make_float2(0.f, 0.f);
-                }
-            }
-        }
+    for (int r = 0; r < Lay<N>::SL; ++r) d.v[r] = in ? d.v[r] : make_float2(1.f, 0.f);
+    return d;
+}
+
+// Completes an issued chunk: checks the dictionary indices (an index outside
+// [0,K) becomes 0 and is reported) and looks up the steps' in-degree class;
+// padded steps use the identity dictionary entry K.
+template <int N, int TAU>
+__device__ __forceinline__ void finish_chunk(const FusedArgs& a, const Smem& s, int lane, Chunk<N, TAU>& q,
+                                             bool& bad) {
+    if (lane < q.len) {
+        const bool bk = (unsigned)q.kv >= (unsigned)a.K;
+        bad |= bk;
+        q.kv = bk ? 0 : q.kv;
+    } else {
+        q.kv = a.K;
     }
+    q.mv = s.mtab[q.kv];
+}
+
+template <int N, int TAU, bool LOAD_B, bool LOAD_C>
+__device__ __forceinline__ void load_chunk(const FusedArgs& a, const Smem& s, int bb, int hh, int ch,
+                                           int lane, bool act, Chunk<N, TAU>& q, bool& bad) {
+    issue_chunk<N, TAU, LOAD_B, LOAD_C>(a, bb, hh, ch, lane, act, q);
+    finish_chunk<N, TAU>(a, s, lane, q, bad);
 }
 
 // ================================================================== forward
+// Cross-lane exchange primitives for the reduction below (VALU only, no LDS):
+// permlane32/16 swaps trade the upper half of one register with the lower
+// half of another across lanes l and l^32 (resp. l^16); DPP mirrors pair a
+// lane with l^15 (16-lane row) and l^7 (8-lane half row); quad_perm pairs l^2
+// and l^1.
+__device__ __forceinline__ float dpp_f(float v, int ctrl) {
+    switch (ctrl) {  // the control word must be a constant
+        case 0x140: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false));
+        case 0x141: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false));
+        case 0x4e: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4e, 0xf, 0xf, false));
+        default: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xb1, 0xf, 0xf, false));
+    }
+}
+
+// Sum over the 64 lanes of each of T per-lane values v[t] (T a power of two
+// <= 64), as a transpose-reduction: log2(T) halving exchanges in which each
+// lane keeps half of its values (the half picked by one bit of its lane
+// index), then plain butterflies.  Lane l ends with the total of value
+// t = l / (64 / T).
+template <int T>
+__device__ __forceinline__ float transpose_sum(float (&v)[T], int lane) {
+    int n = T;
+#pragma unroll
+    for (int lvl = 0; lvl < 6; ++lvl) {
+        const int d = 32 >> lvl;
+        if (n > 1) {
+            const int h = n / 2;
+#pragma unroll
+            for (int i = 0; i < T / 2; ++i) {
+                if (i < h) {
+                    if (d >= 16) {
+                        // lower lanes keep v[i] and receive the partner's v[i];
+                        // upper lanes keep v[i+h] and receive the partner's v[i+h]
+                        auto r = d == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]),
+                                                                          __float_as_uint(v[i + h]), false, false)
+                                         : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]),
+                                                                          __float_as_uint(v[i + h]), false, false);
+                        v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+                    } else {
+                        const bool up = (lane & d) != 0;
+                        const float send = up ? v[i] : v[i + h];
+                        const float keep = up ? v[i + h] : v[i];
+                        v[i] = keep + dpp_f(send, d == 8 ? 0x140 : d == 4 ? 0x141 : d == 2 ? 0x4e : 0xb1);
+                    }
+                }
+            }
+            n = h;
+        } else {
+            if (d >= 16) {
+                auto r = d == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[0]),
+                                                                  false, false)
+                                 : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[0]), __float_as_uint(v[0]),
+                                                                  false, false);
+                v[0] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+            } else {
+                v[0] += dpp_f(v[0], d == 8 ? 0x140 : d == 4 ? 0x141 : d == 2 ? 0x4e : 0xb1);
+            }
+        }
+    }
+    return v[0];
+}
+
+// One chunk is run once, from a zero state (Algorithm 1 Phase A), while the
+// readout is split as in Phase C: with M_t = A_t ... A_s in PD form
+// (Pi_t, Delta_t) and x_t = x_t^loc + M_t carry,
+//   y_t = Re<c_t, x_t^loc> + Re sum_j w_t[j] carry[j],  w_t[j] = Delta_t[j] c_t[Pi_t[j]].
+// The wave keeps w_t and the local readout partials, hands the carry on as
+// soon as the chunk is folded, and finishes y once its own carry arrives.
 template <int N, int TAU, int W, int G, bool FB>
-__device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+__device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int seq, int bb, int hh, int ch,
+                                          Chunk<N, TAU>& q, bool& bad) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     float4* vd = s.vd + wv * (N + 1);
     float2* X = s.x + wv * N;
-    bool bad = false;
+    float2* CS = s.cs + wv * N;
+    finish_chunk<N, TAU>(a, s, lane, q, bad);
 
-    for (int ch = wv; ch < a.C; ch += W) {
-        // ---- 1. load the chunk
-        Chunk<N, TAU> q;
-        load_chunk<N, TAU, true, true>(a, s, bb, hh, ch, lane, act, q, bad);
+    // ---- 2. one pass: local state B, chunk operator (Pi, Delta), w_t, local readout
+    IV<SL> pm;
+    CV<SL> dm, Bm = cv_zero<SL>();
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        pm.v[r] = lane * SL + r;
+        dm.v[r] = make_float2(1.f, 0.f);
+    }
+    CV<SL> wt[TAU];
+    float yl[TAU];
+#pragma unroll
+    for (int t = 0; t < TAU; ++t) {
+        const int k = readlane_i(q.kv, t);
+        const int M = FB ? readlane_i(q.mv, t) : 0;
+        if (act) {
+            wave_sync();
+#pragma unroll
+            for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
+        }
+        pd_step<N, G, FB, true>(s, vd, X, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
+        float part = 0.f;
+        if (act) {
+#pragma unroll
+            for (int r = 0; r < SL; ++r) {
+                // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in vd.zw
+                const int p = pm.v[r];
+                dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
+                pm.v[r] = s.dict[k * N + p];
+                wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
+                part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+            }
+        } else {
+            wt[t] = cv_zero<SL>();
+        }
+        yl[t] = part;
+    }
 
-        // ---- 2. chunk operator (pi_c, d_c) and local state B_c
-        IV<SL> pm;
-        CV<SL> dm, Bm = cv_zero<SL>();
+    // ---- 3. publish the chunk operator for the frontier wave, take carry_c.
+    // Slot reuse: the operator of chunk ch + 2W goes where that of ch went.
+    // This wave writes it only after carry_{ch+W} arrived, which the frontier
+    // publishes after it read operator ch.  Carry slot ch % (W + 1) is
+    // rewritten with carry_{ch+W+1} only after the frontier took operator
+    // ch + W from this same wave, which this wave publishes after its read
+    // of carry_ch below (one wave's LDS accesses complete in order).
+    {
+        const int slot = ch % (2 * W);
+        wave_sync();
+        if (act) {
+#pragma unroll
+            for (int r = 0; r < SL; ++r) {
+                s.agg[slot * N + lane * SL + r] = make_float4(Bm.v[r].x, Bm.v[r].y, dm.v[r].x, dm.v[r].y);
+                s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
+            }
+        }
+        wave_sync();
+        if (lane == 0) publish_ready(s.aflag + slot, ch);
+    }
+    wait_ready(s.ready, ch + 1, a.status, s.ready, 1 + 2 * W);
+    CV<SL> carry = cv_zero<SL>();
+    if (act) carry = ld_cv<SL>(s.ring + (ch % (W + 1)) * N, lane);
+    if (act && a.saved) st_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane, carry);
+
+    // ---- 4. readout correction with the true carry, then one store per chunk
+#pragma unroll
+    for (int t = 0; t < TAU; ++t) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r)
+            yl[t] += wt[t].v[r].x * carry.v[r].x - wt[t].v[r].y * carry.v[r].y;
+    }
+    const float yv = transpose_sum<TAU>(yl, lane);
+    const int t = lane / (kWave / TAU);
+    if (lane % (kWave / TAU) == 0 && t < q.len)
+        a.y[((size_t)bb * a.L + ch * TAU + t) * a.H + hh] = yv;
+}
+
+// A published chunk operator as the frontier wave holds it.
+template <int SL>
+struct ChunkOp {
+    CV<SL> B, d;
+    IV<SL> p;
+};
+
+template <int N>
+__device__ __forceinline__ ChunkOp<Lay<N>::SL> read_op(const Smem& s, int slot, int lane, bool act) {
+    constexpr int SL = Lay<N>::SL;
+    ChunkOp<SL> o;
+    if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
-            pm.v[r] = lane * SL + r;
-            dm.v[r] = make_float2(1.f, 0.f);
+            const float4 e = s.agg[slot * N + lane * SL + r];
+            o.B.v[r] = make_float2(e.x, e.y);
+            o.d.v[r] = make_float2(e.z, e.w);
+            o.p.v[r] = s.agp[slot * N + lane * SL + r];
         }
+    } else {
+        o.B = cv_zero<SL>();
+        o.d = cv_zero<SL>();
 #pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t);
-            const int M = FB ? readlane_i(q.mv, t) : 0;
-            pd_step<N, G, FB, true>(s, vd, X, lane, act, k, M, Bm, q.D[t], q.b[t]);
-            // (pi, d) <- (pi_t[pi], D_t[pi] * d), D_t staged in vd.zw
-            if (act) {
+        for (int r = 0; r < SL; ++r) o.p.v[r] = 0;
+    }
+    return o;
+}
+
+// The frontier wave: keeps the running state in registers and, chunk by
+// chunk, hands carry_c to the chunk's wave and applies the chunk's published
+// operator: carry_{c+1} = B_c + (Pi_c, Delta_c) carry_c.  Per chunk its
+// critical path is one pipelined batch of LDS accesses: the carry store, the
+// scatter and the read-back, with the next chunk's operator read
+// speculatively in the same batch (LDS accesses of one wave complete in issue
+// order, so operator data read after a flag that shows it published is that
+// operator's; a flag still behind sends the wave to a bounded wait and a
+// re-read).  The wave runs at raised issue priority: it shares its SIMD with
+// chunk waves whose long arithmetic runs would otherwise delay it.
+template <int N, int W, int G, bool FB>
+__device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, int seq) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    constexpr bool kPerm = G == 1 && !FB;
+    const int lane = lane_id();
+    const bool act = lane < LANES;
+    float2* X = s.x + W * N;
+    int* flags = s.ready;
+    const int nflags = 1 + 2 * W;
+    __builtin_amdgcn_s_setprio(3);
+    CV<SL> carry = cv_zero<SL>();
+    if (a.h0 && act) carry = ld_cv<SL>(a.h0 + (size_t)seq * N, lane);
+    wait_ready(s.aflag, 0, a.status, flags, nflags);
+    ChunkOp<SL> op = read_op<N>(s, 0, lane, act);
+    if (!kPerm) {
+        wave_sync();
+        if (act) st_cv<SL>(X, lane, op.B);
+    }
+    for (int c = 0; c < a.C; ++c) {
+        CV<SL> v;
+#pragma unroll
+        for (int r = 0; r < SL; ++r) v.v[r] = cmul(op.d.v[r], carry.v[r]);
+        wave_sync();
+        if (act) st_cv<SL>(s.ring + (c % (W + 1)) * N, lane, carry);
+        if (act) {
+            if constexpr (kPerm) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) X[op.p.v[r]] = v.v[r];
+            } else {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
-                    const int p = pm.v[r];
-                    dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
-                    pm.v[r] = s.dict[k * N + p];
+                    float* dst = reinterpret_cast<float*>(X + op.p.v[r]);
+                    atomicAdd(dst, v.v[r].x);
+                    atomicAdd(dst + 1, v.v[r].y);
                 }
             }
         }
-
-        // ---- 3. hand-off: carry_{c+1} = B_c + (pi_c, d_c) carry_c
-        wait_ready(s.ready, ch, a.status);
-        CV<SL> carry = cv_zero<SL>();
-        if (act) carry = ld_cv<SL>(s.ring + (ch & 1) * N, lane);
-        CV<SL> nxt = carry;
-        pd_scatter_step<N>(X, lane, act, nxt, dm, Bm, pm);
-        if (act) st_cv<SL>(s.ring + ((ch + 1) & 1) * N, lane, nxt);
+        const bool more = c + 1 < a.C;
+        const int nslot = (c + 1) % (2 * W);
+        int seen = 0x7fffffff;
+        ChunkOp<SL> nx;
+        if (more) {
+            seen = __hip_atomic_load(s.aflag + nslot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            issue_fence();
+            nx = read_op<N>(s, nslot, lane, act);
+        }
         wave_sync();
-        if (lane == 0) publish_ready(s.ready, ch + 1);
-        if (act) {
-            if (a.saved) st_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane, carry);
-            if (ch == a.C - 1 && a.hfinal) st_cv<SL>(a.hfinal + (size_t)seq * N, lane, nxt);
+        CV<SL> nxt = cv_zero<SL>();
+        if (act) nxt = ld_cv<SL>(X, lane);
+        wave_sync();
+        if (lane == 0) publish_ready(s.ready, c + 1);
+        if constexpr (kPerm) {
+#pragma unroll
+            for (int r = 0; r < SL; ++r) nxt.v[r] = cadd(nxt.v[r], op.B.v[r]);
         }
+        carry = nxt;
+        if (more) {
+            if (__builtin_amdgcn_readfirstlane(seen) < c + 1) {
+                wait_ready(s.aflag + nslot, c + 1, a.status, flags, nflags);
+                nx = read_op<N>(s, nslot, lane, act);
+            }
+            if (!kPerm) {
+                wave_sync();
+                if (act) st_cv<SL>(X, lane, nx.B);
+            }
+            op = nx;
+        }
+    }
+    __builtin_amdgcn_s_setprio(0);
+    if (act && a.hfinal) st_cv<SL>(a.hfinal + (size_t)seq * N, lane, carry);
+}
 
-        // ---- 4. replay from carry_c with the fused readout
-        CV<SL> h = carry;
-        float yv = 0.f;
-#pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t);
-            const int M = FB ? readlane_i(q.mv, t) : 0;
-            pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, h, q.D[t], q.b[t]);
-            float part = 0.f;
-#pragma unroll
-            for (int r = 0; r < SL; ++r) part += q.c[t].v[r].x * h.v[r].x - q.c[t].v[r].y * h.v[r].y;
-            const float tot = readlane_f(wave_sum_last(part), kWave - 1);
-            yv = lane == t ? tot : yv;
+// Wave wv owns chunks wv, wv+W, ...; with PREFETCH the loads of its next chunk
+// are in flight while it computes the current one (two register buffers).
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH>
+__device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+    constexpr int LANES = Lay<N>::LANES;
+    const int wv = wave_id(), lane = lane_id();
+    const bool act = lane < LANES;
+    if (wv == W) {
+        fwd_frontier<N, W, G, FB>(a, s, seq);
+        return;
+    }
+    bool bad = false;
+    if constexpr (PREFETCH) {
+        Chunk<N, TAU> qa, qb;
+        issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, wv, lane, act, qa);
+        for (int ch = wv; ch < a.C; ch += 2 * W) {
+            issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch + W, lane, act, qb);
+            issue_fence();
+            fwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, ch, qa, bad);
+            if (ch + W >= a.C) break;
+            issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch + 2 * W, lane, act, qa);
+            issue_fence();
+            fwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, ch + W, qb, bad);
         }
-        if (lane < q.len) a.y[((size_t)bb * a.L + ch * TAU + lane) * a.H + hh] = yv;
+    } else {
+        for (int ch = wv; ch < a.C; ch += W) {
+            Chunk<N, TAU> q;
+            issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch, lane, act, q);
+            fwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, ch, q, bad);
+        }
     }
     if (bad) report_index_error(a.status);
 }
 
 template <int N, int TAU, int W>
-__global__ __launch_bounds__(W * 64) void k_fwd_fused(FusedArgs a) {
-    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+__global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     extern __shared__ __align__(16) unsigned char lds[];
     const Smem s = carve_smem(lds, a.lds);
-    const int wv = threadIdx.x >> 6, lane = lane_id();
-    const bool act = lane < LANES;
     const int seq = xcd_seq(a.B * a.H);
     const int bb = seq / a.H, hh = seq - bb * a.H;
 
     stage_tables<N, W>(a, s, hh);
-    if (wv == 0) {
-        CV<SL> h0 = cv_zero<SL>();
-        if (a.h0 && act) h0 = ld_cv<SL>(a.h0 + (size_t)seq * N, lane);
-        if (act) st_cv<SL>(s.ring, lane, h0);
-        if (lane == 0) *s.ready = 0;
-    }
+    if (threadIdx.x == 0) *s.ready = 0;
+    for (int i = threadIdx.x; i < 2 * W; i += blockDim.x) s.aflag[i] = -1;
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
-    if (fb) fwd_body<N, TAU, W, 7, true>(a, s, seq, bb, hh);
-    else if (G == 1) fwd_body<N, TAU, W, 1, false>(a, s, seq, bb, hh);
-    else if (G == 3) fwd_body<N, TAU, W, 3, false>(a, s, seq, bb, hh);
-    else fwd_body<N, TAU, W, 7, false>(a, s, seq, bb, hh);
+    constexpr bool PF = fused_prefetch(N, TAU);
+    if (fb) fwd_body<N, TAU, W, 7, true, PF>(a, s, seq, bb, hh);
+    else if (G == 1) fwd_body<N, TAU, W, 1, false, PF>(a, s, seq, bb, hh);
+    else if (G == 3) fwd_body<N, TAU, W, 3, false, PF>(a, s, seq, bb, hh);
+    else fwd_body<N, TAU, W, 7, false, PF>(a, s, seq, bb, hh);
 }
 
 // ================================================================== backward
 template <int N, int TAU, int W, int G, bool FB>
 __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     float4* vd = s.vd + wv * (N + 1);
     float2* X = s.x + wv * N;
@@ -475,23 +737,35 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int 
                 for (int i = 0; i < SL; ++i) {
                     const float4 e = vd[pt.v[i]];
                     pa.v[i] = PA[pt.v[i]];
-                    da.v[i] = cmul(make_float2(e.z, e.w), q.D[t].v[i]);
-                    g.v[i] = cmulc(q.D[t].v[i], make_float2(e.x, e.y));
+                    da.v[i] = cmul(make_float2(e.z, e.w), Dt(q, t).v[i]);
+                    g.v[i] = cmulc(Dt(q, t).v[i], make_float2(e.x, e.y));
                 }
             }
         }
 
         // ---- start the loads the recompute needs while the hand-off waits
+        {
+            const uint32_t rstride = (uint32_t)a.H * N * 8;
+            const __amdgpu_buffer_rsrc_t rb = row_block(a.b + base, (uint32_t)(q.len - 1) * rstride + N * 8);
+            const __amdgpu_buffer_rsrc_t rnull = row_block(a.b, 0);
 #pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const size_t off = base + (size_t)min(t, q.len - 1) * stride;
-            q.b[t] = act ? ld_cv<SL>(a.b + off, lane) : cv_zero<SL>();
+            for (int t = 0; t < TAU; ++t)
+                q.b[t] = act ? ld_row<SL>(t < q.len ? rb : rnull, (uint32_t)lane * SL * 8, (uint32_t)t * rstride)
+                             : cv_zero<SL>();
         }
         CV<SL> hs = cv_zero<SL>();
         if (act) hs = ld_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane);
 
         // ---- hand-off: U_{c-1} = gamma_c + Phi_c^H U_c (a gather from the ring)
-        wait_ready(s.ready, r, a.status);
+#pragma unroll
+        for (int i = 0; i < SL; ++i) {
+            materialize(pa.v[i]);
+            materialize(da.v[i].x);
+            materialize(da.v[i].y);
+            materialize(g.v[i].x);
+            materialize(g.v[i].y);
+        }
+        wait_ready(s.ready, r, a.status, s.ready, 1);
         CV<SL> U = cv_zero<SL>(), Up;
         if (act) {
             const float2* ring = s.ring + (r & 1) * N;
@@ -505,18 +779,13 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int 
         if (ch == 0 && a.dh0 && act) st_cv<SL>(a.dh0 + (size_t)seq * N, lane, Up);
 
         // ---- recompute the chunk's states from the saved entering state
-        if (q.len < TAU) {
-#pragma unroll
-            for (int t = 0; t < TAU; ++t)
-                if (t >= q.len) q.b[t] = cv_zero<SL>();
-        }
         CV<SL> Hs[TAU + 1];
         Hs[0] = hs;
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
             const int k = readlane_i(q.kv, t);
             const int M = FB ? readlane_i(q.mv, t) : 0;
-            pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, hs, q.D[t], q.b[t]);
+            pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
             Hs[t + 1] = hs;
         }
 
@@ -551,7 +820,7 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int 
                 for (int i = 0; i < SL; ++i) {
                     const float2 gp = reinterpret_cast<const float2*>(vd)[2 * pt.v[i]];
                     dDt.v[i] = cmulc(Hs[t].v[i], gp);
-                    g.v[i] = cmulc(q.D[t].v[i], gp);
+                    g.v[i] = cmulc(Dt(q, t).v[i], gp);
                 }
                 if (t < q.len) st_cv<SL>(a.dD + off, lane, dDt);
             }
@@ -565,7 +834,7 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     extern __shared__ __align__(16) unsigned char lds[];
     const Smem s = carve_smem(lds, a.lds);
-    const int wv = threadIdx.x >> 6, lane = lane_id();
+    const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     const int seq = xcd_seq(a.B * a.H);
     const int bb = seq / a.H, hh = seq - bb * a.H;
@@ -592,7 +861,7 @@ hipError_t fwd_launch(const FusedArgs& a, hipStream_t st) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(W * 64), a.lds.total, st, a);
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3((W + 1) * 64), a.lds.total, st, a);
     return hipGetLastError();
 }
 
@@ -617,14 +886,22 @@ hipError_t prep_launch(const PrepArgs& p, hipStream_t st) {
 template <int N, bool FWD>
 hipError_t dispatch_tau(const FusedArgs& a, hipStream_t st) {
     constexpr int SL = Lay<N>::SL;
-    constexpr int W = kFusedWaves;
     switch (a.tau) {
-        case 4: return FWD ? fwd_launch<N, 4, W>(a, st) : bwd_launch<N, 4, W>(a, st);
+        case 4: {
+            constexpr int W = fused_waves(N, 4);
+            return FWD ? fwd_launch<N, 4, W>(a, st) : bwd_launch<N, 4, W>(a, st);
+        }
         case 8:
-            if constexpr (8 * SL <= 16) return FWD ? fwd_launch<N, 8, W>(a, st) : bwd_launch<N, 8, W>(a, st);
+            if constexpr (8 * SL <= 16) {
+                constexpr int W = fused_waves(N, 8);
+                return FWD ? fwd_launch<N, 8, W>(a, st) : bwd_launch<N, 8, W>(a, st);
+            }
             break;
         case 16:
-            if constexpr (16 * SL <= 16) return FWD ? fwd_launch<N, 16, W>(a, st) : bwd_launch<N, 16, W>(a, st);
+            if constexpr (16 * SL <= 16) {
+                constexpr int W = fused_waves(N, 16);
+                return FWD ? fwd_launch<N, 16, W>(a, st) : bwd_launch<N, 16, W>(a, st);
+            }
             break;
         default: break;
     }

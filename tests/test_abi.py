@@ -37,11 +37,13 @@ def test_exports_every_declared_function(lib):
 
 def test_chunk_and_workspace_queries(lib):
     d = pdssm.desc(16, 2048, 16, 64, 16)
-    assert pdssm.chunk_len(d) == 16
-    assert pdssm.num_chunks(d) == 128
-    d = pdssm.desc(8, 18000, 8, 128, 32)
     assert pdssm.chunk_len(d) == 8
-    assert pdssm.num_chunks(d) == 2250
+    assert pdssm.num_chunks(d) == 256
+    assert pdssm.num_chunks(pdssm.desc(16, 2048, 16, 64, 16, chunk=16)) == 128
+    d = pdssm.desc(8, 18000, 8, 128, 32)
+    assert pdssm.chunk_len(d) == 4
+    assert pdssm.num_chunks(d) == 4500
+    assert pdssm.num_chunks(pdssm.desc(8, 18000, 8, 128, 32, chunk=8)) == 2250
     assert pdssm.num_chunks(pdssm.desc(8, 18000, 8, 128, 32, chunk=16)) == pdssm.ERR_UNSUPPORTED
     assert pdssm.chunk_len(pdssm.desc(1, 10, 1, 256, 4)) == 4
     for op in (pdssm.OP_FWD, pdssm.OP_BWD):

@@ -40,6 +40,12 @@ def run_gpu(inp, chunk=0, bwd=True):
     return out
 
 
+def eff_chunk(inp, chunk=0):
+    B, L, H = inp["idx"].shape
+    _, K, N = inp["pi"].shape
+    return pdssm.chunk_len(pdssm.desc(B, L, H, N, K, chunk))
+
+
 def check_all(inp, got, chunk_eff, bwd=True):
     ry, rhf, rsaved = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"],
                                  h0=inp.get("h0"), chunk=chunk_eff)
@@ -78,14 +84,14 @@ def test_map_kinds_default_chunk(pi_kind):
     inp = make_inputs(B=3, L=200, H=2, N=64, K=7, seed=7, pi_kind=pi_kind, with_h0=True,
                       with_dhf=True)
     got = run_gpu(inp)
-    check_all(inp, got, 16)
+    check_all(inp, got, eff_chunk(inp))
 
 
 def test_single_dictionary_entry_and_k256():
     for K in (1, 256):
         inp = make_inputs(B=1, L=70, H=2, N=32, K=K, seed=K)
         got = run_gpu(inp)
-        check_all(inp, got, 16)
+        check_all(inp, got, eff_chunk(inp))
 
 
 @pytest.mark.parametrize("N", [64, 128])
@@ -95,7 +101,7 @@ def test_all_maps_collapse_to_one_row(N):
     inp = make_inputs(B=1, L=250, H=1, N=N, K=3, seed=3)
     inp["pi"][:] = 0
     got = run_gpu(inp)
-    check_all(inp, got, 16 // max(1, N // 64))
+    check_all(inp, got, eff_chunk(inp))
 
 
 def test_mixed_degenerate_and_regular_entries():
@@ -105,7 +111,7 @@ def test_mixed_degenerate_and_regular_entries():
     inp["pi"][0, 1, :9] = 5
     inp["pi"][1, 4, :] = 63
     got = run_gpu(inp)
-    check_all(inp, got, 16)
+    check_all(inp, got, eff_chunk(inp))
 
 
 @pytest.mark.parametrize("N,K", [(128, 128), (256, 64)])
@@ -114,7 +120,7 @@ def test_large_dictionary_chunked_path(N, K):
     kernels run instead, with the same saved-state layout."""
     inp = make_inputs(B=2, L=90, H=2, N=N, K=K, seed=N + K, with_h0=True, with_dhf=True)
     got = run_gpu(inp)
-    check_all(inp, got, 16 // max(1, N // 64))
+    check_all(inp, got, eff_chunk(inp))
 
 
 # ------------------------------------------------------------------ automaton: exact
