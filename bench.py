@@ -2,16 +2,20 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2]
 
-One step = one forward scan (pdssm_scan_fwd: y, h_final, saved chunk states)
-plus one backward scan (pdssm_scan_bwd: dD, db, dc, dh0) over one batch of
-seeded synthetic inputs already resident in HBM.  Prints ONE JSON line.
+One step = dictionary preparation (pdssm_prepare), one forward scan
+(pdssm_scan_fwd: y, h_final, saved chunk states) and one backward scan
+(pdssm_scan_bwd: dD, db, dc, dh0) over one batch of seeded synthetic inputs
+already resident in HBM.  A 512 MiB buffer is rewritten between steps (not
+timed) so that no input of a step is still cached.  Prints ONE JSON line.
 
-value = state updates (B*L*H*N) per second of the whole fwd+bwd step.
-roofline = the dominant call's algorithmic bytes (every input read once,
+value = state updates (B*L*H*N) per second of the whole step.
+roofline = the dominant kernel's algorithmic bytes (every input read once,
 every output written once) over its average duration, measured with HIP
-events on the stream the kernels are launched on, against the 8 TB/s HBM peak.
+events on the stream the kernels are launched on, against the 8 TB/s HBM
+peak; traffic = the HBM bytes per launch that rocprofv3 counters measured for
+the same kernel source (profiles/), else null.
 cpu_baseline = the float64 oracle timed on a bounded sample of the same
-workload on this host.
+workload on this host's cores.
 """
 import argparse
 import json
@@ -25,6 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+FLUSH_BYTES = 512 << 20
 METRIC = "PD-scan state-updates/s (B*L*H*N) fwd and fwd+bwd; achieved HBM GB/s vs peak"
 
 
@@ -41,26 +46,53 @@ def alg_bytes(w, C, op):
     return steps * 8 + 3 * su * 8 + dict_b + B * H * C * N * 8 + 3 * su * 8 + B * H * N * 8
 
 
-def cpu_baseline(w, inp, target_s=12.0):
-    """Time the oracle (fwd + bwd, float64, one thread) on whole sequences of
-    the workload until about target_s seconds of CPU work are done."""
+def cpu_baseline(w, inp, target_s=12.0, max_threads=16, sample_seqs=32):
+    """Time the float64 oracle (fwd + bwd, one whole sequence per task) on
+    this host: a fixed sample of the workload's sequences, cycled over a pool
+    of threads (the oracle's C loops run without the GIL) until about
+    target_s seconds of wall time have passed."""
+    from concurrent.futures import ThreadPoolExecutor
+
     from oracle import oracle_bwd, oracle_fwd
     from paper_2605_19150_amd.inputs import sub_sequence
-    done_su, t_used, nseq = 0, 0.0, 0
     seqs = [(bb, hh) for bb in range(w.B) for hh in range(w.H)]
-    for bb, hh in seqs:
+    step = max(1, len(seqs) // sample_seqs)
+    picked = seqs[::step][:sample_seqs]
+    subs = []
+    for bb, hh in picked:
         sub = sub_sequence(inp, bb, hh)
-        t0 = time.perf_counter()
+        for k in ("D", "b", "c"):
+            sub[k] = sub[k].astype(np.complex128)
+        sub["dy"] = sub["dy"].astype(np.float64)
+        subs.append(sub)
+    threads = max(1, min(max_threads, os.cpu_count() or 1))
+
+    def one(sub):
         oracle_fwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"])
         oracle_bwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"], sub["dy"])
-        t_used += time.perf_counter() - t0
-        done_su += w.L * w.N
-        nseq += 1
-        if t_used >= target_s:
-            break
-    return {"value": done_su / t_used, "unit": "state-updates/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d sequences (whole L=%d each), fwd+bwd float64, %.1f s"
-                      % (nseq, len(seqs), w.L, t_used)}
+        return w.L * w.N
+
+    done_su, rounds = 0, 0
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=threads) as pool:
+        while True:
+            done_su += sum(pool.map(one, subs))
+            rounds += 1
+            if time.perf_counter() - t0 >= target_s:
+                break
+    wall = time.perf_counter() - t0
+    return {"value": done_su / wall, "unit": "state-updates/s", "cores": threads, "kind": "oracle",
+            "sample": "fwd+bwd float64 oracle on %d of %d whole sequences (L=%d, N=%d), "
+                      "cycled %d times on %d threads, %.1f s wall"
+                      % (len(subs), len(seqs), w.L, w.N, rounds, threads, wall)}
+
+
+def traffic_from_profiles(kernel, workload_name):
+    """HBM bytes per launch of `kernel` on this workload from the committed
+    counter summary, or None when there is none or the kernel sources have
+    changed since the counters were taken."""
+    from paper_2605_19150_amd.profiling import read_traffic_summary
+    return read_traffic_summary(os.path.join(ROOT, "profiles"), kernel, workload_name)
 
 
 def main():
@@ -110,44 +142,54 @@ def main():
     T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
     s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K)
     stream = torch.cuda.current_stream()
+    # Written between timed steps so that no input is still in L2 / MALL.
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
 
     def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
+        rec = (lambda i: ev[i].record(stream)) if ev is not None else (lambda i: None)
+        rec(0)
+        s.prepare(T["pi"])
+        rec(1)
         if args.only in ("fwd", "both"):
             s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
-        if ev is not None:
-            ev[1].record(stream)
+        rec(2)
         if args.only in ("bwd", "both"):
             s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
-        if ev is not None:
-            ev[2].record(stream)
+        rec(3)
 
     if args.only == "bwd":
+        s.prepare(T["pi"])
         s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
     for _ in range(args.warmup):
+        flush.fill_(1.0)
         step()
     torch.cuda.synchronize()
     s.check_status()
     print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        flush.fill_(float(i))
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    ms_step = float(np.mean([e[0].elapsed_time(e[2]) for e in evs]))
+    prep_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    fwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    ms_step = float(np.mean([e[0].elapsed_time(e[3]) for e in evs]))
     s.check_status()
 
     su = w.state_updates
     fwd_b, bwd_b = alg_bytes(w, s.C, "fwd"), alg_bytes(w, s.C, "bwd")
+    fused = s.fused
+    kern = {"fwd": "k_fwd_fused" if fused else "k_fwd_*(chunked)",
+            "bwd": "k_bwd_fused" if fused else "k_bwd_*(chunked)"}
     dom = "bwd" if (bwd_ms >= fwd_ms and args.only != "fwd") else "fwd"
     dom_ms, dom_b = (bwd_ms, bwd_b) if dom == "bwd" else (fwd_ms, fwd_b)
     achieved = dom_b / (dom_ms * 1e-3) / 1e9
+    traffic = traffic_from_profiles(kern[dom], w.name) if fused else None
     out = {
         "metric": METRIC,
         "value": su / (ms_step * 1e-3),
@@ -162,15 +204,18 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded, shapes and distributions of the named workload)",
         "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
-                   "chunk": s.chunk, "step": "fwd+bwd" if args.only == "both" else args.only,
+                   "chunk": s.chunk, "step": "prepare+fwd+bwd" if args.only == "both" else args.only,
                    "global_batch": w.B, "seq_len": w.L, "parallelism": "single-gpu"},
-        "roofline": {"bound": "hbm", "kernel": "pdssm_scan_%s" % dom,
+        "roofline": {"bound": "hbm", "kernel": kern[dom],
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None},
-        "fwd": {"ms": fwd_ms, "state_updates_per_s": su / (fwd_ms * 1e-3),
-                "alg_bytes": fwd_b, "alg_GBps": fwd_b / (fwd_ms * 1e-3) / 1e9},
-        "bwd": {"ms": bwd_ms, "state_updates_per_s": su / (bwd_ms * 1e-3),
-                "alg_bytes": bwd_b, "alg_GBps": bwd_b / (bwd_ms * 1e-3) / 1e9},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
+        "prepare": {"ms": prep_ms},
+        "fwd": {"kernel": kern["fwd"], "ms": fwd_ms, "state_updates_per_s": su / (fwd_ms * 1e-3),
+                "alg_bytes": fwd_b, "alg_GBps": fwd_b / (fwd_ms * 1e-3) / 1e9,
+                "frac": fwd_b / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        "bwd": {"kernel": kern["bwd"], "ms": bwd_ms, "state_updates_per_s": su / (bwd_ms * 1e-3),
+                "alg_bytes": bwd_b, "alg_GBps": bwd_b / (bwd_ms * 1e-3) / 1e9,
+                "frac": bwd_b / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
         "fwd_bwd_alg_GBps": (fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9,
         "wall_s_timed": wall,
         "device": torch.cuda.get_device_name(dev),

@@ -50,8 +50,12 @@
  *   - Complex gradients follow dX = dl/dRe(X) + i*dl/dIm(X) (torch's
  *     convention) for the loss l = sum_t dy_t*y_t + Re(sum conj(dh_final)*h_L).
  *   - Supported sizes: N in {8, 16, 32, 64, 128, 256}; 1 <= K <= 256;
- *     B, L, H >= 1 with B*L*H*N < 2^31; chunk in {16, 32, 64} or 0 (default,
- *     32) for scan_fwd / scan_bwd; any chunk >= 1 for pdssm_compose_chunks.
+ *     B, L, H >= 1 with B*L*H*N < 2^31.  For scan_fwd / scan_bwd the chunk is
+ *     4, 8 or 16 steps with chunk * max(1, N/64) <= 16, or 0 for the default
+ *     (8 for N <= 64, 4 for N >= 128); pdssm_compose_chunks takes any chunk
+ *     >= 1 (0 = 32).  One head's dictionary tables, (K+1)*N*9 bytes plus the
+ *     per-wave buffers, are staged in the 160 KiB LDS of a workgroup; larger
+ *     dictionaries run slower multi-pass kernels with the same results.
  *   - Calls on different streams may run concurrently if their outputs and
  *     workspaces do not overlap; the library keeps no mutable global state.
  */
@@ -74,12 +78,17 @@ typedef struct pdssm_c64 {
 typedef struct pdssm_desc {
     int32_t B, L, H, N, K; /* batch, steps, heads, state size, dictionary size */
     int32_t chunk;         /* steps per chunk; 0 = default; fwd and bwd must agree */
-    uint32_t flags;        /* reserved, must be 0 */
+    uint32_t flags;        /* 0 or PDSSM_FLAG_PREPARED */
 } pdssm_desc;
+
+/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd: the dictionary tables in
+ * ws were built by pdssm_prepare for this desc and the current contents of pi;
+ * the scan reuses them instead of rebuilding them. */
+#define PDSSM_FLAG_PREPARED 1u
 
 typedef enum pdssm_status {
     PDSSM_OK = 0,
-    PDSSM_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, overlap, flags != 0 */
+    PDSSM_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, overlap, unknown flags */
     PDSSM_ERR_UNSUPPORTED = -2, /* N, K or chunk outside the supported set */
     PDSSM_ERR_WORKSPACE = -3,   /* ws NULL or smaller than pdssm_workspace_size */
     PDSSM_ERR_HIP = -4,         /* a HIP launch reported an error */
@@ -105,8 +114,32 @@ int pdssm_num_chunks(const pdssm_desc* desc);
  * invalid. */
 size_t pdssm_workspace_size(const pdssm_desc* desc, int op);
 
+/* 1 if the scans of desc run the single-read kernels (one head's dictionary
+ * tables fit in LDS), 0 if they run the multi-pass kernels, or a negative
+ * status for an invalid desc. */
+int pdssm_uses_fused(const pdssm_desc* desc);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* pdssm_status_string(int status);
+
+/*
+ * Dictionary preparation (App. E.2.1: the per-head transition dictionary is
+ * shared by every step of a call, so its per-step tables are built once).
+ * Builds, in ws, a byte copy of every map pi[h,k,:], per destination row the
+ * list of its sources (the gather form of the column-one-hot map) and each
+ * map's largest in-degree.  pdssm_scan_fwd and pdssm_scan_bwd always do this
+ * themselves first, unless desc->flags has PDSSM_FLAG_PREPARED: then they use
+ * the tables already in ws, which must come from pdssm_prepare with the same
+ * desc (flags aside), the same ws and the current contents of pi, enqueued
+ * before them on the same stream or ordered before them by the caller.
+ * An entry of pi outside [0,N) is reported through *dev_status here.
+ * ws: at least pdssm_workspace_size(desc, PDSSM_OP_FWD) bytes (the forward and
+ * backward sizes are equal), 256-byte aligned, not overlapping pi.  When the
+ * scans of desc run the chunked kernels (dictionaries too large for LDS) no
+ * tables are needed and the call enqueues nothing.
+ */
+int pdssm_prepare(const pdssm_desc* desc, const int32_t* pi, void* ws, size_t ws_bytes,
+                  int* dev_status, void* stream);
 
 /*
  * Forward scan (App. E.1 Algorithm 1 / App. E.2 recurrence, readout of

@@ -33,7 +33,7 @@ bool scan_chunk_ok(int N, int tau) {
 // Dimension checks shared by every op.  Returns PDSSM_OK or a status.
 int check_dims(const pdssm_desc* d) {
     if (!d) return PDSSM_ERR_INVALID_ARG;
-    if (d->flags != 0) return PDSSM_ERR_INVALID_ARG;
+    if ((d->flags & ~PDSSM_FLAG_PREPARED) != 0) return PDSSM_ERR_INVALID_ARG;
     if (d->B < 1 || d->L < 1 || d->H < 1 || d->N < 1 || d->K < 1 || d->chunk < 0)
         return PDSSM_ERR_INVALID_ARG;
     if (!n_supported(d->N) || d->K > 256) return PDSSM_ERR_UNSUPPORTED;
@@ -121,9 +121,8 @@ void carve_chunked(ScanArgs& a, void* ws, const Sizes& s) {
     a.U = reinterpret_cast<float2*>(p);  // fwd: carry when saved == NULL
 }
 
-// Builds the dictionary tables into ws and fills the fused args.
-hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* pi, void* ws,
-                      const Sizes& s, int* status, hipStream_t st) {
+// Dictionary tables of the fused kernels at the start of ws.
+pdssm::PrepArgs carve_tables(const pdssm_desc* d, const int32_t* pi, void* ws, const Sizes& s, int* status) {
     char* p = static_cast<char*>(ws);
     pdssm::PrepArgs pa;
     pa.H = d->H;
@@ -136,10 +135,19 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     p += align_up(s.dictN * 8);
     pa.mtab = reinterpret_cast<uint8_t*>(p);
     pa.status = status;
+    return pa;
+}
+
+// Points the fused args at the tables in ws and builds them there unless the
+// caller prepared them (PDSSM_FLAG_PREPARED).
+hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* pi, void* ws,
+                      const Sizes& s, int* status, hipStream_t st) {
+    const pdssm::PrepArgs pa = carve_tables(d, pi, ws, s, status);
     f.dict = pa.dict;
     f.rec = pa.rec;
     f.mtab = pa.mtab;
     f.lds = pdssm::fused_lds_layout(d->N, d->K, pdssm::fused_waves(d->N, f.tau));
+    if (d->flags & PDSSM_FLAG_PREPARED) return hipSuccess;
     return pdssm::launch_prep(pa, st);
 }
 
@@ -215,6 +223,27 @@ const char* pdssm_status_string(int st) {
         case PDSSM_ERR_INDEX: return "PDSSM_ERR_INDEX: idx or pi entry out of range";
         default: return "unknown pdssm status";
     }
+}
+
+int pdssm_uses_fused(const pdssm_desc* d) {
+    const int tau = scan_chunk(d);
+    if (tau < 0) return tau;
+    return use_fused(d) ? 1 : 0;
+}
+
+int pdssm_prepare(const pdssm_desc* d, const int32_t* pi, void* ws, size_t ws_bytes, int* dev_status,
+                  void* stream) {
+    int tau = scan_chunk(d);
+    if (tau < 0) return tau;
+    if (!pi || misaligned(pi)) return PDSSM_ERR_INVALID_ARG;
+    const Sizes s = sizes_of(d, (d->L + tau - 1) / tau);
+    const size_t need = ws_bytes_for(s, d);
+    if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
+        return PDSSM_ERR_WORKSPACE;
+    if (overlap({ws, need}, {pi, (size_t)d->H * d->K * d->N * 4})) return PDSSM_ERR_INVALID_ARG;
+    if (!use_fused(d)) return PDSSM_OK;  // the chunked kernels need no tables
+    const hipError_t e = pdssm::launch_prep(carve_tables(d, pi, ws, s, dev_status), static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
 int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,

@@ -20,6 +20,7 @@ _lib = None
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INDEX = 0, -1, -2, -3, -4, -5
 OP_FWD, OP_BWD, OP_COMPOSE = 1, 2, 3
+FLAG_PREPARED = 1
 
 
 class PdssmError(RuntimeError):
@@ -35,7 +36,8 @@ class Desc(ctypes.Structure):
 
 
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
-           "pdssm_status_string", "pdssm_scan_fwd", "pdssm_scan_bwd", "pdssm_compose_chunks")
+           "pdssm_uses_fused", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
+           "pdssm_scan_bwd", "pdssm_compose_chunks")
 
 
 def lib_path():
@@ -57,6 +59,8 @@ def load():
     L.pdssm_num_chunks.argtypes, L.pdssm_num_chunks.restype = [D], I
     L.pdssm_workspace_size.argtypes, L.pdssm_workspace_size.restype = [D, I], Z
     L.pdssm_status_string.argtypes, L.pdssm_status_string.restype = [I], ctypes.c_char_p
+    L.pdssm_uses_fused.argtypes, L.pdssm_uses_fused.restype = [D], I
+    L.pdssm_prepare.argtypes, L.pdssm_prepare.restype = [D, P, P, Z, P, P], I
     L.pdssm_scan_fwd.argtypes = [D] + [P] * 10 + [Z, P, P]
     L.pdssm_scan_fwd.restype = I
     L.pdssm_scan_bwd.argtypes = [D] + [P] * 13 + [Z, P, P]
@@ -133,20 +137,28 @@ def _check_inputs(idx, pi, D, b, c):
 
 
 class Scan:
-    """Pre-allocated outputs and workspaces for one problem size; fwd() and
-    bwd() allocate nothing, so they can be timed in a loop."""
+    """Pre-allocated outputs and one workspace for one problem size; prepare(),
+    fwd() and bwd() allocate nothing, so they can be timed in a loop.
+
+    Without prepare() every scan builds the dictionary tables itself.  After
+    prepare(pi) the scans reuse the tables in the workspace; call prepare()
+    again whenever the contents of pi change."""
 
     def __init__(self, B, L, H, N, K, chunk=0, device="cuda"):
         self.d = desc(B, L, H, N, K, chunk)
+        self.dp = desc(B, L, H, N, K, chunk)
+        self.dp.flags = FLAG_PREPARED
+        self.prepared = False
         self.dims = (B, L, H, N, K)
         self.device = torch.device(device)
         self.C = num_chunks(self.d)
         if self.C < 0:
             raise PdssmError(self.C, "num_chunks")
         self.chunk = chunk_len(self.d)
+        self.fused = load().pdssm_uses_fused(ctypes.byref(self.d)) == 1
         dev = self.device
-        self.ws_fwd = torch.empty(max(workspace_size(self.d, OP_FWD), 1), dtype=torch.uint8, device=dev)
-        self.ws_bwd = torch.empty(max(workspace_size(self.d, OP_BWD), 1), dtype=torch.uint8, device=dev)
+        nws = max(workspace_size(self.d, OP_FWD), workspace_size(self.d, OP_BWD), 1)
+        self.ws = torch.empty(nws, dtype=torch.uint8, device=dev)
         self.y = torch.empty((B, L, H), dtype=torch.float32, device=dev)
         self.h_final = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
         self.saved = torch.empty((B, H, self.C, N), dtype=torch.complex64, device=dev)
@@ -156,20 +168,29 @@ class Scan:
         self.dh0 = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
 
+    def _desc(self):
+        return ctypes.byref(self.dp if self.prepared else self.d)
+
+    def prepare(self, pi, stream=None):
+        st = load().pdssm_prepare(ctypes.byref(self.d), _p(pi), _p(self.ws), self.ws.numel(),
+                                  _p(self.status), _stream(stream))
+        if st != OK:
+            raise PdssmError(st, "pdssm_prepare")
+        self.prepared = True
+
     def fwd(self, idx, pi, D, b, c, h0=None, stream=None):
-        st = load().pdssm_scan_fwd(ctypes.byref(self.d), _p(idx), _p(pi), _p(D), _p(b), _p(c),
+        st = load().pdssm_scan_fwd(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
                                    _p(h0), _p(self.y), _p(self.h_final), _p(self.saved),
-                                   _p(self.ws_fwd), self.ws_fwd.numel(), _p(self.status),
-                                   _stream(stream))
+                                   _p(self.ws), self.ws.numel(), _p(self.status), _stream(stream))
         if st != OK:
             raise PdssmError(st, "pdssm_scan_fwd")
         return self.y, self.h_final, self.saved
 
     def bwd(self, idx, pi, D, b, c, dy, dh_final=None, stream=None):
-        st = load().pdssm_scan_bwd(ctypes.byref(self.d), _p(idx), _p(pi), _p(D), _p(b), _p(c),
+        st = load().pdssm_scan_bwd(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
                                    _p(self.saved), _p(dy), _p(dh_final), _p(self.dD), _p(self.db),
-                                   _p(self.dc), _p(self.dh0), _p(self.ws_bwd),
-                                   self.ws_bwd.numel(), _p(self.status), _stream(stream))
+                                   _p(self.dc), _p(self.dh0), _p(self.ws), self.ws.numel(),
+                                   _p(self.status), _stream(stream))
         if st != OK:
             raise PdssmError(st, "pdssm_scan_bwd")
         return self.dD, self.db, self.dc, self.dh0

@@ -1,0 +1,141 @@
+"""Summaries of rocprofv3 output for profiles/ (text files), and the reader
+bench.py uses to attach counter-measured HBM traffic to its roofline object.
+
+    # per-kernel durations (rocprofv3 --kernel-trace --stats ... -o run --output-format csv)
+    python -m paper_2605_19150_amd.profiling stats DIR --title T --command "CMD" > profiles/X.md
+
+    # HBM bytes per launch from two counter runs of a kernel and two of the
+    # 1 GiB device copy of `bench.py --copy-calibration` (the scale factors)
+    python -m paper_2605_19150_amd.profiling traffic --kernel k_fwd_fused --workload NAME \\
+        --fetch DIR --write DIR --copy-fetch DIR --copy-write DIR --command "..." > profiles/Y.md
+
+A traffic summary records a hash of the library sources; read_traffic_summary
+returns None once the sources differ from the ones the counters were taken on.
+"""
+import argparse
+import collections
+import csv
+import glob
+import hashlib
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+COPY_BYTES = 1 << 30  # bench.py --copy-calibration copies 1 GiB (reads 1 GiB, writes 1 GiB)
+
+
+def source_hash():
+    """Hash of every source file the kernels are built from."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(PKG, "csrc", "*"))) + [os.path.join(ROOT, "include", "pdssm.h")]
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def _rows(d, name):
+    paths = glob.glob(os.path.join(d, "**", name), recursive=True)
+    if not paths:
+        raise FileNotFoundError("no %s under %s" % (name, d))
+    with open(paths[0], newline="") as fh:
+        return list(csv.DictReader(fh))
+
+
+def stats_markdown(d, title, command):
+    rows = _rows(d, "*kernel_stats.csv")
+    out = ["# %s" % title, "", "Command (from the repository root, one MI355X):", "", "    " + command, "",
+           "| kernel | calls | total (us) | average (us) | min (us) | max (us) | % |",
+           "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append("| %s | %s | %.1f | %.2f | %.2f | %.2f | %.1f |" % (
+            r["Name"], r["Calls"], float(r["TotalDurationNs"]) / 1e3, float(r["AverageNs"]) / 1e3,
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    return "\n".join(out) + "\n"
+
+
+def _counter_mean(d, counter, kernel_substr):
+    """Mean per-dispatch value (KiB for FETCH_SIZE / WRITE_SIZE) of a counter
+    over the dispatches whose kernel name contains kernel_substr."""
+    vals = collections.defaultdict(float)
+    for r in _rows(d, "*counter_collection.csv"):
+        if r["Counter_Name"] == counter and kernel_substr in r["Kernel_Name"]:
+            vals[r["Dispatch_Id"]] += float(r["Counter_Value"])
+    if not vals:
+        raise ValueError("no %s samples for %s in %s" % (counter, kernel_substr, d))
+    return sum(vals.values()) / len(vals), len(vals)
+
+
+def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, command):
+    f_kib, nf = _counter_mean(fetch, "FETCH_SIZE", kernel)
+    w_kib, nw = _counter_mean(write, "WRITE_SIZE", kernel)
+    cf_kib, _ = _counter_mean(copy_fetch, "FETCH_SIZE", "copyBuffer")
+    cw_kib, _ = _counter_mean(copy_write, "WRITE_SIZE", "copyBuffer")
+    sf = COPY_BYTES / (cf_kib * 1024.0)
+    sw = COPY_BYTES / (cw_kib * 1024.0)
+    fetch_b = f_kib * 1024.0 * sf
+    write_b = w_kib * 1024.0 * sw
+    lines = [
+        "# HBM traffic per launch: %s, workload %s" % (kernel, workload),
+        "",
+        "kernel: %s" % kernel,
+        "workload: %s" % workload,
+        "source-hash: %s" % source_hash(),
+        "fetch-bytes-per-launch: %.0f" % fetch_b,
+        "write-bytes-per-launch: %.0f" % write_b,
+        "traffic-bytes-per-launch: %.0f" % (fetch_b + write_b),
+        "",
+        "FETCH_SIZE %.1f KiB/dispatch (%d dispatches) x scale %.4f; WRITE_SIZE %.1f KiB/dispatch "
+        "(%d dispatches) x scale %.4f." % (f_kib, nf, sf, w_kib, nw, sw),
+        "Scales: a 1 GiB device copy (bench.py --copy-calibration) reads 1 GiB and writes 1 GiB; "
+        "its counters read FETCH_SIZE %.1f KiB and WRITE_SIZE %.1f KiB per dispatch." % (cf_kib, cw_kib),
+        "",
+        "Commands (from the repository root, one MI355X, one counter per run):",
+        "",
+    ] + ["    " + c for c in command.split(" ;; ")]
+    return "\n".join(lines) + "\n"
+
+
+def read_traffic_summary(profiles_dir, kernel, workload):
+    """traffic-bytes-per-launch of the matching summary in profiles_dir, or
+    None (no summary, or taken on other kernel sources)."""
+    want = source_hash()
+    for path in sorted(glob.glob(os.path.join(profiles_dir, "*.md"))):
+        kv = {}
+        with open(path) as fh:
+            for line in fh:
+                if ": " in line and not line.startswith(("#", " ", "|")):
+                    k, v = line.rstrip("\n").split(": ", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("kernel") == kernel and kv.get("workload") == workload:
+            if kv.get("source-hash") != want:
+                return None
+            return float(kv["traffic-bytes-per-launch"])
+    return None
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("dir")
+    s.add_argument("--title", required=True)
+    s.add_argument("--command", required=True)
+    t = sub.add_parser("traffic")
+    for k in ("kernel", "workload", "fetch", "write", "copy_fetch", "copy_write", "command"):
+        t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    sub.add_parser("hash")
+    a = ap.parse_args(argv)
+    if a.cmd == "stats":
+        sys.stdout.write(stats_markdown(a.dir, a.title, a.command))
+    elif a.cmd == "traffic":
+        sys.stdout.write(traffic_markdown(a.kernel, a.workload, a.fetch, a.write, a.copy_fetch,
+                                          a.copy_write, a.command))
+    else:
+        print(source_hash())
+
+
+if __name__ == "__main__":
+    main()

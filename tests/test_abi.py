@@ -74,10 +74,29 @@ def test_bad_descriptors(lib, kw, code):
         pdssm.workspace_size(d, pdssm.OP_FWD)
 
 
-def test_flags_must_be_zero(lib):
+def test_flags_only_prepared(lib):
     d = pdssm.desc(2, 10, 2, 64, 4)
-    d.flags = 1
+    d.flags = pdssm.FLAG_PREPARED
+    assert pdssm.num_chunks(d) == 2
+    d.flags = 2
     assert pdssm.num_chunks(d) == pdssm.ERR_INVALID_ARG
+
+
+def test_prepare_host_checks(lib):
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    f = FakeBufs()
+    pi = f(2 * 4 * 64 * 4)
+    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_FWD)
+    assert need == lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
+    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+    assert lib.pdssm_prepare(ctypes.byref(d), None, ws, need, None, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_prepare(ctypes.byref(d), pi, None, need, None, None) == pdssm.ERR_WORKSPACE
+    assert lib.pdssm_prepare(ctypes.byref(d), pi, ws, need - 1, None, None) == pdssm.ERR_WORKSPACE
+    assert lib.pdssm_prepare(ctypes.byref(d), pi, ctypes.c_void_p(ws.value + 16), need, None,
+                             None) == pdssm.ERR_WORKSPACE
+    assert lib.pdssm_prepare(ctypes.byref(d), pi, pi, need, None, None) == pdssm.ERR_INVALID_ARG
+    bad = pdssm.desc(2, 40, 2, 48, 4)
+    assert lib.pdssm_prepare(ctypes.byref(bad), pi, ws, need, None, None) == pdssm.ERR_UNSUPPORTED
 
 
 def test_status_strings(lib):

@@ -169,6 +169,35 @@ def test_deterministic():
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
 
 
+@pytest.mark.parametrize("N,K,pi_kind", [(64, 16, "perm"), (64, 16, "uniform"), (128, 64, "uniform"),
+                                         (128, 128, "uniform")])
+def test_prepared_tables_match_per_call_build(N, K, pi_kind):
+    """Scans on tables from pdssm_prepare give the same bits as scans that
+    build them per call; after pi changes, prepare again and the scans follow
+    the new dictionary."""
+    inp = make_inputs(B=2, L=77, H=3, N=N, K=K, seed=N + K, pi_kind=pi_kind, with_h0=True,
+                      with_dhf=True)
+    T = to_dev(inp)
+    ref = run_gpu(inp)
+    s = pdssm.Scan(2, 77, 3, N, K)
+    s.prepare(T["pi"])
+    for _ in range(2):
+        s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=T["h0"])
+        s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"], dh_final=T["dh_final"])
+        s.check_status()
+        for k in ("y", "h_final", "saved", "dD", "db", "dc", "dh0"):
+            np.testing.assert_array_equal(getattr(s, k).cpu().numpy(), ref[k], err_msg=k)
+    inp2 = dict(inp)
+    inp2["pi"] = np.ascontiguousarray(inp["pi"][:, ::-1])
+    T["pi"].copy_(torch.from_numpy(inp2["pi"]))
+    s.prepare(T["pi"])
+    s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=T["h0"])
+    s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"], dh_final=T["dh_final"])
+    s.check_status()
+    got = {k: getattr(s, k).cpu().numpy() for k in ("y", "h_final", "saved", "dD", "db", "dc", "dh0")}
+    check_all(inp2, got, s.chunk)
+
+
 def test_out_of_range_indices_flagged_not_faulting():
     inp = make_inputs(B=1, L=40, H=2, N=64, K=4, seed=9)
     bad = dict(inp)
@@ -218,6 +247,7 @@ def test_workload_full_size_sampled(wi):
     inp = workload(wi)
     s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K)
     T = to_dev(inp)
+    s.prepare(T["pi"])
     s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
     s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
     s.check_status()
