@@ -1,22 +1,28 @@
 // pdssm_fused.hip -- single-read fused PD scan for gfx950.
 //
-// Layout of the work.  One workgroup of W waves owns one (batch, head)
-// sequence.  The sequence is cut into chunks of TAU steps (App. E.1
-// Algorithm 1); wave w takes chunks w, w+W, w+2W, ... .  For each chunk the
-// wave
+// Layout of the work.  One workgroup owns one (batch, head) sequence.  The
+// sequence is cut into chunks of TAU steps (App. E.1 Algorithm 1).
+//
+// Forward: W chunk waves plus one frontier wave.  Chunk wave w takes chunks
+// w, w+W, w+2W, ...; for each chunk it
 //   1. loads the chunk's D, b, c rows (and idx) into registers -- the only
-//      time they are read from HBM;
-//   2. folds the chunk into its PD operator (pi_c, d_c) and local state B_c
-//      (the state the chunk reaches from zero), App. E.3.1 accumulator update;
-//   3. waits for the state entering the chunk from the wave that owns the
-//      previous chunk (an LDS hand-off, no workgroup barrier), passes on
-//      carry_{c+1} = B_c + (pi_c, d_c) carry_c at once, and records carry_c as
-//      the saved chunk state;
-//   4. replays the chunk from carry_c out of its registers and reduces the
-//      readout y_t = Re<c_t, h_t> on the fly; h_t never reaches memory.
-// The backward runs the same schedule in reverse time with the adjoint
-// recurrence (a gather: g_{t-1}[j] = conj(D_t[j]) g_t[pi_t[j]] + readout term),
-// recomputing the chunk's states from its saved entering state.
+//      time they are read from HBM -- while it still computes the previous
+//      chunk (two register buffers);
+//   2. runs the chunk once from a zero state (Algorithm 1 Phase A): the local
+//      state B_c, the chunk's PD operator (Pi, Delta) built by the App. E.3.1
+//      accumulator update, and per step the local readout Re<c_t, x_t^loc>
+//      and the weights w_t[j] = Delta_t[j] c_t[Pi_t(j)] that carry the
+//      entering state to y_t (Phase C in Algorithm 1's form);
+//   3. publishes (B_c, Pi_c, Delta_c) in an LDS slot; the frontier wave, which
+//      keeps the running state in registers, applies
+//      carry_{c+1} = B_c + (Pi_c, Delta_c) carry_c (Phase B) and hands carry_c
+//      back through an LDS ring;
+//   4. finishes y_t = Re<c_t, x_t^loc> + Re sum_j w_t[j] carry_c[j] and
+//      stores carry_c as the chunk's saved state; h_t never reaches memory.
+// Backward: W waves, chunks in reverse order, the adjoint recurrence (a
+// gather: g_{t-1}[j] = conj(D_t[j]) g_t[pi_t[j]] + readout term) folded the
+// same way, the chunk-to-chunk hand-off passed wave to wave, and the chunk's
+// states recomputed from its saved entering state.
 //
 // Scatter as gathers.  The forward step h'[r] = b[r] + sum_{j: pi(j)=r}
 // D[j] h[j] adds up every source that lands on row r.  For each dictionary

@@ -18,6 +18,7 @@ import csv
 import glob
 import hashlib
 import os
+import re
 import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
@@ -25,14 +26,23 @@ ROOT = os.path.dirname(PKG)
 COPY_BYTES = 1 << 30  # bench.py --copy-calibration copies 1 GiB (reads 1 GiB, writes 1 GiB)
 
 
+def _code_only(text):
+    """Source text without comments and blank space, so that documentation
+    edits do not count as kernel changes."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_hash():
-    """Hash of every source file the kernels are built from."""
+    """Hash of the code (comments and layout ignored) of every source file the
+    kernels are built from."""
     h = hashlib.sha256()
     files = sorted(glob.glob(os.path.join(PKG, "csrc", "*"))) + [os.path.join(ROOT, "include", "pdssm.h")]
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 
