@@ -91,9 +91,14 @@ Sizes sizes_of(const pdssm_desc* d, int C) {
 
 // The fused single-read kernels stage one head's dictionary tables in LDS;
 // when they do not fit, the chunked three-pass kernels run instead.
+pdssm::LdsLayout fused_layout(const pdssm_desc* d, int tau, bool fwd) {
+    const int W = fwd ? pdssm::fused_waves(d->N, tau) : pdssm::fused_waves_bwd(d->N, tau);
+    return pdssm::fused_lds_layout(d->N, d->K, W);
+}
+
 bool use_fused(const pdssm_desc* d) {
     const int tau = scan_chunk(d);
-    return pdssm::fused_lds_layout(d->N, d->K, pdssm::fused_waves(d->N, tau)).total <= pdssm::kMaxLds;
+    return fused_layout(d, tau, true).total <= pdssm::kMaxLds && fused_layout(d, tau, false).total <= pdssm::kMaxLds;
 }
 
 // Fused workspace: byte dictionary, row records, per-entry max in-degree.
@@ -141,12 +146,12 @@ pdssm::PrepArgs carve_tables(const pdssm_desc* d, const int32_t* pi, void* ws, c
 // Points the fused args at the tables in ws and builds them there unless the
 // caller prepared them (PDSSM_FLAG_PREPARED).
 hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* pi, void* ws,
-                      const Sizes& s, int* status, hipStream_t st) {
+                      const Sizes& s, int* status, hipStream_t st, bool fwd) {
     const pdssm::PrepArgs pa = carve_tables(d, pi, ws, s, status);
     f.dict = pa.dict;
     f.rec = pa.rec;
     f.mtab = pa.mtab;
-    f.lds = pdssm::fused_lds_layout(d->N, d->K, pdssm::fused_waves(d->N, f.tau));
+    f.lds = fused_layout(d, f.tau, fwd);
     if (d->flags & PDSSM_FLAG_PREPARED) return hipSuccess;
     return pdssm::launch_prep(pa, st);
 }
@@ -279,7 +284,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     if (use_fused(d)) {
         pdssm::FusedArgs f = fused_base(a);
         f.saved = reinterpret_cast<float2*>(saved);
-        e = prep_fused(f, d, pi, ws, s, dev_status, st);
+        e = prep_fused(f, d, pi, ws, s, dev_status, st, true);
         if (e == hipSuccess) e = pdssm::launch_fwd_fused(f, st);
     } else {
         carve_chunked(a, ws, s);
@@ -329,7 +334,7 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     if (use_fused(d)) {
         pdssm::FusedArgs f = fused_base(a);
         f.saved = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
-        e = prep_fused(f, d, pi, ws, s, dev_status, st);
+        e = prep_fused(f, d, pi, ws, s, dev_status, st, false);
         if (e == hipSuccess) e = pdssm::launch_bwd_fused(f, st);
     } else {
         carve_chunked(a, ws, s);

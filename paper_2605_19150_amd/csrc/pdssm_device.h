@@ -123,7 +123,8 @@ __device__ __forceinline__ CV<SL> ld_cv(const float2* __restrict__ row, int lane
 // Raw buffer access to rows of a [.., N] complex tensor: a scalar resource
 // descriptor holds the base of a block of rows, a scalar offset selects the
 // row and one shared 32-bit VGPR holds the lane's byte offset, so a chunk of
-// row loads costs no per-load 64-bit address registers.
+// row loads costs no per-load 64-bit address registers.  Callers keep every
+// row inside the tensor; a load through a zero-size descriptor returns 0.
 constexpr int kBufferDword3 = 0x00020000;  // raw buffer, gfx9 family
 // Cache-policy operand of a load that streams data read exactly once: the
 // nontemporal hint (nt) of gfx94x/gfx950.
@@ -161,6 +162,26 @@ __device__ __forceinline__ void st_cv(float2* __restrict__ row, int lane, const 
 #pragma unroll
         for (int s = 0; s < SL; s += 2)
             *reinterpret_cast<float4*>(p + s) = make_float4(x.v[s].x, x.v[s].y, x.v[s + 1].x, x.v[s + 1].y);
+    }
+}
+
+// st_cv with the nontemporal hint, for output rows written once and never
+// read back by the kernel.  Global stores, not raw buffer stores: a buffer
+// store of more than 8 bytes with a scalar-register offset has shown its data
+// registers overwritten before the store read them on gfx950 (the compiler
+// inserts no wait state for that form).
+template <int SL>
+__device__ __forceinline__ void st_cv_stream(float2* __restrict__ row, int lane, const CV<SL>& x) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    float2* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        __builtin_nontemporal_store(f32x2{x.v[0].x, x.v[0].y}, reinterpret_cast<f32x2*>(p));
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 2)
+            __builtin_nontemporal_store(f32x4{x.v[s].x, x.v[s].y, x.v[s + 1].x, x.v[s + 1].y},
+                                        reinterpret_cast<f32x4*>(p + s));
     }
 }
 

@@ -16,9 +16,13 @@ namespace pdssm {
 #ifndef PDSSM_PF_MAX_ROWS
 #define PDSSM_PF_MAX_ROWS 8
 #endif
+#ifndef PDSSM_BWD_PF_WAVES
+#define PDSSM_BWD_PF_WAVES 8
+#endif
 constexpr int kFusedWaves = 11;
 constexpr bool fused_prefetch(int N, int tau) { return tau * (N > 64 ? N / 64 : 1) <= PDSSM_PF_MAX_ROWS; }
 constexpr int fused_waves(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_PF_WAVES : kFusedWaves; }
+constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_BWD_PF_WAVES : kFusedWaves; }
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {

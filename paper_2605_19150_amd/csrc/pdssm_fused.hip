@@ -63,42 +63,54 @@ struct Sentinel {
 template <int N>
 __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    __shared__ int psh[4][N];
     const int wv = wave_id(), lane = lane_id();
     const int e = blockIdx.x * 4 + wv;
     if (e >= a.H * a.K) return;
     const bool act = lane < LANES;
-    int* P = psh[wv];
     bool bad = false;
+    IV<SL> p;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) p.v[s] = 0;
     if (act) {
-        IV<SL> p = ld_iv<SL>(a.pi + (size_t)e * N, lane);
+        p = ld_iv<SL>(a.pi + (size_t)e * N, lane);
         bad = sanitize_map<N, SL>(p);
-        st_iv<SL>(P, lane, p);
 #pragma unroll
         for (int s = 0; s < SL; ++s) a.dict[(size_t)e * N + lane * SL + s] = (uint8_t)p.v[s];
     }
-    wave_sync();
+    // Every lane walks the sources j = 0..N-1 in ascending order (the map
+    // value of source j is read from the lane that holds it) and keeps the
+    // ones that land on its rows.
+    uint64_t rec[SL];
+    int cnt[SL];
+#pragma unroll
+    for (int s = 0; s < SL; ++s) {
+        rec[s] = 0;
+#pragma unroll
+        for (int m = 0; m < kMaxSrc; ++m) rec[s] |= (uint64_t)Sentinel<N>::kByte << (8 * m);
+        cnt[s] = 0;
+    }
+    for (int jl = 0; jl < LANES; ++jl) {
+#pragma unroll
+        for (int sj = 0; sj < SL; ++sj) {
+            const int j = jl * SL + sj;
+            const int pj = readlane_i(p.v[sj], jl);
+#pragma unroll
+            for (int s = 0; s < SL; ++s) {
+                const bool hit = pj == lane * SL + s;
+                const int c = cnt[s];
+                const int sh = 8 * min(c, kMaxSrc - 1);
+                const uint64_t put = (rec[s] & ~((uint64_t)255 << sh)) | ((uint64_t)j << sh);
+                rec[s] = hit && c < kMaxSrc ? put : rec[s];
+                cnt[s] = c + (hit ? 1 : 0);
+            }
+        }
+    }
     int maxdeg = 0;
     if (act) {
 #pragma unroll
         for (int s = 0; s < SL; ++s) {
-            const int r = lane * SL + s;
-            uint64_t rec = 0;
-#pragma unroll
-            for (int m = 0; m < kMaxSrc; ++m) rec |= (uint64_t)Sentinel<N>::kByte << (8 * m);
-            int cnt = 0;
-            for (int j = 0; j < N; ++j) {
-                if (P[j] == r) {
-                    if (cnt < kMaxSrc) {
-                        rec &= ~((uint64_t)255 << (8 * cnt));
-                        rec |= (uint64_t)j << (8 * cnt);
-                    }
-                    ++cnt;
-                }
-            }
-            rec |= (uint64_t)min(cnt, 255) << 56;
-            a.rec[(size_t)e * N + r] = rec;
-            maxdeg = max(maxdeg, cnt);
+            a.rec[(size_t)e * N + lane * SL + s] = rec[s] | (uint64_t)min(cnt[s], 255) << 56;
+            maxdeg = max(maxdeg, cnt[s]);
         }
     }
     for (int off = 32; off >= 1; off >>= 1) maxdeg = max(maxdeg, __shfl_xor(maxdeg, off));
@@ -692,8 +704,39 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
 }
 
 // ================================================================== backward
+// The backward streams its inputs and its gradient rows (each byte is read
+// or written once): nontemporal loads and stores.
+template <int SL>
+__device__ __forceinline__ void st_out(float2* row, int lane, const CV<SL>& x) {
+    st_cv_stream<SL>(row, lane, x);
+}
+// Per-chunk registers of the backward: the chunk's rows, the saved state
+// entering it and its dy values (lane t holds dy of step t).
+template <int N, int TAU>
+struct BwdChunk {
+    Chunk<N, TAU> q;
+    CV<Lay<N>::SL> hs;
+    float dyv;
+};
+
+// Issues every load of reverse-order chunk r (chunk C-1-r); r >= C issues an
+// empty chunk through the null descriptor, as issue_chunk does.
+template <int N, int TAU>
+__device__ __forceinline__ void issue_bwd(const FusedArgs& a, int seq, int bb, int hh, int r, int lane, bool act,
+                                          BwdChunk<N, TAU>& u) {
+    constexpr int SL = Lay<N>::SL;
+    const int ch = r < a.C ? a.C - 1 - r : a.C;
+    issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch, lane, act, u.q);
+    const int chc = min(ch, a.C - 1);
+    const int s0 = chc * TAU;
+    const int lenc = min(TAU, a.L - s0);
+    u.dyv = a.dy[((size_t)bb * a.L + s0 + min(lane, lenc - 1)) * a.H + hh];
+    u.hs = act ? ld_cv<SL>(a.saved + ((size_t)seq * a.C + chc) * N, lane) : cv_zero<SL>();
+}
+
 template <int N, int TAU, int W, int G, bool FB>
-__device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+__device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, int seq, int bb, int hh, int r,
+                                          BwdChunk<N, TAU>& u, bool& bad) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
@@ -701,135 +744,148 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int 
     float2* X = s.x + wv * N;
     uint8_t* PA = s.pa + wv * N;
     const size_t stride = (size_t)a.H * N;
-    bool bad = false;
+    const int ch = a.C - 1 - r;
+    const int s0 = ch * TAU;
+    const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
+    Chunk<N, TAU>& q = u.q;
+    finish_chunk<N, TAU>(a, s, lane, q, bad);
+    const float dyv = lane < q.len ? u.dyv : 0.f;
 
-    for (int r = wv; r < a.C; r += W) {
-        const int ch = a.C - 1 - r;
-        const int s0 = ch * TAU;
-        const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
-        Chunk<N, TAU> q;
-        load_chunk<N, TAU, false, true>(a, s, bb, hh, ch, lane, act, q, bad);
-        float dyv = 0.f;
-        if (lane < q.len) dyv = a.dy[((size_t)bb * a.L + s0 + lane) * a.H + hh];
-
-        // ---- local adjoint from zero and the chunk operator, reverse time:
-        // Phi <- Phi A_t: pa(j) <- pa[pi_t(j)], da(j) <- da[pi_t(j)] D_t(j)
-        CV<SL> g = cv_zero<SL>(), da;
-        IV<SL> pa;
+    // ---- local adjoint from zero and the chunk operator, reverse time:
+    // Phi <- Phi A_t: pa(j) <- pa[pi_t(j)], da(j) <- da[pi_t(j)] D_t(j)
+    CV<SL> g = cv_zero<SL>(), da;
+    IV<SL> pa;
 #pragma unroll
-        for (int i = 0; i < SL; ++i) {
-            pa.v[i] = lane * SL + i;
-            da.v[i] = make_float2(1.f, 0.f);
-        }
+    for (int i = 0; i < SL; ++i) {
+        pa.v[i] = lane * SL + i;
+        da.v[i] = make_float2(1.f, 0.f);
+    }
 #pragma unroll
-        for (int t = TAU - 1; t >= 0; --t) {
-            const int k = readlane_i(q.kv, t);
-            const float dyt = readlane_f(dyv, t);
-            IV<SL> pt;
-            wave_sync();
-            if (act) {
-#pragma unroll
-                for (int i = 0; i < SL; ++i) {
-                    pt.v[i] = s.dict[k * N + lane * SL + i];
-                    g.v[i].x += dyt * q.c[t].v[i].x;
-                    g.v[i].y -= dyt * q.c[t].v[i].y;
-                    vd[lane * SL + i] = make_float4(g.v[i].x, g.v[i].y, da.v[i].x, da.v[i].y);
-                    PA[lane * SL + i] = (uint8_t)pa.v[i];
-                }
-            }
-            wave_sync();
-            if (act) {
-#pragma unroll
-                for (int i = 0; i < SL; ++i) {
-                    const float4 e = vd[pt.v[i]];
-                    pa.v[i] = PA[pt.v[i]];
-                    da.v[i] = cmul(make_float2(e.z, e.w), Dt(q, t).v[i]);
-                    g.v[i] = cmulc(Dt(q, t).v[i], make_float2(e.x, e.y));
-                }
-            }
-        }
-
-        // ---- start the loads the recompute needs while the hand-off waits
-        {
-            const uint32_t rstride = (uint32_t)a.H * N * 8;
-            const __amdgpu_buffer_rsrc_t rb = row_block(a.b + base, (uint32_t)(q.len - 1) * rstride + N * 8);
-            const __amdgpu_buffer_rsrc_t rnull = row_block(a.b, 0);
-#pragma unroll
-            for (int t = 0; t < TAU; ++t)
-                q.b[t] = act ? ld_row<SL>(t < q.len ? rb : rnull, (uint32_t)lane * SL * 8, (uint32_t)t * rstride)
-                             : cv_zero<SL>();
-        }
-        CV<SL> hs = cv_zero<SL>();
-        if (act) hs = ld_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane);
-
-        // ---- hand-off: U_{c-1} = gamma_c + Phi_c^H U_c (a gather from the ring)
-#pragma unroll
-        for (int i = 0; i < SL; ++i) {
-            materialize(pa.v[i]);
-            materialize(da.v[i].x);
-            materialize(da.v[i].y);
-            materialize(g.v[i].x);
-            materialize(g.v[i].y);
-        }
-        wait_ready(s.ready, r, a.status, s.ready, 1);
-        CV<SL> U = cv_zero<SL>(), Up;
+    for (int t = TAU - 1; t >= 0; --t) {
+        const int k = readlane_i(q.kv, t);
+        const float dyt = readlane_f(dyv, t);
+        IV<SL> pt;
+        wave_sync();
         if (act) {
-            const float2* ring = s.ring + (r & 1) * N;
-            U = ld_cv<SL>(ring, lane);
 #pragma unroll
-            for (int i = 0; i < SL; ++i) Up.v[i] = cadd(g.v[i], cmulc(da.v[i], ring[pa.v[i]]));
-            st_cv<SL>(s.ring + ((r + 1) & 1) * N, lane, Up);
+            for (int i = 0; i < SL; ++i) {
+                pt.v[i] = s.dict[k * N + lane * SL + i];
+                g.v[i].x += dyt * q.c[t].v[i].x;
+                g.v[i].y -= dyt * q.c[t].v[i].y;
+                vd[lane * SL + i] = make_float4(g.v[i].x, g.v[i].y, da.v[i].x, da.v[i].y);
+                PA[lane * SL + i] = (uint8_t)pa.v[i];
+            }
         }
         wave_sync();
-        if (lane == 0) publish_ready(s.ready, r + 1);
-        if (ch == 0 && a.dh0 && act) st_cv<SL>(a.dh0 + (size_t)seq * N, lane, Up);
-
-        // ---- recompute the chunk's states from the saved entering state
-        CV<SL> Hs[TAU + 1];
-        Hs[0] = hs;
+        if (act) {
 #pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t);
-            const int M = FB ? readlane_i(q.mv, t) : 0;
-            pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
-            Hs[t + 1] = hs;
+            for (int i = 0; i < SL; ++i) {
+                const float4 e = vd[pt.v[i]];
+                pa.v[i] = PA[pt.v[i]];
+                da.v[i] = cmul(make_float2(e.z, e.w), Dt(q, t).v[i]);
+                g.v[i] = cmulc(Dt(q, t).v[i], make_float2(e.x, e.y));
+            }
         }
+    }
 
-        // ---- final reverse walk with the true incoming gradient
-        g = U;
+    // ---- hand-off: U_{c-1} = gamma_c + Phi_c^H U_c (a gather from the ring)
 #pragma unroll
-        for (int t = TAU - 1; t >= 0; --t) {
-            const int k = readlane_i(q.kv, t);
-            const float dyt = readlane_f(dyv, t);
-            const size_t off = base + (size_t)t * stride;
-            IV<SL> pt;
-            CV<SL> dct;
-            wave_sync();
-            if (act) {
+    for (int i = 0; i < SL; ++i) {
+        materialize(pa.v[i]);
+        materialize(da.v[i].x);
+        materialize(da.v[i].y);
+        materialize(g.v[i].x);
+        materialize(g.v[i].y);
+    }
+    wait_ready(s.ready, r, a.status, s.ready, 1);
+    CV<SL> U = cv_zero<SL>(), Up;
+    if (act) {
+        const float2* ring = s.ring + (r & 1) * N;
+        U = ld_cv<SL>(ring, lane);
 #pragma unroll
-                for (int i = 0; i < SL; ++i) {
-                    pt.v[i] = s.dict[k * N + lane * SL + i];
-                    g.v[i].x += dyt * q.c[t].v[i].x;
-                    g.v[i].y -= dyt * q.c[t].v[i].y;
-                    dct.v[i] = make_float2(dyt * Hs[t + 1].v[i].x, -dyt * Hs[t + 1].v[i].y);
-                    reinterpret_cast<float2*>(vd)[2 * (lane * SL + i)] = g.v[i];
-                }
-            }
-            if (t < q.len && act) {
-                st_cv<SL>(a.db + off, lane, g);
-                st_cv<SL>(a.dc + off, lane, dct);
-            }
-            wave_sync();
-            if (act) {
-                CV<SL> dDt;
+        for (int i = 0; i < SL; ++i) Up.v[i] = cadd(g.v[i], cmulc(da.v[i], ring[pa.v[i]]));
+        st_cv<SL>(s.ring + ((r + 1) & 1) * N, lane, Up);
+    }
+    wave_sync();
+    if (lane == 0) publish_ready(s.ready, r + 1);
+    if (ch == 0 && a.dh0 && act) st_cv<SL>(a.dh0 + (size_t)seq * N, lane, Up);
+
+    // ---- recompute the chunk's states from the saved entering state
+    CV<SL> Hs[TAU + 1];
+    CV<SL> hs = u.hs;
+    Hs[0] = hs;
 #pragma unroll
-                for (int i = 0; i < SL; ++i) {
-                    const float2 gp = reinterpret_cast<const float2*>(vd)[2 * pt.v[i]];
-                    dDt.v[i] = cmulc(Hs[t].v[i], gp);
-                    g.v[i] = cmulc(Dt(q, t).v[i], gp);
-                }
-                if (t < q.len) st_cv<SL>(a.dD + off, lane, dDt);
+    for (int t = 0; t < TAU; ++t) {
+        const int k = readlane_i(q.kv, t);
+        const int M = FB ? readlane_i(q.mv, t) : 0;
+        pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
+        Hs[t + 1] = hs;
+    }
+
+    // ---- final reverse walk with the true incoming gradient
+    g = U;
+#pragma unroll
+    for (int t = TAU - 1; t >= 0; --t) {
+        const int k = readlane_i(q.kv, t);
+        const float dyt = readlane_f(dyv, t);
+        IV<SL> pt;
+        CV<SL> dct;
+        wave_sync();
+        if (act) {
+#pragma unroll
+            for (int i = 0; i < SL; ++i) {
+                pt.v[i] = s.dict[k * N + lane * SL + i];
+                g.v[i].x += dyt * q.c[t].v[i].x;
+                g.v[i].y -= dyt * q.c[t].v[i].y;
+                dct.v[i] = make_float2(dyt * Hs[t + 1].v[i].x, -dyt * Hs[t + 1].v[i].y);
+                reinterpret_cast<float2*>(vd)[2 * (lane * SL + i)] = g.v[i];
             }
+        }
+        const bool in = t < q.len;
+        const size_t off = base + (size_t)t * stride;
+        if (act && in) {
+            st_out<SL>(a.db + off, lane, g);
+            st_out<SL>(a.dc + off, lane, dct);
+        }
+        wave_sync();
+        if (act) {
+            CV<SL> dDt;
+#pragma unroll
+            for (int i = 0; i < SL; ++i) {
+                const float2 gp = reinterpret_cast<const float2*>(vd)[2 * pt.v[i]];
+                dDt.v[i] = cmulc(Hs[t].v[i], gp);
+                g.v[i] = cmulc(Dt(q, t).v[i], gp);
+            }
+            if (in) st_out<SL>(a.dD + off, lane, dDt);
+        }
+    }
+}
+
+// Wave wv owns reverse-order chunks wv, wv+W, ...; with PREFETCH every load of
+// its next chunk is in flight while it computes the current one.
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH>
+__device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+    constexpr int LANES = Lay<N>::LANES;
+    const int wv = wave_id(), lane = lane_id();
+    const bool act = lane < LANES;
+    bool bad = false;
+    if constexpr (PREFETCH) {
+        BwdChunk<N, TAU> ua, ub;
+        issue_bwd<N, TAU>(a, seq, bb, hh, wv, lane, act, ua);
+        for (int r = wv; r < a.C; r += 2 * W) {
+            issue_bwd<N, TAU>(a, seq, bb, hh, r + W, lane, act, ub);
+            issue_fence();
+            bwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, r, ua, bad);
+            if (r + W >= a.C) break;
+            issue_bwd<N, TAU>(a, seq, bb, hh, r + 2 * W, lane, act, ua);
+            issue_fence();
+            bwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, r + W, ub, bad);
+        }
+    } else {
+        for (int r = wv; r < a.C; r += W) {
+            BwdChunk<N, TAU> u;
+            issue_bwd<N, TAU>(a, seq, bb, hh, r, lane, act, u);
+            bwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, r, u, bad);
         }
     }
     if (bad) report_index_error(a.status);
@@ -855,10 +911,11 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
-    if (fb) bwd_body<N, TAU, W, 7, true>(a, s, seq, bb, hh);
-    else if (G == 1) bwd_body<N, TAU, W, 1, false>(a, s, seq, bb, hh);
-    else if (G == 3) bwd_body<N, TAU, W, 3, false>(a, s, seq, bb, hh);
-    else bwd_body<N, TAU, W, 7, false>(a, s, seq, bb, hh);
+    constexpr bool PF = fused_prefetch(N, TAU);
+    if (fb) bwd_body<N, TAU, W, 7, true, PF>(a, s, seq, bb, hh);
+    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF>(a, s, seq, bb, hh);
+    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF>(a, s, seq, bb, hh);
+    else bwd_body<N, TAU, W, 7, false, PF>(a, s, seq, bb, hh);
 }
 
 template <int N, int TAU, int W>
@@ -893,21 +950,17 @@ template <int N, bool FWD>
 hipError_t dispatch_tau(const FusedArgs& a, hipStream_t st) {
     constexpr int SL = Lay<N>::SL;
     switch (a.tau) {
-        case 4: {
-            constexpr int W = fused_waves(N, 4);
-            return FWD ? fwd_launch<N, 4, W>(a, st) : bwd_launch<N, 4, W>(a, st);
-        }
+        case 4:
+            return FWD ? fwd_launch<N, 4, fused_waves(N, 4)>(a, st) : bwd_launch<N, 4, fused_waves_bwd(N, 4)>(a, st);
         case 8:
-            if constexpr (8 * SL <= 16) {
-                constexpr int W = fused_waves(N, 8);
-                return FWD ? fwd_launch<N, 8, W>(a, st) : bwd_launch<N, 8, W>(a, st);
-            }
+            if constexpr (8 * SL <= 16)
+                return FWD ? fwd_launch<N, 8, fused_waves(N, 8)>(a, st)
+                           : bwd_launch<N, 8, fused_waves_bwd(N, 8)>(a, st);
             break;
         case 16:
-            if constexpr (16 * SL <= 16) {
-                constexpr int W = fused_waves(N, 16);
-                return FWD ? fwd_launch<N, 16, W>(a, st) : bwd_launch<N, 16, W>(a, st);
-            }
+            if constexpr (16 * SL <= 16)
+                return FWD ? fwd_launch<N, 16, fused_waves(N, 16)>(a, st)
+                           : bwd_launch<N, 16, fused_waves_bwd(N, 16)>(a, st);
             break;
         default: break;
     }

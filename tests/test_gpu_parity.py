@@ -198,6 +198,56 @@ def test_prepared_tables_match_per_call_build(N, K, pi_kind):
     check_all(inp2, got, s.chunk)
 
 
+def _guarded(shape, dtype, pad=4096):
+    """An output tensor inside a larger buffer whose margins hold a marker."""
+    n = int(np.prod(shape))
+    buf = torch.full((n + 2 * pad,), 7.25, dtype=dtype, device=DEV)
+    return buf, buf[pad:pad + n].view(shape), pad
+
+
+def _margins_intact(buf, pad):
+    m = torch.cat([buf[:pad], buf[-pad:]])
+    return bool((m == 7.25).all())
+
+
+@pytest.mark.parametrize("N,K,L,chunk", [(64, 16, 77, 8), (64, 16, 75, 16), (128, 64, 77, 4),
+                                         (128, 128, 77, 0), (256, 8, 43, 4), (8, 4, 13, 8)])
+def test_outputs_stay_inside_their_tensors(N, K, L, chunk):
+    """Every output is written inside its own tensor: with ragged last chunks
+    (padded steps) the bytes around each output stay untouched, and the
+    values match the oracle."""
+    import ctypes
+    B, H = 2, 3
+    inp = make_inputs(B=B, L=L, H=H, N=N, K=K, seed=L + N, with_h0=True, with_dhf=True)
+    T = to_dev(inp)
+    lib = pdssm.load()
+    d = pdssm.desc(B, L, H, N, K, chunk)
+    C = pdssm.num_chunks(d)
+    ws = torch.empty(max(pdssm.workspace_size(d, pdssm.OP_FWD), 1), dtype=torch.uint8, device=DEV)
+    status = torch.zeros(1, dtype=torch.int32, device=DEV)
+    outs = {"y": _guarded((B, L, H), torch.float32), "h_final": _guarded((B, H, N), torch.complex64),
+            "saved": _guarded((B, H, C, N), torch.complex64),
+            "dD": _guarded((B, L, H, N), torch.complex64), "db": _guarded((B, L, H, N), torch.complex64),
+            "dc": _guarded((B, L, H, N), torch.complex64), "dh0": _guarded((B, H, N), torch.complex64)}
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    st = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    o = {k: v[1] for k, v in outs.items()}
+    rc = lib.pdssm_scan_fwd(ctypes.byref(d), P(T["idx"]), P(T["pi"]), P(T["D"]), P(T["b"]), P(T["c"]),
+                            P(T["h0"]), P(o["y"]), P(o["h_final"]), P(o["saved"]), P(ws), ws.numel(),
+                            P(status), st)
+    assert rc == 0
+    rc = lib.pdssm_scan_bwd(ctypes.byref(d), P(T["idx"]), P(T["pi"]), P(T["D"]), P(T["b"]), P(T["c"]),
+                            P(o["saved"]), P(T["dy"]), P(T["dh_final"]), P(o["dD"]), P(o["db"]),
+                            P(o["dc"]), P(o["dh0"]), P(ws), ws.numel(), P(status), st)
+    assert rc == 0
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    for k, (buf, _, pad) in outs.items():
+        assert _margins_intact(buf, pad), k
+    got = {k: v.cpu().numpy() for k, v in o.items()}
+    check_all(inp, got, pdssm.chunk_len(d))
+
+
 def test_out_of_range_indices_flagged_not_faulting():
     inp = make_inputs(B=1, L=40, H=2, N=64, K=4, seed=9)
     bad = dict(inp)
