@@ -11,7 +11,7 @@ namespace pdssm {
 // Kernels that prefetch the next chunk (two register buffers, when a chunk
 // holds <= 8 rows per lane) run fewer, fatter waves.
 #ifndef PDSSM_PF_WAVES
-#define PDSSM_PF_WAVES 8
+#define PDSSM_PF_WAVES 7
 #endif
 #ifndef PDSSM_PF_MAX_ROWS
 #define PDSSM_PF_MAX_ROWS 8
@@ -19,14 +19,14 @@ namespace pdssm {
 #ifndef PDSSM_BWD_PF_WAVES
 #define PDSSM_BWD_PF_WAVES 8
 #endif
-constexpr int kFusedWaves = 11;
+constexpr int kFusedWaves = 7;
 constexpr bool fused_prefetch(int N, int tau) { return tau * (N > 64 ? N / 64 : 1) <= PDSSM_PF_MAX_ROWS; }
 constexpr int fused_waves(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_PF_WAVES : kFusedWaves; }
 constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_BWD_PF_WAVES : kFusedWaves; }
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
-    uint32_t rec, dict, mtab, ring, ready, agg, agp, aflag, vd, x, cs, pa, total;
+    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, aflag, vd, x, cs, pa, total;
 };
 
 inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
@@ -35,8 +35,10 @@ inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
 // pads the last, partial chunk of a sequence with exact no-op steps.  Each
 // wave's vd row block has N + 1 rows; row N stays zero.  W is the number of
 // chunk-computing waves; one more wave (the frontier wave) carries the state
-// from chunk to chunk.  ring: W + 1 carry slots; agg/agp/aflag: 2W slots of
-// published chunk operators (local state, diagonal, map) and their chunk ids.
+// from chunk to chunk.  ring: W + 1 carry slots; agg/agp/age/agh/aflag: 2W
+// slots of published chunk operators (local state and diagonal; the map, or
+// for many-to-one heads its sorted form: position of each source, last
+// position of each destination's run, run-start flags) and their chunk ids.
 inline LdsLayout fused_lds_layout(int N, int K, int W) {
     LdsLayout l;
     size_t o = 0;
@@ -50,6 +52,8 @@ inline LdsLayout fused_lds_layout(int N, int K, int W) {
     o += align16((size_t)(1 + 2 * W) * 4);
     l.agg = (uint32_t)o;   o += (size_t)2 * W * N * 16;
     l.agp = (uint32_t)o;   o += align16((size_t)2 * W * N);
+    l.age = (uint32_t)o;   o += align16((size_t)2 * W * N * 2);
+    l.agh = (uint32_t)o;   o += align16((size_t)2 * W * N);
     l.vd = (uint32_t)o;    o += (size_t)W * (N + 1) * 16;
     l.x = (uint32_t)o;     o += (size_t)(W + 1) * N * 8;
     l.cs = (uint32_t)o;    o += (size_t)W * N * 8;

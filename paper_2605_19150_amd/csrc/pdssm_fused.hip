@@ -126,7 +126,9 @@ struct Smem {
     float2* ring;   // [W+1][N] carry slots
     int* ready;     // carry counter, followed by the operator-slot flags
     float4* agg;    // [2W][N] published chunk operator: local state (xy), diagonal (zw)
-    uint8_t* agp;   // [2W][N] published chunk map
+    uint8_t* agp;   // [2W][N] published chunk map, or the sorted position of each source
+    uint16_t* age;  // [2W][N] last sorted position of each destination's run (kNoRun: none)
+    uint8_t* agh;   // [2W][N] 1 where a sorted position starts a destination's run
     int* aflag;     // [2W] chunk id held by each operator slot
     float4* vd;     // [W][N+1]
     float2* x;      // [W][N]
@@ -143,6 +145,8 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
     s.ready = reinterpret_cast<int*>(base + l.ready);
     s.agg = reinterpret_cast<float4*>(base + l.agg);
     s.agp = base + l.agp;
+    s.age = reinterpret_cast<uint16_t*>(base + l.age);
+    s.agh = base + l.agh;
     s.aflag = reinterpret_cast<int*>(base + l.aflag);
     s.vd = reinterpret_cast<float4*>(base + l.vd);
     s.x = reinterpret_cast<float2*>(base + l.x);
@@ -447,6 +451,138 @@ __device__ __forceinline__ float transpose_sum(float (&v)[T], int lane) {
     return v[0];
 }
 
+// ------------------------------------------------------------------ sorted chunk maps
+// For a many-to-one chunk map the frontier applies carry -> Pi (Delta .* carry)
+// without float atomics: the chunk wave orders the map's sources by
+// (destination, source); the frontier stores Delta_j carry_j at source j's
+// sorted position (a permutation, no collisions), adds up each
+// destination's run with a segmented scan across lanes, and every
+// destination reads the total at the end of its run.  Runs add their sources
+// in ascending source order, so the result is deterministic.
+constexpr uint16_t kNoRun = 0xffff;
+
+// DPP move with zero for lanes outside the row mask or without a source.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, true);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_fr(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, true));
+}
+
+// Inclusive prefix sum of an int over the 64 lanes.
+__device__ __forceinline__ int wave_incl_scan_i(int v) {
+    v += dpp_i<0x111, 0xf>(v);
+    v += dpp_i<0x112, 0xf>(v);
+    v += dpp_i<0x114, 0xf>(v);
+    v += dpp_i<0x118, 0xf>(v);
+    v += dpp_i<0x142, 0xa>(v);
+    v += dpp_i<0x143, 0xc>(v);
+    return v;
+}
+
+// One step of the segmented scan: add the value DPP brings in when `take`.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void seg_step(float2& v, bool take) {
+    const float tx = dpp_fr<CTRL, ROWS>(v.x), ty = dpp_fr<CTRL, ROWS>(v.y);
+    v.x += take ? tx : 0.f;
+    v.y += take ? ty : 0.f;
+}
+
+// Inclusive segmented sum over the 64 lanes of a complex value: a lane whose
+// bit is set in `starts` begins a new segment (lane 0 always does).  Row-wise
+// shifts, then the row broadcasts carry row totals across rows, each term
+// taken only when its source lane lies in the same segment.
+__device__ __forceinline__ float2 wave_seg_scan(float2 v, uint64_t starts, int lane) {
+    const uint64_t le = starts & ((2ull << lane) - 1ull);  // lane 63: 2 << 63 wraps to 0
+    const int s0 = le ? 63 - __builtin_clzll(le) : 0;      // first lane of this lane's segment
+    seg_step<0x111, 0xf>(v, lane - 1 >= s0);
+    seg_step<0x112, 0xf>(v, lane - 2 >= s0);
+    seg_step<0x114, 0xf>(v, lane - 4 >= s0);
+    seg_step<0x118, 0xf>(v, lane - 8 >= s0);
+    seg_step<0x142, 0xa>(v, s0 < (lane & ~15));
+    seg_step<0x143, 0xc>(v, s0 < 32);
+    return v;
+}
+
+template <int N>
+struct Log2 {
+    static constexpr int v = N <= 1 ? 0 : 1 + Log2<N / 2>::v;
+};
+
+// Sorted form of the map pm (source j = lane*SL + r goes to row pm[r]),
+// written into operator slot `slot`: agp = sorted position of every source,
+// age = last position of every destination's run (kNoRun if it has no
+// source), agh = run-start flags of the positions.  Ranks among equal
+// destinations come from ballots over the destination bits, so the order is
+// exact and deterministic.  OFF: N ints of this wave's scratch.
+template <int N>
+__device__ __forceinline__ void publish_sorted_map(const Smem& s, int slot, const IV<Lay<N>::SL>& pm, int lane,
+                                                   bool act, int* OFF) {
+    constexpr int SL = Lay<N>::SL, BITS = Log2<N>::v;
+    const uint64_t actm = __builtin_amdgcn_ballot_w64(act);
+    const uint64_t lt = (1ull << lane) - 1ull;
+    // mr[r][q]: lanes whose slot q goes to the row of this lane's source r;
+    // mo[r][q]: lanes whose slot q goes to this lane's own row r.  One ballot
+    // per destination bit and slot narrows both.
+    uint64_t mr[SL][SL], mo[SL][SL];
+#pragma unroll
+    for (int r = 0; r < SL; ++r)
+#pragma unroll
+        for (int q = 0; q < SL; ++q) mr[r][q] = mo[r][q] = actm;
+#pragma unroll 1
+    for (int b = 0; b < BITS; ++b) {
+#pragma unroll
+        for (int q = 0; q < SL; ++q) {
+            const uint64_t m = __builtin_amdgcn_ballot_w64(act && ((pm.v[q] >> b) & 1));
+#pragma unroll
+            for (int r = 0; r < SL; ++r) {
+                mr[r][q] &= ((pm.v[r] >> b) & 1) ? m : ~m;
+                mo[r][q] &= (((lane * SL + r) >> b) & 1) ? m : ~m;
+            }
+        }
+    }
+    int rank[SL], cnt[SL];
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        int rk = 0, c = 0;
+#pragma unroll
+        for (int q = 0; q < SL; ++q) {
+            rk += __builtin_popcountll(mr[r][q] & lt);
+            if (q < r) rk += pm.v[q] == pm.v[r] ? 1 : 0;
+            c += __builtin_popcountll(mo[r][q]);
+        }
+        rank[r] = rk;
+        cnt[r] = act ? c : 0;
+    }
+    int tot = 0;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) tot += cnt[r];
+    int off = wave_incl_scan_i(tot) - tot;  // first position of this lane's first row
+    uint16_t* AE = s.age + slot * N;
+    uint8_t* AH = s.agh + slot * N;
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            OFF[lane * SL + r] = off;
+            AE[lane * SL + r] = cnt[r] ? (uint16_t)(off + cnt[r] - 1) : kNoRun;
+            AH[lane * SL + r] = 0;
+            off += cnt[r];
+        }
+    }
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            const int p = OFF[pm.v[r]] + rank[r];
+            s.agp[slot * N + lane * SL + r] = (uint8_t)p;
+            if (rank[r] == 0) AH[p] = 1;
+        }
+    }
+}
+
 // One chunk is run once, from a zero state (Algorithm 1 Phase A), while the
 // readout is split as in Phase C: with M_t = A_t ... A_s in PD form
 // (Pi_t, Delta_t) and x_t = x_t^loc + M_t carry,
@@ -515,9 +651,10 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int
 #pragma unroll
             for (int r = 0; r < SL; ++r) {
                 s.agg[slot * N + lane * SL + r] = make_float4(Bm.v[r].x, Bm.v[r].y, dm.v[r].x, dm.v[r].y);
-                s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
+                if constexpr (G == 1 && !FB) s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
             }
         }
+        if constexpr (!(G == 1 && !FB)) publish_sorted_map<N>(s, slot, pm, lane, act, reinterpret_cast<int*>(X));
         wave_sync();
         if (lane == 0) publish_ready(s.aflag + slot, ch);
     }
@@ -539,32 +676,89 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int
         a.y[((size_t)bb * a.L + ch * TAU + t) * a.H + hh] = yv;
 }
 
-// A published chunk operator as the frontier wave holds it.
+// A published chunk operator as the frontier wave holds it: local state B
+// and diagonal d; p = the map (permutation heads) or the sorted position of
+// each source; e, h = run ends per destination and run-start flags per
+// position (many-to-one heads).
 template <int SL>
 struct ChunkOp {
     CV<SL> B, d;
-    IV<SL> p;
+    IV<SL> p, e, h;
 };
 
-template <int N>
+template <int N, bool SORTED>
 __device__ __forceinline__ ChunkOp<Lay<N>::SL> read_op(const Smem& s, int slot, int lane, bool act) {
     constexpr int SL = Lay<N>::SL;
     ChunkOp<SL> o;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        o.B.v[r] = o.d.v[r] = make_float2(0.f, 0.f);
+        o.p.v[r] = o.e.v[r] = o.h.v[r] = 0;
+    }
     if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
-            const float4 e = s.agg[slot * N + lane * SL + r];
+            const int i = slot * N + lane * SL + r;
+            const float4 e = s.agg[i];
             o.B.v[r] = make_float2(e.x, e.y);
             o.d.v[r] = make_float2(e.z, e.w);
-            o.p.v[r] = s.agp[slot * N + lane * SL + r];
+            o.p.v[r] = s.agp[i];
+            if constexpr (SORTED) {
+                o.e.v[r] = s.age[i];
+                o.h.v[r] = s.agh[i];
+            }
         }
-    } else {
-        o.B = cv_zero<SL>();
-        o.d = cv_zero<SL>();
-#pragma unroll
-        for (int r = 0; r < SL; ++r) o.p.v[r] = 0;
     }
     return o;
+}
+
+// nxt = B + Pi (Delta .* carry) for a sorted many-to-one operator; X: N
+// complex values of LDS scratch.
+template <int N>
+__device__ __forceinline__ CV<Lay<N>::SL> apply_sorted(const ChunkOp<Lay<N>::SL>& op, const CV<Lay<N>::SL>& carry,
+                                                       float2* X, int lane, bool act) {
+    constexpr int SL = Lay<N>::SL;
+    CV<SL> u = cv_zero<SL>();
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) X[op.p.v[r]] = cmul(op.d.v[r], carry.v[r]);
+    }
+    wave_sync();
+    if (act) u = ld_cv<SL>(X, lane);
+    // runs within the lane, then across lanes
+    bool seen = false;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        if (r > 0 && !op.h.v[r]) u.v[r] = cadd(u.v[r], u.v[r - 1]);
+        seen |= op.h.v[r] != 0;
+    }
+    const uint64_t starts = __builtin_amdgcn_ballot_w64(act && seen);
+    const float2 C = wave_seg_scan(u.v[SL - 1], starts, lane);
+    if constexpr (SL == 1) {
+        u.v[0] = C;
+    } else {
+        const float2 Cp = make_float2(dpp_fr<0x138, 0xf>(C.x), dpp_fr<0x138, 0xf>(C.y));  // from lane - 1
+        bool head = false;
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            head |= op.h.v[r] != 0;
+            if (!head) u.v[r] = cadd(u.v[r], Cp);
+        }
+    }
+    wave_sync();
+    if (act) st_cv<SL>(X, lane, u);
+    wave_sync();
+    CV<SL> nxt = cv_zero<SL>();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            const int e = op.e.v[r];
+            const float2 t = X[e == kNoRun ? 0 : e];
+            nxt.v[r] = cadd(op.B.v[r], e == kNoRun ? make_float2(0.f, 0.f) : t);
+        }
+    }
+    return nxt;
 }
 
 // The frontier wave: keeps the running state in registers and, chunk by
@@ -590,28 +784,16 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     CV<SL> carry = cv_zero<SL>();
     if (a.h0 && act) carry = ld_cv<SL>(a.h0 + (size_t)seq * N, lane);
     wait_ready(s.aflag, 0, a.status, flags, nflags);
-    ChunkOp<SL> op = read_op<N>(s, 0, lane, act);
-    if (!kPerm) {
-        wave_sync();
-        if (act) st_cv<SL>(X, lane, op.B);
-    }
+    ChunkOp<SL> op = read_op<N, !kPerm>(s, 0, lane, act);
     for (int c = 0; c < a.C; ++c) {
-        CV<SL> v;
-#pragma unroll
-        for (int r = 0; r < SL; ++r) v.v[r] = cmul(op.d.v[r], carry.v[r]);
         wave_sync();
         if (act) st_cv<SL>(s.ring + (c % (W + 1)) * N, lane, carry);
-        if (act) {
-            if constexpr (kPerm) {
+        CV<SL> nxt;
+        if constexpr (kPerm) {
+            // every entry is a permutation, so is Pi_c: scatter by plain stores
+            if (act) {
 #pragma unroll
-                for (int r = 0; r < SL; ++r) X[op.p.v[r]] = v.v[r];
-            } else {
-#pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    float* dst = reinterpret_cast<float*>(X + op.p.v[r]);
-                    atomicAdd(dst, v.v[r].x);
-                    atomicAdd(dst + 1, v.v[r].y);
-                }
+                for (int r = 0; r < SL; ++r) X[op.p.v[r]] = cmul(op.d.v[r], carry.v[r]);
             }
         }
         const bool more = c + 1 < a.C;
@@ -621,26 +803,24 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         if (more) {
             seen = __hip_atomic_load(s.aflag + nslot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             issue_fence();
-            nx = read_op<N>(s, nslot, lane, act);
+            nx = read_op<N, !kPerm>(s, nslot, lane, act);
         }
-        wave_sync();
-        CV<SL> nxt = cv_zero<SL>();
-        if (act) nxt = ld_cv<SL>(X, lane);
-        wave_sync();
-        if (lane == 0) publish_ready(s.ready, c + 1);
         if constexpr (kPerm) {
+            wave_sync();
+            nxt = cv_zero<SL>();
+            if (act) nxt = ld_cv<SL>(X, lane);
 #pragma unroll
             for (int r = 0; r < SL; ++r) nxt.v[r] = cadd(nxt.v[r], op.B.v[r]);
+        } else {
+            nxt = apply_sorted<N>(op, carry, X, lane, act);
         }
+        wave_sync();
+        if (lane == 0) publish_ready(s.ready, c + 1);
         carry = nxt;
         if (more) {
             if (__builtin_amdgcn_readfirstlane(seen) < c + 1) {
                 wait_ready(s.aflag + nslot, c + 1, a.status, flags, nflags);
-                nx = read_op<N>(s, nslot, lane, act);
-            }
-            if (!kPerm) {
-                wave_sync();
-                if (act) st_cv<SL>(X, lane, nx.B);
+                nx = read_op<N, !kPerm>(s, nslot, lane, act);
             }
             op = nx;
         }
