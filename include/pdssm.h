@@ -119,6 +119,14 @@ size_t pdssm_workspace_size(const pdssm_desc* desc, int op);
  * status for an invalid desc. */
 int pdssm_uses_fused(const pdssm_desc* desc);
 
+/* Number of segments each sequence is cut into along L by the single-read
+ * scans (1, or up to 8 when there are fewer than 256 sequences and at least
+ * 32 chunks per segment): segment s covers chunks [s*Cs, min((s+1)*Cs, C)),
+ * Cs = ceil(C/S), one workgroup each, after a pass that folds every segment
+ * into one PD operator (App. E.1 Algorithm 1's aggregate-then-carry
+ * structure, one level up).  Negative status for an invalid desc. */
+int pdssm_scan_segments(const pdssm_desc* desc);
+
 /* Human-readable name of a status code (static string, never NULL). */
 const char* pdssm_status_string(int status);
 

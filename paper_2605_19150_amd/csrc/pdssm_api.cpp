@@ -101,9 +101,48 @@ bool use_fused(const pdssm_desc* d) {
     return fused_layout(d, tau, true).total <= pdssm::kMaxLds && fused_layout(d, tau, false).total <= pdssm::kMaxLds;
 }
 
-// Fused workspace: byte dictionary, row records, per-entry max in-degree.
-size_t fused_ws_bytes(const Sizes& s, const pdssm_desc* d) {
+// Segments per sequence of the fused scans.  One workgroup per sequence
+// keeps a CU busy; with fewer sequences than kSegTarget workgroups the
+// sequences are cut along L into up to kMaxSeg segments of at least
+// kMinSegChunks chunks (so the extra aggregate pass stays short relative to
+// the scan).
+#ifndef PDSSM_SEG_TARGET
+#define PDSSM_SEG_TARGET 256
+#endif
+constexpr int kSegTarget = PDSSM_SEG_TARGET;
+constexpr int kMaxSeg = 8;
+constexpr int kMinSegChunks = 32;
+
+struct Segs {
+    int S, Cs;
+};
+
+Segs segments(const pdssm_desc* d, int C) {
+    const long long seqs = (long long)d->B * d->H;
+    int S = 1;
+    if (seqs < kSegTarget) {
+        S = (int)((kSegTarget + seqs - 1) / seqs);
+        if (S > kMaxSeg) S = kMaxSeg;
+        if (S > C / kMinSegChunks) S = C / kMinSegChunks;
+        if (S < 1) S = 1;
+    }
+    Segs g;
+    g.Cs = (C + S - 1) / S;
+    g.S = (C + g.Cs - 1) / g.Cs;  // no empty segment
+    return g;
+}
+
+// Fused workspace: byte dictionary, row records, per-entry max in-degree,
+// then the segment aggregates when sequences are cut into segments.
+size_t fused_tables_bytes(const Sizes& s, const pdssm_desc* d) {
     return align_up(s.dictN) + align_up(s.dictN * 8) + align_up((size_t)d->H * d->K);
+}
+
+size_t fused_ws_bytes(const Sizes& s, const pdssm_desc* d, int C) {
+    const Segs g = segments(d, C);
+    size_t n = fused_tables_bytes(s, d);
+    if (g.S > 1) n += 2 * align_up(s.seqN * g.S * 8) + align_up(s.seqN * g.S * 4);
+    return n;
 }
 
 // Chunked workspace: int map, complex diag, complex term, complex carry/U.
@@ -111,8 +150,8 @@ size_t chunked_ws_bytes(const Sizes& s) {
     return align_up(s.perChunk * 4) + 3 * align_up(s.perChunk * 8);
 }
 
-size_t ws_bytes_for(const Sizes& s, const pdssm_desc* d) {
-    return use_fused(d) ? fused_ws_bytes(s, d) : chunked_ws_bytes(s);
+size_t ws_bytes_for(const Sizes& s, const pdssm_desc* d, int C) {
+    return use_fused(d) ? fused_ws_bytes(s, d, C) : chunked_ws_bytes(s);
 }
 
 void carve_chunked(ScanArgs& a, void* ws, const Sizes& s) {
@@ -152,6 +191,19 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     f.rec = pa.rec;
     f.mtab = pa.mtab;
     f.lds = fused_layout(d, f.tau, fwd);
+    const Segs g = segments(d, f.C);
+    f.S = g.S;
+    f.Cs = g.Cs;
+    f.segA = f.segD = nullptr;
+    f.segP = nullptr;
+    if (g.S > 1) {
+        char* p = static_cast<char*>(ws) + fused_tables_bytes(s, d);
+        f.segA = reinterpret_cast<float2*>(p);
+        p += align_up(s.seqN * g.S * 8);
+        f.segD = reinterpret_cast<float2*>(p);
+        p += align_up(s.seqN * g.S * 8);
+        f.segP = reinterpret_cast<int*>(p);
+    }
     if (d->flags & PDSSM_FLAG_PREPARED) return hipSuccess;
     return pdssm::launch_prep(pa, st);
 }
@@ -215,7 +267,8 @@ size_t pdssm_workspace_size(const pdssm_desc* d, int op) {
     if (op != PDSSM_OP_FWD && op != PDSSM_OP_BWD) return (size_t)-1;
     int tau = scan_chunk(d);
     if (tau < 0) return (size_t)-1;
-    return ws_bytes_for(sizes_of(d, (d->L + tau - 1) / tau), d);
+    const int C = (d->L + tau - 1) / tau;
+    return ws_bytes_for(sizes_of(d, C), d, C);
 }
 
 const char* pdssm_status_string(int st) {
@@ -230,6 +283,13 @@ const char* pdssm_status_string(int st) {
     }
 }
 
+int pdssm_scan_segments(const pdssm_desc* d) {
+    const int tau = scan_chunk(d);
+    if (tau < 0) return tau;
+    if (!use_fused(d)) return 1;
+    return segments(d, (d->L + tau - 1) / tau).S;
+}
+
 int pdssm_uses_fused(const pdssm_desc* d) {
     const int tau = scan_chunk(d);
     if (tau < 0) return tau;
@@ -241,8 +301,9 @@ int pdssm_prepare(const pdssm_desc* d, const int32_t* pi, void* ws, size_t ws_by
     int tau = scan_chunk(d);
     if (tau < 0) return tau;
     if (!pi || misaligned(pi)) return PDSSM_ERR_INVALID_ARG;
-    const Sizes s = sizes_of(d, (d->L + tau - 1) / tau);
-    const size_t need = ws_bytes_for(s, d);
+    const int C = (d->L + tau - 1) / tau;
+    const Sizes s = sizes_of(d, C);
+    const size_t need = ws_bytes_for(s, d, C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (overlap({ws, need}, {pi, (size_t)d->H * d->K * d->N * 4})) return PDSSM_ERR_INVALID_ARG;
@@ -263,7 +324,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
     ScanArgs a = base_args(d, tau);
     const Sizes s = sizes_of(d, a.C);
-    const size_t need = ws_bytes_for(s, d);
+    const size_t need = ws_bytes_for(s, d, a.C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
@@ -309,7 +370,7 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
     ScanArgs a = base_args(d, tau);
     const Sizes s = sizes_of(d, a.C);
-    const size_t need = ws_bytes_for(s, d);
+    const size_t need = ws_bytes_for(s, d, a.C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;

@@ -26,7 +26,7 @@ constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? 
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
-    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, aflag, vd, x, cs, pa, total;
+    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, agm, aflag, vd, x, cs, pa, total;
 };
 
 inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
@@ -38,7 +38,8 @@ inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
 // from chunk to chunk.  ring: W + 1 carry slots; agg/agp/age/agh/aflag: 2W
 // slots of published chunk operators (local state and diagonal; the map, or
 // for many-to-one heads its sorted form: position of each source, last
-// position of each destination's run, run-start flags) and their chunk ids.
+// position of each destination's run, run-start flags; agm: the map itself,
+// for the aggregate pass) and their chunk ids.
 inline LdsLayout fused_lds_layout(int N, int K, int W) {
     LdsLayout l;
     size_t o = 0;
@@ -54,6 +55,7 @@ inline LdsLayout fused_lds_layout(int N, int K, int W) {
     l.agp = (uint32_t)o;   o += align16((size_t)2 * W * N);
     l.age = (uint32_t)o;   o += align16((size_t)2 * W * N * 2);
     l.agh = (uint32_t)o;   o += align16((size_t)2 * W * N);
+    l.agm = (uint32_t)o;   o += align16((size_t)2 * W * N);
     l.vd = (uint32_t)o;    o += (size_t)W * (N + 1) * 16;
     l.x = (uint32_t)o;     o += (size_t)(W + 1) * N * 8;
     l.cs = (uint32_t)o;    o += (size_t)W * N * 8;
@@ -97,6 +99,14 @@ struct FusedArgs {
     const uint8_t* mtab;
     int* status;
     LdsLayout lds;
+    // Long sequences are cut into S segments of Cs chunks, one workgroup
+    // each; an aggregate pass first folds every segment into one PD operator
+    // (forward: local state, map, diagonal; backward: local adjoint, map,
+    // diagonal), [B*H][S][N] each.  S = 1: one workgroup per sequence.
+    int S, Cs;
+    float2* segA;
+    float2* segD;
+    int* segP;
 };
 
 hipError_t launch_prep(const PrepArgs& p, hipStream_t s);

@@ -129,6 +129,7 @@ struct Smem {
     uint8_t* agp;   // [2W][N] published chunk map, or the sorted position of each source
     uint16_t* age;  // [2W][N] last sorted position of each destination's run (kNoRun: none)
     uint8_t* agh;   // [2W][N] 1 where a sorted position starts a destination's run
+    uint8_t* agm;   // [2W][N] the chunk map itself (aggregate pass)
     int* aflag;     // [2W] chunk id held by each operator slot
     float4* vd;     // [W][N+1]
     float2* x;      // [W][N]
@@ -147,6 +148,7 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
     s.agp = base + l.agp;
     s.age = reinterpret_cast<uint16_t*>(base + l.age);
     s.agh = base + l.agh;
+    s.agm = base + l.agm;
     s.aflag = reinterpret_cast<int*>(base + l.aflag);
     s.vd = reinterpret_cast<float4*>(base + l.vd);
     s.x = reinterpret_cast<float2*>(base + l.x);
@@ -583,18 +585,81 @@ __device__ __forceinline__ void publish_sorted_map(const Smem& s, int slot, cons
     }
 }
 
+// ------------------------------------------------------------------ work units
+// The chunk range of one workgroup: chunks [c0, c0 + nc) of sequence seq,
+// segment sg of S (S = 1: the whole sequence).  A grid of B*H*nseg
+// workgroups covers segments first_sg .. first_sg + nseg - 1 of every
+// sequence; the segments of one sequence sit on one XCD.
+struct Work {
+    int seq, bb, hh, sg, c0, nc;
+};
+
+__device__ __forceinline__ Work work_of(const FusedArgs& a, int nseg, int first_sg) {
+    Work w;
+    const int u = xcd_seq(a.B * a.H * nseg);
+    w.seq = u / nseg;
+    w.sg = u - w.seq * nseg + first_sg;
+    w.bb = w.seq / a.H;
+    w.hh = w.seq - w.bb * a.H;
+    w.c0 = w.sg * a.Cs;
+    w.nc = min(a.C - w.c0, a.Cs);
+    return w;
+}
+
+// The state entering segment w.sg: h0 (or 0) pushed through the aggregates
+// of segments 0 .. w.sg-1, carry <- B_s + Phi_s carry, each row adding its
+// sources in ascending order (cross-lane values by readlane).
+template <int N>
+__device__ __forceinline__ CV<Lay<N>::SL> seg_enter_fwd(const FusedArgs& a, const Work& w, int lane, bool act) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    CV<SL> carry = cv_zero<SL>();
+    if (a.h0 && act) carry = ld_cv<SL>(a.h0 + (size_t)w.seq * N, lane);
+    for (int sp = 0; sp < w.sg; ++sp) {
+        const size_t base = ((size_t)w.seq * a.S + sp) * N;
+        CV<SL> acc = cv_zero<SL>(), v = cv_zero<SL>();
+        IV<SL> P;
+#pragma unroll
+        for (int r = 0; r < SL; ++r) P.v[r] = 0;
+        if (act) {
+            acc = ld_cv<SL>(a.segA + base, lane);
+            const CV<SL> d = ld_cv<SL>(a.segD + base, lane);
+            P = ld_iv<SL>(a.segP + base, lane);
+#pragma unroll
+            for (int r = 0; r < SL; ++r) v.v[r] = cmul(d.v[r], carry.v[r]);
+        }
+        for (int jl = 0; jl < LANES; ++jl) {
+#pragma unroll
+            for (int q = 0; q < SL; ++q) {
+                const int pj = readlane_i(P.v[q], jl);
+                const float vx = readlane_f(v.v[q].x, jl), vy = readlane_f(v.v[q].y, jl);
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    const bool hit = pj == lane * SL + r;
+                    acc.v[r].x += hit ? vx : 0.f;
+                    acc.v[r].y += hit ? vy : 0.f;
+                }
+            }
+        }
+        carry = acc;
+    }
+    return carry;
+}
+
 // One chunk is run once, from a zero state (Algorithm 1 Phase A), while the
 // readout is split as in Phase C: with M_t = A_t ... A_s in PD form
 // (Pi_t, Delta_t) and x_t = x_t^loc + M_t carry,
 //   y_t = Re<c_t, x_t^loc> + Re sum_j w_t[j] carry[j],  w_t[j] = Delta_t[j] c_t[Pi_t[j]].
 // The wave keeps w_t and the local readout partials, hands the carry on as
 // soon as the chunk is folded, and finishes y once its own carry arrives.
-template <int N, int TAU, int W, int G, bool FB>
-__device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int seq, int bb, int hh, int ch,
+// AGG: the aggregate pass of a segment -- the wave only builds and publishes
+// the chunk operator (c is not loaded, no readout).
+template <int N, int TAU, int W, int G, bool FB, bool AGG>
+__device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int lc,
                                           Chunk<N, TAU>& q, bool& bad) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
+    const int ch = w.c0 + lc;
     float4* vd = s.vd + wv * (N + 1);
     float2* X = s.x + wv * N;
     float2* CS = s.cs + wv * N;
@@ -614,7 +679,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int
     for (int t = 0; t < TAU; ++t) {
         const int k = readlane_i(q.kv, t);
         const int M = FB ? readlane_i(q.mv, t) : 0;
-        if (act) {
+        if (!AGG && act) {
             wave_sync();
 #pragma unroll
             for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
@@ -628,40 +693,46 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int
                 const int p = pm.v[r];
                 dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
                 pm.v[r] = s.dict[k * N + p];
-                wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
-                part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+                if constexpr (!AGG) {
+                    wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
+                    part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+                }
             }
-        } else {
+        } else if constexpr (!AGG) {
             wt[t] = cv_zero<SL>();
         }
         yl[t] = part;
     }
 
     // ---- 3. publish the chunk operator for the frontier wave, take carry_c.
-    // Slot reuse: the operator of chunk ch + 2W goes where that of ch went.
-    // This wave writes it only after carry_{ch+W} arrived, which the frontier
-    // publishes after it read operator ch.  Carry slot ch % (W + 1) is
-    // rewritten with carry_{ch+W+1} only after the frontier took operator
-    // ch + W from this same wave, which this wave publishes after its read
-    // of carry_ch below (one wave's LDS accesses complete in order).
+    // Slot reuse: the operator of local chunk lc + 2W goes where that of lc
+    // went.  This wave writes it only after carry_{lc+W} arrived, which the
+    // frontier publishes after it read operator lc (the aggregate pass waits
+    // for that hand-off count explicitly).  Carry slot lc % (W + 1) is
+    // rewritten with carry_{lc+W+1} only after the frontier took operator
+    // lc + W from this same wave, which this wave publishes after its read
+    // of carry_lc below (one wave's LDS accesses complete in order).
     {
-        const int slot = ch % (2 * W);
+        const int slot = lc % (2 * W);
+        if constexpr (AGG) wait_ready(s.ready, lc - 2 * W + 1, a.status, s.ready, 1 + 2 * W);
         wave_sync();
         if (act) {
 #pragma unroll
             for (int r = 0; r < SL; ++r) {
                 s.agg[slot * N + lane * SL + r] = make_float4(Bm.v[r].x, Bm.v[r].y, dm.v[r].x, dm.v[r].y);
                 if constexpr (G == 1 && !FB) s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
+                if constexpr (AGG) s.agm[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
             }
         }
         if constexpr (!(G == 1 && !FB)) publish_sorted_map<N>(s, slot, pm, lane, act, reinterpret_cast<int*>(X));
         wave_sync();
-        if (lane == 0) publish_ready(s.aflag + slot, ch);
+        if (lane == 0) publish_ready(s.aflag + slot, lc);
     }
-    wait_ready(s.ready, ch + 1, a.status, s.ready, 1 + 2 * W);
+    if constexpr (AGG) return;
+    wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * W);
     CV<SL> carry = cv_zero<SL>();
-    if (act) carry = ld_cv<SL>(s.ring + (ch % (W + 1)) * N, lane);
-    if (act && a.saved) st_cv<SL>(a.saved + ((size_t)seq * a.C + ch) * N, lane, carry);
+    if (act) carry = ld_cv<SL>(s.ring + (lc % (W + 1)) * N, lane);
+    if (act && a.saved) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
 
     // ---- 4. readout correction with the true carry, then one store per chunk
 #pragma unroll
@@ -673,7 +744,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, int
     const float yv = transpose_sum<TAU>(yl, lane);
     const int t = lane / (kWave / TAU);
     if (lane % (kWave / TAU) == 0 && t < q.len)
-        a.y[((size_t)bb * a.L + ch * TAU + t) * a.H + hh] = yv;
+        a.y[((size_t)w.bb * a.L + ch * TAU + t) * a.H + w.hh] = yv;
 }
 
 // A published chunk operator as the frontier wave holds it: local state B
@@ -771,8 +842,8 @@ __device__ __forceinline__ CV<Lay<N>::SL> apply_sorted(const ChunkOp<Lay<N>::SL>
 // operator's; a flag still behind sends the wave to a bounded wait and a
 // re-read).  The wave runs at raised issue priority: it shares its SIMD with
 // chunk waves whose long arithmetic runs would otherwise delay it.
-template <int N, int W, int G, bool FB>
-__device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, int seq) {
+template <int N, int W, int G, bool FB, bool AGG>
+__device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     constexpr bool kPerm = G == 1 && !FB;
     const int lane = lane_id();
@@ -780,14 +851,22 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     float2* X = s.x + W * N;
     int* flags = s.ready;
     const int nflags = 1 + 2 * W;
+    // The aggregate pass folds the segment from zero and composes its map;
+    // the scan starts from the state entering its segment.
+    CV<SL> carry = AGG ? cv_zero<SL>() : seg_enter_fwd<N>(a, w, lane, act);
+    IV<SL> accP;
+    CV<SL> accD;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        accP.v[r] = lane * SL + r;
+        accD.v[r] = make_float2(1.f, 0.f);
+    }
     __builtin_amdgcn_s_setprio(3);
-    CV<SL> carry = cv_zero<SL>();
-    if (a.h0 && act) carry = ld_cv<SL>(a.h0 + (size_t)seq * N, lane);
     wait_ready(s.aflag, 0, a.status, flags, nflags);
     ChunkOp<SL> op = read_op<N, !kPerm>(s, 0, lane, act);
-    for (int c = 0; c < a.C; ++c) {
+    for (int c = 0; c < w.nc; ++c) {
         wave_sync();
-        if (act) st_cv<SL>(s.ring + (c % (W + 1)) * N, lane, carry);
+        if (!AGG && act) st_cv<SL>(s.ring + (c % (W + 1)) * N, lane, carry);
         CV<SL> nxt;
         if constexpr (kPerm) {
             // every entry is a permutation, so is Pi_c: scatter by plain stores
@@ -796,7 +875,7 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
                 for (int r = 0; r < SL; ++r) X[op.p.v[r]] = cmul(op.d.v[r], carry.v[r]);
             }
         }
-        const bool more = c + 1 < a.C;
+        const bool more = c + 1 < w.nc;
         const int nslot = (c + 1) % (2 * W);
         int seen = 0x7fffffff;
         ChunkOp<SL> nx;
@@ -814,6 +893,19 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         } else {
             nxt = apply_sorted<N>(op, carry, X, lane, act);
         }
+        if constexpr (AGG) {
+            // Phi_acc <- Phi_c Phi_acc: (Pi_c[Pi_acc], Delta_c[Pi_acc] * Delta_acc)
+            const int slot = c % (2 * W);
+            if (act) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    const int p = accP.v[r];
+                    const float4 e = s.agg[slot * N + p];
+                    accD.v[r] = cmul(make_float2(e.z, e.w), accD.v[r]);
+                    accP.v[r] = s.agm[slot * N + p];
+                }
+            }
+        }
         wave_sync();
         if (lane == 0) publish_ready(s.ready, c + 1);
         carry = nxt;
@@ -826,61 +918,73 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         }
     }
     __builtin_amdgcn_s_setprio(0);
-    if (act && a.hfinal) st_cv<SL>(a.hfinal + (size_t)seq * N, lane, carry);
+    if constexpr (AGG) {
+        const size_t base = ((size_t)w.seq * a.S + w.sg) * N;
+        if (act) {
+            st_cv<SL>(a.segA + base, lane, carry);
+            st_cv<SL>(a.segD + base, lane, accD);
+            st_iv<SL>(a.segP + base, lane, accP);
+        }
+    } else if (act && a.hfinal && w.sg == a.S - 1) {
+        st_cv<SL>(a.hfinal + (size_t)w.seq * N, lane, carry);
+    }
 }
 
-// Wave wv owns chunks wv, wv+W, ...; with PREFETCH the loads of its next chunk
-// are in flight while it computes the current one (two register buffers).
-template <int N, int TAU, int W, int G, bool FB, bool PREFETCH>
-__device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+// Wave wv owns local chunks wv, wv+W, ...; with PREFETCH the loads of its next
+// chunk are in flight while it computes the current one (two register
+// buffers).  A local chunk past the range issues an empty chunk.
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG>
+__device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     if (wv == W) {
-        fwd_frontier<N, W, G, FB>(a, s, seq);
+        fwd_frontier<N, W, G, FB, AGG>(a, s, w);
         return;
     }
+    auto issue = [&](int lc, Chunk<N, TAU>& q) {
+        issue_chunk<N, TAU, true, !AGG, kLoadStream>(a, w.bb, w.hh, lc < w.nc ? w.c0 + lc : a.C, lane, act, q);
+    };
     bool bad = false;
     if constexpr (PREFETCH) {
         Chunk<N, TAU> qa, qb;
-        issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, wv, lane, act, qa);
-        for (int ch = wv; ch < a.C; ch += 2 * W) {
-            issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch + W, lane, act, qb);
+        issue(wv, qa);
+        for (int lc = wv; lc < w.nc; lc += 2 * W) {
+            issue(lc + W, qb);
             issue_fence();
-            fwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, ch, qa, bad);
-            if (ch + W >= a.C) break;
-            issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch + 2 * W, lane, act, qa);
+            fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc, qa, bad);
+            if (lc + W >= w.nc) break;
+            issue(lc + 2 * W, qa);
             issue_fence();
-            fwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, ch + W, qb, bad);
+            fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc + W, qb, bad);
         }
     } else {
-        for (int ch = wv; ch < a.C; ch += W) {
+        for (int lc = wv; lc < w.nc; lc += W) {
             Chunk<N, TAU> q;
-            issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch, lane, act, q);
-            fwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, ch, q, bad);
+            issue(lc, q);
+            fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc, q, bad);
         }
     }
     if (bad) report_index_error(a.status);
 }
 
-template <int N, int TAU, int W>
+template <int N, int TAU, int W, bool AGG>
 __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     extern __shared__ __align__(16) unsigned char lds[];
     const Smem s = carve_smem(lds, a.lds);
-    const int seq = xcd_seq(a.B * a.H);
-    const int bb = seq / a.H, hh = seq - bb * a.H;
+    const Work w = AGG ? work_of(a, a.S - 1, 0) : work_of(a, a.S, 0);
 
-    stage_tables<N, W>(a, s, hh);
+    stage_tables<N, W>(a, s, w.hh);
     if (threadIdx.x == 0) *s.ready = 0;
     for (int i = threadIdx.x; i < 2 * W; i += blockDim.x) s.aflag[i] = -1;
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
     constexpr bool PF = fused_prefetch(N, TAU);
-    if (fb) fwd_body<N, TAU, W, 7, true, PF>(a, s, seq, bb, hh);
-    else if (G == 1) fwd_body<N, TAU, W, 1, false, PF>(a, s, seq, bb, hh);
-    else if (G == 3) fwd_body<N, TAU, W, 3, false, PF>(a, s, seq, bb, hh);
-    else fwd_body<N, TAU, W, 7, false, PF>(a, s, seq, bb, hh);
+    if (fb) fwd_body<N, TAU, W, 7, true, PF, AGG>(a, s, w);
+    else if (G == 1) fwd_body<N, TAU, W, 1, false, PF, AGG>(a, s, w);
+    else if (G == 3) fwd_body<N, TAU, W, 3, false, PF, AGG>(a, s, w);
+    else fwd_body<N, TAU, W, 7, false, PF, AGG>(a, s, w);
 }
 
 // ================================================================== backward
@@ -899,23 +1003,26 @@ struct BwdChunk {
     float dyv;
 };
 
-// Issues every load of reverse-order chunk r (chunk C-1-r); r >= C issues an
-// empty chunk through the null descriptor, as issue_chunk does.
-template <int N, int TAU>
-__device__ __forceinline__ void issue_bwd(const FusedArgs& a, int seq, int bb, int hh, int r, int lane, bool act,
+// Issues every load of reverse-order local chunk r (chunk c0 + nc - 1 - r);
+// r >= nc issues an empty chunk through the null descriptor, as issue_chunk
+// does.  The aggregate pass needs neither b nor the saved states.
+template <int N, int TAU, bool AGG>
+__device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int r, int lane, bool act,
                                           BwdChunk<N, TAU>& u) {
     constexpr int SL = Lay<N>::SL;
-    const int ch = r < a.C ? a.C - 1 - r : a.C;
-    issue_chunk<N, TAU, true, true, kLoadStream>(a, bb, hh, ch, lane, act, u.q);
+    const int ch = r < w.nc ? w.c0 + w.nc - 1 - r : a.C;
+    issue_chunk<N, TAU, !AGG, true, kLoadStream>(a, w.bb, w.hh, ch, lane, act, u.q);
     const int chc = min(ch, a.C - 1);
     const int s0 = chc * TAU;
     const int lenc = min(TAU, a.L - s0);
-    u.dyv = a.dy[((size_t)bb * a.L + s0 + min(lane, lenc - 1)) * a.H + hh];
-    u.hs = act ? ld_cv<SL>(a.saved + ((size_t)seq * a.C + chc) * N, lane) : cv_zero<SL>();
+    u.dyv = a.dy[((size_t)w.bb * a.L + s0 + min(lane, lenc - 1)) * a.H + w.hh];
+    if constexpr (!AGG) u.hs = act ? ld_cv<SL>(a.saved + ((size_t)w.seq * a.C + chc) * N, lane) : cv_zero<SL>();
 }
 
-template <int N, int TAU, int W, int G, bool FB>
-__device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, int seq, int bb, int hh, int r,
+// AGG: the aggregate pass of a segment -- each chunk's adjoint operator is
+// composed into the running aggregate passed from wave to wave.
+template <int N, int TAU, int W, int G, bool FB, bool AGG>
+__device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int r,
                                           BwdChunk<N, TAU>& u, bool& bad) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
@@ -924,9 +1031,10 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, int
     float2* X = s.x + wv * N;
     uint8_t* PA = s.pa + wv * N;
     const size_t stride = (size_t)a.H * N;
-    const int ch = a.C - 1 - r;
+    const int ch = w.c0 + w.nc - 1 - r;
     const int s0 = ch * TAU;
-    const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
+    const size_t base = (((size_t)w.bb * a.L + s0) * a.H + w.hh) * N;
+    const int seq = w.seq;
     Chunk<N, TAU>& q = u.q;
     finish_chunk<N, TAU>(a, s, lane, q, bad);
     const float dyv = lane < q.len ? u.dyv : 0.f;
@@ -978,6 +1086,38 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, int
         materialize(g.v[i].y);
     }
     wait_ready(s.ready, r, a.status, s.ready, 1);
+    if constexpr (AGG) {
+        // (Gamma, Pi, Delta)_acc <- (gamma_c + Phi_c^H Gamma_acc, Pi_acc[Pi_c], Delta_acc[Pi_c] Delta_c):
+        // the aggregate of chunks c .. c1-1, mapping the gradient entering
+        // the segment's last chunk to the one leaving chunk c.
+        const float2* GA = s.ring + (r & 1) * N;
+        const float2* DA = s.ring + (2 + (r & 1)) * N;
+        const uint8_t* PAc = s.agp + (r & 1) * N;
+        CV<SL> Gn, Dn;
+        IV<SL> Pn;
+        if (act) {
+#pragma unroll
+            for (int i = 0; i < SL; ++i) {
+                const int p = pa.v[i];
+                Gn.v[i] = cadd(g.v[i], cmulc(da.v[i], GA[p]));
+                Dn.v[i] = cmul(DA[p], da.v[i]);
+                Pn.v[i] = PAc[p];
+            }
+            st_cv<SL>(s.ring + ((r + 1) & 1) * N, lane, Gn);
+            st_cv<SL>(s.ring + (2 + ((r + 1) & 1)) * N, lane, Dn);
+#pragma unroll
+            for (int i = 0; i < SL; ++i) s.agp[((r + 1) & 1) * N + lane * SL + i] = (uint8_t)Pn.v[i];
+        }
+        wave_sync();
+        if (lane == 0) publish_ready(s.ready, r + 1);
+        if (r == w.nc - 1 && act) {
+            const size_t sb = ((size_t)seq * a.S + w.sg) * N;
+            st_cv<SL>(a.segA + sb, lane, Gn);
+            st_cv<SL>(a.segD + sb, lane, Dn);
+            st_iv<SL>(a.segP + sb, lane, Pn);
+        }
+        return;
+    }
     CV<SL> U = cv_zero<SL>(), Up;
     if (act) {
         const float2* ring = s.ring + (r & 1) * N;
@@ -1041,80 +1181,135 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, int
     }
 }
 
-// Wave wv owns reverse-order chunks wv, wv+W, ...; with PREFETCH every load of
-// its next chunk is in flight while it computes the current one.
-template <int N, int TAU, int W, int G, bool FB, bool PREFETCH>
-__device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, int seq, int bb, int hh) {
+// Wave wv owns reverse-order local chunks wv, wv+W, ...; with PREFETCH every
+// load of its next chunk is in flight while it computes the current one.
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG>
+__device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     bool bad = false;
     if constexpr (PREFETCH) {
         BwdChunk<N, TAU> ua, ub;
-        issue_bwd<N, TAU>(a, seq, bb, hh, wv, lane, act, ua);
-        for (int r = wv; r < a.C; r += 2 * W) {
-            issue_bwd<N, TAU>(a, seq, bb, hh, r + W, lane, act, ub);
+        issue_bwd<N, TAU, AGG>(a, w, wv, lane, act, ua);
+        for (int r = wv; r < w.nc; r += 2 * W) {
+            issue_bwd<N, TAU, AGG>(a, w, r + W, lane, act, ub);
             issue_fence();
-            bwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, r, ua, bad);
-            if (r + W >= a.C) break;
-            issue_bwd<N, TAU>(a, seq, bb, hh, r + 2 * W, lane, act, ua);
+            bwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, r, ua, bad);
+            if (r + W >= w.nc) break;
+            issue_bwd<N, TAU, AGG>(a, w, r + 2 * W, lane, act, ua);
             issue_fence();
-            bwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, r + W, ub, bad);
+            bwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, r + W, ub, bad);
         }
     } else {
-        for (int r = wv; r < a.C; r += W) {
+        for (int r = wv; r < w.nc; r += W) {
             BwdChunk<N, TAU> u;
-            issue_bwd<N, TAU>(a, seq, bb, hh, r, lane, act, u);
-            bwd_chunk<N, TAU, W, G, FB>(a, s, seq, bb, hh, r, u, bad);
+            issue_bwd<N, TAU, AGG>(a, w, r, lane, act, u);
+            bwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, r, u, bad);
         }
     }
     if (bad) report_index_error(a.status);
 }
 
-template <int N, int TAU, int W>
+// The gradient entering segment w.sg from the right: dh_final (or 0) pulled
+// back through the aggregates of segments S-1 .. w.sg+1,
+// U <- Gamma_s + Phi_s^H U (a gather through the wave's LDS buffer X).
+template <int N>
+__device__ __forceinline__ CV<Lay<N>::SL> seg_enter_bwd(const FusedArgs& a, const Work& w, float2* X, int lane,
+                                                        bool act) {
+    constexpr int SL = Lay<N>::SL;
+    CV<SL> U = cv_zero<SL>();
+    if (a.dhf && act) U = ld_cv<SL>(a.dhf + (size_t)w.seq * N, lane);
+    for (int sp = a.S - 1; sp > w.sg; --sp) {
+        const size_t base = ((size_t)w.seq * a.S + sp) * N;
+        CV<SL> Un = cv_zero<SL>();
+        wave_sync();
+        if (act) st_cv<SL>(X, lane, U);
+        wave_sync();
+        if (act) {
+            const CV<SL> G = ld_cv<SL>(a.segA + base, lane);
+            const CV<SL> d = ld_cv<SL>(a.segD + base, lane);
+            const IV<SL> P = ld_iv<SL>(a.segP + base, lane);
+#pragma unroll
+            for (int i = 0; i < SL; ++i) Un.v[i] = cadd(G.v[i], cmulc(d.v[i], X[P.v[i]]));
+        }
+        U = Un;
+    }
+    return U;
+}
+
+template <int N, int TAU, int W, bool AGG>
 __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     extern __shared__ __align__(16) unsigned char lds[];
     const Smem s = carve_smem(lds, a.lds);
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
-    const int seq = xcd_seq(a.B * a.H);
-    const int bb = seq / a.H, hh = seq - bb * a.H;
+    const Work w = AGG ? work_of(a, a.S - 1, 1) : work_of(a, a.S, 0);
 
-    stage_tables<N, W>(a, s, hh);
+    stage_tables<N, W>(a, s, w.hh);
     if (wv == 0) {
-        CV<SL> u = cv_zero<SL>();
-        if (a.dhf && act) u = ld_cv<SL>(a.dhf + (size_t)seq * N, lane);
-        if (act) st_cv<SL>(s.ring, lane, u);
+        if constexpr (AGG) {
+            // identity aggregate: Gamma = 0, Pi = id, Delta = 1
+            if (act) {
+                st_cv<SL>(s.ring, lane, cv_zero<SL>());
+                CV<SL> one;
+#pragma unroll
+                for (int i = 0; i < SL; ++i) {
+                    one.v[i] = make_float2(1.f, 0.f);
+                    s.agp[lane * SL + i] = (uint8_t)(lane * SL + i);
+                }
+                st_cv<SL>(s.ring + 2 * N, lane, one);
+            }
+        } else {
+            const CV<SL> u = seg_enter_bwd<N>(a, w, s.x, lane, act);
+            if (act) st_cv<SL>(s.ring, lane, u);
+        }
         if (lane == 0) *s.ready = 0;
     }
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
     constexpr bool PF = fused_prefetch(N, TAU);
-    if (fb) bwd_body<N, TAU, W, 7, true, PF>(a, s, seq, bb, hh);
-    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF>(a, s, seq, bb, hh);
-    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF>(a, s, seq, bb, hh);
-    else bwd_body<N, TAU, W, 7, false, PF>(a, s, seq, bb, hh);
+    if (fb) bwd_body<N, TAU, W, 7, true, PF, AGG>(a, s, w);
+    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF, AGG>(a, s, w);
+    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF, AGG>(a, s, w);
+    else bwd_body<N, TAU, W, 7, false, PF, AGG>(a, s, w);
 }
 
+// Segmented scans (S > 1) first run the aggregate pass over segments that
+// have a neighbour to hand to, then the scan over every segment.
 template <int N, int TAU, int W>
 hipError_t fwd_launch(const FusedArgs& a, hipStream_t st) {
-    auto kern = k_fwd_fused<N, TAU, W>;
+    if (a.S > 1) {
+        auto agg = k_fwd_fused<N, TAU, W, true>;
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(agg),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3((W + 1) * 64), a.lds.total, st, a);
+    }
+    auto kern = k_fwd_fused<N, TAU, W, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3((W + 1) * 64), a.lds.total, st, a);
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H * a.S), dim3((W + 1) * 64), a.lds.total, st, a);
     return hipGetLastError();
 }
 
 template <int N, int TAU, int W>
 hipError_t bwd_launch(const FusedArgs& a, hipStream_t st) {
-    auto kern = k_bwd_fused<N, TAU, W>;
+    if (a.S > 1) {
+        auto agg = k_bwd_fused<N, TAU, W, true>;
+        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(agg),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3(W * 64), a.lds.total, st, a);
+    }
+    auto kern = k_bwd_fused<N, TAU, W, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(a.B * a.H), dim3(W * 64), a.lds.total, st, a);
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H * a.S), dim3(W * 64), a.lds.total, st, a);
     return hipGetLastError();
 }
 

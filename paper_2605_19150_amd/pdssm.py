@@ -36,7 +36,7 @@ class Desc(ctypes.Structure):
 
 
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
-           "pdssm_uses_fused", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
+           "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
            "pdssm_scan_bwd", "pdssm_compose_chunks")
 
 
@@ -60,6 +60,7 @@ def load():
     L.pdssm_workspace_size.argtypes, L.pdssm_workspace_size.restype = [D, I], Z
     L.pdssm_status_string.argtypes, L.pdssm_status_string.restype = [I], ctypes.c_char_p
     L.pdssm_uses_fused.argtypes, L.pdssm_uses_fused.restype = [D], I
+    L.pdssm_scan_segments.argtypes, L.pdssm_scan_segments.restype = [D], I
     L.pdssm_prepare.argtypes, L.pdssm_prepare.restype = [D, P, P, Z, P, P], I
     L.pdssm_scan_fwd.argtypes = [D] + [P] * 10 + [Z, P, P]
     L.pdssm_scan_fwd.restype = I
@@ -79,6 +80,10 @@ def status_string(st):
 
 def desc(B, L, H, N, K, chunk=0):
     return Desc(int(B), int(L), int(H), int(N), int(K), int(chunk), 0)
+
+
+def scan_segments(d):
+    return load().pdssm_scan_segments(ctypes.byref(d))
 
 
 def chunk_len(d):
@@ -156,6 +161,7 @@ class Scan:
             raise PdssmError(self.C, "num_chunks")
         self.chunk = chunk_len(self.d)
         self.fused = load().pdssm_uses_fused(ctypes.byref(self.d)) == 1
+        self.segments = load().pdssm_scan_segments(ctypes.byref(self.d))
         dev = self.device
         nws = max(workspace_size(self.d, OP_FWD), workspace_size(self.d, OP_BWD), 1)
         self.ws = torch.empty(nws, dtype=torch.uint8, device=dev)

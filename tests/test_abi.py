@@ -52,6 +52,11 @@ def test_chunk_and_workspace_queries(lib):
     assert pdssm.workspace_size(d, pdssm.OP_COMPOSE) == 0
     d = pdssm.desc(1, 1, 1, 8, 1)
     assert pdssm.num_chunks(d) == 1
+    # few long sequences are cut into segments; many sequences are not
+    assert pdssm.scan_segments(pdssm.desc(8, 18000, 8, 128, 32)) == 4
+    assert pdssm.scan_segments(pdssm.desc(16, 2048, 16, 64, 16)) == 1
+    assert pdssm.scan_segments(pdssm.desc(1, 1000, 2, 64, 16)) == 3
+    assert pdssm.scan_segments(pdssm.desc(1, 100, 2, 64, 16)) == 1
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -198,6 +198,21 @@ def test_prepared_tables_match_per_call_build(N, K, pi_kind):
     check_all(inp2, got, s.chunk)
 
 
+@pytest.mark.parametrize("N,chunk,L,B,H,pi_kind", [
+    (64, 8, 1000, 1, 2, "perm"), (64, 8, 1003, 1, 2, "uniform"), (128, 4, 701, 1, 3, "uniform"),
+    (8, 8, 2100, 1, 1, "uniform"), (128, 8, 1100, 1, 1, "perm"), (32, 16, 1500, 2, 1, "uniform")])
+def test_segmented_scan(N, chunk, L, B, H, pi_kind):
+    """Few long sequences run cut into segments along L (an aggregate pass,
+    then one workgroup per segment); results match the oracle like the
+    unsegmented scan, including the saved chunk states, h_final and dh0."""
+    d = pdssm.desc(B, L, H, N, 5, chunk)
+    assert pdssm.scan_segments(d) > 1
+    inp = make_inputs(B=B, L=L, H=H, N=N, K=5, seed=L + N, pi_kind=pi_kind, with_h0=True,
+                      with_dhf=True)
+    got = run_gpu(inp, chunk=chunk)
+    check_all(inp, got, chunk)
+
+
 def _guarded(shape, dtype, pad=4096):
     """An output tensor inside a larger buffer whose margins hold a marker."""
     n = int(np.prod(shape))
