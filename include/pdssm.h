@@ -52,7 +52,7 @@
  *   - Supported sizes: N in {8, 16, 32, 64, 128, 256}; 1 <= K <= 256;
  *     B, L, H >= 1 with B*L*H*N < 2^31.  For scan_fwd / scan_bwd the chunk is
  *     4, 8 or 16 steps with chunk * max(1, N/64) <= 16, or 0 for the default
- *     (8 for N <= 64, 4 for N >= 128); pdssm_compose_chunks takes any chunk
+ *     (8 for N <= 128, 4 for N = 256); pdssm_compose_chunks takes any chunk
  *     >= 1 (0 = 32).  One head's dictionary tables, (K+1)*N*9 bytes plus the
  *     per-wave buffers, are staged in the 160 KiB LDS of a workgroup; larger
  *     dictionaries run slower multi-pass kernels with the same results.

@@ -41,11 +41,12 @@ def test_chunk_and_workspace_queries(lib):
     assert pdssm.num_chunks(d) == 256
     assert pdssm.num_chunks(pdssm.desc(16, 2048, 16, 64, 16, chunk=16)) == 128
     d = pdssm.desc(8, 18000, 8, 128, 32)
-    assert pdssm.chunk_len(d) == 4
-    assert pdssm.num_chunks(d) == 4500
-    assert pdssm.num_chunks(pdssm.desc(8, 18000, 8, 128, 32, chunk=8)) == 2250
+    assert pdssm.chunk_len(d) == 8
+    assert pdssm.num_chunks(d) == 2250
+    assert pdssm.num_chunks(pdssm.desc(8, 18000, 8, 128, 32, chunk=4)) == 4500
     assert pdssm.num_chunks(pdssm.desc(8, 18000, 8, 128, 32, chunk=16)) == pdssm.ERR_UNSUPPORTED
     assert pdssm.chunk_len(pdssm.desc(1, 10, 1, 256, 4)) == 4
+    assert pdssm.chunk_len(pdssm.desc(1, 10, 1, 128, 4)) == 8
     for op in (pdssm.OP_FWD, pdssm.OP_BWD):
         n = pdssm.workspace_size(d, op)
         assert n >= 8 * 32 * 128 * 9  # dictionary tables of the fused path
