@@ -97,6 +97,19 @@ pdssm::LdsLayout fused_layout(const pdssm_desc* d, int tau, bool fwd) {
     return pdssm::fused_lds_layout(d->N, d->K, W);
 }
 
+// Saved-state rows the forward stages in LDS before writing them out in one
+// burst: stores of chunk states interleaved with the row loads cost far more
+// HBM time than the same bytes written together.  As many rows as the free
+// LDS holds (up to a whole sequence), at least 16, else none.
+constexpr int kMinStaging = 16;
+
+int staging_rows(const pdssm_desc* d, const pdssm::LdsLayout& l, int C) {
+    if (l.total >= pdssm::kMaxLds) return 0;
+    long long m = (long long)(pdssm::kMaxLds - l.total) / ((long long)d->N * 8);
+    if (m > C) m = C;
+    return m >= kMinStaging ? (int)m : 0;
+}
+
 bool use_fused(const pdssm_desc* d) {
     const int tau = scan_chunk(d);
     return fused_layout(d, tau, true).total <= pdssm::kMaxLds && fused_layout(d, tau, false).total <= pdssm::kMaxLds;
@@ -192,6 +205,8 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     f.rec = pa.rec;
     f.mtab = pa.mtab;
     f.lds = fused_layout(d, f.tau, fwd);
+    f.sbM = fwd ? staging_rows(d, f.lds, f.C) : 0;
+    f.lds = pdssm::fused_lds_add_staging(f.lds, d->N, f.sbM);
     const Segs g = segments(d, f.C);
     f.S = g.S;
     f.Cs = g.Cs;

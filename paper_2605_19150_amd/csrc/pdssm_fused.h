@@ -26,7 +26,7 @@ constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? 
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
-    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, agm, aflag, vd, x, cs, pa, total;
+    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, agm, aflag, vd, x, cs, pa, sb, total;
 };
 
 inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
@@ -58,9 +58,17 @@ inline LdsLayout fused_lds_layout(int N, int K, int W) {
     l.agm = (uint32_t)o;   o += align16((size_t)2 * W * N);
     l.vd = (uint32_t)o;    o += (size_t)W * (N + 1) * 16;
     l.x = (uint32_t)o;     o += (size_t)(W + 1) * N * 8;
-    l.cs = (uint32_t)o;    o += (size_t)W * N * 8;
+    l.cs = (uint32_t)o;    o += (size_t)2 * W * N * 8;
     l.pa = (uint32_t)o;    o += align16((size_t)W * N);
+    l.sb = (uint32_t)o;    // saved-state staging, sized by the caller (fused_lds_add_staging)
     l.total = (uint32_t)o;
+    return l;
+}
+
+// Adds M saved-state rows of staging to a layout (the forward writes chunk
+// states there and flushes them to HBM in bursts of M rows).
+inline LdsLayout fused_lds_add_staging(LdsLayout l, int N, int M) {
+    l.total = l.sb + (uint32_t)((size_t)M * N * 8);
     return l;
 }
 
@@ -104,6 +112,7 @@ struct FusedArgs {
     // (forward: local state, map, diagonal; backward: local adjoint, map,
     // diagonal), [B*H][S][N] each.  S = 1: one workgroup per sequence.
     int S, Cs;
+    int sbM;  // saved-state rows staged in LDS by the forward (0: stored as computed)
     float2* segA;
     float2* segD;
     int* segP;

@@ -133,8 +133,9 @@ struct Smem {
     int* aflag;     // [2W] chunk id held by each operator slot
     float4* vd;     // [W][N+1]
     float2* x;      // [W][N]
-    float2* cs;     // [W][N] (forward: staged c_t)
+    float2* cs;     // [W][2][N] (forward: staged c_t, two steps)
     uint8_t* pa;    // [W][N] (backward)
+    float2* sb;     // [sbM][N] forward: staged saved states
 };
 
 __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout& l) {
@@ -154,6 +155,7 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
     s.x = reinterpret_cast<float2*>(base + l.x);
     s.cs = reinterpret_cast<float2*>(base + l.cs);
     s.pa = base + l.pa;
+    s.sb = reinterpret_cast<float2*>(base + l.sb);
     return s;
 }
 
@@ -257,6 +259,21 @@ __device__ __forceinline__ void gather_rows(const float4* vd, const uint64_t* re
             acc.v[s].x += v.x;
             acc.v[s].y += v.y;
         }
+    }
+}
+
+// acc += sum over the G listed sources of V (the .xy half of vd rows), for a
+// record already in registers.
+template <int G>
+__device__ __forceinline__ void gather_rec(const float4* vd, uint64_t r, float2& acc) {
+    const float2* V = reinterpret_cast<const float2*>(vd);
+    const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
+#pragma unroll
+    for (int m = 0; m < G; ++m) {
+        const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
+        const float2 v = V[2 * src];
+        acc.x += v.x;
+        acc.y += v.y;
     }
 }
 
@@ -662,7 +679,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     const int ch = w.c0 + lc;
     float4* vd = s.vd + wv * (N + 1);
     float2* X = s.x + wv * N;
-    float2* CS = s.cs + wv * N;
+    float2* CS = s.cs + wv * N;  // buffer 0; buffer 1 is W*N further
     finish_chunk<N, TAU>(a, s, lane, q, bad);
 
     // ---- 2. one pass: local state B, chunk operator (Pi, Delta), w_t, local readout
@@ -675,33 +692,95 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     }
     CV<SL> wt[TAU];
     float yl[TAU];
+    if constexpr (!FB && Sentinel<N>::kZeroRow) {
+        // Pipelined form: every step's gather records are read at chunk start;
+        // step t then issues one batch of LDS reads -- its gathers, D_t and
+        // pi_t at Pi_{t-1}, and c_{t-1} at Pi_{t-1} for w_{t-1} (c staged in
+        // two alternating buffers) -- so each step waits for one round trip.
+        uint64_t rec[TAU][SL];
 #pragma unroll
-    for (int t = 0; t < TAU; ++t) {
-        const int k = readlane_i(q.kv, t);
-        const int M = FB ? readlane_i(q.mv, t) : 0;
-        if (!AGG && act) {
-            wave_sync();
+        for (int t = 0; t < TAU; ++t) {
+            const int k = readlane_i(q.kv, t);
 #pragma unroll
-            for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
+            for (int r = 0; r < SL; ++r) rec[t][r] = act ? s.rec[(size_t)k * N + lane * SL + r] : 0;
         }
-        pd_step<N, G, FB, true>(s, vd, X, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
-        float part = 0.f;
-        if (act) {
 #pragma unroll
-            for (int r = 0; r < SL; ++r) {
-                // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in vd.zw
-                const int p = pm.v[r];
-                dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
-                pm.v[r] = s.dict[k * N + p];
-                if constexpr (!AGG) {
-                    wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
-                    part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+        for (int t = 0; t < TAU; ++t) {
+            const int k = readlane_i(q.kv, t);
+            float2* CSt = CS + (t & 1) * (W * N);
+            const float2* CSp = CS + ((t + 1) & 1) * (W * N);
+            const CV<SL> Dv = Dt(q, t);
+            wave_sync();
+            if (act) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
+                    const float2 v = cmul(Dv.v[r], Bm.v[r]);
+                    vd[lane * SL + r] = make_float4(v.x, v.y, Dv.v[r].x, Dv.v[r].y);
                 }
             }
-        } else if constexpr (!AGG) {
-            wt[t] = cv_zero<SL>();
+            wave_sync();
+            float part = 0.f;
+            if (act) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    float2 acc = q.b[t].v[r];
+                    gather_rec<G>(vd, rec[t][r], acc);
+                    const int p = pm.v[r];
+                    const float2 Dp = reinterpret_cast<const float2*>(vd)[2 * p + 1];
+                    const int np = s.dict[k * N + p];
+                    if constexpr (!AGG) {
+                        if (t > 0) wt[t - 1].v[r] = cmul(dm.v[r], CSp[p]);
+                    }
+                    Bm.v[r] = acc;
+                    dm.v[r] = cmul(Dp, dm.v[r]);
+                    pm.v[r] = np;
+                    if constexpr (!AGG) part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+                }
+            } else if constexpr (!AGG) {
+                if (t > 0) wt[t - 1] = cv_zero<SL>();
+            }
+            yl[t] = part;
         }
-        yl[t] = part;
+        if constexpr (!AGG) {
+            const float2* CSl = CS + ((TAU - 1) & 1) * (W * N);
+            wave_sync();
+            if (act) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) wt[TAU - 1].v[r] = cmul(dm.v[r], CSl[pm.v[r]]);
+            } else {
+                wt[TAU - 1] = cv_zero<SL>();
+            }
+        }
+    } else {
+#pragma unroll
+        for (int t = 0; t < TAU; ++t) {
+            const int k = readlane_i(q.kv, t);
+            const int M = FB ? readlane_i(q.mv, t) : 0;
+            if (!AGG && act) {
+                wave_sync();
+#pragma unroll
+                for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
+            }
+            pd_step<N, G, FB, true>(s, vd, X, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
+            float part = 0.f;
+            if (act) {
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in vd.zw
+                    const int p = pm.v[r];
+                    dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
+                    pm.v[r] = s.dict[k * N + p];
+                    if constexpr (!AGG) {
+                        wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
+                        part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+                    }
+                }
+            } else if constexpr (!AGG) {
+                wt[t] = cv_zero<SL>();
+            }
+            yl[t] = part;
+        }
     }
 
     // ---- 3. publish the chunk operator for the frontier wave, take carry_c.
@@ -732,7 +811,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * W);
     CV<SL> carry = cv_zero<SL>();
     if (act) carry = ld_cv<SL>(s.ring + (lc % (W + 1)) * N, lane);
-    if (act && a.saved) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
+    if (act && a.saved && a.sbM == 0) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
 
     // ---- 4. readout correction with the true carry, then one store per chunk
 #pragma unroll
@@ -864,9 +943,16 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     __builtin_amdgcn_s_setprio(3);
     wait_ready(s.aflag, 0, a.status, flags, nflags);
     ChunkOp<SL> op = read_op<N, !kPerm>(s, 0, lane, act);
+    const int M = AGG || !a.saved ? 0 : a.sbM;
     for (int c = 0; c < w.nc; ++c) {
         wave_sync();
         if (!AGG && act) st_cv<SL>(s.ring + (c % (W + 1)) * N, lane, carry);
+        if (M > 0 && act) {
+            // the first M chunk states wait in LDS until the whole workgroup
+            // has read its rows; later ones (near the end anyway) go out now
+            if (c < M) st_cv<SL>(s.sb + c * N, lane, carry);
+            else st_cv<SL>(a.saved + ((size_t)w.seq * a.C + w.c0 + c) * N, lane, carry);
+        }
         CV<SL> nxt;
         if constexpr (kPerm) {
             // every entry is a permutation, so is Pi_c: scatter by plain stores
@@ -985,6 +1071,19 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     else if (G == 1) fwd_body<N, TAU, W, 1, false, PF, AGG>(a, s, w);
     else if (G == 3) fwd_body<N, TAU, W, 3, false, PF, AGG>(a, s, w);
     else fwd_body<N, TAU, W, 7, false, PF, AGG>(a, s, w);
+    if constexpr (!AGG) {
+        // write out the staged chunk states, every wave a share of the rows
+        if (a.sbM > 0 && a.saved) {
+            constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+            const int lane = lane_id();
+            __syncthreads();
+            const int rows = min(a.sbM, w.nc);
+            float2* dst = a.saved + ((size_t)w.seq * a.C + w.c0) * N;
+            if (lane < LANES)
+                for (int i = wave_id(); i < rows; i += W + 1)
+                    st_cv<SL>(dst + (size_t)i * N, lane, ld_cv<SL>(s.sb + i * N, lane));
+        }
+    }
 }
 
 // ================================================================== backward
