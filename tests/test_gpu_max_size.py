@@ -1,0 +1,87 @@
+"""GPU: the largest problem the ABI accepts (B*L*H*N just below 2^31 complex
+entries, 17 GB per [B,L,H,N] tensor), on the automaton embedding of App. D
+so that the forward can be checked bit for bit against an integer
+simulation at every step.  It exercises 64-bit offsets, a ragged last chunk
+and the segmented scan (16 sequences)."""
+import numpy as np
+import pytest
+
+from oracle import oracle_bwd
+from helpers import assert_close
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU machines, never run there
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2605_19150_amd import pdssm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def _simulate(P, idx_h, q0):
+    """Integer automaton run: state after every step (App. D)."""
+    Pl = P.tolist()
+    states = [0] * len(idx_h)
+    q = int(q0)
+    for t, k in enumerate(idx_h.tolist()):
+        q = Pl[k][q]
+        states[t] = q
+    return np.asarray(states, np.int64)
+
+
+def test_largest_problem_automaton():
+    B, H, N, K = 1, 16, 64, 16
+    L = (2**31 - 1) // (B * H * N)  # 2097151 steps: B*L*H*N = 2^31 - 1024
+    d = pdssm.desc(B, L, H, N, K)
+    assert pdssm.num_chunks(d) > 0
+    print("largest problem: B=%d L=%d H=%d N=%d, %d segments" % (B, L, H, N, pdssm.scan_segments(d)),
+          flush=True)
+    rng = np.random.default_rng(7)
+    idx = rng.integers(0, K, size=(B, L, H), dtype=np.int32)
+    pi = rng.integers(0, N, size=(H, K, N)).astype(np.int32)
+    start = rng.integers(0, N, size=(B, H))
+    acc = (rng.random((H, N)) < 0.5).astype(np.float32)
+    dy = rng.standard_normal((B, L, H), dtype=np.float32)
+
+    idx_d = torch.from_numpy(idx).to(DEV)
+    pi_d = torch.from_numpy(pi).to(DEV)
+    shape = (B, L, H, N)
+    D = torch.ones(shape, dtype=torch.complex64, device=DEV)
+    b = torch.zeros(shape, dtype=torch.complex64, device=DEV)
+    c = torch.from_numpy(acc).to(DEV).to(torch.complex64).expand(shape).contiguous()
+    h0 = torch.zeros((B, H, N), dtype=torch.complex64, device=DEV)
+    h0[0, torch.arange(H), torch.from_numpy(start[0]).to(DEV)] = 1.0
+    dy_d = torch.from_numpy(dy).to(DEV)
+
+    s = pdssm.Scan(B, L, H, N, K)
+    s.prepare(pi_d)
+    s.fwd(idx_d, pi_d, D, b, c, h0=h0)
+    s.bwd(idx_d, pi_d, D, b, c, dy_d)
+    s.check_status()
+
+    T = 2048  # tail window for the gradient check
+    for hh in (0, H - 1):
+        st = _simulate(pi[hh], idx[0, :, hh], start[0, hh])
+        y = s.y[0, :, hh].cpu().numpy()
+        np.testing.assert_array_equal(y, acc[hh][st], err_msg="y, head %d" % hh)
+        hf = s.h_final[0, hh].cpu().numpy()
+        ref = np.zeros(N, np.complex64)
+        ref[st[-1]] = 1.0
+        np.testing.assert_array_equal(hf, ref, err_msg="h_final, head %d" % hh)
+        # gradients of the last T steps only depend on those steps
+        t0 = L - T
+        h_in = np.zeros((1, 1, N), np.complex128)
+        h_in[0, 0, st[t0 - 1]] = 1.0
+        sub_idx = np.ascontiguousarray(idx[:, t0:, hh:hh + 1])
+        ones = np.ones((1, T, 1, N), np.complex128)
+        zeros = np.zeros((1, T, 1, N), np.complex128)
+        cc = np.broadcast_to(acc[hh].astype(np.complex128), (1, T, 1, N)).copy()
+        rdD, rdb, rdc, _ = oracle_bwd(sub_idx, pi[hh:hh + 1], ones, zeros, cc,
+                                      np.ascontiguousarray(dy[:, t0:, hh:hh + 1]), h0=h_in)
+        assert_close("db tail", s.db[:, t0:, hh:hh + 1].cpu().numpy(), rdb)
+        assert_close("dc tail", s.dc[:, t0:, hh:hh + 1].cpu().numpy(), rdc)
+        assert_close("dD tail", s.dD[:, t0:, hh:hh + 1].cpu().numpy(), rdD)
+    del s, D, b, c, idx_d, pi_d, h0, dy_d
+    torch.cuda.empty_cache()
