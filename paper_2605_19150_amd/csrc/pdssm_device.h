@@ -258,13 +258,4 @@ __device__ __forceinline__ void pd_scatter_step(float2* X, int lane, bool act,
     if (act) x = ld_cv<SL>(X, lane);
 }
 
-// Gather: out[j] = V[pt[j]] where V is the wave's staged N-vector in LDS.
-template <int N>
-__device__ __forceinline__ CV<Lay<N>::SL> gather_cv(const float2* V, const IV<Lay<N>::SL>& pt) {
-    CV<Lay<N>::SL> r;
-#pragma unroll
-    for (int s = 0; s < Lay<N>::SL; ++s) r.v[s] = V[pt.v[s]];
-    return r;
-}
-
 }  // namespace pdssm

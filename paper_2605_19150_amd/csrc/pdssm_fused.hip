@@ -1,7 +1,9 @@
 // pdssm_fused.hip -- single-read fused PD scan for gfx950.
 //
-// Layout of the work.  One workgroup owns one (batch, head) sequence.  The
-// sequence is cut into chunks of TAU steps (App. E.1 Algorithm 1).
+// Layout of the work.  One workgroup owns one (batch, head) sequence, or one
+// segment of it when there are too few sequences to fill the chip (see the
+// work units below).  The sequence is cut into chunks of TAU steps (App. E.1
+// Algorithm 1).
 //
 // Forward: W chunk waves plus one frontier wave.  Chunk wave w takes chunks
 // w, w+W, w+2W, ...; for each chunk it
@@ -17,8 +19,10 @@
 //      keeps the running state in registers, applies
 //      carry_{c+1} = B_c + (Pi_c, Delta_c) carry_c (Phase B) and hands carry_c
 //      back through an LDS ring;
-//   4. finishes y_t = Re<c_t, x_t^loc> + Re sum_j w_t[j] carry_c[j] and
-//      stores carry_c as the chunk's saved state; h_t never reaches memory.
+//   4. finishes y_t = Re<c_t, x_t^loc> + Re sum_j w_t[j] carry_c[j]; h_t
+//      never reaches memory.  The frontier keeps the chunk-entering states
+//      (the saved states) in LDS and the workgroup writes them out once all
+//      its rows are read.
 // Backward: W waves, chunks in reverse order, the adjoint recurrence (a
 // gather: g_{t-1}[j] = conj(D_t[j]) g_t[pi_t[j]] + readout term) folded the
 // same way, the chunk-to-chunk hand-off passed wave to wave, and the chunk's
@@ -400,12 +404,6 @@ __device__ __forceinline__ void finish_chunk(const FusedArgs& a, const Smem& s, 
     q.mv = s.mtab[q.kv];
 }
 
-template <int N, int TAU, bool LOAD_B, bool LOAD_C>
-__device__ __forceinline__ void load_chunk(const FusedArgs& a, const Smem& s, int bb, int hh, int ch,
-                                           int lane, bool act, Chunk<N, TAU>& q, bool& bad) {
-    issue_chunk<N, TAU, LOAD_B, LOAD_C>(a, bb, hh, ch, lane, act, q);
-    finish_chunk<N, TAU>(a, s, lane, q, bad);
-}
 
 // ================================================================== forward
 // Cross-lane exchange primitives for the reduction below (VALU only, no LDS):
