@@ -53,7 +53,7 @@ namespace {
 constexpr int kMaxSrc = 7;          // sources per row record
 constexpr unsigned kFallback = 255; // mtab value: entry needs the atomic scatter
 
-// Unused source slots: row N of the wave's vd block (kept zero) when it fits
+// Unused source slots: row N of the wave's staged values V (kept zero) when it fits
 // in a byte; for N = 256 the in-degree byte masks them instead.
 template <int N>
 struct Sentinel {
@@ -135,7 +135,7 @@ struct Smem {
     uint8_t* agh;   // [2W][N] 1 where a sorted position starts a destination's run
     uint8_t* agm;   // [2W][N] the chunk map itself (aggregate pass)
     int* aflag;     // [2W] chunk id held by each operator slot
-    float4* vd;     // [W][N+1]
+    float4* vd;     // [W][N+1] per wave: staged values V[N+1], then Z[N+1] (see Stage)
     float2* x;      // [W][N]
     float2* cs;     // [W][2][N] (forward: staged c_t, two steps)
     uint8_t* pa;    // [W][N] (backward)
@@ -163,6 +163,21 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
     return s;
 }
 
+// A wave's staging rows: values V[0..N] (V[N] stays zero, the target of
+// unused gather slots) and a second operand Z[0..N] (D_t, or the backward's
+// diagonal), as two arrays of 8-byte words so that a 64-lane gather from V
+// spreads over all 32 bank pairs.
+struct Stage {
+    float2* V;
+    float2* Z;
+};
+
+template <int N>
+__device__ __forceinline__ Stage stage_of(const Smem& s, int wv) {
+    float2* base = reinterpret_cast<float2*>(s.vd + wv * (N + 1));
+    return Stage{base, base + N + 1};
+}
+
 // Copy head hh's dictionary tables into LDS, append the identity entry and
 // clear every wave's zero row (all threads; a barrier follows).
 template <int N, int W>
@@ -184,7 +199,7 @@ __device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, 
         s.dict[K * N + j] = (uint8_t)j;
     }
     if (tid == 0) s.mtab[K] = 1;
-    for (int w = tid; w < W; w += nthr) s.vd[w * (N + 1) + N] = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int w = tid; w < W; w += nthr) reinterpret_cast<float2*>(s.vd + w * (N + 1))[N] = make_float2(0.f, 0.f);
 }
 
 // Gather variant of a head: the smallest of 1, 3, 7 sources covering every
@@ -242,12 +257,11 @@ __device__ __forceinline__ void publish_ready(int* ready, int v) {
 }
 
 // acc[j] += sum of V[src] over the G listed sources of destination row j;
-// V = the .xy half of the wave's vd rows.  Straight-line: G reads, no tests.
+// V = the wave's staged values.  Straight-line: G reads, no tests.
 template <int N, int G>
-__device__ __forceinline__ void gather_rows(const float4* vd, const uint64_t* recrow, int lane,
+__device__ __forceinline__ void gather_rows(const float2* V, const uint64_t* recrow, int lane,
                                             CV<Lay<N>::SL>& acc) {
     constexpr int SL = Lay<N>::SL;
-    const float2* V = reinterpret_cast<const float2*>(vd);
 #pragma unroll
     for (int s = 0; s < SL; ++s) {
         const uint64_t r = recrow[lane * SL + s];
@@ -255,7 +269,7 @@ __device__ __forceinline__ void gather_rows(const float4* vd, const uint64_t* re
 #pragma unroll
         for (int m = 0; m < G; ++m) {
             const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
-            float2 v = V[2 * src];
+            float2 v = V[src];
             if constexpr (!Sentinel<N>::kZeroRow) {
                 const bool use = m < (int)(hi >> 24);
                 v = use ? v : make_float2(0.f, 0.f);
@@ -266,16 +280,15 @@ __device__ __forceinline__ void gather_rows(const float4* vd, const uint64_t* re
     }
 }
 
-// acc += sum over the G listed sources of V (the .xy half of vd rows), for a
-// record already in registers.
+// acc += sum over the G listed sources of the staged values V, for a record
+// already in registers.
 template <int G>
-__device__ __forceinline__ void gather_rec(const float4* vd, uint64_t r, float2& acc) {
-    const float2* V = reinterpret_cast<const float2*>(vd);
+__device__ __forceinline__ void gather_rec(const float2* V, uint64_t r, float2& acc) {
     const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
 #pragma unroll
     for (int m = 0; m < G; ++m) {
         const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
-        const float2 v = V[2 * src];
+        const float2 v = V[src];
         acc.x += v.x;
         acc.y += v.y;
     }
@@ -290,10 +303,10 @@ struct Chunk {
 };
 
 // One step h <- bt + P(k) (Dt .* h).  With STAGE_D the step also leaves D_t
-// in vd.zw for a map composition.  FB: the head has entries that need the
+// in Z for a map composition.  FB: the head has entries that need the
 // atomic scatter, tested per step.
 template <int N, int G, bool FB, bool STAGE_D>
-__device__ __forceinline__ void pd_step(const Smem& s, float4* vd, float2* X, int lane, bool act,
+__device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, float2* X, int lane, bool act,
                                         int k, int M, CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt,
                                         const CV<Lay<N>::SL>& bt) {
     constexpr int SL = Lay<N>::SL;
@@ -304,7 +317,7 @@ __device__ __forceinline__ void pd_step(const Smem& s, float4* vd, float2* X, in
                 if (act) {
 #pragma unroll
                     for (int q = 0; q < SL; ++q)
-                        reinterpret_cast<float2*>(vd)[2 * (lane * SL + q) + 1] = Dt.v[q];
+                        st.Z[lane * SL + q] = Dt.v[q];
                 }
             }
             IV<SL> pt;
@@ -321,16 +334,14 @@ __device__ __forceinline__ void pd_step(const Smem& s, float4* vd, float2* X, in
 #pragma unroll
         for (int q = 0; q < SL; ++q) {
             const float2 v = cmul(Dt.v[q], h.v[q]);
-            if constexpr (STAGE_D)
-                vd[lane * SL + q] = make_float4(v.x, v.y, Dt.v[q].x, Dt.v[q].y);
-            else
-                reinterpret_cast<float2*>(vd)[2 * (lane * SL + q)] = v;
+            st.V[lane * SL + q] = v;
+            if constexpr (STAGE_D) st.Z[lane * SL + q] = Dt.v[q];
         }
     }
     wave_sync();
     if (act) {
         CV<SL> acc = bt;
-        gather_rows<N, G>(vd, s.rec + (size_t)k * N, lane, acc);
+        gather_rows<N, G>(st.V, s.rec + (size_t)k * N, lane, acc);
         h = acc;
     }
 }
@@ -675,7 +686,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     const int ch = w.c0 + lc;
-    float4* vd = s.vd + wv * (N + 1);
+    const Stage st = stage_of<N>(s, wv);
     float2* X = s.x + wv * N;
     float2* CS = s.cs + wv * N;  // buffer 0; buffer 1 is W*N further
     finish_chunk<N, TAU>(a, s, lane, q, bad);
@@ -714,7 +725,8 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                 for (int r = 0; r < SL; ++r) {
                     if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
                     const float2 v = cmul(Dv.v[r], Bm.v[r]);
-                    vd[lane * SL + r] = make_float4(v.x, v.y, Dv.v[r].x, Dv.v[r].y);
+                    st.V[lane * SL + r] = v;
+                    st.Z[lane * SL + r] = Dv.v[r];
                 }
             }
             wave_sync();
@@ -723,9 +735,9 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
                     float2 acc = q.b[t].v[r];
-                    gather_rec<G>(vd, rec[t][r], acc);
+                    gather_rec<G>(st.V, rec[t][r], acc);
                     const int p = pm.v[r];
-                    const float2 Dp = reinterpret_cast<const float2*>(vd)[2 * p + 1];
+                    const float2 Dp = st.Z[p];
                     const int np = s.dict[k * N + p];
                     if constexpr (!AGG) {
                         if (t > 0) wt[t - 1].v[r] = cmul(dm.v[r], CSp[p]);
@@ -760,14 +772,14 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
                 for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
             }
-            pd_step<N, G, FB, true>(s, vd, X, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
+            pd_step<N, G, FB, true>(s, st, X, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
             float part = 0.f;
             if (act) {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
-                    // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in vd.zw
+                    // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in Z
                     const int p = pm.v[r];
-                    dm.v[r] = cmul(reinterpret_cast<const float2*>(vd)[2 * p + 1], dm.v[r]);
+                    dm.v[r] = cmul(st.Z[p], dm.v[r]);
                     pm.v[r] = s.dict[k * N + p];
                     if constexpr (!AGG) {
                         wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
@@ -1124,7 +1136,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
-    float4* vd = s.vd + wv * (N + 1);
+    const Stage st = stage_of<N>(s, wv);
     float2* X = s.x + wv * N;
     uint8_t* PA = s.pa + wv * N;
     const size_t stride = (size_t)a.H * N;
@@ -1157,7 +1169,8 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
                 pt.v[i] = s.dict[k * N + lane * SL + i];
                 g.v[i].x += dyt * q.c[t].v[i].x;
                 g.v[i].y -= dyt * q.c[t].v[i].y;
-                vd[lane * SL + i] = make_float4(g.v[i].x, g.v[i].y, da.v[i].x, da.v[i].y);
+                st.V[lane * SL + i] = g.v[i];
+                st.Z[lane * SL + i] = da.v[i];
                 PA[lane * SL + i] = (uint8_t)pa.v[i];
             }
         }
@@ -1165,10 +1178,10 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
         if (act) {
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
-                const float4 e = vd[pt.v[i]];
+                const float2 gv = st.V[pt.v[i]], dz = st.Z[pt.v[i]];
                 pa.v[i] = PA[pt.v[i]];
-                da.v[i] = cmul(make_float2(e.z, e.w), Dt(q, t).v[i]);
-                g.v[i] = cmulc(Dt(q, t).v[i], make_float2(e.x, e.y));
+                da.v[i] = cmul(dz, Dt(q, t).v[i]);
+                g.v[i] = cmulc(Dt(q, t).v[i], gv);
             }
         }
     }
@@ -1235,7 +1248,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
     for (int t = 0; t < TAU; ++t) {
         const int k = readlane_i(q.kv, t);
         const int M = FB ? readlane_i(q.mv, t) : 0;
-        pd_step<N, G, FB, false>(s, vd, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
+        pd_step<N, G, FB, false>(s, st, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
         Hs[t + 1] = hs;
     }
 
@@ -1255,7 +1268,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
                 g.v[i].x += dyt * q.c[t].v[i].x;
                 g.v[i].y -= dyt * q.c[t].v[i].y;
                 dct.v[i] = make_float2(dyt * Hs[t + 1].v[i].x, -dyt * Hs[t + 1].v[i].y);
-                reinterpret_cast<float2*>(vd)[2 * (lane * SL + i)] = g.v[i];
+                st.V[lane * SL + i] = g.v[i];
             }
         }
         const bool in = t < q.len;
@@ -1269,7 +1282,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
             CV<SL> dDt;
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
-                const float2 gp = reinterpret_cast<const float2*>(vd)[2 * pt.v[i]];
+                const float2 gp = st.V[pt.v[i]];
                 dDt.v[i] = cmulc(Hs[t].v[i], gp);
                 g.v[i] = cmulc(Dt(q, t).v[i], gp);
             }
