@@ -6,7 +6,10 @@ One step = dictionary preparation (pdssm_prepare), one forward scan
 (pdssm_scan_fwd: y, h_final, saved chunk states) and one backward scan
 (pdssm_scan_bwd: dD, db, dc, dh0) over one batch of seeded synthetic inputs
 already resident in HBM.  A 512 MiB buffer is rewritten between steps (not
-timed) so that no input of a step is still cached.  Prints ONE JSON line.
+timed) so that no input of a step is still cached.  The default 200 untimed
+steps let the GPU clocks settle (the compute-heavier workloads run up to 20%
+slower during the first ~100 ms of load); then 50 steps are timed.  Prints
+ONE JSON line.
 
 value = state updates (B*L*H*N) per second of the whole step.
 roofline = the dominant kernel's algorithmic bytes (every input read once,
@@ -98,8 +101,9 @@ def traffic_from_profiles(kernel, workload_name):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=200,
+                    help="untimed steps first: the GPU clocks ramp up over the first ~100 ms of load")
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["fwd", "bwd", "both"], default="both",
