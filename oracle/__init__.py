@@ -7,7 +7,8 @@ shares no code with it.
 ``pdssm_oracle.c`` holds the arithmetic: a plain sequential float64 loop per
 (batch, head) sequence, written from the paper's statement of the recurrence
 (Flash PD-SSM, App. E.2 recurrence; Sec. 2.3/3.1 column-one-hot maps; Sec. 2.1
-eq. (1) readout; App. E.3.1 composition rule; App. E.1 Algorithm 1 chunking).
+eq. (1) readout; App. E.3.1 composition rule; App. E.1 Algorithm 1 chunking;
+Sec. 3.1 Prop. 2 straight-through surrogate gradients).
 This module only marshals numpy arrays into it.
 """
 from .oracle import (  # noqa: F401
@@ -15,6 +16,9 @@ from .oracle import (  # noqa: F401
     oracle_fwd,
     oracle_bwd,
     oracle_compose,
+    oracle_ste,
+    oracle_softmax_vjp,
+    oracle_surrogate_grads,
     oracle_num_chunks,
     oracle_lib_path,
 )

@@ -45,8 +45,9 @@ def _load():
         lib.pdssm_oracle_bwd.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P, P]
         lib.pdssm_oracle_compose.argtypes = [I, I, I, I, I, P, P, P, I, P, P]
         lib.pdssm_oracle_num_chunks.argtypes = [I, I]
+        lib.pdssm_oracle_ste.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, P, P]
         for f in (lib.pdssm_oracle_fwd, lib.pdssm_oracle_bwd, lib.pdssm_oracle_compose,
-                  lib.pdssm_oracle_num_chunks):
+                  lib.pdssm_oracle_num_chunks, lib.pdssm_oracle_ste):
             f.restype = I
         _lib = lib
     return _lib
@@ -131,3 +132,41 @@ def oracle_compose(idx, pi, D, chunk):
                                       int(chunk), _ptr(pm), _ptr(dm))
     _check(rc, "oracle_compose")
     return pm, dm
+
+
+def oracle_ste(idx, pi, D, b, c, dy, h0=None, dh_final=None):
+    """Straight-through surrogate inputs (Sec. 3.1 Prop. 2 and its appendix
+    derivation): q [B,L,H,K] f64, the score of every candidate map at every
+    step, and G [H,K,N,N] f64, the gradient of every dictionary matrix summed
+    over the steps that selected it (rows = destination i, columns = source
+    j, as in the dense P_k whose column j has its one in row pi[h,k,j])."""
+    idx, pi = _i32(idx), _i32(pi)
+    D, b, c, h0, dhf = _cplx(D), _cplx(b), _cplx(c), _cplx(h0), _cplx(dh_final)
+    dy = np.ascontiguousarray(dy, dtype=np.float64)
+    B, L, H, N, K = _dims(idx, pi, D)
+    assert dy.shape == (B, L, H)
+    q = np.empty((B, L, H, K), np.float64)
+    G = np.empty((H, K, N, N), np.float64)
+    rc = _load().pdssm_oracle_ste(B, L, H, N, K, _ptr(idx), _ptr(pi), _ptr(D), _ptr(b),
+                                  _ptr(c), _ptr(h0), _ptr(dy), _ptr(dhf), _ptr(q), _ptr(G))
+    _check(rc, "oracle_ste")
+    return q, G
+
+
+def oracle_softmax_vjp(x, gy, axis, temp):
+    """Vector-Jacobian product of the tempered softmax s = softmax(x / temp)
+    along `axis` (the backward stand-in for a hard argmax in Prop. 2):
+    gx = s * (gy - sum(s * gy)) / temp, in float64."""
+    x = np.asarray(x, np.float64) / float(temp)
+    gy = np.asarray(gy, np.float64)
+    e = np.exp(x - x.max(axis=axis, keepdims=True))
+    s = e / e.sum(axis=axis, keepdims=True)
+    return s * (gy - (s * gy).sum(axis=axis, keepdims=True)) / float(temp)
+
+
+def oracle_surrogate_grads(q, G, logits, M, temp):
+    """The two surrogate gradients of Prop. 2 from the oracle_ste outputs:
+    d logits [B,L,H,K] (routing scores k(u_t), softmax over k) and
+    dM [H,K,N,N] (dense dictionary, softmax over the rows i of every
+    column j, the argmax that gives pi[h,k,j])."""
+    return oracle_softmax_vjp(logits, q, -1, temp), oracle_softmax_vjp(M, G, 2, temp)

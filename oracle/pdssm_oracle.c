@@ -287,3 +287,105 @@ int pdssm_oracle_compose(int B, int L, int H, int N, int K,
     }
     return 0;
 }
+
+/*
+ * Straight-through surrogate gradients of the hard map selection (Sec. 3.1,
+ * Prop. 2 "Surrogate Gradients", derived in the appendix section on the
+ * surrogate gradient expressions).  The selected matrix P_t is a real N x N
+ * matrix in the dense view, with the state scaled before the map:
+ *     h_t = P_t z_t + b_t,   z_t = D_t .* h_{t-1}.
+ * The loss is linear in each single P_t, and its gradient with respect to the
+ * real entries of P_t is, under the convention dX = dl/dRe(X) + i dl/dIm(X),
+ *     dP_t[i][j] = Re( g_t[i] * conj(z_t[j]) ),
+ * where g_t is the gradient reaching h_t (db_t of the backward).  Two
+ * quantities follow:
+ *   - the score of every candidate map k at every step (the gradient of the
+ *     loss with respect to the weight of map k in P_t = sum_k v_t[k] P_k,
+ *     taken at the one-hot v_t of the forward pass):
+ *         q[b,t,h,k] = <dP_t, P_k>_F = sum_j Re( g_t[pi[h,k,j]] * conj(z_t[j]) );
+ *   - the gradient of every dictionary matrix, summed over the steps that
+ *     selected it:
+ *         G[h,k,i,j] = sum over (b,t) with idx[b,t,h] == k of dP_t[i][j].
+ * Both are the inputs of the tempered-softmax Jacobians of Prop. 2.
+ * q [B,L,H,K] double (may be NULL), G [H,K,N,N] double (may be NULL).
+ */
+int pdssm_oracle_ste(int B, int L, int H, int N, int K,
+                     const int32_t* idx, const int32_t* pi,
+                     const double* D, const double* b, const double* c,
+                     const double* h0, const double* dy, const double* dh_final,
+                     double* q, double* G)
+{
+    if (bad_dims(B, L, H, N, K) || !idx || !pi || !D || !b || !c || !dy) return -2;
+    if (check_indices(B, L, H, N, K, idx, pi)) return -1;
+
+    double* hs = malloc(sizeof(double) * 2 * N * ((size_t)L + 1));
+    double* Dt = malloc(sizeof(double) * 2 * N);
+    double* bt = malloc(sizeof(double) * 2 * N);
+    double* g = malloc(sizeof(double) * 2 * N);
+    double* gn = malloc(sizeof(double) * 2 * N);
+    double* z = malloc(sizeof(double) * 2 * N);
+    if (!hs || !Dt || !bt || !g || !gn || !z) {
+        free(hs); free(Dt); free(bt); free(g); free(gn); free(z); return -3;
+    }
+    if (G) memset(G, 0, sizeof(double) * (size_t)H * K * N * N);
+
+    for (int bb = 0; bb < B; ++bb) {
+        for (int h = 0; h < H; ++h) {
+            size_t sh = ((size_t)bb * H + h) * N;
+            /* states of the whole sequence: hs[t+1] = h_t, hs[0] = initial state */
+            if (h0) memcpy(hs, h0 + 2 * sh, sizeof(double) * 2 * N);
+            else memset(hs, 0, sizeof(double) * 2 * N);
+            for (int t = 0; t < L; ++t) {
+                const int32_t* p = pi + ((size_t)h * K + idx[((size_t)bb * L + t) * H + h]) * N;
+                load_vec(D, L, H, N, bb, t, h, Dt);
+                load_vec(b, L, H, N, bb, t, h, bt);
+                pd_step(N, p, Dt, bt, hs + 2 * (size_t)N * t, hs + 2 * (size_t)N * (t + 1));
+            }
+
+            if (dh_final) memcpy(g, dh_final + 2 * sh, sizeof(double) * 2 * N);
+            else memset(g, 0, sizeof(double) * 2 * N);
+            for (int t = L - 1; t >= 0; --t) {
+                double dyt = dy[((size_t)bb * L + t) * H + h];
+                const double* ct = c + 2 * at4(L, H, N, bb, t, h, 0);
+                for (int n = 0; n < N; ++n) { /* g_t: add the readout term dy_t conj(c_t) */
+                    RE(g, n) += dyt * RE(ct, n);
+                    IM(g, n) -= dyt * IM(ct, n);
+                }
+                int kt = idx[((size_t)bb * L + t) * H + h];
+                load_vec(D, L, H, N, bb, t, h, Dt);
+                const double* hprev = hs + 2 * (size_t)N * t;
+                for (int j = 0; j < N; ++j) { /* z_t = D_t .* h_{t-1} */
+                    RE(z, j) = RE(Dt, j) * RE(hprev, j) - IM(Dt, j) * IM(hprev, j);
+                    IM(z, j) = RE(Dt, j) * IM(hprev, j) + IM(Dt, j) * RE(hprev, j);
+                }
+                if (q) {
+                    double* qt = q + ((size_t)bb * L + t) * H * K + (size_t)h * K;
+                    for (int k = 0; k < K; ++k) {
+                        const int32_t* pk = pi + ((size_t)h * K + k) * N;
+                        double acc = 0.0;
+                        for (int j = 0; j < N; ++j) /* Re(g[pk[j]] * conj(z[j])) */
+                            acc += RE(g, pk[j]) * RE(z, j) + IM(g, pk[j]) * IM(z, j);
+                        qt[k] = acc;
+                    }
+                }
+                if (G) {
+                    double* Gk = G + ((size_t)h * K + kt) * N * N;
+                    for (int i = 0; i < N; ++i)
+                        for (int j = 0; j < N; ++j)
+                            Gk[(size_t)i * N + j] += RE(g, i) * RE(z, j) + IM(g, i) * IM(z, j);
+                }
+                /* gradient reaching h_{t-1}: conj(D_t[j]) * g_t[pi_t(j)] */
+                const int32_t* p = pi + ((size_t)h * K + kt) * N;
+                for (int j = 0; j < N; ++j) {
+                    double gr = RE(g, p[j]), gi = IM(g, p[j]);
+                    double dr = RE(Dt, j), di = IM(Dt, j);
+                    RE(gn, j) = dr * gr + di * gi;
+                    IM(gn, j) = dr * gi - di * gr;
+                }
+                double* sw = g; g = gn; gn = sw;
+            }
+        }
+    }
+    free(hs); free(Dt); free(bt); free(g); free(gn); free(z);
+    return 0;
+}

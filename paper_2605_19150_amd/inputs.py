@@ -182,3 +182,26 @@ def sub_sequence(inp, bb, hh):
         if inp.get(k) is not None:
             out[k] = np.ascontiguousarray(inp[k][bb:bb + 1, hh:hh + 1])
     return out
+
+
+def selection_inputs(idx, pi, seed=0, margin=(0.1, 1.0)):
+    """Dense scores behind the hard selections, for the surrogate gradients:
+    routing logits [B,L,H,K] float32 whose largest entry at (b,t,h) is
+    idx[b,t,h], and a dense dictionary M [H,K,N,N] float32 whose largest entry
+    in column j of M[h,k] is row pi[h,k,j].  Entries are N(0,1); the selected
+    one is then raised to the column's (row's) maximum plus U(margin)."""
+    rng = np.random.default_rng(seed)
+    B, L, H = idx.shape
+    _, K, N = pi.shape
+    logits = rng.standard_normal((B, L, H, K), dtype=np.float32)
+    bump = rng.uniform(margin[0], margin[1], size=(B, L, H)).astype(np.float32)
+    sel = np.take_along_axis(logits, idx[..., None].astype(np.int64), axis=3)[..., 0]
+    top = logits.max(axis=3)
+    np.put_along_axis(logits, idx[..., None].astype(np.int64),
+                      np.maximum(top, sel)[..., None] + bump[..., None], axis=3)
+    M = rng.standard_normal((H, K, N, N), dtype=np.float32)
+    bump = rng.uniform(margin[0], margin[1], size=(H, K, N)).astype(np.float32)
+    top = M.max(axis=2)                                      # [H,K,N] over rows
+    rows = pi[:, :, None, :].astype(np.int64)                # [H,K,1,N]
+    np.put_along_axis(M, rows, (top + bump)[:, :, None, :], axis=2)
+    return logits, M
