@@ -45,7 +45,7 @@ def _load():
         lib.pdssm_oracle_bwd.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P, P]
         lib.pdssm_oracle_compose.argtypes = [I, I, I, I, I, P, P, P, I, P, P]
         lib.pdssm_oracle_num_chunks.argtypes = [I, I]
-        lib.pdssm_oracle_ste.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, P, P]
+        lib.pdssm_oracle_ste.argtypes = [I, I, I, I, I, P, P, P, P, P, P, P, P, P, P, P]
         for f in (lib.pdssm_oracle_fwd, lib.pdssm_oracle_bwd, lib.pdssm_oracle_compose,
                   lib.pdssm_oracle_num_chunks, lib.pdssm_oracle_ste):
             f.restype = I
@@ -134,12 +134,13 @@ def oracle_compose(idx, pi, D, chunk):
     return pm, dm
 
 
-def oracle_ste(idx, pi, D, b, c, dy, h0=None, dh_final=None):
+def oracle_ste(idx, pi, D, b, c, dy, h0=None, dh_final=None, want_z=False):
     """Straight-through surrogate inputs (Sec. 3.1 Prop. 2 and its appendix
     derivation): q [B,L,H,K] f64, the score of every candidate map at every
     step, and G [H,K,N,N] f64, the gradient of every dictionary matrix summed
     over the steps that selected it (rows = destination i, columns = source
-    j, as in the dense P_k whose column j has its one in row pi[h,k,j])."""
+    j, as in the dense P_k whose column j has its one in row pi[h,k,j]).
+    With want_z, also z [B,L,H,N] c128: z_t = D_t .* h_{t-1} of every step."""
     idx, pi = _i32(idx), _i32(pi)
     D, b, c, h0, dhf = _cplx(D), _cplx(b), _cplx(c), _cplx(h0), _cplx(dh_final)
     dy = np.ascontiguousarray(dy, dtype=np.float64)
@@ -147,10 +148,11 @@ def oracle_ste(idx, pi, D, b, c, dy, h0=None, dh_final=None):
     assert dy.shape == (B, L, H)
     q = np.empty((B, L, H, K), np.float64)
     G = np.empty((H, K, N, N), np.float64)
+    z = np.empty((B, L, H, N), np.complex128) if want_z else None
     rc = _load().pdssm_oracle_ste(B, L, H, N, K, _ptr(idx), _ptr(pi), _ptr(D), _ptr(b),
-                                  _ptr(c), _ptr(h0), _ptr(dy), _ptr(dhf), _ptr(q), _ptr(G))
+                                  _ptr(c), _ptr(h0), _ptr(dy), _ptr(dhf), _ptr(q), _ptr(G), _ptr(z))
     _check(rc, "oracle_ste")
-    return q, G
+    return (q, G, z) if want_z else (q, G)
 
 
 def oracle_softmax_vjp(x, gy, axis, temp):

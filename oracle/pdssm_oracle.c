@@ -307,13 +307,14 @@ int pdssm_oracle_compose(int B, int L, int H, int N, int K,
  *     selected it:
  *         G[h,k,i,j] = sum over (b,t) with idx[b,t,h] == k of dP_t[i][j].
  * Both are the inputs of the tempered-softmax Jacobians of Prop. 2.
- * q [B,L,H,K] double (may be NULL), G [H,K,N,N] double (may be NULL).
+ * q [B,L,H,K] double (may be NULL), G [H,K,N,N] double (may be NULL),
+ * zout [B,L,H,N] complex (may be NULL): z_t of every step.
  */
 int pdssm_oracle_ste(int B, int L, int H, int N, int K,
                      const int32_t* idx, const int32_t* pi,
                      const double* D, const double* b, const double* c,
                      const double* h0, const double* dy, const double* dh_final,
-                     double* q, double* G)
+                     double* q, double* G, double* zout)
 {
     if (bad_dims(B, L, H, N, K) || !idx || !pi || !D || !b || !c || !dy) return -2;
     if (check_indices(B, L, H, N, K, idx, pi)) return -1;
@@ -358,6 +359,7 @@ int pdssm_oracle_ste(int B, int L, int H, int N, int K,
                     RE(z, j) = RE(Dt, j) * RE(hprev, j) - IM(Dt, j) * IM(hprev, j);
                     IM(z, j) = RE(Dt, j) * IM(hprev, j) + IM(Dt, j) * RE(hprev, j);
                 }
+                if (zout) memcpy(zout + 2 * at4(L, H, N, bb, t, h, 0), z, sizeof(double) * 2 * N);
                 if (q) {
                     double* qt = q + ((size_t)bb * L + t) * H * K + (size_t)h * K;
                     for (int k = 0; k < K; ++k) {

@@ -280,6 +280,8 @@ int pdssm_num_chunks(const pdssm_desc* d) {
 
 size_t pdssm_workspace_size(const pdssm_desc* d, int op) {
     if (op == PDSSM_OP_COMPOSE) return check_dims(d) == PDSSM_OK ? 0 : (size_t)-1;
+    if (op == PDSSM_OP_DICT_GRAD)
+        return check_dims(d) == PDSSM_OK ? pdssm::dict_plan(d->B, d->L, d->H, d->N, d->K).bytes : (size_t)-1;
     if (op != PDSSM_OP_FWD && op != PDSSM_OP_BWD) return (size_t)-1;
     int tau = scan_chunk(d);
     if (tau < 0) return (size_t)-1;
@@ -371,11 +373,12 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
-int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
-                   const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
-                   const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
-                   pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
-                   void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+namespace {
+
+int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, const pdssm_c64* D,
+                  const pdssm_c64* b, const pdssm_c64* c, const pdssm_c64* saved, const float* dy,
+                  const pdssm_c64* dh_final, pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
+                  float* q, pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status, void* stream) {
     int tau = scan_chunk(d);
     if (tau < 0) return tau;
     if (!idx || !pi || !D || !b || !c || !saved || !dy || !dD || !db || !dc)
@@ -389,8 +392,9 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     const size_t need = ws_bytes_for(s, d, a.C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
+    if (misaligned(z) || (reinterpret_cast<uintptr_t>(q) & 3) != 0) return PDSSM_ERR_INVALID_ARG;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
-    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {ws, need}},
+    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {q, nidx * d->K}, {z, nst}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * 8},
                      {dy, nidx}, {dh_final, s.seqN * 8}}))
         return PDSSM_ERR_INVALID_ARG;
@@ -405,12 +409,16 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     a.db = reinterpret_cast<float2*>(db);
     a.dc = reinterpret_cast<float2*>(dc);
     a.dh0 = reinterpret_cast<float2*>(dh0);
+    a.q = q;
+    a.z = reinterpret_cast<float2*>(z);
     a.status = dev_status;
     const hipStream_t st = static_cast<hipStream_t>(stream);
     hipError_t e;
     if (use_fused(d)) {
         pdssm::FusedArgs f = fused_base(a);
         f.saved = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
+        f.q = q;
+        f.z = reinterpret_cast<float2*>(z);
         e = prep_fused(f, d, pi, ws, s, dev_status, st, false);
         if (e == hipSuccess) e = pdssm::launch_bwd_fused(f, st);
     } else {
@@ -419,6 +427,72 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
         e = pdssm::launch_bwd_chunked(a, st);
     }
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+}  // namespace
+
+int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
+                   const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                   const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
+                   pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
+                   void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+    return scan_bwd_impl(d, idx, pi, D, b, c, saved, dy, dh_final, dD, db, dc, dh0, nullptr, nullptr, ws,
+                         ws_bytes, dev_status, stream);
+}
+
+int pdssm_scan_bwd_ste(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
+                       const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                       const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
+                       pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
+                       float* q, pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status,
+                       void* stream) {
+    return scan_bwd_impl(d, idx, pi, D, b, c, saved, dy, dh_final, dD, db, dc, dh0, q, z, ws, ws_bytes,
+                         dev_status, stream);
+}
+
+int pdssm_dict_grad(const pdssm_desc* d, const int32_t* idx, const pdssm_c64* g, const pdssm_c64* z,
+                    float* G, void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+    const int st = check_dims(d);
+    if (st != PDSSM_OK) return st;
+    if (!idx || !g || !z || !G) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned(g) || misaligned(z) || (reinterpret_cast<uintptr_t>(G) & 3) != 0)
+        return PDSSM_ERR_INVALID_ARG;
+    const pdssm::DictPlan plan = pdssm::dict_plan(d->B, d->L, d->H, d->N, d->K);
+    if (!ws || ws_bytes < plan.bytes || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
+        return PDSSM_ERR_WORKSPACE;
+    const size_t nidx = (size_t)d->B * d->L * d->H * 4, nst = nidx / 4 * d->N * 8;
+    const size_t nG = (size_t)d->H * d->K * d->N * d->N * 4;
+    if (any_overlap({{G, nG}, {ws, plan.bytes}}, {{idx, nidx}, {g, nst}, {z, nst}})) return PDSSM_ERR_INVALID_ARG;
+    pdssm::DictGradArgs a = {};
+    a.B = d->B;
+    a.L = d->L;
+    a.H = d->H;
+    a.N = d->N;
+    a.K = d->K;
+    a.idx = idx;
+    a.g = reinterpret_cast<const float2*>(g);
+    a.z = reinterpret_cast<const float2*>(z);
+    a.G = G;
+    a.plan = plan;
+    a.ws = static_cast<unsigned char*>(ws);
+    a.status = dev_status;
+    return pdssm::launch_dict_grad(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int32_t len, int64_t inner,
+                      float temp, void* stream) {
+    if (!x || !gy || !gx || outer < 0 || len < 1 || inner < 1) return PDSSM_ERR_INVALID_ARG;
+    if (!(temp > 0.f) || temp > 3.0e38f) return PDSSM_ERR_INVALID_ARG;
+    // one thread per (outer, inner) fibre: keep the grid below 2^30 blocks
+    if (outer > (1LL << 40) / len / inner || outer > (1LL << 38) / inner) return PDSSM_ERR_UNSUPPORTED;
+    const size_t n = (size_t)outer * len * inner * 4;
+    if (((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(gy) | reinterpret_cast<uintptr_t>(gx)) & 3) != 0)
+        return PDSSM_ERR_INVALID_ARG;
+    if (any_overlap({{gx, n}}, {{x, n}, {gy, n}})) return PDSSM_ERR_INVALID_ARG;
+    return pdssm::launch_softmax_vjp(x, gy, gx, outer, len, inner, 1.f / temp, static_cast<hipStream_t>(stream)) ==
+                   hipSuccess
+               ? PDSSM_OK
+               : PDSSM_ERR_HIP;
 }
 
 int pdssm_compose_chunks(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,

@@ -258,4 +258,98 @@ __device__ __forceinline__ void pd_scatter_step(float2* X, int lane, bool act,
     if (act) x = ld_cv<SL>(X, lane);
 }
 
+// ------------------------------------------------------------------ cross-lane sums
+// Cross-lane exchange primitives for the reduction below (VALU only, no LDS):
+// permlane32/16 swaps trade the upper half of one register with the lower
+// half of another across lanes l and l^32 (resp. l^16); DPP mirrors pair a
+// lane with l^15 (16-lane row) and l^7 (8-lane half row); quad_perm pairs l^2
+// and l^1.
+__device__ __forceinline__ float dpp_f(float v, int ctrl) {
+    switch (ctrl) {  // the control word must be a constant
+        case 0x140: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false));
+        case 0x141: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false));
+        case 0x4e: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4e, 0xf, 0xf, false));
+        default: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xb1, 0xf, 0xf, false));
+    }
+}
+
+// Sum over the 64 lanes of each of T per-lane values v[t] (T a power of two
+// <= 64), as a transpose-reduction: log2(T) halving exchanges in which each
+// lane keeps half of its values (the half picked by one bit of its lane
+// index), then plain butterflies.  Lane l ends with the total of value
+// t = l / (64 / T).
+template <int T>
+__device__ __forceinline__ float transpose_sum(float (&v)[T], int lane) {
+    int n = T;
+#pragma unroll
+    for (int lvl = 0; lvl < 6; ++lvl) {
+        const int d = 32 >> lvl;
+        if (n > 1) {
+            const int h = n / 2;
+#pragma unroll
+            for (int i = 0; i < T / 2; ++i) {
+                if (i < h) {
+                    if (d >= 16) {
+                        // lower lanes keep v[i] and receive the partner's v[i];
+                        // upper lanes keep v[i+h] and receive the partner's v[i+h]
+                        auto r = d == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]),
+                                                                          __float_as_uint(v[i + h]), false, false)
+                                         : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]),
+                                                                          __float_as_uint(v[i + h]), false, false);
+                        v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+                    } else {
+                        const bool up = (lane & d) != 0;
+                        const float send = up ? v[i] : v[i + h];
+                        const float keep = up ? v[i + h] : v[i];
+                        v[i] = keep + dpp_f(send, d == 8 ? 0x140 : d == 4 ? 0x141 : d == 2 ? 0x4e : 0xb1);
+                    }
+                }
+            }
+            n = h;
+        } else {
+            if (d >= 16) {
+                auto r = d == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[0]),
+                                                                  false, false)
+                                 : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[0]), __float_as_uint(v[0]),
+                                                                  false, false);
+                v[0] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+            } else {
+                v[0] += dpp_f(v[0], d == 8 ? 0x140 : d == 4 ? 0x141 : d == 2 ? 0x4e : 0xb1);
+            }
+        }
+    }
+    return v[0];
+}
+
+// ------------------------------------------------------------------ surrogate scores
+// Straight-through score of every dictionary map at one step (Sec. 3.1
+// Prop. 2): q[k] = sum_j Re(g[pi_k(j)] * conj(z[j])) for k = 0..K-1, where
+// g (the gradient reaching h_t, N values) is staged in LDS at Gs, z = D_t .* h_{t-1}
+// is held by the lanes (entry lane*SL + s) and map(k, j) returns pi_k(j) in
+// [0, N).  Maps go in blocks of 16: per-lane partial sums, then one
+// transpose-reduction leaves the total of map kb + l/4 in lane l.  Every lane
+// of the wave must call it (K uniform); lanes l % 4 == 0 store when `store`.
+template <int N, class MapFn>
+__device__ __forceinline__ void ste_scores(const float2* __restrict__ Gs, const CV<Lay<N>::SL>& z, int lane,
+                                           bool act, int K, MapFn map, float* __restrict__ qrow, bool store) {
+    constexpr int SL = Lay<N>::SL;
+    for (int kb = 0; kb < K; kb += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            v[u] = 0.f;
+            if (act && kb + u < K) {
+#pragma unroll
+                for (int s = 0; s < SL; ++s) {
+                    const float2 g = Gs[map(kb + u, lane * SL + s)];
+                    v[u] = fmaf(g.x, z.v[s].x, fmaf(g.y, z.v[s].y, v[u]));
+                }
+            }
+        }
+        const float tot = transpose_sum<16>(v, lane);
+        const int k = kb + (lane >> 2);
+        if (store && (lane & 3) == 0 && k < K) qrow[k] = tot;
+    }
+}
+
 }  // namespace pdssm

@@ -116,10 +116,52 @@ struct FusedArgs {
     float2* segA;
     float2* segD;
     int* segP;
+    // Backward only, optional: straight-through scores q [B,L,H,K] and the
+    // scaled states z = D_t .* h_{t-1} [B,L,H,N] (Sec. 3.1 Prop. 2).
+    float* q;
+    float2* z;
 };
 
-hipError_t launch_prep(const PrepArgs& p, hipStream_t s);
-hipError_t launch_fwd_fused(const FusedArgs& a, hipStream_t s);
-hipError_t launch_bwd_fused(const FusedArgs& a, hipStream_t s);
+// Per state size N (one translation unit each) ...
+template <int N>
+hipError_t launch_prep_n(const PrepArgs& p, hipStream_t s);
+template <int N>
+hipError_t launch_fwd_fused_n(const FusedArgs& a, hipStream_t s);
+template <int N>
+hipError_t launch_bwd_fused_n(const FusedArgs& a, hipStream_t s);
+
+#define PDSSM_DECLARE_N(N_)                                                    \
+    template <>                                                                \
+    hipError_t launch_prep_n<N_>(const PrepArgs& p, hipStream_t s);           \
+    template <>                                                                \
+    hipError_t launch_fwd_fused_n<N_>(const FusedArgs& a, hipStream_t s);     \
+    template <>                                                                \
+    hipError_t launch_bwd_fused_n<N_>(const FusedArgs& a, hipStream_t s);
+PDSSM_DECLARE_N(8)
+PDSSM_DECLARE_N(16)
+PDSSM_DECLARE_N(32)
+PDSSM_DECLARE_N(64)
+PDSSM_DECLARE_N(128)
+PDSSM_DECLARE_N(256)
+#undef PDSSM_DECLARE_N
+
+// ... and the dispatch on N.
+#define PDSSM_DISPATCH_N(N_, F_, ARGS_)            \
+    switch (N_) {                                  \
+        case 8: return F_<8> ARGS_;                \
+        case 16: return F_<16> ARGS_;              \
+        case 32: return F_<32> ARGS_;              \
+        case 64: return F_<64> ARGS_;              \
+        case 128: return F_<128> ARGS_;            \
+        case 256: return F_<256> ARGS_;            \
+        default: return hipErrorInvalidValue;      \
+    }
+inline hipError_t launch_prep(const PrepArgs& p, hipStream_t s) { PDSSM_DISPATCH_N(p.N, launch_prep_n, (p, s)) }
+inline hipError_t launch_fwd_fused(const FusedArgs& a, hipStream_t s) {
+    PDSSM_DISPATCH_N(a.N, launch_fwd_fused_n, (a, s))
+}
+inline hipError_t launch_bwd_fused(const FusedArgs& a, hipStream_t s) {
+    PDSSM_DISPATCH_N(a.N, launch_bwd_fused_n, (a, s))
+}
 
 }  // namespace pdssm

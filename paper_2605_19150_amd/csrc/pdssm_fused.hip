@@ -417,68 +417,6 @@ __device__ __forceinline__ void finish_chunk(const FusedArgs& a, const Smem& s, 
 
 
 // ================================================================== forward
-// Cross-lane exchange primitives for the reduction below (VALU only, no LDS):
-// permlane32/16 swaps trade the upper half of one register with the lower
-// half of another across lanes l and l^32 (resp. l^16); DPP mirrors pair a
-// lane with l^15 (16-lane row) and l^7 (8-lane half row); quad_perm pairs l^2
-// and l^1.
-__device__ __forceinline__ float dpp_f(float v, int ctrl) {
-    switch (ctrl) {  // the control word must be a constant
-        case 0x140: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x140, 0xf, 0xf, false));
-        case 0x141: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x141, 0xf, 0xf, false));
-        case 0x4e: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4e, 0xf, 0xf, false));
-        default: return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xb1, 0xf, 0xf, false));
-    }
-}
-
-// Sum over the 64 lanes of each of T per-lane values v[t] (T a power of two
-// <= 64), as a transpose-reduction: log2(T) halving exchanges in which each
-// lane keeps half of its values (the half picked by one bit of its lane
-// index), then plain butterflies.  Lane l ends with the total of value
-// t = l / (64 / T).
-template <int T>
-__device__ __forceinline__ float transpose_sum(float (&v)[T], int lane) {
-    int n = T;
-#pragma unroll
-    for (int lvl = 0; lvl < 6; ++lvl) {
-        const int d = 32 >> lvl;
-        if (n > 1) {
-            const int h = n / 2;
-#pragma unroll
-            for (int i = 0; i < T / 2; ++i) {
-                if (i < h) {
-                    if (d >= 16) {
-                        // lower lanes keep v[i] and receive the partner's v[i];
-                        // upper lanes keep v[i+h] and receive the partner's v[i+h]
-                        auto r = d == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[i]),
-                                                                          __float_as_uint(v[i + h]), false, false)
-                                         : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[i]),
-                                                                          __float_as_uint(v[i + h]), false, false);
-                        v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-                    } else {
-                        const bool up = (lane & d) != 0;
-                        const float send = up ? v[i] : v[i + h];
-                        const float keep = up ? v[i + h] : v[i];
-                        v[i] = keep + dpp_f(send, d == 8 ? 0x140 : d == 4 ? 0x141 : d == 2 ? 0x4e : 0xb1);
-                    }
-                }
-            }
-            n = h;
-        } else {
-            if (d >= 16) {
-                auto r = d == 32 ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v[0]), __float_as_uint(v[0]),
-                                                                  false, false)
-                                 : __builtin_amdgcn_permlane16_swap(__float_as_uint(v[0]), __float_as_uint(v[0]),
-                                                                  false, false);
-                v[0] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-            } else {
-                v[0] += dpp_f(v[0], d == 8 ? 0x140 : d == 4 ? 0x141 : d == 2 ? 0x4e : 0xb1);
-            }
-        }
-    }
-    return v[0];
-}
-
 // ------------------------------------------------------------------ sorted chunk maps
 // For a many-to-one chunk map the frontier applies carry -> Pi (Delta .* carry)
 // without float atomics: the chunk wave orders the map's sources by
@@ -1130,7 +1068,7 @@ __device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int
 
 // AGG: the aggregate pass of a segment -- each chunk's adjoint operator is
 // composed into the running aggregate passed from wave to wave.
-template <int N, int TAU, int W, int G, bool FB, bool AGG>
+template <int N, int TAU, int W, int G, bool FB, bool AGG, bool STE>
 __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int r,
                                           BwdChunk<N, TAU>& u, bool& bad) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
@@ -1288,12 +1226,25 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
             }
             if (in) st_out<SL>(a.dD + off, lane, dDt);
         }
+        if constexpr (STE) {
+            // straight-through scores of every map against g_t (still in
+            // st.V) and the scaled state z_t = D_t .* h_{t-1}
+            CV<SL> zt;
+#pragma unroll
+            for (int i = 0; i < SL; ++i) zt.v[i] = cmul(Dt(q, t).v[i], Hs[t].v[i]);
+            if (a.z && act && in) st_out<SL>(a.z + off, lane, zt);
+            if (a.q) {
+                const uint8_t* dict = s.dict;
+                ste_scores<N>(st.V, zt, lane, act, a.K, [dict](int k, int j) { return (int)dict[k * N + j]; },
+                              a.q + (((size_t)w.bb * a.L + s0 + t) * a.H + w.hh) * a.K, in);
+            }
+        }
     }
 }
 
 // Wave wv owns reverse-order local chunks wv, wv+W, ...; with PREFETCH every
 // load of its next chunk is in flight while it computes the current one.
-template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG>
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, bool STE>
 __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
@@ -1305,17 +1256,17 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, cons
         for (int r = wv; r < w.nc; r += 2 * W) {
             issue_bwd<N, TAU, AGG>(a, w, r + W, lane, act, ub);
             issue_fence();
-            bwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, r, ua, bad);
+            bwd_chunk<N, TAU, W, G, FB, AGG, STE>(a, s, w, r, ua, bad);
             if (r + W >= w.nc) break;
             issue_bwd<N, TAU, AGG>(a, w, r + 2 * W, lane, act, ua);
             issue_fence();
-            bwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, r + W, ub, bad);
+            bwd_chunk<N, TAU, W, G, FB, AGG, STE>(a, s, w, r + W, ub, bad);
         }
     } else {
         for (int r = wv; r < w.nc; r += W) {
             BwdChunk<N, TAU> u;
             issue_bwd<N, TAU, AGG>(a, w, r, lane, act, u);
-            bwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, r, u, bad);
+            bwd_chunk<N, TAU, W, G, FB, AGG, STE>(a, s, w, r, u, bad);
         }
     }
     if (bad) report_index_error(a.status);
@@ -1348,7 +1299,7 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_bwd(const FusedArgs& a, cons
     return U;
 }
 
-template <int N, int TAU, int W, bool AGG>
+template <int N, int TAU, int W, bool AGG, bool STE>
 __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     extern __shared__ __align__(16) unsigned char lds[];
@@ -1381,10 +1332,10 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     bool fb;
     const int G = head_variant(s, a.K, fb);
     constexpr bool PF = fused_prefetch(N, TAU);
-    if (fb) bwd_body<N, TAU, W, 7, true, PF, AGG>(a, s, w);
-    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF, AGG>(a, s, w);
-    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF, AGG>(a, s, w);
-    else bwd_body<N, TAU, W, 7, false, PF, AGG>(a, s, w);
+    if (fb) bwd_body<N, TAU, W, 7, true, PF, AGG, STE>(a, s, w);
+    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF, AGG, STE>(a, s, w);
+    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF, AGG, STE>(a, s, w);
+    else bwd_body<N, TAU, W, 7, false, PF, AGG, STE>(a, s, w);
 }
 
 // Segmented scans (S > 1) first run the aggregate pass over segments that
@@ -1409,13 +1360,14 @@ hipError_t fwd_launch(const FusedArgs& a, hipStream_t st) {
 template <int N, int TAU, int W>
 hipError_t bwd_launch(const FusedArgs& a, hipStream_t st) {
     if (a.S > 1) {
-        auto agg = k_bwd_fused<N, TAU, W, true>;
+        auto agg = k_bwd_fused<N, TAU, W, true, false>;
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(agg),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3(W * 64), a.lds.total, st, a);
     }
-    auto kern = k_bwd_fused<N, TAU, W, false>;
+    // the straight-through outputs are computed by the scan pass only
+    auto kern = a.q || a.z ? k_bwd_fused<N, TAU, W, false, true> : k_bwd_fused<N, TAU, W, false, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;
@@ -1454,23 +1406,22 @@ hipError_t dispatch_tau(const FusedArgs& a, hipStream_t st) {
 
 }  // namespace
 
-#define PDSSM_FUSED_N(N_, EXPR_T)                     \
-    switch (N_) {                                     \
-        case 8: { constexpr int NN = 8; EXPR_T; }     \
-        case 16: { constexpr int NN = 16; EXPR_T; }   \
-        case 32: { constexpr int NN = 32; EXPR_T; }   \
-        case 64: { constexpr int NN = 64; EXPR_T; }   \
-        case 128: { constexpr int NN = 128; EXPR_T; } \
-        case 256: { constexpr int NN = 256; EXPR_T; } \
-        default: return hipErrorInvalidValue;         \
-    }
-
-hipError_t launch_prep(const PrepArgs& p, hipStream_t st) { PDSSM_FUSED_N(p.N, return prep_launch<NN>(p, st)) }
-hipError_t launch_fwd_fused(const FusedArgs& a, hipStream_t st) {
-    PDSSM_FUSED_N(a.N, return (dispatch_tau<NN, true>(a, st)))
+// This file is compiled once per state size N (-DPDSSM_N=...), so the six
+// sizes build in parallel; pdssm_api.cpp dispatches on N.
+#ifndef PDSSM_N
+#error "compile pdssm_fused.hip with -DPDSSM_N=<state size>"
+#endif
+template <>
+hipError_t launch_prep_n<PDSSM_N>(const PrepArgs& p, hipStream_t st) {
+    return prep_launch<PDSSM_N>(p, st);
 }
-hipError_t launch_bwd_fused(const FusedArgs& a, hipStream_t st) {
-    PDSSM_FUSED_N(a.N, return (dispatch_tau<NN, false>(a, st)))
+template <>
+hipError_t launch_fwd_fused_n<PDSSM_N>(const FusedArgs& a, hipStream_t st) {
+    return dispatch_tau<PDSSM_N, true>(a, st);
+}
+template <>
+hipError_t launch_bwd_fused_n<PDSSM_N>(const FusedArgs& a, hipStream_t st) {
+    return dispatch_tau<PDSSM_N, false>(a, st);
 }
 
 }  // namespace pdssm

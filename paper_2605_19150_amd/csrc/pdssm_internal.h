@@ -36,6 +36,10 @@ struct ScanArgs {
     float2* agg_v;
     float2* U;       // bwd: gradient reaching the last state of each chunk from later chunks
     int* status;
+    // bwd, optional: straight-through scores q [B,L,H,K] and scaled states
+    // z = D_t .* h_{t-1} [B,L,H,N] (Sec. 3.1 Prop. 2)
+    float* q;
+    float2* z;
 };
 
 struct ComposeArgs {
@@ -49,10 +53,70 @@ struct ComposeArgs {
     int* status;
 };
 
+// Dictionary gradient of the straight-through estimator (Sec. 3.1 Prop. 2):
+// G[h,k] = sum over the steps (b,t) with idx[b,t,h] == k of Re(g_t z_t^H).
+// The steps of every head are first grouped by map (a stable counting sort),
+// then each group is cut into items of at most P steps; an item sums its
+// steps' outer products on the matrix cores and writes G[h,k] itself when it
+// is the group's only item, else a partial that a last pass adds up in item
+// order.  All sums run in a fixed order (deterministic results).
+struct DictPlan {
+    int seg, S;      // steps per counting segment, segments per head
+    int P;           // steps per item
+    int max_items;   // bound on the number of items (grid size)
+    int max_slots;   // bound on the partials of groups with several items
+    size_t off_order, off_hist, off_n, off_pos, off_item, off_slot, off_partial, bytes;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+inline DictPlan dict_plan(int B, int L, int H, int N, int K) {
+    DictPlan p;
+    const size_t BL = (size_t)B * L, total = BL * H;
+    p.seg = 4096;
+    p.S = (int)((BL + p.seg - 1) / p.seg);
+    const size_t cell = (size_t)N * N * 4;
+    size_t P = (total + 1023) / 1024;                           // about 1024 items
+    const size_t Pmem = (2 * total * cell + (1u << 28) - 1) >> 28;  // partials <= 256 MiB
+    if (P < Pmem) P = Pmem;
+    if (P < 64) P = 64;
+    P = (P + 63) & ~(size_t)63;
+    p.P = (int)P;
+    // a group of n > P steps has ceil(n/P) <= 2n/P items; others have at most one
+    p.max_slots = (int)(2 * total / P);
+    p.max_items = (int)((total + P - 1) / P + (size_t)H * K);
+    size_t o = 0;
+    p.off_order = o; o = align256(o + total * 4);
+    p.off_hist = o; o = align256(o + (size_t)H * p.S * K * 4);
+    p.off_n = o; o = align256(o + (size_t)H * K * 4);
+    p.off_pos = o; o = align256(o + (size_t)H * K * 4);
+    p.off_item = o; o = align256(o + ((size_t)H * K + 1) * 4);
+    p.off_slot = o; o = align256(o + (size_t)H * K * 4);
+    p.off_partial = o; o = align256(o + (size_t)p.max_slots * cell);
+    p.bytes = o;
+    return p;
+}
+
+struct DictGradArgs {
+    int B, L, H, N, K;
+    const int* idx;    // [B,L,H]
+    const float2* g;   // [B,L,H,N] gradient reaching h_t (db of the backward)
+    const float2* z;   // [B,L,H,N] D_t .* h_{t-1}
+    float* G;          // [H,K,N,N]
+    DictPlan plan;
+    unsigned char* ws;
+    int* status;
+};
+
 // Each returns hipSuccess or the launch error.
 hipError_t launch_fwd_chunked(const ScanArgs& a, hipStream_t s);
 hipError_t launch_bwd_chunked(const ScanArgs& a, hipStream_t s);
 hipError_t launch_compose(const ComposeArgs& a, hipStream_t s);
+hipError_t launch_dict_grad(const DictGradArgs& a, hipStream_t s);
+// gx = s .* (gy - <s, gy>) * inv_temp along the middle axis of [outer, len, inner],
+// s = softmax(x * inv_temp).
+hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int len,
+                              int64_t inner, float inv_temp, hipStream_t s);
 
 // LDS bytes the chunked backward's emit kernel needs per workgroup.
 inline size_t bwd_emit_lds_bytes(int N, int tau) { return (size_t)(tau + 2) * N * 8; }

@@ -1,0 +1,425 @@
+// pdssm_ste.hip -- straight-through surrogate gradients for gfx950 (Sec. 3.1
+// Prop. 2 and its derivation in the appendix).
+//
+// The backward scan already emits, per step, the gradient g_t reaching h_t
+// (db) and, when asked, the scaled state z_t = D_t .* h_{t-1} and the scores
+// q_t[k] of every dictionary map.  This file holds what remains:
+//
+//   dictionary gradient  G[h,k] = sum over the steps (b,t) with
+//                        idx[b,t,h] == k of Re(g_t z_t^H)   (an N x N matrix)
+//     k_dict_hist     per (head, segment of steps): how many steps chose each map
+//     k_dict_plan     one workgroup: per group (h,k) its step count, its first
+//                     position in the grouped order, its first item and, for
+//                     groups of several items, its first partial slot
+//     k_dict_scatter  per (head, segment): step ids into the grouped order,
+//                     stable (ranks from ballots over the key bits)
+//     k_dict_gemm     per item (at most P steps of one group): the sum of the
+//                     steps' outer products on the matrix cores,
+//                     v_mfma_f32_32x32x2f32 with the contraction pair
+//                     (re, im): Re(g_i conj(z_j)) = g_i.re z_j.re + g_i.im z_j.im
+//     k_dict_reduce   groups of several items: their partials added in item
+//                     order; groups no step chose: zeros
+//   tempered softmax    k_softmax_vjp: gx = s .* (gy - <s, gy>) / temp along
+//                     one axis, s = softmax(x / temp) -- the backward stand-in
+//                     for a hard argmax (routing logits: over k; dictionary:
+//                     down each column of M[h,k]).
+//
+// Every sum runs in a fixed order, so the results do not change from run to run.
+#include "pdssm_device.h"
+#include "pdssm_internal.h"
+
+namespace pdssm {
+
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+struct DictWs {
+    int* order;      // [B*L*H] step ids u = b*L + t, grouped by (head, map)
+    int* hist;       // [H][S][K]
+    int* n;          // [H*K] steps per group
+    int* pos;        // [H*K] first position of the group in order
+    int* item;       // [H*K + 1] first item of the group; item[H*K] = number of items
+    int* slot;       // [H*K] first partial slot (groups of several items), else -1
+    float* partial;  // [max_slots][N*N]
+};
+
+__device__ __forceinline__ DictWs dict_ws(const DictGradArgs& a) {
+    DictWs w;
+    w.order = reinterpret_cast<int*>(a.ws + a.plan.off_order);
+    w.hist = reinterpret_cast<int*>(a.ws + a.plan.off_hist);
+    w.n = reinterpret_cast<int*>(a.ws + a.plan.off_n);
+    w.pos = reinterpret_cast<int*>(a.ws + a.plan.off_pos);
+    w.item = reinterpret_cast<int*>(a.ws + a.plan.off_item);
+    w.slot = reinterpret_cast<int*>(a.ws + a.plan.off_slot);
+    w.partial = reinterpret_cast<float*>(a.ws + a.plan.off_partial);
+    return w;
+}
+
+// An idx entry outside [0,K) counts as map 0 (and is reported) so that every
+// access stays in bounds; the histogram and the scatter treat it alike.
+__device__ __forceinline__ int map_key(int k, int K, bool& bad) {
+    const bool b = (unsigned)k >= (unsigned)K;
+    bad |= b;
+    return b ? 0 : k;
+}
+
+// ------------------------------------------------------------------ grouping
+// Block x = h * S + segment: steps u in [segment*seg, min(+seg, B*L)).
+__global__ __launch_bounds__(256) void k_dict_hist(DictGradArgs a) {
+    __shared__ int cnt[256];
+    const int h = blockIdx.x / a.plan.S, sg = blockIdx.x - h * a.plan.S;
+    for (int k = threadIdx.x; k < a.K; k += 256) cnt[k] = 0;
+    __syncthreads();
+    const long BL = (long)a.B * a.L;
+    const long u0 = (long)sg * a.plan.seg, u1 = min(u0 + (long)a.plan.seg, BL);
+    bool bad = false;
+    for (long u = u0 + threadIdx.x; u < u1; u += 256) atomicAdd(&cnt[map_key(a.idx[u * a.H + h], a.K, bad)], 1);
+    __syncthreads();
+    const DictWs w = dict_ws(a);
+    for (int k = threadIdx.x; k < a.K; k += 256) w.hist[((size_t)h * a.plan.S + sg) * a.K + k] = cnt[k];
+    if (bad) report_index_error(a.status);
+}
+
+// One workgroup: exclusive prefix sums over the groups gi = h*K + k of their
+// step counts (positions; head h starts at h*B*L), item counts and partial
+// slots.  Thread t owns a contiguous range of groups.
+__global__ __launch_bounds__(1024) void k_dict_plan(DictGradArgs a) {
+    constexpr int T = 1024;
+    __shared__ int sh[3][T];
+    const DictWs w = dict_ws(a);
+    const int HK = a.H * a.K, t = threadIdx.x, P = a.plan.P, S = a.plan.S;
+    const int per = (HK + T - 1) / T;
+    const int g0 = min(t * per, HK), g1 = min(g0 + per, HK);
+    int sn = 0, si = 0, ss = 0;
+    for (int gi = g0; gi < g1; ++gi) {
+        const int h = gi / a.K, k = gi - h * a.K;
+        int n = 0;
+        for (int sg = 0; sg < S; ++sg) n += w.hist[((size_t)h * S + sg) * a.K + k];
+        w.n[gi] = n;
+        const int pieces = (n + P - 1) / P;
+        sn += n;
+        si += pieces;
+        ss += pieces >= 2 ? pieces : 0;
+    }
+    sh[0][t] = sn;
+    sh[1][t] = si;
+    sh[2][t] = ss;
+    __syncthreads();
+    for (int d = 1; d < T; d <<= 1) {
+        const int v0 = t >= d ? sh[0][t - d] : 0, v1 = t >= d ? sh[1][t - d] : 0, v2 = t >= d ? sh[2][t - d] : 0;
+        __syncthreads();
+        sh[0][t] += v0;
+        sh[1][t] += v1;
+        sh[2][t] += v2;
+        __syncthreads();
+    }
+    int pn = sh[0][t] - sn, pi = sh[1][t] - si, ps = sh[2][t] - ss;
+    for (int gi = g0; gi < g1; ++gi) {
+        const int n = w.n[gi];
+        const int pieces = (n + P - 1) / P;
+        w.pos[gi] = pn;
+        w.item[gi] = pi;
+        w.slot[gi] = pieces >= 2 ? ps : -1;
+        pn += n;
+        pi += pieces;
+        if (pieces >= 2) ps += pieces;
+    }
+    if (t == T - 1) w.item[HK] = sh[1][T - 1];
+}
+
+// Block x = h * S + segment.  Tiles of 256 steps in order; within a tile a
+// step's rank among the earlier steps with the same map comes from ballots
+// over the key bits (wave) and per-wave counts in LDS (tile), so the grouped
+// order keeps the steps of each group in increasing u.
+__global__ __launch_bounds__(256) void k_dict_scatter(DictGradArgs a) {
+    __shared__ int base[256];
+    __shared__ int wc[4][256];
+    const int h = blockIdx.x / a.plan.S, sg = blockIdx.x - h * a.plan.S;
+    const int t = threadIdx.x, wv = t >> 6, lane = t & 63;
+    const DictWs w = dict_ws(a);
+    for (int k = t; k < a.K; k += 256) {
+        int b = w.pos[h * a.K + k];
+        for (int s2 = 0; s2 < sg; ++s2) b += w.hist[((size_t)h * a.plan.S + s2) * a.K + k];
+        base[k] = b;
+        wc[0][k] = wc[1][k] = wc[2][k] = wc[3][k] = 0;
+    }
+    __syncthreads();
+    const long BL = (long)a.B * a.L;
+    const long u0 = (long)sg * a.plan.seg, u1 = min(u0 + (long)a.plan.seg, BL);
+    int nbits = 0;
+    while ((1 << nbits) < a.K) ++nbits;
+    const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+    bool bad = false;
+    for (long tb = u0; tb < u1; tb += 256) {
+        const long u = tb + t;
+        const bool valid = u < u1;
+        const int key = valid ? map_key(a.idx[u * a.H + h], a.K, bad) : 0;
+        uint64_t peers = __ballot(valid);
+        for (int bit = 0; bit < nbits; ++bit) {
+            const bool on = (key >> bit) & 1;
+            const uint64_t m = __ballot(on);
+            peers &= on ? m : ~m;
+        }
+        const int rank = __popcll(peers & below);
+        if (valid && rank == 0) wc[wv][key] = __popcll(peers);
+        __syncthreads();
+        if (valid) {
+            int p = base[key] + rank;
+            for (int w2 = 0; w2 < wv; ++w2) p += wc[w2][key];
+            w.order[p] = (int)u;
+        }
+        __syncthreads();
+        for (int k = t; k < a.K; k += 256) {
+            base[k] += wc[0][k] + wc[1][k] + wc[2][k] + wc[3][k];
+            wc[0][k] = wc[1][k] = wc[2][k] = wc[3][k] = 0;
+        }
+        __syncthreads();
+    }
+}
+
+// ------------------------------------------------------------------ outer products
+// A wave owns an NB x NB block of G[h,k] (NB = 64: 2 x 2 tiles of 32 x 32;
+// NB = 32 for N <= 32, rows and columns past N zero).  N <= 64: one block,
+// four waves each take a quarter of the item's steps and add up in LDS at
+// the end.  N = 128 / 256: 4 / 16 waves, one block each, every step.
+template <int N>
+struct DictCfg {
+    static constexpr int NB = N >= 64 ? 64 : 32;
+    static constexpr int GRID = N >= 64 ? N / 64 : 1;  // blocks per edge
+    static constexpr int BLOCKS = GRID * GRID;
+    static constexpr int SPLIT = BLOCKS >= 4 ? 1 : 4;
+    static constexpr int WAVES = BLOCKS * SPLIT;
+    static constexpr int TILES = NB / 32;
+    static constexpr int U = N >= 256 ? 4 : 8;  // steps per load batch (16 waves: 128 registers each)
+};
+
+// One step's operands: lane l holds g[i0 + l] and z[j0 + l] (NB = 64) or
+// g[i0 + l%32], z[j0 + l%32] (NB = 32).
+template <int N>
+__device__ __forceinline__ void load_step(const DictGradArgs& a, int u, int h, int i0, int j0, int lane, bool on,
+                                          float2& gv, float2& zv) {
+    constexpr int NB = DictCfg<N>::NB;
+    const int r = NB == 64 ? lane : (lane & 31);
+    gv = make_float2(0.f, 0.f);
+    zv = make_float2(0.f, 0.f);
+    if (on && (NB == 64 || r < N)) {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const size_t row = ((size_t)u * a.H + h) * N;
+        const f32x2 gq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.g + row + i0 + r));
+        const f32x2 zq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.z + row + j0 + r));
+        gv = make_float2(gq.x, gq.y);
+        zv = make_float2(zq.x, zq.y);
+    }
+}
+
+// acc[ti][tj] += A_ti B_tj with A[m][0..1] = (g[m].re, g[m].im) and
+// B[0..1][n] = (z[n].re, z[n].im): lane l supplies A[l%32][l/32] and
+// B[l/32][l%32].  NB = 64: a permlane32 swap of (re, im) gives both tiles'
+// operands: lanes 0-31 keep re of rows 0-31 and get im of rows 0-31 (tile 0),
+// and the other half the same for rows 32-63 (tile 1).
+template <int N>
+__device__ __forceinline__ void mfma_step(f32x16 (&acc)[DictCfg<N>::TILES][DictCfg<N>::TILES], float2 gv, float2 zv,
+                                          int lane) {
+    if constexpr (DictCfg<N>::NB == 64) {
+        const auto ga = __builtin_amdgcn_permlane32_swap(__float_as_uint(gv.x), __float_as_uint(gv.y), false, false);
+        const auto zb = __builtin_amdgcn_permlane32_swap(__float_as_uint(zv.x), __float_as_uint(zv.y), false, false);
+        const float A[2] = {__uint_as_float(ga[0]), __uint_as_float(ga[1])};
+        const float Bv[2] = {__uint_as_float(zb[0]), __uint_as_float(zb[1])};
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+            for (int tj = 0; tj < 2; ++tj)
+                acc[ti][tj] = __builtin_amdgcn_mfma_f32_32x32x2f32(A[ti], Bv[tj], acc[ti][tj], 0, 0, 0);
+    } else {
+        const float A = lane < 32 ? gv.x : gv.y;
+        const float Bv = lane < 32 ? zv.x : zv.y;
+        acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(A, Bv, acc[0][0], 0, 0, 0);
+    }
+}
+
+// Element r of tile (ti, tj) in lane l sits at row 32 ti + 8 (r/4) + 4 (l/32) + r%4,
+// column 32 tj + l%32 of the wave's block.
+__device__ __forceinline__ int acc_row(int ti, int r, int lane) { return 32 * ti + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+__device__ __forceinline__ int acc_col(int tj, int lane) { return 32 * tj + (lane & 31); }
+
+template <int N>
+__global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradArgs a) {
+    using Cfg = DictCfg<N>;
+    constexpr int NB = Cfg::NB, T = Cfg::TILES, U = Cfg::U;
+    __shared__ float red[Cfg::SPLIT > 1 ? Cfg::SPLIT - 1 : 1][Cfg::SPLIT > 1 ? NB * NB : 1];
+    const DictWs w = dict_ws(a);
+    const int HK = a.H * a.K;
+    const int item = blockIdx.x;
+    if (item >= w.item[HK]) return;
+    // the group holding this item: the last gi with item[gi] <= item
+    int lo = 0, hi = HK;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (w.item[mid] <= item) lo = mid;
+        else hi = mid;
+    }
+    const int gi = lo, h = gi / a.K;
+    const int pieces = w.item[gi + 1] - w.item[gi], piece = item - w.item[gi];
+    const int first = piece * a.plan.P;
+    const int cnt = min(a.plan.P, w.n[gi] - first);
+    const int* ord = w.order + w.pos[gi] + first;
+
+    const int wv = wave_id(), lane = lane_id();
+    const int blk = wv / Cfg::SPLIT, part = wv - blk * Cfg::SPLIT;
+    const int i0 = (blk / Cfg::GRID) * NB, j0 = (blk % Cfg::GRID) * NB;
+    const int s0 = (int)((long)cnt * part / Cfg::SPLIT), s1 = (int)((long)cnt * (part + 1) / Cfg::SPLIT);
+
+    f32x16 acc[T][T];
+#pragma unroll
+    for (int ti = 0; ti < T; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < T; ++tj)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[ti][tj][r] = 0.f;
+
+    // steps in runs of 64 ids (one per lane), operands in batches of U with
+    // the next batch in flight while the current one is multiplied
+    for (int s = s0; s < s1; s += 64) {
+        const int m = min(64, s1 - s);
+        const int sid = lane < m ? ord[s + lane] : 0;
+        float2 ga[U], za[U], gb[U], zb[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) load_step<N>(a, readlane_i(sid, u < m ? u : 0), h, i0, j0, lane, u < m, ga[u], za[u]);
+        for (int j = 0; j < m; j += 2 * U) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int jj = j + U + u;
+                load_step<N>(a, readlane_i(sid, jj < m ? jj : 0), h, i0, j0, lane, jj < m, gb[u], zb[u]);
+            }
+            issue_fence();
+#pragma unroll
+            for (int u = 0; u < U; ++u) mfma_step<N>(acc, ga[u], za[u], lane);
+            if (j + U >= m) break;
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int jj = j + 2 * U + u;
+                load_step<N>(a, readlane_i(sid, jj < m ? jj : 0), h, i0, j0, lane, jj < m, ga[u], za[u]);
+            }
+            issue_fence();
+#pragma unroll
+            for (int u = 0; u < U; ++u) mfma_step<N>(acc, gb[u], zb[u], lane);
+        }
+    }
+
+    if constexpr (Cfg::SPLIT > 1) {
+        if (part > 0) {
+#pragma unroll
+            for (int ti = 0; ti < T; ++ti)
+#pragma unroll
+                for (int tj = 0; tj < T; ++tj)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        red[part - 1][acc_row(ti, r, lane) * NB + acc_col(tj, lane)] = acc[ti][tj][r];
+        }
+        __syncthreads();
+        if (part > 0) return;
+#pragma unroll 1
+        for (int p = 0; p < Cfg::SPLIT - 1; ++p)
+#pragma unroll
+            for (int ti = 0; ti < T; ++ti)
+#pragma unroll
+                for (int tj = 0; tj < T; ++tj)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        acc[ti][tj][r] += red[p][acc_row(ti, r, lane) * NB + acc_col(tj, lane)];
+    }
+    float* dst = pieces == 1 ? a.G + (size_t)gi * N * N : w.partial + (size_t)(w.slot[gi] + piece) * N * N;
+#pragma unroll
+    for (int ti = 0; ti < T; ++ti)
+#pragma unroll
+        for (int tj = 0; tj < T; ++tj)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = i0 + acc_row(ti, r, lane), col = j0 + acc_col(tj, lane);
+                if (NB == 64 || (row < N && col < N)) dst[(size_t)row * N + col] = acc[ti][tj][r];
+            }
+}
+
+// Block (gi, y): groups of several items add their partials in item order;
+// groups no step chose get zeros; single-item groups were written directly.
+template <int N>
+__global__ __launch_bounds__(256) void k_dict_reduce(DictGradArgs a) {
+    const DictWs w = dict_ws(a);
+    const int gi = blockIdx.x;
+    const int pieces = w.item[gi + 1] - w.item[gi];
+    if (pieces == 1) return;
+    constexpr int NN = N * N;
+    float* dst = a.G + (size_t)gi * NN;
+    const float* src = w.partial + (size_t)(pieces ? w.slot[gi] : 0) * NN;
+    for (int e = blockIdx.y * 256 + threadIdx.x; e < NN; e += 256 * gridDim.y) {
+        float sum = 0.f;
+        for (int p = 0; p < pieces; ++p) sum += src[(size_t)p * NN + e];
+        dst[e] = sum;
+    }
+}
+
+template <int N>
+hipError_t dict_launch(const DictGradArgs& a, hipStream_t st) {
+    const int HK = a.H * a.K;
+    hipLaunchKernelGGL(k_dict_gemm<N>, dim3(a.plan.max_items), dim3(DictCfg<N>::WAVES * 64), 0, st, a);
+    const int ys = (N * N + 255) / 256 < 16 ? (N * N + 255) / 256 : 16;
+    hipLaunchKernelGGL(k_dict_reduce<N>, dim3(HK, ys), dim3(256), 0, st, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ tempered softmax
+// Thread per (o, j) of x [outer, len, inner]: three passes down the axis
+// (maximum, then the exponential sums, then the product).
+__global__ __launch_bounds__(256) void k_softmax_vjp(const float* __restrict__ x, const float* __restrict__ gy,
+                                                     float* __restrict__ gx, int64_t outer, int len, int64_t inner,
+                                                     float it) {
+    const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (id >= outer * inner) return;
+    const int64_t o = id / inner, j = id - o * inner;
+    const int64_t base = o * len * inner + j;
+    float m = -INFINITY;
+    for (int i = 0; i < len; ++i) m = fmaxf(m, x[base + i * inner] * it);
+    float se = 0.f, sg = 0.f;
+    for (int i = 0; i < len; ++i) {
+        const float e = expf(x[base + i * inner] * it - m);
+        se += e;
+        sg += e * gy[base + i * inner];
+    }
+    const float r = 1.f / se, dot = sg * r;
+    for (int i = 0; i < len; ++i) {
+        const float s = expf(x[base + i * inner] * it - m) * r;
+        gx[base + i * inner] = s * (gy[base + i * inner] - dot) * it;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_dict_grad(const DictGradArgs& a, hipStream_t st) {
+    const int nb = a.H * a.plan.S;
+    hipLaunchKernelGGL(k_dict_hist, dim3(nb), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_dict_plan, dim3(1), dim3(1024), 0, st, a);
+    hipLaunchKernelGGL(k_dict_scatter, dim3(nb), dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    switch (a.N) {
+        case 8: return dict_launch<8>(a, st);
+        case 16: return dict_launch<16>(a, st);
+        case 32: return dict_launch<32>(a, st);
+        case 64: return dict_launch<64>(a, st);
+        case 128: return dict_launch<128>(a, st);
+        case 256: return dict_launch<256>(a, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int len, int64_t inner,
+                              float inv_temp, hipStream_t st) {
+    const int64_t n = outer * inner;
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(k_softmax_vjp, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, x, gy, gx, outer, len,
+                       inner, inv_temp);
+    return hipGetLastError();
+}
+
+}  // namespace pdssm

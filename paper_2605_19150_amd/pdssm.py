@@ -9,6 +9,9 @@ Tensor layouts (all contiguous, on one GPU):
   idx [B,L,H] int32, pi [H,K,N] int32, D/b/c [B,L,H,N] complex64,
   h0/h_final/dh_final/dh0 [B,H,N] complex64, y/dy [B,L,H] float32,
   saved [B,H,C,N] complex64 (C = num_chunks).
+Straight-through surrogate gradients (Sec. 3.1 Prop. 2): q [B,L,H,K] float32,
+  z [B,L,H,N] complex64, G [H,K,N,N] float32, routing logits [B,L,H,K] and
+  dense dictionary M [H,K,N,N] float32.
 """
 import ctypes
 import os
@@ -19,7 +22,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpdssm.s
 _lib = None
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INDEX = 0, -1, -2, -3, -4, -5
-OP_FWD, OP_BWD, OP_COMPOSE = 1, 2, 3
+OP_FWD, OP_BWD, OP_COMPOSE, OP_DICT_GRAD = 1, 2, 3, 4
 FLAG_PREPARED = 1
 
 
@@ -37,7 +40,8 @@ class Desc(ctypes.Structure):
 
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
            "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
-           "pdssm_scan_bwd", "pdssm_compose_chunks")
+           "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_dict_grad",
+           "pdssm_softmax_vjp")
 
 
 def lib_path():
@@ -68,6 +72,13 @@ def load():
     L.pdssm_scan_bwd.restype = I
     L.pdssm_compose_chunks.argtypes = [D] + [P] * 7
     L.pdssm_compose_chunks.restype = I
+    L.pdssm_scan_bwd_ste.argtypes = [D] + [P] * 15 + [Z, P, P]
+    L.pdssm_scan_bwd_ste.restype = I
+    L.pdssm_dict_grad.argtypes = [D] + [P] * 5 + [Z, P, P]
+    L.pdssm_dict_grad.restype = I
+    L.pdssm_softmax_vjp.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int64,
+                                    ctypes.c_float, P]
+    L.pdssm_softmax_vjp.restype = I
     if L.pdssm_abi_version() != 1:
         raise ImportError("libpdssm.so ABI version mismatch")
     _lib = L
@@ -149,7 +160,7 @@ class Scan:
     prepare(pi) the scans reuse the tables in the workspace; call prepare()
     again whenever the contents of pi change."""
 
-    def __init__(self, B, L, H, N, K, chunk=0, device="cuda"):
+    def __init__(self, B, L, H, N, K, chunk=0, device="cuda", ste=False):
         self.d = desc(B, L, H, N, K, chunk)
         self.dp = desc(B, L, H, N, K, chunk)
         self.dp.flags = FLAG_PREPARED
@@ -173,6 +184,13 @@ class Scan:
         self.dc = torch.empty_like(self.dD)
         self.dh0 = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.ste = ste
+        if ste:
+            self.q = torch.empty((B, L, H, K), dtype=torch.float32, device=dev)
+            self.z = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
+            self.G = torch.empty((H, K, N, N), dtype=torch.float32, device=dev)
+            self.ws_dict = torch.empty(max(workspace_size(self.d, OP_DICT_GRAD), 1), dtype=torch.uint8,
+                                       device=dev)
 
     def _desc(self):
         return ctypes.byref(self.dp if self.prepared else self.d)
@@ -200,6 +218,25 @@ class Scan:
         if st != OK:
             raise PdssmError(st, "pdssm_scan_bwd")
         return self.dD, self.db, self.dc, self.dh0
+
+    def bwd_ste(self, idx, pi, D, b, c, dy, dh_final=None, stream=None):
+        """bwd() plus the straight-through scores q and the scaled states z
+        (Scan(..., ste=True))."""
+        st = load().pdssm_scan_bwd_ste(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
+                                       _p(self.saved), _p(dy), _p(dh_final), _p(self.dD), _p(self.db),
+                                       _p(self.dc), _p(self.dh0), _p(self.q), _p(self.z), _p(self.ws),
+                                       self.ws.numel(), _p(self.status), _stream(stream))
+        if st != OK:
+            raise PdssmError(st, "pdssm_scan_bwd_ste")
+        return self.dD, self.db, self.dc, self.dh0, self.q, self.z
+
+    def dict_grad(self, idx, stream=None):
+        """G [H,K,N,N] from the db and z of the last bwd_ste()."""
+        st = load().pdssm_dict_grad(ctypes.byref(self.d), _p(idx), _p(self.db), _p(self.z), _p(self.G),
+                                    _p(self.ws_dict), self.ws_dict.numel(), _p(self.status), _stream(stream))
+        if st != OK:
+            raise PdssmError(st, "pdssm_dict_grad")
+        return self.G
 
     def check_status(self):
         """Synchronise and raise if a kernel flagged an out-of-range index."""
@@ -257,3 +294,67 @@ def compose_chunks(idx, pi, D, chunk, stream=None):
     if int(status.item()) != OK:
         raise PdssmError(int(status.item()), "kernel index check")
     return pi_out, d_out
+
+
+def scan_bwd_ste(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
+    """Returns (dD, db, dc, dh0, q [B,L,H,K] f32, z [B,L,H,N] c64)."""
+    B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
+    s = Scan(B, L, H, N, K, chunk, dev, ste=True)
+    _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
+    _need(dy, "dy", torch.float32, (B, L, H), dev)
+    if dh_final is not None:
+        _need(dh_final, "dh_final", torch.complex64, (B, H, N), dev)
+    s.saved = saved
+    out = s.bwd_ste(idx, pi, D, b, c, dy, dh_final, stream)
+    s.check_status()
+    return out
+
+
+def dict_grad(idx, g, z, K, stream=None):
+    """G [H,K,N,N] f32: per head and map, the sum of Re(g_t z_t^H) over the
+    steps that chose the map (g = db and z from scan_bwd_ste)."""
+    B, L, H = idx.shape
+    N = g.shape[3]
+    dev = idx.device
+    _need(idx, "idx", torch.int32, (B, L, H), dev)
+    _need(g, "g", torch.complex64, (B, L, H, N), dev)
+    _need(z, "z", torch.complex64, (B, L, H, N), dev)
+    d = desc(B, L, H, N, K)
+    ws = torch.empty(max(workspace_size(d, OP_DICT_GRAD), 1), dtype=torch.uint8, device=dev)
+    G = torch.empty((H, K, N, N), dtype=torch.float32, device=dev)
+    status = torch.zeros(1, dtype=torch.int32, device=dev)
+    st = load().pdssm_dict_grad(ctypes.byref(d), _p(idx), _p(g), _p(z), _p(G), _p(ws), ws.numel(),
+                                _p(status), _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_dict_grad")
+    torch.cuda.synchronize(dev)
+    if int(status.item()) != OK:
+        raise PdssmError(int(status.item()), "kernel index check")
+    return G
+
+
+def softmax_vjp(x, gy, dim, temp, out=None, stream=None):
+    """gx = s * (gy - sum(s * gy, dim)) / temp with s = softmax(x / temp, dim)."""
+    if x.dtype != torch.float32 or gy.dtype != torch.float32 or x.shape != gy.shape:
+        raise TypeError("x and gy must be float32 tensors of one shape")
+    if not (x.is_contiguous() and gy.is_contiguous()) or x.device.type != "cuda" or gy.device != x.device:
+        raise ValueError("x and gy must be contiguous and on one GPU")
+    dim = dim % x.dim()
+    outer = 1
+    for n in x.shape[:dim]:
+        outer *= int(n)
+    inner = 1
+    for n in x.shape[dim + 1:]:
+        inner *= int(n)
+    gx = torch.empty_like(x) if out is None else out
+    _need(gx, "out", torch.float32, tuple(x.shape), x.device)
+    st = load().pdssm_softmax_vjp(_p(x), _p(gy), _p(gx), outer, int(x.shape[dim]), inner, float(temp),
+                                  _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_softmax_vjp")
+    return gx
+
+
+def surrogate_grads(q, G, logits, M, temp, stream=None):
+    """The two surrogate gradients of Prop. 2: (d logits [B,L,H,K], dM [H,K,N,N])."""
+    return softmax_vjp(logits, q, 3, temp, stream=stream), softmax_vjp(M, G, 2, temp, stream=stream)

@@ -26,3 +26,39 @@ def assert_close(name, got, ref, rtol=RTOL, atol=ATOL):
         i = np.unravel_index(np.argmax(err - tol), err.shape)
         raise AssertionError("%s: %d/%d components out of tolerance; worst at %s: got %r ref %r"
                              % (name, int(bad.sum()), bad.size, i, g[i], r[i]))
+
+
+def assert_close_sum(name, got, ref, scale, rtol=RTOL, atol=ATOL):
+    """Bar for a quantity that is a sum of products of scan outputs (the
+    straight-through scores q and the dictionary gradient G): |got - ref| <=
+    atol + rtol*scale, where scale >= |ref| is the sum of the magnitudes of the
+    summands.  Each factor is itself only known to the scan's bar (1e-4
+    relative), so a sum whose terms cancel inherits an error proportional to
+    the size of its terms, not of its result."""
+    g, r, s = np.asarray(got, np.float64), np.asarray(ref, np.float64), np.asarray(scale, np.float64)
+    assert g.shape == r.shape == s.shape, (name, g.shape, r.shape, s.shape)
+    assert (s >= np.abs(r) * (1 - 1e-9) - 1e-300).all(), name + ": scale below |ref|"
+    err = np.abs(g - r)
+    tol = atol + rtol * s
+    bad = ~(err <= tol)
+    if bad.any():
+        i = np.unravel_index(np.argmax(err - tol), err.shape)
+        raise AssertionError("%s: %d/%d components out of tolerance; worst at %s: got %r ref %r scale %r"
+                             % (name, int(bad.sum()), bad.size, i, g[i], r[i], s[i]))
+
+
+def ste_scales(pi, idx, g, z):
+    """Magnitude sums for assert_close_sum: qs[b,t,h,k] = sum_j |g_t[pi_k(j)]| |z_t[j]|
+    and Gs[h,k,i,j] = sum over the steps that chose k of |g_t[i]| |z_t[j]|."""
+    ag, az = np.abs(g), np.abs(z)
+    B, L, H, N = ag.shape
+    K = pi.shape[1]
+    qs = np.empty((B, L, H, K))
+    Gs = np.zeros((H, K, N, N))
+    for h in range(H):
+        qs[:, :, h, :] = np.einsum("blkn,bln->blk", ag[:, :, h, :][:, :, pi[h]], az[:, :, h, :])
+        for k in range(K):
+            m = idx[:, :, h] == k
+            if m.any():
+                Gs[h, k] = ag[:, :, h][m].T @ az[:, :, h][m]
+    return qs, Gs

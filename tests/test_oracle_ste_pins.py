@@ -176,3 +176,18 @@ def test_selection_inputs_agree_with_the_hard_choices():
     logits, M = selection_inputs(inp["idx"], inp["pi"], seed=5)
     np.testing.assert_array_equal(logits.argmax(axis=3), inp["idx"])
     np.testing.assert_array_equal(M.argmax(axis=2), inp["pi"])
+
+
+def test_scaled_states_are_d_times_previous_state():
+    from oracle import oracle_fwd
+    inp = make_inputs(2, 9, 2, 5, 3, seed=11, with_h0=True)
+    _, _, z = oracle_ste(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"],
+                         want_z=True)
+    # h_{t-1} from prefix runs of the forward: the final state of steps 0..t-1
+    for t in range(9):
+        if t == 0:
+            hp = inp["h0"].astype(np.complex128)
+        else:
+            sub = {k: np.ascontiguousarray(inp[k][:, :t]) for k in ("idx", "D", "b", "c")}
+            _, hp, _ = oracle_fwd(sub["idx"], inp["pi"], sub["D"], sub["b"], sub["c"], h0=inp["h0"])
+        np.testing.assert_allclose(z[:, t], inp["D"][:, t].astype(np.complex128) * hp, rtol=1e-13, atol=1e-14)
