@@ -19,6 +19,12 @@ peak; traffic = the HBM bytes per launch that rocprofv3 counters measured for
 the same kernel source (profiles/), else null.
 cpu_baseline = the float64 oracle timed on a bounded sample of the same
 workload on this host's cores.
+
+--ste times the straight-through training step instead (Sec. 3.1 Prop. 2):
+prepare, forward, the backward with the scaled states (pdssm_scan_bwd_ste),
+the candidate-map scores and the dictionary gradient (pdssm_ste_grads) and
+the two tempered-softmax products (routing logits, dense dictionary); the
+line then carries an "ste" object with each call's time and roofline.
 """
 import argparse
 import json
@@ -32,6 +38,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_FP32_PEAK_TFS = 157.3
 FLUSH_BYTES = 512 << 20
 METRIC = "PD-scan state-updates/s (B*L*H*N) fwd and fwd+bwd; achieved HBM GB/s vs peak"
 
@@ -47,6 +54,23 @@ def alg_bytes(w, C, op):
         return steps * 4 + 3 * su * 8 + dict_b + steps * 4 + B * H * N * 8 + B * H * C * N * 8
     # idx, dy, D, b, c, saved in; dD, db, dc, dh0 out
     return steps * 8 + 3 * su * 8 + dict_b + B * H * C * N * 8 + 3 * su * 8 + B * H * N * 8
+
+
+def ste_bytes(w, C):
+    """Algorithmic bytes and flops of the straight-through calls."""
+    B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
+    steps = B * L * H
+    su = steps * N
+    return {
+        # the plain backward, plus z [B,L,H,N] c64 written
+        "bwd_ste": alg_bytes(w, C, "bwd") + su * 8,
+        # idx, pi, g (= db) and z read once, q [B,L,H,K] and G [H,K,N,N] f32 written once
+        "ste_grads": steps * 4 + H * K * N * 4 + 2 * su * 8 + steps * K * 4 + H * K * N * N * 4,
+        # per step and (i, j): Re(g_i conj z_j) = two real multiply-adds
+        "ste_grads_flops": 4 * steps * N * N,
+        # logits and q in, d logits out; M and G in, dM out
+        "softmax": 3 * steps * K * 4 + 3 * H * K * N * N * 4,
+    }
 
 
 def cpu_baseline(w, inp, target_s=12.0, max_threads=16, sample_seqs=32):
@@ -108,6 +132,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", choices=["fwd", "bwd", "both"], default="both",
                     help="profiling aid: launch only one call per step")
+    ap.add_argument("--ste", action="store_true",
+                    help="time the straight-through step (scores, dictionary gradient, softmax products)")
+    ap.add_argument("--temp", type=float, default=1.0, help="softmax temperature of --ste")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling aid: time a plain 1 GiB device copy instead")
     args = ap.parse_args()
@@ -144,7 +171,12 @@ def main():
           flush=True)
     inp = workload_inputs(args.workload, seed=0)
     T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
-    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K)
+    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste)
+    if args.ste:
+        from paper_2605_19150_amd.inputs import selection_inputs
+        logits, M = selection_inputs(inp["idx"], inp["pi"], seed=0)
+        T["logits"], T["M"] = torch.from_numpy(logits).to(dev), torch.from_numpy(M).to(dev)
+        dlogits, dM = torch.empty_like(T["logits"]), torch.empty_like(T["M"])
     stream = torch.cuda.current_stream()
     # Written between timed steps so that no input is still in L2 / MALL.
     flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
@@ -158,8 +190,17 @@ def main():
             s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
         rec(2)
         if args.only in ("bwd", "both"):
-            s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
+            if args.ste:
+                s.bwd_ste(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
+            else:
+                s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
         rec(3)
+        if args.ste:
+            s.ste_grads(T["idx"], T["pi"])
+            rec(4)
+            pdssm.softmax_vjp(T["logits"], s.q, 3, args.temp, out=dlogits)
+            pdssm.softmax_vjp(T["M"], s.G, 2, args.temp, out=dM)
+            rec(5)
 
     if args.only == "bwd":
         s.prepare(T["pi"])
@@ -171,7 +212,8 @@ def main():
     s.check_status()
     print("bench: timing %d steps" % args.steps, file=sys.stderr, flush=True)
 
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    nev = 6 if args.ste else 4
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nev)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -182,7 +224,7 @@ def main():
     prep_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     fwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    ms_step = float(np.mean([e[0].elapsed_time(e[3]) for e in evs]))
+    ms_step = float(np.mean([e[0].elapsed_time(e[nev - 1]) for e in evs]))
     s.check_status()
 
     su = w.state_updates
@@ -208,7 +250,9 @@ def main():
         "dtype": "f32",
         "data": "synthetic (seeded, shapes and distributions of the named workload)",
         "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
-                   "chunk": s.chunk, "step": "prepare+fwd+bwd" if args.only == "both" else args.only,
+                   "chunk": s.chunk,
+                   "step": ("prepare+fwd+bwd_ste+ste_grads+softmax_vjp" if args.ste else "prepare+fwd+bwd")
+                   if args.only == "both" else args.only,
                    "global_batch": w.B, "seq_len": w.L, "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "kernel": kern[dom],
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -220,11 +264,34 @@ def main():
         "bwd": {"kernel": kern["bwd"], "ms": bwd_ms, "state_updates_per_s": su / (bwd_ms * 1e-3),
                 "alg_bytes": bwd_b, "alg_GBps": bwd_b / (bwd_ms * 1e-3) / 1e9,
                 "frac": bwd_b / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        "fwd_bwd_alg_GBps": (fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9,
+        "fwd_bwd_alg_GBps": (fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9 if not args.ste else None,
         "wall_s_timed": wall,
         "device": torch.cuda.get_device_name(dev),
     }
-    if not args.no_cpu_baseline and args.only == "both":
+    if args.ste:
+        sb = ste_bytes(w, s.C)
+        out["bwd"]["alg_bytes"] = sb["bwd_ste"]
+        out["bwd"]["kernel"] = kern["bwd"] + " (+ z)"
+        out["bwd"]["alg_GBps"] = sb["bwd_ste"] / (bwd_ms * 1e-3) / 1e9
+        out["bwd"]["frac"] = out["bwd"]["alg_GBps"] / HBM_PEAK_GBS
+        out["roofline"]["achieved"] = out["bwd"]["alg_GBps"] if dom == "bwd" else achieved
+        out["roofline"]["frac"] = out["roofline"]["achieved"] / HBM_PEAK_GBS
+        out["roofline"]["traffic"] = traffic_from_profiles("k_bwd_fused_ste", w.name) if fused else None
+        out["roofline"]["kernel"] = kern[dom] + (" (+ z)" if dom == "bwd" else "")
+        dg_ms = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
+        sm_ms = float(np.mean([e[4].elapsed_time(e[5]) for e in evs]))
+        gbps = sb["ste_grads"] / (dg_ms * 1e-3) / 1e9
+        tfs = sb["ste_grads_flops"] / (dg_ms * 1e-3) / 1e12
+        out["ste"] = {
+            "temp": args.temp,
+            "ste_grads": {"ms": dg_ms, "alg_bytes": sb["ste_grads"], "alg_GBps": gbps,
+                          "frac_hbm": gbps / HBM_PEAK_GBS, "flops": sb["ste_grads_flops"],
+                          "TFLOPs": tfs, "frac_mfma_fp32": tfs / MFMA_FP32_PEAK_TFS,
+                          "traffic": traffic_from_profiles("k_ste_gemm", w.name)},
+            "softmax_vjp": {"ms": sm_ms, "alg_bytes": sb["softmax"],
+                            "alg_GBps": sb["softmax"] / (sm_ms * 1e-3) / 1e9},
+        }
+    if not args.no_cpu_baseline and args.only == "both" and not args.ste:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(out), flush=True)

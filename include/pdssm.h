@@ -99,7 +99,7 @@ typedef enum pdssm_op {
     PDSSM_OP_FWD = 1,
     PDSSM_OP_BWD = 2,
     PDSSM_OP_COMPOSE = 3,
-    PDSSM_OP_DICT_GRAD = 4
+    PDSSM_OP_STE_GRADS = 4
 } pdssm_op;
 
 /* ABI version of the loaded library (PDSSM_ABI_VERSION at build time). */
@@ -183,47 +183,46 @@ int pdssm_scan_bwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi
                    void* ws, size_t ws_bytes, int* dev_status, void* stream);
 
 /*
- * Backward scan with the straight-through surrogate inputs of the hard map
+ * Backward scan for the straight-through surrogate gradients of the hard map
  * selection (Sec. 3.1 Prop. 2 and its derivation in the appendix).  Does
  * everything pdssm_scan_bwd does (same arguments, same results) and also
- * writes, when the pointers are not NULL:
- *   q [B,L,H,K] float32: q[b,t,h,k] = sum_j Re(g_t[pi[h,k,j]] * conj(z_t[j])),
- *       the gradient of the loss with respect to the weight of dictionary map
- *       k at step t when P_t = sum_k v_t[k] P_k, taken at the one-hot v_t of
- *       the forward (g_t = db_t is the gradient reaching h_t).  Apply
- *       pdssm_softmax_vjp over k with the routing logits to get their
- *       surrogate gradient.
- *   z [B,L,H,N] complex: z_t = D_t .* h_{t-1}, the state entering the map of
- *       step t (h_{-1} = h0), which pdssm_dict_grad needs with db.
- * Same workspace as pdssm_scan_bwd (PDSSM_OP_BWD).  q and z must not overlap
- * any other argument.  The scores cost O(N*K) LDS reads per step.
+ * writes z [B,L,H,N] complex (required): z_t = D_t .* h_{t-1} (h_{-1} = h0),
+ * the state entering the map of step t, which pdssm_ste_grads needs together
+ * with db (the gradient g_t reaching h_t).  Same workspace as pdssm_scan_bwd
+ * (PDSSM_OP_BWD).  z must not overlap any other argument.
  */
 int pdssm_scan_bwd_ste(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
                        const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
                        const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
                        pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
-                       float* q, pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status,
-                       void* stream);
+                       pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status, void* stream);
 
 /*
- * Dictionary gradient of the straight-through estimator (Sec. 3.1 Prop. 2):
- *   G[h,k,i,j] = sum over the steps (b,t) with idx[b,t,h] == k of
- *                Re(g[b,t,h,i] * conj(z[b,t,h,j])),
- * the gradient of the loss with respect to the real N x N matrix P_k (row i =
- * destination, column j = source, so column j of P_k has its one in row
- * pi[h,k,j]).  g = db and z from pdssm_scan_bwd_ste.  Apply
- * pdssm_softmax_vjp down the columns of the dense dictionary M[h,k] to get
- * its surrogate gradient.  Maps no step chose get zeros.  The sum over steps
- * runs in a fixed order (deterministic).
- * In:  idx [B,L,H], g, z [B,L,H,N] (desc->chunk is ignored).
- * Out: G [H,K,N,N] float32 (required).
- * ws:  at least pdssm_workspace_size(desc, PDSSM_OP_DICT_GRAD) bytes, 256-byte
+ * The inputs of the two straight-through surrogate gradients (Sec. 3.1
+ * Prop. 2), from g = db and z of pdssm_scan_bwd_ste.  With P_t the real
+ * N x N matrix of step t (column j has its one in row pi_t[j]), the loss
+ * gradient for P_t is dP_t[i][j] = Re(g_t[i] * conj(z_t[j])), and:
+ *   q [B,L,H,K] float32 (optional): q[b,t,h,k] = <dP_t, P_k> =
+ *       sum_j Re(g_t[pi[h,k,j]] * conj(z_t[j])), the gradient with respect to
+ *       the weight of map k at step t when P_t = sum_k v_t[k] P_k, at the
+ *       one-hot v_t of the forward.  pdssm_softmax_vjp over k with the
+ *       routing logits turns it into their surrogate gradient.
+ *   G [H,K,N,N] float32 (optional): G[h,k,i,j] = sum over the steps (b,t)
+ *       with idx[b,t,h] == k of dP_t[i][j], the gradient of dictionary matrix
+ *       P_k (row i = destination, column j = source).  pdssm_softmax_vjp down
+ *       the columns of the dense dictionary M[h,k] turns it into its surrogate
+ *       gradient.  Maps no step chose get zeros.
+ * At least one of q, G.  The steps are grouped by map (a stable counting
+ * sort) and every sum runs in a fixed order (deterministic results).
+ * In:  idx [B,L,H], pi [H,K,N] (needed for q), g, z [B,L,H,N]; desc->chunk
+ *      is ignored.
+ * ws:  at least pdssm_workspace_size(desc, PDSSM_OP_STE_GRADS) bytes, 256-byte
  *      aligned.  An idx entry outside [0,K) counts as map 0 and is reported
- *      through *dev_status.
+ *      through *dev_status; a pi entry outside [0,N) reads row 0.
  */
-int pdssm_dict_grad(const pdssm_desc* desc, const int32_t* idx, const pdssm_c64* g,
-                    const pdssm_c64* z, float* G, void* ws, size_t ws_bytes, int* dev_status,
-                    void* stream);
+int pdssm_ste_grads(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
+                    const pdssm_c64* g, const pdssm_c64* z, float* q, float* G, void* ws,
+                    size_t ws_bytes, int* dev_status, void* stream);
 
 /*
  * Vector-Jacobian product of the tempered softmax that stands in for a hard
@@ -234,7 +233,8 @@ int pdssm_dict_grad(const pdssm_desc* desc, const int32_t* idx, const pdssm_c64*
  * Routing logits [B,L,H,K] with q: outer = B*L*H, len = K, inner = 1.
  * Dense dictionary M [H,K,N,N] with G: outer = H*K, len = N, inner = N (the
  * softmax runs down each column, where the argmax gives pi[h,k,j]).
- * x, gy, gx float32 device arrays; gx must not overlap x or gy; temp > 0.
+ * x, gy, gx float32 device arrays; gx must not overlap x or gy; temp > 0;
+ * outer*inner < 2^31 and outer*len*inner <= 2^40 (else PDSSM_ERR_UNSUPPORTED).
  * Needs no workspace.
  */
 int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int32_t len,

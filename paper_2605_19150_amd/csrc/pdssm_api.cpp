@@ -280,7 +280,7 @@ int pdssm_num_chunks(const pdssm_desc* d) {
 
 size_t pdssm_workspace_size(const pdssm_desc* d, int op) {
     if (op == PDSSM_OP_COMPOSE) return check_dims(d) == PDSSM_OK ? 0 : (size_t)-1;
-    if (op == PDSSM_OP_DICT_GRAD)
+    if (op == PDSSM_OP_STE_GRADS)
         return check_dims(d) == PDSSM_OK ? pdssm::dict_plan(d->B, d->L, d->H, d->N, d->K).bytes : (size_t)-1;
     if (op != PDSSM_OP_FWD && op != PDSSM_OP_BWD) return (size_t)-1;
     int tau = scan_chunk(d);
@@ -378,7 +378,7 @@ namespace {
 int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, const pdssm_c64* D,
                   const pdssm_c64* b, const pdssm_c64* c, const pdssm_c64* saved, const float* dy,
                   const pdssm_c64* dh_final, pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
-                  float* q, pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+                  pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status, void* stream) {
     int tau = scan_chunk(d);
     if (tau < 0) return tau;
     if (!idx || !pi || !D || !b || !c || !saved || !dy || !dD || !db || !dc)
@@ -392,9 +392,9 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     const size_t need = ws_bytes_for(s, d, a.C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
-    if (misaligned(z) || (reinterpret_cast<uintptr_t>(q) & 3) != 0) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned(z)) return PDSSM_ERR_INVALID_ARG;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * 8;
-    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {q, nidx * d->K}, {z, nst}, {ws, need}},
+    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, nst}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * 8},
                      {dy, nidx}, {dh_final, s.seqN * 8}}))
         return PDSSM_ERR_INVALID_ARG;
@@ -409,7 +409,6 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     a.db = reinterpret_cast<float2*>(db);
     a.dc = reinterpret_cast<float2*>(dc);
     a.dh0 = reinterpret_cast<float2*>(dh0);
-    a.q = q;
     a.z = reinterpret_cast<float2*>(z);
     a.status = dev_status;
     const hipStream_t st = static_cast<hipStream_t>(stream);
@@ -417,7 +416,6 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     if (use_fused(d)) {
         pdssm::FusedArgs f = fused_base(a);
         f.saved = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
-        f.q = q;
         f.z = reinterpret_cast<float2*>(z);
         e = prep_fused(f, d, pi, ws, s, dev_status, st, false);
         if (e == hipSuccess) e = pdssm::launch_bwd_fused(f, st);
@@ -436,55 +434,61 @@ int pdssm_scan_bwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
                    const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
                    pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
                    void* ws, size_t ws_bytes, int* dev_status, void* stream) {
-    return scan_bwd_impl(d, idx, pi, D, b, c, saved, dy, dh_final, dD, db, dc, dh0, nullptr, nullptr, ws,
-                         ws_bytes, dev_status, stream);
+    return scan_bwd_impl(d, idx, pi, D, b, c, saved, dy, dh_final, dD, db, dc, dh0, nullptr, ws, ws_bytes,
+                         dev_status, stream);
 }
 
 int pdssm_scan_bwd_ste(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
                        const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
                        const pdssm_c64* saved, const float* dy, const pdssm_c64* dh_final,
                        pdssm_c64* dD, pdssm_c64* db, pdssm_c64* dc, pdssm_c64* dh0,
-                       float* q, pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status,
-                       void* stream) {
-    return scan_bwd_impl(d, idx, pi, D, b, c, saved, dy, dh_final, dD, db, dc, dh0, q, z, ws, ws_bytes,
-                         dev_status, stream);
+                       pdssm_c64* z, void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+    if (!z) return PDSSM_ERR_INVALID_ARG;
+    return scan_bwd_impl(d, idx, pi, D, b, c, saved, dy, dh_final, dD, db, dc, dh0, z, ws, ws_bytes, dev_status,
+                         stream);
 }
 
-int pdssm_dict_grad(const pdssm_desc* d, const int32_t* idx, const pdssm_c64* g, const pdssm_c64* z,
-                    float* G, void* ws, size_t ws_bytes, int* dev_status, void* stream) {
+int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, const pdssm_c64* g,
+                    const pdssm_c64* z, float* q, float* G, void* ws, size_t ws_bytes, int* dev_status,
+                    void* stream) {
     const int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (!idx || !g || !z || !G) return PDSSM_ERR_INVALID_ARG;
-    if (misaligned(g) || misaligned(z) || (reinterpret_cast<uintptr_t>(G) & 3) != 0)
+    if (!idx || !g || !z || (!q && !G) || (q && !pi)) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned(g) || misaligned(z) || misaligned(pi) || (reinterpret_cast<uintptr_t>(G) & 3) != 0 ||
+        (reinterpret_cast<uintptr_t>(q) & 3) != 0)
         return PDSSM_ERR_INVALID_ARG;
     const pdssm::DictPlan plan = pdssm::dict_plan(d->B, d->L, d->H, d->N, d->K);
     if (!ws || ws_bytes < plan.bytes || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     const size_t nidx = (size_t)d->B * d->L * d->H * 4, nst = nidx / 4 * d->N * 8;
-    const size_t nG = (size_t)d->H * d->K * d->N * d->N * 4;
-    if (any_overlap({{G, nG}, {ws, plan.bytes}}, {{idx, nidx}, {g, nst}, {z, nst}})) return PDSSM_ERR_INVALID_ARG;
-    pdssm::DictGradArgs a = {};
+    const size_t nG = (size_t)d->H * d->K * d->N * d->N * 4, npi = (size_t)d->H * d->K * d->N * 4;
+    if (any_overlap({{G, nG}, {q, nidx * d->K}, {ws, plan.bytes}}, {{idx, nidx}, {g, nst}, {z, nst}, {pi, npi}}))
+        return PDSSM_ERR_INVALID_ARG;
+    pdssm::SteGradArgs a = {};
     a.B = d->B;
     a.L = d->L;
     a.H = d->H;
     a.N = d->N;
     a.K = d->K;
     a.idx = idx;
+    a.pi = pi;
     a.g = reinterpret_cast<const float2*>(g);
     a.z = reinterpret_cast<const float2*>(z);
+    a.q = q;
     a.G = G;
     a.plan = plan;
     a.ws = static_cast<unsigned char*>(ws);
     a.status = dev_status;
-    return pdssm::launch_dict_grad(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+    return pdssm::launch_ste_grads(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
 int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int32_t len, int64_t inner,
                       float temp, void* stream) {
     if (!x || !gy || !gx || outer < 0 || len < 1 || inner < 1) return PDSSM_ERR_INVALID_ARG;
     if (!(temp > 0.f) || temp > 3.0e38f) return PDSSM_ERR_INVALID_ARG;
-    // one thread per (outer, inner) fibre: keep the grid below 2^30 blocks
-    if (outer > (1LL << 40) / len / inner || outer > (1LL << 38) / inner) return PDSSM_ERR_UNSUPPORTED;
+    // up to 64 lanes per (outer, inner) fibre: fewer than 2^31 fibres keeps
+    // the grid below 2^29 blocks
+    if (outer > (1LL << 40) / len / inner || outer >= (1LL << 31) / inner) return PDSSM_ERR_UNSUPPORTED;
     const size_t n = (size_t)outer * len * inner * 4;
     if (((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(gy) | reinterpret_cast<uintptr_t>(gx)) & 3) != 0)
         return PDSSM_ERR_INVALID_ARG;

@@ -451,20 +451,12 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
             }
             st_cv<SL>(a.dD + off, lane, dDt);
         }
-        if (a.q || a.z) {
-            // straight-through scores of every map against g_t (still in X)
-            // and the scaled state z_t = D_t .* h_{t-1}
+        if (a.z && act) {
+            // the scaled state z_t = D_t .* h_{t-1} for the straight-through gradients
             CV<SL> zt;
 #pragma unroll
             for (int s = 0; s < SL; ++s) zt.v[s] = cmul(Dt.v[s], hp.v[s]);
-            if (a.z && act) st_cv<SL>(a.z + off, lane, zt);
-            if (a.q)
-                ste_scores<N>(X, zt, lane, act, a.K,
-                              [pih](int k, int j) {
-                                  const int p = pih[(size_t)k * N + j];
-                                  return (unsigned)p < (unsigned)N ? p : 0;  // reported by k_bwd_agg
-                              },
-                              a.q + (((size_t)bb * a.L + s0 + t) * a.H + hh) * a.K, true);
+            st_cv<SL>(a.z + off, lane, zt);
         }
     }
 }

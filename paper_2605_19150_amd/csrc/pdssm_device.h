@@ -321,35 +321,4 @@ __device__ __forceinline__ float transpose_sum(float (&v)[T], int lane) {
     return v[0];
 }
 
-// ------------------------------------------------------------------ surrogate scores
-// Straight-through score of every dictionary map at one step (Sec. 3.1
-// Prop. 2): q[k] = sum_j Re(g[pi_k(j)] * conj(z[j])) for k = 0..K-1, where
-// g (the gradient reaching h_t, N values) is staged in LDS at Gs, z = D_t .* h_{t-1}
-// is held by the lanes (entry lane*SL + s) and map(k, j) returns pi_k(j) in
-// [0, N).  Maps go in blocks of 16: per-lane partial sums, then one
-// transpose-reduction leaves the total of map kb + l/4 in lane l.  Every lane
-// of the wave must call it (K uniform); lanes l % 4 == 0 store when `store`.
-template <int N, class MapFn>
-__device__ __forceinline__ void ste_scores(const float2* __restrict__ Gs, const CV<Lay<N>::SL>& z, int lane,
-                                           bool act, int K, MapFn map, float* __restrict__ qrow, bool store) {
-    constexpr int SL = Lay<N>::SL;
-    for (int kb = 0; kb < K; kb += 16) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-            v[u] = 0.f;
-            if (act && kb + u < K) {
-#pragma unroll
-                for (int s = 0; s < SL; ++s) {
-                    const float2 g = Gs[map(kb + u, lane * SL + s)];
-                    v[u] = fmaf(g.x, z.v[s].x, fmaf(g.y, z.v[s].y, v[u]));
-                }
-            }
-        }
-        const float tot = transpose_sum<16>(v, lane);
-        const int k = kb + (lane >> 2);
-        if (store && (lane & 3) == 0 && k < K) qrow[k] = tot;
-    }
-}
-
 }  // namespace pdssm

@@ -116,9 +116,8 @@ struct FusedArgs {
     float2* segA;
     float2* segD;
     int* segP;
-    // Backward only, optional: straight-through scores q [B,L,H,K] and the
-    // scaled states z = D_t .* h_{t-1} [B,L,H,N] (Sec. 3.1 Prop. 2).
-    float* q;
+    // Backward only, optional: the scaled states z = D_t .* h_{t-1}
+    // [B,L,H,N] that the straight-through gradients need (Sec. 3.1 Prop. 2).
     float2* z;
 };
 

@@ -1227,16 +1227,12 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
             if (in) st_out<SL>(a.dD + off, lane, dDt);
         }
         if constexpr (STE) {
-            // straight-through scores of every map against g_t (still in
-            // st.V) and the scaled state z_t = D_t .* h_{t-1}
-            CV<SL> zt;
+            // the scaled state z_t = D_t .* h_{t-1} for the straight-through gradients
+            if (act && in) {
+                CV<SL> zt;
 #pragma unroll
-            for (int i = 0; i < SL; ++i) zt.v[i] = cmul(Dt(q, t).v[i], Hs[t].v[i]);
-            if (a.z && act && in) st_out<SL>(a.z + off, lane, zt);
-            if (a.q) {
-                const uint8_t* dict = s.dict;
-                ste_scores<N>(st.V, zt, lane, act, a.K, [dict](int k, int j) { return (int)dict[k * N + j]; },
-                              a.q + (((size_t)w.bb * a.L + s0 + t) * a.H + w.hh) * a.K, in);
+                for (int i = 0; i < SL; ++i) zt.v[i] = cmul(Dt(q, t).v[i], Hs[t].v[i]);
+                st_out<SL>(a.z + off, lane, zt);
             }
         }
     }
@@ -1366,8 +1362,8 @@ hipError_t bwd_launch(const FusedArgs& a, hipStream_t st) {
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3(W * 64), a.lds.total, st, a);
     }
-    // the straight-through outputs are computed by the scan pass only
-    auto kern = a.q || a.z ? k_bwd_fused<N, TAU, W, false, true> : k_bwd_fused<N, TAU, W, false, false>;
+    // the scaled states for the straight-through gradients come from the scan pass only
+    auto kern = a.z ? k_bwd_fused<N, TAU, W, false, true> : k_bwd_fused<N, TAU, W, false, false>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;

@@ -36,9 +36,8 @@ struct ScanArgs {
     float2* agg_v;
     float2* U;       // bwd: gradient reaching the last state of each chunk from later chunks
     int* status;
-    // bwd, optional: straight-through scores q [B,L,H,K] and scaled states
-    // z = D_t .* h_{t-1} [B,L,H,N] (Sec. 3.1 Prop. 2)
-    float* q;
+    // bwd, optional: the scaled states z = D_t .* h_{t-1} [B,L,H,N] that
+    // the straight-through gradients need (Sec. 3.1 Prop. 2)
     float2* z;
 };
 
@@ -53,8 +52,9 @@ struct ComposeArgs {
     int* status;
 };
 
-// Dictionary gradient of the straight-through estimator (Sec. 3.1 Prop. 2):
-// G[h,k] = sum over the steps (b,t) with idx[b,t,h] == k of Re(g_t z_t^H).
+// Straight-through surrogate inputs (Sec. 3.1 Prop. 2): the dictionary
+// gradient G[h,k] = sum over the steps (b,t) with idx[b,t,h] == k of
+// Re(g_t z_t^H), and the scores q[b,t,h,k] = sum_j Re(g_t[pi_k(j)] conj(z_t[j])).
 // The steps of every head are first grouped by map (a stable counting sort),
 // then each group is cut into items of at most P steps; an item sums its
 // steps' outer products on the matrix cores and writes G[h,k] itself when it
@@ -97,12 +97,14 @@ inline DictPlan dict_plan(int B, int L, int H, int N, int K) {
     return p;
 }
 
-struct DictGradArgs {
+struct SteGradArgs {
     int B, L, H, N, K;
     const int* idx;    // [B,L,H]
+    const int* pi;     // [H,K,N] (scores only)
     const float2* g;   // [B,L,H,N] gradient reaching h_t (db of the backward)
     const float2* z;   // [B,L,H,N] D_t .* h_{t-1}
-    float* G;          // [H,K,N,N]
+    float* q;          // [B,L,H,K] scores of every map, or null
+    float* G;          // [H,K,N,N] or null
     DictPlan plan;
     unsigned char* ws;
     int* status;
@@ -112,7 +114,7 @@ struct DictGradArgs {
 hipError_t launch_fwd_chunked(const ScanArgs& a, hipStream_t s);
 hipError_t launch_bwd_chunked(const ScanArgs& a, hipStream_t s);
 hipError_t launch_compose(const ComposeArgs& a, hipStream_t s);
-hipError_t launch_dict_grad(const DictGradArgs& a, hipStream_t s);
+hipError_t launch_ste_grads(const SteGradArgs& a, hipStream_t s);
 // gx = s .* (gy - <s, gy>) * inv_temp along the middle axis of [outer, len, inner],
 // s = softmax(x * inv_temp).
 hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int len,

@@ -1,9 +1,9 @@
 // pdssm_ste.hip -- straight-through surrogate gradients for gfx950 (Sec. 3.1
 // Prop. 2 and its derivation in the appendix).
 //
-// The backward scan already emits, per step, the gradient g_t reaching h_t
-// (db) and, when asked, the scaled state z_t = D_t .* h_{t-1} and the scores
-// q_t[k] of every dictionary map.  This file holds what remains:
+// The backward scan emits, per step, the gradient g_t reaching h_t (db) and,
+// when asked, the scaled state z_t = D_t .* h_{t-1}.  This file holds what
+// follows from them:
 //
 //   dictionary gradient  G[h,k] = sum over the steps (b,t) with
 //                        idx[b,t,h] == k of Re(g_t z_t^H)   (an N x N matrix)
@@ -13,16 +13,22 @@
 //                     groups of several items, its first partial slot
 //     k_dict_scatter  per (head, segment): step ids into the grouped order,
 //                     stable (ranks from ballots over the key bits)
-//     k_dict_gemm     per item (at most P steps of one group): the sum of the
+//     k_ste_gemm      per item (at most P steps of one group): the sum of the
 //                     steps' outer products on the matrix cores,
 //                     v_mfma_f32_32x32x2f32 with the contraction pair
-//                     (re, im): Re(g_i conj(z_j)) = g_i.re z_j.re + g_i.im z_j.im
+//                     (re, im): Re(g_i conj(z_j)) = g_i.re z_j.re + g_i.im z_j.im;
+//                     and, from the same g and z rows staged in LDS, the
+//                     scores q_t[k] = sum_j Re(g_t[pi_k(j)] conj(z_t[j])) of
+//                     every map at each of its steps (K gathers per entry,
+//                     one transpose-reduction per 16 maps)
 //     k_dict_reduce   groups of several items: their partials added in item
 //                     order; groups no step chose: zeros
-//   tempered softmax    k_softmax_vjp: gx = s .* (gy - <s, gy>) / temp along
-//                     one axis, s = softmax(x / temp) -- the backward stand-in
-//                     for a hard argmax (routing logits: over k; dictionary:
-//                     down each column of M[h,k]).
+//   tempered softmax    gx = s .* (gy - <s, gy>) / temp along one axis,
+//                     s = softmax(x / temp) -- the backward stand-in for a hard
+//                     argmax -- in two passes with an online (max, sums)
+//                     state: k_softmax_rows for a contiguous axis (routing
+//                     logits over k), k_softmax_cols for a strided one (down
+//                     each column of the dense dictionary M[h,k]).
 //
 // Every sum runs in a fixed order, so the results do not change from run to run.
 #include "pdssm_device.h"
@@ -44,7 +50,7 @@ struct DictWs {
     float* partial;  // [max_slots][N*N]
 };
 
-__device__ __forceinline__ DictWs dict_ws(const DictGradArgs& a) {
+__device__ __forceinline__ DictWs dict_ws(const SteGradArgs& a) {
     DictWs w;
     w.order = reinterpret_cast<int*>(a.ws + a.plan.off_order);
     w.hist = reinterpret_cast<int*>(a.ws + a.plan.off_hist);
@@ -66,7 +72,7 @@ __device__ __forceinline__ int map_key(int k, int K, bool& bad) {
 
 // ------------------------------------------------------------------ grouping
 // Block x = h * S + segment: steps u in [segment*seg, min(+seg, B*L)).
-__global__ __launch_bounds__(256) void k_dict_hist(DictGradArgs a) {
+__global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
     __shared__ int cnt[256];
     const int h = blockIdx.x / a.plan.S, sg = blockIdx.x - h * a.plan.S;
     for (int k = threadIdx.x; k < a.K; k += 256) cnt[k] = 0;
@@ -84,7 +90,7 @@ __global__ __launch_bounds__(256) void k_dict_hist(DictGradArgs a) {
 // One workgroup: exclusive prefix sums over the groups gi = h*K + k of their
 // step counts (positions; head h starts at h*B*L), item counts and partial
 // slots.  Thread t owns a contiguous range of groups.
-__global__ __launch_bounds__(1024) void k_dict_plan(DictGradArgs a) {
+__global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
     constexpr int T = 1024;
     __shared__ int sh[3][T];
     const DictWs w = dict_ws(a);
@@ -132,7 +138,7 @@ __global__ __launch_bounds__(1024) void k_dict_plan(DictGradArgs a) {
 // step's rank among the earlier steps with the same map comes from ballots
 // over the key bits (wave) and per-wave counts in LDS (tile), so the grouped
 // order keeps the steps of each group in increasing u.
-__global__ __launch_bounds__(256) void k_dict_scatter(DictGradArgs a) {
+__global__ __launch_bounds__(256) void k_dict_scatter(SteGradArgs a) {
     __shared__ int base[256];
     __shared__ int wc[4][256];
     const int h = blockIdx.x / a.plan.S, sg = blockIdx.x - h * a.plan.S;
@@ -178,11 +184,12 @@ __global__ __launch_bounds__(256) void k_dict_scatter(DictGradArgs a) {
     }
 }
 
-// ------------------------------------------------------------------ outer products
+// ------------------------------------------------------------------ outer products and scores
 // A wave owns an NB x NB block of G[h,k] (NB = 64: 2 x 2 tiles of 32 x 32;
 // NB = 32 for N <= 32, rows and columns past N zero).  N <= 64: one block,
-// four waves each take a quarter of the item's steps and add up in LDS at
-// the end.  N = 128 / 256: 4 / 16 waves, one block each, every step.
+// four waves each take a quarter of the item's steps (each wave then holds
+// whole g and z rows of its steps) and add up in LDS at the end.  N = 128 /
+// 256: 4 / 16 waves, one block each, every step in lockstep.
 template <int N>
 struct DictCfg {
     static constexpr int NB = N >= 64 ? 64 : 32;
@@ -191,13 +198,27 @@ struct DictCfg {
     static constexpr int SPLIT = BLOCKS >= 4 ? 1 : 4;
     static constexpr int WAVES = BLOCKS * SPLIT;
     static constexpr int TILES = NB / 32;
-    static constexpr int U = N >= 256 ? 4 : 8;  // steps per load batch (16 waves: 128 registers each)
+    static constexpr int U = N >= 256 ? 2 : 8;  // steps per load batch (16 waves: 128 registers each)
+    static constexpr bool OWN_ROWS = N <= 64;   // a wave holds whole rows of its steps
+    static constexpr int SLQ = N > 64 ? N / 64 : 1;
+    // LDS: the cross-wave sum (after the loop) aliases the staged rows and the dictionary
+    static constexpr int RED_BYTES = SPLIT > 1 ? (SPLIT - 1) * NB * NB * 4 : 0;
+    static constexpr int ROW_BYTES = (OWN_ROWS ? WAVES : 1) * U * 2 * N * 8;
 };
+
+__host__ __device__ inline int score_kp(int K) { return (K + 15) & ~15; }
+
+template <int N>
+size_t ste_gemm_lds(int K, bool q) {
+    using Cfg = DictCfg<N>;
+    const size_t stage = q ? (size_t)Cfg::ROW_BYTES + (size_t)N * score_kp(K) : 0;
+    return stage > (size_t)Cfg::RED_BYTES ? stage : (size_t)Cfg::RED_BYTES;
+}
 
 // One step's operands: lane l holds g[i0 + l] and z[j0 + l] (NB = 64) or
 // g[i0 + l%32], z[j0 + l%32] (NB = 32).
 template <int N>
-__device__ __forceinline__ void load_step(const DictGradArgs& a, int u, int h, int i0, int j0, int lane, bool on,
+__device__ __forceinline__ void load_step(const SteGradArgs& a, int u, int h, int i0, int j0, int lane, bool on,
                                           float2& gv, float2& zv) {
     constexpr int NB = DictCfg<N>::NB;
     const int r = NB == 64 ? lane : (lane & 31);
@@ -238,18 +259,58 @@ __device__ __forceinline__ void mfma_step(f32x16 (&acc)[DictCfg<N>::TILES][DictC
     }
 }
 
+// Scores of every map at one step (Sec. 3.1 Prop. 2):
+// q[k] = sum_j Re(g[pi_k(j)] conj(z[j])) with the g and z rows in LDS (gs,
+// zs) and the head's maps transposed in dT (row j: pi_k(j) for every k, KP
+// bytes).  Lane l owns j = l*SLQ + s; maps go in blocks of 16 (one 16-byte
+// read of dT per j), then one transpose-reduction leaves the total of map
+// kb + l/4 in lane l.  Padding maps (k >= K) read row 0 and are not stored.
+template <int N>
+__device__ __forceinline__ void score_step(const float2* gs, const float2* zs, const uint8_t* dT, int KP, int K,
+                                           int lane, float* __restrict__ qrow) {
+    constexpr int SLQ = DictCfg<N>::SLQ;
+    for (int kb = 0; kb < K; kb += 16) {
+        float v[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) v[u] = 0.f;
+#pragma unroll
+        for (int s = 0; s < SLQ; ++s) {
+            const int j = lane * SLQ + s;
+            if (j < N) {
+                const float2 zj = zs[j];
+                const uint4 pk = *reinterpret_cast<const uint4*>(dT + j * KP + kb);
+                const uint32_t wds[4] = {pk.x, pk.y, pk.z, pk.w};
+#pragma unroll
+                for (int u = 0; u < 16; ++u) {
+                    const float2 g = gs[(wds[u >> 2] >> (8 * (u & 3))) & 0xff];
+                    v[u] = fmaf(g.x, zj.x, fmaf(g.y, zj.y, v[u]));
+                }
+            }
+        }
+        const float tot = transpose_sum<16>(v, lane);
+        const int k = kb + (lane >> 2);
+        if ((lane & 3) == 0 && k < K) qrow[k] = tot;
+    }
+}
+
 // Element r of tile (ti, tj) in lane l sits at row 32 ti + 8 (r/4) + 4 (l/32) + r%4,
 // column 32 tj + l%32 of the wave's block.
 __device__ __forceinline__ int acc_row(int ti, int r, int lane) { return 32 * ti + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 __device__ __forceinline__ int acc_col(int tj, int lane) { return 32 * tj + (lane & 31); }
 
-template <int N>
-__global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradArgs a) {
+// Per item: the outer products of its steps into G[h,k] (DO_G) and the
+// scores of every map at each of its steps (DO_Q; every step of the call
+// belongs to exactly one item).
+template <int N, bool DO_Q, bool DO_G>
+__global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs a) {
     using Cfg = DictCfg<N>;
     constexpr int NB = Cfg::NB, T = Cfg::TILES, U = Cfg::U;
-    __shared__ float red[Cfg::SPLIT > 1 ? Cfg::SPLIT - 1 : 1][Cfg::SPLIT > 1 ? NB * NB : 1];
+    extern __shared__ __align__(16) unsigned char lds[];
+    float* red = reinterpret_cast<float*>(lds);
+    float2* rows = reinterpret_cast<float2*>(lds);
+    uint8_t* dT = lds + Cfg::ROW_BYTES;
     const DictWs w = dict_ws(a);
-    const int HK = a.H * a.K;
+    const int HK = a.H * a.K, KP = score_kp(a.K);
     const int item = blockIdx.x;
     if (item >= w.item[HK]) return;
     // the group holding this item: the last gi with item[gi] <= item
@@ -267,8 +328,20 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
 
     const int wv = wave_id(), lane = lane_id();
     const int blk = wv / Cfg::SPLIT, part = wv - blk * Cfg::SPLIT;
-    const int i0 = (blk / Cfg::GRID) * NB, j0 = (blk % Cfg::GRID) * NB;
+    const int bi = blk / Cfg::GRID, bj = blk % Cfg::GRID;
+    const int i0 = bi * NB, j0 = bj * NB;
     const int s0 = (int)((long)cnt * part / Cfg::SPLIT), s1 = (int)((long)cnt * (part + 1) / Cfg::SPLIT);
+
+    if constexpr (DO_Q) {
+        // the head's maps, transposed: dT[j*KP + k] = pi[h,k,j] (0 for k >= K)
+        const int* pih = a.pi + (size_t)h * a.K * N;
+        for (int e = threadIdx.x; e < N * KP; e += Cfg::WAVES * 64) {
+            const int k = e / N, j = e - k * N;
+            const int p = k < a.K ? pih[(size_t)k * N + j] : 0;
+            dT[j * KP + k] = (uint8_t)((unsigned)p < (unsigned)N ? p : 0);
+        }
+        __syncthreads();
+    }
 
     f32x16 acc[T][T];
 #pragma unroll
@@ -277,6 +350,40 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
         for (int tj = 0; tj < T; ++tj)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[ti][tj][r] = 0.f;
+
+    // the scores of one batch: stage its g and z rows in LDS, then one step each
+    auto scores = [&](const float2 (&gq)[U], const float2 (&zq)[U], int sid, int jb, int m) {
+        if constexpr (Cfg::OWN_ROWS) {
+            float2* gw = rows + wv * U * 2 * N;
+            wave_sync();
+            if (lane < N) {
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    gw[u * N + lane] = gq[u];
+                    gw[(U + u) * N + lane] = zq[u];
+                }
+            }
+            wave_sync();
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (jb + u < m)
+                    score_step<N>(gw + u * N, gw + (U + u) * N, dT, KP, a.K, lane,
+                                  a.q + ((size_t)readlane_i(sid, jb + u) * a.H + h) * a.K);
+        } else {
+            // waves of block column 0 hold the g slices, of block row 0 the z slices
+            __syncthreads();
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (bj == 0) rows[u * N + i0 + lane] = gq[u];
+                if (bi == 0) rows[(U + u) * N + j0 + lane] = zq[u];
+            }
+            __syncthreads();
+            for (int u = wv; u < U; u += Cfg::WAVES)
+                if (jb + u < m)
+                    score_step<N>(rows + u * N, rows + (U + u) * N, dT, KP, a.K, lane,
+                                  a.q + ((size_t)readlane_i(sid, jb + u) * a.H + h) * a.K);
+        }
+    };
 
     // steps in runs of 64 ids (one per lane), operands in batches of U with
     // the next batch in flight while the current one is multiplied
@@ -293,8 +400,11 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
                 load_step<N>(a, readlane_i(sid, jj < m ? jj : 0), h, i0, j0, lane, jj < m, gb[u], zb[u]);
             }
             issue_fence();
+            if constexpr (DO_G) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) mfma_step<N>(acc, ga[u], za[u], lane);
+                for (int u = 0; u < U; ++u) mfma_step<N>(acc, ga[u], za[u], lane);
+            }
+            if constexpr (DO_Q) scores(ga, za, sid, j, m);
             if (j + U >= m) break;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
@@ -302,12 +412,17 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
                 load_step<N>(a, readlane_i(sid, jj < m ? jj : 0), h, i0, j0, lane, jj < m, ga[u], za[u]);
             }
             issue_fence();
+            if constexpr (DO_G) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) mfma_step<N>(acc, gb[u], zb[u], lane);
+                for (int u = 0; u < U; ++u) mfma_step<N>(acc, gb[u], zb[u], lane);
+            }
+            if constexpr (DO_Q) scores(gb, zb, sid, j + U, m);
         }
     }
+    if constexpr (!DO_G) return;
 
     if constexpr (Cfg::SPLIT > 1) {
+        __syncthreads();  // red aliases the staged rows
         if (part > 0) {
 #pragma unroll
             for (int ti = 0; ti < T; ++ti)
@@ -315,7 +430,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
                 for (int tj = 0; tj < T; ++tj)
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
-                        red[part - 1][acc_row(ti, r, lane) * NB + acc_col(tj, lane)] = acc[ti][tj][r];
+                        red[(part - 1) * NB * NB + acc_row(ti, r, lane) * NB + acc_col(tj, lane)] = acc[ti][tj][r];
         }
         __syncthreads();
         if (part > 0) return;
@@ -327,7 +442,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
                 for (int tj = 0; tj < T; ++tj)
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
-                        acc[ti][tj][r] += red[p][acc_row(ti, r, lane) * NB + acc_col(tj, lane)];
+                        acc[ti][tj][r] += red[p * NB * NB + acc_row(ti, r, lane) * NB + acc_col(tj, lane)];
     }
     float* dst = pieces == 1 ? a.G + (size_t)gi * N * N : w.partial + (size_t)(w.slot[gi] + piece) * N * N;
 #pragma unroll
@@ -344,7 +459,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_dict_gemm(DictGradAr
 // Block (gi, y): groups of several items add their partials in item order;
 // groups no step chose get zeros; single-item groups were written directly.
 template <int N>
-__global__ __launch_bounds__(256) void k_dict_reduce(DictGradArgs a) {
+__global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
     const DictWs w = dict_ws(a);
     const int gi = blockIdx.x;
     const int pieces = w.item[gi + 1] - w.item[gi];
@@ -359,43 +474,108 @@ __global__ __launch_bounds__(256) void k_dict_reduce(DictGradArgs a) {
     }
 }
 
+template <int N, bool DO_Q, bool DO_G>
+hipError_t gemm_launch(const SteGradArgs& a, hipStream_t st) {
+    auto kern = k_ste_gemm<N, DO_Q, DO_G>;
+    const size_t lds = ste_gemm_lds<N>(a.K, DO_Q);
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3(a.plan.max_items), dim3(DictCfg<N>::WAVES * 64), lds, st, a);
+    return hipGetLastError();
+}
+
 template <int N>
-hipError_t dict_launch(const DictGradArgs& a, hipStream_t st) {
-    const int HK = a.H * a.K;
-    hipLaunchKernelGGL(k_dict_gemm<N>, dim3(a.plan.max_items), dim3(DictCfg<N>::WAVES * 64), 0, st, a);
+hipError_t dict_launch(const SteGradArgs& a, hipStream_t st) {
+    hipError_t e = a.q ? (a.G ? gemm_launch<N, true, true>(a, st) : gemm_launch<N, true, false>(a, st))
+                       : gemm_launch<N, false, true>(a, st);
+    if (e != hipSuccess || !a.G) return e;
     const int ys = (N * N + 255) / 256 < 16 ? (N * N + 255) / 256 : 16;
-    hipLaunchKernelGGL(k_dict_reduce<N>, dim3(HK, ys), dim3(256), 0, st, a);
+    hipLaunchKernelGGL(k_dict_reduce<N>, dim3(a.H * a.K, ys), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ tempered softmax
-// Thread per (o, j) of x [outer, len, inner]: three passes down the axis
-// (maximum, then the exponential sums, then the product).
-__global__ __launch_bounds__(256) void k_softmax_vjp(const float* __restrict__ x, const float* __restrict__ gy,
-                                                     float* __restrict__ gx, int64_t outer, int len, int64_t inner,
-                                                     float it) {
+// Online softmax state of one fibre: m = max(x * it), s = sum exp(x*it - m),
+// d = sum exp(x*it - m) * gy.
+struct SoftState {
+    float m, s, d;
+};
+
+__device__ __forceinline__ void soft_add(SoftState& a, float xi, float gi) {
+    const float mn = fmaxf(a.m, xi);
+    const float r = __expf(a.m - mn), e = __expf(xi - mn);
+    a.s = a.s * r + e;
+    a.d = a.d * r + e * gi;
+    a.m = mn;
+}
+
+__device__ __forceinline__ void soft_merge(SoftState& a, const SoftState& b) {
+    const float mn = fmaxf(a.m, b.m);
+    if (mn == -INFINITY) return;  // both empty
+    const float ra = __expf(a.m - mn), rb = __expf(b.m - mn);
+    a.s = a.s * ra + b.s * rb;
+    a.d = a.d * ra + b.d * rb;
+    a.m = mn;
+}
+
+// inner == 1 (the axis is contiguous, e.g. routing logits over k): a team of
+// T lanes (T = min(64, len rounded up to a power of two)) per row, lane t
+// taking entries t, t + T, ...; the team merges its states with butterfly
+// shuffles.  Loads of a wave cover 64 consecutive floats.
+template <int T>
+__global__ __launch_bounds__(256) void k_softmax_rows(const float* __restrict__ x, const float* __restrict__ gy,
+                                                      float* __restrict__ gx, int64_t rows, int len, float it) {
+    const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t row = gid / T;
+    const int t = (int)(gid % T);
+    const bool on = row < rows;
+    const int64_t base = (on ? row : 0) * len;
+    SoftState st = {-INFINITY, 0.f, 0.f};
+    if (on)
+        for (int i = t; i < len; i += T) soft_add(st, x[base + i] * it, gy[base + i]);
+#pragma unroll
+    for (int off = T / 2; off > 0; off >>= 1) {
+        SoftState o;
+        o.m = __shfl_xor(st.m, off, T);
+        o.s = __shfl_xor(st.s, off, T);
+        o.d = __shfl_xor(st.d, off, T);
+        soft_merge(st, o);
+    }
+    if (!on) return;
+    const float rs = 1.f / st.s, dot = st.d * rs;
+    for (int i = t; i < len; i += T) gx[base + i] = __expf(x[base + i] * it - st.m) * rs * (gy[base + i] - dot) * it;
+}
+
+// inner > 1 (e.g. down the columns of M[h,k]): a thread per fibre (o, j);
+// neighbouring threads take neighbouring j, so every load is coalesced.
+__global__ __launch_bounds__(256) void k_softmax_cols(const float* __restrict__ x, const float* __restrict__ gy,
+                                                      float* __restrict__ gx, int64_t outer, int len, int64_t inner,
+                                                      float it) {
     const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (id >= outer * inner) return;
     const int64_t o = id / inner, j = id - o * inner;
     const int64_t base = o * len * inner + j;
-    float m = -INFINITY;
-    for (int i = 0; i < len; ++i) m = fmaxf(m, x[base + i * inner] * it);
-    float se = 0.f, sg = 0.f;
-    for (int i = 0; i < len; ++i) {
-        const float e = expf(x[base + i * inner] * it - m);
-        se += e;
-        sg += e * gy[base + i * inner];
-    }
-    const float r = 1.f / se, dot = sg * r;
-    for (int i = 0; i < len; ++i) {
-        const float s = expf(x[base + i * inner] * it - m) * r;
-        gx[base + i * inner] = s * (gy[base + i * inner] - dot) * it;
-    }
+    SoftState st = {-INFINITY, 0.f, 0.f};
+#pragma unroll 4
+    for (int i = 0; i < len; ++i) soft_add(st, x[base + i * inner] * it, gy[base + i * inner]);
+    const float rs = 1.f / st.s, dot = st.d * rs;
+#pragma unroll 4
+    for (int i = 0; i < len; ++i)
+        gx[base + i * inner] = __expf(x[base + i * inner] * it - st.m) * rs * (gy[base + i * inner] - dot) * it;
+}
+
+template <int T>
+void softmax_rows_launch(const float* x, const float* gy, float* gx, int64_t rows, int len, float it,
+                         hipStream_t st) {
+    const int64_t lanes = rows * T;
+    hipLaunchKernelGGL(k_softmax_rows<T>, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, st, x, gy, gx, rows,
+                       len, it);
 }
 
 }  // namespace
 
-hipError_t launch_dict_grad(const DictGradArgs& a, hipStream_t st) {
+hipError_t launch_ste_grads(const SteGradArgs& a, hipStream_t st) {
     const int nb = a.H * a.plan.S;
     hipLaunchKernelGGL(k_dict_hist, dim3(nb), dim3(256), 0, st, a);
     hipLaunchKernelGGL(k_dict_plan, dim3(1), dim3(1024), 0, st, a);
@@ -417,8 +597,17 @@ hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_
                               float inv_temp, hipStream_t st) {
     const int64_t n = outer * inner;
     if (n == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_softmax_vjp, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, x, gy, gx, outer, len,
-                       inner, inv_temp);
+    if (inner == 1) {
+        if (len <= 2) softmax_rows_launch<2>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 4) softmax_rows_launch<4>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 8) softmax_rows_launch<8>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 16) softmax_rows_launch<16>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 32) softmax_rows_launch<32>(x, gy, gx, outer, len, inv_temp, st);
+        else softmax_rows_launch<64>(x, gy, gx, outer, len, inv_temp, st);
+    } else {
+        hipLaunchKernelGGL(k_softmax_cols, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, x, gy, gx, outer, len,
+                           inner, inv_temp);
+    }
     return hipGetLastError();
 }
 

@@ -22,7 +22,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpdssm.s
 _lib = None
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INDEX = 0, -1, -2, -3, -4, -5
-OP_FWD, OP_BWD, OP_COMPOSE, OP_DICT_GRAD = 1, 2, 3, 4
+OP_FWD, OP_BWD, OP_COMPOSE, OP_STE_GRADS = 1, 2, 3, 4
 FLAG_PREPARED = 1
 
 
@@ -40,7 +40,7 @@ class Desc(ctypes.Structure):
 
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
            "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
-           "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_dict_grad",
+           "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_ste_grads",
            "pdssm_softmax_vjp")
 
 
@@ -72,10 +72,10 @@ def load():
     L.pdssm_scan_bwd.restype = I
     L.pdssm_compose_chunks.argtypes = [D] + [P] * 7
     L.pdssm_compose_chunks.restype = I
-    L.pdssm_scan_bwd_ste.argtypes = [D] + [P] * 15 + [Z, P, P]
+    L.pdssm_scan_bwd_ste.argtypes = [D] + [P] * 14 + [Z, P, P]
     L.pdssm_scan_bwd_ste.restype = I
-    L.pdssm_dict_grad.argtypes = [D] + [P] * 5 + [Z, P, P]
-    L.pdssm_dict_grad.restype = I
+    L.pdssm_ste_grads.argtypes = [D] + [P] * 7 + [Z, P, P]
+    L.pdssm_ste_grads.restype = I
     L.pdssm_softmax_vjp.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int64,
                                     ctypes.c_float, P]
     L.pdssm_softmax_vjp.restype = I
@@ -189,8 +189,8 @@ class Scan:
             self.q = torch.empty((B, L, H, K), dtype=torch.float32, device=dev)
             self.z = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
             self.G = torch.empty((H, K, N, N), dtype=torch.float32, device=dev)
-            self.ws_dict = torch.empty(max(workspace_size(self.d, OP_DICT_GRAD), 1), dtype=torch.uint8,
-                                       device=dev)
+            self.ws_ste = torch.empty(max(workspace_size(self.d, OP_STE_GRADS), 1), dtype=torch.uint8,
+                                      device=dev)
 
     def _desc(self):
         return ctypes.byref(self.dp if self.prepared else self.d)
@@ -220,23 +220,25 @@ class Scan:
         return self.dD, self.db, self.dc, self.dh0
 
     def bwd_ste(self, idx, pi, D, b, c, dy, dh_final=None, stream=None):
-        """bwd() plus the straight-through scores q and the scaled states z
-        (Scan(..., ste=True))."""
+        """bwd() plus the scaled states z (Scan(..., ste=True))."""
         st = load().pdssm_scan_bwd_ste(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
                                        _p(self.saved), _p(dy), _p(dh_final), _p(self.dD), _p(self.db),
-                                       _p(self.dc), _p(self.dh0), _p(self.q), _p(self.z), _p(self.ws),
+                                       _p(self.dc), _p(self.dh0), _p(self.z), _p(self.ws),
                                        self.ws.numel(), _p(self.status), _stream(stream))
         if st != OK:
             raise PdssmError(st, "pdssm_scan_bwd_ste")
-        return self.dD, self.db, self.dc, self.dh0, self.q, self.z
+        return self.dD, self.db, self.dc, self.dh0, self.z
 
-    def dict_grad(self, idx, stream=None):
-        """G [H,K,N,N] from the db and z of the last bwd_ste()."""
-        st = load().pdssm_dict_grad(ctypes.byref(self.d), _p(idx), _p(self.db), _p(self.z), _p(self.G),
-                                    _p(self.ws_dict), self.ws_dict.numel(), _p(self.status), _stream(stream))
+    def ste_grads(self, idx, pi, q=True, G=True, stream=None):
+        """Scores q [B,L,H,K] and dictionary gradient G [H,K,N,N] from the db
+        and z of the last bwd_ste() (each None when not asked for)."""
+        qq, GG = (self.q if q else None), (self.G if G else None)
+        st = load().pdssm_ste_grads(ctypes.byref(self.d), _p(idx), _p(pi), _p(self.db), _p(self.z), _p(qq),
+                                    _p(GG), _p(self.ws_ste), self.ws_ste.numel(), _p(self.status),
+                                    _stream(stream))
         if st != OK:
-            raise PdssmError(st, "pdssm_dict_grad")
-        return self.G
+            raise PdssmError(st, "pdssm_ste_grads")
+        return qq, GG
 
     def check_status(self):
         """Synchronise and raise if a kernel flagged an out-of-range index."""
@@ -297,7 +299,7 @@ def compose_chunks(idx, pi, D, chunk, stream=None):
 
 
 def scan_bwd_ste(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
-    """Returns (dD, db, dc, dh0, q [B,L,H,K] f32, z [B,L,H,N] c64)."""
+    """Returns (dD, db, dc, dh0, z [B,L,H,N] c64)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
     s = Scan(B, L, H, N, K, chunk, dev, ste=True)
     _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
@@ -310,27 +312,31 @@ def scan_bwd_ste(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=Non
     return out
 
 
-def dict_grad(idx, g, z, K, stream=None):
-    """G [H,K,N,N] f32: per head and map, the sum of Re(g_t z_t^H) over the
-    steps that chose the map (g = db and z from scan_bwd_ste)."""
+def ste_grads(idx, pi, g, z, q=True, G=True, stream=None):
+    """(q [B,L,H,K] f32 or None, G [H,K,N,N] f32 or None) from g = db and z
+    of scan_bwd_ste: the scores of every map at every step and, per head and
+    map, the sum of Re(g_t z_t^H) over the steps that chose the map."""
     B, L, H = idx.shape
     N = g.shape[3]
+    K = pi.shape[1]
     dev = idx.device
     _need(idx, "idx", torch.int32, (B, L, H), dev)
+    _need(pi, "pi", torch.int32, (H, K, N), dev)
     _need(g, "g", torch.complex64, (B, L, H, N), dev)
     _need(z, "z", torch.complex64, (B, L, H, N), dev)
     d = desc(B, L, H, N, K)
-    ws = torch.empty(max(workspace_size(d, OP_DICT_GRAD), 1), dtype=torch.uint8, device=dev)
-    G = torch.empty((H, K, N, N), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(workspace_size(d, OP_STE_GRADS), 1), dtype=torch.uint8, device=dev)
+    qq = torch.empty((B, L, H, K), dtype=torch.float32, device=dev) if q else None
+    GG = torch.empty((H, K, N, N), dtype=torch.float32, device=dev) if G else None
     status = torch.zeros(1, dtype=torch.int32, device=dev)
-    st = load().pdssm_dict_grad(ctypes.byref(d), _p(idx), _p(g), _p(z), _p(G), _p(ws), ws.numel(),
-                                _p(status), _stream(stream))
+    st = load().pdssm_ste_grads(ctypes.byref(d), _p(idx), _p(pi), _p(g), _p(z), _p(qq), _p(GG), _p(ws),
+                                ws.numel(), _p(status), _stream(stream))
     if st != OK:
-        raise PdssmError(st, "pdssm_dict_grad")
+        raise PdssmError(st, "pdssm_ste_grads")
     torch.cuda.synchronize(dev)
     if int(status.item()) != OK:
         raise PdssmError(int(status.item()), "kernel index check")
-    return G
+    return qq, GG
 
 
 def softmax_vjp(x, gy, dim, temp, out=None, stream=None):

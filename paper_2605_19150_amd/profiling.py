@@ -78,9 +78,13 @@ def _counter_mean(d, counter, kernel_substr):
     return sum(vals.values()) / len(vals), len(vals)
 
 
-def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, command):
-    f_kib, nf = _counter_mean(fetch, "FETCH_SIZE", kernel)
-    w_kib, nw = _counter_mean(write, "WRITE_SIZE", kernel)
+def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, command, match=None):
+    """`kernel` names the summary (what read_traffic_summary looks up);
+    `match` (default: kernel) selects the dispatches by a substring of their
+    demangled name."""
+    match = match or kernel
+    f_kib, nf = _counter_mean(fetch, "FETCH_SIZE", match)
+    w_kib, nw = _counter_mean(write, "WRITE_SIZE", match)
     cf_kib, _ = _counter_mean(copy_fetch, "FETCH_SIZE", "copyBuffer")
     cw_kib, _ = _counter_mean(copy_write, "WRITE_SIZE", "copyBuffer")
     sf = COPY_BYTES / (cf_kib * 1024.0)
@@ -91,6 +95,7 @@ def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, com
         "# HBM traffic per launch: %s, workload %s" % (kernel, workload),
         "",
         "kernel: %s" % kernel,
+        "dispatches: %s" % match,
         "workload: %s" % workload,
         "source-hash: %s" % source_hash(),
         "fetch-bytes-per-launch: %.0f" % fetch_b,
@@ -136,13 +141,14 @@ def main(argv=None):
     t = sub.add_parser("traffic")
     for k in ("kernel", "workload", "fetch", "write", "copy_fetch", "copy_write", "command"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    t.add_argument("--match", default=None, help="substring of the dispatches' kernel name (default: --kernel)")
     sub.add_parser("hash")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         sys.stdout.write(stats_markdown(a.dir, a.title, a.command))
     elif a.cmd == "traffic":
         sys.stdout.write(traffic_markdown(a.kernel, a.workload, a.fetch, a.write, a.copy_fetch,
-                                          a.copy_write, a.command))
+                                          a.copy_write, a.command, a.match))
     else:
         print(source_hash())
 

@@ -170,35 +170,41 @@ def test_ste_entry_points_host_checks(lib):
     f = FakeBufs()
     st = 2 * 40 * 2 * 64 * 8
     # the straight-through backward checks what the plain backward checks ...
-    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *([None] * 15), 0, None, None) == pdssm.ERR_INVALID_ARG
-    # ... and that q / z do not overlap the other arguments
+    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *([None] * 14), 0, None, None) == pdssm.ERR_INVALID_ARG
     args = [f(2 * 40 * 2 * 4), f(2 * 4 * 64 * 4)] + [f(st) for _ in range(3)] + [f(2 * 2 * 5 * 64 * 8),
                                                                                 f(2 * 40 * 2 * 4), None]
     outs = [f(st) for _ in range(3)] + [None]
     need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
     ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
-    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, *outs, args[2], None, ws, need, None,
-                                  None) == pdssm.ERR_INVALID_ARG   # q over D
-    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, *outs, None, outs[0], ws, need, None,
+    # ... and needs z, disjoint from everything else
+    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, *outs, None, ws, need, None, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, *outs, args[2], ws, need, None,
+                                  None) == pdssm.ERR_INVALID_ARG   # z over D
+    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, *outs, outs[0], ws, need, None,
                                   None) == pdssm.ERR_INVALID_ARG   # z over dD
-    # dictionary gradient: required pointers, workspace size and alignment, overlap
-    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_DICT_GRAD)
-    plan_min = 2 * 40 * 2 * 4 + 2 * 4 * 64 * 64 * 4
+    # scores and dictionary gradient: required pointers, workspace size and alignment, overlap
+    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_STE_GRADS)
     assert need >= 2 * 40 * 2 * 4 and need != ctypes.c_size_t(-1).value
-    idx, g, z, G = f(2 * 40 * 2 * 4), f(st), f(st), f(2 * 4 * 64 * 64 * 4)
-    ws = ctypes.c_void_p(f(need + plan_min).value // 256 * 256 + 256)
-    call = lambda *a: lib.pdssm_dict_grad(ctypes.byref(d), *a, None, None)  # noqa: E731
-    assert call(None, g, z, G, ws, need) == pdssm.ERR_INVALID_ARG
-    assert call(idx, g, z, None, ws, need) == pdssm.ERR_INVALID_ARG
-    assert call(idx, g, z, G, None, need) == pdssm.ERR_WORKSPACE
-    assert call(idx, g, z, G, ws, need - 1) == pdssm.ERR_WORKSPACE
-    assert call(idx, g, z, G, ctypes.c_void_p(ws.value + 16), need) == pdssm.ERR_WORKSPACE
-    assert call(idx, g, z, g, ws, need) == pdssm.ERR_INVALID_ARG   # G over g
-    assert call(idx, ctypes.c_void_p(g.value + 8), z, G, ws, need) == pdssm.ERR_INVALID_ARG
+    idx, pi, g, z = f(2 * 40 * 2 * 4), f(2 * 4 * 64 * 4), f(st), f(st)
+    q, G = f(2 * 40 * 2 * 4 * 4), f(2 * 4 * 64 * 64 * 4)
+    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+    call = lambda *a: lib.pdssm_ste_grads(ctypes.byref(d), *a, None, None)  # noqa: E731
+    assert call(None, pi, g, z, q, G, ws, need) == pdssm.ERR_INVALID_ARG
+    assert call(idx, pi, g, z, None, None, ws, need) == pdssm.ERR_INVALID_ARG   # nothing asked for
+    assert call(idx, None, g, z, q, G, ws, need) == pdssm.ERR_INVALID_ARG    # scores need pi
+    assert call(idx, pi, g, None, q, G, ws, need) == pdssm.ERR_INVALID_ARG
+    assert call(idx, pi, g, z, q, G, None, need) == pdssm.ERR_WORKSPACE
+    assert call(idx, pi, g, z, q, G, ws, need - 1) == pdssm.ERR_WORKSPACE
+    assert call(idx, pi, g, z, q, G, ctypes.c_void_p(ws.value + 16), need) == pdssm.ERR_WORKSPACE
+    assert call(idx, pi, g, z, q, g, ws, need) == pdssm.ERR_INVALID_ARG    # G over g
+    assert call(idx, pi, g, z, pi, G, ws, need) == pdssm.ERR_INVALID_ARG   # q over pi
+    assert call(idx, pi, g, z, q, q, ws, need) == pdssm.ERR_INVALID_ARG    # q over G
+    assert call(idx, pi, ctypes.c_void_p(g.value + 8), z, q, G, ws, need) == pdssm.ERR_INVALID_ARG
     bad = pdssm.desc(2, 40, 2, 48, 4)
-    assert lib.pdssm_dict_grad(ctypes.byref(bad), idx, g, z, G, ws, need, None, None) == pdssm.ERR_UNSUPPORTED
+    assert lib.pdssm_ste_grads(ctypes.byref(bad), idx, pi, g, z, q, G, ws, need, None,
+                               None) == pdssm.ERR_UNSUPPORTED
     with pytest.raises(pdssm.PdssmError):
-        pdssm.workspace_size(bad, pdssm.OP_DICT_GRAD)
+        pdssm.workspace_size(bad, pdssm.OP_STE_GRADS)
     # tempered softmax: sizes, temperature, overlap
     x, gy, gx = f(4096), f(4096), f(4096)
     sm = lib.pdssm_softmax_vjp
@@ -210,15 +216,16 @@ def test_ste_entry_points_host_checks(lib):
     assert sm(None, gy, gx, 8, 16, 1, ctypes.c_float(1.0), None) == pdssm.ERR_INVALID_ARG
     assert sm(x, gy, x, 8, 16, 1, ctypes.c_float(1.0), None) == pdssm.ERR_INVALID_ARG
     assert sm(x, gy, ctypes.c_void_p(gx.value + 2), 8, 16, 1, ctypes.c_float(1.0), None) == pdssm.ERR_INVALID_ARG
+    assert sm(x, gy, gx, 1 << 31, 1, 1, ctypes.c_float(1.0), None) == pdssm.ERR_UNSUPPORTED
     # an empty outer extent enqueues nothing and succeeds
     assert sm(x, gy, gx, 0, 16, 1, ctypes.c_float(1.0), None) == pdssm.OK
 
 
-def test_dict_grad_workspace_bounds(lib):
+def test_ste_grads_workspace_bounds(lib):
     # the partial buffer stays bounded (<= 256 MiB) even for the largest N
     for dims in ((16, 2048, 16, 64, 16), (8, 4096, 32, 128, 64), (1, 32767, 256, 256, 256),
                  (8, 18000, 8, 128, 32), (1, 1, 1, 8, 1)):
         d = pdssm.desc(*dims)
         B, L, H, N, K = dims
-        n = pdssm.workspace_size(d, pdssm.OP_DICT_GRAD)
+        n = pdssm.workspace_size(d, pdssm.OP_STE_GRADS)
         assert n <= B * L * H * 4 + H * K * 64 * 1024 + (1 << 28) + 64 * 256, dims

@@ -1,7 +1,7 @@
 """GPU parity of the straight-through surrogate gradients (Sec. 3.1 Prop. 2):
-the candidate-map scores q and scaled states z written by the backward scan,
-the dictionary gradient G and the tempered-softmax products, through the C
-ABI, against the float64 oracle.
+the scaled states z written by the backward scan, the candidate-map scores q
+and the dictionary gradient G (pdssm_ste_grads) and the tempered-softmax
+products, through the C ABI, against the float64 oracle.
 
 Tolerance: z, the plain backward outputs and the softmax products as for the
 scan, |gpu - ref| <= 1e-5 + 1e-4*|ref| on every real component.  q and G are
@@ -41,7 +41,7 @@ def run_ste(inp, chunk=0):
     s = pdssm.Scan(B, L, H, N, K, chunk, DEV, ste=True)
     s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=T.get("h0"))
     s.bwd_ste(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"], dh_final=T.get("dh_final"))
-    s.dict_grad(T["idx"])
+    s.ste_grads(T["idx"], T["pi"])
     s.check_status()
     out = {k: getattr(s, k).cpu().numpy() for k in ("dD", "db", "dc", "dh0", "q", "z", "G")}
     return s, T, out
@@ -107,68 +107,71 @@ def test_ste_outputs_are_optional_and_plain_outputs_unchanged():
     torch.cuda.synchronize()
     for k in ("dD", "db", "dc", "dh0"):   # same kernels' arithmetic: identical bits
         np.testing.assert_array_equal(got[k], getattr(plain, k).cpu().numpy(), err_msg=k)
-    # q alone, then z alone, through the C ABI
-    L_ = pdssm.load()
-    q2 = torch.full_like(s.q, 7.0)
-    z2 = torch.full_like(s.z, 7.0)
-    p = pdssm._p
-    for qq, zz in ((q2, None), (None, z2)):
-        st = L_.pdssm_scan_bwd_ste(ctypes.byref(s.d), p(T["idx"]), p(T["pi"]), p(T["D"]), p(T["b"]),
-                                   p(T["c"]), p(s.saved), p(T["dy"]), p(T["dh_final"]), p(s.dD), p(s.db),
-                                   p(s.dc), p(s.dh0), p(qq), p(zz), p(s.ws), s.ws.numel(), p(s.status),
-                                   pdssm._stream(None))
-        assert st == pdssm.OK
-    torch.cuda.synchronize()
-    np.testing.assert_array_equal(q2.cpu().numpy(), got["q"])
-    np.testing.assert_array_equal(z2.cpu().numpy(), got["z"])
+    # q alone and G alone equal the joint call bit for bit
+    q1, G0 = pdssm.ste_grads(T["idx"], T["pi"], s.db, s.z, q=True, G=False)
+    q0, G1 = pdssm.ste_grads(T["idx"], T["pi"], s.db, s.z, q=False, G=True)
+    assert q0 is None and G0 is None
+    np.testing.assert_array_equal(q1.cpu().numpy(), got["q"])
+    np.testing.assert_array_equal(G1.cpu().numpy(), got["G"])
 
 
-def test_dict_grad_alone_many_items_and_deterministic():
+def _dense_ref(idx, pi, g, z):
+    """q and G straight from their definitions, float64."""
+    B, L, H, N = g.shape
+    K = pi.shape[1]
+    g, z = g.astype(np.complex128), z.astype(np.complex128)
+    q = np.empty((B, L, H, K))
+    G = np.zeros((H, K, N, N))
+    for h in range(H):
+        q[:, :, h, :] = (g[:, :, h, :][:, :, pi[h]] * np.conj(z[:, :, h, None, :])).real.sum(-1)
+        for k in range(K):
+            m = idx[:, :, h] == k
+            G[h, k] = (g[:, :, h][m][:, :, None] * np.conj(z[:, :, h][m][:, None, :])).real.sum(0)
+    return q, G
+
+
+def test_ste_grads_alone_many_items_and_deterministic():
     # long groups: each is cut into many items whose partials are added in order
     rng = np.random.default_rng(9)
     B, L, H, N, K = 4, 3000, 2, 64, 3
     idx = rng.integers(0, K, size=(B, L, H), dtype=np.int32)
+    pi = rng.integers(0, N, size=(H, K, N), dtype=np.int32)
     g = (rng.standard_normal((B, L, H, N)) + 1j * rng.standard_normal((B, L, H, N))).astype(np.complex64)
     z = (rng.standard_normal((B, L, H, N)) + 1j * rng.standard_normal((B, L, H, N))).astype(np.complex64)
-    gd, zd, idd = (torch.from_numpy(a).to(DEV) for a in (g, z, idx))
-    G1 = pdssm.dict_grad(idd, gd, zd, K).cpu().numpy()
-    G2 = pdssm.dict_grad(idd, gd, zd, K).cpu().numpy()
+    dv = [torch.from_numpy(a).to(DEV) for a in (idx, pi, g, z)]
+    q1, G1 = (t.cpu().numpy() for t in pdssm.ste_grads(*dv))
+    q2, G2 = (t.cpu().numpy() for t in pdssm.ste_grads(*dv))
     np.testing.assert_array_equal(G1, G2)
-    ref = np.zeros((H, K, N, N))
-    for h in range(H):
-        for k in range(K):
-            m = idx[:, :, h] == k
-            gg, zz = g[:, :, h][m].astype(np.complex128), z[:, :, h][m].astype(np.complex128)
-            ref[h, k] = (gg[:, :, None] * np.conj(zz[:, None, :])).real.sum(0)
-    _, Gs = ste_scales(np.zeros((H, K, N), np.int64), idx, g.astype(np.complex128), z.astype(np.complex128))
-    assert_close_sum("G", G1, ref, Gs)
+    np.testing.assert_array_equal(q1, q2)
+    rq, rG = _dense_ref(idx, pi, g, z)
+    qs, Gs = ste_scales(pi, idx, g.astype(np.complex128), z.astype(np.complex128))
+    assert_close_sum("q", q1, rq, qs)
+    assert_close_sum("G", G1, rG, Gs)
 
 
-@pytest.mark.parametrize("N", [8, 32, 128, 256])
-def test_dict_grad_alone_sizes(N):
-    rng = np.random.default_rng(N)
-    B, L, H, K = 2, 300, 3, 4
+@pytest.mark.parametrize("N,K", [(8, 3), (16, 17), (32, 40), (128, 9), (256, 4), (64, 256)])
+def test_ste_grads_alone_sizes(N, K):
+    rng = np.random.default_rng(N + K)
+    B, L, H = 2, 300, 3
     idx = rng.integers(0, K, size=(B, L, H), dtype=np.int32)
+    pi = rng.integers(0, N, size=(H, K, N), dtype=np.int32)
     g = ((rng.standard_normal((B, L, H, N)) + 1j * rng.standard_normal((B, L, H, N))) / 8).astype(np.complex64)
     z = ((rng.standard_normal((B, L, H, N)) + 1j * rng.standard_normal((B, L, H, N))) / 8).astype(np.complex64)
-    G = pdssm.dict_grad(*(torch.from_numpy(a).to(DEV) for a in (idx, g, z)), K).cpu().numpy()
-    ref = np.zeros((H, K, N, N))
-    for h in range(H):
-        for k in range(K):
-            m = idx[:, :, h] == k
-            gg, zz = g[:, :, h][m].astype(np.complex128), z[:, :, h][m].astype(np.complex128)
-            ref[h, k] = (gg[:, :, None] * np.conj(zz[:, None, :])).real.sum(0)
-    _, Gs = ste_scales(np.zeros((H, K, N), np.int64), idx, g.astype(np.complex128), z.astype(np.complex128))
-    assert_close_sum("G", G, ref, Gs)
+    q, G = (t.cpu().numpy() for t in pdssm.ste_grads(*(torch.from_numpy(a).to(DEV) for a in (idx, pi, g, z))))
+    rq, rG = _dense_ref(idx, pi, g, z)
+    qs, Gs = ste_scales(pi, idx, g.astype(np.complex128), z.astype(np.complex128))
+    assert_close_sum("q", q, rq, qs)
+    assert_close_sum("G", G, rG, Gs)
 
 
-def test_dict_grad_reports_bad_index():
+def test_ste_grads_reports_bad_index():
     B, L, H, N, K = 1, 50, 1, 64, 4
     idx = torch.zeros((B, L, H), dtype=torch.int32, device=DEV)
     idx[0, 7, 0] = 9
+    pi = torch.zeros((H, K, N), dtype=torch.int32, device=DEV)
     g = torch.zeros((B, L, H, N), dtype=torch.complex64, device=DEV)
     with pytest.raises(pdssm.PdssmError):
-        pdssm.dict_grad(idx, g, g.clone(), K)
+        pdssm.ste_grads(idx, pi, g, g.clone())
 
 
 @pytest.mark.parametrize("temp", [0.5, 1.0, 3.0])
