@@ -17,10 +17,10 @@
 //                     steps' outer products on the matrix cores,
 //                     v_mfma_f32_32x32x2f32 with the contraction pair
 //                     (re, im): Re(g_i conj(z_j)) = g_i.re z_j.re + g_i.im z_j.im;
-//                     and, from the same g and z rows staged in LDS, the
-//                     scores q_t[k] = sum_j Re(g_t[pi_k(j)] conj(z_t[j])) of
-//                     every map at each of its steps (K gathers per entry,
-//                     one transpose-reduction per 16 maps)
+//                     and, from the same g and z rows staged transposed in
+//                     LDS (lane = step), the scores
+//                     q_t[k] = sum_j Re(g_t[pi_k(j)] conj(z_t[j])) of every
+//                     map at each of its steps
 //     k_dict_reduce   groups of several items: their partials added in item
 //                     order; groups no step chose: zeros
 //   tempered softmax    gx = s .* (gy - <s, gy>) / temp along one axis,
@@ -40,7 +40,7 @@ namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-struct DictWs {
+struct SteWs {
     int* order;      // [B*L*H] step ids u = b*L + t, grouped by (head, map)
     int* hist;       // [H][S][K]
     int* n;          // [H*K] steps per group
@@ -50,8 +50,8 @@ struct DictWs {
     float* partial;  // [max_slots][N*N]
 };
 
-__device__ __forceinline__ DictWs dict_ws(const SteGradArgs& a) {
-    DictWs w;
+__device__ __forceinline__ SteWs ste_ws(const SteGradArgs& a) {
+    SteWs w;
     w.order = reinterpret_cast<int*>(a.ws + a.plan.off_order);
     w.hist = reinterpret_cast<int*>(a.ws + a.plan.off_hist);
     w.n = reinterpret_cast<int*>(a.ws + a.plan.off_n);
@@ -82,7 +82,7 @@ __global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
     bool bad = false;
     for (long u = u0 + threadIdx.x; u < u1; u += 256) atomicAdd(&cnt[map_key(a.idx[u * a.H + h], a.K, bad)], 1);
     __syncthreads();
-    const DictWs w = dict_ws(a);
+    const SteWs w = ste_ws(a);
     for (int k = threadIdx.x; k < a.K; k += 256) w.hist[((size_t)h * a.plan.S + sg) * a.K + k] = cnt[k];
     if (bad) report_index_error(a.status);
 }
@@ -93,7 +93,7 @@ __global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
 __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
     constexpr int T = 1024;
     __shared__ int sh[3][T];
-    const DictWs w = dict_ws(a);
+    const SteWs w = ste_ws(a);
     const int HK = a.H * a.K, t = threadIdx.x, P = a.plan.P, S = a.plan.S;
     const int per = (HK + T - 1) / T;
     const int g0 = min(t * per, HK), g1 = min(g0 + per, HK);
@@ -143,7 +143,7 @@ __global__ __launch_bounds__(256) void k_dict_scatter(SteGradArgs a) {
     __shared__ int wc[4][256];
     const int h = blockIdx.x / a.plan.S, sg = blockIdx.x - h * a.plan.S;
     const int t = threadIdx.x, wv = t >> 6, lane = t & 63;
-    const DictWs w = dict_ws(a);
+    const SteWs w = ste_ws(a);
     for (int k = t; k < a.K; k += 256) {
         int b = w.pos[h * a.K + k];
         for (int s2 = 0; s2 < sg; ++s2) b += w.hist[((size_t)h * a.plan.S + s2) * a.K + k];
@@ -185,11 +185,17 @@ __global__ __launch_bounds__(256) void k_dict_scatter(SteGradArgs a) {
 }
 
 // ------------------------------------------------------------------ outer products and scores
-// A wave owns an NB x NB block of G[h,k] (NB = 64: 2 x 2 tiles of 32 x 32;
-// NB = 32 for N <= 32, rows and columns past N zero).  N <= 64: one block,
-// four waves each take a quarter of the item's steps (each wave then holds
-// whole g and z rows of its steps) and add up in LDS at the end.  N = 128 /
-// 256: 4 / 16 waves, one block each, every step in lockstep.
+// An item's steps go in runs of RS steps that every wave of the workgroup
+// works on together.
+//   Outer products: a wave owns an NB x NB block of G[h,k] (NB = 64: 2 x 2
+//   tiles of 32 x 32; NB = 32 for N <= 32, rows and columns past N zero).
+//   N <= 64: one block, the four waves take a quarter of each run and add up
+//   in LDS at the end; N = 128 / 256: 4 / 16 waves, one block each, every step.
+//   Scores: the run's g and z rows are staged in LDS transposed, Gt[i][t] and
+//   Zt[j][t] (t = step of the run); lane t then reads Gt[pi_k(j)][t] for every
+//   (j, k): all lanes read one row, so the reads are contiguous and free of
+//   bank conflicts, and each lane sums its own step (no cross-lane
+//   reduction).  The waves split the maps in blocks of 16.
 template <int N>
 struct DictCfg {
     static constexpr int NB = N >= 64 ? 64 : 32;
@@ -198,12 +204,15 @@ struct DictCfg {
     static constexpr int SPLIT = BLOCKS >= 4 ? 1 : 4;
     static constexpr int WAVES = BLOCKS * SPLIT;
     static constexpr int TILES = NB / 32;
-    static constexpr int U = N >= 256 ? 2 : 8;  // steps per load batch (16 waves: 128 registers each)
-    static constexpr bool OWN_ROWS = N <= 64;   // a wave holds whole rows of its steps
-    static constexpr int SLQ = N > 64 ? N / 64 : 1;
-    // LDS: the cross-wave sum (after the loop) aliases the staged rows and the dictionary
+    static constexpr int RS = N <= 64 ? 64 : (N == 128 ? 32 : 16);  // steps per run (staged tiles <= ~70 KB)
+    static constexpr int MY = RS / SPLIT;                            // steps of a run one wave multiplies
+    static constexpr int U = N >= 256 ? 4 : 8;                       // steps per load batch
+    static constexpr int NBAT = MY / U;                              // load batches per run (even)
+    static constexpr int GP = RS + 1;                                // padded tile row (complex entries)
+    static constexpr int TILE_BYTES = 2 * N * GP * 8;
+    // the cross-wave sum after the loop aliases the tiles
     static constexpr int RED_BYTES = SPLIT > 1 ? (SPLIT - 1) * NB * NB * 4 : 0;
-    static constexpr int ROW_BYTES = (OWN_ROWS ? WAVES : 1) * U * 2 * N * 8;
+    static_assert(NBAT % 2 == 0 && NBAT >= 2, "runs are processed in pairs of batches");
 };
 
 __host__ __device__ inline int score_kp(int K) { return (K + 15) & ~15; }
@@ -211,27 +220,26 @@ __host__ __device__ inline int score_kp(int K) { return (K + 15) & ~15; }
 template <int N>
 size_t ste_gemm_lds(int K, bool q) {
     using Cfg = DictCfg<N>;
-    const size_t stage = q ? (size_t)Cfg::ROW_BYTES + (size_t)N * score_kp(K) : 0;
+    const size_t stage = q ? (size_t)Cfg::TILE_BYTES + (size_t)N * score_kp(K) : 0;
     return stage > (size_t)Cfg::RED_BYTES ? stage : (size_t)Cfg::RED_BYTES;
 }
 
 // One step's operands: lane l holds g[i0 + l] and z[j0 + l] (NB = 64) or
-// g[i0 + l%32], z[j0 + l%32] (NB = 32).
+// g[i0 + l%32], z[j0 + l%32] (NB = 32; lanes past N repeat entry N-1, which
+// only reaches rows and columns of the tile past N, never stored).  The loads
+// are unconditional (u is always a valid step) so that the compiler's wait
+// counts stay exact and the loads of later batches stay in flight.
 template <int N>
-__device__ __forceinline__ void load_step(const SteGradArgs& a, int u, int h, int i0, int j0, int lane, bool on,
+__device__ __forceinline__ void load_step(const SteGradArgs& a, int u, int h, int i0, int j0, int lane,
                                           float2& gv, float2& zv) {
     constexpr int NB = DictCfg<N>::NB;
-    const int r = NB == 64 ? lane : (lane & 31);
-    gv = make_float2(0.f, 0.f);
-    zv = make_float2(0.f, 0.f);
-    if (on && (NB == 64 || r < N)) {
-        typedef float f32x2 __attribute__((ext_vector_type(2)));
-        const size_t row = ((size_t)u * a.H + h) * N;
-        const f32x2 gq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.g + row + i0 + r));
-        const f32x2 zq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.z + row + j0 + r));
-        gv = make_float2(gq.x, gq.y);
-        zv = make_float2(zq.x, zq.y);
-    }
+    const int r = NB == 64 ? lane : min(lane & 31, N - 1);
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    const size_t row = ((size_t)u * a.H + h) * N;
+    const f32x2 gq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.g + row + i0 + r));
+    const f32x2 zq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.z + row + j0 + r));
+    gv = make_float2(gq.x, gq.y);
+    zv = make_float2(zq.x, zq.y);
 }
 
 // acc[ti][tj] += A_ti B_tj with A[m][0..1] = (g[m].re, g[m].im) and
@@ -259,57 +267,26 @@ __device__ __forceinline__ void mfma_step(f32x16 (&acc)[DictCfg<N>::TILES][DictC
     }
 }
 
-// Scores of every map at one step (Sec. 3.1 Prop. 2):
-// q[k] = sum_j Re(g[pi_k(j)] conj(z[j])) with the g and z rows in LDS (gs,
-// zs) and the head's maps transposed in dT (row j: pi_k(j) for every k, KP
-// bytes).  Lane l owns j = l*SLQ + s; maps go in blocks of 16 (one 16-byte
-// read of dT per j), then one transpose-reduction leaves the total of map
-// kb + l/4 in lane l.  Padding maps (k >= K) read row 0 and are not stored.
-template <int N>
-__device__ __forceinline__ void score_step(const float2* gs, const float2* zs, const uint8_t* dT, int KP, int K,
-                                           int lane, float* __restrict__ qrow) {
-    constexpr int SLQ = DictCfg<N>::SLQ;
-    for (int kb = 0; kb < K; kb += 16) {
-        float v[16];
-#pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = 0.f;
-#pragma unroll
-        for (int s = 0; s < SLQ; ++s) {
-            const int j = lane * SLQ + s;
-            if (j < N) {
-                const float2 zj = zs[j];
-                const uint4 pk = *reinterpret_cast<const uint4*>(dT + j * KP + kb);
-                const uint32_t wds[4] = {pk.x, pk.y, pk.z, pk.w};
-#pragma unroll
-                for (int u = 0; u < 16; ++u) {
-                    const float2 g = gs[(wds[u >> 2] >> (8 * (u & 3))) & 0xff];
-                    v[u] = fmaf(g.x, zj.x, fmaf(g.y, zj.y, v[u]));
-                }
-            }
-        }
-        const float tot = transpose_sum<16>(v, lane);
-        const int k = kb + (lane >> 2);
-        if ((lane & 3) == 0 && k < K) qrow[k] = tot;
-    }
-}
-
 // Element r of tile (ti, tj) in lane l sits at row 32 ti + 8 (r/4) + 4 (l/32) + r%4,
 // column 32 tj + l%32 of the wave's block.
 __device__ __forceinline__ int acc_row(int ti, int r, int lane) { return 32 * ti + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 __device__ __forceinline__ int acc_col(int tj, int lane) { return 32 * tj + (lane & 31); }
 
 // Per item: the outer products of its steps into G[h,k] (DO_G) and the
-// scores of every map at each of its steps (DO_Q; every step of the call
-// belongs to exactly one item).
-template <int N, bool DO_Q, bool DO_G>
+// scores q[b,t,h,k] = sum_j Re(g_t[pi_k(j)] conj(z_t[j])) of every map at
+// each of its steps (KW > 0: tasks of KW maps, spread over the waves; every
+// step of the call belongs to one item).
+template <int N, int KW, bool DO_G>
 __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs a) {
     using Cfg = DictCfg<N>;
-    constexpr int NB = Cfg::NB, T = Cfg::TILES, U = Cfg::U;
+    constexpr bool DO_Q = KW > 0;
+    constexpr int NB = Cfg::NB, T = Cfg::TILES, U = Cfg::U, RS = Cfg::RS, GP = Cfg::GP;
     extern __shared__ __align__(16) unsigned char lds[];
     float* red = reinterpret_cast<float*>(lds);
-    float2* rows = reinterpret_cast<float2*>(lds);
-    uint8_t* dT = lds + Cfg::ROW_BYTES;
-    const DictWs w = dict_ws(a);
+    float2* Gt = reinterpret_cast<float2*>(lds);
+    float2* Zt = Gt + N * GP;
+    uint8_t* dT = lds + Cfg::TILE_BYTES;
+    const SteWs w = ste_ws(a);
     const int HK = a.H * a.K, KP = score_kp(a.K);
     const int item = blockIdx.x;
     if (item >= w.item[HK]) return;
@@ -330,7 +307,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
     const int blk = wv / Cfg::SPLIT, part = wv - blk * Cfg::SPLIT;
     const int bi = blk / Cfg::GRID, bj = blk % Cfg::GRID;
     const int i0 = bi * NB, j0 = bj * NB;
-    const int s0 = (int)((long)cnt * part / Cfg::SPLIT), s1 = (int)((long)cnt * (part + 1) / Cfg::SPLIT);
+    const int my0 = part * Cfg::MY;  // this wave's first step within a run
 
     if constexpr (DO_Q) {
         // the head's maps, transposed: dT[j*KP + k] = pi[h,k,j] (0 for k >= K)
@@ -340,7 +317,6 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
             const int p = k < a.K ? pih[(size_t)k * N + j] : 0;
             dT[j * KP + k] = (uint8_t)((unsigned)p < (unsigned)N ? p : 0);
         }
-        __syncthreads();
     }
 
     f32x16 acc[T][T];
@@ -351,78 +327,115 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[ti][tj][r] = 0.f;
 
-    // the scores of one batch: stage its g and z rows in LDS, then one step each
-    auto scores = [&](const float2 (&gq)[U], const float2 (&zq)[U], int sid, int jb, int m) {
-        if constexpr (Cfg::OWN_ROWS) {
-            float2* gw = rows + wv * U * 2 * N;
-            wave_sync();
-            if (lane < N) {
+    // step ids of run r (lane t: step t; past the item: the item's last step,
+    // so every load below stays valid and unconditional)
+    auto run_ids = [&](int r) { return ord[min(r * RS + lane, cnt - 1)]; };
+    // batch b of run r (sidv = run_ids(r))
+    auto issue = [&](float2 (&gq)[U], float2 (&zq)[U], int sidv, int b) {
 #pragma unroll
-                for (int u = 0; u < U; ++u) {
-                    gw[u * N + lane] = gq[u];
-                    gw[(U + u) * N + lane] = zq[u];
+        for (int u = 0; u < U; ++u)
+            load_step<N>(a, readlane_i(sidv, my0 + b * U + u), h, i0, j0, lane, gq[u], zq[u]);
+    };
+    // rows of batch b into the tiles: column t = the step's place in the run
+    auto stage = [&](const float2 (&gq)[U], const float2 (&zq)[U], int b) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int t = my0 + b * U + u;
+            if constexpr (Cfg::SPLIT > 1) {
+                if (lane < N) {
+                    Gt[lane * GP + t] = gq[u];
+                    Zt[lane * GP + t] = zq[u];
+                }
+            } else {
+                if (bj == 0) Gt[(i0 + lane) * GP + t] = gq[u];
+                if (bi == 0) Zt[(j0 + lane) * GP + t] = zq[u];
+            }
+        }
+    };
+    auto multiply = [&](const float2 (&gq)[U], const float2 (&zq)[U], int r, int b) {
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (r * RS + my0 + b * U + u < cnt) mfma_step<N>(acc, gq[u], zq[u], lane);
+    };
+    // scores of the run's steps: lane t = step t of the run, KW maps per task
+    auto scores = [&](int sidv, int r) {
+        const bool on = lane < RS && r * RS + lane < cnt;
+        const int tt = on ? lane : 0;
+        constexpr int KWD = KW > 0 ? KW : 1;
+        const int ntask = (a.K + KWD - 1) / KWD;
+        for (int task = wv; task < ntask; task += Cfg::WAVES) {
+            const int kb = task * KW;
+            float v[KW > 0 ? KW : 1];
+#pragma unroll
+            for (int u = 0; u < KW; ++u) v[u] = 0.f;
+#pragma unroll 2
+            for (int j = 0; j < N; ++j) {
+                const float2 zt = Zt[j * GP + tt];
+                uint32_t wds[KW / 4 > 0 ? KW / 4 : 1];
+                if constexpr (KW == 16) {
+                    const uint4 pk = *reinterpret_cast<const uint4*>(dT + j * KP + kb);
+                    wds[0] = pk.x, wds[1] = pk.y, wds[2] = pk.z, wds[3] = pk.w;
+                } else if constexpr (KW == 8) {
+                    const uint2 pk = *reinterpret_cast<const uint2*>(dT + j * KP + kb);
+                    wds[0] = pk.x, wds[1] = pk.y;
+                } else {
+                    wds[0] = *reinterpret_cast<const uint32_t*>(dT + j * KP + kb);
+                }
+#pragma unroll
+                for (int u = 0; u < KW; ++u) {
+                    const float2 g = Gt[((wds[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
+                    v[u] = fmaf(g.x, zt.x, fmaf(g.y, zt.y, v[u]));
                 }
             }
-            wave_sync();
+            if (on) {
+                float* qrow = a.q + ((size_t)sidv * a.H + h) * a.K + kb;
+                if (kb + KW <= a.K && (a.K & 3) == 0) {
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (jb + u < m)
-                    score_step<N>(gw + u * N, gw + (U + u) * N, dT, KP, a.K, lane,
-                                  a.q + ((size_t)readlane_i(sid, jb + u) * a.H + h) * a.K);
-        } else {
-            // waves of block column 0 hold the g slices, of block row 0 the z slices
-            __syncthreads();
+                    for (int u = 0; u < KW; u += 4)
+                        *reinterpret_cast<float4*>(qrow + u) = make_float4(v[u], v[u + 1], v[u + 2], v[u + 3]);
+                } else {
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                if (bj == 0) rows[u * N + i0 + lane] = gq[u];
-                if (bi == 0) rows[(U + u) * N + j0 + lane] = zq[u];
+                    for (int u = 0; u < KW; ++u)
+                        if (kb + u < a.K) qrow[u] = v[u];
+                }
             }
-            __syncthreads();
-            for (int u = wv; u < U; u += Cfg::WAVES)
-                if (jb + u < m)
-                    score_step<N>(rows + u * N, rows + (U + u) * N, dT, KP, a.K, lane,
-                                  a.q + ((size_t)readlane_i(sid, jb + u) * a.H + h) * a.K);
         }
     };
 
-    // steps in runs of 64 ids (one per lane), operands in batches of U with
-    // the next batch in flight while the current one is multiplied
-    for (int s = s0; s < s1; s += 64) {
-        const int m = min(64, s1 - s);
-        const int sid = lane < m ? ord[s + lane] : 0;
-        float2 ga[U], za[U], gb[U], zb[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) load_step<N>(a, readlane_i(sid, u < m ? u : 0), h, i0, j0, lane, u < m, ga[u], za[u]);
-        for (int j = 0; j < m; j += 2 * U) {
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int jj = j + U + u;
-                load_step<N>(a, readlane_i(sid, jj < m ? jj : 0), h, i0, j0, lane, jj < m, gb[u], zb[u]);
-            }
+    // Two load batches are always in flight or ready: batch b is multiplied,
+    // then its registers take batch b + 2 (of the next run for the last two,
+    // so those loads run during the scores).  Step ids come two runs ahead.
+    const int nrun = (cnt + RS - 1) / RS;
+    int sid = run_ids(0), sidn = run_ids(1);
+    float2 ga[U], za[U], gb[U], zb[U];
+    issue(ga, za, sid, 0);
+    issue(gb, zb, sid, 1);
+    for (int r = 0; r < nrun; ++r) {
+        const int sidnn = run_ids(r + 2);
+        for (int b = 0; b < Cfg::NBAT; b += 2) {
+            if constexpr (DO_G) multiply(ga, za, r, b);
+            if constexpr (DO_Q) stage(ga, za, b);
+            if (b + 2 < Cfg::NBAT) issue(ga, za, sid, b + 2);
+            else issue(ga, za, sidn, 0);
             issue_fence();
-            if constexpr (DO_G) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) mfma_step<N>(acc, ga[u], za[u], lane);
-            }
-            if constexpr (DO_Q) scores(ga, za, sid, j, m);
-            if (j + U >= m) break;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int jj = j + 2 * U + u;
-                load_step<N>(a, readlane_i(sid, jj < m ? jj : 0), h, i0, j0, lane, jj < m, ga[u], za[u]);
-            }
+            if constexpr (DO_G) multiply(gb, zb, r, b + 1);
+            if constexpr (DO_Q) stage(gb, zb, b + 1);
+            if (b + 3 < Cfg::NBAT) issue(gb, zb, sid, b + 3);
+            else issue(gb, zb, sidn, 1);
             issue_fence();
-            if constexpr (DO_G) {
-#pragma unroll
-                for (int u = 0; u < U; ++u) mfma_step<N>(acc, gb[u], zb[u], lane);
-            }
-            if constexpr (DO_Q) scores(gb, zb, sid, j + U, m);
         }
+        if constexpr (DO_Q) {
+            __syncthreads();  // tiles (and, in the first run, the maps) complete
+            scores(sid, r);
+            __syncthreads();  // tiles free for the next run
+        }
+        sid = sidn;
+        sidn = sidnn;
     }
     if constexpr (!DO_G) return;
 
     if constexpr (Cfg::SPLIT > 1) {
-        __syncthreads();  // red aliases the staged rows
+        __syncthreads();  // red aliases the tiles
         if (part > 0) {
 #pragma unroll
             for (int ti = 0; ti < T; ++ti)
@@ -460,7 +473,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 // groups no step chose get zeros; single-item groups were written directly.
 template <int N>
 __global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
-    const DictWs w = dict_ws(a);
+    const SteWs w = ste_ws(a);
     const int gi = blockIdx.x;
     const int pieces = w.item[gi + 1] - w.item[gi];
     if (pieces == 1) return;
@@ -474,10 +487,10 @@ __global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
     }
 }
 
-template <int N, bool DO_Q, bool DO_G>
+template <int N, int KW, bool DO_G>
 hipError_t gemm_launch(const SteGradArgs& a, hipStream_t st) {
-    auto kern = k_ste_gemm<N, DO_Q, DO_G>;
-    const size_t lds = ste_gemm_lds<N>(a.K, DO_Q);
+    auto kern = k_ste_gemm<N, KW, DO_G>;
+    const size_t lds = ste_gemm_lds<N>(a.K, KW > 0);
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
@@ -487,8 +500,15 @@ hipError_t gemm_launch(const SteGradArgs& a, hipStream_t st) {
 
 template <int N>
 hipError_t dict_launch(const SteGradArgs& a, hipStream_t st) {
-    hipError_t e = a.q ? (a.G ? gemm_launch<N, true, true>(a, st) : gemm_launch<N, true, false>(a, st))
-                       : gemm_launch<N, false, true>(a, st);
+    // score tasks of 16, 8 or 4 maps: wide enough to amortise each z read,
+    // many enough to keep every wave busy
+    const int waves = DictCfg<N>::WAVES;
+    hipError_t e;
+    if (!a.q) e = gemm_launch<N, 0, true>(a, st);
+    else if (N < 256 && a.K >= 16 * waves)  // (16 waves x 16 maps would spill registers)
+        e = a.G ? gemm_launch<N, N < 256 ? 16 : 8, true>(a, st) : gemm_launch<N, N < 256 ? 16 : 8, false>(a, st);
+    else if (a.K >= 8 * waves) e = a.G ? gemm_launch<N, 8, true>(a, st) : gemm_launch<N, 8, false>(a, st);
+    else e = a.G ? gemm_launch<N, 4, true>(a, st) : gemm_launch<N, 4, false>(a, st);
     if (e != hipSuccess || !a.G) return e;
     const int ys = (N * N + 255) / 256 < 16 ? (N * N + 255) / 256 : 16;
     hipLaunchKernelGGL(k_dict_reduce<N>, dim3(a.H * a.K, ys), dim3(256), 0, st, a);
