@@ -9,8 +9,9 @@ bench.py uses to attach counter-measured HBM traffic to its roofline object.
     python -m paper_2605_19150_amd.profiling traffic --kernel k_fwd_fused --workload NAME \\
         --fetch DIR --write DIR --copy-fetch DIR --copy-write DIR --command "..." > profiles/Y.md
 
-A traffic summary records a hash of the library sources; read_traffic_summary
-returns None once the sources differ from the ones the counters were taken on.
+A traffic summary records a hash of the kernel's sources (KERNEL_SOURCES);
+read_traffic_summary returns None once they differ from the ones the counters
+were taken on.
 """
 import argparse
 import collections
@@ -34,11 +35,26 @@ def _code_only(text):
     return " ".join(text.split())
 
 
-def source_hash():
-    """Hash of the code (comments and layout ignored) of every source file the
-    kernels are built from."""
+# The device code of each measured kernel: its translation unit and the
+# headers it includes.  A traffic summary stays valid while these are
+# unchanged (comments aside).
+KERNEL_SOURCES = {
+    "k_fwd_fused": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
+    "k_bwd_fused": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
+    "k_bwd_fused_ste": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
+    "k_ste_gemm": ["pdssm_ste.hip", "pdssm_internal.h", "pdssm_device.h"],
+}
+
+
+def source_hash(kernel=None):
+    """Hash of the code (comments and layout ignored) of the source files the
+    kernel is built from (every library source when the kernel is not
+    listed in KERNEL_SOURCES)."""
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(PKG, "csrc", "*"))) + [os.path.join(ROOT, "include", "pdssm.h")]
+    if kernel in KERNEL_SOURCES:
+        files = [os.path.join(PKG, "csrc", f) for f in KERNEL_SOURCES[kernel]]
+    else:
+        files = sorted(glob.glob(os.path.join(PKG, "csrc", "*"))) + [os.path.join(ROOT, "include", "pdssm.h")]
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, encoding="utf-8") as fh:
@@ -97,7 +113,7 @@ def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, com
         "kernel: %s" % kernel,
         "dispatches: %s" % match,
         "workload: %s" % workload,
-        "source-hash: %s" % source_hash(),
+        "source-hash: %s" % source_hash(kernel),
         "fetch-bytes-per-launch: %.0f" % fetch_b,
         "write-bytes-per-launch: %.0f" % write_b,
         "traffic-bytes-per-launch: %.0f" % (fetch_b + write_b),
@@ -116,7 +132,7 @@ def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, com
 def read_traffic_summary(profiles_dir, kernel, workload):
     """traffic-bytes-per-launch of the matching summary in profiles_dir, or
     None (no summary, or taken on other kernel sources)."""
-    want = source_hash()
+    want = source_hash(kernel)
     for path in sorted(glob.glob(os.path.join(profiles_dir, "*.md"))):
         kv = {}
         with open(path) as fh:
@@ -150,7 +166,8 @@ def main(argv=None):
         sys.stdout.write(traffic_markdown(a.kernel, a.workload, a.fetch, a.write, a.copy_fetch,
                                           a.copy_write, a.command, a.match))
     else:
-        print(source_hash())
+        for k in sorted(KERNEL_SOURCES):
+            print(k, source_hash(k))
 
 
 if __name__ == "__main__":
