@@ -25,8 +25,13 @@ prepare, forward, the backward with the scaled states (pdssm_scan_bwd_ste),
 the candidate-map scores and the dictionary gradient (pdssm_ste_grads) and
 the two tempered-softmax products (routing logits, dense dictionary); the
 line then carries an "ste" object with each call's time and roofline.
+
+--decode times single-step decode instead (pdssm_decode_step: one recurrence
+step per sequence, state updated in place), back to back on the workload's
+B, H, N, K; value = state updates (B*H*N) per second, with its bytes per step.
 """
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -122,6 +127,57 @@ def traffic_from_profiles(kernel, workload_name):
     return read_traffic_summary(os.path.join(ROOT, "profiles"), kernel, workload_name)
 
 
+def decode_bench(args, w, dev):
+    """Single-step decode: steps of one token for every (batch, head)
+    sequence, in place, back to back (launch cost included)."""
+    import torch
+    from paper_2605_19150_amd import pdssm
+    from paper_2605_19150_amd.inputs import make_inputs
+
+    T = 64  # distinct tokens cycled through
+    inp = make_inputs(w.B, T, w.H, w.N, w.K, seed=0, pi_kind=w.pi_kind, dmag=w.dmag, bc_var=w.bc_var,
+                      idx_kind=w.idx_kind, with_h0=True)
+    tok = [{k: torch.from_numpy(np.ascontiguousarray(inp[k][:, t])).to(dev) for k in ("idx", "D", "b", "c")}
+           for t in range(T)]
+    pi = torch.from_numpy(inp["pi"]).to(dev)
+    h = torch.from_numpy(inp["h0"]).to(dev)
+    y = torch.empty((w.B, w.H), dtype=torch.float32, device=dev)
+    L = pdssm.load()
+    d = pdssm.desc(w.B, 1, w.H, w.N, w.K)
+    st = pdssm._stream(None)
+    args_of = [[ctypes.byref(d), pdssm._p(x["idx"]), pdssm._p(pi), pdssm._p(x["D"]), pdssm._p(x["b"]),
+                pdssm._p(x["c"]), pdssm._p(h), pdssm._p(h), pdssm._p(y), None, st] for x in tok]
+
+    def run(n):
+        for i in range(n):
+            rc = L.pdssm_decode_step(*args_of[i % T])
+            if rc != pdssm.OK:
+                raise pdssm.PdssmError(rc, "pdssm_decode_step")
+
+    steps = max(args.steps, 1) * 20
+    run(max(args.warmup, 1) * 5)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    run(steps)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    nseq = w.B * w.H
+    nbytes = nseq * (4 + 4 + 5 * w.N * 8) + w.H * w.K * w.N * 4  # idx, y; D, b, c, h in, h out; dictionary
+    print(json.dumps({
+        "metric": "PD-scan single-step decode state-updates/s (B*H*N per step)",
+        "value": nseq * w.N / (ms * 1e-3), "unit": "state-updates/s", "n_gpus": 1, "steps": steps,
+        "warmup": max(args.warmup, 1) * 5, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic (seeded, shapes and distributions of the named workload)",
+        "config": {"workload": w.name + " decode", "B": w.B, "H": w.H, "N": w.N, "K": w.K, "step": "decode",
+                   "parallelism": "single-gpu"},
+        "decode": {"kernel": "k_decode", "alg_bytes": nbytes, "alg_GBps": nbytes / (ms * 1e-3) / 1e9,
+                   "note": "back-to-back launches, one per token: launch-bound at these sizes"},
+        "device": torch.cuda.get_device_name(dev),
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -135,6 +191,7 @@ def main():
     ap.add_argument("--ste", action="store_true",
                     help="time the straight-through step (scores, dictionary gradient, softmax products)")
     ap.add_argument("--temp", type=float, default=1.0, help="softmax temperature of --ste")
+    ap.add_argument("--decode", action="store_true", help="time single-step decode instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling aid: time a plain 1 GiB device copy instead")
     args = ap.parse_args()
@@ -167,6 +224,9 @@ def main():
         return
 
     w = WORKLOADS[args.workload]
+    if args.decode:
+        decode_bench(args, w, dev)
+        return
     print("bench: workload %d (%s): generating inputs" % (args.workload, w.name), file=sys.stderr,
           flush=True)
     inp = workload_inputs(args.workload, seed=0)

@@ -241,6 +241,25 @@ int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer,
                       int64_t inner, float temp, void* stream);
 
 /*
+ * One step of the recurrence for every (batch, head) sequence: the
+ * constant-memory recurrent form used for token-by-token inference (App. E.2
+ * recurrence with the column-one-hot map of Sec. 3.1 eq. (5), readout of
+ * Sec. 2.1 eq. (1)):
+ *   h_out[r] = b[r] + sum_{j: pi_t[j] = r} D[j] * h_in[j],  pi_t = pi[h, idx[b,h], :],
+ *   y = Re( sum_n c[n] * h_out[n] ).
+ * Colliding sources add in ascending source order.  desc: B, H, N, K are
+ * used (N and K as for the scans), L and chunk are ignored.
+ * In:  idx [B,H] int32, pi [H,K,N] int32, D, b, c [B,H,N] complex,
+ *      h_in [B,H,N] complex (NULL = zero state).
+ * Out: h_out [B,H,N] complex (may be the same buffer as h_in: in-place
+ *      update), y [B,H] float32.  Needs no workspace.
+ */
+int pdssm_decode_step(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
+                      const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                      const pdssm_c64* h_in, pdssm_c64* h_out, float* y, int* dev_status,
+                      void* stream);
+
+/*
  * Composed operator of every chunk in PD form (App. E.3.1 accumulator update,
  * App. E.2 associative operator): for chunk c of sequence (b,h),
  * A_{e-1} ... A_s with A_t = P_t D_t is returned as pi_out[b,h,c,:] (int32,

@@ -16,6 +16,7 @@ SOURCES = [("pdssm_fused.hip", ["-DPDSSM_N=%d" % n], "pdssm_fused_n%d" % n)
            for n in (64, 128, 256, 32, 16, 8)] + [
     ("pdssm_chunked.hip", [], "pdssm_chunked"),
     ("pdssm_ste.hip", [], "pdssm_ste"),
+    ("pdssm_decode.hip", [], "pdssm_decode"),
     ("pdssm_api.cpp", [], "pdssm_api"),
 ]
 

@@ -6,6 +6,7 @@
 
 #include <initializer_list>
 
+#include "pdssm_decode.h"
 #include "pdssm_fused.h"
 #include "pdssm_internal.h"
 
@@ -480,6 +481,38 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
     a.ws = static_cast<unsigned char*>(ws);
     a.status = dev_status;
     return pdssm::launch_ste_grads(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+int pdssm_decode_step(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, const pdssm_c64* D,
+                      const pdssm_c64* b, const pdssm_c64* c, const pdssm_c64* h_in, pdssm_c64* h_out, float* y,
+                      int* dev_status, void* stream) {
+    const int st = check_dims(d);
+    if (st != PDSSM_OK) return st;
+    if (!idx || !pi || !D || !b || !c || !h_out || !y) return PDSSM_ERR_INVALID_ARG;
+    for (const void* p : {(const void*)pi, (const void*)D, (const void*)b, (const void*)c, (const void*)h_in,
+                          (const void*)h_out})
+        if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    const size_t nseq = (size_t)d->B * d->H, nrow = nseq * d->N * 8;
+    const size_t npi = (size_t)d->H * d->K * d->N * 4;
+    // the state may be updated in place (h_out == h_in); no other overlap
+    if (any_overlap({{h_out, nrow}, {y, nseq * 4}},
+                    {{idx, nseq * 4}, {pi, npi}, {D, nrow}, {b, nrow}, {c, nrow}, {h_in == h_out ? nullptr : h_in, nrow}}))
+        return PDSSM_ERR_INVALID_ARG;
+    pdssm::DecodeArgs a = {};
+    a.B = d->B;
+    a.H = d->H;
+    a.N = d->N;
+    a.K = d->K;
+    a.idx = idx;
+    a.pi = pi;
+    a.D = reinterpret_cast<const float2*>(D);
+    a.b = reinterpret_cast<const float2*>(b);
+    a.c = reinterpret_cast<const float2*>(c);
+    a.h_in = reinterpret_cast<const float2*>(h_in);
+    a.h_out = reinterpret_cast<float2*>(h_out);
+    a.y = y;
+    a.status = dev_status;
+    return pdssm::launch_decode(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
 int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int32_t len, int64_t inner,

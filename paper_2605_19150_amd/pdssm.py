@@ -41,7 +41,7 @@ class Desc(ctypes.Structure):
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
            "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
            "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_ste_grads",
-           "pdssm_softmax_vjp")
+           "pdssm_softmax_vjp", "pdssm_decode_step")
 
 
 def lib_path():
@@ -79,6 +79,8 @@ def load():
     L.pdssm_softmax_vjp.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32, ctypes.c_int64,
                                     ctypes.c_float, P]
     L.pdssm_softmax_vjp.restype = I
+    L.pdssm_decode_step.argtypes = [D] + [P] * 10
+    L.pdssm_decode_step.restype = I
     if L.pdssm_abi_version() != 1:
         raise ImportError("libpdssm.so ABI version mismatch")
     _lib = L
@@ -364,3 +366,33 @@ def softmax_vjp(x, gy, dim, temp, out=None, stream=None):
 def surrogate_grads(q, G, logits, M, temp, stream=None):
     """The two surrogate gradients of Prop. 2: (d logits [B,L,H,K], dM [H,K,N,N])."""
     return softmax_vjp(logits, q, 3, temp, stream=stream), softmax_vjp(M, G, 2, temp, stream=stream)
+
+
+def decode_step(idx, pi, D, b, c, h=None, out=None, y=None, stream=None, check=True):
+    """One recurrence step per sequence: returns (h_new [B,H,N] c64, y [B,H] f32).
+    idx [B,H] int32; D, b, c [B,H,N] c64; h [B,H,N] c64 or None (zero state).
+    out may be h itself (in-place update)."""
+    B, H = idx.shape
+    H2, K, N = pi.shape
+    if H2 != H:
+        raise ValueError("idx and pi disagree on H")
+    dev = idx.device
+    _need(idx, "idx", torch.int32, (B, H), dev)
+    _need(pi, "pi", torch.int32, (H, K, N), dev)
+    for t, n in ((D, "D"), (b, "b"), (c, "c")):
+        _need(t, n, torch.complex64, (B, H, N), dev)
+    if h is not None:
+        _need(h, "h", torch.complex64, (B, H, N), dev)
+    out = torch.empty((B, H, N), dtype=torch.complex64, device=dev) if out is None else out
+    y = torch.empty((B, H), dtype=torch.float32, device=dev) if y is None else y
+    status = torch.zeros(1, dtype=torch.int32, device=dev) if check else None
+    d = desc(B, 1, H, N, K)
+    st = load().pdssm_decode_step(ctypes.byref(d), _p(idx), _p(pi), _p(D), _p(b), _p(c), _p(h), _p(out), _p(y),
+                                  _p(status), _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_decode_step")
+    if check:
+        torch.cuda.synchronize(dev)
+        if int(status.item()) != OK:
+            raise PdssmError(int(status.item()), "kernel index check")
+    return out, y

@@ -229,3 +229,22 @@ def test_ste_grads_workspace_bounds(lib):
         B, L, H, N, K = dims
         n = pdssm.workspace_size(d, pdssm.OP_STE_GRADS)
         assert n <= B * L * H * 4 + H * K * 64 * 1024 + (1 << 28) + 64 * 256, dims
+
+
+def test_decode_host_checks(lib):
+    d = pdssm.desc(2, 1, 3, 64, 4)
+    f = FakeBufs()
+    row = 2 * 3 * 64 * 8
+    idx, pi, D, b, c, h, y = f(2 * 3 * 4), f(3 * 4 * 64 * 4), f(row), f(row), f(row), f(row), f(2 * 3 * 4)
+    call = lambda *a: lib.pdssm_decode_step(ctypes.byref(d), *a, None, None)  # noqa: E731
+    for i in (0, 1, 2, 3, 4, 6, 7):   # every pointer but h_in is required
+        args = [idx, pi, D, b, c, h, h, y]
+        args[i] = None
+        assert call(*args) == pdssm.ERR_INVALID_ARG, i
+    assert call(idx, pi, D, b, c, h, D, y) == pdssm.ERR_INVALID_ARG            # h_out over D
+    assert call(idx, pi, D, b, c, h, ctypes.c_void_p(h.value + 64), y) == pdssm.ERR_INVALID_ARG  # partial overlap
+    assert call(idx, pi, D, b, c, h, h, ctypes.c_void_p(h.value + 8)) == pdssm.ERR_INVALID_ARG   # y over h
+    assert call(idx, pi, ctypes.c_void_p(D.value + 8), b, c, None, h, y) == pdssm.ERR_INVALID_ARG
+    bad = pdssm.desc(2, 1, 3, 48, 4)
+    assert lib.pdssm_decode_step(ctypes.byref(bad), idx, pi, D, b, c, None, h, y, None,
+                                 None) == pdssm.ERR_UNSUPPORTED

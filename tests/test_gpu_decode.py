@@ -1,0 +1,107 @@
+"""GPU parity of the single-step decode (pdssm_decode_step) against the
+float64 oracle: one step of the recurrence is the oracle's forward with L = 1
+and h0 = the incoming state.  Tolerance as for the scan (|gpu - ref| <=
+1e-5 + 1e-4*|ref| per real component); the automaton embedding is exact."""
+import numpy as np
+import pytest
+
+from helpers import assert_close
+from oracle import oracle_fwd
+from paper_2605_19150_amd.inputs import fsa_inputs, make_inputs
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU machines, never run there
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2605_19150_amd import pdssm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def step_inputs(inp, t):
+    """The [B,H,...] slices of step t of a [B,L,H,...] input set."""
+    return {k: np.ascontiguousarray(inp[k][:, t]) for k in ("idx", "D", "b", "c")}
+
+
+@pytest.mark.parametrize("N", [8, 16, 32, 64, 128, 256])
+@pytest.mark.parametrize("pi_kind", ["uniform", "perm"])
+def test_one_step_matches_oracle(N, pi_kind):
+    print("decode N=%d %s" % (N, pi_kind), flush=True)
+    inp = make_inputs(3, 1, 5, N, 7, seed=N + (pi_kind == "perm"), pi_kind=pi_kind, with_h0=True)
+    s = step_inputs(inp, 0)
+    h, y = pdssm.decode_step(dev(s["idx"]), dev(inp["pi"]), dev(s["D"]), dev(s["b"]), dev(s["c"]),
+                             h=dev(inp["h0"]))
+    ry, rh, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp["h0"])
+    assert_close("y", y.cpu().numpy(), ry[:, 0])
+    assert_close("h", h.cpu().numpy(), rh)
+
+
+def test_zero_state_and_all_to_one_map():
+    N, K = 64, 3
+    inp = make_inputs(2, 1, 4, N, K, seed=3)
+    inp["pi"][:, 1, :] = 0            # map 1 sends every source to row 0
+    inp["idx"][:] = 1
+    s = step_inputs(inp, 0)
+    h, y = pdssm.decode_step(dev(s["idx"]), dev(inp["pi"]), dev(s["D"]), dev(s["b"]), dev(s["c"]))
+    ry, rh, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"])
+    assert_close("y", y.cpu().numpy(), ry[:, 0])
+    assert_close("h", h.cpu().numpy(), rh)
+
+
+@pytest.mark.parametrize("N", [16, 64, 128])
+def test_steps_in_place_follow_the_scan(N):
+    """T decode steps, updating the state in place, against the oracle's
+    T-step forward and against the GPU scan of the same T steps."""
+    B, T, H, K = 2, 37, 3, 5
+    inp = make_inputs(B, T, H, N, K, seed=10 + N, with_h0=True)
+    pi = dev(inp["pi"])
+    h = dev(inp["h0"]).clone()
+    ys = []
+    for t in range(T):
+        s = step_inputs(inp, t)
+        h, y = pdssm.decode_step(dev(s["idx"]), pi, dev(s["D"]), dev(s["b"]), dev(s["c"]), h=h, out=h)
+        ys.append(y.cpu().numpy())
+    ry, rh, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp["h0"])
+    assert_close("y", np.stack(ys, 1), ry)
+    assert_close("h", h.cpu().numpy(), rh)
+    T_ = {k: dev(inp[k]) for k in ("idx", "D", "b", "c", "h0")}
+    sy, sh, _ = pdssm.scan_fwd(T_["idx"], pi, T_["D"], T_["b"], T_["c"], h0=T_["h0"])
+    assert_close("y vs scan", np.stack(ys, 1), sy.cpu().numpy().astype(np.float64))
+    assert_close("h vs scan", h.cpu().numpy(), sh.cpu().numpy().astype(np.complex128))
+
+
+@pytest.mark.parametrize("perm", [False, True])
+def test_automaton_exact(perm):
+    """App. D embedding: D = 1, b = 0, one-hot state; every step moves the one
+    to the automaton's next state exactly."""
+    B, L, H, N, K = 3, 50, 4, 32, 6
+    inp = fsa_inputs(B, L, H, N, K, seed=4, perm=perm)
+    pi = dev(inp["pi"])
+    h = dev(inp["h0"]).clone()
+    P = inp["pi"]
+    q = inp["start"].copy()
+    for t in range(L):
+        s = step_inputs(inp, t)
+        h, y = pdssm.decode_step(dev(s["idx"]), pi, dev(s["D"]), dev(s["b"]), dev(s["c"]), h=h, out=h)
+        for bb in range(B):
+            for hh in range(H):
+                q[bb, hh] = P[hh, inp["idx"][bb, t, hh], q[bb, hh]]
+        ref = np.zeros((B, H, N), np.complex64)
+        ref[np.arange(B)[:, None], np.arange(H)[None, :], q] = 1.0
+        np.testing.assert_array_equal(h.cpu().numpy(), ref)
+        acc = inp["c"][:, t].real
+        np.testing.assert_array_equal(y.cpu().numpy(), np.take_along_axis(acc, q[..., None], 2)[..., 0])
+
+
+def test_bad_index_reported():
+    inp = make_inputs(1, 1, 2, 64, 3, seed=1)
+    s = step_inputs(inp, 0)
+    s["idx"][0, 1] = 5
+    with pytest.raises(pdssm.PdssmError):
+        pdssm.decode_step(dev(s["idx"]), dev(inp["pi"]), dev(s["D"]), dev(s["b"]), dev(s["c"]))
