@@ -78,13 +78,26 @@ typedef struct pdssm_c64 {
 typedef struct pdssm_desc {
     int32_t B, L, H, N, K; /* batch, steps, heads, state size, dictionary size */
     int32_t chunk;         /* steps per chunk; 0 = default; fwd and bwd must agree */
-    uint32_t flags;        /* 0 or PDSSM_FLAG_PREPARED */
+    uint32_t flags;        /* 0 or PDSSM_FLAG_PREPARED | PDSSM_FLAG_BF16_IO */
 } pdssm_desc;
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd: the dictionary tables in
  * ws were built by pdssm_prepare for this desc and the current contents of pi;
  * the scan reuses them instead of rebuilding them. */
 #define PDSSM_FLAG_PREPARED 1u
+
+/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd (and pdssm_prepare,
+ * which ignores it): D, b, c and dD, db, dc are bf16 (re, im) pairs, 4 bytes
+ * per complex entry (real part in the low 16 bits; torch:
+ * view_as_real(x).to(bfloat16)), the paper's bf16 input setting (App. E,
+ * kernel efficiency: the complex inputs split into two bf16 halves, fp32
+ * arithmetic).  Every other tensor (idx, pi, h0, h_final, saved, y, dy,
+ * dh_final, dh0) keeps its type.  The arithmetic is fp32 as without the
+ * flag: inputs widen exactly, gradients are rounded to nearest (ties to
+ * even) when stored.  Only the single-read kernels support it
+ * (pdssm_uses_fused(desc) == 1); other entry points and the multi-pass
+ * kernels return PDSSM_ERR_UNSUPPORTED, as does pdssm_scan_bwd_ste. */
+#define PDSSM_FLAG_BF16_IO 2u
 
 typedef enum pdssm_status {
     PDSSM_OK = 0,

@@ -24,12 +24,15 @@ struct Lay {
 };
 
 // ------------------------------------------------------------------ complex
+// Complex products with explicit fused multiply-adds: the rounding is fixed
+// by the source, not by where the compiler chooses to contract, so every
+// kernel variant (e.g. fp32 or bf16 input/output) computes the same bits.
 __device__ __forceinline__ float2 cmul(float2 a, float2 b) {
-    return make_float2(a.x * b.x - a.y * b.y, a.x * b.y + a.y * b.x);
+    return make_float2(fmaf(a.x, b.x, -(a.y * b.y)), fmaf(a.x, b.y, a.y * b.x));
 }
 // conj(a) * b
 __device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
-    return make_float2(a.x * b.x + a.y * b.y, a.x * b.y - a.y * b.x);
+    return make_float2(fmaf(a.x, b.x, a.y * b.y), fmaf(a.x, b.y, -(a.y * b.x)));
 }
 __device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
 
@@ -130,8 +133,8 @@ constexpr int kBufferDword3 = 0x00020000;  // raw buffer, gfx9 family
 // nontemporal hint (nt) of gfx94x/gfx950.
 constexpr int kLoadStream = 2;
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_block(const float2* base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float2*>(base), 0, bytes, kBufferDword3);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_block(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, bytes, kBufferDword3);
 }
 
 // This lane's SL consecutive complex entries of the row at byte offset soff;
@@ -151,6 +154,65 @@ __device__ __forceinline__ CV<SL> ld_row(__amdgpu_buffer_rsrc_t r, uint32_t voff
         }
     }
     return out;
+}
+
+// ------------------------------------------------------------------ bf16 (re, im) pairs
+// A complex value in 32 bits: bf16 real part in the low half, bf16 imaginary
+// part in the high half (torch: view_as_real(x).to(bfloat16)).  Widening is
+// exact; narrowing rounds each part to nearest, ties to even (finite values).
+__device__ __forceinline__ float2 bf2_to_f2(uint32_t w) {
+    return make_float2(__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u));
+}
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float v) {
+    const uint32_t u = __float_as_uint(v);
+    return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+__device__ __forceinline__ uint32_t f2_to_bf2(float2 v) {
+    return f32_to_bf16_bits(v.x) | (f32_to_bf16_bits(v.y) << 16);
+}
+
+// ld_row for rows of bf16 pairs (4 bytes per entry).
+template <int SL, int AUX = 0>
+__device__ __forceinline__ CV<SL> ld_row_bf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    CV<SL> out;
+    if constexpr (SL == 1) {
+        out.v[0] = bf2_to_f2(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
+    } else if constexpr (SL == 2) {
+        const uint2 q = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
+        out.v[0] = bf2_to_f2(q.x);
+        out.v[1] = bf2_to_f2(q.y);
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4) {
+            const uint4 q =
+                __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff + 4 * s, AUX));
+            out.v[s] = bf2_to_f2(q.x);
+            out.v[s + 1] = bf2_to_f2(q.y);
+            out.v[s + 2] = bf2_to_f2(q.z);
+            out.v[s + 3] = bf2_to_f2(q.w);
+        }
+    }
+    return out;
+}
+
+// This lane's SL entries of a bf16-pair row (row + lane*SL), rounded, with the
+// nontemporal hint (rows written once).
+template <int SL>
+__device__ __forceinline__ void st_row_bf_stream(uint32_t* __restrict__ row, int lane, const CV<SL>& x) {
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    uint32_t* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        __builtin_nontemporal_store(f2_to_bf2(x.v[0]), p);
+    } else if constexpr (SL == 2) {
+        __builtin_nontemporal_store(u32x2{f2_to_bf2(x.v[0]), f2_to_bf2(x.v[1])}, reinterpret_cast<u32x2*>(p));
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4)
+            __builtin_nontemporal_store(u32x4{f2_to_bf2(x.v[s]), f2_to_bf2(x.v[s + 1]), f2_to_bf2(x.v[s + 2]),
+                                              f2_to_bf2(x.v[s + 3])},
+                                        reinterpret_cast<u32x4*>(p + s));
+    }
 }
 
 template <int SL>

@@ -116,6 +116,9 @@ struct FusedArgs {
     float2* segA;
     float2* segD;
     int* segP;
+    // D, b, c and dD, db, dc hold bf16 (re, im) pairs, 4 bytes per entry
+    // (the pointers above are then reinterpreted); everything else is fp32.
+    int bf16;
     // Backward only, optional: the scaled states z = D_t .* h_{t-1}
     // [B,L,H,N] that the straight-through gradients need (Sec. 3.1 Prop. 2).
     float2* z;

@@ -9,6 +9,8 @@ Tensor layouts (all contiguous, on one GPU):
   idx [B,L,H] int32, pi [H,K,N] int32, D/b/c [B,L,H,N] complex64,
   h0/h_final/dh_final/dh0 [B,H,N] complex64, y/dy [B,L,H] float32,
   saved [B,H,C,N] complex64 (C = num_chunks).
+With bf16 I/O (FLAG_BF16_IO), D, b, c and dD, db, dc are bfloat16 tensors
+  [B,L,H,N,2] holding (re, im) (torch.view_as_real(x).to(torch.bfloat16)).
 Straight-through surrogate gradients (Sec. 3.1 Prop. 2): q [B,L,H,K] float32,
   z [B,L,H,N] complex64, G [H,K,N,N] float32, routing logits [B,L,H,K] and
   dense dictionary M [H,K,N,N] float32.
@@ -24,6 +26,7 @@ _lib = None
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INDEX = 0, -1, -2, -3, -4, -5
 OP_FWD, OP_BWD, OP_COMPOSE, OP_STE_GRADS = 1, 2, 3, 4
 FLAG_PREPARED = 1
+FLAG_BF16_IO = 2
 
 
 class PdssmError(RuntimeError):
@@ -144,13 +147,21 @@ def dims_of(idx, pi):
     return B, L, H, N, K
 
 
+def is_bf16_io(D):
+    """D given as bf16 (re, im) pairs [..., N, 2] rather than complex64."""
+    return isinstance(D, torch.Tensor) and D.dtype == torch.bfloat16
+
+
 def _check_inputs(idx, pi, D, b, c):
     B, L, H, N, K = dims_of(idx, pi)
     dev = idx.device
     _need(idx, "idx", torch.int32, (B, L, H), dev)
     _need(pi, "pi", torch.int32, (H, K, N), dev)
     for t, n in ((D, "D"), (b, "b"), (c, "c")):
-        _need(t, n, torch.complex64, (B, L, H, N), dev)
+        if is_bf16_io(D):
+            _need(t, n, torch.bfloat16, (B, L, H, N, 2), dev)
+        else:
+            _need(t, n, torch.complex64, (B, L, H, N), dev)
     return B, L, H, N, K, dev
 
 
@@ -162,10 +173,13 @@ class Scan:
     prepare(pi) the scans reuse the tables in the workspace; call prepare()
     again whenever the contents of pi change."""
 
-    def __init__(self, B, L, H, N, K, chunk=0, device="cuda", ste=False):
+    def __init__(self, B, L, H, N, K, chunk=0, device="cuda", ste=False, bf16=False):
         self.d = desc(B, L, H, N, K, chunk)
         self.dp = desc(B, L, H, N, K, chunk)
-        self.dp.flags = FLAG_PREPARED
+        self.bf16 = bf16
+        if bf16:
+            self.d.flags = FLAG_BF16_IO
+        self.dp.flags = FLAG_PREPARED | self.d.flags
         self.prepared = False
         self.dims = (B, L, H, N, K)
         self.device = torch.device(device)
@@ -181,7 +195,10 @@ class Scan:
         self.y = torch.empty((B, L, H), dtype=torch.float32, device=dev)
         self.h_final = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
         self.saved = torch.empty((B, H, self.C, N), dtype=torch.complex64, device=dev)
-        self.dD = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
+        if bf16:
+            self.dD = torch.empty((B, L, H, N, 2), dtype=torch.bfloat16, device=dev)
+        else:
+            self.dD = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
         self.db = torch.empty_like(self.dD)
         self.dc = torch.empty_like(self.dD)
         self.dh0 = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
@@ -255,16 +272,17 @@ def scan_fwd(idx, pi, D, b, c, h0=None, chunk=0, stream=None):
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
     if h0 is not None:
         _need(h0, "h0", torch.complex64, (B, H, N), dev)
-    s = Scan(B, L, H, N, K, chunk, dev)
+    s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D))
     s.fwd(idx, pi, D, b, c, h0, stream)
     s.check_status()
     return s.y, s.h_final, s.saved
 
 
 def scan_bwd(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
-    """Returns (dD, db, dc [B,L,H,N] c64, dh0 [B,H,N] c64)."""
+    """Returns (dD, db, dc [B,L,H,N] c64, or [B,L,H,N,2] bf16 for bf16 inputs;
+    dh0 [B,H,N] c64)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
-    s = Scan(B, L, H, N, K, chunk, dev)
+    s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D))
     _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
     _need(dy, "dy", torch.float32, (B, L, H), dev)
     if dh_final is not None:

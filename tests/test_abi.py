@@ -80,12 +80,43 @@ def test_bad_descriptors(lib, kw, code):
         pdssm.workspace_size(d, pdssm.OP_FWD)
 
 
-def test_flags_only_prepared(lib):
+def test_flags_known_bits_only(lib):
     d = pdssm.desc(2, 10, 2, 64, 4)
-    d.flags = pdssm.FLAG_PREPARED
-    assert pdssm.num_chunks(d) == 2
-    d.flags = 2
-    assert pdssm.num_chunks(d) == pdssm.ERR_INVALID_ARG
+    for ok in (pdssm.FLAG_PREPARED, pdssm.FLAG_BF16_IO, pdssm.FLAG_PREPARED | pdssm.FLAG_BF16_IO):
+        d.flags = ok
+        assert pdssm.num_chunks(d) == 2
+    for bad in (4, 8, 1 << 31):
+        d.flags = bad
+        assert pdssm.num_chunks(d) == pdssm.ERR_INVALID_ARG
+
+
+def test_bf16_io_only_where_supported(lib):
+    f = FakeBufs()
+    P = lambda n: f(n)  # noqa: E731
+    # composition, decode and the straight-through calls take complex64 only
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    d.flags = pdssm.FLAG_BF16_IO
+    st = 2 * 40 * 2 * 64 * 8
+    assert lib.pdssm_compose_chunks(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), None,
+                                    None) == pdssm.ERR_UNSUPPORTED
+    assert lib.pdssm_decode_step(ctypes.byref(d), P(64), P(2048), P(st), P(st), P(st), None, P(st), P(64),
+                                 None, None) == pdssm.ERR_UNSUPPORTED
+    assert lib.pdssm_ste_grads(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), P(st), P(1 << 20),
+                               1 << 20, None, None) == pdssm.ERR_UNSUPPORTED
+    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
+    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+    args = [P(640), P(2048), P(st), P(st), P(st), P(2 * 2 * 5 * 64 * 8), P(640), None]
+    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, P(st), P(st), P(st), None, P(st), ws, need, None,
+                                  None) == pdssm.ERR_UNSUPPORTED
+    # the multi-pass kernels (dictionary tables beyond LDS) do not read bf16 pairs
+    big = pdssm.desc(1, 40, 1, 128, 128)
+    assert lib.pdssm_uses_fused(ctypes.byref(big)) == 0
+    big.flags = pdssm.FLAG_BF16_IO
+    need = lib.pdssm_workspace_size(ctypes.byref(big), pdssm.OP_FWD)
+    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+    st = 40 * 128 * 8
+    assert lib.pdssm_scan_fwd(ctypes.byref(big), P(160), P(128 * 128 * 4), P(st), P(st), P(st), None, P(160),
+                              None, None, ws, need, None, None) == pdssm.ERR_UNSUPPORTED
 
 
 def test_prepare_host_checks(lib):
