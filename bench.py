@@ -48,17 +48,19 @@ FLUSH_BYTES = 512 << 20
 METRIC = "PD-scan state-updates/s (B*L*H*N) fwd and fwd+bwd; achieved HBM GB/s vs peak"
 
 
-def alg_bytes(w, C, op):
-    """Algorithmic HBM bytes of one call: inputs read once, outputs written once."""
+def alg_bytes(w, C, op, esz=8):
+    """Algorithmic HBM bytes of one call: inputs read once, outputs written
+    once.  esz = bytes per complex entry of D, b, c, dD, db, dc (8 for
+    complex64, 4 for bf16 pairs); states, y and dy are fp32 always."""
     B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
     steps = B * L * H
     su = steps * N
     dict_b = H * K * N * 4
     if op == "fwd":
         # idx, D, b, c in; y, h_final, saved out
-        return steps * 4 + 3 * su * 8 + dict_b + steps * 4 + B * H * N * 8 + B * H * C * N * 8
+        return steps * 4 + 3 * su * esz + dict_b + steps * 4 + B * H * N * 8 + B * H * C * N * 8
     # idx, dy, D, b, c, saved in; dD, db, dc, dh0 out
-    return steps * 8 + 3 * su * 8 + dict_b + B * H * C * N * 8 + 3 * su * 8 + B * H * N * 8
+    return steps * 8 + 3 * su * esz + dict_b + B * H * C * N * 8 + 3 * su * esz + B * H * N * 8
 
 
 def ste_bytes(w, C):
@@ -192,6 +194,8 @@ def main():
                     help="time the straight-through step (scores, dictionary gradient, softmax products)")
     ap.add_argument("--temp", type=float, default=1.0, help="softmax temperature of --ste")
     ap.add_argument("--decode", action="store_true", help="time single-step decode instead")
+    ap.add_argument("--bf16", action="store_true",
+                    help="bf16 (re, im) pairs for D, b, c and the gradients (fp32 arithmetic)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling aid: time a plain 1 GiB device copy instead")
     args = ap.parse_args()
@@ -231,7 +235,12 @@ def main():
           flush=True)
     inp = workload_inputs(args.workload, seed=0)
     T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
-    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste)
+    if args.bf16:
+        if args.ste:
+            sys.exit("bench.py: --bf16 and --ste do not combine (the straight-through path is complex64)")
+        for k in ("D", "b", "c"):
+            T[k] = torch.view_as_real(T[k]).to(torch.bfloat16).contiguous()
+    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste, bf16=args.bf16)
     if args.ste:
         from paper_2605_19150_amd.inputs import selection_inputs
         logits, M = selection_inputs(inp["idx"], inp["pi"], seed=0)
@@ -288,14 +297,15 @@ def main():
     s.check_status()
 
     su = w.state_updates
-    fwd_b, bwd_b = alg_bytes(w, s.C, "fwd"), alg_bytes(w, s.C, "bwd")
+    esz = 4 if args.bf16 else 8
+    fwd_b, bwd_b = alg_bytes(w, s.C, "fwd", esz), alg_bytes(w, s.C, "bwd", esz)
     fused = s.fused
     kern = {"fwd": "k_fwd_fused" if fused else "k_fwd_*(chunked)",
             "bwd": "k_bwd_fused" if fused else "k_bwd_*(chunked)"}
     dom = "bwd" if (bwd_ms >= fwd_ms and args.only != "fwd") else "fwd"
     dom_ms, dom_b = (bwd_ms, bwd_b) if dom == "bwd" else (fwd_ms, fwd_b)
     achieved = dom_b / (dom_ms * 1e-3) / 1e9
-    traffic = traffic_from_profiles(kern[dom], w.name) if fused else None
+    traffic = traffic_from_profiles(kern[dom] + ("_bf16" if args.bf16 else ""), w.name) if fused else None
     out = {
         "metric": METRIC,
         "value": su / (ms_step * 1e-3),
@@ -307,7 +317,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16-io/f32" if args.bf16 else "f32",
         "data": "synthetic (seeded, shapes and distributions of the named workload)",
         "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
                    "chunk": s.chunk,
@@ -351,7 +361,7 @@ def main():
             "softmax_vjp": {"ms": sm_ms, "alg_bytes": sb["softmax"],
                             "alg_GBps": sb["softmax"] / (sm_ms * 1e-3) / 1e9},
         }
-    if not args.no_cpu_baseline and args.only == "both" and not args.ste:
+    if not args.no_cpu_baseline and args.only == "both" and not args.ste and not args.bf16:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(out), flush=True)
