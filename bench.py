@@ -180,6 +180,66 @@ def decode_bench(args, w, dev):
     }), flush=True)
 
 
+def front_bench(args, w, dev):
+    """Selection front end for the workload's layer: the maps of a dense
+    dictionary [H,K,N,N] (pdssm_dict_argmax) and the routing of every token
+    with d_model = H*N (pdssm_route: bf16 product on the matrix cores, fp32
+    logits written, argmax fused)."""
+    import torch
+    from paper_2605_19150_amd import pdssm
+
+    Dm, T = w.H * w.N, w.B * w.L
+    g = torch.Generator(device="cpu").manual_seed(0)
+    u = torch.randn((w.B, w.L, Dm), generator=g).to(torch.bfloat16).to(dev)
+    S = (torch.randn((w.H, w.K, Dm), generator=g) / Dm ** 0.5).to(torch.bfloat16).to(dev)
+    M = torch.randn((w.H, w.K, w.N, w.N), generator=g).to(dev)
+    lg = torch.empty((w.B, w.L, w.H, w.K), dtype=torch.float32, device=dev)
+    idx = torch.empty((w.B, w.L, w.H), dtype=torch.int32, device=dev)
+    pi = torch.empty((w.H, w.K, w.N), dtype=torch.int32, device=dev)
+    L = pdssm.load()
+    st = pdssm._stream(None)
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        assert L.pdssm_dict_argmax(w.H, w.K, w.N, pdssm._p(M), pdssm._p(pi), st) == pdssm.OK
+        if ev is not None:
+            ev[1].record()
+        assert L.pdssm_route(T, Dm, w.H, w.K, pdssm._p(u), pdssm._p(S), pdssm._p(lg), pdssm._p(idx), st) == pdssm.OK
+        if ev is not None:
+            ev[2].record()
+
+    for _ in range(args.warmup):
+        flush.fill_(1.0)
+        step()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        flush.fill_(float(i))
+        step(evs[i])
+    torch.cuda.synchronize()
+    am_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    rt_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    rt_bytes = T * Dm * 2 + w.H * w.K * Dm * 2 + T * w.H * w.K * 4 + T * w.H * 4
+    rt_flops = 2.0 * T * w.H * w.K * Dm
+    am_bytes = w.H * w.K * w.N * w.N * 4 + w.H * w.K * w.N * 4
+    print(json.dumps({
+        "metric": "PD-SSM routing tokens/s (routing product + argmax over the K maps of every head)",
+        "value": T / (rt_ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": am_ms + rt_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16 operands, f32 accumulation", "data": "synthetic (seeded)",
+        "config": {"workload": w.name + " front end", "tokens": T, "d_model": Dm, "H": w.H, "K": w.K, "N": w.N,
+                   "step": "dict_argmax+route", "parallelism": "single-gpu"},
+        "route": {"kernel": "k_route", "ms": rt_ms, "alg_bytes": rt_bytes, "alg_GBps": rt_bytes / (rt_ms * 1e-3) / 1e9,
+                  "flops": rt_flops, "TFLOPs": rt_flops / (rt_ms * 1e-3) / 1e12,
+                  "frac_mfma_bf16": rt_flops / (rt_ms * 1e-3) / 1e12 / 2500.0},
+        "dict_argmax": {"kernel": "k_dict_argmax", "ms": am_ms, "alg_bytes": am_bytes,
+                        "alg_GBps": am_bytes / (am_ms * 1e-3) / 1e9},
+        "device": torch.cuda.get_device_name(dev),
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -194,6 +254,8 @@ def main():
                     help="time the straight-through step (scores, dictionary gradient, softmax products)")
     ap.add_argument("--temp", type=float, default=1.0, help="softmax temperature of --ste")
     ap.add_argument("--decode", action="store_true", help="time single-step decode instead")
+    ap.add_argument("--front", action="store_true",
+                    help="time the selection front end (dictionary argmax, routing product + argmax) instead")
     ap.add_argument("--bf16", action="store_true",
                     help="bf16 (re, im) pairs for D, b, c and the gradients (fp32 arithmetic)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -230,6 +292,9 @@ def main():
     w = WORKLOADS[args.workload]
     if args.decode:
         decode_bench(args, w, dev)
+        return
+    if args.front:
+        front_bench(args, w, dev)
         return
     print("bench: workload %d (%s): generating inputs" % (args.workload, w.name), file=sys.stderr,
           flush=True)

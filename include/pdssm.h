@@ -238,6 +238,28 @@ int pdssm_ste_grads(const pdssm_desc* desc, const int32_t* idx, const int32_t* p
                     size_t ws_bytes, int* dev_status, void* stream);
 
 /*
+ * Selection front end (Sec. 3.1 eqs. (5)-(8), App. E.2.1).  Ties go to the
+ * first maximal index.
+ *
+ * pdssm_dict_argmax: the maps of every dense dictionary matrix,
+ *   pi[h,k,j] = argmax_i M[h,k,i,j] (the column argmax; once per step of the
+ *   optimizer).  M [H,K,N,N] float32 (row i, column j), pi [H,K,N] int32.
+ *   N in {8,...,256}, K <= 256.  Needs no workspace.
+ *
+ * pdssm_route: the routing scores and choices of every token,
+ *   logits[t,h,k] = sum_d u[t,d] * S[h,k,d],  idx[t,h] = argmax_k logits[t,h,k],
+ *   t = 0..T-1 (T = B*L; [T,H,K] is [B,L,H,K], [T,H] is [B,L,H]).
+ *   u [T,Dm] and S [H,K,Dm] bf16 (row-major, 16-byte aligned, Dm a
+ *   multiple of 8), logits [T,H,K] float32 (optional: the straight-through
+ *   backward needs them, inference does not), idx [T,H] int32 (required).
+ *   The product runs on the matrix cores with fp32 accumulation and the
+ *   argmax is taken on the fp32 logits.  Needs no workspace.
+ */
+int pdssm_dict_argmax(int32_t H, int32_t K, int32_t N, const float* M, int32_t* pi, void* stream);
+int pdssm_route(int32_t T, int32_t Dm, int32_t H, int32_t K, const uint16_t* u, const uint16_t* S,
+                float* logits, int32_t* idx, void* stream);
+
+/*
  * Vector-Jacobian product of the tempered softmax that stands in for a hard
  * argmax in the backward pass (Sec. 3.1, slope-annealed straight-through
  * estimation; Prop. 2): along the middle axis of x [outer, len, inner]

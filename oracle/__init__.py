@@ -19,6 +19,8 @@ from .oracle import (  # noqa: F401
     oracle_ste,
     oracle_softmax_vjp,
     oracle_surrogate_grads,
+    oracle_dict_argmax,
+    oracle_route,
     oracle_num_chunks,
     oracle_lib_path,
 )

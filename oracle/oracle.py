@@ -172,3 +172,20 @@ def oracle_surrogate_grads(q, G, logits, M, temp):
     dM [H,K,N,N] (dense dictionary, softmax over the rows i of every
     column j, the argmax that gives pi[h,k,j])."""
     return oracle_softmax_vjp(logits, q, -1, temp), oracle_softmax_vjp(M, G, 2, temp)
+
+
+def oracle_dict_argmax(M):
+    """Maps of the dense dictionary (Sec. 3.1 eq. (5), App. E.2.1):
+    pi[h,k,j] = argmax_i M[h,k,i,j], ties to the first maximal index."""
+    M = np.asarray(M, np.float64)
+    return np.argmax(M, axis=2).astype(np.int32)
+
+
+def oracle_route(u, S):
+    """Routing scores and choices (Sec. 3.1 eqs. (6)-(7)): u [B,L,Dm],
+    S [H,K,Dm] (their exact values, e.g. widened bf16) -> logits [B,L,H,K]
+    float64 = sum_d u[b,t,d] S[h,k,d], idx [B,L,H] = first argmax over k."""
+    u = np.asarray(u, np.float64)
+    S = np.asarray(S, np.float64)
+    logits = np.einsum("bld,hkd->blhk", u, S)
+    return logits, np.argmax(logits, axis=3).astype(np.int32)

@@ -17,6 +17,7 @@ SOURCES = [("pdssm_fused.hip", ["-DPDSSM_N=%d" % n], "pdssm_fused_n%d" % n)
     ("pdssm_chunked.hip", [], "pdssm_chunked"),
     ("pdssm_ste.hip", [], "pdssm_ste"),
     ("pdssm_decode.hip", [], "pdssm_decode"),
+    ("pdssm_select.hip", [], "pdssm_select"),
     ("pdssm_api.cpp", [], "pdssm_api"),
 ]
 

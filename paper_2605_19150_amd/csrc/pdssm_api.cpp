@@ -7,6 +7,7 @@
 #include <initializer_list>
 
 #include "pdssm_decode.h"
+#include "pdssm_select.h"
 #include "pdssm_fused.h"
 #include "pdssm_internal.h"
 
@@ -525,6 +526,44 @@ int pdssm_decode_step(const pdssm_desc* d, const int32_t* idx, const int32_t* pi
     a.y = y;
     a.status = dev_status;
     return pdssm::launch_decode(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
+int pdssm_dict_argmax(int32_t H, int32_t K, int32_t N, const float* M, int32_t* pi, void* stream) {
+    if (H < 1 || K < 1 || !n_supported(N) || K > 256) return H < 1 || K < 1 ? PDSSM_ERR_INVALID_ARG : PDSSM_ERR_UNSUPPORTED;
+    if ((long long)H * K * N * N >= (1LL << 31)) return PDSSM_ERR_UNSUPPORTED;
+    if (!M || !pi || (reinterpret_cast<uintptr_t>(M) & 3) || (reinterpret_cast<uintptr_t>(pi) & 3))
+        return PDSSM_ERR_INVALID_ARG;
+    const size_t nM = (size_t)H * K * N * N * 4, npi = (size_t)H * K * N * 4;
+    if (any_overlap({{pi, npi}}, {{M, nM}})) return PDSSM_ERR_INVALID_ARG;
+    return pdssm::launch_dict_argmax(M, pi, H * K, N, static_cast<hipStream_t>(stream)) == hipSuccess
+               ? PDSSM_OK
+               : PDSSM_ERR_HIP;
+}
+
+int pdssm_route(int32_t T, int32_t Dm, int32_t H, int32_t K, const uint16_t* u, const uint16_t* S,
+                float* logits, int32_t* idx, void* stream) {
+    if (T < 1 || Dm < 1 || H < 1 || K < 1) return PDSSM_ERR_INVALID_ARG;
+    if (K > 256 || Dm % 8 != 0) return PDSSM_ERR_UNSUPPORTED;
+    if ((H + 256 / K - 1) / (256 / K) > 65535) return PDSSM_ERR_UNSUPPORTED;  // head groups (grid y)
+    if ((long long)T * Dm >= (1LL << 31) || (long long)T * H * K >= (1LL << 31) ||
+        (long long)H * K * Dm >= (1LL << 31))
+        return PDSSM_ERR_UNSUPPORTED;
+    if (!u || !S || !idx || misaligned(u) || misaligned(S) || (reinterpret_cast<uintptr_t>(logits) & 3) ||
+        (reinterpret_cast<uintptr_t>(idx) & 3))
+        return PDSSM_ERR_INVALID_ARG;
+    const size_t nu = (size_t)T * Dm * 2, nS = (size_t)H * K * Dm * 2;
+    if (any_overlap({{logits, (size_t)T * H * K * 4}, {idx, (size_t)T * H * 4}}, {{u, nu}, {S, nS}}))
+        return PDSSM_ERR_INVALID_ARG;
+    pdssm::RouteArgs a = {};
+    a.T = T;
+    a.Dm = Dm;
+    a.H = H;
+    a.K = K;
+    a.u = u;
+    a.S = S;
+    a.logits = logits;
+    a.idx = idx;
+    return pdssm::launch_route(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
 int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int32_t len, int64_t inner,

@@ -44,7 +44,7 @@ class Desc(ctypes.Structure):
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
            "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
            "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_ste_grads",
-           "pdssm_softmax_vjp", "pdssm_decode_step")
+           "pdssm_softmax_vjp", "pdssm_decode_step", "pdssm_dict_argmax", "pdssm_route")
 
 
 def lib_path():
@@ -84,6 +84,11 @@ def load():
     L.pdssm_softmax_vjp.restype = I
     L.pdssm_decode_step.argtypes = [D] + [P] * 10
     L.pdssm_decode_step.restype = I
+    I32 = ctypes.c_int32
+    L.pdssm_dict_argmax.argtypes = [I32, I32, I32, P, P, P]
+    L.pdssm_dict_argmax.restype = I
+    L.pdssm_route.argtypes = [I32, I32, I32, I32, P, P, P, P, P]
+    L.pdssm_route.restype = I
     if L.pdssm_abi_version() != 1:
         raise ImportError("libpdssm.so ABI version mismatch")
     _lib = L
@@ -414,3 +419,34 @@ def decode_step(idx, pi, D, b, c, h=None, out=None, y=None, stream=None, check=T
         if int(status.item()) != OK:
             raise PdssmError(int(status.item()), "kernel index check")
     return out, y
+
+
+def dict_argmax(M, stream=None):
+    """pi [H,K,N] int32 = first argmax over the rows i of every column j of
+    the dense dictionary M [H,K,N,N] float32."""
+    H, K, N, N2 = M.shape
+    if N2 != N:
+        raise ValueError("M must be [H,K,N,N]")
+    _need(M, "M", torch.float32, (H, K, N, N), M.device)
+    pi = torch.empty((H, K, N), dtype=torch.int32, device=M.device)
+    st = load().pdssm_dict_argmax(H, K, N, _p(M), _p(pi), _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_dict_argmax")
+    return pi
+
+
+def route(u, S, logits=True, stream=None):
+    """Routing scores and choices: u [B,L,Dm] bf16, S [H,K,Dm] bf16 ->
+    (logits [B,L,H,K] f32 or None, idx [B,L,H] int32)."""
+    B, L, Dm = u.shape
+    H, K, Dm2 = S.shape
+    if Dm2 != Dm:
+        raise ValueError("u and S disagree on the contraction length")
+    _need(u, "u", torch.bfloat16, (B, L, Dm), u.device)
+    _need(S, "S", torch.bfloat16, (H, K, Dm), u.device)
+    lg = torch.empty((B, L, H, K), dtype=torch.float32, device=u.device) if logits else None
+    idx = torch.empty((B, L, H), dtype=torch.int32, device=u.device)
+    st = load().pdssm_route(B * L, Dm, H, K, _p(u), _p(S), _p(lg), _p(idx), _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_route")
+    return lg, idx

@@ -279,3 +279,19 @@ def test_decode_host_checks(lib):
     bad = pdssm.desc(2, 1, 3, 48, 4)
     assert lib.pdssm_decode_step(ctypes.byref(bad), idx, pi, D, b, c, None, h, y, None,
                                  None) == pdssm.ERR_UNSUPPORTED
+
+
+def test_select_host_checks(lib):
+    f = FakeBufs()
+    M, pi = f(4 * 5 * 64 * 64 * 4), f(4 * 5 * 64 * 4)
+    assert lib.pdssm_dict_argmax(4, 5, 48, M, pi, None) == pdssm.ERR_UNSUPPORTED
+    assert lib.pdssm_dict_argmax(0, 5, 64, M, pi, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_dict_argmax(4, 5, 64, None, pi, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_dict_argmax(4, 5, 64, M, M, None) == pdssm.ERR_INVALID_ARG     # pi over M
+    u, S, lg, idx = f(100 * 64 * 2), f(8 * 4 * 64 * 2), f(100 * 32 * 4), f(100 * 8 * 4)
+    assert lib.pdssm_route(100, 60, 8, 4, u, S, lg, idx, None) == pdssm.ERR_UNSUPPORTED   # Dm % 8
+    assert lib.pdssm_route(100, 64, 8, 257, u, S, lg, idx, None) == pdssm.ERR_UNSUPPORTED
+    assert lib.pdssm_route(0, 64, 8, 4, u, S, lg, idx, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_route(100, 64, 8, 4, u, S, lg, None, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_route(100, 64, 8, 4, u, S, u, idx, None) == pdssm.ERR_INVALID_ARG    # logits over u
+    assert lib.pdssm_route(100, 64, 8, 4, ctypes.c_void_p(u.value + 2), S, lg, idx, None) == pdssm.ERR_INVALID_ARG
