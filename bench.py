@@ -48,19 +48,21 @@ FLUSH_BYTES = 512 << 20
 METRIC = "PD-scan state-updates/s (B*L*H*N) fwd and fwd+bwd; achieved HBM GB/s vs peak"
 
 
-def alg_bytes(w, C, op, esz=8):
+def alg_bytes(w, C, op, esz=8, ssz=8):
     """Algorithmic HBM bytes of one call: inputs read once, outputs written
-    once.  esz = bytes per complex entry of D, b, c, dD, db, dc (8 for
-    complex64, 4 for bf16 pairs); states, y and dy are fp32 always."""
+    once.  esz = bytes per entry of D, b, c, dD, db, dc (8 for complex64, 4
+    for bf16 pairs or the real model); ssz = bytes per state entry of h_final,
+    saved and dh0 (8, or 4 for the real model, whose states are real although
+    the library keeps them as complex64); y and dy are fp32 always."""
     B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
     steps = B * L * H
     su = steps * N
     dict_b = H * K * N * 4
     if op == "fwd":
         # idx, D, b, c in; y, h_final, saved out
-        return steps * 4 + 3 * su * esz + dict_b + steps * 4 + B * H * N * 8 + B * H * C * N * 8
+        return steps * 4 + 3 * su * esz + dict_b + steps * 4 + B * H * N * ssz + B * H * C * N * ssz
     # idx, dy, D, b, c, saved in; dD, db, dc, dh0 out
-    return steps * 8 + 3 * su * esz + dict_b + B * H * C * N * 8 + 3 * su * esz + B * H * N * 8
+    return steps * 8 + 3 * su * esz + dict_b + B * H * C * N * ssz + 3 * su * esz + B * H * N * ssz
 
 
 def ste_bytes(w, C):
@@ -258,6 +260,8 @@ def main():
                     help="time the selection front end (dictionary argmax, routing product + argmax) instead")
     ap.add_argument("--bf16", action="store_true",
                     help="bf16 (re, im) pairs for D, b, c and the gradients (fp32 arithmetic)")
+    ap.add_argument("--real", action="store_true",
+                    help="the real-valued model: real fp32 D, b, c and gradients")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling aid: time a plain 1 GiB device copy instead")
     args = ap.parse_args()
@@ -298,14 +302,16 @@ def main():
         return
     print("bench: workload %d (%s): generating inputs" % (args.workload, w.name), file=sys.stderr,
           flush=True)
-    inp = workload_inputs(args.workload, seed=0)
+    if args.real and (args.ste or args.bf16):
+        sys.exit("bench.py: --real combines with neither --ste nor --bf16")
+    inp = workload_inputs(args.workload, seed=0, real=args.real)
     T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
     if args.bf16:
         if args.ste:
             sys.exit("bench.py: --bf16 and --ste do not combine (the straight-through path is complex64)")
         for k in ("D", "b", "c"):
             T[k] = torch.view_as_real(T[k]).to(torch.bfloat16).contiguous()
-    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste, bf16=args.bf16)
+    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste, bf16=args.bf16, real=args.real)
     if args.ste:
         from paper_2605_19150_amd.inputs import selection_inputs
         logits, M = selection_inputs(inp["idx"], inp["pi"], seed=0)
@@ -362,15 +368,17 @@ def main():
     s.check_status()
 
     su = w.state_updates
-    esz = 4 if args.bf16 else 8
-    fwd_b, bwd_b = alg_bytes(w, s.C, "fwd", esz), alg_bytes(w, s.C, "bwd", esz)
+    esz = 4 if (args.bf16 or args.real) else 8
+    ssz = 4 if args.real else 8
+    fwd_b, bwd_b = alg_bytes(w, s.C, "fwd", esz, ssz), alg_bytes(w, s.C, "bwd", esz, ssz)
     fused = s.fused
     kern = {"fwd": "k_fwd_fused" if fused else "k_fwd_*(chunked)",
             "bwd": "k_bwd_fused" if fused else "k_bwd_*(chunked)"}
     dom = "bwd" if (bwd_ms >= fwd_ms and args.only != "fwd") else "fwd"
     dom_ms, dom_b = (bwd_ms, bwd_b) if dom == "bwd" else (fwd_ms, fwd_b)
     achieved = dom_b / (dom_ms * 1e-3) / 1e9
-    traffic = traffic_from_profiles(kern[dom] + ("_bf16" if args.bf16 else ""), w.name) if fused else None
+    suffix = "_bf16" if args.bf16 else ("_real" if args.real else "")
+    traffic = traffic_from_profiles(kern[dom] + suffix, w.name) if fused else None
     out = {
         "metric": METRIC,
         "value": su / (ms_step * 1e-3),
@@ -382,9 +390,9 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16-io/f32" if args.bf16 else "f32",
+        "dtype": "bf16-io/f32" if args.bf16 else ("f32-real" if args.real else "f32"),
         "data": "synthetic (seeded, shapes and distributions of the named workload)",
-        "config": {"workload": w.name, "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
+        "config": {"workload": w.name + (" (real-valued model)" if args.real else ""), "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
                    "chunk": s.chunk,
                    "step": ("prepare+fwd+bwd_ste+ste_grads+softmax_vjp" if args.ste else "prepare+fwd+bwd")
                    if args.only == "both" else args.only,
@@ -426,7 +434,7 @@ def main():
             "softmax_vjp": {"ms": sm_ms, "alg_bytes": sb["softmax"],
                             "alg_GBps": sb["softmax"] / (sm_ms * 1e-3) / 1e9},
         }
-    if not args.no_cpu_baseline and args.only == "both" and not args.ste and not args.bf16:
+    if not args.no_cpu_baseline and args.only == "both" and not args.ste and not args.bf16 and not args.real:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, inp)
     print(json.dumps(out), flush=True)

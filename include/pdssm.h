@@ -78,7 +78,7 @@ typedef struct pdssm_c64 {
 typedef struct pdssm_desc {
     int32_t B, L, H, N, K; /* batch, steps, heads, state size, dictionary size */
     int32_t chunk;         /* steps per chunk; 0 = default; fwd and bwd must agree */
-    uint32_t flags;        /* 0 or PDSSM_FLAG_PREPARED | PDSSM_FLAG_BF16_IO */
+    uint32_t flags;        /* 0 or PDSSM_FLAG_PREPARED | (PDSSM_FLAG_BF16_IO or PDSSM_FLAG_REAL_IO) */
 } pdssm_desc;
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd: the dictionary tables in
@@ -98,6 +98,21 @@ typedef struct pdssm_desc {
  * (pdssm_uses_fused(desc) == 1); other entry points and the multi-pass
  * kernels return PDSSM_ERR_UNSUPPORTED, as does pdssm_scan_bwd_ste. */
 #define PDSSM_FLAG_BF16_IO 2u
+
+/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd (and pdssm_prepare,
+ * which ignores it): the real-valued model (App. B, the MAD and time-series
+ * setups use it): D, b, c and dD, db, dc are real fp32 [B,L,H,N], 4 bytes per
+ * entry, the recurrence h_t = P_t (D_t .* h_{t-1}) + b_t over the reals and
+ * y_t = sum_n c_t[n] h_t[n].  Every other tensor keeps its type: h0, h_final,
+ * saved, dh_final and dh0 stay complex64; for the real model h0 and dh_final
+ * hold real values (imaginary parts 0, or NULL) and h_final, dh0 then come
+ * out with imaginary parts 0.  The arithmetic is the complex64 one on rows
+ * whose imaginary parts are 0, so every result equals, bit for bit, the real
+ * part of a complex64 call on the same values.  Cannot
+ * be combined with PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG); the same
+ * entry points as PDSSM_FLAG_BF16_IO support it, the others return
+ * PDSSM_ERR_UNSUPPORTED. */
+#define PDSSM_FLAG_REAL_IO 4u
 
 typedef enum pdssm_status {
     PDSSM_OK = 0,

@@ -36,7 +36,10 @@ bool scan_chunk_ok(int N, int tau) {
 // Dimension checks shared by every op.  Returns PDSSM_OK or a status.
 int check_dims(const pdssm_desc* d) {
     if (!d) return PDSSM_ERR_INVALID_ARG;
-    if ((d->flags & ~(PDSSM_FLAG_PREPARED | PDSSM_FLAG_BF16_IO)) != 0) return PDSSM_ERR_INVALID_ARG;
+    if ((d->flags & ~(PDSSM_FLAG_PREPARED | PDSSM_FLAG_BF16_IO | PDSSM_FLAG_REAL_IO)) != 0)
+        return PDSSM_ERR_INVALID_ARG;
+    // one row format at a time
+    if ((d->flags & PDSSM_FLAG_BF16_IO) && (d->flags & PDSSM_FLAG_REAL_IO)) return PDSSM_ERR_INVALID_ARG;
     if (d->B < 1 || d->L < 1 || d->H < 1 || d->N < 1 || d->K < 1 || d->chunk < 0)
         return PDSSM_ERR_INVALID_ARG;
     if (!n_supported(d->N) || d->K > 256) return PDSSM_ERR_UNSUPPORTED;
@@ -266,10 +269,18 @@ ScanArgs base_args(const pdssm_desc* d, int tau) {
 
 bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) % 16) != 0; }
 
-bool bf16_io(const pdssm_desc* d) { return (d->flags & PDSSM_FLAG_BF16_IO) != 0; }
+// Row format of D, b, c (and dD, db, dc) selected by the flags.
+int io_format(const pdssm_desc* d) {
+    if (d->flags & PDSSM_FLAG_REAL_IO) return pdssm::kIoReal;
+    if (d->flags & PDSSM_FLAG_BF16_IO) return pdssm::kIoBf16;
+    return pdssm::kIoC64;
+}
 
-// Bytes per complex entry of D, b, c (and dD, db, dc): bf16 pairs or complex64.
-size_t io_bytes(const pdssm_desc* d) { return bf16_io(d) ? 4 : 8; }
+// A 4-byte row format (bf16 pairs or real fp32): single-read kernels only.
+bool narrow_io(const pdssm_desc* d) { return io_format(d) != pdssm::kIoC64; }
+
+// Bytes per entry of D, b, c (and dD, db, dc).
+size_t io_bytes(const pdssm_desc* d) { return narrow_io(d) ? 4 : 8; }
 
 }  // namespace
 
@@ -352,7 +363,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     const size_t need = ws_bytes_for(s, d, a.C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
-    if (bf16_io(d) && !use_fused(d)) return PDSSM_ERR_UNSUPPORTED;
+    if (narrow_io(d) && !use_fused(d)) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
     if (any_overlap({{y, s.idxN * 4}, {h_final, s.seqN * 8}, {saved, s.perChunk * 8}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {h0, s.seqN * 8}}))
@@ -371,7 +382,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     if (use_fused(d)) {
         pdssm::FusedArgs f = fused_base(a);
         f.saved = reinterpret_cast<float2*>(saved);
-        f.bf16 = bf16_io(d);
+        f.io = io_format(d);
         e = prep_fused(f, d, pi, ws, s, dev_status, st, true);
         if (e == hipSuccess) e = pdssm::launch_fwd_fused(f, st);
     } else {
@@ -402,8 +413,8 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (misaligned(z)) return PDSSM_ERR_INVALID_ARG;
-    // bf16 pairs: single-read kernels only; the straight-through path reads db as complex64
-    if (bf16_io(d) && (!use_fused(d) || z)) return PDSSM_ERR_UNSUPPORTED;
+    // 4-byte formats: single-read kernels only; the straight-through path reads db as complex64
+    if (narrow_io(d) && (!use_fused(d) || z)) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
     if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, s.stepN * 8}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * 8},
@@ -428,7 +439,7 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
         pdssm::FusedArgs f = fused_base(a);
         f.saved = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
         f.z = reinterpret_cast<float2*>(z);
-        f.bf16 = bf16_io(d);
+        f.io = io_format(d);
         e = prep_fused(f, d, pi, ws, s, dev_status, st, false);
         if (e == hipSuccess) e = pdssm::launch_bwd_fused(f, st);
     } else {
@@ -465,7 +476,7 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
                     void* stream) {
     const int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (bf16_io(d)) return PDSSM_ERR_UNSUPPORTED;
+    if (narrow_io(d)) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !g || !z || (!q && !G) || (q && !pi)) return PDSSM_ERR_INVALID_ARG;
     if (misaligned(g) || misaligned(z) || misaligned(pi) || (reinterpret_cast<uintptr_t>(G) & 3) != 0 ||
         (reinterpret_cast<uintptr_t>(q) & 3) != 0)
@@ -500,7 +511,7 @@ int pdssm_decode_step(const pdssm_desc* d, const int32_t* idx, const int32_t* pi
                       int* dev_status, void* stream) {
     const int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (bf16_io(d)) return PDSSM_ERR_UNSUPPORTED;
+    if (narrow_io(d)) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !pi || !D || !b || !c || !h_out || !y) return PDSSM_ERR_INVALID_ARG;
     for (const void* p : {(const void*)pi, (const void*)D, (const void*)b, (const void*)c, (const void*)h_in,
                           (const void*)h_out})
@@ -588,7 +599,7 @@ int pdssm_compose_chunks(const pdssm_desc* d, const int32_t* idx, const int32_t*
                          int* dev_status, void* stream) {
     int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (bf16_io(d)) return PDSSM_ERR_UNSUPPORTED;
+    if (narrow_io(d)) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !pi || !D || !pi_out || !d_out) return PDSSM_ERR_INVALID_ARG;
     if (misaligned(D) || misaligned(pi) || misaligned(pi_out) || misaligned(d_out))
         return PDSSM_ERR_INVALID_ARG;

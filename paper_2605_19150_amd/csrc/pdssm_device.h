@@ -11,6 +11,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "pdssm_io.h"
+
 namespace pdssm {
 
 constexpr int kWave = 64;
@@ -171,46 +173,62 @@ __device__ __forceinline__ uint32_t f2_to_bf2(float2 v) {
     return f32_to_bf16_bits(v.x) | (f32_to_bf16_bits(v.y) << 16);
 }
 
-// ld_row for rows of bf16 pairs (4 bytes per entry).
-template <int SL, int AUX = 0>
-__device__ __forceinline__ CV<SL> ld_row_bf(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+// One 4-byte entry widened to a complex value, and back (the real format
+// keeps the real part only).
+template <int IO>
+__device__ __forceinline__ float2 word_to_f2(uint32_t w) {
+    static_assert(IO == kIoBf16 || IO == kIoReal, "4-byte formats only");
+    if constexpr (IO == kIoBf16) return bf2_to_f2(w);
+    else return make_float2(__uint_as_float(w), 0.f);
+}
+template <int IO>
+__device__ __forceinline__ uint32_t f2_to_word(float2 v) {
+    static_assert(IO == kIoBf16 || IO == kIoReal, "4-byte formats only");
+    if constexpr (IO == kIoBf16) return f2_to_bf2(v);
+    else return __float_as_uint(v.x);
+}
+
+// ld_row for rows of 4-byte entries (bf16 pairs or real fp32).
+template <int SL, int AUX, int IO>
+__device__ __forceinline__ CV<SL> ld_row_w(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     CV<SL> out;
     if constexpr (SL == 1) {
-        out.v[0] = bf2_to_f2(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
+        out.v[0] = word_to_f2<IO>(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
     } else if constexpr (SL == 2) {
         const uint2 q = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
-        out.v[0] = bf2_to_f2(q.x);
-        out.v[1] = bf2_to_f2(q.y);
+        out.v[0] = word_to_f2<IO>(q.x);
+        out.v[1] = word_to_f2<IO>(q.y);
     } else {
 #pragma unroll
         for (int s = 0; s < SL; s += 4) {
             const uint4 q =
                 __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff + 4 * s, AUX));
-            out.v[s] = bf2_to_f2(q.x);
-            out.v[s + 1] = bf2_to_f2(q.y);
-            out.v[s + 2] = bf2_to_f2(q.z);
-            out.v[s + 3] = bf2_to_f2(q.w);
+            out.v[s] = word_to_f2<IO>(q.x);
+            out.v[s + 1] = word_to_f2<IO>(q.y);
+            out.v[s + 2] = word_to_f2<IO>(q.z);
+            out.v[s + 3] = word_to_f2<IO>(q.w);
         }
     }
     return out;
 }
 
-// This lane's SL entries of a bf16-pair row (row + lane*SL), rounded, with the
+// This lane's SL entries of a row of 4-byte entries (row + lane*SL), with the
 // nontemporal hint (rows written once).
-template <int SL>
-__device__ __forceinline__ void st_row_bf_stream(uint32_t* __restrict__ row, int lane, const CV<SL>& x) {
+template <int SL, int IO>
+__device__ __forceinline__ void st_row_w_stream(uint32_t* __restrict__ row, int lane, const CV<SL>& x) {
     typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
     uint32_t* p = row + lane * SL;
     if constexpr (SL == 1) {
-        __builtin_nontemporal_store(f2_to_bf2(x.v[0]), p);
+        __builtin_nontemporal_store(f2_to_word<IO>(x.v[0]), p);
     } else if constexpr (SL == 2) {
-        __builtin_nontemporal_store(u32x2{f2_to_bf2(x.v[0]), f2_to_bf2(x.v[1])}, reinterpret_cast<u32x2*>(p));
+        __builtin_nontemporal_store(u32x2{f2_to_word<IO>(x.v[0]), f2_to_word<IO>(x.v[1])},
+                                    reinterpret_cast<u32x2*>(p));
     } else {
 #pragma unroll
         for (int s = 0; s < SL; s += 4)
-            __builtin_nontemporal_store(u32x4{f2_to_bf2(x.v[s]), f2_to_bf2(x.v[s + 1]), f2_to_bf2(x.v[s + 2]),
-                                              f2_to_bf2(x.v[s + 3])},
+            __builtin_nontemporal_store(u32x4{f2_to_word<IO>(x.v[s]), f2_to_word<IO>(x.v[s + 1]),
+                                              f2_to_word<IO>(x.v[s + 2]), f2_to_word<IO>(x.v[s + 3])},
                                         reinterpret_cast<u32x4*>(p + s));
     }
 }

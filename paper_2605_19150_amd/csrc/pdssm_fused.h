@@ -4,6 +4,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "pdssm_io.h"
+
 namespace pdssm {
 
 // Chunk-computing waves per workgroup of the fused kernels (one workgroup per
@@ -116,9 +118,10 @@ struct FusedArgs {
     float2* segA;
     float2* segD;
     int* segP;
-    // D, b, c and dD, db, dc hold bf16 (re, im) pairs, 4 bytes per entry
-    // (the pointers above are then reinterpreted); everything else is fp32.
-    int bf16;
+    // Format of D, b, c and dD, db, dc (kIoC64, kIoBf16 pairs or kIoReal
+    // fp32, 4 bytes per entry for the last two: the pointers above are then
+    // reinterpreted); everything else keeps its complex64 / fp32 type.
+    int io;
     // Backward only, optional: the scaled states z = D_t .* h_{t-1}
     // [B,L,H,N] that the straight-through gradients need (Sec. 3.1 Prop. 2).
     float2* z;

@@ -356,7 +356,7 @@ __device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, float2* 
 // steps, all through the null descriptor): the compiler can then count the
 // outstanding loads exactly and a wave waits only for the chunk it computes.
 // AUX: cache policy of the row loads (the forward streams them, kLoadStream).
-template <int N, int TAU, bool LOAD_B, bool LOAD_C, int AUX = 0, bool BF = false>
+template <int N, int TAU, bool LOAD_B, bool LOAD_C, int AUX = 0, int IO = kIoC64>
 __device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, int ch, int lane, bool act,
                                             Chunk<N, TAU>& q) {
     constexpr int SL = Lay<N>::SL;
@@ -366,7 +366,7 @@ __device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, 
     q.len = ch < a.C ? lenc : 0;
     const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
     q.kv = a.idx[((size_t)bb * a.L + s0 + min(lane, lenc - 1)) * a.H + hh];
-    constexpr uint32_t ESZ = BF ? 4 : 8;              // bytes per complex entry
+    constexpr uint32_t ESZ = IO == kIoC64 ? 8 : 4;    // bytes per entry
     const uint32_t rstride = (uint32_t)a.H * N * ESZ;  // bytes between consecutive steps
     const uint32_t extent = (uint32_t)(lenc - 1) * rstride + N * ESZ;
     const __amdgpu_buffer_rsrc_t rD = row_block(reinterpret_cast<const char*>(a.D) + base * ESZ, extent);
@@ -375,7 +375,7 @@ __device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, 
     const __amdgpu_buffer_rsrc_t rnull = row_block(a.D, 0);
     const uint32_t voff = (uint32_t)lane * SL * ESZ;
     auto ld = [&](__amdgpu_buffer_rsrc_t r, uint32_t so) {
-        if constexpr (BF) return ld_row_bf<SL, AUX>(r, voff, so);
+        if constexpr (IO != kIoC64) return ld_row_w<SL, AUX, IO>(r, voff, so);
         else return ld_row<SL, AUX>(r, voff, so);
     };
 #pragma unroll
@@ -972,7 +972,7 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
 // Wave wv owns local chunks wv, wv+W, ...; with PREFETCH the loads of its next
 // chunk are in flight while it computes the current one (two register
 // buffers).  A local chunk past the range issues an empty chunk.
-template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, bool BF>
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, int IO>
 __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
@@ -982,7 +982,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
         return;
     }
     auto issue = [&](int lc, Chunk<N, TAU>& q) {
-        issue_chunk<N, TAU, true, !AGG, kLoadStream, BF>(a, w.bb, w.hh, lc < w.nc ? w.c0 + lc : a.C, lane, act, q);
+        issue_chunk<N, TAU, true, !AGG, kLoadStream, IO>(a, w.bb, w.hh, lc < w.nc ? w.c0 + lc : a.C, lane, act, q);
     };
     bool bad = false;
     if constexpr (PREFETCH) {
@@ -1007,7 +1007,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
     if (bad) report_index_error(a.status);
 }
 
-template <int N, int TAU, int W, bool AGG, bool BF>
+template <int N, int TAU, int W, bool AGG, int IO>
 __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     extern __shared__ __align__(16) unsigned char lds[];
     const Smem s = carve_smem(lds, a.lds);
@@ -1020,10 +1020,10 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     bool fb;
     const int G = head_variant(s, a.K, fb);
     constexpr bool PF = fused_prefetch(N, TAU);
-    if (fb) fwd_body<N, TAU, W, 7, true, PF, AGG, BF>(a, s, w);
-    else if (G == 1) fwd_body<N, TAU, W, 1, false, PF, AGG, BF>(a, s, w);
-    else if (G == 3) fwd_body<N, TAU, W, 3, false, PF, AGG, BF>(a, s, w);
-    else fwd_body<N, TAU, W, 7, false, PF, AGG, BF>(a, s, w);
+    if (fb) fwd_body<N, TAU, W, 7, true, PF, AGG, IO>(a, s, w);
+    else if (G == 1) fwd_body<N, TAU, W, 1, false, PF, AGG, IO>(a, s, w);
+    else if (G == 3) fwd_body<N, TAU, W, 3, false, PF, AGG, IO>(a, s, w);
+    else fwd_body<N, TAU, W, 7, false, PF, AGG, IO>(a, s, w);
     if constexpr (!AGG) {
         // write out the staged chunk states, every wave a share of the rows
         if (a.sbM > 0 && a.saved) {
@@ -1058,12 +1058,12 @@ struct BwdChunk {
 // Issues every load of reverse-order local chunk r (chunk c0 + nc - 1 - r);
 // r >= nc issues an empty chunk through the null descriptor, as issue_chunk
 // does.  The aggregate pass needs neither b nor the saved states.
-template <int N, int TAU, bool AGG, bool BF>
+template <int N, int TAU, bool AGG, int IO>
 __device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int r, int lane, bool act,
                                           BwdChunk<N, TAU>& u) {
     constexpr int SL = Lay<N>::SL;
     const int ch = r < w.nc ? w.c0 + w.nc - 1 - r : a.C;
-    issue_chunk<N, TAU, !AGG, true, kLoadStream, BF>(a, w.bb, w.hh, ch, lane, act, u.q);
+    issue_chunk<N, TAU, !AGG, true, kLoadStream, IO>(a, w.bb, w.hh, ch, lane, act, u.q);
     const int chc = min(ch, a.C - 1);
     const int s0 = chc * TAU;
     const int lenc = min(TAU, a.L - s0);
@@ -1073,7 +1073,7 @@ __device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int
 
 // AGG: the aggregate pass of a segment -- each chunk's adjoint operator is
 // composed into the running aggregate passed from wave to wave.
-template <int N, int TAU, int W, int G, bool FB, bool AGG, bool STE, bool BF>
+template <int N, int TAU, int W, int G, bool FB, bool AGG, bool STE, int IO>
 __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int r,
                                           BwdChunk<N, TAU>& u, bool& bad) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
@@ -1217,9 +1217,9 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
         const bool in = t < q.len;
         const size_t off = base + (size_t)t * stride;
         if (act && in) {
-            if constexpr (BF) {
-                st_row_bf_stream<SL>(reinterpret_cast<uint32_t*>(a.db) + off, lane, g);
-                st_row_bf_stream<SL>(reinterpret_cast<uint32_t*>(a.dc) + off, lane, dct);
+            if constexpr (IO != kIoC64) {
+                st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.db) + off, lane, g);
+                st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.dc) + off, lane, dct);
             } else {
                 st_out<SL>(a.db + off, lane, g);
                 st_out<SL>(a.dc + off, lane, dct);
@@ -1235,7 +1235,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
                 g.v[i] = cmulc(Dt(q, t).v[i], gp);
             }
             if (in) {
-                if constexpr (BF) st_row_bf_stream<SL>(reinterpret_cast<uint32_t*>(a.dD) + off, lane, dDt);
+                if constexpr (IO != kIoC64) st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.dD) + off, lane, dDt);
                 else st_out<SL>(a.dD + off, lane, dDt);
             }
         }
@@ -1253,7 +1253,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
 
 // Wave wv owns reverse-order local chunks wv, wv+W, ...; with PREFETCH every
 // load of its next chunk is in flight while it computes the current one.
-template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, bool STE, bool BF>
+template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, bool STE, int IO>
 __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
@@ -1261,21 +1261,21 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, cons
     bool bad = false;
     if constexpr (PREFETCH) {
         BwdChunk<N, TAU> ua, ub;
-        issue_bwd<N, TAU, AGG, BF>(a, w, wv, lane, act, ua);
+        issue_bwd<N, TAU, AGG, IO>(a, w, wv, lane, act, ua);
         for (int r = wv; r < w.nc; r += 2 * W) {
-            issue_bwd<N, TAU, AGG, BF>(a, w, r + W, lane, act, ub);
+            issue_bwd<N, TAU, AGG, IO>(a, w, r + W, lane, act, ub);
             issue_fence();
-            bwd_chunk<N, TAU, W, G, FB, AGG, STE, BF>(a, s, w, r, ua, bad);
+            bwd_chunk<N, TAU, W, G, FB, AGG, STE, IO>(a, s, w, r, ua, bad);
             if (r + W >= w.nc) break;
-            issue_bwd<N, TAU, AGG, BF>(a, w, r + 2 * W, lane, act, ua);
+            issue_bwd<N, TAU, AGG, IO>(a, w, r + 2 * W, lane, act, ua);
             issue_fence();
-            bwd_chunk<N, TAU, W, G, FB, AGG, STE, BF>(a, s, w, r + W, ub, bad);
+            bwd_chunk<N, TAU, W, G, FB, AGG, STE, IO>(a, s, w, r + W, ub, bad);
         }
     } else {
         for (int r = wv; r < w.nc; r += W) {
             BwdChunk<N, TAU> u;
-            issue_bwd<N, TAU, AGG, BF>(a, w, r, lane, act, u);
-            bwd_chunk<N, TAU, W, G, FB, AGG, STE, BF>(a, s, w, r, u, bad);
+            issue_bwd<N, TAU, AGG, IO>(a, w, r, lane, act, u);
+            bwd_chunk<N, TAU, W, G, FB, AGG, STE, IO>(a, s, w, r, u, bad);
         }
     }
     if (bad) report_index_error(a.status);
@@ -1308,7 +1308,7 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_bwd(const FusedArgs& a, cons
     return U;
 }
 
-template <int N, int TAU, int W, bool AGG, bool STE, bool BF>
+template <int N, int TAU, int W, bool AGG, bool STE, int IO>
 __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     extern __shared__ __align__(16) unsigned char lds[];
@@ -1341,24 +1341,24 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     bool fb;
     const int G = head_variant(s, a.K, fb);
     constexpr bool PF = fused_prefetch(N, TAU);
-    if (fb) bwd_body<N, TAU, W, 7, true, PF, AGG, STE, BF>(a, s, w);
-    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF, AGG, STE, BF>(a, s, w);
-    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF, AGG, STE, BF>(a, s, w);
-    else bwd_body<N, TAU, W, 7, false, PF, AGG, STE, BF>(a, s, w);
+    if (fb) bwd_body<N, TAU, W, 7, true, PF, AGG, STE, IO>(a, s, w);
+    else if (G == 1) bwd_body<N, TAU, W, 1, false, PF, AGG, STE, IO>(a, s, w);
+    else if (G == 3) bwd_body<N, TAU, W, 3, false, PF, AGG, STE, IO>(a, s, w);
+    else bwd_body<N, TAU, W, 7, false, PF, AGG, STE, IO>(a, s, w);
 }
 
 // Segmented scans (S > 1) first run the aggregate pass over segments that
 // have a neighbour to hand to, then the scan over every segment.
-template <int N, int TAU, int W, bool BF>
+template <int N, int TAU, int W, int IO>
 hipError_t fwd_launch_io(const FusedArgs& a, hipStream_t st) {
     if (a.S > 1) {
-        auto agg = k_fwd_fused<N, TAU, W, true, BF>;
+        auto agg = k_fwd_fused<N, TAU, W, true, IO>;
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(agg),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3((W + 1) * 64), a.lds.total, st, a);
     }
-    auto kern = k_fwd_fused<N, TAU, W, false, BF>;
+    auto kern = k_fwd_fused<N, TAU, W, false, IO>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;
@@ -1366,17 +1366,17 @@ hipError_t fwd_launch_io(const FusedArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-template <int N, int TAU, int W, bool BF>
+template <int N, int TAU, int W, int IO>
 hipError_t bwd_launch_io(const FusedArgs& a, hipStream_t st) {
     if (a.S > 1) {
-        auto agg = k_bwd_fused<N, TAU, W, true, false, BF>;
+        auto agg = k_bwd_fused<N, TAU, W, true, false, IO>;
         hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(agg),
                                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3(W * 64), a.lds.total, st, a);
     }
     // the scaled states for the straight-through gradients come from the scan pass only
-    auto kern = a.z ? k_bwd_fused<N, TAU, W, false, true, BF> : k_bwd_fused<N, TAU, W, false, false, BF>;
+    auto kern = a.z ? k_bwd_fused<N, TAU, W, false, true, IO> : k_bwd_fused<N, TAU, W, false, false, IO>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
     if (e != hipSuccess) return e;
@@ -1384,14 +1384,24 @@ hipError_t bwd_launch_io(const FusedArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-// the input/output format (fp32 or bf16 pairs) picks the instantiation
+// the row format (complex64, bf16 pairs, real fp32) picks the instantiation
 template <int N, int TAU, int W>
 hipError_t fwd_launch(const FusedArgs& a, hipStream_t st) {
-    return a.bf16 ? fwd_launch_io<N, TAU, W, true>(a, st) : fwd_launch_io<N, TAU, W, false>(a, st);
+    switch (a.io) {
+        case kIoC64: return fwd_launch_io<N, TAU, W, kIoC64>(a, st);
+        case kIoBf16: return fwd_launch_io<N, TAU, W, kIoBf16>(a, st);
+        case kIoReal: return fwd_launch_io<N, TAU, W, kIoReal>(a, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 template <int N, int TAU, int W>
 hipError_t bwd_launch(const FusedArgs& a, hipStream_t st) {
-    return a.bf16 ? bwd_launch_io<N, TAU, W, true>(a, st) : bwd_launch_io<N, TAU, W, false>(a, st);
+    switch (a.io) {
+        case kIoC64: return bwd_launch_io<N, TAU, W, kIoC64>(a, st);
+        case kIoBf16: return bwd_launch_io<N, TAU, W, kIoBf16>(a, st);
+        case kIoReal: return bwd_launch_io<N, TAU, W, kIoReal>(a, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int N>

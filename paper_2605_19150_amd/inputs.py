@@ -90,9 +90,21 @@ def _markov_idx(rng, B, L, H, K):
     return idx
 
 
+def _rnormal_c(rng, shape, var):
+    """Real normal values of variance var, as complex64 with imaginary part 0."""
+    out = np.zeros(shape, np.complex64)
+    out.real = rng.standard_normal(shape, dtype=np.float32) * np.float32(np.sqrt(var))
+    return out
+
+
 def make_inputs(B, L, H, N, K, seed=0, pi_kind="uniform", dmag=(0.5, 0.99), bc_var=1.0,
-                idx_kind="uniform", with_h0=False, with_dhf=False, dy=True):
-    """Draw one input set.  Returns a dict of numpy arrays."""
+                idx_kind="uniform", with_h0=False, with_dhf=False, dy=True, real=False):
+    """Draw one input set.  Returns a dict of numpy arrays.
+
+    real: the real-valued model's inputs: D = magnitude * random sign (the
+    real counterpart of the uniform phase), b and c real normal of variance
+    bc_var, all float32; h0 and dh_final real normal values held as complex64
+    with imaginary part 0."""
     rng = np.random.default_rng(seed)
     if idx_kind == "uniform":
         idx = rng.integers(0, K, size=(B, L, H), dtype=np.int32)
@@ -116,20 +128,30 @@ def make_inputs(B, L, H, N, K, seed=0, pi_kind="uniform", dmag=(0.5, 0.99), bc_v
     else:
         lo, hi = dmag
         mag = rng.random(shape, dtype=np.float32) * np.float32(hi - lo) + np.float32(lo)
-    phase = rng.random(shape, dtype=np.float32) * np.float32(2.0 * np.pi)
-    D = np.empty(shape, np.complex64)
-    D.real = mag * np.cos(phase)
-    D.imag = mag * np.sin(phase)
-    del mag, phase
-    b = _cnormal(rng, shape, bc_var)
-    c = _cnormal(rng, shape, bc_var)
+    if real:
+        sign = np.where(rng.random(shape, dtype=np.float32) < 0.5, np.float32(-1.0), np.float32(1.0))
+        D = (mag * sign).astype(np.float32)
+        del mag, sign
+        sd = np.float32(np.sqrt(bc_var))
+        b = rng.standard_normal(shape, dtype=np.float32) * sd
+        c = rng.standard_normal(shape, dtype=np.float32) * sd
+        state = _rnormal_c
+    else:
+        phase = rng.random(shape, dtype=np.float32) * np.float32(2.0 * np.pi)
+        D = np.empty(shape, np.complex64)
+        D.real = mag * np.cos(phase)
+        D.imag = mag * np.sin(phase)
+        del mag, phase
+        b = _cnormal(rng, shape, bc_var)
+        c = _cnormal(rng, shape, bc_var)
+        state = _cnormal
     out = dict(idx=idx, pi=pi, D=D, b=b, c=c)
     if dy:
         out["dy"] = rng.standard_normal((B, L, H), dtype=np.float32)
     if with_h0:
-        out["h0"] = _cnormal(rng, (B, H, N), 1.0)
+        out["h0"] = state(rng, (B, H, N), 1.0)
     if with_dhf:
-        out["dh_final"] = _cnormal(rng, (B, H, N), 1.0)
+        out["dh_final"] = state(rng, (B, H, N), 1.0)
     return out
 
 

@@ -11,6 +11,9 @@ Tensor layouts (all contiguous, on one GPU):
   saved [B,H,C,N] complex64 (C = num_chunks).
 With bf16 I/O (FLAG_BF16_IO), D, b, c and dD, db, dc are bfloat16 tensors
   [B,L,H,N,2] holding (re, im) (torch.view_as_real(x).to(torch.bfloat16)).
+The real-valued model (FLAG_REAL_IO): D, b, c and dD, db, dc are float32
+  [B,L,H,N]; h0, dh_final, h_final, dh0 and saved stay complex64 (scan_fwd and
+  scan_bwd also take a real float32 h0 / dh_final and widen it).
 Straight-through surrogate gradients (Sec. 3.1 Prop. 2): q [B,L,H,K] float32,
   z [B,L,H,N] complex64, G [H,K,N,N] float32, routing logits [B,L,H,K] and
   dense dictionary M [H,K,N,N] float32.
@@ -27,6 +30,7 @@ OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP, ERR_INDEX = 0, -1,
 OP_FWD, OP_BWD, OP_COMPOSE, OP_STE_GRADS = 1, 2, 3, 4
 FLAG_PREPARED = 1
 FLAG_BF16_IO = 2
+FLAG_REAL_IO = 4
 
 
 class PdssmError(RuntimeError):
@@ -157,6 +161,11 @@ def is_bf16_io(D):
     return isinstance(D, torch.Tensor) and D.dtype == torch.bfloat16
 
 
+def is_real_io(D):
+    """D given as real float32 rows (the real-valued model)."""
+    return isinstance(D, torch.Tensor) and D.dtype == torch.float32
+
+
 def _check_inputs(idx, pi, D, b, c):
     B, L, H, N, K = dims_of(idx, pi)
     dev = idx.device
@@ -165,6 +174,8 @@ def _check_inputs(idx, pi, D, b, c):
     for t, n in ((D, "D"), (b, "b"), (c, "c")):
         if is_bf16_io(D):
             _need(t, n, torch.bfloat16, (B, L, H, N, 2), dev)
+        elif is_real_io(D):
+            _need(t, n, torch.float32, (B, L, H, N), dev)
         else:
             _need(t, n, torch.complex64, (B, L, H, N), dev)
     return B, L, H, N, K, dev
@@ -178,12 +189,12 @@ class Scan:
     prepare(pi) the scans reuse the tables in the workspace; call prepare()
     again whenever the contents of pi change."""
 
-    def __init__(self, B, L, H, N, K, chunk=0, device="cuda", ste=False, bf16=False):
+    def __init__(self, B, L, H, N, K, chunk=0, device="cuda", ste=False, bf16=False, real=False):
         self.d = desc(B, L, H, N, K, chunk)
         self.dp = desc(B, L, H, N, K, chunk)
         self.bf16 = bf16
-        if bf16:
-            self.d.flags = FLAG_BF16_IO
+        self.real = real
+        self.d.flags = (FLAG_BF16_IO if bf16 else 0) | (FLAG_REAL_IO if real else 0)
         self.dp.flags = FLAG_PREPARED | self.d.flags
         self.prepared = False
         self.dims = (B, L, H, N, K)
@@ -202,6 +213,8 @@ class Scan:
         self.saved = torch.empty((B, H, self.C, N), dtype=torch.complex64, device=dev)
         if bf16:
             self.dD = torch.empty((B, L, H, N, 2), dtype=torch.bfloat16, device=dev)
+        elif real:
+            self.dD = torch.empty((B, L, H, N), dtype=torch.float32, device=dev)
         else:
             self.dD = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
         self.db = torch.empty_like(self.dD)
@@ -272,26 +285,36 @@ class Scan:
             raise PdssmError(st, "kernel index check")
 
 
+def _state_arg(x, name, real, dims, dev):
+    """A [B,H,N] state argument: complex64, or for the real model also float32
+    (widened to complex64, imaginary part 0)."""
+    if x is None:
+        return None
+    if real and isinstance(x, torch.Tensor) and x.dtype == torch.float32:
+        _need(x, name, torch.float32, dims, dev)
+        return x.to(torch.complex64)
+    _need(x, name, torch.complex64, dims, dev)
+    return x
+
+
 def scan_fwd(idx, pi, D, b, c, h0=None, chunk=0, stream=None):
     """Returns (y [B,L,H] f32, h_final [B,H,N] c64, saved [B,H,C,N] c64)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
-    if h0 is not None:
-        _need(h0, "h0", torch.complex64, (B, H, N), dev)
-    s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D))
+    h0 = _state_arg(h0, "h0", is_real_io(D), (B, H, N), dev)
+    s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D), real=is_real_io(D))
     s.fwd(idx, pi, D, b, c, h0, stream)
     s.check_status()
     return s.y, s.h_final, s.saved
 
 
 def scan_bwd(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
-    """Returns (dD, db, dc [B,L,H,N] c64, or [B,L,H,N,2] bf16 for bf16 inputs;
-    dh0 [B,H,N] c64)."""
+    """Returns (dD, db, dc [B,L,H,N] c64, or [B,L,H,N,2] bf16 for bf16 inputs,
+    or [B,L,H,N] f32 for real inputs; dh0 [B,H,N] c64)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
-    s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D))
+    s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D), real=is_real_io(D))
     _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
     _need(dy, "dy", torch.float32, (B, L, H), dev)
-    if dh_final is not None:
-        _need(dh_final, "dh_final", torch.complex64, (B, H, N), dev)
+    dh_final = _state_arg(dh_final, "dh_final", is_real_io(D), (B, H, N), dev)
     s.saved = saved
     s.bwd(idx, pi, D, b, c, dy, dh_final, stream)
     s.check_status()

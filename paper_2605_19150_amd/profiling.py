@@ -39,12 +39,14 @@ def _code_only(text):
 # headers it includes.  A traffic summary stays valid while these are
 # unchanged (comments aside).
 KERNEL_SOURCES = {
-    "k_fwd_fused": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
-    "k_bwd_fused": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
-    "k_bwd_fused_ste": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
-    "k_fwd_fused_bf16": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
-    "k_bwd_fused_bf16": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h"],
-    "k_ste_gemm": ["pdssm_ste.hip", "pdssm_internal.h", "pdssm_device.h"],
+    "k_fwd_fused": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_bwd_fused": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_bwd_fused_ste": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_fwd_fused_bf16": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_bwd_fused_bf16": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_fwd_fused_real": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_bwd_fused_real": ["pdssm_fused.hip", "pdssm_fused.h", "pdssm_device.h", "pdssm_io.h"],
+    "k_ste_gemm": ["pdssm_ste.hip", "pdssm_internal.h", "pdssm_device.h", "pdssm_io.h"],
 }
 
 

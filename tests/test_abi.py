@@ -82,20 +82,23 @@ def test_bad_descriptors(lib, kw, code):
 
 def test_flags_known_bits_only(lib):
     d = pdssm.desc(2, 10, 2, 64, 4)
-    for ok in (pdssm.FLAG_PREPARED, pdssm.FLAG_BF16_IO, pdssm.FLAG_PREPARED | pdssm.FLAG_BF16_IO):
+    for ok in (pdssm.FLAG_PREPARED, pdssm.FLAG_BF16_IO, pdssm.FLAG_PREPARED | pdssm.FLAG_BF16_IO,
+               pdssm.FLAG_REAL_IO, pdssm.FLAG_PREPARED | pdssm.FLAG_REAL_IO):
         d.flags = ok
         assert pdssm.num_chunks(d) == 2
-    for bad in (4, 8, 1 << 31):
+    # one row format at a time; no unknown bits
+    for bad in (pdssm.FLAG_BF16_IO | pdssm.FLAG_REAL_IO, 8, 1 << 31):
         d.flags = bad
         assert pdssm.num_chunks(d) == pdssm.ERR_INVALID_ARG
 
 
-def test_bf16_io_only_where_supported(lib):
+@pytest.mark.parametrize("flag", ["FLAG_BF16_IO", "FLAG_REAL_IO"])
+def test_narrow_io_only_where_supported(lib, flag):
     f = FakeBufs()
     P = lambda n: f(n)  # noqa: E731
     # composition, decode and the straight-through calls take complex64 only
     d = pdssm.desc(2, 40, 2, 64, 4)
-    d.flags = pdssm.FLAG_BF16_IO
+    d.flags = getattr(pdssm, flag)
     st = 2 * 40 * 2 * 64 * 8
     assert lib.pdssm_compose_chunks(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), None,
                                     None) == pdssm.ERR_UNSUPPORTED
@@ -108,10 +111,10 @@ def test_bf16_io_only_where_supported(lib):
     args = [P(640), P(2048), P(st), P(st), P(st), P(2 * 2 * 5 * 64 * 8), P(640), None]
     assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, P(st), P(st), P(st), None, P(st), ws, need, None,
                                   None) == pdssm.ERR_UNSUPPORTED
-    # the multi-pass kernels (dictionary tables beyond LDS) do not read bf16 pairs
+    # the multi-pass kernels (dictionary tables beyond LDS) read complex64 rows only
     big = pdssm.desc(1, 40, 1, 128, 128)
     assert lib.pdssm_uses_fused(ctypes.byref(big)) == 0
-    big.flags = pdssm.FLAG_BF16_IO
+    big.flags = getattr(pdssm, flag)
     need = lib.pdssm_workspace_size(ctypes.byref(big), pdssm.OP_FWD)
     ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
     st = 40 * 128 * 8

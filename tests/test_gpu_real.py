@@ -1,0 +1,157 @@
+"""GPU parity of the real-valued model (PDSSM_FLAG_REAL_IO): D, b, c and dD,
+db, dc as real fp32 rows, h0 / dh_final real values held as complex64.
+
+Two checks per case:
+  - against the float64 oracle on the same inputs: y, h_final, the saved
+    states and every gradient to the scan's bar |gpu - ref| <= 1e-5 +
+    1e-4*|ref| (the real model is the complex one restricted to real rows);
+  - against the complex64 path on the same values (imaginary parts 0): bit
+    for bit, the real path's gradients equal the complex path's real parts
+    and the complex path's imaginary parts are 0.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+from helpers import assert_close, sub_sequence
+from oracle import oracle_bwd, oracle_fwd
+from paper_2605_19150_amd.inputs import make_inputs, workload_inputs
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU machines, never run there
+    pytest.skip("no GPU", allow_module_level=True)
+
+from paper_2605_19150_amd import pdssm  # noqa: E402
+
+DEV = torch.device("cuda:0")
+
+
+def run_both(inp, chunk=0):
+    """The real path and the complex64 path on the same real values."""
+    B, L, H = inp["idx"].shape
+    _, K, N = inp["pi"].shape
+    real = {k: torch.from_numpy(inp[k]).to(DEV) for k in ("D", "b", "c")}
+    cplx = {k: v.to(torch.complex64) for k, v in real.items()}
+    idx, pi = torch.from_numpy(inp["idx"]).to(DEV), torch.from_numpy(inp["pi"]).to(DEV)
+    h0 = torch.from_numpy(inp["h0"]).to(DEV) if "h0" in inp else None
+    dy = torch.from_numpy(inp["dy"]).to(DEV)
+    dhf = torch.from_numpy(inp["dh_final"]).to(DEV) if "dh_final" in inp else None
+    out = {}
+    for tag, T, re in (("real", real, True), ("c64", cplx, False)):
+        s = pdssm.Scan(B, L, H, N, K, chunk, DEV, real=re)
+        s.fwd(idx, pi, T["D"], T["b"], T["c"], h0=h0)
+        s.bwd(idx, pi, T["D"], T["b"], T["c"], dy, dh_final=dhf)
+        s.check_status()
+        out[tag] = {k: getattr(s, k).clone() for k in ("y", "h_final", "saved", "dD", "db", "dc", "dh0")}
+        out[tag]["chunk"] = s.chunk
+        del s
+    return out
+
+
+def check_bits(out):
+    r, c = out["real"], out["c64"]
+    for k in ("y", "h_final", "saved", "dh0"):
+        assert torch.equal(r[k], c[k]), k
+    for k in ("h_final", "dh0"):
+        assert bool((r[k].imag == 0).all()), k
+    for k in ("dD", "db", "dc"):
+        assert r[k].dtype == torch.float32
+        assert torch.equal(r[k], c[k].real), k
+        assert bool((c[k].imag == 0).all()), k
+
+
+def check_oracle(inp, out):
+    r = out["real"]
+    ry, rhf, rsaved = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp.get("h0"),
+                                 chunk=r["chunk"])
+    assert_close("y", r["y"].cpu().numpy(), ry)
+    assert_close("h_final", r["h_final"].cpu().numpy(), rhf)
+    assert_close("saved", r["saved"].cpu().numpy(), rsaved)
+    rg = oracle_bwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp.get("h0"),
+                    dh_final=inp.get("dh_final"))
+    for k, g in zip(("dD", "db", "dc"), rg[:3]):
+        assert np.all(g.imag == 0), k
+        assert_close(k, r[k].cpu().numpy(), g.real)
+    assert_close("dh0", r["dh0"].cpu().numpy(), rg[3])
+
+
+CASES = []
+for N in (8, 16, 32, 64, 128, 256):
+    for chunk in (4, 8, 16):
+        if chunk * max(1, N // 64) > 16:
+            continue
+        CASES.append((N, chunk, 3 * chunk + 5))
+CASES += [(64, 8, 1), (64, 8, 261), (128, 8, 133)]
+
+
+@pytest.mark.parametrize("N,chunk,L", CASES)
+def test_real_io_small(N, chunk, L):
+    print("real case N=%d chunk=%d L=%d" % (N, chunk, L), flush=True)
+    inp = make_inputs(B=2, L=L, H=3, N=N, K=5, seed=N * 37 + chunk + L, with_h0=True, with_dhf=True, real=True)
+    if pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(2, L, 3, N, 5, chunk))) != 1:
+        # dictionaries beyond LDS run the multi-pass kernels, which take complex64 only
+        with pytest.raises(pdssm.PdssmError) as e:
+            run_both(inp, chunk)
+        assert e.value.status == pdssm.ERR_UNSUPPORTED
+        return
+    out = run_both(inp, chunk)
+    check_bits(out)
+    check_oracle(inp, out)
+
+
+def test_real_io_collisions():
+    # all-to-one maps in one head (the atomic-scatter entries) and random maps in the other
+    inp = make_inputs(B=2, L=45, H=2, N=64, K=4, seed=11, with_h0=True, with_dhf=True, real=True)
+    inp["pi"][0] = 0
+    out = run_both(inp, 8)
+    check_bits(out)
+    check_oracle(inp, out)
+
+
+def test_real_io_segmented():
+    inp = make_inputs(B=1, L=2600, H=2, N=64, K=16, seed=5, pi_kind="perm", with_h0=True, with_dhf=True,
+                      real=True)
+    assert pdssm.scan_segments(pdssm.desc(1, 2600, 2, 64, 16)) > 1
+    out = run_both(inp)
+    check_bits(out)
+    check_oracle(inp, out)
+
+
+def test_real_io_module_functions():
+    # scan_fwd / scan_bwd pick the real format from D's dtype and widen a real h0
+    inp = make_inputs(B=2, L=37, H=2, N=32, K=3, seed=9, with_h0=True, with_dhf=True, real=True)
+    T = {k: torch.from_numpy(np.ascontiguousarray(inp[k])).to(DEV) for k in ("idx", "pi", "D", "b", "c", "dy")}
+    h0r = torch.from_numpy(np.ascontiguousarray(inp["h0"].real)).to(DEV)
+    dhfr = torch.from_numpy(np.ascontiguousarray(inp["dh_final"].real)).to(DEV)
+    y, hf, saved = pdssm.scan_fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=h0r)
+    dD, db, dc, dh0 = pdssm.scan_bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], saved, T["dy"], dh_final=dhfr)
+    assert dD.dtype == torch.float32 and dD.shape == T["D"].shape
+    ry, rhf, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp["h0"])
+    assert_close("y", y.cpu().numpy(), ry)
+    assert_close("h_final", hf.cpu().numpy(), rhf)
+    rg = oracle_bwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"],
+                    dh_final=inp["dh_final"])
+    for k, v, g in zip(("dD", "db", "dc"), (dD, db, dc), rg[:3]):
+        assert_close(k, v.cpu().numpy(), g.real)
+    assert_close("dh0", dh0.cpu().numpy(), rg[3])
+
+
+@pytest.mark.parametrize("wl", [2, 4])
+def test_real_io_full_size(wl):
+    print("real full size workload %d" % wl, flush=True)
+    inp = workload_inputs(wl, seed=0, real=True)
+    out = run_both(inp)
+    check_bits(out)
+    r = out["real"]
+    B, L, H = inp["idx"].shape
+    for bb, hh in ((0, 0), (B - 1, H - 1), (B // 2, H // 3)):
+        sub = sub_sequence(inp, bb, hh)
+        ry, rhf, _ = oracle_fwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"])
+        assert_close("y", r["y"][bb:bb + 1, :, hh:hh + 1].cpu().numpy(), ry)
+        assert_close("h_final", r["h_final"][bb:bb + 1, hh:hh + 1].cpu().numpy(), rhf)
+        rg = oracle_bwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"], sub["dy"])
+        for k, g in zip(("dD", "db", "dc"), rg[:3]):
+            assert_close(k, r[k][bb:bb + 1, :, hh:hh + 1].cpu().numpy(), g.real)
