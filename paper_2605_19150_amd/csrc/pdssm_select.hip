@@ -167,6 +167,238 @@ __global__ __launch_bounds__(256) void k_route(RouteArgs a) {
     }
 }
 
+// ------------------------------------------------------------------ k_route_dma
+// The routing product for contraction sizes that are a multiple of 32, with
+// direct buffer-to-LDS loads (buffer_load_dwordx4 ... lds: every lane of a
+// wave moves 16 bytes to LDS at a wave-uniform base + 16 * lane), so that
+// several slices are in flight without holding them in registers.  Rows past
+// the end of u or S lie past their buffer descriptors and read as 0.
+//
+// A workgroup computes BM tokens x 256 columns (whole heads) with eight
+// waves in a WGM x WGN grid.  The contraction goes in slices of 32 through
+// NS = 4 LDS stages: while slice s is multiplied, slices s+1 .. s+3 are
+// loading.  A stage holds BM rows of u, then 256 rows of S, 64 bytes of each;
+// every 16 consecutive rows form a 1 KB block laid out chunk-major (byte
+// (r/16)*1024 + c*256 + (r%16)*16 for row r, 16-byte chunk c), which is
+// exactly what one wave-wide load instruction writes (lane l: row l%16, chunk
+// l/16) and makes the operand reads (32 rows at one chunk) conflict-free.
+// (Measured: loads of half cache lines, as here, reach about half the L2 rate
+// of full ones, and the slices' loads set the pace of the kernel.)
+//
+// Tiles are numbered so that each XCD (workgroups are dealt round-robin over
+// the 8 XCDs) takes a contiguous range, all column tiles of a few token tiles
+// at a time: u streams from HBM once and the rows of S are shared in L2.
+typedef __attribute__((address_space(3))) void* lds_void_t;
+
+// One wave-wide 16-byte-per-lane load from a buffer into LDS at dst + 16*lane.
+__device__ __forceinline__ void load_lds16(__amdgpu_buffer_rsrc_t r, unsigned char* dst, uint32_t voff,
+                                           uint32_t soff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t)dst, 16, voff, soff, 0, 0);
+}
+
+template <int BM>
+struct RouteDma {
+    static constexpr int BN = 256, BK = 32, NS = 4, NW = 8;
+    static constexpr int WGM = BM / 64, WGN = NW / WGM;  // wave grid: 64-row blocks of the tile
+    static constexpr int TM = BM / WGM, TN = BN / WGN;   // a wave's block
+    static constexpr int WM = TM / 32, WN = TN / 32;     // its 32 x 32 products
+    static constexpr int ROWS = BM + BN;                 // rows of a stage
+    static constexpr int STAGE = ROWS * BK * 2;          // bytes of a stage
+    static constexpr int PER_WAVE = ROWS / 16 / NW;      // load instructions per wave per stage
+    // epilogue tile pitch (floats): 16-byte aligned rows; 16 consecutive rows
+    // start in distinct 16-byte bank groups
+    static constexpr int PITCH = BN + 4;
+    static constexpr size_t kStages = (size_t)NS * STAGE, kTile = (size_t)BM / 2 * PITCH * 4;
+    static constexpr size_t LDS = kStages > kTile ? kStages : kTile;
+    static_assert(ROWS % (16 * NW) == 0, "whole blocks per wave");
+    static_assert(WGM * WGN == NW && TM == 64, "wave grid");
+    static_assert(LDS <= 160 * 1024, "fits the LDS of a CU");
+};
+
+// s_waitcnt vmcnt(n) with the other counters left alone (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int n>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(n >= 0 && n < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier without the memory fence of __syncthreads, whose release
+// half would wait for every outstanding load, the later slices' included.
+// The loads a slice needs are waited for explicitly before it; the compiler
+// fences keep LDS accesses on their side of the barrier.
+__device__ __forceinline__ void barrier_no_fence() {
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+template <int BM>
+__global__ __launch_bounds__(512) void k_route_dma(RouteArgs a) {
+    using C = RouteDma<BM>;
+    constexpr int NT_ = C::NW * 64;
+    extern __shared__ __align__(16) unsigned char lds[];
+    // wave-uniform in a scalar register: the load instructions' LDS base and
+    // descriptor depend on it
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int wm = wv / C::WGN, wn = wv % C::WGN;
+    const int hpb = C::BN / a.K;  // heads per column tile
+    const int NT = (a.H + hpb - 1) / hpb, MT = (a.T + BM - 1) / BM;
+    const int total = NT * MT;
+    int t = blockIdx.x;
+    if (total % 8 == 0) t = (t % 8) * (total / 8) + t / 8;
+    const int nt = t % NT, mt = t / NT;
+    const int h0 = nt * hpb;
+    const int nh = min(hpb, a.H - h0);
+    const int ncol = nh * a.K;
+    const int m0 = mt * BM;
+    const int HK = a.H * a.K;
+
+    // this lane's byte offset of each of its load instructions: row
+    // (wv * PER_WAVE + i) * 16 + lane % 16 of the stage, chunk lane / 16
+    const uint32_t row_bytes = (uint32_t)a.Dm * 2;
+    const __amdgpu_buffer_rsrc_t ru = row_block(a.u, (uint32_t)a.T * row_bytes);
+    const __amdgpu_buffer_rsrc_t rs = row_block(a.S, (uint32_t)HK * row_bytes);
+    uint32_t voff[C::PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < C::PER_WAVE; ++i) {
+        const int row = (wv * C::PER_WAVE + i) * 16 + (lane & 15);
+        const uint32_t r = row < BM ? (uint32_t)(m0 + row) : (uint32_t)(h0 * a.K + row - BM);
+        voff[i] = r * row_bytes + 16u * (uint32_t)(lane >> 4);
+    }
+    auto issue = [&](int s) {
+        unsigned char* st = lds + (s % C::NS) * C::STAGE;
+        const uint32_t so = (uint32_t)s * C::BK * 2;
+#pragma unroll
+        for (int i = 0; i < C::PER_WAVE; ++i)
+            load_lds16((wv * C::PER_WAVE + i) * 16 >= BM ? rs : ru, st + (wv * C::PER_WAVE + i) * 1024, voff[i], so);
+    };
+
+    f32x16 acc[C::WM][C::WN];
+#pragma unroll
+    for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+        for (int j = 0; j < C::WN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int c0 = wn * C::TN;     // this wave's first column of the tile
+    const bool work = c0 < ncol;  // a wave past the tile's columns multiplies zeros and stores nothing
+    const int ra = wm * C::TM + (lane & 31);  // operand rows: A tile i at ra + 32 i
+    const int rb = BM + c0 + (lane & 31);     // B tile j at rb + 32 j
+    auto off = [](int r, int c) { return (r >> 4) * 1024 + c * 256 + (r & 15) * 16; };
+    // every operand read of a slice is issued before its first product, so
+    // the reads of the second half of the slice overlap the products of the first
+    auto compute = [&](int s) {
+        const unsigned char* st = lds + (s % C::NS) * C::STAGE;
+        bf16x8 A[2][C::WM], B[2][C::WN];
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk) {
+            const int c = 2 * kk + (lane >> 5);
+#pragma unroll
+            for (int i = 0; i < C::WM; ++i) A[kk][i] = *reinterpret_cast<const bf16x8*>(st + off(ra + 32 * i, c));
+#pragma unroll
+            for (int j = 0; j < C::WN; ++j) B[kk][j] = *reinterpret_cast<const bf16x8*>(st + off(rb + 32 * j, c));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+            for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::WN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[kk][i], B[kk][j], acc[i][j], 0, 0, 0);
+    };
+
+    const int nsl = a.Dm / C::BK;
+#pragma unroll
+    for (int s = 0; s < C::NS - 1; ++s)
+        if (s < nsl) issue(s);
+    for (int s = 0; s < nsl; ++s) {
+        // this wave's loads of slice s are done once at most the later issued slices are outstanding
+        const int ahead = min(C::NS - 2, nsl - 1 - s);
+        if (ahead >= 2) wait_vmcnt<2 * C::PER_WAVE>();
+        else if (ahead == 1) wait_vmcnt<C::PER_WAVE>();
+        else wait_vmcnt<0>();
+        barrier_no_fence();  // every wave's slice s is in LDS; every wave is done with slice s-1
+        if (s + C::NS - 1 < nsl) issue(s + C::NS - 1);  // into slice s-1's stage
+        compute(s);
+    }
+    __syncthreads();  // the stages are free for the epilogue tile
+
+    float* tile = reinterpret_cast<float*>(lds);
+    constexpr int HALF = BM / 2;
+    // 16-byte logits stores and argmax reads when K % 4 == 0 (then every head,
+    // every tile and every output row starts on a 16-byte boundary)
+    const bool vec = a.K % 4 == 0;
+    for (int half = 0; half < 2; ++half) {
+        if (half) __syncthreads();  // the first half's readers are done
+        const int rlo = wm * C::TM - half * HALF;  // this wave's first row within the half
+        if (rlo >= 0 && rlo < HALF && work) {
+#pragma unroll
+            for (int i = 0; i < C::WM; ++i)
+#pragma unroll
+                for (int j = 0; j < C::WN; ++j)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        tile[(rlo + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3)) * C::PITCH + c0 + 32 * j +
+                             (lane & 31)] = acc[i][j][r];
+        }
+        __syncthreads();
+        const int mb = m0 + half * HALF;
+        const int nm = max(0, min(HALF, a.T - mb));
+        float* lrow = a.logits ? a.logits + (size_t)mb * HK + (size_t)h0 * a.K : nullptr;  // row mb, first column
+        if (vec) {
+            const int nq = ncol / 4;
+            if (lrow)
+                for (int e = threadIdx.x; e < nm * nq; e += NT_) {
+                    const int m = e / nq, q = e - m * nq;
+                    *reinterpret_cast<float4*>(lrow + (size_t)m * HK + 4 * q) =
+                        *reinterpret_cast<const float4*>(tile + m * C::PITCH + 4 * q);
+                }
+        } else if (lrow) {
+            for (int e = threadIdx.x; e < nm * ncol; e += NT_) {
+                const int m = e / ncol, c = e - m * ncol;
+                lrow[(size_t)m * HK + c] = tile[m * C::PITCH + c];
+            }
+        }
+        // first maximal index per (token, head); neighbouring lanes take
+        // neighbouring tokens
+        for (int e = threadIdx.x; e < HALF * nh; e += NT_) {
+            const int m = e % HALF, hh = e / HALF;
+            if (m >= nm) continue;
+            const float* v = tile + m * C::PITCH + hh * a.K;
+            int best = 0;
+            float bv = v[0];
+            if (vec) {
+                for (int q = 0; q < a.K / 4; ++q) {
+                    const float4 x = reinterpret_cast<const float4*>(v)[q];
+                    if (x.x > bv) bv = x.x, best = 4 * q;
+                    if (x.y > bv) bv = x.y, best = 4 * q + 1;
+                    if (x.z > bv) bv = x.z, best = 4 * q + 2;
+                    if (x.w > bv) bv = x.w, best = 4 * q + 3;
+                }
+            } else {
+                for (int k = 1; k < a.K; ++k)
+                    if (v[k] > bv) bv = v[k], best = k;
+            }
+            a.idx[(size_t)(mb + m) * a.H + h0 + hh] = best;
+        }
+    }
+}
+
+template <int BM>
+hipError_t route_dma_launch(const RouteArgs& a, hipStream_t st) {
+    using C = RouteDma<BM>;
+    const int hpb = C::BN / a.K;
+    const int NT = (a.H + hpb - 1) / hpb, MT = (a.T + BM - 1) / BM;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_route_dma<BM>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_route_dma<BM>, dim3((unsigned)(NT * MT)), dim3(C::NW * 64), C::LDS, st, a);
+    return hipGetLastError();
+}
+
 // pi[h,k,j] = argmax_i M[h,k,i,j]: a thread per (h,k,j), loads coalesced over j.
 __global__ __launch_bounds__(256) void k_dict_argmax(const float* __restrict__ M, int* __restrict__ pi, int HK,
                                                      int N) {
@@ -187,6 +419,15 @@ __global__ __launch_bounds__(256) void k_dict_argmax(const float* __restrict__ M
 }  // namespace
 
 hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
+    // byte offsets of the direct-load kernel are 32-bit, rows past the end included
+    const bool fits = (long long)(a.T + 256) * a.Dm * 2 < (1LL << 32) &&
+                      (long long)(a.H * a.K + 256) * a.Dm * 2 < (1LL << 32);
+    if (a.Dm % RouteDma<128>::BK == 0 && fits) {
+        // 256-token tiles when they still give every CU two of them
+        const int NT = (a.H + 256 / a.K - 1) / (256 / a.K);
+        const long long tiles256 = (long long)((a.T + 255) / 256) * NT;
+        return tiles256 >= 512 ? route_dma_launch<256>(a, st) : route_dma_launch<128>(a, st);
+    }
     const int hpb = kRouteTN / a.K;
     dim3 grid((a.T + kRouteTM - 1) / kRouteTM, (a.H + hpb - 1) / hpb);
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_route),

@@ -68,6 +68,8 @@ def check_route(B, L, H, K, Dm, seed):
     (2, 33, 2, 256, 64),      # one head per tile
     (1, 1, 1, 1, 8),          # smallest
     (3, 50, 300, 3, 16),      # many head groups
+    (8, 2048, 32, 64, 64),    # 256-token tiles, 512 of them, two slices of the contraction
+    (1, 18693, 28, 64, 32),   # 256-token tiles, a ragged last one, a tile count not a multiple of 8
 ])
 def test_route(B, L, H, K, Dm):
     print("route B=%d L=%d H=%d K=%d Dm=%d" % (B, L, H, K, Dm), flush=True)
@@ -79,3 +81,28 @@ def test_route_full_size():
     """fsa-perm routing: B16 L2048, 16 heads x 16 maps, d = 1024."""
     frac = check_route(16, 2048, 16, 16, 1024, seed=0)
     assert frac > 0.99
+
+
+def test_route_hybrid_full_size_sampled():
+    """hybrid-lm routing: B8 L4096 (32768 tokens), 32 heads x 64 maps, d = 4096;
+    logits and choices of sampled tokens against the oracle."""
+    rng = np.random.default_rng(3)
+    B, L, H, K, Dm = 8, 4096, 32, 64, 4096
+    ut = torch.from_numpy(rng.standard_normal((B, L, Dm), dtype=np.float32)).to(torch.bfloat16)
+    St = torch.from_numpy(rng.standard_normal((H, K, Dm), dtype=np.float32) / np.float32(np.sqrt(Dm))).to(
+        torch.bfloat16)
+    logits, idx = pdssm.route(ut.to(DEV), St.to(DEV))
+    rows = np.sort(rng.choice(B * L, size=96, replace=False))
+    u = ut.reshape(B * L, Dm)[rows].to(torch.float64).numpy()[None]
+    S = St.to(torch.float64).numpy()
+    lg = logits.reshape(B * L, H, K)[rows].cpu().numpy()[None]
+    ix = idx.reshape(B * L, H)[rows].cpu().numpy()[None]
+    rl, ri = oracle_route(u, S)
+    scale = np.einsum("bld,hkd->blhk", np.abs(u), np.abs(S))
+    assert_close_sum("logits", lg, rl, scale)
+    np.testing.assert_array_equal(ix, np.argmax(lg, axis=3))
+    tol = 1e-5 + 1e-4 * scale.max(axis=3)
+    top2 = np.sort(rl, axis=3)[..., -2:]
+    clear = (top2[..., 1] - top2[..., 0]) > 2 * tol
+    np.testing.assert_array_equal(ix[clear], ri[clear])
+    assert clear.mean() > 0.9
