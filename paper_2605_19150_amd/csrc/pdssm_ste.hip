@@ -205,6 +205,7 @@ struct DictCfg {
     static constexpr int WAVES = BLOCKS * SPLIT;
     static constexpr int TILES = NB / 32;
     static constexpr int RS = N <= 64 ? 64 : (N == 128 ? 32 : 16);  // steps per run (staged tiles <= ~70 KB)
+    static constexpr int SLOTS = 64 / RS;                            // score tasks a wave runs side by side
     static constexpr int MY = RS / SPLIT;                            // steps of a run one wave multiplies
     static constexpr int U = N >= 256 ? 4 : 8;                       // steps per load batch
     static constexpr int NBAT = MY / U;                              // load batches per run (even)
@@ -357,21 +358,29 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
         for (int u = 0; u < U; ++u)
             if (r * RS + my0 + b * U + u < cnt) mfma_step<N>(acc, gq[u], zq[u], lane);
     };
-    // scores of the run's steps: lane t = step t of the run, KW maps per task
+    // scores of the run's steps, KW maps per task: lane l takes step l % RS
+    // of the run, and the 64 / RS lane groups of a wave take different tasks
+    // (every lane reads: a run shorter than the wave leaves none idle)
     auto scores = [&](int sidv, int r) {
-        const bool on = lane < RS && r * RS + lane < cnt;
-        const int tt = on ? lane : 0;
+        const int slot = lane / RS, tt = lane % RS;
+        const int sidt = __shfl(sidv, tt);  // step id of this lane's step
+        const bool step_on = r * RS + tt < cnt;
         constexpr int KWD = KW > 0 ? KW : 1;
         const int ntask = (a.K + KWD - 1) / KWD;
-        for (int task = wv; task < ntask; task += Cfg::WAVES) {
-            const int kb = task * KW;
+        for (int tg = wv; tg * Cfg::SLOTS < ntask; tg += Cfg::WAVES) {
+            const int task = tg * Cfg::SLOTS + slot;
+            const bool on = step_on && task < ntask;
+            const int kb = min(task, ntask - 1) * KW;  // a lane past the tasks reads the last one and stores nothing
             float v[KW > 0 ? KW : 1];
 #pragma unroll
             for (int u = 0; u < KW; ++u) v[u] = 0.f;
-#pragma unroll 2
-            for (int j = 0; j < N; ++j) {
-                const float2 zt = Zt[j * GP + tt];
-                uint32_t wds[KW / 4 > 0 ? KW / 4 : 1];
+            // column j: z_t[j], the KW maps' rows at j (packed bytes), then
+            // the KW gathered g_t[pi(j)]; the next column's z and map bytes
+            // are read with this column's gathers, so each column waits for
+            // one LDS round trip
+            constexpr int NW4 = KW / 4 > 0 ? KW / 4 : 1;
+            auto ld_col = [&](int j, uint32_t (&wds)[NW4], float2& zt) {
+                zt = Zt[j * GP + tt];
                 if constexpr (KW == 16) {
                     const uint4 pk = *reinterpret_cast<const uint4*>(dT + j * KP + kb);
                     wds[0] = pk.x, wds[1] = pk.y, wds[2] = pk.z, wds[3] = pk.w;
@@ -381,14 +390,46 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
                 } else {
                     wds[0] = *reinterpret_cast<const uint32_t*>(dT + j * KP + kb);
                 }
+            };
+            auto column = [&](const uint32_t (&wc)[NW4], float2 zc) {
+                float2 g[KW > 0 ? KW : 1];
 #pragma unroll
-                for (int u = 0; u < KW; ++u) {
-                    const float2 g = Gt[((wds[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
-                    v[u] = fmaf(g.x, zt.x, fmaf(g.y, zt.y, v[u]));
+                for (int u = 0; u < KW; ++u) g[u] = Gt[((wc[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
+#pragma unroll
+                for (int u = 0; u < KW; ++u) v[u] = fmaf(g[u].x, zc.x, fmaf(g[u].y, zc.y, v[u]));
+            };
+            if constexpr (N < 256 && KW >= 8) {
+                uint32_t wc[NW4];
+                float2 zc;
+                ld_col(0, wc, zc);
+#pragma unroll 2
+                for (int j = 0; j < N; ++j) {
+                    uint32_t wn[NW4];
+                    float2 zn;
+                    ld_col(min(j + 1, N - 1), wn, zn);
+                    column(wc, zc);
+#pragma unroll
+                    for (int q = 0; q < NW4; ++q) wc[q] = wn[q];
+                    zc = zn;
+                }
+            } else {
+                // few maps per task (or 16 waves, 128 registers): each gather
+                // added as it arrives, two columns unrolled (measured faster
+                // here than batching the gathers)
+#pragma unroll 2
+                for (int j = 0; j < N; ++j) {
+                    uint32_t wc[NW4];
+                    float2 zc;
+                    ld_col(j, wc, zc);
+#pragma unroll
+                    for (int u = 0; u < KW; ++u) {
+                        const float2 g = Gt[((wc[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
+                        v[u] = fmaf(g.x, zc.x, fmaf(g.y, zc.y, v[u]));
+                    }
                 }
             }
             if (on) {
-                float* qrow = a.q + ((size_t)sidv * a.H + h) * a.K + kb;
+                float* qrow = a.q + ((size_t)sidt * a.H + h) * a.K + kb;
                 if (kb + KW <= a.K && (a.K & 3) == 0) {
 #pragma unroll
                     for (int u = 0; u < KW; u += 4)
@@ -501,13 +542,13 @@ hipError_t gemm_launch(const SteGradArgs& a, hipStream_t st) {
 template <int N>
 hipError_t dict_launch(const SteGradArgs& a, hipStream_t st) {
     // score tasks of 16, 8 or 4 maps: wide enough to amortise each z read,
-    // many enough to keep every wave busy
-    const int waves = DictCfg<N>::WAVES;
+    // many enough to keep every lane group of every wave busy
+    const int waves = DictCfg<N>::WAVES * DictCfg<N>::SLOTS;
     hipError_t e;
+    constexpr int KW16 = N < 256 ? 16 : 4, KW8 = N < 256 ? 8 : 4;  // N = 256 (16 waves): 4 maps per task
     if (!a.q) e = gemm_launch<N, 0, true>(a, st);
-    else if (N < 256 && a.K >= 16 * waves)  // (16 waves x 16 maps would spill registers)
-        e = a.G ? gemm_launch<N, N < 256 ? 16 : 8, true>(a, st) : gemm_launch<N, N < 256 ? 16 : 8, false>(a, st);
-    else if (a.K >= 8 * waves) e = a.G ? gemm_launch<N, 8, true>(a, st) : gemm_launch<N, 8, false>(a, st);
+    else if (a.K >= 16 * waves) e = a.G ? gemm_launch<N, KW16, true>(a, st) : gemm_launch<N, KW16, false>(a, st);
+    else if (a.K >= 8 * waves) e = a.G ? gemm_launch<N, KW8, true>(a, st) : gemm_launch<N, KW8, false>(a, st);
     else e = a.G ? gemm_launch<N, 4, true>(a, st) : gemm_launch<N, 4, false>(a, st);
     if (e != hipSuccess || !a.G) return e;
     const int ys = (N * N + 255) / 256 < 16 ? (N * N + 255) / 256 : 16;
