@@ -398,7 +398,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 #pragma unroll
                 for (int u = 0; u < KW; ++u) v[u] = fmaf(g[u].x, zc.x, fmaf(g[u].y, zc.y, v[u]));
             };
-            if constexpr (N < 256 && KW >= 8) {
+            if constexpr (N < 256 && (KW >= 8 || N == 128)) {
                 uint32_t wc[NW4];
                 float2 zc;
                 ld_col(0, wc, zc);
