@@ -608,6 +608,43 @@ __global__ __launch_bounds__(256) void k_softmax_rows(const float* __restrict__ 
     for (int i = t; i < len; i += T) gx[base + i] = __expf(x[base + i] * it - st.m) * rs * (gy[base + i] - dot) * it;
 }
 
+// inner == 1, len % 4 == 0, len <= 4 T, 16-byte aligned rows (the routing
+// logits over k): a team of T lanes per row, lane t holding entries
+// 4t .. 4t+3 (one 16-byte load of x and one of gy); the row's max, then its
+// two sums, each reduced across the team with butterfly shuffles -- one
+// exponential per entry.
+template <int T>
+__global__ __launch_bounds__(256) void k_softmax_rows4(const float* __restrict__ x, const float* __restrict__ gy,
+                                                       float* __restrict__ gx, int64_t rows, int len, float it) {
+    const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t row = gid / T;
+    const int t = (int)(gid % T);
+    const bool on = row < rows && 4 * t < len;
+    const int64_t off = on ? row * len + 4 * t : 0;
+    float4 xv = make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY), gv = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (on) {
+        xv = *reinterpret_cast<const float4*>(x + off);
+        gv = *reinterpret_cast<const float4*>(gy + off);
+        xv = make_float4(xv.x * it, xv.y * it, xv.z * it, xv.w * it);
+    }
+    float m = fmaxf(fmaxf(xv.x, xv.y), fmaxf(xv.z, xv.w));
+#pragma unroll
+    for (int o = T / 2; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, T));
+    float4 e = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (on) e = make_float4(__expf(xv.x - m), __expf(xv.y - m), __expf(xv.z - m), __expf(xv.w - m));
+    float sum = (e.x + e.y) + (e.z + e.w);
+    float dt = fmaf(e.x, gv.x, fmaf(e.y, gv.y, fmaf(e.z, gv.z, e.w * gv.w)));
+#pragma unroll
+    for (int o = T / 2; o > 0; o >>= 1) {
+        sum += __shfl_xor(sum, o, T);
+        dt += __shfl_xor(dt, o, T);
+    }
+    if (!on) return;
+    const float rs = 1.f / sum, dot = dt * rs, c = rs * it;
+    *reinterpret_cast<float4*>(gx + off) = make_float4(e.x * c * (gv.x - dot), e.y * c * (gv.y - dot),
+                                                       e.z * c * (gv.z - dot), e.w * c * (gv.w - dot));
+}
+
 // inner > 1 (e.g. down the columns of M[h,k]): a thread per fibre (o, j);
 // neighbouring threads take neighbouring j, so every load is coalesced.
 __global__ __launch_bounds__(256) void k_softmax_cols(const float* __restrict__ x, const float* __restrict__ gy,
@@ -624,6 +661,14 @@ __global__ __launch_bounds__(256) void k_softmax_cols(const float* __restrict__ 
 #pragma unroll 4
     for (int i = 0; i < len; ++i)
         gx[base + i * inner] = __expf(x[base + i * inner] * it - st.m) * rs * (gy[base + i * inner] - dot) * it;
+}
+
+template <int T>
+void softmax_rows4_launch(const float* x, const float* gy, float* gx, int64_t rows, int len, float it,
+                          hipStream_t st) {
+    const int64_t lanes = rows * T;
+    hipLaunchKernelGGL(k_softmax_rows4<T>, dim3((unsigned)((lanes + 255) / 256)), dim3(256), 0, st, x, gy, gx, rows,
+                       len, it);
 }
 
 template <int T>
@@ -658,7 +703,17 @@ hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_
                               float inv_temp, hipStream_t st) {
     const int64_t n = outer * inner;
     if (n == 0) return hipSuccess;
-    if (inner == 1) {
+    const bool al16 = ((reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(gy) |
+                        reinterpret_cast<uintptr_t>(gx)) & 15) == 0;
+    if (inner == 1 && len % 4 == 0 && len <= 256 && al16) {
+        if (len <= 4) softmax_rows4_launch<1>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 8) softmax_rows4_launch<2>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 16) softmax_rows4_launch<4>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 32) softmax_rows4_launch<8>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 64) softmax_rows4_launch<16>(x, gy, gx, outer, len, inv_temp, st);
+        else if (len <= 128) softmax_rows4_launch<32>(x, gy, gx, outer, len, inv_temp, st);
+        else softmax_rows4_launch<64>(x, gy, gx, outer, len, inv_temp, st);
+    } else if (inner == 1) {
         if (len <= 2) softmax_rows_launch<2>(x, gy, gx, outer, len, inv_temp, st);
         else if (len <= 4) softmax_rows_launch<4>(x, gy, gx, outer, len, inv_temp, st);
         else if (len <= 8) softmax_rows_launch<8>(x, gy, gx, outer, len, inv_temp, st);

@@ -192,6 +192,20 @@ def test_softmax_vjp(temp):
                      oracle_softmax_vjp(x.cpu().numpy(), gy.cpu().numpy(), dim, temp))
 
 
+@pytest.mark.parametrize("length", [1, 3, 4, 8, 12, 20, 64, 100, 256, 300])
+def test_softmax_vjp_row_lengths(length):
+    """Contiguous axis: the 16-byte path (length % 4 == 0, up to 256, aligned
+    rows), the general path, and a row view that starts off a 16-byte boundary."""
+    rng = np.random.default_rng(length)
+    x = torch.from_numpy(rng.standard_normal((37, length + 1)).astype(np.float32) * 3).to(DEV)
+    gy = torch.from_numpy(rng.standard_normal((37, length + 1)).astype(np.float32)).to(DEV)
+    for xs, gs in ((x[:, :length].contiguous(), gy[:, :length].contiguous()),
+                   (x.reshape(-1)[1:1 + 37 * length].reshape(37, length),
+                    gy.reshape(-1)[1:1 + 37 * length].reshape(37, length))):
+        got = pdssm.softmax_vjp(xs, gs, 1, 0.7).cpu().numpy()
+        assert_close("len%d" % length, got, oracle_softmax_vjp(xs.cpu().numpy(), gs.cpu().numpy(), 1, 0.7))
+
+
 @pytest.mark.parametrize("wl", [2, 3])
 def test_full_size_sampled(wl):
     """Workload sizes (B16 L2048 H16 N64 K16): q and z on sampled sequences,
