@@ -95,18 +95,31 @@ Sizes sizes_of(const pdssm_desc* d, int C) {
     return s;
 }
 
-// The fused single-read kernels stage one head's dictionary tables in LDS;
-// when they do not fit, the chunked three-pass kernels run instead.
-pdssm::LdsLayout fused_layout(const pdssm_desc* d, int tau, bool fwd) {
-    const int W = fwd ? pdssm::fused_waves(d->N, tau) : pdssm::fused_waves_bwd(d->N, tau);
-    return pdssm::fused_lds_layout(d->N, d->K, W);
-}
-
 // Saved-state rows the forward stages in LDS before writing them out in one
 // burst: stores of chunk states interleaved with the row loads cost far more
 // HBM time than the same bytes written together.  As many rows as the free
-// LDS holds (up to a whole sequence), at least 16, else none.
+// LDS holds (up to a whole sequence), at least kMinStaging, else none.
 constexpr int kMinStaging = 16;
+
+// Chunk waves of the fused forward: the wide count for the 4-byte row
+// formats (their forward waits on its chunk passes, not on HBM) when the
+// prefetching kernel runs and its tables leave room for the minimum
+// saved-state staging.  Complex64 rows keep 7 (measured 3% faster at
+// fsa-perm, where the forward is HBM-bound).
+int fwd_waves(const pdssm_desc* d, int tau) {
+    if ((d->flags & (PDSSM_FLAG_BF16_IO | PDSSM_FLAG_REAL_IO)) && pdssm::fused_prefetch(d->N, tau) &&
+        pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWavesWide).total + (size_t)kMinStaging * d->N * 8 <=
+            pdssm::kMaxLds)
+        return pdssm::kFusedWavesWide;
+    return pdssm::fused_waves(d->N, tau);
+}
+
+// The fused single-read kernels stage one head's dictionary tables in LDS;
+// when they do not fit, the chunked three-pass kernels run instead.
+pdssm::LdsLayout fused_layout(const pdssm_desc* d, int tau, bool fwd) {
+    const int W = fwd ? fwd_waves(d, tau) : pdssm::fused_waves_bwd(d->N, tau);
+    return pdssm::fused_lds_layout(d->N, d->K, W);
+}
 
 int staging_rows(const pdssm_desc* d, const pdssm::LdsLayout& l, int C) {
     if (l.total >= pdssm::kMaxLds) return 0;
@@ -209,6 +222,7 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     f.dict = pa.dict;
     f.rec = pa.rec;
     f.mtab = pa.mtab;
+    f.W = fwd ? fwd_waves(d, f.tau) : pdssm::fused_waves_bwd(d->N, f.tau);
     f.lds = fused_layout(d, f.tau, fwd);
     f.sbM = fwd ? staging_rows(d, f.lds, f.C) : 0;
     f.lds = pdssm::fused_lds_add_staging(f.lds, d->N, f.sbM);

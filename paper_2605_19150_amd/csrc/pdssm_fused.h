@@ -25,6 +25,11 @@ constexpr int kFusedWaves = 7;
 constexpr bool fused_prefetch(int N, int tau) { return tau * (N > 64 ? N / 64 : 1) <= PDSSM_PF_MAX_ROWS; }
 constexpr int fused_waves(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_PF_WAVES : kFusedWaves; }
 constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? PDSSM_BWD_PF_WAVES : kFusedWaves; }
+// The prefetching forward also comes with 11 chunk waves (12 with the
+// frontier, three per SIMD), used for the 4-byte row formats when the head's
+// tables leave LDS room for them: more waves in flight hide the chunk
+// passes' LDS round trips (the backward measured faster with 8).
+constexpr int kFusedWavesWide = 11;
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
@@ -118,6 +123,9 @@ struct FusedArgs {
     float2* segA;
     float2* segD;
     int* segP;
+    // Chunk waves of the forward (fused_waves or kFusedWavesWide); the
+    // backward's count follows from N and tau.
+    int W;
     // Format of D, b, c and dD, db, dc (kIoC64, kIoBf16 pairs or kIoReal
     // fp32, 4 bytes per entry for the last two: the pointers above are then
     // reinterpreted); everything else keeps its complex64 / fp32 type.

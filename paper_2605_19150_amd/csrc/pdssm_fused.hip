@@ -1412,21 +1412,30 @@ hipError_t prep_launch(const PrepArgs& p, hipStream_t st) {
 
 // Chunk lengths compiled per N: TAU * max(1, N/64) <= 16 keeps a chunk's
 // D, b, c rows (and the backward's recomputed states) in registers.
+// The forward's chunk-wave count: fused_waves(N, TAU), or kFusedWavesWide
+// for the prefetching kernels when the caller's layout was built for it.
+template <int N, int TAU>
+hipError_t fwd_dispatch_waves(const FusedArgs& a, hipStream_t st) {
+    if constexpr (fused_prefetch(N, TAU)) {
+        if (a.W == kFusedWavesWide) return fwd_launch<N, TAU, kFusedWavesWide>(a, st);
+    }
+    if (a.W != fused_waves(N, TAU)) return hipErrorInvalidValue;
+    return fwd_launch<N, TAU, fused_waves(N, TAU)>(a, st);
+}
+
 template <int N, bool FWD>
 hipError_t dispatch_tau(const FusedArgs& a, hipStream_t st) {
     constexpr int SL = Lay<N>::SL;
     switch (a.tau) {
         case 4:
-            return FWD ? fwd_launch<N, 4, fused_waves(N, 4)>(a, st) : bwd_launch<N, 4, fused_waves_bwd(N, 4)>(a, st);
+            return FWD ? fwd_dispatch_waves<N, 4>(a, st) : bwd_launch<N, 4, fused_waves_bwd(N, 4)>(a, st);
         case 8:
             if constexpr (8 * SL <= 16)
-                return FWD ? fwd_launch<N, 8, fused_waves(N, 8)>(a, st)
-                           : bwd_launch<N, 8, fused_waves_bwd(N, 8)>(a, st);
+                return FWD ? fwd_dispatch_waves<N, 8>(a, st) : bwd_launch<N, 8, fused_waves_bwd(N, 8)>(a, st);
             break;
         case 16:
             if constexpr (16 * SL <= 16)
-                return FWD ? fwd_launch<N, 16, fused_waves(N, 16)>(a, st)
-                           : bwd_launch<N, 16, fused_waves_bwd(N, 16)>(a, st);
+                return FWD ? fwd_dispatch_waves<N, 16>(a, st) : bwd_launch<N, 16, fused_waves_bwd(N, 16)>(a, st);
             break;
         default: break;
     }
