@@ -161,6 +161,56 @@ def test_split_invariance_through_h0():
     assert_close("h_final split", h2.cpu().numpy(), rhf)
 
 
+@pytest.mark.parametrize("N,pi_kind", [(64, "perm"), (64, "uniform"), (128, "uniform")])
+def test_segment_protocol_from_entry_points(N, pi_kind):
+    """The sequence-sharded scan, run on one GPU with three segments as if each
+    were another device: a segment's aggregate is pdssm_compose_chunks over the
+    whole segment (map, diagonal) plus its scan from zero (local state); an
+    aggregate is applied to the incoming state by a one-step scan whose
+    dictionary holds each sequence's composed map (idx[b] = b); every segment
+    then scans from its composed entering state.  Outputs match the oracle's
+    scan of the whole sequence."""
+    B, H, K = 3, 2, 5
+    cuts = [0, 41, 90, 157]
+    inp = make_inputs(B=B, L=cuts[-1], H=H, N=N, K=K, seed=N + len(pi_kind), pi_kind=pi_kind, with_h0=True)
+    T = to_dev(inp)
+    sl = lambda k, a, b: T[k][:, a:b].contiguous()  # noqa: E731
+    seg = [tuple(sl(k, cuts[g], cuts[g + 1]) for k in ("idx", "D", "b", "c")) for g in range(3)]
+
+    def aggregate(g):
+        idx, D, b, c = seg[g]
+        pm, dm = pdssm.compose_chunks(idx, T["pi"], D, idx.shape[1])
+        _, local, _ = pdssm.scan_fwd(idx, T["pi"], D, b, c)
+        return pm[:, :, 0], dm[:, :, 0], local.clone()
+
+    def apply(agg, carry):
+        pm, dm, local = agg
+        idx1 = torch.arange(B, dtype=torch.int32, device=DEV).view(B, 1, 1).expand(B, 1, H).contiguous()
+        pi1 = pm.permute(1, 0, 2).contiguous()  # [H, K = B, N]
+        zero = torch.zeros((B, 1, H, N), dtype=torch.complex64, device=DEV)
+        _, hf, _ = pdssm.scan_fwd(idx1, pi1, dm.unsqueeze(1).contiguous(), local.unsqueeze(1).contiguous(), zero,
+                                  h0=carry)
+        return hf.clone()
+
+    aggs = [None] + [aggregate(g) for g in (1, 2)]  # computed independently of segment 0
+    carry = [T["h0"]]
+    run = lambda parts, h0: pdssm.scan_fwd(parts[0], T["pi"], *parts[1:], h0=h0)  # noqa: E731
+    _, h1, _ = run(seg[0], T["h0"])
+    carry.append(h1.clone())
+    carry.append(apply(aggs[1], carry[1]))
+    ys, hfin = [], None
+    for g in range(3):
+        y, hf, _ = run(seg[g], carry[g])
+        ys.append(y.clone())
+        hfin = hf.clone()
+    # the composed entering state of segment 2 equals the state the scan reaches there
+    _, h_two, _ = run([torch.cat([seg[0][i], seg[1][i]], 1) for i in range(4)], T["h0"])
+    assert_close("carry 2", carry[2].cpu().numpy(), h_two.cpu().numpy())
+    ry, rhf, _ = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp["h0"])
+    assert_close("y by segments", torch.cat(ys, 1).cpu().numpy(), ry)
+    assert_close("h_final by segments", hfin.cpu().numpy(), rhf)
+
+
 def test_deterministic():
     inp = make_inputs(B=2, L=300, H=4, N=128, K=8, seed=5, with_dhf=True)
     a = run_gpu(inp)
