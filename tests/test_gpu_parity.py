@@ -161,6 +161,30 @@ def test_split_invariance_through_h0():
     assert_close("h_final split", h2.cpu().numpy(), rhf)
 
 
+@pytest.mark.parametrize("N", [64, 128])
+def test_split_invariance_backward_through_dh_final(N):
+    """Two calls chained backwards: the second segment's dh0 is the first
+    segment's dh_final; the gradients match one backward over the whole
+    sequence (the oracle's)."""
+    L, L1 = 133, 58
+    inp = make_inputs(B=2, L=L, H=2, N=N, K=4, seed=31 + N, with_h0=True, with_dhf=True)
+    T = to_dev(inp)
+    sl = lambda k, a, b: T[k][:, a:b].contiguous()  # noqa: E731
+    parts = [tuple(sl(k, a, b) for k in ("idx", "D", "b", "c", "dy")) for a, b in ((0, L1), (L1, L))]
+    _, h1, s1 = pdssm.scan_fwd(parts[0][0], T["pi"], *parts[0][1:4], h0=T["h0"])
+    h1, s1 = h1.clone(), s1.clone()
+    _, _, s2 = pdssm.scan_fwd(parts[1][0], T["pi"], *parts[1][1:4], h0=h1)
+    g2 = [t.clone() for t in pdssm.scan_bwd(parts[1][0], T["pi"], *parts[1][1:4], s2.clone(), parts[1][4],
+                                            dh_final=T["dh_final"])]
+    g1 = [t.clone() for t in pdssm.scan_bwd(parts[0][0], T["pi"], *parts[0][1:4], s1, parts[0][4],
+                                            dh_final=g2[3])]
+    rg = oracle_bwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"],
+                    dh_final=inp["dh_final"])
+    for i, name in enumerate(("dD", "db", "dc")):
+        assert_close(name + " split", torch.cat([g1[i], g2[i]], 1).cpu().numpy(), rg[i])
+    assert_close("dh0 split", g1[3].cpu().numpy(), rg[3])
+
+
 @pytest.mark.parametrize("N,pi_kind", [(64, "perm"), (64, "uniform"), (128, "uniform")])
 def test_segment_protocol_from_entry_points(N, pi_kind):
     """The sequence-sharded scan, run on one GPU with three segments as if each
