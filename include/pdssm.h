@@ -86,21 +86,21 @@ typedef struct pdssm_desc {
  * the scan reuses them instead of rebuilding them. */
 #define PDSSM_FLAG_PREPARED 1u
 
-/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd (and pdssm_prepare,
- * which ignores it): D, b, c and dD, db, dc are bf16 (re, im) pairs, 4 bytes
+/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd / pdssm_decode_step (and
+ * pdssm_prepare, which ignores it): D, b, c and dD, db, dc are bf16 (re, im) pairs, 4 bytes
  * per complex entry (real part in the low 16 bits; torch:
  * view_as_real(x).to(bfloat16)), the paper's bf16 input setting (App. E,
  * kernel efficiency: the complex inputs split into two bf16 halves, fp32
  * arithmetic).  Every other tensor (idx, pi, h0, h_final, saved, y, dy,
  * dh_final, dh0) keeps its type.  The arithmetic is fp32 as without the
  * flag: inputs widen exactly, gradients are rounded to nearest (ties to
- * even) when stored.  Only the single-read kernels support it
- * (pdssm_uses_fused(desc) == 1); other entry points and the multi-pass
- * kernels return PDSSM_ERR_UNSUPPORTED, as does pdssm_scan_bwd_ste. */
+ * even) when stored.  The scans support it on the single-read kernels only
+ * (pdssm_uses_fused(desc) == 1); the multi-pass kernels, pdssm_compose_chunks,
+ * pdssm_scan_bwd_ste and pdssm_ste_grads return PDSSM_ERR_UNSUPPORTED. */
 #define PDSSM_FLAG_BF16_IO 2u
 
-/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd (and pdssm_prepare,
- * which ignores it): the real-valued model (App. B, the MAD and time-series
+/* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd / pdssm_decode_step (and
+ * pdssm_prepare, which ignores it): the real-valued model (App. B, the MAD and time-series
  * setups use it): D, b, c and dD, db, dc are real fp32 [B,L,H,N], 4 bytes per
  * entry, the recurrence h_t = P_t (D_t .* h_{t-1}) + b_t over the reals and
  * y_t = sum_n c_t[n] h_t[n].  Every other tensor keeps its type: h0, h_final,
@@ -303,6 +303,10 @@ int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer,
  *      h_in [B,H,N] complex (NULL = zero state).
  * Out: h_out [B,H,N] complex (may be the same buffer as h_in: in-place
  *      update), y [B,H] float32.  Needs no workspace.
+ * With PDSSM_FLAG_BF16_IO or PDSSM_FLAG_REAL_IO in desc->flags, D, b, c are
+ * bf16 (re, im) pairs or real fp32 (4 bytes per entry) as for the scans;
+ * h_in, h_out stay complex64 and the arithmetic is the same fp32 (the
+ * results equal a complex64 call on the widened values bit for bit).
  */
 int pdssm_decode_step(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
                       const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,

@@ -525,16 +525,15 @@ int pdssm_decode_step(const pdssm_desc* d, const int32_t* idx, const int32_t* pi
                       int* dev_status, void* stream) {
     const int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (narrow_io(d)) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !pi || !D || !b || !c || !h_out || !y) return PDSSM_ERR_INVALID_ARG;
     for (const void* p : {(const void*)pi, (const void*)D, (const void*)b, (const void*)c, (const void*)h_in,
                           (const void*)h_out})
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
-    const size_t nseq = (size_t)d->B * d->H, nrow = nseq * d->N * 8;
+    const size_t nseq = (size_t)d->B * d->H, nrow = nseq * d->N * 8, nio = nseq * d->N * io_bytes(d);
     const size_t npi = (size_t)d->H * d->K * d->N * 4;
     // the state may be updated in place (h_out == h_in); no other overlap
     if (any_overlap({{h_out, nrow}, {y, nseq * 4}},
-                    {{idx, nseq * 4}, {pi, npi}, {D, nrow}, {b, nrow}, {c, nrow}, {h_in == h_out ? nullptr : h_in, nrow}}))
+                    {{idx, nseq * 4}, {pi, npi}, {D, nio}, {b, nio}, {c, nio}, {h_in == h_out ? nullptr : h_in, nrow}}))
         return PDSSM_ERR_INVALID_ARG;
     pdssm::DecodeArgs a = {};
     a.B = d->B;
@@ -543,9 +542,10 @@ int pdssm_decode_step(const pdssm_desc* d, const int32_t* idx, const int32_t* pi
     a.K = d->K;
     a.idx = idx;
     a.pi = pi;
-    a.D = reinterpret_cast<const float2*>(D);
-    a.b = reinterpret_cast<const float2*>(b);
-    a.c = reinterpret_cast<const float2*>(c);
+    a.io = io_format(d);
+    a.D = D;
+    a.b = b;
+    a.c = c;
     a.h_in = reinterpret_cast<const float2*>(h_in);
     a.h_out = reinterpret_cast<float2*>(h_out);
     a.y = y;

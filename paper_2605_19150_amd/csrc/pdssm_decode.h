@@ -8,11 +8,12 @@ namespace pdssm {
 // One recurrence step per (batch, head) sequence (token-by-token decode).
 struct DecodeArgs {
     int B, H, N, K;
+    int io;              // row format of D, b, c (kIoC64, kIoBf16, kIoReal: pdssm_io.h)
     const int* idx;      // [B,H]
     const int* pi;       // [H,K,N]
-    const float2* D;     // [B,H,N]
-    const float2* b;
-    const float2* c;
+    const void* D;       // [B,H,N] in the row format
+    const void* b;
+    const void* c;
     const float2* h_in;  // [B,H,N] or null (zero state)
     float2* h_out;       // [B,H,N], may equal h_in
     float* y;            // [B,H]

@@ -5,6 +5,10 @@
 //   h'[r] = b[r] + sum_{j: pi(j) = r} D[j] h[j],   y = Re sum_n c[n] h'[n],
 //   pi = pi[h, idx[b,h], :].
 //
+// The rows D, b, c come as complex64, bf16 (re, im) pairs or real fp32 (the
+// real-valued model), widened to complex in registers as the scan kernels
+// do; the state h stays complex64.
+//
 // One wave (one workgroup) per (batch, head) sequence; lane l owns entries
 // l*SL .. l*SL+SL-1.  The scaled sources D[j] h[j] and the map are staged in
 // LDS; each destination then adds its sources in ascending source order (a
@@ -20,7 +24,21 @@ namespace {
 
 constexpr int kDecodeWaves = 1;  // one wave per workgroup: B*H workgroups spread over the CUs
 
-template <int N>
+// This lane's SL entries of row `row` (entries) of a [.., N] tensor in row format IO.
+template <int SL, int IO>
+__device__ __forceinline__ CV<SL> ld_row_io(const void* base, size_t row, int lane) {
+    if constexpr (IO == kIoC64) {
+        return ld_cv<SL>(static_cast<const float2*>(base) + row, lane);
+    } else {
+        const uint32_t* p = static_cast<const uint32_t*>(base) + row + (size_t)lane * SL;
+        CV<SL> out;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) out.v[s] = word_to_f2<IO>(p[s]);
+        return out;
+    }
+}
+
+template <int N, int IO>
 __global__ __launch_bounds__(kDecodeWaves * 64) void k_decode(DecodeArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 vs[kDecodeWaves][N];
@@ -39,9 +57,9 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void k_decode(DecodeArgs a) {
     CV<SL> h = cv_zero<SL>(), D = cv_zero<SL>(), b = cv_zero<SL>(), c = cv_zero<SL>();
     if (act) {
         h = a.h_in ? ld_cv<SL>(a.h_in + row, lane) : cv_zero<SL>();
-        D = ld_cv<SL>(a.D + row, lane);
-        b = ld_cv<SL>(a.b + row, lane);
-        c = ld_cv<SL>(a.c + row, lane);
+        D = ld_row_io<SL, IO>(a.D, row, lane);
+        b = ld_row_io<SL, IO>(a.b, row, lane);
+        c = ld_row_io<SL, IO>(a.c, row, lane);
     }
     int k = a.idx[seq];
     bool bad = (unsigned)k >= (unsigned)a.K;
@@ -78,12 +96,22 @@ __global__ __launch_bounds__(kDecodeWaves * 64) void k_decode(DecodeArgs a) {
     if (bad) report_index_error(a.status);
 }
 
+template <int N, int IO>
+hipError_t decode_launch_io(const DecodeArgs& a, hipStream_t st) {
+    const int nseq = a.B * a.H;
+    auto kern = k_decode<N, IO>;
+    hipLaunchKernelGGL(kern, dim3((nseq + kDecodeWaves - 1) / kDecodeWaves), dim3(kDecodeWaves * 64), 0, st, a);
+    return hipGetLastError();
+}
+
 template <int N>
 hipError_t decode_launch(const DecodeArgs& a, hipStream_t st) {
-    const int nseq = a.B * a.H;
-    hipLaunchKernelGGL(k_decode<N>, dim3((nseq + kDecodeWaves - 1) / kDecodeWaves), dim3(kDecodeWaves * 64), 0, st,
-                       a);
-    return hipGetLastError();
+    switch (a.io) {
+        case kIoC64: return decode_launch_io<N, kIoC64>(a, st);
+        case kIoBf16: return decode_launch_io<N, kIoBf16>(a, st);
+        case kIoReal: return decode_launch_io<N, kIoReal>(a, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace

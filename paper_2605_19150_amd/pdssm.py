@@ -416,7 +416,8 @@ def surrogate_grads(q, G, logits, M, temp, stream=None):
 
 def decode_step(idx, pi, D, b, c, h=None, out=None, y=None, stream=None, check=True):
     """One recurrence step per sequence: returns (h_new [B,H,N] c64, y [B,H] f32).
-    idx [B,H] int32; D, b, c [B,H,N] c64; h [B,H,N] c64 or None (zero state).
+    idx [B,H] int32; D, b, c [B,H,N] c64 (or [B,H,N,2] bf16 pairs, or [B,H,N]
+    float32 for the real-valued model); h [B,H,N] c64 or None (zero state).
     out may be h itself (in-place update)."""
     B, H = idx.shape
     H2, K, N = pi.shape
@@ -426,13 +427,19 @@ def decode_step(idx, pi, D, b, c, h=None, out=None, y=None, stream=None, check=T
     _need(idx, "idx", torch.int32, (B, H), dev)
     _need(pi, "pi", torch.int32, (H, K, N), dev)
     for t, n in ((D, "D"), (b, "b"), (c, "c")):
-        _need(t, n, torch.complex64, (B, H, N), dev)
+        if is_bf16_io(D):
+            _need(t, n, torch.bfloat16, (B, H, N, 2), dev)
+        elif is_real_io(D):
+            _need(t, n, torch.float32, (B, H, N), dev)
+        else:
+            _need(t, n, torch.complex64, (B, H, N), dev)
     if h is not None:
         _need(h, "h", torch.complex64, (B, H, N), dev)
     out = torch.empty((B, H, N), dtype=torch.complex64, device=dev) if out is None else out
     y = torch.empty((B, H), dtype=torch.float32, device=dev) if y is None else y
     status = torch.zeros(1, dtype=torch.int32, device=dev) if check else None
     d = desc(B, 1, H, N, K)
+    d.flags = (FLAG_BF16_IO if is_bf16_io(D) else 0) | (FLAG_REAL_IO if is_real_io(D) else 0)
     st = load().pdssm_decode_step(ctypes.byref(d), _p(idx), _p(pi), _p(D), _p(b), _p(c), _p(h), _p(out), _p(y),
                                   _p(status), _stream(stream))
     if st != OK:

@@ -96,14 +96,13 @@ def test_flags_known_bits_only(lib):
 def test_narrow_io_only_where_supported(lib, flag):
     f = FakeBufs()
     P = lambda n: f(n)  # noqa: E731
-    # composition, decode and the straight-through calls take complex64 only
+    # composition and the straight-through calls take complex64 only (the
+    # scans and the decode step take both 4-byte formats)
     d = pdssm.desc(2, 40, 2, 64, 4)
     d.flags = getattr(pdssm, flag)
     st = 2 * 40 * 2 * 64 * 8
     assert lib.pdssm_compose_chunks(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), None,
                                     None) == pdssm.ERR_UNSUPPORTED
-    assert lib.pdssm_decode_step(ctypes.byref(d), P(64), P(2048), P(st), P(st), P(st), None, P(st), P(64),
-                                 None, None) == pdssm.ERR_UNSUPPORTED
     assert lib.pdssm_ste_grads(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), P(st), P(1 << 20),
                                1 << 20, None, None) == pdssm.ERR_UNSUPPORTED
     need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)

@@ -42,6 +42,35 @@ def test_one_step_matches_oracle(N, pi_kind):
     assert_close("h", h.cpu().numpy(), rh)
 
 
+@pytest.mark.parametrize("N", [8, 64, 128, 256])
+@pytest.mark.parametrize("fmt", ["real", "bf16"])
+def test_row_formats(N, fmt):
+    """D, b, c as real fp32 rows (the real-valued model) or bf16 pairs: bit
+    for bit the complex64 step on the widened values, and the oracle on them."""
+    print("decode %s N=%d" % (fmt, N), flush=True)
+    inp = make_inputs(3, 1, 5, N, 7, seed=N + 11, with_h0=True, real=(fmt == "real"))
+    s = step_inputs(inp, 0)
+    if fmt == "real":
+        rows = {k: dev(s[k]) for k in ("D", "b", "c")}
+        exact = {k: s[k].astype(np.complex128) for k in ("D", "b", "c")}
+    else:
+        rows, exact = {}, {}
+        for k in ("D", "b", "c"):
+            t = torch.view_as_real(torch.from_numpy(s[k])).to(torch.bfloat16)
+            rows[k] = t.contiguous().to(DEV)
+            f = t.to(torch.float64).numpy()
+            exact[k] = f[..., 0] + 1j * f[..., 1]
+    wide = {k: dev(exact[k].astype(np.complex64)) for k in ("D", "b", "c")}
+    idx, pi, h0 = dev(s["idx"]), dev(inp["pi"]), dev(inp["h0"])
+    h, y = pdssm.decode_step(idx, pi, rows["D"], rows["b"], rows["c"], h=h0)
+    hw, yw = pdssm.decode_step(idx, pi, wide["D"], wide["b"], wide["c"], h=h0)
+    assert torch.equal(h, hw) and torch.equal(y, yw)
+    full = {k: exact[k][:, None] for k in ("D", "b", "c")}
+    ry, rh, _ = oracle_fwd(inp["idx"], inp["pi"], full["D"], full["b"], full["c"], h0=inp["h0"])
+    assert_close("y", y.cpu().numpy(), ry[:, 0])
+    assert_close("h", h.cpu().numpy(), rh)
+
+
 def test_zero_state_and_all_to_one_map():
     N, K = 64, 3
     inp = make_inputs(2, 1, 4, N, K, seed=3)
