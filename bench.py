@@ -65,18 +65,20 @@ def alg_bytes(w, C, op, esz=8, ssz=8):
     return steps * 8 + 3 * su * esz + dict_b + B * H * C * N * ssz + 3 * su * esz + B * H * N * ssz
 
 
-def ste_bytes(w, C):
-    """Algorithmic bytes and flops of the straight-through calls."""
+def ste_bytes(w, C, real=False):
+    """Algorithmic bytes and flops of the straight-through calls (real: the
+    real-valued model, 4-byte rows and real states)."""
     B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
     steps = B * L * H
     su = steps * N
+    esz = 4 if real else 8
     return {
-        # the plain backward, plus z [B,L,H,N] c64 written
-        "bwd_ste": alg_bytes(w, C, "bwd") + su * 8,
+        # the plain backward, plus z [B,L,H,N] written
+        "bwd_ste": alg_bytes(w, C, "bwd", esz, esz) + su * esz,
         # idx, pi, g (= db) and z read once, q [B,L,H,K] and G [H,K,N,N] f32 written once
-        "ste_grads": steps * 4 + H * K * N * 4 + 2 * su * 8 + steps * K * 4 + H * K * N * N * 4,
-        # per step and (i, j): Re(g_i conj z_j) = two real multiply-adds
-        "ste_grads_flops": 4 * steps * N * N,
+        "ste_grads": steps * 4 + H * K * N * 4 + 2 * su * esz + steps * K * 4 + H * K * N * N * 4,
+        # per step and (i, j): Re(g_i conj z_j) = two real multiply-adds (one when real)
+        "ste_grads_flops": (2 if real else 4) * steps * N * N,
         # logits and q in, d logits out; M and G in, dM out
         "softmax": 3 * steps * K * 4 + 3 * H * K * N * N * 4,
     }
@@ -302,8 +304,8 @@ def main():
         return
     print("bench: workload %d (%s): generating inputs" % (args.workload, w.name), file=sys.stderr,
           flush=True)
-    if args.real and (args.ste or args.bf16):
-        sys.exit("bench.py: --real combines with neither --ste nor --bf16")
+    if args.real and args.bf16:
+        sys.exit("bench.py: --real and --bf16 do not combine (one row format at a time)")
     inp = workload_inputs(args.workload, seed=0, real=args.real)
     T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
     if args.bf16:
@@ -412,14 +414,14 @@ def main():
         "device": torch.cuda.get_device_name(dev),
     }
     if args.ste:
-        sb = ste_bytes(w, s.C)
+        sb = ste_bytes(w, s.C, real=args.real)
         out["bwd"]["alg_bytes"] = sb["bwd_ste"]
         out["bwd"]["kernel"] = kern["bwd"] + " (+ z)"
         out["bwd"]["alg_GBps"] = sb["bwd_ste"] / (bwd_ms * 1e-3) / 1e9
         out["bwd"]["frac"] = out["bwd"]["alg_GBps"] / HBM_PEAK_GBS
         out["roofline"]["achieved"] = out["bwd"]["alg_GBps"] if dom == "bwd" else achieved
         out["roofline"]["frac"] = out["roofline"]["achieved"] / HBM_PEAK_GBS
-        out["roofline"]["traffic"] = traffic_from_profiles("k_bwd_fused_ste", w.name) if fused else None
+        out["roofline"]["traffic"] = traffic_from_profiles("k_bwd_fused_ste" + suffix, w.name) if fused else None
         out["roofline"]["kernel"] = kern[dom] + (" (+ z)" if dom == "bwd" else "")
         dg_ms = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
         sm_ms = float(np.mean([e[4].elapsed_time(e[5]) for e in evs]))
@@ -430,7 +432,7 @@ def main():
             "ste_grads": {"ms": dg_ms, "alg_bytes": sb["ste_grads"], "alg_GBps": gbps,
                           "frac_hbm": gbps / HBM_PEAK_GBS, "flops": sb["ste_grads_flops"],
                           "TFLOPs": tfs, "frac_mfma_fp32": tfs / MFMA_FP32_PEAK_TFS,
-                          "traffic": traffic_from_profiles("k_ste_gemm", w.name)},
+                          "traffic": traffic_from_profiles("k_ste_gemm" + suffix, w.name)},
             "softmax_vjp": {"ms": sm_ms, "alg_bytes": sb["softmax"],
                             "alg_GBps": sb["softmax"] / (sm_ms * 1e-3) / 1e9},
         }

@@ -96,7 +96,8 @@ typedef struct pdssm_desc {
  * flag: inputs widen exactly, gradients are rounded to nearest (ties to
  * even) when stored.  The scans support it on the single-read kernels only
  * (pdssm_uses_fused(desc) == 1); the multi-pass kernels, pdssm_compose_chunks,
- * pdssm_scan_bwd_ste and pdssm_ste_grads return PDSSM_ERR_UNSUPPORTED. */
+ * pdssm_scan_bwd_ste and pdssm_ste_grads return PDSSM_ERR_UNSUPPORTED (z in
+ * bf16 would round the straight-through inputs). */
 #define PDSSM_FLAG_BF16_IO 2u
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd / pdssm_decode_step (and
@@ -108,9 +109,11 @@ typedef struct pdssm_desc {
  * hold real values (imaginary parts 0, or NULL) and h_final, dh0 then come
  * out with imaginary parts 0.  The arithmetic is the complex64 one on rows
  * whose imaginary parts are 0, so every result equals, bit for bit, the real
- * part of a complex64 call on the same values.  Cannot
- * be combined with PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG); the same
- * entry points as PDSSM_FLAG_BF16_IO support it, the others return
+ * part of a complex64 call on the same values.  Cannot be combined with
+ * PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG).  The scans (single-read kernels
+ * only), pdssm_decode_step, and the straight-through pair
+ * pdssm_scan_bwd_ste / pdssm_ste_grads support it (z, g real fp32 rows);
+ * the multi-pass kernels and pdssm_compose_chunks return
  * PDSSM_ERR_UNSUPPORTED. */
 #define PDSSM_FLAG_REAL_IO 4u
 
@@ -217,7 +220,9 @@ int pdssm_scan_bwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi
  * writes z [B,L,H,N] complex (required): z_t = D_t .* h_{t-1} (h_{-1} = h0),
  * the state entering the map of step t, which pdssm_ste_grads needs together
  * with db (the gradient g_t reaching h_t).  Same workspace as pdssm_scan_bwd
- * (PDSSM_OP_BWD).  z must not overlap any other argument.
+ * (PDSSM_OP_BWD).  z must not overlap any other argument.  With
+ * PDSSM_FLAG_REAL_IO z is a real fp32 row like db (PDSSM_FLAG_BF16_IO:
+ * PDSSM_ERR_UNSUPPORTED).
  */
 int pdssm_scan_bwd_ste(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
                        const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
@@ -242,8 +247,10 @@ int pdssm_scan_bwd_ste(const pdssm_desc* desc, const int32_t* idx, const int32_t
  *       gradient.  Maps no step chose get zeros.
  * At least one of q, G.  The steps are grouped by map (a stable counting
  * sort) and every sum runs in a fixed order (deterministic results).
- * In:  idx [B,L,H], pi [H,K,N] (needed for q), g, z [B,L,H,N]; desc->chunk
- *      is ignored.
+ * In:  idx [B,L,H], pi [H,K,N] (needed for q), g, z [B,L,H,N] complex64, or
+ *      real fp32 with PDSSM_FLAG_REAL_IO (the real-valued model: Re(g conj z)
+ *      is then g z); desc->chunk is ignored; PDSSM_FLAG_BF16_IO gives
+ *      PDSSM_ERR_UNSUPPORTED.
  * ws:  at least pdssm_workspace_size(desc, PDSSM_OP_STE_GRADS) bytes, 256-byte
  *      aligned.  An idx entry outside [0,K) counts as map 0 and is reported
  *      through *dev_status; a pi entry outside [0,N) reads row 0.

@@ -427,10 +427,12 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (misaligned(z)) return PDSSM_ERR_INVALID_ARG;
-    // 4-byte formats: single-read kernels only; the straight-through path reads db as complex64
-    if (narrow_io(d) && (!use_fused(d) || z)) return PDSSM_ERR_UNSUPPORTED;
+    // 4-byte formats: single-read kernels only; z in bf16 pairs would round the
+    // straight-through inputs, so that pair is not offered
+    if (narrow_io(d) && !use_fused(d)) return PDSSM_ERR_UNSUPPORTED;
+    if (z && io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
-    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, s.stepN * 8}, {ws, need}},
+    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, nst}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * 8},
                      {dy, nidx}, {dh_final, s.seqN * 8}}))
         return PDSSM_ERR_INVALID_ARG;
@@ -490,7 +492,7 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
                     void* stream) {
     const int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (narrow_io(d)) return PDSSM_ERR_UNSUPPORTED;
+    if (io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !g || !z || (!q && !G) || (q && !pi)) return PDSSM_ERR_INVALID_ARG;
     if (misaligned(g) || misaligned(z) || misaligned(pi) || (reinterpret_cast<uintptr_t>(G) & 3) != 0 ||
         (reinterpret_cast<uintptr_t>(q) & 3) != 0)
@@ -498,7 +500,7 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
     const pdssm::DictPlan plan = pdssm::dict_plan(d->B, d->L, d->H, d->N, d->K);
     if (!ws || ws_bytes < plan.bytes || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
-    const size_t nidx = (size_t)d->B * d->L * d->H * 4, nst = nidx / 4 * d->N * 8;
+    const size_t nidx = (size_t)d->B * d->L * d->H * 4, nst = nidx / 4 * d->N * io_bytes(d);
     const size_t nG = (size_t)d->H * d->K * d->N * d->N * 4, npi = (size_t)d->H * d->K * d->N * 4;
     if (any_overlap({{G, nG}, {q, nidx * d->K}, {ws, plan.bytes}}, {{idx, nidx}, {g, nst}, {z, nst}, {pi, npi}}))
         return PDSSM_ERR_INVALID_ARG;
@@ -510,6 +512,7 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
     a.K = d->K;
     a.idx = idx;
     a.pi = pi;
+    a.io = io_format(d);
     a.g = reinterpret_cast<const float2*>(g);
     a.z = reinterpret_cast<const float2*>(z);
     a.q = q;

@@ -131,7 +131,8 @@ struct FusedArgs {
     // reinterpreted); everything else keeps its complex64 / fp32 type.
     int io;
     // Backward only, optional: the scaled states z = D_t .* h_{t-1}
-    // [B,L,H,N] that the straight-through gradients need (Sec. 3.1 Prop. 2).
+    // [B,L,H,N] that the straight-through gradients need (Sec. 3.1 Prop. 2),
+    // in the row format of the gradients.
     float2* z;
 };
 

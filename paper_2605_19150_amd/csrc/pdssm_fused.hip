@@ -1245,7 +1245,8 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
                 CV<SL> zt;
 #pragma unroll
                 for (int i = 0; i < SL; ++i) zt.v[i] = cmul(Dt(q, t).v[i], Hs[t].v[i]);
-                st_out<SL>(a.z + off, lane, zt);
+                if constexpr (IO != kIoC64) st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.z) + off, lane, zt);
+                else st_out<SL>(a.z + off, lane, zt);
             }
         }
     }

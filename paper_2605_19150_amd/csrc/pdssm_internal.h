@@ -101,6 +101,7 @@ struct SteGradArgs {
     int B, L, H, N, K;
     const int* idx;    // [B,L,H]
     const int* pi;     // [H,K,N] (scores only)
+    int io;            // row format of g and z: kIoC64 or kIoReal (real fp32, pdssm_io.h)
     const float2* g;   // [B,L,H,N] gradient reaching h_t (db of the backward)
     const float2* z;   // [B,L,H,N] D_t .* h_{t-1}
     float* q;          // [B,L,H,K] scores of every map, or null

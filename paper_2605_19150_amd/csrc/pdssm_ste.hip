@@ -230,17 +230,25 @@ size_t ste_gemm_lds(int K, bool q) {
 // only reaches rows and columns of the tile past N, never stored).  The loads
 // are unconditional (u is always a valid step) so that the compiler's wait
 // counts stay exact and the loads of later batches stay in flight.
-template <int N>
+// Real rows (the real-valued model) widen to (x, 0).
+template <int N, int IO>
 __device__ __forceinline__ void load_step(const SteGradArgs& a, int u, int h, int i0, int j0, int lane,
                                           float2& gv, float2& zv) {
     constexpr int NB = DictCfg<N>::NB;
     const int r = NB == 64 ? lane : min(lane & 31, N - 1);
-    typedef float f32x2 __attribute__((ext_vector_type(2)));
     const size_t row = ((size_t)u * a.H + h) * N;
-    const f32x2 gq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.g + row + i0 + r));
-    const f32x2 zq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.z + row + j0 + r));
-    gv = make_float2(gq.x, gq.y);
-    zv = make_float2(zq.x, zq.y);
+    if constexpr (IO == kIoReal) {
+        const float gq = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.g) + row + i0 + r);
+        const float zq = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.z) + row + j0 + r);
+        gv = make_float2(gq, 0.f);
+        zv = make_float2(zq, 0.f);
+    } else {
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const f32x2 gq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.g + row + i0 + r));
+        const f32x2 zq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.z + row + j0 + r));
+        gv = make_float2(gq.x, gq.y);
+        zv = make_float2(zq.x, zq.y);
+    }
 }
 
 // acc[ti][tj] += A_ti B_tj with A[m][0..1] = (g[m].re, g[m].im) and
@@ -277,7 +285,7 @@ __device__ __forceinline__ int acc_col(int tj, int lane) { return 32 * tj + (lan
 // scores q[b,t,h,k] = sum_j Re(g_t[pi_k(j)] conj(z_t[j])) of every map at
 // each of its steps (KW > 0: tasks of KW maps, spread over the waves; every
 // step of the call belongs to one item).
-template <int N, int KW, bool DO_G>
+template <int N, int KW, bool DO_G, int IO>
 __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs a) {
     using Cfg = DictCfg<N>;
     constexpr bool DO_Q = KW > 0;
@@ -335,7 +343,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
     auto issue = [&](float2 (&gq)[U], float2 (&zq)[U], int sidv, int b) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            load_step<N>(a, readlane_i(sidv, my0 + b * U + u), h, i0, j0, lane, gq[u], zq[u]);
+            load_step<N, IO>(a, readlane_i(sidv, my0 + b * U + u), h, i0, j0, lane, gq[u], zq[u]);
     };
     // rows of batch b into the tiles: column t = the step's place in the run
     auto stage = [&](const float2 (&gq)[U], const float2 (&zq)[U], int b) {
@@ -530,7 +538,7 @@ __global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
 
 template <int N, int KW, bool DO_G>
 hipError_t gemm_launch(const SteGradArgs& a, hipStream_t st) {
-    auto kern = k_ste_gemm<N, KW, DO_G>;
+    auto kern = a.io == kIoReal ? k_ste_gemm<N, KW, DO_G, kIoReal> : k_ste_gemm<N, KW, DO_G, kIoC64>;
     const size_t lds = ste_gemm_lds<N>(a.K, KW > 0);
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -96,20 +96,21 @@ def test_flags_known_bits_only(lib):
 def test_narrow_io_only_where_supported(lib, flag):
     f = FakeBufs()
     P = lambda n: f(n)  # noqa: E731
-    # composition and the straight-through calls take complex64 only (the
-    # scans and the decode step take both 4-byte formats)
+    # composition takes complex64 only; the straight-through pair takes real
+    # rows but not bf16 pairs (the scans and the decode step take both)
     d = pdssm.desc(2, 40, 2, 64, 4)
     d.flags = getattr(pdssm, flag)
     st = 2 * 40 * 2 * 64 * 8
     assert lib.pdssm_compose_chunks(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), None,
                                     None) == pdssm.ERR_UNSUPPORTED
-    assert lib.pdssm_ste_grads(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), P(st), P(1 << 20),
-                               1 << 20, None, None) == pdssm.ERR_UNSUPPORTED
-    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
-    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
-    args = [P(640), P(2048), P(st), P(st), P(st), P(2 * 2 * 5 * 64 * 8), P(640), None]
-    assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, P(st), P(st), P(st), None, P(st), ws, need, None,
-                                  None) == pdssm.ERR_UNSUPPORTED
+    if flag == "FLAG_BF16_IO":
+        assert lib.pdssm_ste_grads(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), P(st), P(1 << 20),
+                                   1 << 20, None, None) == pdssm.ERR_UNSUPPORTED
+        need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
+        ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+        args = [P(640), P(2048), P(st), P(st), P(st), P(2 * 2 * 5 * 64 * 8), P(640), None]
+        assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, P(st), P(st), P(st), None, P(st), ws, need, None,
+                                      None) == pdssm.ERR_UNSUPPORTED
     # the multi-pass kernels (dictionary tables beyond LDS) read complex64 rows only
     big = pdssm.desc(1, 40, 1, 128, 128)
     assert lib.pdssm_uses_fused(ctypes.byref(big)) == 0

@@ -14,8 +14,8 @@ import ctypes
 import numpy as np
 import pytest
 
-from helpers import assert_close, sub_sequence
-from oracle import oracle_bwd, oracle_fwd
+from helpers import assert_close, assert_close_sum, ste_scales, sub_sequence
+from oracle import oracle_bwd, oracle_fwd, oracle_ste
 from paper_2605_19150_amd.inputs import make_inputs, workload_inputs
 
 torch = pytest.importorskip("torch")
@@ -155,3 +155,60 @@ def test_real_io_full_size(wl):
         rg = oracle_bwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"], sub["dy"])
         for k, g in zip(("dD", "db", "dc"), rg[:3]):
             assert_close(k, r[k][bb:bb + 1, :, hh:hh + 1].cpu().numpy(), g.real)
+
+
+# (N, K, B, L, H, chunk)
+STE_CASES = [(8, 5, 2, 37, 3, 4), (32, 7, 2, 45, 2, 16), (64, 16, 2, 263, 3, 8), (128, 9, 2, 80, 2, 8),
+             (64, 16, 1, 1100, 1, 8)]
+
+
+def test_real_ste_needs_the_single_read_kernels():
+    # N = 256 tables exceed LDS here: the multi-pass kernels read complex64 rows only
+    B, L, H, N, K = 1, 40, 2, 256, 5
+    assert pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(B, L, H, N, K, 4))) == 0
+    inp = make_inputs(B, L, H, N, K, seed=1, real=True)
+    T = {k: torch.from_numpy(inp[k]).to(DEV) for k in ("idx", "pi", "D", "b", "c")}
+    s = pdssm.Scan(B, L, H, N, K, 4, DEV, ste=True, real=True)
+    with pytest.raises(pdssm.PdssmError) as e:
+        s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+    assert e.value.status == pdssm.ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("N,K,B,L,H,chunk", STE_CASES)
+def test_real_ste(N, K, B, L, H, chunk):
+    """Straight-through inputs of the real-valued model (real z and g = db,
+    scores q, dictionary gradient G): bit for bit the complex64 path on the
+    same values, and the oracle."""
+    print("real ste N=%d K=%d L=%d" % (N, K, L), flush=True)
+    inp = make_inputs(B, L, H, N, K, seed=N * 3 + K + L, with_h0=True, with_dhf=True, real=True)
+    idx, pi = torch.from_numpy(inp["idx"]).to(DEV), torch.from_numpy(inp["pi"]).to(DEV)
+    h0, dhf = torch.from_numpy(inp["h0"]).to(DEV), torch.from_numpy(inp["dh_final"]).to(DEV)
+    dy = torch.from_numpy(inp["dy"]).to(DEV)
+    real = {k: torch.from_numpy(inp[k]).to(DEV) for k in ("D", "b", "c")}
+    out = {}
+    for tag, re in (("real", True), ("c64", False)):
+        T = real if re else {k: v.to(torch.complex64) for k, v in real.items()}
+        s = pdssm.Scan(B, L, H, N, K, chunk, DEV, ste=True, real=re)
+        s.fwd(idx, pi, T["D"], T["b"], T["c"], h0=h0)
+        s.bwd_ste(idx, pi, T["D"], T["b"], T["c"], dy, dh_final=dhf)
+        s.ste_grads(idx, pi)
+        s.check_status()
+        out[tag] = {k: getattr(s, k).clone() for k in ("db", "z", "q", "G")}
+        del s
+    r, c = out["real"], out["c64"]
+    assert r["z"].dtype == torch.float32
+    for k in ("db", "z"):
+        assert torch.equal(r[k], c[k].real), k
+    for k in ("q", "G"):
+        assert torch.equal(r[k], c[k]), k
+    rg = oracle_bwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"],
+                    dh_final=inp["dh_final"])
+    q, G, z = oracle_ste(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"],
+                         dh_final=inp["dh_final"], want_z=True)
+    assert_close("z", r["z"].cpu().numpy(), np.asarray(z).real)
+    qs, Gs = ste_scales(inp["pi"], inp["idx"], rg[1], z)
+    assert_close_sum("q", r["q"].cpu().numpy(), q, qs)
+    assert_close_sum("G", r["G"].cpu().numpy(), G, Gs)
+    # the module functions take real g and z
+    q2, G2 = pdssm.ste_grads(idx, pi, r["db"], r["z"])
+    assert torch.equal(q2, r["q"]) and torch.equal(G2, r["G"])

@@ -93,3 +93,40 @@ def test_real_grads_match_finite_differences(seed):
             Qm[k][pos] -= eps
             fd = (loss(Qp) - loss(Qm)) / (2 * eps)
             assert abs(g.real[pos] - fd) <= 1e-6 + 1e-6 * abs(fd), (k, pos, g.real[pos], fd)
+
+
+def test_real_surrogate_inputs_match_real_autograd():
+    """Straight-through inputs of the real-valued model: on a dense real
+    model (float64 throughout, no complex numbers anywhere) with leaf
+    dictionary matrices P_k and one-hot routing weights v_t
+    (P_t = sum_k v_t[k] P_k), v.grad is the oracle's q and P.grad its G."""
+    torch = pytest.importorskip("torch")
+    from oracle import oracle_ste
+    inp = real_case(5, N=5, K=3, L=7)
+    idx, pi = inp["idx"], inp["pi"]
+    B, L, H = idx.shape
+    K, N = pi.shape[1], pi.shape[2]
+    dense = np.zeros((H, K, N, N))
+    for h in range(H):
+        for k in range(K):
+            dense[h, k, pi[h, k], np.arange(N)] = 1.0
+    Pk = torch.tensor(dense, dtype=torch.float64, requires_grad=True)
+    v = torch.tensor(np.eye(K)[idx], dtype=torch.float64, requires_grad=True)
+    R = lambda a: torch.tensor(np.asarray(a, np.float64))  # noqa: E731
+    D, b, c, dy = R(inp["D"]), R(inp["b"]), R(inp["c"]), R(inp["dy"])
+    h0, dhf = R(inp["h0"].real), R(inp["dh_final"].real)
+    loss = 0
+    for bb in range(B):
+        for h in range(H):
+            x = h0[bb, h]
+            for t in range(L):
+                P = (v[bb, t, h][:, None, None] * Pk[h]).sum(0)
+                x = P @ (D[bb, t, h] * x) + b[bb, t, h]
+                loss = loss + dy[bb, t, h] * (c[bb, t, h] @ x)
+            loss = loss + dhf[bb, h] @ x
+    loss.backward()
+    q, G, z = oracle_ste(idx, pi, inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"],
+                         dh_final=inp["dh_final"], want_z=True)
+    assert np.all(np.asarray(z).imag == 0)
+    np.testing.assert_allclose(q, v.grad.numpy(), rtol=1e-11, atol=1e-11)
+    np.testing.assert_allclose(G, Pk.grad.numpy(), rtol=1e-11, atol=1e-11)
