@@ -399,21 +399,39 @@ hipError_t route_dma_launch(const RouteArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-// pi[h,k,j] = argmax_i M[h,k,i,j]: a thread per (h,k,j), loads coalesced over j.
+// pi[h,k,j] = argmax_i M[h,k,i,j].  A workgroup takes 64 columns of one
+// matrix (h,k) (loads coalesced over j); its four waves each scan a quarter
+// of the rows with eight loads in flight, and wave 0 combines the quarters in
+// row order, so the first maximal row wins as in a single pass.
+constexpr int kArgCols = 64;
 __global__ __launch_bounds__(256) void k_dict_argmax(const float* __restrict__ M, int* __restrict__ pi, int HK,
                                                      int N) {
-    const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (id >= (int64_t)HK * N) return;
-    const int64_t g = id / N;
-    const int j = (int)(id - g * N);
-    const float* col = M + (size_t)g * N * N + j;
-    int best = 0;
+    __shared__ float sv[4][kArgCols];
+    __shared__ int si[4][kArgCols];
+    const int lane = threadIdx.x & 63, part = threadIdx.x >> 6;
+    const int per = (N + kArgCols - 1) / kArgCols;  // column blocks per matrix
+    const int g = blockIdx.x / per;
+    const int j = (blockIdx.x - g * per) * kArgCols + lane;
+    const bool on = g < HK && j < N;
+    const int rows = N / 4;  // N is a power of two >= 8
+    const int i0 = part * rows;
+    const float* col = M + ((size_t)(on ? g : 0) * N + i0) * N + (on ? j : 0);
+    int best = i0;
     float bv = col[0];
-    for (int i = 1; i < N; ++i) {
+#pragma unroll 8
+    for (int i = 1; i < rows; ++i) {
         const float v = col[(size_t)i * N];
-        if (v > bv) bv = v, best = i;
+        if (v > bv) bv = v, best = i0 + i;
     }
-    pi[id] = best;
+    sv[part][lane] = bv;
+    si[part][lane] = best;
+    __syncthreads();
+    if (part == 0 && on) {
+#pragma unroll
+        for (int q = 1; q < 4; ++q)
+            if (sv[q][lane] > bv) bv = sv[q][lane], best = si[q][lane];
+        pi[(size_t)g * N + j] = best;
+    }
 }
 
 }  // namespace
@@ -438,8 +456,8 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_dict_argmax(const float* M, int* pi, int HK, int N, hipStream_t st) {
-    const int64_t n = (int64_t)HK * N;
-    hipLaunchKernelGGL(k_dict_argmax, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, M, pi, HK, N);
+    const int64_t blocks = (int64_t)HK * ((N + kArgCols - 1) / kArgCols);
+    hipLaunchKernelGGL(k_dict_argmax, dim3((unsigned)blocks), dim3(256), 0, st, M, pi, HK, N);
     return hipGetLastError();
 }
 
