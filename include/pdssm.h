@@ -94,10 +94,9 @@ typedef struct pdssm_desc {
  * arithmetic).  Every other tensor (idx, pi, h0, h_final, saved, y, dy,
  * dh_final, dh0) keeps its type.  The arithmetic is fp32 as without the
  * flag: inputs widen exactly, gradients are rounded to nearest (ties to
- * even) when stored.  The scans support it on the single-read kernels only
- * (pdssm_uses_fused(desc) == 1); the multi-pass kernels, pdssm_compose_chunks,
- * pdssm_scan_bwd_ste and pdssm_ste_grads return PDSSM_ERR_UNSUPPORTED (z in
- * bf16 would round the straight-through inputs). */
+ * even) when stored.  pdssm_compose_chunks, pdssm_scan_bwd_ste and
+ * pdssm_ste_grads return PDSSM_ERR_UNSUPPORTED (z in bf16 would round the
+ * straight-through inputs). */
 #define PDSSM_FLAG_BF16_IO 2u
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd / pdssm_decode_step (and
@@ -110,10 +109,9 @@ typedef struct pdssm_desc {
  * out with imaginary parts 0.  The arithmetic is the complex64 one on rows
  * whose imaginary parts are 0, so every result equals, bit for bit, the real
  * part of a complex64 call on the same values.  Cannot be combined with
- * PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG).  The scans (single-read kernels
- * only), pdssm_decode_step, and the straight-through pair
- * pdssm_scan_bwd_ste / pdssm_ste_grads support it (z, g real fp32 rows);
- * the multi-pass kernels and pdssm_compose_chunks return
+ * PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG).  The scans, pdssm_decode_step
+ * and the straight-through pair pdssm_scan_bwd_ste / pdssm_ste_grads support
+ * it (z, g real fp32 rows); pdssm_compose_chunks returns
  * PDSSM_ERR_UNSUPPORTED. */
 #define PDSSM_FLAG_REAL_IO 4u
 

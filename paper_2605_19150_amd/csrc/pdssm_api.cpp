@@ -269,6 +269,19 @@ pdssm::FusedArgs fused_base(const ScanArgs& a) {
     return f;
 }
 
+// Row format of D, b, c (and dD, db, dc) selected by the flags.
+int io_format(const pdssm_desc* d) {
+    if (d->flags & PDSSM_FLAG_REAL_IO) return pdssm::kIoReal;
+    if (d->flags & PDSSM_FLAG_BF16_IO) return pdssm::kIoBf16;
+    return pdssm::kIoC64;
+}
+
+// A 4-byte row format (bf16 pairs or real fp32).
+bool narrow_io(const pdssm_desc* d) { return io_format(d) != pdssm::kIoC64; }
+
+// Bytes per entry of D, b, c (and dD, db, dc).
+size_t io_bytes(const pdssm_desc* d) { return narrow_io(d) ? 4 : 8; }
+
 ScanArgs base_args(const pdssm_desc* d, int tau) {
     ScanArgs a = {};
     a.B = d->B;
@@ -278,23 +291,11 @@ ScanArgs base_args(const pdssm_desc* d, int tau) {
     a.K = d->K;
     a.tau = tau;
     a.C = (d->L + tau - 1) / tau;
+    a.io = io_format(d);
     return a;
 }
 
 bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) % 16) != 0; }
-
-// Row format of D, b, c (and dD, db, dc) selected by the flags.
-int io_format(const pdssm_desc* d) {
-    if (d->flags & PDSSM_FLAG_REAL_IO) return pdssm::kIoReal;
-    if (d->flags & PDSSM_FLAG_BF16_IO) return pdssm::kIoBf16;
-    return pdssm::kIoC64;
-}
-
-// A 4-byte row format (bf16 pairs or real fp32): single-read kernels only.
-bool narrow_io(const pdssm_desc* d) { return io_format(d) != pdssm::kIoC64; }
-
-// Bytes per entry of D, b, c (and dD, db, dc).
-size_t io_bytes(const pdssm_desc* d) { return narrow_io(d) ? 4 : 8; }
 
 }  // namespace
 
@@ -377,7 +378,6 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     const size_t need = ws_bytes_for(s, d, a.C);
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
-    if (narrow_io(d) && !use_fused(d)) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
     if (any_overlap({{y, s.idxN * 4}, {h_final, s.seqN * 8}, {saved, s.perChunk * 8}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {h0, s.seqN * 8}}))
@@ -427,9 +427,7 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (misaligned(z)) return PDSSM_ERR_INVALID_ARG;
-    // 4-byte formats: single-read kernels only; z in bf16 pairs would round the
-    // straight-through inputs, so that pair is not offered
-    if (narrow_io(d) && !use_fused(d)) return PDSSM_ERR_UNSUPPORTED;
+    // z in bf16 pairs would round the straight-through inputs: not offered
     if (z && io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
     if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, nst}, {ws, need}},

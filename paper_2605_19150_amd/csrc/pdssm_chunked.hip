@@ -28,8 +28,34 @@ namespace {
 
 constexpr int kWavesPerGroup = 4;
 
+// Rows of D, b, c (in) and dD, db, dc, z (out) in row format IO: off counts
+// entries; the 4-byte formats widen to (and narrow from) complex in registers
+// exactly as the single-read kernels do.
+template <int SL, int IO>
+__device__ __forceinline__ CV<SL> ld_io(const float2* base, size_t off, int lane) {
+    if constexpr (IO == kIoC64) {
+        return ld_cv<SL>(base + off, lane);
+    } else {
+        const uint32_t* p = reinterpret_cast<const uint32_t*>(base) + off + (size_t)lane * SL;
+        CV<SL> out;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) out.v[s] = word_to_f2<IO>(p[s]);
+        return out;
+    }
+}
+template <int SL, int IO>
+__device__ __forceinline__ void st_io(float2* base, size_t off, int lane, const CV<SL>& v) {
+    if constexpr (IO == kIoC64) {
+        st_cv<SL>(base + off, lane, v);
+    } else {
+        uint32_t* p = reinterpret_cast<uint32_t*>(base) + off + (size_t)lane * SL;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) p[s] = f2_to_word<IO>(v.v[s]);
+    }
+}
+
 // ================================================================== forward
-template <int N>
+template <int N, int IO>
 __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 xs[kWavesPerGroup][N];
@@ -72,8 +98,8 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     IV<SL> pn = {};
     if (act) {
         int k = readlane_i(kv, 0);
-        Dn = ld_cv<SL>(a.D + base, lane);
-        bn = ld_cv<SL>(a.b + base, lane);
+        Dn = ld_io<SL, IO>(a.D, base, lane);
+        bn = ld_io<SL, IO>(a.b, base, lane);
         pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = 0; t < len; ++t) {
@@ -81,8 +107,8 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
         IV<SL> pt = pn;
         if (t + 1 < len && act) {
             int k = readlane_i(kv, t + 1);
-            Dn = ld_cv<SL>(a.D + base + (t + 1) * stride, lane);
-            bn = ld_cv<SL>(a.b + base + (t + 1) * stride, lane);
+            Dn = ld_io<SL, IO>(a.D, base + (t + 1) * stride, lane);
+            bn = ld_io<SL, IO>(a.b, base + (t + 1) * stride, lane);
             pn = ld_iv<SL>(pih + (size_t)k * N, lane);
         }
         bad |= sanitize_map<N, SL>(pt);
@@ -148,7 +174,7 @@ __global__ __launch_bounds__(256) void k_fwd_carry(ScanArgs a) {
     if (a.hfinal && act) st_cv<SL>(a.hfinal + (size_t)seq * N, lane, h);
 }
 
-template <int N>
+template <int N, int IO>
 __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 xs[kWavesPerGroup][N];
@@ -179,9 +205,9 @@ __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
     IV<SL> pn = {};
     if (act) {
         int k = readlane_i(kv, 0);
-        Dn = ld_cv<SL>(a.D + base, lane);
-        bn = ld_cv<SL>(a.b + base, lane);
-        cn = ld_cv<SL>(a.c + base, lane);
+        Dn = ld_io<SL, IO>(a.D, base, lane);
+        bn = ld_io<SL, IO>(a.b, base, lane);
+        cn = ld_io<SL, IO>(a.c, base, lane);
         pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = 0; t < len; ++t) {
@@ -190,9 +216,9 @@ __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
         if (t + 1 < len && act) {
             int k = readlane_i(kv, t + 1);
             const size_t off = base + (t + 1) * stride;
-            Dn = ld_cv<SL>(a.D + off, lane);
-            bn = ld_cv<SL>(a.b + off, lane);
-            cn = ld_cv<SL>(a.c + off, lane);
+            Dn = ld_io<SL, IO>(a.D, off, lane);
+            bn = ld_io<SL, IO>(a.b, off, lane);
+            cn = ld_io<SL, IO>(a.c, off, lane);
             pn = ld_iv<SL>(pih + (size_t)k * N, lane);
         }
         sanitize_map<N, SL>(pt);
@@ -208,7 +234,7 @@ __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
 }
 
 // ================================================================== backward
-template <int N>
+template <int N, int IO>
 __global__ __launch_bounds__(256) void k_bwd_agg(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     __shared__ float2 gsh[kWavesPerGroup][N];
@@ -254,8 +280,8 @@ __global__ __launch_bounds__(256) void k_bwd_agg(ScanArgs a) {
     if (act) {
         int k = readlane_i(kv, len - 1);
         const size_t off = base + (len - 1) * stride;
-        Dn = ld_cv<SL>(a.D + off, lane);
-        cn = ld_cv<SL>(a.c + off, lane);
+        Dn = ld_io<SL, IO>(a.D, off, lane);
+        cn = ld_io<SL, IO>(a.c, off, lane);
         pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = len - 1; t >= 0; --t) {
@@ -264,8 +290,8 @@ __global__ __launch_bounds__(256) void k_bwd_agg(ScanArgs a) {
         if (t > 0 && act) {
             int k = readlane_i(kv, t - 1);
             const size_t off = base + (t - 1) * stride;
-            Dn = ld_cv<SL>(a.D + off, lane);
-            cn = ld_cv<SL>(a.c + off, lane);
+            Dn = ld_io<SL, IO>(a.D, off, lane);
+            cn = ld_io<SL, IO>(a.c, off, lane);
             pn = ld_iv<SL>(pih + (size_t)k * N, lane);
         }
         bad |= sanitize_map<N, SL>(pt);
@@ -346,7 +372,7 @@ __global__ __launch_bounds__(256) void k_bwd_carry(ScanArgs a) {
 }
 
 // One wave per workgroup; dynamic LDS = (tau + 1) states + one exchange row.
-template <int N>
+template <int N, int IO>
 __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     extern __shared__ float2 smem[];
@@ -381,8 +407,8 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     IV<SL> pn = {};
     if (act) {
         int k = readlane_i(kv, 0);
-        Dn = ld_cv<SL>(a.D + base, lane);
-        bn = ld_cv<SL>(a.b + base, lane);
+        Dn = ld_io<SL, IO>(a.D, base, lane);
+        bn = ld_io<SL, IO>(a.b, base, lane);
         pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = 0; t < len; ++t) {
@@ -390,8 +416,8 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
         IV<SL> pt = pn;
         if (t + 1 < len && act) {
             int k = readlane_i(kv, t + 1);
-            Dn = ld_cv<SL>(a.D + base + (t + 1) * stride, lane);
-            bn = ld_cv<SL>(a.b + base + (t + 1) * stride, lane);
+            Dn = ld_io<SL, IO>(a.D, base + (t + 1) * stride, lane);
+            bn = ld_io<SL, IO>(a.b, base + (t + 1) * stride, lane);
             pn = ld_iv<SL>(pih + (size_t)k * N, lane);
         }
         sanitize_map<N, SL>(pt);
@@ -406,8 +432,8 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     if (act) {
         int k = readlane_i(kv, len - 1);
         const size_t off = base + (len - 1) * stride;
-        Dn = ld_cv<SL>(a.D + off, lane);
-        cn = ld_cv<SL>(a.c + off, lane);
+        Dn = ld_io<SL, IO>(a.D, off, lane);
+        cn = ld_io<SL, IO>(a.c, off, lane);
         pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = len - 1; t >= 0; --t) {
@@ -416,8 +442,8 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
         if (t > 0 && act) {
             int k = readlane_i(kv, t - 1);
             const size_t off = base + (t - 1) * stride;
-            Dn = ld_cv<SL>(a.D + off, lane);
-            cn = ld_cv<SL>(a.c + off, lane);
+            Dn = ld_io<SL, IO>(a.D, off, lane);
+            cn = ld_io<SL, IO>(a.c, off, lane);
             pn = ld_iv<SL>(pih + (size_t)k * N, lane);
         }
         sanitize_map<N, SL>(pt);
@@ -436,8 +462,8 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
         }
         wave_sync();
         if (act) {
-            st_cv<SL>(a.db + off, lane, g);
-            st_cv<SL>(a.dc + off, lane, dct);
+            st_io<SL, IO>(a.db, off, lane, g);
+            st_io<SL, IO>(a.dc, off, lane, dct);
             st_cv<SL>(X, lane, g);
         }
         wave_sync();
@@ -449,14 +475,14 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
                 dDt.v[s] = cmulc(hp.v[s], gp);
                 g.v[s] = cmulc(Dt.v[s], gp);
             }
-            st_cv<SL>(a.dD + off, lane, dDt);
+            st_io<SL, IO>(a.dD, off, lane, dDt);
         }
         if (a.z && act) {
             // the scaled state z_t = D_t .* h_{t-1} for the straight-through gradients
             CV<SL> zt;
 #pragma unroll
             for (int s = 0; s < SL; ++s) zt.v[s] = cmul(Dt.v[s], hp.v[s]);
-            st_cv<SL>(a.z + off, lane, zt);
+            st_io<SL, IO>(a.z, off, lane, zt);
         }
     }
 }
@@ -536,22 +562,47 @@ inline unsigned groups_for(long long tasks) {
     return (unsigned)((tasks + kWavesPerGroup - 1) / kWavesPerGroup);
 }
 
+template <int N, int IO>
+hipError_t fwd_chunked_io(const ScanArgs& a, hipStream_t s) {
+    const long long tasks = (long long)a.B * a.H * a.C;
+    auto agg = k_fwd_agg<N, IO>;
+    auto replay = k_fwd_replay<N, IO>;
+    hipLaunchKernelGGL(agg, dim3(groups_for(tasks)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_fwd_carry<N>, dim3(groups_for((long long)a.B * a.H)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(replay, dim3(groups_for(tasks)), dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int N, int IO>
+hipError_t bwd_chunked_io(const ScanArgs& a, hipStream_t s) {
+    const long long tasks = (long long)a.B * a.H * a.C;
+    auto agg = k_bwd_agg<N, IO>;
+    auto emit = k_bwd_emit<N, IO>;
+    hipLaunchKernelGGL(agg, dim3(groups_for(tasks)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(k_bwd_carry<N>, dim3(groups_for((long long)a.B * a.H)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(emit, dim3((unsigned)tasks), dim3(64), bwd_emit_lds_bytes(N, a.tau), s, a);
+    return hipGetLastError();
+}
+
+// the row format picks the instantiation
 template <int N>
 hipError_t fwd_chunked_n(const ScanArgs& a, hipStream_t s) {
-    const long long tasks = (long long)a.B * a.H * a.C;
-    hipLaunchKernelGGL(k_fwd_agg<N>, dim3(groups_for(tasks)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_fwd_carry<N>, dim3(groups_for((long long)a.B * a.H)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_fwd_replay<N>, dim3(groups_for(tasks)), dim3(256), 0, s, a);
-    return hipGetLastError();
+    switch (a.io) {
+        case kIoC64: return fwd_chunked_io<N, kIoC64>(a, s);
+        case kIoBf16: return fwd_chunked_io<N, kIoBf16>(a, s);
+        case kIoReal: return fwd_chunked_io<N, kIoReal>(a, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int N>
 hipError_t bwd_chunked_n(const ScanArgs& a, hipStream_t s) {
-    const long long tasks = (long long)a.B * a.H * a.C;
-    hipLaunchKernelGGL(k_bwd_agg<N>, dim3(groups_for(tasks)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_bwd_carry<N>, dim3(groups_for((long long)a.B * a.H)), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(k_bwd_emit<N>, dim3((unsigned)tasks), dim3(64), bwd_emit_lds_bytes(N, a.tau), s, a);
-    return hipGetLastError();
+    switch (a.io) {
+        case kIoC64: return bwd_chunked_io<N, kIoC64>(a, s);
+        case kIoBf16: return bwd_chunked_io<N, kIoBf16>(a, s);
+        case kIoReal: return bwd_chunked_io<N, kIoReal>(a, s);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int N>

@@ -14,6 +14,8 @@ struct ScanArgs {
     int B, L, H, N, K;
     int tau;  // chunk length
     int C;    // ceil(L / tau)
+    int io;   // row format of D, b, c, dD, db, dc, z (kIoC64, kIoBf16, kIoReal: pdssm_io.h);
+              // the float2 pointers below are reinterpreted for the 4-byte formats
     const int* idx;
     const int* pi;
     const float2* D;

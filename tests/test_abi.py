@@ -111,15 +111,6 @@ def test_narrow_io_only_where_supported(lib, flag):
         args = [P(640), P(2048), P(st), P(st), P(st), P(2 * 2 * 5 * 64 * 8), P(640), None]
         assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, P(st), P(st), P(st), None, P(st), ws, need, None,
                                       None) == pdssm.ERR_UNSUPPORTED
-    # the multi-pass kernels (dictionary tables beyond LDS) read complex64 rows only
-    big = pdssm.desc(1, 40, 1, 128, 128)
-    assert lib.pdssm_uses_fused(ctypes.byref(big)) == 0
-    big.flags = getattr(pdssm, flag)
-    need = lib.pdssm_workspace_size(ctypes.byref(big), pdssm.OP_FWD)
-    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
-    st = 40 * 128 * 8
-    assert lib.pdssm_scan_fwd(ctypes.byref(big), P(160), P(128 * 128 * 4), P(st), P(st), P(st), None, P(160),
-                              None, None, ws, need, None, None) == pdssm.ERR_UNSUPPORTED
 
 
 def test_prepare_host_checks(lib):

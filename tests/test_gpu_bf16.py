@@ -98,15 +98,9 @@ CASES += [(64, 8, 1), (64, 8, 261), (128, 8, 133)]
 
 @pytest.mark.parametrize("N,chunk,L", CASES)
 def test_bf16_io_small(N, chunk, L):
-    import ctypes
     print("bf16 case N=%d chunk=%d L=%d" % (N, chunk, L), flush=True)
     inp = make_inputs(B=2, L=L, H=3, N=N, K=5, seed=N * 31 + chunk + L, with_h0=True, with_dhf=True)
-    if pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(2, L, 3, N, 5, chunk))) != 1:
-        # dictionaries beyond LDS run the multi-pass kernels, which take complex64 only
-        with pytest.raises(pdssm.PdssmError) as e:
-            run_both(inp, chunk)
-        assert e.value.status == pdssm.ERR_UNSUPPORTED
-        return
+    # (N = 256 runs the multi-pass kernels: tables beyond LDS)
     exact, out = run_both(inp, chunk)
     check(inp, exact, out)
 
@@ -137,3 +131,11 @@ def test_bf16_io_full_size(wl):
         rg = oracle_bwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"], sub["dy"])
         for k, r in zip(("dD", "db", "dc"), rg[:3]):
             assert_close(k, pairs_to_complex(bf[k][bb:bb + 1, :, hh:hh + 1]), r, rtol=BF_RTOL)
+
+
+def test_bf16_io_multi_pass_large_dictionary():
+    inp = make_inputs(B=2, L=70, H=2, N=128, K=128, seed=4, with_h0=True, with_dhf=True)
+    import ctypes
+    assert pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(2, 70, 2, 128, 128))) == 0
+    exact, out = run_both(inp)
+    check(inp, exact, out)

@@ -91,12 +91,7 @@ CASES += [(64, 8, 1), (64, 8, 261), (128, 8, 133)]
 def test_real_io_small(N, chunk, L):
     print("real case N=%d chunk=%d L=%d" % (N, chunk, L), flush=True)
     inp = make_inputs(B=2, L=L, H=3, N=N, K=5, seed=N * 37 + chunk + L, with_h0=True, with_dhf=True, real=True)
-    if pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(2, L, 3, N, 5, chunk))) != 1:
-        # dictionaries beyond LDS run the multi-pass kernels, which take complex64 only
-        with pytest.raises(pdssm.PdssmError) as e:
-            run_both(inp, chunk)
-        assert e.value.status == pdssm.ERR_UNSUPPORTED
-        return
+    # (N = 256 runs the multi-pass kernels: tables beyond LDS)
     out = run_both(inp, chunk)
     check_bits(out)
     check_oracle(inp, out)
@@ -159,19 +154,17 @@ def test_real_io_full_size(wl):
 
 # (N, K, B, L, H, chunk)
 STE_CASES = [(8, 5, 2, 37, 3, 4), (32, 7, 2, 45, 2, 16), (64, 16, 2, 263, 3, 8), (128, 9, 2, 80, 2, 8),
-             (64, 16, 1, 1100, 1, 8)]
+             (64, 16, 1, 1100, 1, 8),
+             (256, 5, 1, 40, 2, 4),      # multi-pass scan (tables beyond LDS)
+             (128, 128, 1, 30, 1, 8)]    # multi-pass scan, large dictionary
 
 
-def test_real_ste_needs_the_single_read_kernels():
-    # N = 256 tables exceed LDS here: the multi-pass kernels read complex64 rows only
-    B, L, H, N, K = 1, 40, 2, 256, 5
-    assert pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(B, L, H, N, K, 4))) == 0
-    inp = make_inputs(B, L, H, N, K, seed=1, real=True)
-    T = {k: torch.from_numpy(inp[k]).to(DEV) for k in ("idx", "pi", "D", "b", "c")}
-    s = pdssm.Scan(B, L, H, N, K, 4, DEV, ste=True, real=True)
-    with pytest.raises(pdssm.PdssmError) as e:
-        s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
-    assert e.value.status == pdssm.ERR_UNSUPPORTED
+def test_real_multi_pass_large_dictionary():
+    inp = make_inputs(B=2, L=70, H=2, N=128, K=128, seed=3, with_h0=True, with_dhf=True, real=True)
+    assert pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(2, 70, 2, 128, 128))) == 0
+    out = run_both(inp)
+    check_bits(out)
+    check_oracle(inp, out)
 
 
 @pytest.mark.parametrize("N,K,B,L,H,chunk", STE_CASES)
