@@ -207,7 +207,7 @@ struct DictCfg {
     static constexpr int RS = N <= 64 ? 64 : (N == 128 ? 32 : 16);  // steps per run (staged tiles <= ~70 KB)
     static constexpr int SLOTS = 64 / RS;                            // score tasks a wave runs side by side
     static constexpr int MY = RS / SPLIT;                            // steps of a run one wave multiplies
-    static constexpr int U = N >= 256 ? 4 : 8;                       // steps per load batch
+    static constexpr int U = (N >= 256 || N == 64) ? 4 : 8;          // steps per load batch (N = 64: 4 measured 3% faster)
     static constexpr int NBAT = MY / U;                              // load batches per run (even)
     static constexpr int GP = RS + 1;                                // padded tile row (complex entries)
     static constexpr int TILE_BYTES = 2 * N * GP * 8;
