@@ -268,8 +268,8 @@ def main():
                     help="profiling aid: time a plain 1 GiB device copy instead")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on exactly one GPU; --gpus %d is not supported "
-              "(the PD scan shards by sequence without communication; see DESIGN.md)" % args.gpus,
+        print("bench.py: runs on exactly one GPU; --gpus %d is not supported "
+              "(the PD scan shards by sequence without communication)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
 
