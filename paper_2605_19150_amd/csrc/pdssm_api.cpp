@@ -101,6 +101,18 @@ Sizes sizes_of(const pdssm_desc* d, int C) {
 // LDS holds (up to a whole sequence), at least kMinStaging, else none.
 constexpr int kMinStaging = 16;
 
+// N = 256: a narrower wave count when the default one leaves the head's
+// tables no room in LDS (compiled for N = 256 only): the wider of the two
+// that fits, else the narrowest (the layout check then picks multi-pass).
+int narrow_if_needed(const pdssm_desc* d, int W) {
+    if (d->N != 256 || pdssm::fused_lds_layout(d->N, d->K, W).total <= pdssm::kMaxLds) return W;
+    if (pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWavesNarrow).total <= pdssm::kMaxLds)
+        return pdssm::kFusedWavesNarrow;
+    return pdssm::kFusedWavesNarrowest;
+}
+
+int bwd_waves(const pdssm_desc* d, int tau) { return narrow_if_needed(d, pdssm::fused_waves_bwd(d->N, tau)); }
+
 // Chunk waves of the fused forward: the wide count for the 4-byte row
 // formats (their forward waits on its chunk passes, not on HBM) when the
 // prefetching kernel runs and its tables leave room for the minimum
@@ -111,13 +123,13 @@ int fwd_waves(const pdssm_desc* d, int tau) {
         pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWavesWide).total + (size_t)kMinStaging * d->N * 8 <=
             pdssm::kMaxLds)
         return pdssm::kFusedWavesWide;
-    return pdssm::fused_waves(d->N, tau);
+    return narrow_if_needed(d, pdssm::fused_waves(d->N, tau));
 }
 
 // The fused single-read kernels stage one head's dictionary tables in LDS;
 // when they do not fit, the chunked three-pass kernels run instead.
 pdssm::LdsLayout fused_layout(const pdssm_desc* d, int tau, bool fwd) {
-    const int W = fwd ? fwd_waves(d, tau) : pdssm::fused_waves_bwd(d->N, tau);
+    const int W = fwd ? fwd_waves(d, tau) : bwd_waves(d, tau);
     return pdssm::fused_lds_layout(d->N, d->K, W);
 }
 
@@ -222,7 +234,7 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     f.dict = pa.dict;
     f.rec = pa.rec;
     f.mtab = pa.mtab;
-    f.W = fwd ? fwd_waves(d, f.tau) : pdssm::fused_waves_bwd(d->N, f.tau);
+    f.W = fwd ? fwd_waves(d, f.tau) : bwd_waves(d, f.tau);
     f.lds = fused_layout(d, f.tau, fwd);
     f.sbM = fwd ? staging_rows(d, f.lds, f.C) : 0;
     f.lds = pdssm::fused_lds_add_staging(f.lds, d->N, f.sbM);

@@ -30,6 +30,13 @@ constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? 
 // tables leave LDS room for them: more waves in flight hide the chunk
 // passes' LDS round trips (the backward measured faster with 8).
 constexpr int kFusedWavesWide = 11;
+// At N = 256 the per-wave LDS buffers (2W published operators of N entries
+// and their sorted forms, W staging rows, 2W readout rows) leave room for the
+// head's tables only with fewer chunk waves: 5, else 3, in both directions,
+// used when 7 do not fit (dictionaries of up to 16, else 32 entries; larger
+// ones run the multi-pass kernels).
+constexpr int kFusedWavesNarrow = 5;
+constexpr int kFusedWavesNarrowest = 3;
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
@@ -123,8 +130,9 @@ struct FusedArgs {
     float2* segA;
     float2* segD;
     int* segP;
-    // Chunk waves of the forward (fused_waves or kFusedWavesWide); the
-    // backward's count follows from N and tau.
+    // Chunk waves of this call's kernel: fused_waves / fused_waves_bwd, or
+    // kFusedWavesWide (forward), or kFusedWavesNarrow / kFusedWavesNarrowest
+    // (N = 256).
     int W;
     // Format of D, b, c and dD, db, dc (kIoC64, kIoBf16 pairs or kIoReal
     // fp32, 4 bytes per entry for the last two: the pointers above are then

@@ -1420,8 +1420,24 @@ hipError_t fwd_dispatch_waves(const FusedArgs& a, hipStream_t st) {
     if constexpr (fused_prefetch(N, TAU)) {
         if (a.W == kFusedWavesWide) return fwd_launch<N, TAU, kFusedWavesWide>(a, st);
     }
+    if constexpr (N == 256) {
+        if (a.W == kFusedWavesNarrow) return fwd_launch<N, TAU, kFusedWavesNarrow>(a, st);
+        if (a.W == kFusedWavesNarrowest) return fwd_launch<N, TAU, kFusedWavesNarrowest>(a, st);
+    }
     if (a.W != fused_waves(N, TAU)) return hipErrorInvalidValue;
     return fwd_launch<N, TAU, fused_waves(N, TAU)>(a, st);
+}
+
+// The backward's: fused_waves_bwd(N, TAU), or at N = 256 kFusedWavesNarrow or
+// kFusedWavesNarrowest.
+template <int N, int TAU>
+hipError_t bwd_dispatch_waves(const FusedArgs& a, hipStream_t st) {
+    if constexpr (N == 256) {
+        if (a.W == kFusedWavesNarrow) return bwd_launch<N, TAU, kFusedWavesNarrow>(a, st);
+        if (a.W == kFusedWavesNarrowest) return bwd_launch<N, TAU, kFusedWavesNarrowest>(a, st);
+    }
+    if (a.W != fused_waves_bwd(N, TAU)) return hipErrorInvalidValue;
+    return bwd_launch<N, TAU, fused_waves_bwd(N, TAU)>(a, st);
 }
 
 template <int N, bool FWD>
@@ -1429,14 +1445,14 @@ hipError_t dispatch_tau(const FusedArgs& a, hipStream_t st) {
     constexpr int SL = Lay<N>::SL;
     switch (a.tau) {
         case 4:
-            return FWD ? fwd_dispatch_waves<N, 4>(a, st) : bwd_launch<N, 4, fused_waves_bwd(N, 4)>(a, st);
+            return FWD ? fwd_dispatch_waves<N, 4>(a, st) : bwd_dispatch_waves<N, 4>(a, st);
         case 8:
             if constexpr (8 * SL <= 16)
-                return FWD ? fwd_dispatch_waves<N, 8>(a, st) : bwd_launch<N, 8, fused_waves_bwd(N, 8)>(a, st);
+                return FWD ? fwd_dispatch_waves<N, 8>(a, st) : bwd_dispatch_waves<N, 8>(a, st);
             break;
         case 16:
             if constexpr (16 * SL <= 16)
-                return FWD ? fwd_dispatch_waves<N, 16>(a, st) : bwd_launch<N, 16, fused_waves_bwd(N, 16)>(a, st);
+                return FWD ? fwd_dispatch_waves<N, 16>(a, st) : bwd_dispatch_waves<N, 16>(a, st);
             break;
         default: break;
     }

@@ -111,6 +111,12 @@ def scan_segments(d):
     return load().pdssm_scan_segments(ctypes.byref(d))
 
 
+def uses_fused(d):
+    """1 when the single-read kernels run this descriptor, 0 when the
+    multi-pass kernels do (dictionary tables beyond LDS), < 0 on error."""
+    return load().pdssm_uses_fused(ctypes.byref(d))
+
+
 def chunk_len(d):
     return load().pdssm_chunk_len(ctypes.byref(d))
 
@@ -203,7 +209,7 @@ class Scan:
         if self.C < 0:
             raise PdssmError(self.C, "num_chunks")
         self.chunk = chunk_len(self.d)
-        self.fused = load().pdssm_uses_fused(ctypes.byref(self.d)) == 1
+        self.fused = uses_fused(self.d) == 1
         self.segments = load().pdssm_scan_segments(ctypes.byref(self.d))
         dev = self.device
         nws = max(workspace_size(self.d, OP_FWD), workspace_size(self.d, OP_BWD), 1)

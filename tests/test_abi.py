@@ -60,6 +60,19 @@ def test_chunk_and_workspace_queries(lib):
     assert pdssm.scan_segments(pdssm.desc(1, 100, 2, 64, 16)) == 1
 
 
+@pytest.mark.parametrize("N,K,flags,fused", [
+    (64, 16, 0, 1), (128, 32, 0, 1), (128, 128, 0, 0),
+    (256, 8, 0, 1), (256, 16, 0, 1),        # five chunk waves keep small dictionaries single-read,
+    (256, 32, 0, 1),                        # three the next size up
+    (256, 8, pdssm.FLAG_REAL_IO, 1), (256, 8, pdssm.FLAG_BF16_IO, 1),
+    (256, 32, pdssm.FLAG_BF16_IO, 1), (256, 64, 0, 0), (256, 64, pdssm.FLAG_REAL_IO, 0),
+])
+def test_single_read_or_multi_pass(lib, N, K, flags, fused):
+    d = pdssm.desc(8, 4096, 16, N, K)
+    d.flags = flags
+    assert pdssm.uses_fused(d) == fused
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(N=48), pdssm.ERR_UNSUPPORTED),
     (dict(N=512), pdssm.ERR_UNSUPPORTED),

@@ -123,6 +123,18 @@ def test_large_dictionary_chunked_path(N, K):
     check_all(inp, got, eff_chunk(inp))
 
 
+@pytest.mark.parametrize("K,fused", [(16, 1), (32, 1), (64, 0)])
+def test_state_size_256_wave_counts(K, fused):
+    """N = 256: five chunk waves (K <= 16), three (K = 32), multi-pass beyond;
+    segmented (one sequence) and many sequences, with h0 and dh_final."""
+    for B, L, H in ((1, 900, 1), (3, 61, 4)):
+        print("N=256 K=%d B=%d L=%d H=%d" % (K, B, L, H), flush=True)
+        assert pdssm.uses_fused(pdssm.desc(B, L, H, 256, K)) == fused
+        inp = make_inputs(B=B, L=L, H=H, N=256, K=K, seed=K + L, with_h0=True, with_dhf=True)
+        got = run_gpu(inp)
+        check_all(inp, got, eff_chunk(inp))
+
+
 # ------------------------------------------------------------------ automaton: exact
 @pytest.mark.parametrize("N,perm", [(8, False), (64, True), (64, False), (128, False), (256, True)])
 def test_fsa_bit_exact(N, perm):
