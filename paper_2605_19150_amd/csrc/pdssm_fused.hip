@@ -302,9 +302,31 @@ struct Chunk {
     int kv, mv, len;
 };
 
+// The same sums reading only as many sources as the step's map needs: gk is
+// that map's max in-degree (wave-uniform), and every record byte past a
+// row's own sources names the zero row or an unused slot, so stopping after
+// gk of them changes nothing.  Heads of the 7-source class pick 3, 4, 5 or 7
+// reads with a scalar branch per step (uniform maps at N = 64..128 mostly
+// need 4 or 5).  The forward's pipelined chunk pass keeps its fixed count:
+// there the branch splits the step's one batch of LDS reads and measured
+// slower.
+template <int N, int G>
+__device__ __forceinline__ void gather_rows_k(const float2* V, const uint64_t* recrow, int lane,
+                                              CV<Lay<N>::SL>& acc, int gk) {
+    if constexpr (G <= 3) {
+        gather_rows<N, G>(V, recrow, lane, acc);
+    } else {
+        if (gk <= 3) gather_rows<N, 3>(V, recrow, lane, acc);
+        else if (gk <= 4) gather_rows<N, 4>(V, recrow, lane, acc);
+        else if (gk <= 5) gather_rows<N, 5>(V, recrow, lane, acc);
+        else gather_rows<N, G>(V, recrow, lane, acc);
+    }
+}
+
 // One step h <- bt + P(k) (Dt .* h).  With STAGE_D the step also leaves D_t
 // in Z for a map composition.  FB: the head has entries that need the
-// atomic scatter, tested per step.
+// atomic scatter, tested per step.  M: the step's in-degree class (its map's
+// max in-degree, or kFallback).
 template <int N, int G, bool FB, bool STAGE_D>
 __device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, float2* X, int lane, bool act,
                                         int k, int M, CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt,
@@ -341,7 +363,7 @@ __device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, float2* 
     wave_sync();
     if (act) {
         CV<SL> acc = bt;
-        gather_rows<N, G>(st.V, s.rec + (size_t)k * N, lane, acc);
+        gather_rows_k<N, G>(st.V, s.rec + (size_t)k * N, lane, acc, M);
         h = acc;
     }
 }
@@ -709,7 +731,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
             const int k = readlane_i(q.kv, t);
-            const int M = FB ? readlane_i(q.mv, t) : 0;
+            const int M = readlane_i(q.mv, t);
             if (!AGG && act) {
                 wave_sync();
 #pragma unroll
@@ -1190,7 +1212,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
     for (int t = 0; t < TAU; ++t) {
         const int k = readlane_i(q.kv, t);
-        const int M = FB ? readlane_i(q.mv, t) : 0;
+        const int M = readlane_i(q.mv, t);
         pd_step<N, G, FB, false>(s, st, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
         Hs[t + 1] = hs;
     }
