@@ -499,55 +499,47 @@ __device__ __forceinline__ float2 wave_seg_scan(float2 v, uint64_t starts, int l
     return v;
 }
 
-template <int N>
-struct Log2 {
-    static constexpr int v = N <= 1 ? 0 : 1 + Log2<N / 2>::v;
-};
-
 // Sorted form of the map pm (source j = lane*SL + r goes to row pm[r]),
 // written into operator slot `slot`: agp = sorted position of every source,
 // age = last position of every destination's run (kNoRun if it has no
-// source), agh = run-start flags of the positions.  Ranks among equal
-// destinations come from ballots over the destination bits, so the order is
-// exact and deterministic.  OFF: N ints of this wave's scratch.
+// source), agh = run-start flags of the positions.  Runs list their sources
+// in ascending order.  The ranks come from lane masks: table q (N 64-bit
+// words, MT[q]) collects, per row, the lanes whose slot q maps there (an
+// atomic OR, so the result does not depend on the order of the ORs); a
+// source's rank counts the lanes below its own in the tables at its row,
+// plus its lane's earlier slots with the same row, and a row's source count
+// is the popcount of its words.  OFF: N ints of this wave's scratch; MT: SL
+// tables of N words in this wave's staging buffers, free outside the pass.
 template <int N>
 __device__ __forceinline__ void publish_sorted_map(const Smem& s, int slot, const IV<Lay<N>::SL>& pm, int lane,
-                                                   bool act, int* OFF) {
-    constexpr int SL = Lay<N>::SL, BITS = Log2<N>::v;
-    const uint64_t actm = __builtin_amdgcn_ballot_w64(act);
+                                                   bool act, int* OFF, uint64_t* const (&MT)[Lay<N>::SL]) {
+    constexpr int SL = Lay<N>::SL;
     const uint64_t lt = (1ull << lane) - 1ull;
-    // mr[r][q]: lanes whose slot q goes to the row of this lane's source r;
-    // mo[r][q]: lanes whose slot q goes to this lane's own row r.  One ballot
-    // per destination bit and slot narrows both.
-    uint64_t mr[SL][SL], mo[SL][SL];
+    wave_sync();
 #pragma unroll
-    for (int r = 0; r < SL; ++r)
+    for (int q = 0; q < SL; ++q)
+        for (int i = lane; i < N; i += kWave) MT[q][i] = 0;
+    wave_sync();
+    if (act) {
 #pragma unroll
-        for (int q = 0; q < SL; ++q) mr[r][q] = mo[r][q] = actm;
-#pragma unroll 1
-    for (int b = 0; b < BITS; ++b) {
-#pragma unroll
-        for (int q = 0; q < SL; ++q) {
-            const uint64_t m = __builtin_amdgcn_ballot_w64(act && ((pm.v[q] >> b) & 1));
-#pragma unroll
-            for (int r = 0; r < SL; ++r) {
-                mr[r][q] &= ((pm.v[r] >> b) & 1) ? m : ~m;
-                mo[r][q] &= (((lane * SL + r) >> b) & 1) ? m : ~m;
-            }
-        }
+        for (int q = 0; q < SL; ++q)
+            __hip_atomic_fetch_or(MT[q] + pm.v[q], 1ull << lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
     }
+    wave_sync();
     int rank[SL], cnt[SL];
 #pragma unroll
     for (int r = 0; r < SL; ++r) {
         int rk = 0, c = 0;
+        if (act) {
 #pragma unroll
-        for (int q = 0; q < SL; ++q) {
-            rk += __builtin_popcountll(mr[r][q] & lt);
-            if (q < r) rk += pm.v[q] == pm.v[r] ? 1 : 0;
-            c += __builtin_popcountll(mo[r][q]);
+            for (int q = 0; q < SL; ++q) {
+                rk += __builtin_popcountll(MT[q][pm.v[r]] & lt);
+                if (q < r) rk += pm.v[q] == pm.v[r] ? 1 : 0;
+                c += __builtin_popcountll(MT[q][lane * SL + r]);
+            }
         }
         rank[r] = rk;
-        cnt[r] = act ? c : 0;
+        cnt[r] = c;
     }
     int tot = 0;
 #pragma unroll
@@ -778,7 +770,16 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                 if constexpr (AGG) s.agm[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
             }
         }
-        if constexpr (!(G == 1 && !FB)) publish_sorted_map<N>(s, slot, pm, lane, act, reinterpret_cast<int*>(X));
+        if constexpr (!(G == 1 && !FB)) {
+            uint64_t* mt[SL];
+            mt[0] = reinterpret_cast<uint64_t*>(CS);
+            if constexpr (SL > 1) mt[1] = reinterpret_cast<uint64_t*>(CS + W * N);
+            if constexpr (SL > 2) {
+                mt[2] = reinterpret_cast<uint64_t*>(st.Z);
+                mt[3] = reinterpret_cast<uint64_t*>(st.V);  // rows 0..N-1: the zero row V[N] stays
+            }
+            publish_sorted_map<N>(s, slot, pm, lane, act, reinterpret_cast<int*>(X), mt);
+        }
         wave_sync();
         if (lane == 0) publish_ready(s.aflag + slot, lc);
     }
