@@ -119,10 +119,22 @@ def cpu_baseline(w, inp, target_s=12.0, max_threads=16, sample_seqs=32):
             if time.perf_counter() - t0 >= target_s:
                 break
     wall = time.perf_counter() - t0
+    # the same oracle on one thread: whole sequences one after another
+    one_su, one_n = 0, 0
+    t1 = time.perf_counter()
+    while True:
+        one_su += one(subs[one_n % len(subs)])
+        one_n += 1
+        if time.perf_counter() - t1 >= target_s / 4:
+            break
+    one_wall = time.perf_counter() - t1
     return {"value": done_su / wall, "unit": "state-updates/s", "cores": threads, "kind": "oracle",
             "sample": "fwd+bwd float64 oracle on %d of %d whole sequences (L=%d, N=%d), "
                       "cycled %d times on %d threads, %.1f s wall"
-                      % (len(subs), len(seqs), w.L, w.N, rounds, threads, wall)}
+                      % (len(subs), len(seqs), w.L, w.N, rounds, threads, wall),
+            "single_thread": {"value": one_su / one_wall, "unit": "state-updates/s",
+                              "sample": "%d whole sequences one after another on one thread, %.1f s wall"
+                                        % (one_n, one_wall)}}
 
 
 def traffic_from_profiles(kernel, workload_name):
