@@ -280,13 +280,12 @@ __device__ __forceinline__ void gather_rows(const float2* V, const uint64_t* rec
     }
 }
 
-// acc += sum over the G listed sources of the staged values V, for a record
-// already in registers.
-template <int G>
-__device__ __forceinline__ void gather_rec(const float2* V, uint64_t r, float2& acc) {
+// acc += the sources M0 .. M1-1 of a record already in registers.
+template <int M0, int M1>
+__device__ __forceinline__ void gather_rec_range(const float2* V, uint64_t r, float2& acc) {
     const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
 #pragma unroll
-    for (int m = 0; m < G; ++m) {
+    for (int m = M0; m < M1; ++m) {
         const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
         const float2 v = V[src];
         acc.x += v.x;
@@ -672,7 +671,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
         }
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t);
+            const int k = readlane_i(q.kv, t), gk = readlane_i(q.mv, t);
             float2* CSt = CS + (t & 1) * (W * N);
             const float2* CSp = CS + ((t + 1) & 1) * (W * N);
             const CV<SL> Dv = Dt(q, t);
@@ -689,19 +688,35 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
             wave_sync();
             float part = 0.f;
             if (act) {
+                // the first GM sources of every row with the step's other
+                // reads in one batch; the 7-source class reads the rest only
+                // at steps whose map has a row with more than GM sources
+                constexpr int GM = G > 4 ? 4 : G;
+                float2 acc[SL], Dp[SL], Cp[SL];
+                int np[SL];
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
-                    float2 acc = q.b[t].v[r];
-                    gather_rec<G>(st.V, rec[t][r], acc);
+                    acc[r] = q.b[t].v[r];
+                    gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
                     const int p = pm.v[r];
-                    const float2 Dp = st.Z[p];
-                    const int np = s.dict[k * N + p];
-                    if constexpr (!AGG) {
-                        if (t > 0) wt[t - 1].v[r] = cmul(dm.v[r], CSp[p]);
+                    Dp[r] = st.Z[p];
+                    np[r] = s.dict[k * N + p];
+                    if constexpr (!AGG) Cp[r] = CSp[p];
+                }
+                if constexpr (G > GM) {
+                    if (gk > GM) {
+#pragma unroll
+                        for (int r = 0; r < SL; ++r) gather_rec_range<GM, G>(st.V, rec[t][r], acc[r]);
                     }
-                    Bm.v[r] = acc;
-                    dm.v[r] = cmul(Dp, dm.v[r]);
-                    pm.v[r] = np;
+                }
+#pragma unroll
+                for (int r = 0; r < SL; ++r) {
+                    if constexpr (!AGG) {
+                        if (t > 0) wt[t - 1].v[r] = cmul(dm.v[r], Cp[r]);
+                    }
+                    Bm.v[r] = acc[r];
+                    dm.v[r] = cmul(Dp[r], dm.v[r]);
+                    pm.v[r] = np[r];
                     if constexpr (!AGG) part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
                 }
             } else if constexpr (!AGG) {
