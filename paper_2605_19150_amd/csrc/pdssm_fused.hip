@@ -627,6 +627,47 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_fwd(const FusedArgs& a, cons
     return carry;
 }
 
+// A wave's running fold in the aggregate pass: map, diagonal and local state
+// of the chunks it has folded so far (identity and zero at its first one).
+template <int SL>
+struct RunState {
+    IV<SL> pm;
+    CV<SL> dm, Bm;
+};
+
+// Writes an operator (local state Bm, diagonal dm, map pm) into operator slot
+// `slot` (and its sorted map, many-to-one heads), then raises the slot's flag
+// to `flag`.  AGG also keeps the plain map for the frontier's composition.
+template <int N, int W, int G, bool FB, bool AGG>
+__device__ __forceinline__ void publish_op(const Smem& s, int wv, int slot, int flag, const IV<Lay<N>::SL>& pm,
+                                           const CV<Lay<N>::SL>& dm, const CV<Lay<N>::SL>& Bm, int lane, bool act) {
+    constexpr int SL = Lay<N>::SL;
+    const Stage st = stage_of<N>(s, wv);
+    float2* X = s.x + wv * N;
+    float2* CS = s.cs + wv * N;
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            s.agg[slot * N + lane * SL + r] = make_float4(Bm.v[r].x, Bm.v[r].y, dm.v[r].x, dm.v[r].y);
+            if constexpr (G == 1 && !FB) s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
+            if constexpr (AGG) s.agm[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
+        }
+    }
+    if constexpr (!(G == 1 && !FB)) {
+        uint64_t* mt[SL];
+        mt[0] = reinterpret_cast<uint64_t*>(CS);
+        if constexpr (SL > 1) mt[1] = reinterpret_cast<uint64_t*>(CS + W * N);
+        if constexpr (SL > 2) {
+            mt[2] = reinterpret_cast<uint64_t*>(st.Z);
+            mt[3] = reinterpret_cast<uint64_t*>(st.V);  // rows 0..N-1: the zero row V[N] stays
+        }
+        publish_sorted_map<N>(s, slot, pm, lane, act, reinterpret_cast<int*>(X), mt);
+    }
+    wave_sync();
+    if (lane == 0) publish_ready(s.aflag + slot, flag);
+}
+
 // One chunk is run once, from a zero state (Algorithm 1 Phase A), while the
 // readout is split as in Phase C: with M_t = A_t ... A_s in PD form
 // (Pi_t, Delta_t) and x_t = x_t^loc + M_t carry,
@@ -634,10 +675,12 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_fwd(const FusedArgs& a, cons
 // The wave keeps w_t and the local readout partials, hands the carry on as
 // soon as the chunk is folded, and finishes y once its own carry arrives.
 // AGG: the aggregate pass of a segment -- the wave only builds and publishes
-// the chunk operator (c is not loaded, no readout).
-template <int N, int TAU, int W, int G, bool FB, bool AGG>
+// the chunk operator (c is not loaded, no readout).  RUN (with AGG): the pass
+// starts from and returns to *run instead, and publishes nothing.
+template <int N, int TAU, int W, int G, bool FB, bool AGG, bool RUN = false>
 __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int lc,
-                                          Chunk<N, TAU>& q, bool& bad) {
+                                          Chunk<N, TAU>& q, bool& bad, RunState<Lay<N>::SL>* run = nullptr) {
+    static_assert(!RUN || AGG, "a run fold is an aggregate pass");
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
@@ -654,6 +697,11 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     for (int r = 0; r < SL; ++r) {
         pm.v[r] = lane * SL + r;
         dm.v[r] = make_float2(1.f, 0.f);
+    }
+    if constexpr (RUN) {
+        pm = run->pm;
+        dm = run->dm;
+        Bm = run->Bm;
     }
     CV<SL> wt[TAU];
     float yl[TAU];
@@ -773,30 +821,16 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     // rewritten with carry_{lc+W+1} only after the frontier took operator
     // lc + W from this same wave, which this wave publishes after its read
     // of carry_lc below (one wave's LDS accesses complete in order).
+    if constexpr (RUN) {
+        run->pm = pm;
+        run->dm = dm;
+        run->Bm = Bm;
+        return;
+    }
     {
         const int slot = lc % (2 * W);
         if constexpr (AGG) wait_ready(s.ready, lc - 2 * W + 1, a.status, s.ready, 1 + 2 * W);
-        wave_sync();
-        if (act) {
-#pragma unroll
-            for (int r = 0; r < SL; ++r) {
-                s.agg[slot * N + lane * SL + r] = make_float4(Bm.v[r].x, Bm.v[r].y, dm.v[r].x, dm.v[r].y);
-                if constexpr (G == 1 && !FB) s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
-                if constexpr (AGG) s.agm[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
-            }
-        }
-        if constexpr (!(G == 1 && !FB)) {
-            uint64_t* mt[SL];
-            mt[0] = reinterpret_cast<uint64_t*>(CS);
-            if constexpr (SL > 1) mt[1] = reinterpret_cast<uint64_t*>(CS + W * N);
-            if constexpr (SL > 2) {
-                mt[2] = reinterpret_cast<uint64_t*>(st.Z);
-                mt[3] = reinterpret_cast<uint64_t*>(st.V);  // rows 0..N-1: the zero row V[N] stays
-            }
-            publish_sorted_map<N>(s, slot, pm, lane, act, reinterpret_cast<int*>(X), mt);
-        }
-        wave_sync();
-        if (lane == 0) publish_ready(s.aflag + slot, lc);
+        publish_op<N, W, G, FB, AGG>(s, wv, slot, lc, pm, dm, Bm, lane, act);
     }
     if constexpr (AGG) return;
     wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * W);
@@ -1015,14 +1049,64 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
-    if (wv == W) {
-        fwd_frontier<N, W, G, FB, AGG>(a, s, w);
-        return;
-    }
     auto issue = [&](int lc, Chunk<N, TAU>& q) {
         issue_chunk<N, TAU, true, !AGG, kLoadStream, IO>(a, w.bb, w.hh, lc < w.nc ? w.c0 + lc : a.C, lane, act, q);
     };
     bool bad = false;
+    if constexpr (AGG) {
+        // The aggregate needs no chunk-by-chunk hand-off: wave wv folds a
+        // contiguous run of chunks, carrying map, diagonal and local state
+        // from chunk to chunk, and publishes the run's operator in slot wv
+        // (flag wv); the frontier composes the runs in order, as it would
+        // chunks.  Runs <= W < 2W slots, so no slot is reused.  The cut into
+        // at most kFusedWaves runs does not depend on W, so the wide kernels
+        // of the 4-byte formats add in the same order as complex64's (same
+        // bits on the same values).
+        constexpr int SL = Lay<N>::SL, RUNS = W < kFusedWaves ? W : kFusedWaves;
+        const int per = max(1, (w.nc + RUNS - 1) / RUNS);
+        const int runs = (w.nc + per - 1) / per;
+        if (wv == W) {
+            Work wr = w;
+            wr.nc = runs;
+            fwd_frontier<N, W, G, FB, true>(a, s, wr);
+            return;
+        }
+        if (wv >= runs) return;
+        const int r0 = wv * per, r1 = min(w.nc, r0 + per);
+        RunState<SL> rs;
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            rs.pm.v[r] = lane * SL + r;
+            rs.dm.v[r] = make_float2(1.f, 0.f);
+            rs.Bm.v[r] = make_float2(0.f, 0.f);
+        }
+        if constexpr (PREFETCH) {
+            Chunk<N, TAU> qa, qb;
+            issue(r0, qa);
+            for (int lc = r0; lc < r1; lc += 2) {
+                issue(lc + 1 < r1 ? lc + 1 : w.nc, qb);
+                issue_fence();
+                fwd_chunk<N, TAU, W, G, FB, true, true>(a, s, w, lc, qa, bad, &rs);
+                if (lc + 1 >= r1) break;
+                issue(lc + 2 < r1 ? lc + 2 : w.nc, qa);
+                issue_fence();
+                fwd_chunk<N, TAU, W, G, FB, true, true>(a, s, w, lc + 1, qb, bad, &rs);
+            }
+        } else {
+            for (int lc = r0; lc < r1; ++lc) {
+                Chunk<N, TAU> q;
+                issue(lc, q);
+                fwd_chunk<N, TAU, W, G, FB, true, true>(a, s, w, lc, q, bad, &rs);
+            }
+        }
+        publish_op<N, W, G, FB, true>(s, wv, wv, wv, rs.pm, rs.dm, rs.Bm, lane, act);
+        if (bad) report_index_error(a.status);
+        return;
+    }
+    if (wv == W) {
+        fwd_frontier<N, W, G, FB, AGG>(a, s, w);
+        return;
+    }
     if constexpr (PREFETCH) {
         Chunk<N, TAU> qa, qb;
         issue(wv, qa);
@@ -1057,7 +1141,9 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
-    constexpr bool PF = fused_prefetch(N, TAU);
+    // The aggregate pass loads D and b only and keeps no readout state: its
+    // runs prefetch the next chunk at every N (measured registers fit).
+    constexpr bool PF = fused_prefetch(N, TAU) || AGG;
     if (fb) fwd_body<N, TAU, W, 7, true, PF, AGG, IO>(a, s, w);
     else if (G == 1) fwd_body<N, TAU, W, 1, false, PF, AGG, IO>(a, s, w);
     else if (G == 3) fwd_body<N, TAU, W, 3, false, PF, AGG, IO>(a, s, w);
