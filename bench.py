@@ -7,18 +7,25 @@ One step = dictionary preparation (pdssm_prepare), one forward scan
 (pdssm_scan_bwd: dD, db, dc, dh0) over one batch of seeded synthetic inputs
 already resident in HBM.  A 512 MiB buffer is rewritten between steps (not
 timed) so that no input of a step is still cached.  The default 200 untimed
-steps let the GPU clocks settle (the compute-heavier workloads run up to 20%
-slower during the first ~100 ms of load); then 50 steps are timed.  Prints
-ONE JSON line.
+steps, preceded by at least 0.3 s of the same step (clock_settle in the line;
+also with a short --warmup), let the GPU clocks settle: the compute-heavier
+workloads run up to 20% slower during the first ~100 ms of load.  Then 50
+steps are timed.  Prints ONE JSON line.
 
-value = state updates (B*L*H*N) per second of the whole step.
-roofline = the dominant kernel's algorithmic bytes (every input read once,
-every output written once) over its average duration, measured with HIP
-events on the stream the kernels are launched on, against the 8 TB/s HBM
-peak; traffic = the HBM bytes per launch that rocprofv3 counters measured for
-the same kernel source (profiles/), else null.
-cpu_baseline = the float64 oracle timed on a bounded sample of the same
-workload on this host's cores.
+value = state updates (B*L*H*N) per second of the whole step (mean step
+time; every call also reports its median).
+roofline = the dominant kernel's algorithmic bytes (each tensor of the method
+read or written once: 24 + 8/N bytes per state update forward, 48 + 8/N
+backward, in complex64) over its average duration, measured with HIP events
+on the stream the kernels are launched on, against the 8 TB/s HBM peak;
+traffic = the HBM bytes per launch that rocprofv3 counters measured for the
+same kernel source (profiles/), else null.  The chunk-entering states handed
+from the forward to the backward are reported apart (design_bytes).
+markov_manyone = with the default workload, the many-to-one workload of the
+same shape (L=2048, d=1024 as 16 heads of 64, Markov-chain map choices),
+timed the same way in the same run.
+cpu_baseline = the float64 oracle timed on this host: whole passes over every
+sequence of the workload on the 16-core CPU share of a one-GPU machine.
 
 --ste times the straight-through training step instead (Sec. 3.1 Prop. 2):
 prepare, forward, the backward with the scaled states (pdssm_scan_bwd_ste),
@@ -45,24 +52,34 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_FP32_PEAK_TFS = 157.3
 FLUSH_BYTES = 512 << 20
+SETTLE_S = 0.3  # untimed sustained load before the warm-up steps (clock ramp)
 METRIC = "PD-scan state-updates/s (B*L*H*N) fwd and fwd+bwd; achieved HBM GB/s vs peak"
 
 
 def alg_bytes(w, C, op, esz=8, ssz=8):
-    """Algorithmic HBM bytes of one call: inputs read once, outputs written
-    once.  esz = bytes per entry of D, b, c, dD, db, dc (8 for complex64, 4
-    for bf16 pairs or the real model); ssz = bytes per state entry of h_final,
-    saved and dh0 (8, or 4 for the real model, whose states are real although
-    the library keeps them as complex64); y and dy are fp32 always."""
+    """Algorithmic HBM bytes of one call: every tensor of the method read or
+    written once.  Forward: idx, D, b, c and the dictionary in; y and h_final
+    out (24 + 8/N bytes per state update in complex64).  Backward: idx, dy,
+    D, b, c and the dictionary in; dD, db, dc and dh0 out (48 + 8/N).  The
+    chunk-entering states that the forward hands to the backward are this
+    design's own intermediate, not the method's, and are counted apart
+    (design_bytes).  esz = bytes per entry of D, b, c, dD, db, dc (8 for
+    complex64, 4 for bf16 pairs or the real model); ssz = bytes per state
+    entry of h_final and dh0 (8, or 4 for the real model, whose states are
+    real although the library keeps them as complex64); y and dy are fp32."""
     B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
     steps = B * L * H
     su = steps * N
     dict_b = H * K * N * 4
     if op == "fwd":
-        # idx, D, b, c in; y, h_final, saved out
-        return steps * 4 + 3 * su * esz + dict_b + steps * 4 + B * H * N * ssz + B * H * C * N * ssz
-    # idx, dy, D, b, c, saved in; dD, db, dc, dh0 out
-    return steps * 8 + 3 * su * esz + dict_b + B * H * C * N * ssz + 3 * su * esz + B * H * N * ssz
+        return steps * 4 + 3 * su * esz + dict_b + steps * 4 + B * H * N * ssz
+    return steps * 8 + 3 * su * esz + dict_b + 3 * su * esz + B * H * N * ssz
+
+
+def saved_bytes(w, C, ssz=8):
+    """The chunk-entering states: written once by the forward, read once by
+    the backward (ssz bytes per entry, C chunks per sequence)."""
+    return w.B * w.H * C * w.N * ssz
 
 
 def ste_bytes(w, C, real=False):
@@ -84,57 +101,86 @@ def ste_bytes(w, C, real=False):
     }
 
 
-def cpu_baseline(w, inp, target_s=12.0, max_threads=16, sample_seqs=32):
+def host_cpu():
+    """What the host offers: nproc (the cores this process may run on), the
+    machine's logical CPU count and the CPU model."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        nproc = len(os.sched_getaffinity(0))
+    except AttributeError:
+        nproc = os.cpu_count() or 1
+    return {"nproc": nproc, "logical_cpus": os.cpu_count(), "model": model}
+
+
+# A one-GPU box grants its job a 16-core share of the host, whatever nproc
+# shows; the oracle's thread pool uses that share.
+CPU_SHARE = 16
+
+
+def cpu_baseline(w, inp, target_s=12.0):
     """Time the float64 oracle (fwd + bwd, one whole sequence per task) on
-    this host: a fixed sample of the workload's sequences, cycled over a pool
-    of threads (the oracle's C loops run without the GIL) until about
-    target_s seconds of wall time have passed."""
+    this host: whole passes over every sequence of the workload on a pool of
+    threads (the oracle's C loops run without the GIL), repeated until about
+    target_s seconds have passed; the median pass gives the rate.  Then the
+    same oracle on one thread, whole sequences one after another (median
+    sequence time)."""
     from concurrent.futures import ThreadPoolExecutor
 
     from oracle import oracle_bwd, oracle_fwd
     from paper_2605_19150_amd.inputs import sub_sequence
     seqs = [(bb, hh) for bb in range(w.B) for hh in range(w.H)]
-    step = max(1, len(seqs) // sample_seqs)
-    picked = seqs[::step][:sample_seqs]
     subs = []
-    for bb, hh in picked:
+    for bb, hh in seqs:
         sub = sub_sequence(inp, bb, hh)
         for k in ("D", "b", "c"):
             sub[k] = sub[k].astype(np.complex128)
         sub["dy"] = sub["dy"].astype(np.float64)
         subs.append(sub)
-    threads = max(1, min(max_threads, os.cpu_count() or 1))
+    host = host_cpu()
+    threads = max(1, min(CPU_SHARE, host["nproc"]))
 
     def one(sub):
         oracle_fwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"])
         oracle_bwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"], sub["dy"])
         return w.L * w.N
 
-    done_su, rounds = 0, 0
+    passes = []
     t0 = time.perf_counter()
     with ThreadPoolExecutor(max_workers=threads) as pool:
         while True:
-            done_su += sum(pool.map(one, subs))
-            rounds += 1
-            if time.perf_counter() - t0 >= target_s:
+            t = time.perf_counter()
+            done = sum(pool.map(one, subs))
+            passes.append(time.perf_counter() - t)
+            if time.perf_counter() - t0 >= target_s and len(passes) >= 3:
                 break
     wall = time.perf_counter() - t0
+    med = float(np.median(passes))
     # the same oracle on one thread: whole sequences one after another
-    one_su, one_n = 0, 0
+    per_seq = []
     t1 = time.perf_counter()
-    while True:
-        one_su += one(subs[one_n % len(subs)])
-        one_n += 1
-        if time.perf_counter() - t1 >= target_s / 4:
-            break
-    one_wall = time.perf_counter() - t1
-    return {"value": done_su / wall, "unit": "state-updates/s", "cores": threads, "kind": "oracle",
-            "sample": "fwd+bwd float64 oracle on %d of %d whole sequences (L=%d, N=%d), "
-                      "cycled %d times on %d threads, %.1f s wall"
-                      % (len(subs), len(seqs), w.L, w.N, rounds, threads, wall),
-            "single_thread": {"value": one_su / one_wall, "unit": "state-updates/s",
-                              "sample": "%d whole sequences one after another on one thread, %.1f s wall"
-                                        % (one_n, one_wall)}}
+    while time.perf_counter() - t1 < target_s / 4 or len(per_seq) < 3:
+        t = time.perf_counter()
+        one(subs[len(per_seq) % len(subs)])
+        per_seq.append(time.perf_counter() - t)
+    one_med = float(np.median(per_seq))
+    return {"value": done / med, "unit": "state-updates/s", "cores": threads, "kind": "oracle",
+            "sample": "fwd+bwd float64 oracle on all %d sequences of the workload (L=%d, N=%d) per pass, "
+                      "%d passes on %d threads (median pass %.3f s), %.1f s wall"
+                      % (len(subs), w.L, w.N, len(passes), threads, med, wall),
+            "host": host,
+            "note": "thread pool = the %d-core CPU share of a one-GPU box (nproc %d)"
+                    % (CPU_SHARE, host["nproc"]),
+            "single_thread": {"value": w.L * w.N / one_med, "unit": "state-updates/s",
+                              "sample": "%d whole sequences one after another on one thread "
+                                        "(median %.4f s per sequence)" % (len(per_seq), one_med)}}
 
 
 def traffic_from_profiles(kernel, workload_name):
@@ -264,6 +310,8 @@ def main():
                     help="untimed steps first: the GPU clocks ramp up over the first ~100 ms of load")
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-second-leg", action="store_true",
+                    help="with the default workload, skip timing the many-to-one workload of the same shape")
     ap.add_argument("--only", choices=["fwd", "bwd", "both"], default="both",
                     help="profiling aid: launch only one call per step")
     ap.add_argument("--ste", action="store_true",
@@ -314,15 +362,51 @@ def main():
     if args.front:
         front_bench(args, w, dev)
         return
-    print("bench: workload %d (%s): generating inputs" % (args.workload, w.name), file=sys.stderr,
-          flush=True)
     if args.real and args.bf16:
         sys.exit("bench.py: --real and --bf16 do not combine (one row format at a time)")
-    inp = workload_inputs(args.workload, seed=0, real=args.real)
+    if args.bf16 and args.ste:
+        sys.exit("bench.py: --bf16 and --ste do not combine (the straight-through path is complex64)")
+    # Written between timed steps so that no input is still in L2 / MALL.
+    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    res, inp = time_scan(args, args.workload, dev, flush)
+    out = scan_line(args, w, res)
+    out["device"] = torch.cuda.get_device_name(dev)
+    plain = args.only == "both" and not args.ste and not args.bf16 and not args.real
+    if plain and args.workload == 2 and not args.no_second_leg:
+        # the second workload of the same shape (L=2048, d=1024 as 16 heads
+        # of 64): many-to-one maps chosen by a Markov chain, timed the same way
+        w3 = WORKLOADS[3]
+        del inp
+        res3, inp = time_scan(args, 3, dev, flush)
+        leg = scan_line(args, w3, res3)
+        out["markov_manyone"] = {k: leg[k] for k in ("ms_per_step", "ms_per_step_median", "value", "prepare",
+                                                      "fwd", "bwd", "fwd_bwd")}
+        out["markov_manyone"]["workload"] = w3.name
+        out["markov_manyone"]["chunk"] = leg["config"]["chunk"]
+        if not args.no_cpu_baseline:
+            inp = None
+    if not args.no_cpu_baseline and plain:
+        if inp is None:
+            from paper_2605_19150_amd.inputs import workload_inputs
+            inp = workload_inputs(args.workload, seed=0)
+        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(out), flush=True)
+
+
+def time_scan(args, wi, dev, flush):
+    """Time args.steps steps of workload wi after args.warmup untimed ones;
+    every call bracketed by HIP events on the stream the kernels run on.
+    Returns (per-call times and the Scan, the host inputs)."""
+    import torch
+    from paper_2605_19150_amd import pdssm
+    from paper_2605_19150_amd.inputs import WORKLOADS, workload_inputs
+
+    w = WORKLOADS[wi]
+    print("bench: workload %d (%s): generating inputs" % (wi, w.name), file=sys.stderr, flush=True)
+    inp = workload_inputs(wi, seed=0, real=args.real)
     T = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
     if args.bf16:
-        if args.ste:
-            sys.exit("bench.py: --bf16 and --ste do not combine (the straight-through path is complex64)")
         for k in ("D", "b", "c"):
             T[k] = torch.view_as_real(T[k]).to(torch.bfloat16).contiguous()
     s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste, bf16=args.bf16, real=args.real)
@@ -332,8 +416,6 @@ def main():
         T["logits"], T["M"] = torch.from_numpy(logits).to(dev), torch.from_numpy(M).to(dev)
         dlogits, dM = torch.empty_like(T["logits"]), torch.empty_like(T["M"])
     stream = torch.cuda.current_stream()
-    # Written between timed steps so that no input is still in L2 / MALL.
-    flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
 
     def step(ev=None):
         rec = (lambda i: ev[i].record(stream)) if ev is not None else (lambda i: None)
@@ -359,6 +441,19 @@ def main():
     if args.only == "bwd":
         s.prepare(T["pi"])
         s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+    # The GPU clocks ramp up over the first ~100 ms of sustained load: the
+    # same step runs for at least SETTLE_S seconds before the W warm-up steps
+    # (untimed; the timed region is the K steps below either way).
+    settle, t_settle = 0, time.perf_counter()
+    while True:
+        flush.fill_(1.0)
+        step()
+        settle += 1
+        if settle % 8 == 0:
+            torch.cuda.synchronize()
+            if time.perf_counter() - t_settle >= SETTLE_S:
+                break
+    settle_s = time.perf_counter() - t_settle
     for _ in range(args.warmup):
         flush.fill_(1.0)
         step()
@@ -375,24 +470,48 @@ def main():
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    prep_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    fwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
-    ms_step = float(np.mean([e[0].elapsed_time(e[nev - 1]) for e in evs]))
     s.check_status()
+    ms = lambda a, b: np.array([e[a].elapsed_time(e[b]) for e in evs])  # noqa: E731
+    res = {"scan": s, "wall": wall, "prepare": ms(0, 1), "fwd": ms(1, 2), "bwd": ms(2, 3),
+           "step": ms(0, nev - 1), "settle": {"steps": settle, "s": settle_s}}
+    if args.ste:
+        res["ste_grads"] = ms(3, 4)
+        res["softmax"] = ms(4, 5)
+    return res, inp
 
+
+def scan_line(args, w, res):
+    """The bench line of one timed workload: means (the roofline's kernel
+    durations) and medians of every call, algorithmic bytes and fractions of
+    the HBM peak."""
+    s = res["scan"]
+    mean = lambda k: float(np.mean(res[k]))  # noqa: E731
+    med = lambda k: float(np.median(res[k]))  # noqa: E731
     su = w.state_updates
     esz = 4 if (args.bf16 or args.real) else 8
     ssz = 4 if args.real else 8
     fwd_b, bwd_b = alg_bytes(w, s.C, "fwd", esz, ssz), alg_bytes(w, s.C, "bwd", esz, ssz)
+    sv_b = saved_bytes(w, s.C, ssz)
     fused = s.fused
     kern = {"fwd": "k_fwd_fused" if fused else "k_fwd_*(chunked)",
             "bwd": "k_bwd_fused" if fused else "k_bwd_*(chunked)"}
+    fwd_ms, bwd_ms = mean("fwd"), mean("bwd")
     dom = "bwd" if (bwd_ms >= fwd_ms and args.only != "fwd") else "fwd"
     dom_ms, dom_b = (bwd_ms, bwd_b) if dom == "bwd" else (fwd_ms, fwd_b)
     achieved = dom_b / (dom_ms * 1e-3) / 1e9
     suffix = "_bf16" if args.bf16 else ("_real" if args.real else "")
     traffic = traffic_from_profiles(kern[dom] + suffix, w.name) if fused else None
+
+    def call(k, nbytes):
+        m, d = mean(k), med(k)
+        return {"kernel": kern[k], "ms": m, "ms_median": d, "state_updates_per_s": su / (m * 1e-3),
+                "alg_bytes": nbytes, "alg_GBps": nbytes / (m * 1e-3) / 1e9,
+                "frac": nbytes / (m * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "frac_median": nbytes / (d * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                "design_bytes": nbytes + sv_b}
+
+    ms_step, ms_step_med = mean("step"), med("step")
+    fb_ms, fb_med = fwd_ms + bwd_ms, med("fwd") + med("bwd")
     out = {
         "metric": METRIC,
         "value": su / (ms_step * 1e-3),
@@ -401,57 +520,61 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_median": ms_step_med,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16-io/f32" if args.bf16 else ("f32-real" if args.real else "f32"),
         "data": "synthetic (seeded, shapes and distributions of the named workload)",
-        "config": {"workload": w.name + (" (real-valued model)" if args.real else ""), "B": w.B, "L": w.L, "H": w.H, "N": w.N, "K": w.K,
-                   "chunk": s.chunk,
+        "config": {"workload": w.name + (" (real-valued model)" if args.real else ""), "B": w.B, "L": w.L,
+                   "H": w.H, "N": w.N, "K": w.K, "chunk": s.chunk, "segments": s.segments,
                    "step": ("prepare+fwd+bwd_ste+ste_grads+softmax_vjp" if args.ste else "prepare+fwd+bwd")
                    if args.only == "both" else args.only,
                    "global_batch": w.B, "seq_len": w.L, "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "kernel": kern[dom],
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic},
-        "prepare": {"ms": prep_ms},
-        "fwd": {"kernel": kern["fwd"], "ms": fwd_ms, "state_updates_per_s": su / (fwd_ms * 1e-3),
-                "alg_bytes": fwd_b, "alg_GBps": fwd_b / (fwd_ms * 1e-3) / 1e9,
-                "frac": fwd_b / (fwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        "bwd": {"kernel": kern["bwd"], "ms": bwd_ms, "state_updates_per_s": su / (bwd_ms * 1e-3),
-                "alg_bytes": bwd_b, "alg_GBps": bwd_b / (bwd_ms * 1e-3) / 1e9,
-                "frac": bwd_b / (bwd_ms * 1e-3) / 1e9 / HBM_PEAK_GBS},
-        "fwd_bwd_alg_GBps": (fwd_b + bwd_b) / (ms_step * 1e-3) / 1e9 if not args.ste else None,
-        "wall_s_timed": wall,
-        "device": torch.cuda.get_device_name(dev),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "bytes": "algorithmic: %s (%.1f + 8/N bytes per state update)"
+                              % ("idx, dy, D, b, c in; dD, db, dc, dh0 out" if dom == "bwd"
+                                 else "idx, D, b, c in; y, h_final out", (48.0 if dom == "bwd" else 24.0) * esz / 8)},
+        "prepare": {"ms": mean("prepare"), "ms_median": med("prepare")},
+        "fwd": call("fwd", fwd_b),
+        "bwd": call("bwd", bwd_b),
+        "fwd_bwd": {"ms": fb_ms, "ms_median": fb_med, "alg_bytes": fwd_b + bwd_b,
+                    "state_updates_per_s": su / (fb_ms * 1e-3),
+                    "frac": (fwd_b + bwd_b) / (fb_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                    "frac_median": (fwd_b + bwd_b) / (fb_med * 1e-3) / 1e9 / HBM_PEAK_GBS},
+        "design_bytes": {"saved_states": sv_b,
+                         "note": "chunk-entering states written by the forward and read by the backward; "
+                                 "part of each call's traffic, not of its algorithmic bytes"},
+        "wall_s_timed": res["wall"],
+        "clock_settle": res["settle"],
     }
     if args.ste:
         sb = ste_bytes(w, s.C, real=args.real)
+        out["fwd_bwd"] = None
         out["bwd"]["alg_bytes"] = sb["bwd_ste"]
         out["bwd"]["kernel"] = kern["bwd"] + " (+ z)"
         out["bwd"]["alg_GBps"] = sb["bwd_ste"] / (bwd_ms * 1e-3) / 1e9
         out["bwd"]["frac"] = out["bwd"]["alg_GBps"] / HBM_PEAK_GBS
+        out["bwd"]["frac_median"] = sb["bwd_ste"] / (med("bwd") * 1e-3) / 1e9 / HBM_PEAK_GBS
         out["roofline"]["achieved"] = out["bwd"]["alg_GBps"] if dom == "bwd" else achieved
         out["roofline"]["frac"] = out["roofline"]["achieved"] / HBM_PEAK_GBS
         out["roofline"]["traffic"] = traffic_from_profiles("k_bwd_fused_ste" + suffix, w.name) if fused else None
         out["roofline"]["kernel"] = kern[dom] + (" (+ z)" if dom == "bwd" else "")
-        dg_ms = float(np.mean([e[3].elapsed_time(e[4]) for e in evs]))
-        sm_ms = float(np.mean([e[4].elapsed_time(e[5]) for e in evs]))
+        dg_ms, sm_ms = mean("ste_grads"), mean("softmax")
         gbps = sb["ste_grads"] / (dg_ms * 1e-3) / 1e9
         tfs = sb["ste_grads_flops"] / (dg_ms * 1e-3) / 1e12
         out["ste"] = {
             "temp": args.temp,
-            "ste_grads": {"ms": dg_ms, "alg_bytes": sb["ste_grads"], "alg_GBps": gbps,
-                          "frac_hbm": gbps / HBM_PEAK_GBS, "flops": sb["ste_grads_flops"],
+            "ste_grads": {"ms": dg_ms, "ms_median": med("ste_grads"), "alg_bytes": sb["ste_grads"],
+                          "alg_GBps": gbps, "frac_hbm": gbps / HBM_PEAK_GBS, "flops": sb["ste_grads_flops"],
                           "TFLOPs": tfs, "frac_mfma_fp32": tfs / MFMA_FP32_PEAK_TFS,
                           "traffic": traffic_from_profiles("k_ste_gemm" + suffix, w.name)},
-            "softmax_vjp": {"ms": sm_ms, "alg_bytes": sb["softmax"],
+            "softmax_vjp": {"ms": sm_ms, "ms_median": med("softmax"), "alg_bytes": sb["softmax"],
                             "alg_GBps": sb["softmax"] / (sm_ms * 1e-3) / 1e9},
         }
-    if not args.no_cpu_baseline and args.only == "both" and not args.ste and not args.bf16 and not args.real:
-        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, inp)
-    print(json.dumps(out), flush=True)
+    return out
 
 
 if __name__ == "__main__":

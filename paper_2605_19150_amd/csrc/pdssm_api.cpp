@@ -113,13 +113,14 @@ int narrow_if_needed(const pdssm_desc* d, int W) {
 
 int bwd_waves(const pdssm_desc* d, int tau) { return narrow_if_needed(d, pdssm::fused_waves_bwd(d->N, tau)); }
 
-// Chunk waves of the fused forward: the wide count for the 4-byte row
-// formats (their forward waits on its chunk passes, not on HBM) when the
-// prefetching kernel runs and its tables leave room for the minimum
-// saved-state staging.  Complex64 rows keep 7 (measured 3% faster at
-// fsa-perm, where the forward is HBM-bound).
+// Chunk waves of the fused forward: the wide count when the prefetching
+// kernel runs and its tables leave room for the minimum saved-state staging.
+// More waves in flight cover the chunk passes of many-to-one maps (which
+// bound their forward) and of the 4-byte row formats; in complex64 a head of
+// permutations, bound by HBM, runs kPermWaves of them on a layout of its
+// own (measured: markov-manyone 168 -> 154 us, fsa-perm unchanged).
 int fwd_waves(const pdssm_desc* d, int tau) {
-    if ((d->flags & (PDSSM_FLAG_BF16_IO | PDSSM_FLAG_REAL_IO)) && pdssm::fused_prefetch(d->N, tau) &&
+    if (pdssm::fused_prefetch(d->N, tau) &&
         pdssm::fused_lds_layout(d->N, d->K, pdssm::kFusedWavesWide).total + (size_t)kMinStaging * d->N * 8 <=
             pdssm::kMaxLds)
         return pdssm::kFusedWavesWide;
@@ -189,17 +190,19 @@ size_t fused_ws_bytes(const Sizes& s, const pdssm_desc* d, int C) {
     return n;
 }
 
-// Chunked workspace: int map, complex diag, complex term, complex carry/U.
-size_t chunked_ws_bytes(const Sizes& s) {
-    return align_up(s.perChunk * 4) + 3 * align_up(s.perChunk * 8);
+// Chunked workspace: the dictionary tables (read from memory by the
+// dictionary steps), then int map, complex diag, complex term, complex
+// carry/U per chunk.
+size_t chunked_ws_bytes(const Sizes& s, const pdssm_desc* d) {
+    return fused_tables_bytes(s, d) + align_up(s.perChunk * 4) + 3 * align_up(s.perChunk * 8);
 }
 
 size_t ws_bytes_for(const Sizes& s, const pdssm_desc* d, int C) {
-    return use_fused(d) ? fused_ws_bytes(s, d, C) : chunked_ws_bytes(s);
+    return use_fused(d) ? fused_ws_bytes(s, d, C) : chunked_ws_bytes(s, d);
 }
 
-void carve_chunked(ScanArgs& a, void* ws, const Sizes& s) {
-    char* p = static_cast<char*>(ws);
+void carve_chunked(ScanArgs& a, void* ws, const Sizes& s, const pdssm_desc* d) {
+    char* p = static_cast<char*>(ws) + fused_tables_bytes(s, d);
     a.agg_p = reinterpret_cast<int*>(p);
     p += align_up(s.perChunk * 4);
     a.agg_d = reinterpret_cast<float2*>(p);
@@ -208,6 +211,8 @@ void carve_chunked(ScanArgs& a, void* ws, const Sizes& s) {
     p += align_up(s.perChunk * 8);
     a.U = reinterpret_cast<float2*>(p);  // fwd: carry when saved == NULL
 }
+
+bool narrow_io(const pdssm_desc* d);
 
 // Dictionary tables of the fused kernels at the start of ws.
 pdssm::PrepArgs carve_tables(const pdssm_desc* d, const int32_t* pi, void* ws, const Sizes& s, int* status) {
@@ -238,6 +243,15 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
     f.lds = fused_layout(d, f.tau, fwd);
     f.sbM = fwd ? staging_rows(d, f.lds, f.C) : 0;
     f.lds = pdssm::fused_lds_add_staging(f.lds, d->N, f.sbM);
+    // heads of permutations in a wide complex64 forward run kPermWaves
+    // chunk waves on their own layout (more rows of staged chunk states)
+    f.lds_perm = f.lds;
+    f.sbM_perm = f.sbM;
+    if (fwd && f.W > pdssm::kPermWaves && !narrow_io(d)) {
+        f.lds_perm = pdssm::fused_lds_layout(d->N, d->K, pdssm::kPermWaves);
+        f.sbM_perm = staging_rows(d, f.lds_perm, f.C);
+        f.lds_perm = pdssm::fused_lds_add_staging(f.lds_perm, d->N, f.sbM_perm);
+    }
     const Segs g = segments(d, f.C);
     f.S = g.S;
     f.Cs = g.Cs;
@@ -251,6 +265,18 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
         p += align_up(s.seqN * g.S * 8);
         f.segP = reinterpret_cast<int*>(p);
     }
+    if (d->flags & PDSSM_FLAG_PREPARED) return hipSuccess;
+    return pdssm::launch_prep(pa, st);
+}
+
+// The chunked kernels' per-chunk buffers and dictionary tables in ws; the
+// tables are built there unless the caller prepared them.
+hipError_t prep_chunked(ScanArgs& a, const pdssm_desc* d, const int32_t* pi, void* ws, const Sizes& s,
+                        int* status, hipStream_t st) {
+    carve_chunked(a, ws, s, d);
+    const pdssm::PrepArgs pa = carve_tables(d, pi, ws, s, status);
+    a.rec = pa.rec;
+    a.mtab = pa.mtab;
     if (d->flags & PDSSM_FLAG_PREPARED) return hipSuccess;
     return pdssm::launch_prep(pa, st);
 }
@@ -308,6 +334,9 @@ ScanArgs base_args(const pdssm_desc* d, int tau) {
 }
 
 bool misaligned(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) % 16) != 0; }
+
+// int32 / fp32 arrays (idx, y, dy) are read and written as 4-byte words.
+bool misaligned4(const void* p) { return p && (reinterpret_cast<uintptr_t>(p) % 4) != 0; }
 
 }  // namespace
 
@@ -370,7 +399,6 @@ int pdssm_prepare(const pdssm_desc* d, const int32_t* pi, void* ws, size_t ws_by
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (overlap({ws, need}, {pi, (size_t)d->H * d->K * d->N * 4})) return PDSSM_ERR_INVALID_ARG;
-    if (!use_fused(d)) return PDSSM_OK;  // the chunked kernels need no tables
     const hipError_t e = pdssm::launch_prep(carve_tables(d, pi, ws, s, dev_status), static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
@@ -385,6 +413,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     for (const void* p : {(const void*)D, (const void*)b, (const void*)c, (const void*)h0,
                           (const void*)h_final, (const void*)saved, (const void*)pi})
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned4(idx) || misaligned4(y)) return PDSSM_ERR_INVALID_ARG;
     ScanArgs a = base_args(d, tau);
     const Sizes s = sizes_of(d, a.C);
     const size_t need = ws_bytes_for(s, d, a.C);
@@ -412,9 +441,9 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
         e = prep_fused(f, d, pi, ws, s, dev_status, st, true);
         if (e == hipSuccess) e = pdssm::launch_fwd_fused(f, st);
     } else {
-        carve_chunked(a, ws, s);
+        e = prep_chunked(a, d, pi, ws, s, dev_status, st);
         a.carry = saved ? reinterpret_cast<float2*>(saved) : a.U;
-        e = pdssm::launch_fwd_chunked(a, st);
+        if (e == hipSuccess) e = pdssm::launch_fwd_chunked(a, st);
     }
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
@@ -433,6 +462,7 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
                           (const void*)dh_final, (const void*)dD, (const void*)db,
                           (const void*)dc, (const void*)dh0, (const void*)pi})
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned4(idx) || misaligned4(dy)) return PDSSM_ERR_INVALID_ARG;
     ScanArgs a = base_args(d, tau);
     const Sizes s = sizes_of(d, a.C);
     const size_t need = ws_bytes_for(s, d, a.C);
@@ -469,9 +499,9 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
         e = prep_fused(f, d, pi, ws, s, dev_status, st, false);
         if (e == hipSuccess) e = pdssm::launch_bwd_fused(f, st);
     } else {
-        carve_chunked(a, ws, s);
+        e = prep_chunked(a, d, pi, ws, s, dev_status, st);
         a.carry = const_cast<float2*>(reinterpret_cast<const float2*>(saved));
-        e = pdssm::launch_bwd_chunked(a, st);
+        if (e == hipSuccess) e = pdssm::launch_bwd_chunked(a, st);
     }
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
@@ -504,6 +534,7 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
     if (st != PDSSM_OK) return st;
     if (io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !g || !z || (!q && !G) || (q && !pi)) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned4(idx)) return PDSSM_ERR_INVALID_ARG;
     if (misaligned(g) || misaligned(z) || misaligned(pi) || (reinterpret_cast<uintptr_t>(G) & 3) != 0 ||
         (reinterpret_cast<uintptr_t>(q) & 3) != 0)
         return PDSSM_ERR_INVALID_ARG;
@@ -542,6 +573,7 @@ int pdssm_decode_step(const pdssm_desc* d, const int32_t* idx, const int32_t* pi
     for (const void* p : {(const void*)pi, (const void*)D, (const void*)b, (const void*)c, (const void*)h_in,
                           (const void*)h_out})
         if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned4(idx) || misaligned4(y)) return PDSSM_ERR_INVALID_ARG;
     const size_t nseq = (size_t)d->B * d->H, nrow = nseq * d->N * 8, nio = nseq * d->N * io_bytes(d);
     const size_t npi = (size_t)d->H * d->K * d->N * 4;
     // the state may be updated in place (h_out == h_in); no other overlap
@@ -628,7 +660,7 @@ int pdssm_compose_chunks(const pdssm_desc* d, const int32_t* idx, const int32_t*
     if (st != PDSSM_OK) return st;
     if (narrow_io(d)) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !pi || !D || !pi_out || !d_out) return PDSSM_ERR_INVALID_ARG;
-    if (misaligned(D) || misaligned(pi) || misaligned(pi_out) || misaligned(d_out))
+    if (misaligned(D) || misaligned(pi) || misaligned(pi_out) || misaligned(d_out) || misaligned4(idx))
         return PDSSM_ERR_INVALID_ARG;
     pdssm::ComposeArgs a = {};
     a.B = d->B;

@@ -19,6 +19,12 @@
 //   k_bwd_emit   per chunk: recomputes the chunk's states from the saved
 //                entering state into LDS, then walks backwards emitting dD, db,
 //                dc.
+//
+// Every scatter-add runs in a fixed order (no float atomics): dictionary steps
+// use the per-entry tables of the prep kernel (source records, or the sorted
+// form for maps with a row of more than kMaxSrc sources), read from the
+// workspace; the carry pass uses the sorted form of every chunk's composed
+// map, built once per chunk by k_fwd_agg.
 #include "pdssm_device.h"
 #include "pdssm_internal.h"
 
@@ -54,13 +60,27 @@ __device__ __forceinline__ void st_io(float2* base, size_t off, int lane, const 
     }
 }
 
+// This lane's prep words of dictionary entry k of head hh, and the entry's
+// class (max in-degree, or kFallback for the sorted form).
+template <int N>
+__device__ __forceinline__ int load_entry(const ScanArgs& a, int hh, int k, int lane, bool act,
+                                          uint64_t (&w)[Lay<N>::SL]) {
+    constexpr int SL = Lay<N>::SL;
+    const size_t e = (size_t)hh * a.K + k;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) w[r] = act ? a.rec[e * N + lane * SL + r] : 0;
+    return __builtin_amdgcn_readfirstlane((int)a.mtab[e]);
+}
+
 // ================================================================== forward
 template <int N, int IO>
 __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    __shared__ float2 xs[kWavesPerGroup][N];
+    __shared__ float2 xs[kWavesPerGroup][N + 1];
     __shared__ float2 dsh[kWavesPerGroup][N];
     __shared__ int psh[kWavesPerGroup][N];
+    __shared__ uint64_t mts[kWavesPerGroup][SL][N];
+    __shared__ uint8_t sts[kWavesPerGroup][N];
     const int wv = wave_id(), lane = lane_id();
     const int nseq = a.B * a.H;
     const int task = blockIdx.x * kWavesPerGroup + wv;
@@ -72,6 +92,7 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     float2* X = xs[wv];
     float2* Ds = dsh[wv];
     int* Ps = psh[wv];
+    if (lane == 0) X[N] = make_float2(0.f, 0.f);  // zero row of the source records
 
     bool bad = false;
     int kv = 0;
@@ -96,6 +117,8 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
 
     CV<SL> Dn = cv_zero<SL>(), bn = cv_zero<SL>();
     IV<SL> pn = {};
+    uint64_t wn[SL];
+    int cn = load_entry<N>(a, hh, readlane_i(kv, 0), lane, act, wn);
     if (act) {
         int k = readlane_i(kv, 0);
         Dn = ld_io<SL, IO>(a.D, base, lane);
@@ -105,15 +128,22 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     for (int t = 0; t < len; ++t) {
         CV<SL> Dt = Dn, bt = bn;
         IV<SL> pt = pn;
-        if (t + 1 < len && act) {
+        uint64_t wt[SL];
+#pragma unroll
+        for (int r = 0; r < SL; ++r) wt[r] = wn[r];
+        const int ct = cn;
+        if (t + 1 < len) {
             int k = readlane_i(kv, t + 1);
-            Dn = ld_io<SL, IO>(a.D, base + (t + 1) * stride, lane);
-            bn = ld_io<SL, IO>(a.b, base + (t + 1) * stride, lane);
-            pn = ld_iv<SL>(pih + (size_t)k * N, lane);
+            cn = load_entry<N>(a, hh, k, lane, act, wn);
+            if (act) {
+                Dn = ld_io<SL, IO>(a.D, base + (t + 1) * stride, lane);
+                bn = ld_io<SL, IO>(a.b, base + (t + 1) * stride, lane);
+                pn = ld_iv<SL>(pih + (size_t)k * N, lane);
+            }
         }
         bad |= sanitize_map<N, SL>(pt);
         // B <- b_t + P_t (D_t .* B)
-        pd_scatter_step<N>(X, lane, act, bm, Dt, bt, pt);
+        table_step<N>(X, ct, wt, bm, Dt, bt, lane, act);
         // (pi, d) <- (pi_t[pi], D_t[pi] * d): stage D_t and pi_t for random access
         wave_sync();
         if (act) {
@@ -130,9 +160,18 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
             }
         }
     }
+    // the composed map in sorted form, for the carry pass's scatter
+    uint64_t* mt[SL];
+#pragma unroll
+    for (int q = 0; q < SL; ++q) mt[q] = mts[wv][q];
+    uint64_t sw[SL];
+    map_sorted_words<N>(pm, lane, act, mt, Ps, sts[wv], sw);
     if (act) {
         const size_t o = ((size_t)seq * a.C + ch) * N;
-        st_iv<SL>(a.agg_p + o, lane, pm);
+        IV<SL> packed;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) packed.v[s] = (int)sw[s];
+        st_iv<SL>(a.agg_p + o, lane, packed);
         st_cv<SL>(a.agg_d + o, lane, dm);
         st_cv<SL>(a.agg_v + o, lane, bm);
     }
@@ -162,14 +201,16 @@ __global__ __launch_bounds__(256) void k_fwd_carry(ScanArgs a) {
     for (int ch = 0; ch < a.C; ++ch) {
         const size_t o = o0 + (size_t)ch * N;
         if (act) st_cv<SL>(a.carry + o, lane, h);
-        IV<SL> pc = pn;
+        uint64_t wc[SL];
+#pragma unroll
+        for (int s = 0; s < SL; ++s) wc[s] = (uint32_t)pn.v[s];  // sorted form of the chunk map
         CV<SL> dc = dn, vc = vn;
         if (ch + 1 < a.C && act) {
             pn = ld_iv<SL>(a.agg_p + o + N, lane);
             dn = ld_cv<SL>(a.agg_d + o + N, lane);
             vn = ld_cv<SL>(a.agg_v + o + N, lane);
         }
-        pd_scatter_step<N>(X, lane, act, h, dc, vc, pc);
+        sorted_step<N>(X, wc, h, dc, vc, lane, act);
     }
     if (a.hfinal && act) st_cv<SL>(a.hfinal + (size_t)seq * N, lane, h);
 }
@@ -177,7 +218,7 @@ __global__ __launch_bounds__(256) void k_fwd_carry(ScanArgs a) {
 template <int N, int IO>
 __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    __shared__ float2 xs[kWavesPerGroup][N];
+    __shared__ float2 xs[kWavesPerGroup][N + 1];
     const int wv = wave_id(), lane = lane_id();
     const int nseq = a.B * a.H;
     const int task = blockIdx.x * kWavesPerGroup + wv;
@@ -187,6 +228,7 @@ __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
     const int s0 = ch * a.tau, len = min(a.tau, a.L - s0);
     const bool act = lane < LANES;
     float2* X = xs[wv];
+    if (lane == 0) X[N] = make_float2(0.f, 0.f);  // zero row of the source records
 
     int kv = 0;
     if (lane < len) {
@@ -198,31 +240,32 @@ __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
 
     const size_t stride = (size_t)a.H * N;
     const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
-    const int* pih = a.pi + (size_t)hh * a.K * N;
     float* yrow = a.y + ((size_t)bb * a.L + s0) * a.H + hh;
 
     CV<SL> Dn = cv_zero<SL>(), bn = cv_zero<SL>(), cn = cv_zero<SL>();
-    IV<SL> pn = {};
+    uint64_t wn[SL];
+    int kn = load_entry<N>(a, hh, readlane_i(kv, 0), lane, act, wn);
     if (act) {
-        int k = readlane_i(kv, 0);
         Dn = ld_io<SL, IO>(a.D, base, lane);
         bn = ld_io<SL, IO>(a.b, base, lane);
         cn = ld_io<SL, IO>(a.c, base, lane);
-        pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = 0; t < len; ++t) {
         CV<SL> Dt = Dn, bt = bn, ct = cn;
-        IV<SL> pt = pn;
-        if (t + 1 < len && act) {
-            int k = readlane_i(kv, t + 1);
-            const size_t off = base + (t + 1) * stride;
-            Dn = ld_io<SL, IO>(a.D, off, lane);
-            bn = ld_io<SL, IO>(a.b, off, lane);
-            cn = ld_io<SL, IO>(a.c, off, lane);
-            pn = ld_iv<SL>(pih + (size_t)k * N, lane);
+        uint64_t wt[SL];
+#pragma unroll
+        for (int r = 0; r < SL; ++r) wt[r] = wn[r];
+        const int kc = kn;
+        if (t + 1 < len) {
+            kn = load_entry<N>(a, hh, readlane_i(kv, t + 1), lane, act, wn);
+            if (act) {
+                const size_t off = base + (t + 1) * stride;
+                Dn = ld_io<SL, IO>(a.D, off, lane);
+                bn = ld_io<SL, IO>(a.b, off, lane);
+                cn = ld_io<SL, IO>(a.c, off, lane);
+            }
         }
-        sanitize_map<N, SL>(pt);
-        pd_scatter_step<N>(X, lane, act, h, Dt, bt, pt);
+        table_step<N>(X, kc, wt, h, Dt, bt, lane, act);
         float part = 0.f;
         if (act) {
 #pragma unroll
@@ -371,7 +414,8 @@ __global__ __launch_bounds__(256) void k_bwd_carry(ScanArgs a) {
     if (a.dh0 && act) st_cv<SL>(a.dh0 + (size_t)seq * N, lane, u);
 }
 
-// One wave per workgroup; dynamic LDS = (tau + 1) states + one exchange row.
+// One wave per workgroup; dynamic LDS = (tau + 1) states + one exchange row
+// of N + 1 entries (the last one the zero row of the source records).
 template <int N, int IO>
 __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
@@ -382,8 +426,9 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     const int bb = seq / a.H, hh = seq - bb * a.H;
     const int s0 = ch * a.tau, len = min(a.tau, a.L - s0);
     const bool act = lane < LANES;
-    float2* X = smem;       // exchange row
-    float2* Hs = smem + N;  // Hs[i*N + j] = state before step s0 + i
+    float2* Hs = smem;                           // Hs[i*N + j] = state before step s0 + i
+    float2* X = smem + (size_t)(a.tau + 1) * N;  // exchange row
+    if (lane == 0) X[N] = make_float2(0.f, 0.f);
 
     int kv = 0;
     float dyv = 0.f;
@@ -405,23 +450,26 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     }
     CV<SL> Dn = cv_zero<SL>(), bn = cv_zero<SL>();
     IV<SL> pn = {};
+    uint64_t wn[SL];
+    int kn = load_entry<N>(a, hh, readlane_i(kv, 0), lane, act, wn);
     if (act) {
-        int k = readlane_i(kv, 0);
         Dn = ld_io<SL, IO>(a.D, base, lane);
         bn = ld_io<SL, IO>(a.b, base, lane);
-        pn = ld_iv<SL>(pih + (size_t)k * N, lane);
     }
     for (int t = 0; t < len; ++t) {
         CV<SL> Dt = Dn, bt = bn;
-        IV<SL> pt = pn;
-        if (t + 1 < len && act) {
-            int k = readlane_i(kv, t + 1);
-            Dn = ld_io<SL, IO>(a.D, base + (t + 1) * stride, lane);
-            bn = ld_io<SL, IO>(a.b, base + (t + 1) * stride, lane);
-            pn = ld_iv<SL>(pih + (size_t)k * N, lane);
+        uint64_t wt[SL];
+#pragma unroll
+        for (int r = 0; r < SL; ++r) wt[r] = wn[r];
+        const int kc = kn;
+        if (t + 1 < len) {
+            kn = load_entry<N>(a, hh, readlane_i(kv, t + 1), lane, act, wn);
+            if (act) {
+                Dn = ld_io<SL, IO>(a.D, base + (t + 1) * stride, lane);
+                bn = ld_io<SL, IO>(a.b, base + (t + 1) * stride, lane);
+            }
         }
-        sanitize_map<N, SL>(pt);
-        pd_scatter_step<N>(X, lane, act, h, Dt, bt, pt);
+        table_step<N>(X, kc, wt, h, Dt, bt, lane, act);
         if (act) st_cv<SL>(Hs + (size_t)(t + 1) * N, lane, h);
     }
 

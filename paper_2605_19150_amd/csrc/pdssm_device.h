@@ -311,31 +311,289 @@ __device__ __forceinline__ void report_index_error(int* status) {
     if (status) *status = kErrIndex;
 }
 
-// ------------------------------------------------------------------ the PD step
-// x <- bt + P(pt) (Dt .* x): every lane scatters D_t[j]*x[j] to row pt[j] of
-// the wave's LDS buffer X (pre-filled with b_t); colliding rows add up
-// through LDS float atomics.  X holds N complex values.
+// ------------------------------------------------------------------ lane scans
+// DPP move with zero for lanes outside the row mask or without a source.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_i(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, true);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_fr(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, true));
+}
+
+// Inclusive prefix sum of an int over the 64 lanes.
+__device__ __forceinline__ int wave_incl_scan_i(int v) {
+    v += dpp_i<0x111, 0xf>(v);
+    v += dpp_i<0x112, 0xf>(v);
+    v += dpp_i<0x114, 0xf>(v);
+    v += dpp_i<0x118, 0xf>(v);
+    v += dpp_i<0x142, 0xa>(v);
+    v += dpp_i<0x143, 0xc>(v);
+    return v;
+}
+
+// One step of the segmented scan: add the value DPP brings in when `take`.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void seg_step(float2& v, bool take) {
+    const float tx = dpp_fr<CTRL, ROWS>(v.x), ty = dpp_fr<CTRL, ROWS>(v.y);
+    v.x += take ? tx : 0.f;
+    v.y += take ? ty : 0.f;
+}
+
+// Inclusive segmented sum over the 64 lanes of a complex value: a lane whose
+// bit is set in `starts` begins a new segment (lane 0 always does).  Row-wise
+// shifts, then the row broadcasts carry row totals across rows, each term
+// taken only when its source lane lies in the same segment.
+__device__ __forceinline__ float2 wave_seg_scan(float2 v, uint64_t starts, int lane) {
+    const uint64_t le = starts & ((2ull << lane) - 1ull);  // lane 63: 2 << 63 wraps to 0
+    const int s0 = le ? 63 - __builtin_clzll(le) : 0;      // first lane of this lane's segment
+    seg_step<0x111, 0xf>(v, lane - 1 >= s0);
+    seg_step<0x112, 0xf>(v, lane - 2 >= s0);
+    seg_step<0x114, 0xf>(v, lane - 4 >= s0);
+    seg_step<0x118, 0xf>(v, lane - 8 >= s0);
+    seg_step<0x142, 0xa>(v, s0 < (lane & ~15));
+    seg_step<0x143, 0xc>(v, s0 < 32);
+    return v;
+}
+
+// ------------------------------------------------------------------ collisions in a fixed order
+// The scatter-add h'[r] = b[r] + sum_{j: pi(j) = r} D[j] h[j] adds every
+// source that lands on row r.  No float atomics anywhere: the sum of each row
+// runs in an order fixed by the map alone, so results are deterministic.
+//
+// Per dictionary entry the prep kernel stores one 64-bit word per index j:
+//  - in-degree <= kMaxSrc everywhere (the usual case): the record of row j,
+//    its sources in ascending order, one byte each (unused bytes name a row
+//    that stays zero, or are masked by the in-degree), in-degree in the top
+//    byte.  The step writes D .* h once and every row gathers its sources.
+//  - some row above kMaxSrc (mtab = kFallback): the map's sorted form.  The
+//    sources are ordered by (destination, source); bits 0-7 hold source j's
+//    position in that order, bits 8-15 the last position of row j's run,
+//    bit 16 says row j has a source, bit 17 that position j starts a run.
+//    The step stores D[j] h[j] at j's position (a permutation, no
+//    collisions), sums every run with a segmented scan across lanes, and each
+//    row reads its run's total.
+constexpr int kMaxSrc = 7;
+constexpr unsigned kFallback = 255;
+
+__device__ __forceinline__ int srt_pos(uint64_t w) { return (int)(w & 255u); }
+__device__ __forceinline__ int srt_end(uint64_t w) { return (w >> 16) & 1u ? (int)((w >> 8) & 255u) : -1; }
+__device__ __forceinline__ bool srt_start(uint64_t w) { return ((w >> 17) & 1u) != 0; }
+__device__ __forceinline__ uint64_t srt_word(int pos, int end, bool has, bool start) {
+    return (uint64_t)(pos & 255) | (uint64_t)(end & 255) << 8 | (uint64_t)(has ? 1 : 0) << 16 |
+           (uint64_t)(start ? 1 : 0) << 17;
+}
+
+// Run totals of values in sorted order.  V holds N values, every row's
+// sources contiguous; u = this lane's entries V[lane*SL + r], st[r] = whether
+// position lane*SL + r starts a run, e[r] = the last position of the run of
+// row lane*SL + r (-1: the row has no source).  Runs are summed by an
+// in-lane pass and a segmented scan across lanes (a fixed order); V is
+// overwritten.  Returns the run total of each of this lane's rows (0 when
+// empty).  All 64 lanes must call it; act = lane holds entries.
 template <int N>
-__device__ __forceinline__ void pd_scatter_step(float2* X, int lane, bool act,
-                                                CV<Lay<N>::SL>& x,
-                                                const CV<Lay<N>::SL>& Dt,
-                                                const CV<Lay<N>::SL>& bt,
-                                                const IV<Lay<N>::SL>& pt) {
+__device__ __forceinline__ CV<Lay<N>::SL> run_totals(float2* V, CV<Lay<N>::SL> u, const bool (&st)[Lay<N>::SL],
+                                                     const int (&e)[Lay<N>::SL], int lane, bool act) {
     constexpr int SL = Lay<N>::SL;
-    wave_sync();
-    if (act) st_cv<SL>(X, lane, bt);
-    wave_sync();
-    if (act) {
+    bool seen = false;
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            float2 v = cmul(Dt.v[s], x.v[s]);
-            float* dst = reinterpret_cast<float*>(X + pt.v[s]);
-            atomicAdd(dst, v.x);
-            atomicAdd(dst + 1, v.y);
+    for (int r = 0; r < SL; ++r) {
+        if (r > 0 && !st[r]) u.v[r] = cadd(u.v[r], u.v[r - 1]);
+        seen |= st[r];
+    }
+    const uint64_t starts = __builtin_amdgcn_ballot_w64(act && seen);
+    const float2 C = wave_seg_scan(u.v[SL - 1], starts, lane);
+    if constexpr (SL == 1) {
+        u.v[0] = C;
+    } else {
+        const float2 Cp = make_float2(dpp_fr<0x138, 0xf>(C.x), dpp_fr<0x138, 0xf>(C.y));  // from lane - 1
+        bool head = false;
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            head |= st[r];
+            if (!head) u.v[r] = cadd(u.v[r], Cp);
         }
     }
     wave_sync();
-    if (act) x = ld_cv<SL>(X, lane);
+    if (act) st_cv<SL>(V, lane, u);
+    wave_sync();
+    CV<SL> tot = cv_zero<SL>();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            const float2 t = V[e[r] < 0 ? 0 : e[r]];
+            tot.v[r] = e[r] < 0 ? make_float2(0.f, 0.f) : t;
+        }
+    }
+    return tot;
+}
+
+// h <- bt + P (Dt .* h) for a map given in sorted form (w = this lane's words
+// of the entry).  V: N values of the wave's LDS scratch.
+template <int N>
+__device__ __forceinline__ void sorted_step(float2* V, const uint64_t (&w)[Lay<N>::SL], CV<Lay<N>::SL>& h,
+                                            const CV<Lay<N>::SL>& Dt, const CV<Lay<N>::SL>& bt, int lane,
+                                            bool act) {
+    constexpr int SL = Lay<N>::SL;
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) V[srt_pos(w[r])] = cmul(Dt.v[r], h.v[r]);
+    }
+    wave_sync();
+    CV<SL> u = cv_zero<SL>();
+    if (act) u = ld_cv<SL>(V, lane);
+    bool st[SL];
+    int e[SL];
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        st[r] = srt_start(w[r]);
+        e[r] = srt_end(w[r]);
+    }
+    const CV<SL> tot = run_totals<N>(V, u, st, e, lane, act);
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) h.v[r] = cadd(bt.v[r], tot.v[r]);
+    }
+}
+
+// Unused source bytes of a record: row N of the staged values (kept zero)
+// when it fits in a byte; at N = 256 the in-degree byte masks them instead.
+template <int N>
+struct Sentinel {
+    static constexpr bool kZeroRow = N <= 128;
+    static constexpr unsigned kByte = N <= 128 ? (unsigned)N : 0u;
+};
+
+// Ranks of a map's sources in (destination, source) order.  pm: this lane's
+// entries (source j = lane*SL + r goes to row pm[r]).  MT: SL tables of N
+// 64-bit words in this wave's LDS scratch; table q collects, per row, the
+// lanes whose slot q maps there (an atomic OR, whose result does not depend
+// on the order of the ORs).  Returns, per source of this lane, its rank among
+// the sources of its row (the lanes below it in the tables at its row, plus
+// its own earlier slots with the same row), and per row of this lane its
+// source count.
+template <int N>
+__device__ __forceinline__ void map_ranks(const IV<Lay<N>::SL>& pm, int lane, bool act,
+                                          uint64_t* const (&MT)[Lay<N>::SL], int (&rank)[Lay<N>::SL],
+                                          int (&cnt)[Lay<N>::SL]) {
+    constexpr int SL = Lay<N>::SL;
+    const uint64_t lt = (1ull << lane) - 1ull;
+    wave_sync();
+#pragma unroll
+    for (int q = 0; q < SL; ++q)
+        for (int i = lane; i < N; i += kWave) MT[q][i] = 0;
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int q = 0; q < SL; ++q)
+            __hip_atomic_fetch_or(MT[q] + pm.v[q], 1ull << lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+    }
+    wave_sync();
+#pragma unroll
+    for (int r = 0; r < SL; ++r) {
+        int rk = 0, c = 0;
+        if (act) {
+#pragma unroll
+            for (int q = 0; q < SL; ++q) {
+                rk += __builtin_popcountll(MT[q][pm.v[r]] & lt);
+                if (q < r) rk += pm.v[q] == pm.v[r] ? 1 : 0;
+                c += __builtin_popcountll(MT[q][lane * SL + r]);
+            }
+        }
+        rank[r] = rk;
+        cnt[r] = c;
+    }
+}
+
+// The sorted-form words (srt_word) of a map held in registers.  MT as for
+// map_ranks; OFF: N ints and ST: N bytes of this wave's LDS scratch.
+template <int N>
+__device__ __forceinline__ void map_sorted_words(const IV<Lay<N>::SL>& pm, int lane, bool act,
+                                                 uint64_t* const (&MT)[Lay<N>::SL], int* OFF, uint8_t* ST,
+                                                 uint64_t (&w)[Lay<N>::SL]) {
+    constexpr int SL = Lay<N>::SL;
+    int rank[SL], cnt[SL];
+    map_ranks<N>(pm, lane, act, MT, rank, cnt);
+    int tot = 0;
+#pragma unroll
+    for (int r = 0; r < SL; ++r) tot += cnt[r];
+    int off = wave_incl_scan_i(tot) - tot;  // first position of this lane's first row
+    int ends[SL];
+    wave_sync();
+    for (int i = lane; i < N; i += kWave) ST[i] = 0;
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            OFF[lane * SL + r] = off;
+            ends[r] = off + cnt[r] - 1;
+            off += cnt[r];
+        }
+    }
+    wave_sync();
+    int pos[SL];
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            pos[r] = OFF[pm.v[r]] + rank[r];
+            if (rank[r] == 0) ST[pos[r]] = 1;
+        }
+    }
+    wave_sync();
+#pragma unroll
+    for (int r = 0; r < SL; ++r)
+        w[r] = act ? srt_word(pos[r], ends[r], cnt[r] > 0, ST[lane * SL + r] != 0) : 0;
+}
+
+// h <- bt + P (Dt .* h) for a dictionary entry given by its prep words w
+// (this lane's records, or its sorted form when cls == kFallback).  V: N + 1
+// values of the wave's LDS scratch; V[N] must hold zero (N <= 128).  Every
+// record's seven source slots are read; unused ones add zero.
+template <int N>
+__device__ __forceinline__ void table_step(float2* V, int cls, const uint64_t (&w)[Lay<N>::SL],
+                                           CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt,
+                                           const CV<Lay<N>::SL>& bt, int lane, bool act) {
+    constexpr int SL = Lay<N>::SL;
+    if (cls == (int)kFallback) {
+        sorted_step<N>(V, w, h, Dt, bt, lane, act);
+        return;
+    }
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) V[lane * SL + r] = cmul(Dt.v[r], h.v[r]);
+    }
+    wave_sync();
+    if (act) {
+#pragma unroll
+        for (int r = 0; r < SL; ++r) {
+            float2 acc = bt.v[r];
+            const unsigned lo = (unsigned)w[r], hi = (unsigned)(w[r] >> 32);
+#pragma unroll
+            for (int m = 0; m < kMaxSrc; ++m) {
+                const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
+                float2 v = V[src];
+                if constexpr (!Sentinel<N>::kZeroRow) v = m < (int)(hi >> 24) ? v : make_float2(0.f, 0.f);
+                acc.x += v.x;
+                acc.y += v.y;
+            }
+            h.v[r] = acc;
+        }
+    }
+}
+
+// acc += the sources M0 .. M1-1 of a record (V = the wave's staged values).
+template <int M0, int M1>
+__device__ __forceinline__ void gather_rec_range(const float2* V, uint64_t r, float2& acc) {
+    const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
+#pragma unroll
+    for (int m = M0; m < M1; ++m) {
+        const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
+        const float2 v = V[src];
+        acc.x += v.x;
+        acc.y += v.y;
+    }
 }
 
 // ------------------------------------------------------------------ cross-lane sums

@@ -30,6 +30,9 @@ constexpr int fused_waves_bwd(int N, int tau) { return fused_prefetch(N, tau) ? 
 // tables leave LDS room for them: more waves in flight hide the chunk
 // passes' LDS round trips (the backward measured faster with 8).
 constexpr int kFusedWavesWide = 11;
+// Chunk waves a wide forward uses for a head of permutation maps in
+// complex64 rows (the rest stay idle).
+constexpr int kPermWaves = 7;
 // At N = 256 the per-wave LDS buffers (2W published operators of N entries
 // and their sorted forms, W staging rows, 2W readout rows) leave room for the
 // head's tables only with fewer chunk waves: 5, else 3, in both directions,
@@ -40,7 +43,7 @@ constexpr int kFusedWavesNarrowest = 3;
 
 // Byte offsets of the fused kernels' dynamic LDS regions.
 struct LdsLayout {
-    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, agm, aflag, vd, x, cs, pa, sb, total;
+    uint32_t rec, dict, mtab, ring, ready, agg, agp, age, agh, agm, aflag, prog, vd, x, cs, pa, sb, total;
 };
 
 inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
@@ -53,7 +56,8 @@ inline uint32_t align16(size_t x) { return (uint32_t)((x + 15) / 16 * 16); }
 // slots of published chunk operators (local state and diagonal; the map, or
 // for many-to-one heads its sorted form: position of each source, last
 // position of each destination's run, run-start flags; agm: the map itself,
-// for the aggregate pass) and their chunk ids.
+// for the aggregate pass) and their chunk ids; prog: chunks the workgroup's
+// waves have finished (the waits' progress measure).
 inline LdsLayout fused_lds_layout(int N, int K, int W) {
     LdsLayout l;
     size_t o = 0;
@@ -62,9 +66,10 @@ inline LdsLayout fused_lds_layout(int N, int K, int W) {
     l.dict = (uint32_t)o;  o += align16(KE * N);
     l.mtab = (uint32_t)o;  o += align16(KE);
     l.ring = (uint32_t)o;  o += (size_t)(W + 1) * N * 8;
-    l.ready = (uint32_t)o; // followed by the 2W operator-slot flags
+    l.ready = (uint32_t)o; // followed by the 2W operator-slot flags and the progress count
     l.aflag = (uint32_t)(o + 4);
-    o += align16((size_t)(1 + 2 * W) * 4);
+    l.prog = (uint32_t)(o + 4 * (1 + 2 * (size_t)W));
+    o += align16((size_t)(2 + 2 * W) * 4);
     l.agg = (uint32_t)o;   o += (size_t)2 * W * N * 16;
     l.agp = (uint32_t)o;   o += align16((size_t)2 * W * N);
     l.age = (uint32_t)o;   o += align16((size_t)2 * W * N * 2);
@@ -93,9 +98,10 @@ struct PrepArgs {
     int H, K, N;
     const int* pi;   // [H][K][N]
     uint8_t* dict;   // [H][K][N] byte copy of pi (sanitised)
-    uint64_t* rec;   // [H][K][N] per destination row: 7 source bytes + in-degree byte;
-                     // unused source bytes hold N (a zero row) when N <= 128, else 0
-    uint8_t* mtab;   // [H][K] max in-degree of the entry, 255 = needs the atomic scatter
+    uint64_t* rec;   // [H][K][N] per destination row: 7 source bytes + in-degree byte
+                     // (unused source bytes hold N, a zero row, when N <= 128, else 0);
+                     // for an entry with a row of more sources, its sorted form (srt_word)
+    uint8_t* mtab;   // [H][K] max in-degree of the entry, kFallback (255) = sorted form
     int* status;
 };
 
@@ -127,6 +133,11 @@ struct FusedArgs {
     // diagonal), [B*H][S][N] each.  S = 1: one workgroup per sequence.
     int S, Cs;
     int sbM;  // saved-state rows staged in LDS by the forward (0: stored as computed)
+    // The forward's layout and staging rows for heads of permutations in a
+    // wide complex64 kernel (kPermWaves chunk waves; otherwise equal to lds
+    // and sbM).  The tables sit at the same offsets as in lds.
+    LdsLayout lds_perm;
+    int sbM_perm;
     float2* segA;
     float2* segD;
     int* segP;

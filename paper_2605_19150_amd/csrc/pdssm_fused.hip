@@ -32,13 +32,14 @@
 // D[j] h[j] adds up every source that lands on row r.  For each dictionary
 // entry a prep kernel lists, per destination row, its sources in ascending
 // order (up to 7, plus the in-degree) once per call; the step then writes
-// D .* h to LDS once and every lane gathers its row's sources.  The order of
-// the sum is fixed, so results are deterministic.  The number of gathers per
-// step is fixed per head (1, 3 or 7, the head's largest in-degree rounded
-// up), so the step has no branches: unused record slots point at a row that
-// stays zero.  An entry with a row of in-degree above 7 (rare for random maps,
-// e.g. an all-to-one map) takes an LDS float-atomic scatter instead; heads
-// without such entries never test for it.
+// D .* h to LDS once and every lane gathers its row's sources.  The number of
+// gathers per step is fixed per head (1, 3 or 7, the head's largest in-degree
+// rounded up), so the step has no branches: unused record slots point at a
+// row that stays zero.  An entry with a row of in-degree above 7 (rare for
+// random maps, e.g. an all-to-one map) is stored in sorted form instead and
+// its steps sum each row's run with a segmented scan across lanes, behind one
+// scalar branch per step; heads without such entries never test for it.  No
+// sum uses float atomics, so results are deterministic.
 //
 // The last chunk of a sequence may be short; its missing steps run as exact
 // no-ops (D = 1, b = 0, an identity dictionary entry at index K), so no step
@@ -50,23 +51,14 @@ namespace pdssm {
 
 namespace {
 
-constexpr int kMaxSrc = 7;          // sources per row record
-constexpr unsigned kFallback = 255; // mtab value: entry needs the atomic scatter
-
-// Unused source slots: row N of the wave's staged values V (kept zero) when it fits
-// in a byte; for N = 256 the in-degree byte masks them instead.
-template <int N>
-struct Sentinel {
-    static constexpr bool kZeroRow = N <= 128;
-    static constexpr unsigned kByte = N <= 128 ? (unsigned)N : 0u;
-};
-
 // ------------------------------------------------------------------ prep
 // One wave per dictionary entry (h, k): byte dictionary, per-row source
-// records, per-entry max in-degree.
+// records, per-entry max in-degree; an entry with a row of more than kMaxSrc
+// sources gets its sorted form instead of records.
 template <int N>
 __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    __shared__ uint8_t spos[4][N], sstart[4][N];
     const int wv = wave_id(), lane = lane_id();
     const int e = blockIdx.x * 4 + wv;
     if (e >= a.H * a.K) return;
@@ -112,12 +104,61 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
     int maxdeg = 0;
     if (act) {
 #pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            a.rec[(size_t)e * N + lane * SL + s] = rec[s] | (uint64_t)min(cnt[s], 255) << 56;
-            maxdeg = max(maxdeg, cnt[s]);
-        }
+        for (int s = 0; s < SL; ++s) maxdeg = max(maxdeg, cnt[s]);
     }
     for (int off = 32; off >= 1; off >>= 1) maxdeg = max(maxdeg, __shfl_xor(maxdeg, off));
+    uint64_t* out = a.rec + (size_t)e * N;
+    if (maxdeg <= kMaxSrc) {
+        if (act) {
+#pragma unroll
+            for (int s = 0; s < SL; ++s) out[lane * SL + s] = rec[s] | (uint64_t)cnt[s] << 56;
+        }
+    } else {
+        // Sorted form: row r's run starts at the number of sources of rows
+        // below r; source j sits in its row's run at its rank among that
+        // row's sources (a second walk in ascending j, as above).
+        uint8_t* P = spos[wv];
+        uint8_t* S = sstart[wv];
+        int tot = 0;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) tot += act ? cnt[s] : 0;
+        int off = wave_incl_scan_i(tot) - tot;
+        int roff[SL], c2[SL];
+#pragma unroll
+        for (int s = 0; s < SL; ++s) {
+            roff[s] = off;
+            off += act ? cnt[s] : 0;
+            c2[s] = 0;
+        }
+        for (int i = lane; i < N; i += kWave) S[i] = 0;
+        wave_sync();
+        for (int jl = 0; jl < LANES; ++jl) {
+#pragma unroll
+            for (int sj = 0; sj < SL; ++sj) {
+                const int pj = readlane_i(p.v[sj], jl);
+#pragma unroll
+                for (int s = 0; s < SL; ++s) {
+                    if (act && pj == lane * SL + s) {
+                        P[jl * SL + sj] = (uint8_t)(roff[s] + c2[s]);
+                        ++c2[s];
+                    }
+                }
+            }
+        }
+        if (act) {
+#pragma unroll
+            for (int s = 0; s < SL; ++s)
+                if (cnt[s] > 0) S[roff[s]] = 1;
+        }
+        wave_sync();
+        if (act) {
+#pragma unroll
+            for (int s = 0; s < SL; ++s) {
+                const int j = lane * SL + s;
+                out[j] = srt_word(P[j], roff[s] + cnt[s] - 1, cnt[s] > 0, S[j] != 0);
+            }
+        }
+    }
     if (lane == 0) a.mtab[e] = (uint8_t)(maxdeg <= kMaxSrc ? maxdeg : kFallback);
     if (bad) report_index_error(a.status);
 }
@@ -135,6 +176,7 @@ struct Smem {
     uint8_t* agh;   // [2W][N] 1 where a sorted position starts a destination's run
     uint8_t* agm;   // [2W][N] the chunk map itself (aggregate pass)
     int* aflag;     // [2W] chunk id held by each operator slot
+    int* prog;      // chunks finished by the workgroup's waves (bounded waits)
     float4* vd;     // [W][N+1] per wave: staged values V[N+1], then Z[N+1] (see Stage)
     float2* x;      // [W][N]
     float2* cs;     // [W][2][N] (forward: staged c_t, two steps)
@@ -155,6 +197,7 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
     s.agh = base + l.agh;
     s.agm = base + l.agm;
     s.aflag = reinterpret_cast<int*>(base + l.aflag);
+    s.prog = reinterpret_cast<int*>(base + l.prog);
     s.vd = reinterpret_cast<float4*>(base + l.vd);
     s.x = reinterpret_cast<float2*>(base + l.x);
     s.cs = reinterpret_cast<float2*>(base + l.cs);
@@ -178,9 +221,10 @@ __device__ __forceinline__ Stage stage_of(const Smem& s, int wv) {
     return Stage{base, base + N + 1};
 }
 
-// Copy head hh's dictionary tables into LDS, append the identity entry and
-// clear every wave's zero row (all threads; a barrier follows).
-template <int N, int W>
+// Copy head hh's dictionary tables into LDS and append the identity entry
+// (all threads; a barrier follows).  The tables sit at the start of every
+// layout of one (N, K), whatever its wave count.
+template <int N>
 __device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, int hh) {
     const int nthr = blockDim.x, tid = threadIdx.x;
     const int K = a.K;
@@ -199,7 +243,12 @@ __device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, 
         s.dict[K * N + j] = (uint8_t)j;
     }
     if (tid == 0) s.mtab[K] = 1;
-    for (int w = tid; w < W; w += nthr) reinterpret_cast<float2*>(s.vd + w * (N + 1))[N] = make_float2(0.f, 0.f);
+}
+
+// Clear the zero row V[N] of the first nw waves' staging rows.
+template <int N>
+__device__ __forceinline__ void clear_zero_rows(const Smem& s, int nw) {
+    for (int w = threadIdx.x; w < nw; w += blockDim.x) reinterpret_cast<float2*>(s.vd + w * (N + 1))[N] = make_float2(0.f, 0.f);
 }
 
 // Gather variant of a head: the smallest of 1, 3, 7 sources covering every
@@ -216,8 +265,10 @@ __device__ __forceinline__ int head_variant(const Smem& s, int K, bool& fallback
         m = max(m, __shfl_xor(m, off));
         fb |= __shfl_xor(fb, off);
     }
-    fallback = fb != 0;
-    return m <= 1 ? 1 : (m <= 3 ? 3 : 7);
+    // the same in every lane: scalar values, so that everything derived
+    // from them (branches, layout offsets) stays scalar
+    fallback = __builtin_amdgcn_readfirstlane(fb) != 0;
+    return __builtin_amdgcn_readfirstlane(m <= 1 ? 1 : (m <= 3 ? 3 : 7));
 }
 
 // Sequence handled by this workgroup.  Workgroups are dispatched round-robin
@@ -232,24 +283,42 @@ __device__ __forceinline__ int xcd_seq(int nseq) {
 
 // Spin on a workgroup hand-off flag until it reaches `want`.  Every flag only
 // grows (atomic max), so a late or early publish can never hide a value
-// another wave waits for.  Bounded: after kSpinLimit polls the wave reports an
-// error and raises every flag of the workgroup (the nflags ints at `all`) to
-// INT_MAX, so that all other waiting waves are released at once and the grid
-// drains.
+// another wave waits for.  Bounded: a wave gives up only after two windows
+// of kSpinLimit polls without the flag, the second one also without progress
+// of the workgroup (*prog did not move: a long but live wait, e.g. for a run
+// of thousands of chunks, keeps going).  It then reports PDSSM_ERR_HIP and raises every flag of the
+// workgroup (the nflags ints at `all`) to INT_MAX, so that all other waiting
+// waves are released at once and the grid drains.
 constexpr int kSpinLimit = 1 << 22;
 constexpr int kErrHang = -4;  // PDSSM_ERR_HIP
 
-__device__ __forceinline__ void wait_ready(int* ready, int want, int* status, int* all, int nflags) {
+__device__ __forceinline__ void wait_ready(int* ready, int want, int* status, int* all, int nflags, const int* prog) {
     int spins = 0;
+    int seen = -1;  // progress count at the end of the last window (none yet)
     while (__hip_atomic_load(ready, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < want) {
         __builtin_amdgcn_s_sleep(1);
         if (++spins > kSpinLimit) {
+            // a window without the flag: keep waiting while the workgroup
+            // finishes chunks, give up after a window in which none finished
+            const int now = __hip_atomic_load(prog, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+            if (seen < 0 || now != seen) {
+                seen = now;
+                spins = 0;
+                continue;
+            }
             if (status && lane_id() == 0) *status = kErrHang;
             for (int i = lane_id(); i < nflags; i += kWave)
                 __hip_atomic_fetch_max(all + i, 0x7fffffff, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             return;
         }
     }
+}
+
+// One more chunk folded by this wave.  Only the aggregate pass's run folds
+// count: they are the one place where a wave waits for another's many chunks
+// (every other hand-off waits for a single chunk, far below one window).
+__device__ __forceinline__ void note_progress(const Smem& s) {
+    if (lane_id() == 0) __hip_atomic_fetch_add(s.prog, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 __device__ __forceinline__ void publish_ready(int* ready, int v) {
@@ -277,19 +346,6 @@ __device__ __forceinline__ void gather_rows(const float2* V, const uint64_t* rec
             acc.v[s].x += v.x;
             acc.v[s].y += v.y;
         }
-    }
-}
-
-// acc += the sources M0 .. M1-1 of a record already in registers.
-template <int M0, int M1>
-__device__ __forceinline__ void gather_rec_range(const float2* V, uint64_t r, float2& acc) {
-    const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
-#pragma unroll
-    for (int m = M0; m < M1; ++m) {
-        const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
-        const float2 v = V[src];
-        acc.x += v.x;
-        acc.y += v.y;
     }
 }
 
@@ -323,30 +379,26 @@ __device__ __forceinline__ void gather_rows_k(const float2* V, const uint64_t* r
 }
 
 // One step h <- bt + P(k) (Dt .* h).  With STAGE_D the step also leaves D_t
-// in Z for a map composition.  FB: the head has entries that need the
-// atomic scatter, tested per step.  M: the step's in-degree class (its map's
-// max in-degree, or kFallback).
+// in Z for a map composition.  FB: the head has entries in sorted form
+// (a row of more than kMaxSrc sources), tested per step.  M: the step's
+// in-degree class (its map's max in-degree, or kFallback).
 template <int N, int G, bool FB, bool STAGE_D>
-__device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, float2* X, int lane, bool act,
-                                        int k, int M, CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt,
-                                        const CV<Lay<N>::SL>& bt) {
+__device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, int lane, bool act, int k, int M,
+                                        CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt, const CV<Lay<N>::SL>& bt) {
     constexpr int SL = Lay<N>::SL;
     if constexpr (FB) {
         if (M == (int)kFallback) {
+            uint64_t w[SL];
+#pragma unroll
+            for (int q = 0; q < SL; ++q) w[q] = act ? s.rec[(size_t)k * N + lane * SL + q] : 0;
             if constexpr (STAGE_D) {
                 wave_sync();
                 if (act) {
 #pragma unroll
-                    for (int q = 0; q < SL; ++q)
-                        st.Z[lane * SL + q] = Dt.v[q];
+                    for (int q = 0; q < SL; ++q) st.Z[lane * SL + q] = Dt.v[q];
                 }
             }
-            IV<SL> pt;
-            if (act) {
-#pragma unroll
-                for (int q = 0; q < SL; ++q) pt.v[q] = s.dict[k * N + lane * SL + q];
-            }
-            pd_scatter_step<N>(X, lane, act, h, Dt, bt, pt);
+            sorted_step<N>(st.V, w, h, Dt, bt, lane, act);
             return;
         }
     }
@@ -453,93 +505,19 @@ __device__ __forceinline__ void finish_chunk(const FusedArgs& a, const Smem& s, 
 // in ascending source order, so the result is deterministic.
 constexpr uint16_t kNoRun = 0xffff;
 
-// DPP move with zero for lanes outside the row mask or without a source.
-template <int CTRL, int ROWS>
-__device__ __forceinline__ int dpp_i(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, true);
-}
-template <int CTRL, int ROWS>
-__device__ __forceinline__ float dpp_fr(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, true));
-}
-
-// Inclusive prefix sum of an int over the 64 lanes.
-__device__ __forceinline__ int wave_incl_scan_i(int v) {
-    v += dpp_i<0x111, 0xf>(v);
-    v += dpp_i<0x112, 0xf>(v);
-    v += dpp_i<0x114, 0xf>(v);
-    v += dpp_i<0x118, 0xf>(v);
-    v += dpp_i<0x142, 0xa>(v);
-    v += dpp_i<0x143, 0xc>(v);
-    return v;
-}
-
-// One step of the segmented scan: add the value DPP brings in when `take`.
-template <int CTRL, int ROWS>
-__device__ __forceinline__ void seg_step(float2& v, bool take) {
-    const float tx = dpp_fr<CTRL, ROWS>(v.x), ty = dpp_fr<CTRL, ROWS>(v.y);
-    v.x += take ? tx : 0.f;
-    v.y += take ? ty : 0.f;
-}
-
-// Inclusive segmented sum over the 64 lanes of a complex value: a lane whose
-// bit is set in `starts` begins a new segment (lane 0 always does).  Row-wise
-// shifts, then the row broadcasts carry row totals across rows, each term
-// taken only when its source lane lies in the same segment.
-__device__ __forceinline__ float2 wave_seg_scan(float2 v, uint64_t starts, int lane) {
-    const uint64_t le = starts & ((2ull << lane) - 1ull);  // lane 63: 2 << 63 wraps to 0
-    const int s0 = le ? 63 - __builtin_clzll(le) : 0;      // first lane of this lane's segment
-    seg_step<0x111, 0xf>(v, lane - 1 >= s0);
-    seg_step<0x112, 0xf>(v, lane - 2 >= s0);
-    seg_step<0x114, 0xf>(v, lane - 4 >= s0);
-    seg_step<0x118, 0xf>(v, lane - 8 >= s0);
-    seg_step<0x142, 0xa>(v, s0 < (lane & ~15));
-    seg_step<0x143, 0xc>(v, s0 < 32);
-    return v;
-}
-
 // Sorted form of the map pm (source j = lane*SL + r goes to row pm[r]),
 // written into operator slot `slot`: agp = sorted position of every source,
 // age = last position of every destination's run (kNoRun if it has no
 // source), agh = run-start flags of the positions.  Runs list their sources
-// in ascending order.  The ranks come from lane masks: table q (N 64-bit
-// words, MT[q]) collects, per row, the lanes whose slot q maps there (an
-// atomic OR, so the result does not depend on the order of the ORs); a
-// source's rank counts the lanes below its own in the tables at its row,
-// plus its lane's earlier slots with the same row, and a row's source count
-// is the popcount of its words.  OFF: N ints of this wave's scratch; MT: SL
-// tables of N words in this wave's staging buffers, free outside the pass.
+// in ascending order; the ranks come from lane-mask tables (map_ranks).
+// OFF: N ints of this wave's scratch; MT: SL tables of N words in this
+// wave's staging buffers, free outside the pass.
 template <int N>
 __device__ __forceinline__ void publish_sorted_map(const Smem& s, int slot, const IV<Lay<N>::SL>& pm, int lane,
                                                    bool act, int* OFF, uint64_t* const (&MT)[Lay<N>::SL]) {
     constexpr int SL = Lay<N>::SL;
-    const uint64_t lt = (1ull << lane) - 1ull;
-    wave_sync();
-#pragma unroll
-    for (int q = 0; q < SL; ++q)
-        for (int i = lane; i < N; i += kWave) MT[q][i] = 0;
-    wave_sync();
-    if (act) {
-#pragma unroll
-        for (int q = 0; q < SL; ++q)
-            __hip_atomic_fetch_or(MT[q] + pm.v[q], 1ull << lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
-    }
-    wave_sync();
     int rank[SL], cnt[SL];
-#pragma unroll
-    for (int r = 0; r < SL; ++r) {
-        int rk = 0, c = 0;
-        if (act) {
-#pragma unroll
-            for (int q = 0; q < SL; ++q) {
-                rk += __builtin_popcountll(MT[q][pm.v[r]] & lt);
-                if (q < r) rk += pm.v[q] == pm.v[r] ? 1 : 0;
-                c += __builtin_popcountll(MT[q][lane * SL + r]);
-            }
-        }
-        rank[r] = rk;
-        cnt[r] = c;
-    }
+    map_ranks<N>(pm, lane, act, MT, rank, cnt);
     int tot = 0;
 #pragma unroll
     for (int r = 0; r < SL; ++r) tot += cnt[r];
@@ -574,6 +552,8 @@ __device__ __forceinline__ void publish_sorted_map(const Smem& s, int slot, cons
 // sequence; the segments of one sequence sit on one XCD.
 struct Work {
     int seq, bb, hh, sg, c0, nc;
+    int wa;   // chunk waves the forward uses (<= W; the rest stay idle); its LDS layout is built for wa
+    int sbm;  // saved-state rows the forward stages in LDS (0: stored as computed)
 };
 
 __device__ __forceinline__ Work work_of(const FusedArgs& a, int nseg, int first_sg) {
@@ -585,6 +565,8 @@ __device__ __forceinline__ Work work_of(const FusedArgs& a, int nseg, int first_
     w.hh = w.seq - w.bb * a.H;
     w.c0 = w.sg * a.Cs;
     w.nc = min(a.C - w.c0, a.Cs);
+    w.wa = 0;
+    w.sbm = 0;
     return w;
 }
 
@@ -638,8 +620,8 @@ struct RunState {
 // Writes an operator (local state Bm, diagonal dm, map pm) into operator slot
 // `slot` (and its sorted map, many-to-one heads), then raises the slot's flag
 // to `flag`.  AGG also keeps the plain map for the frontier's composition.
-template <int N, int W, int G, bool FB, bool AGG>
-__device__ __forceinline__ void publish_op(const Smem& s, int wv, int slot, int flag, const IV<Lay<N>::SL>& pm,
+template <int N, int G, bool FB, bool AGG>
+__device__ __forceinline__ void publish_op(const Smem& s, int wa, int wv, int slot, int flag, const IV<Lay<N>::SL>& pm,
                                            const CV<Lay<N>::SL>& dm, const CV<Lay<N>::SL>& Bm, int lane, bool act) {
     constexpr int SL = Lay<N>::SL;
     const Stage st = stage_of<N>(s, wv);
@@ -657,7 +639,7 @@ __device__ __forceinline__ void publish_op(const Smem& s, int wv, int slot, int 
     if constexpr (!(G == 1 && !FB)) {
         uint64_t* mt[SL];
         mt[0] = reinterpret_cast<uint64_t*>(CS);
-        if constexpr (SL > 1) mt[1] = reinterpret_cast<uint64_t*>(CS + W * N);
+        if constexpr (SL > 1) mt[1] = reinterpret_cast<uint64_t*>(CS + wa * N);
         if constexpr (SL > 2) {
             mt[2] = reinterpret_cast<uint64_t*>(st.Z);
             mt[3] = reinterpret_cast<uint64_t*>(st.V);  // rows 0..N-1: the zero row V[N] stays
@@ -686,8 +668,8 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     const bool act = lane < LANES;
     const int ch = w.c0 + lc;
     const Stage st = stage_of<N>(s, wv);
-    float2* X = s.x + wv * N;
-    float2* CS = s.cs + wv * N;  // buffer 0; buffer 1 is W*N further
+    float2* CS = s.cs + wv * N;  // buffer 0; buffer 1 is Wa*N further (the layout's wave count)
+    const int csb = w.wa * N;
     finish_chunk<N, TAU>(a, s, lane, q, bad);
 
     // ---- 2. one pass: local state B, chunk operator (Pi, Delta), w_t, local readout
@@ -705,11 +687,14 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     }
     CV<SL> wt[TAU];
     float yl[TAU];
-    if constexpr (!FB && Sentinel<N>::kZeroRow) {
+    if constexpr (Sentinel<N>::kZeroRow) {
         // Pipelined form: every step's gather records are read at chunk start;
         // step t then issues one batch of LDS reads -- its gathers, D_t and
         // pi_t at Pi_{t-1}, and c_{t-1} at Pi_{t-1} for w_{t-1} (c staged in
         // two alternating buffers) -- so each step waits for one round trip.
+        // FB: a step whose map is in sorted form (scalar test) stores its
+        // values at their sorted positions and reads its own positions back
+        // in that batch instead of the gathers, then sums the runs.
         uint64_t rec[TAU][SL];
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
@@ -720,8 +705,9 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
             const int k = readlane_i(q.kv, t), gk = readlane_i(q.mv, t);
-            float2* CSt = CS + (t & 1) * (W * N);
-            const float2* CSp = CS + ((t + 1) & 1) * (W * N);
+            const bool fbs = FB && gk == (int)kFallback;
+            float2* CSt = CS + (t & 1) * csb;
+            const float2* CSp = CS + ((t + 1) & 1) * csb;
             const CV<SL> Dv = Dt(q, t);
             wave_sync();
             if (act) {
@@ -729,34 +715,61 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                 for (int r = 0; r < SL; ++r) {
                     if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
                     const float2 v = cmul(Dv.v[r], Bm.v[r]);
-                    st.V[lane * SL + r] = v;
+                    st.V[fbs ? srt_pos(rec[t][r]) : lane * SL + r] = v;
                     st.Z[lane * SL + r] = Dv.v[r];
                 }
             }
             wave_sync();
             float part = 0.f;
+            // the first GM sources of every row with the step's other
+            // reads in one batch; the 7-source class reads the rest only
+            // at steps whose map has a row with more than GM sources
+            constexpr int GM = G > 4 ? 4 : G;
+            float2 acc[SL], Dp[SL], Cp[SL];
+            int np[SL];
+            if constexpr (FB) {
+                // the run sums below take every lane's values
+#pragma unroll
+                for (int r = 0; r < SL; ++r) acc[r] = make_float2(0.f, 0.f);
+            }
             if (act) {
-                // the first GM sources of every row with the step's other
-                // reads in one batch; the 7-source class reads the rest only
-                // at steps whose map has a row with more than GM sources
-                constexpr int GM = G > 4 ? 4 : G;
-                float2 acc[SL], Dp[SL], Cp[SL];
-                int np[SL];
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
-                    acc[r] = q.b[t].v[r];
-                    gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
+                    if (fbs) {
+                        acc[r] = st.V[lane * SL + r];
+                    } else {
+                        acc[r] = q.b[t].v[r];
+                        gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
+                    }
                     const int p = pm.v[r];
                     Dp[r] = st.Z[p];
                     np[r] = s.dict[k * N + p];
                     if constexpr (!AGG) Cp[r] = CSp[p];
                 }
                 if constexpr (G > GM) {
-                    if (gk > GM) {
+                    if (gk > GM && !fbs) {
 #pragma unroll
                         for (int r = 0; r < SL; ++r) gather_rec_range<GM, G>(st.V, rec[t][r], acc[r]);
                     }
                 }
+            }
+            if constexpr (FB) {
+                if (fbs) {
+                    CV<SL> u;
+                    bool sf[SL];
+                    int e[SL];
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) {
+                        u.v[r] = acc[r];
+                        sf[r] = srt_start(rec[t][r]);
+                        e[r] = srt_end(rec[t][r]);
+                    }
+                    const CV<SL> tot = run_totals<N>(st.V, u, sf, e, lane, act);
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) acc[r] = cadd(q.b[t].v[r], tot.v[r]);
+                }
+            }
+            if (act) {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
                     if constexpr (!AGG) {
@@ -773,7 +786,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
             yl[t] = part;
         }
         if constexpr (!AGG) {
-            const float2* CSl = CS + ((TAU - 1) & 1) * (W * N);
+            const float2* CSl = CS + ((TAU - 1) & 1) * csb;
             wave_sync();
             if (act) {
 #pragma unroll
@@ -792,7 +805,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
                 for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
             }
-            pd_step<N, G, FB, true>(s, st, X, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
+            pd_step<N, G, FB, true>(s, st, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
             float part = 0.f;
             if (act) {
 #pragma unroll
@@ -814,29 +827,31 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     }
 
     // ---- 3. publish the chunk operator for the frontier wave, take carry_c.
-    // Slot reuse: the operator of local chunk lc + 2W goes where that of lc
-    // went.  This wave writes it only after carry_{lc+W} arrived, which the
-    // frontier publishes after it read operator lc (the aggregate pass waits
-    // for that hand-off count explicitly).  Carry slot lc % (W + 1) is
-    // rewritten with carry_{lc+W+1} only after the frontier took operator
-    // lc + W from this same wave, which this wave publishes after its read
-    // of carry_lc below (one wave's LDS accesses complete in order).
+    // Slot reuse (Wa = w.wa chunk waves, the stride of the chunks): the
+    // operator of local chunk lc + 2Wa goes where that of lc went.  This wave
+    // writes it only after carry_{lc+Wa} arrived, which the frontier
+    // publishes after it read operator lc (the aggregate pass waits for that
+    // hand-off count explicitly).  Carry slot lc % (Wa + 1) is rewritten with
+    // carry_{lc+Wa+1} only after the frontier took operator lc + Wa from this
+    // same wave, which this wave publishes after its read of carry_lc below
+    // (one wave's LDS accesses complete in order).
     if constexpr (RUN) {
         run->pm = pm;
         run->dm = dm;
         run->Bm = Bm;
+        note_progress(s);
         return;
     }
     {
-        const int slot = lc % (2 * W);
-        if constexpr (AGG) wait_ready(s.ready, lc - 2 * W + 1, a.status, s.ready, 1 + 2 * W);
-        publish_op<N, W, G, FB, AGG>(s, wv, slot, lc, pm, dm, Bm, lane, act);
+        const int slot = lc % (2 * w.wa);
+        if constexpr (AGG) wait_ready(s.ready, lc - 2 * w.wa + 1, a.status, s.ready, 1 + 2 * w.wa, s.prog);
+        publish_op<N, G, FB, AGG>(s, w.wa, wv, slot, lc, pm, dm, Bm, lane, act);
     }
     if constexpr (AGG) return;
-    wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * W);
+    wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * w.wa, s.prog);
     CV<SL> carry = cv_zero<SL>();
-    if (act) carry = ld_cv<SL>(s.ring + (lc % (W + 1)) * N, lane);
-    if (act && a.saved && a.sbM == 0) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
+    if (act) carry = ld_cv<SL>(s.ring + (lc % (w.wa + 1)) * N, lane);
+    if (act && a.saved && w.sbm == 0) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
 
     // ---- 4. readout correction with the true carry, then one store per chunk
 #pragma unroll
@@ -901,37 +916,18 @@ __device__ __forceinline__ CV<Lay<N>::SL> apply_sorted(const ChunkOp<Lay<N>::SL>
     }
     wave_sync();
     if (act) u = ld_cv<SL>(X, lane);
-    // runs within the lane, then across lanes
-    bool seen = false;
+    bool st[SL];
+    int e[SL];
 #pragma unroll
     for (int r = 0; r < SL; ++r) {
-        if (r > 0 && !op.h.v[r]) u.v[r] = cadd(u.v[r], u.v[r - 1]);
-        seen |= op.h.v[r] != 0;
+        st[r] = op.h.v[r] != 0;
+        e[r] = op.e.v[r] == kNoRun ? -1 : op.e.v[r];
     }
-    const uint64_t starts = __builtin_amdgcn_ballot_w64(act && seen);
-    const float2 C = wave_seg_scan(u.v[SL - 1], starts, lane);
-    if constexpr (SL == 1) {
-        u.v[0] = C;
-    } else {
-        const float2 Cp = make_float2(dpp_fr<0x138, 0xf>(C.x), dpp_fr<0x138, 0xf>(C.y));  // from lane - 1
-        bool head = false;
-#pragma unroll
-        for (int r = 0; r < SL; ++r) {
-            head |= op.h.v[r] != 0;
-            if (!head) u.v[r] = cadd(u.v[r], Cp);
-        }
-    }
-    wave_sync();
-    if (act) st_cv<SL>(X, lane, u);
-    wave_sync();
+    const CV<SL> tot = run_totals<N>(X, u, st, e, lane, act);
     CV<SL> nxt = cv_zero<SL>();
     if (act) {
 #pragma unroll
-        for (int r = 0; r < SL; ++r) {
-            const int e = op.e.v[r];
-            const float2 t = X[e == kNoRun ? 0 : e];
-            nxt.v[r] = cadd(op.B.v[r], e == kNoRun ? make_float2(0.f, 0.f) : t);
-        }
+        for (int r = 0; r < SL; ++r) nxt.v[r] = cadd(op.B.v[r], tot.v[r]);
     }
     return nxt;
 }
@@ -952,9 +948,9 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     constexpr bool kPerm = G == 1 && !FB;
     const int lane = lane_id();
     const bool act = lane < LANES;
-    float2* X = s.x + W * N;
+    float2* X = s.x + w.wa * N;
     int* flags = s.ready;
-    const int nflags = 1 + 2 * W;
+    const int nflags = 1 + 2 * w.wa;
     // The aggregate pass folds the segment from zero and composes its map;
     // the scan starts from the state entering its segment.
     CV<SL> carry = AGG ? cv_zero<SL>() : seg_enter_fwd<N>(a, w, lane, act);
@@ -966,12 +962,17 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         accD.v[r] = make_float2(1.f, 0.f);
     }
     __builtin_amdgcn_s_setprio(3);
-    wait_ready(s.aflag, 0, a.status, flags, nflags);
+    wait_ready(s.aflag, 0, a.status, flags, nflags, s.prog);
     ChunkOp<SL> op = read_op<N, !kPerm>(s, 0, lane, act);
-    const int M = AGG || !a.saved ? 0 : a.sbM;
+    const int M = AGG || !a.saved ? 0 : w.sbm;
+    // slot indices c % (Wa + 1) (carry ring) and c % (2 Wa) (operators),
+    // advanced by one per chunk
+    const int nring = w.wa + 1, nops = 2 * w.wa;
+    int rslot = 0, oslot = 0;
     for (int c = 0; c < w.nc; ++c) {
         wave_sync();
-        if (!AGG && act) st_cv<SL>(s.ring + (c % (W + 1)) * N, lane, carry);
+        if (!AGG && act) st_cv<SL>(s.ring + rslot * N, lane, carry);
+        rslot = rslot + 1 == nring ? 0 : rslot + 1;
         if (M > 0 && act) {
             // the first M chunk states wait in LDS until the whole workgroup
             // has read its rows; later ones (near the end anyway) go out now
@@ -987,7 +988,9 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
             }
         }
         const bool more = c + 1 < w.nc;
-        const int nslot = (c + 1) % (2 * W);
+        [[maybe_unused]] const int slot = oslot;
+        const int nslot = oslot + 1 == nops ? 0 : oslot + 1;
+        oslot = nslot;
         int seen = 0x7fffffff;
         ChunkOp<SL> nx;
         if (more) {
@@ -1006,7 +1009,6 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         }
         if constexpr (AGG) {
             // Phi_acc <- Phi_c Phi_acc: (Pi_c[Pi_acc], Delta_c[Pi_acc] * Delta_acc)
-            const int slot = c % (2 * W);
             if (act) {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
@@ -1022,7 +1024,7 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         carry = nxt;
         if (more) {
             if (__builtin_amdgcn_readfirstlane(seen) < c + 1) {
-                wait_ready(s.aflag + nslot, c + 1, a.status, flags, nflags);
+                wait_ready(s.aflag + nslot, c + 1, a.status, flags, nflags, s.prog);
                 nx = read_op<N, !kPerm>(s, nslot, lane, act);
             }
             op = nx;
@@ -1099,7 +1101,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
                 fwd_chunk<N, TAU, W, G, FB, true, true>(a, s, w, lc, q, bad, &rs);
             }
         }
-        publish_op<N, W, G, FB, true>(s, wv, wv, wv, rs.pm, rs.dm, rs.Bm, lane, act);
+        publish_op<N, G, FB, true>(s, w.wa, wv, wv, wv, rs.pm, rs.dm, rs.Bm, lane, act);
         if (bad) report_index_error(a.status);
         return;
     }
@@ -1107,20 +1109,22 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
         fwd_frontier<N, W, G, FB, AGG>(a, s, w);
         return;
     }
+    const int WA = w.wa;
+    if (wv >= WA) return;
     if constexpr (PREFETCH) {
         Chunk<N, TAU> qa, qb;
         issue(wv, qa);
-        for (int lc = wv; lc < w.nc; lc += 2 * W) {
-            issue(lc + W, qb);
+        for (int lc = wv; lc < w.nc; lc += 2 * WA) {
+            issue(lc + WA, qb);
             issue_fence();
             fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc, qa, bad);
-            if (lc + W >= w.nc) break;
-            issue(lc + 2 * W, qa);
+            if (lc + WA >= w.nc) break;
+            issue(lc + 2 * WA, qa);
             issue_fence();
-            fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc + W, qb, bad);
+            fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc + WA, qb, bad);
         }
     } else {
-        for (int lc = wv; lc < w.nc; lc += W) {
+        for (int lc = wv; lc < w.nc; lc += WA) {
             Chunk<N, TAU> q;
             issue(lc, q);
             fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc, q, bad);
@@ -1132,15 +1136,29 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
 template <int N, int TAU, int W, bool AGG, int IO>
 __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     extern __shared__ __align__(16) unsigned char lds[];
-    const Smem s = carve_smem(lds, a.lds);
-    const Work w = AGG ? work_of(a, a.S - 1, 0) : work_of(a, a.S, 0);
+    Smem s = carve_smem(lds, a.lds);
+    Work w = AGG ? work_of(a, a.S - 1, 0) : work_of(a, a.S, 0);
 
-    stage_tables<N, W>(a, s, w.hh);
-    if (threadIdx.x == 0) *s.ready = 0;
-    for (int i = threadIdx.x; i < 2 * W; i += blockDim.x) s.aflag[i] = -1;
+    stage_tables<N>(a, s, w.hh);
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
+    // Heads of permutations stream complex64 rows at the pace of HBM with
+    // kPermWaves chunk waves: more waves only add loads in flight, and the
+    // layout of fewer waves leaves LDS for more staged chunk states.  Other
+    // heads are bound by their chunk passes and use all W.  The tables sit
+    // at the same offsets in both layouts.
+    const bool narrow = __builtin_amdgcn_readfirstlane(!AGG && IO == kIoC64 && G == 1 && !fb && W > kPermWaves) != 0;
+    w.wa = narrow ? kPermWaves : W;
+    w.sbm = narrow ? a.sbM_perm : a.sbM;
+    if (narrow) s = carve_smem(lds, a.lds_perm);
+    clear_zero_rows<N>(s, w.wa);
+    if (threadIdx.x == 0) {
+        *s.ready = 0;
+        *s.prog = 0;
+    }
+    for (int i = threadIdx.x; i < 2 * w.wa; i += blockDim.x) s.aflag[i] = -1;
+    __syncthreads();
     // The aggregate pass loads D and b only and keeps no readout state: its
     // runs prefetch the next chunk at every N (measured registers fit).
     constexpr bool PF = fused_prefetch(N, TAU) || AGG;
@@ -1150,11 +1168,11 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     else fwd_body<N, TAU, W, 7, false, PF, AGG, IO>(a, s, w);
     if constexpr (!AGG) {
         // write out the staged chunk states, every wave a share of the rows
-        if (a.sbM > 0 && a.saved) {
+        if (w.sbm > 0 && a.saved) {
             constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
             const int lane = lane_id();
             __syncthreads();
-            const int rows = min(a.sbM, w.nc);
+            const int rows = min(w.sbm, w.nc);
             float2* dst = a.saved + ((size_t)w.seq * a.C + w.c0) * N;
             if (lane < LANES)
                 for (int i = wave_id(); i < rows; i += W + 1)
@@ -1204,7 +1222,6 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     const Stage st = stage_of<N>(s, wv);
-    float2* X = s.x + wv * N;
     uint8_t* PA = s.pa + wv * N;
     const size_t stride = (size_t)a.H * N;
     const int ch = w.c0 + w.nc - 1 - r;
@@ -1262,7 +1279,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
         materialize(g.v[i].x);
         materialize(g.v[i].y);
     }
-    wait_ready(s.ready, r, a.status, s.ready, 1);
+    wait_ready(s.ready, r, a.status, s.ready, 1, s.prog);
     if constexpr (AGG) {
         // (Gamma, Pi, Delta)_acc <- (gamma_c + Phi_c^H Gamma_acc, Pi_acc[Pi_c], Delta_acc[Pi_c] Delta_c):
         // the aggregate of chunks c .. c1-1, mapping the gradient entering
@@ -1315,7 +1332,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
     for (int t = 0; t < TAU; ++t) {
         const int k = readlane_i(q.kv, t);
         const int M = readlane_i(q.mv, t);
-        pd_step<N, G, FB, false>(s, st, X, lane, act, k, M, hs, Dt(q, t), q.b[t]);
+        pd_step<N, G, FB, false>(s, st, lane, act, k, M, hs, Dt(q, t), q.b[t]);
         Hs[t + 1] = hs;
     }
 
@@ -1442,7 +1459,8 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     const bool act = lane < LANES;
     const Work w = AGG ? work_of(a, a.S - 1, 1) : work_of(a, a.S, 0);
 
-    stage_tables<N, W>(a, s, w.hh);
+    stage_tables<N>(a, s, w.hh);
+    clear_zero_rows<N>(s, W);
     if (wv == 0) {
         if constexpr (AGG) {
             // identity aggregate: Gamma = 0, Pi = id, Delta = 1
@@ -1460,7 +1478,10 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
             const CV<SL> u = seg_enter_bwd<N>(a, w, s.x, lane, act);
             if (act) st_cv<SL>(s.ring, lane, u);
         }
-        if (lane == 0) *s.ready = 0;
+        if (lane == 0) {
+            *s.ready = 0;
+            *s.prog = 0;
+        }
     }
     __syncthreads();
     bool fb;
@@ -1483,11 +1504,13 @@ hipError_t fwd_launch_io(const FusedArgs& a, hipStream_t st) {
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(agg, dim3(a.B * a.H * (a.S - 1)), dim3((W + 1) * 64), a.lds.total, st, a);
     }
+    // every workgroup gets the larger of the two layouts' bytes
+    const uint32_t bytes = a.lds.total > a.lds_perm.total ? a.lds.total : a.lds_perm.total;
     auto kern = k_fwd_fused<N, TAU, W, false, IO>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)a.lds.total);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3(a.B * a.H * a.S), dim3((W + 1) * 64), a.lds.total, st, a);
+    hipLaunchKernelGGL(kern, dim3(a.B * a.H * a.S), dim3((W + 1) * 64), bytes, st, a);
     return hipGetLastError();
 }
 

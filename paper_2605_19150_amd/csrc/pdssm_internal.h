@@ -32,11 +32,15 @@ struct ScanArgs {
     float2* dh0;
     float2* carry;   // [seq][C][N] state entering each chunk (saved or workspace)
     // per-chunk operator (pi_c, d_c) and local term (bias B_c in fwd, local
-    // adjoint gamma_c in bwd)
+    // adjoint gamma_c in bwd); the forward keeps pi_c in sorted form (srt_word)
     int* agg_p;
     float2* agg_d;
     float2* agg_v;
     float2* U;       // bwd: gradient reaching the last state of each chunk from later chunks
+    // per-entry dictionary tables of the prep kernel (PrepArgs), [H][K][N]
+    // words and [H][K] classes: the scatter-adds of the dictionary steps
+    const uint64_t* rec;
+    const uint8_t* mtab;
     int* status;
     // bwd, optional: the scaled states z = D_t .* h_{t-1} [B,L,H,N] that
     // the straight-through gradients need (Sec. 3.1 Prop. 2)
@@ -133,8 +137,9 @@ hipError_t launch_ste_grads(const SteGradArgs& a, hipStream_t s);
 hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int len,
                               int64_t inner, float inv_temp, hipStream_t s);
 
-// LDS bytes the chunked backward's emit kernel needs per workgroup.
-inline size_t bwd_emit_lds_bytes(int N, int tau) { return (size_t)(tau + 2) * N * 8; }
+// LDS bytes the chunked backward's emit kernel needs per workgroup: tau + 1
+// states and an exchange row of N + 1 entries.
+inline size_t bwd_emit_lds_bytes(int N, int tau) { return ((size_t)(tau + 1) * N + N + 1) * 8; }
 constexpr size_t kMaxLdsPerGroup = 65536;
 
 }  // namespace pdssm

@@ -238,7 +238,29 @@ class Scan:
     def _desc(self):
         return ctypes.byref(self.dp if self.prepared else self.d)
 
+    def _check(self, idx, pi, D, b, c, h0=None, dy=None, dh_final=None):
+        """Every tensor argument has the type, shape, device and layout this
+        Scan was built for (the library reads them through raw pointers)."""
+        B, L, H, N, K = self.dims
+        dev = self.device if self.device.index is not None else idx.device
+        _need(idx, "idx", torch.int32, (B, L, H), dev)
+        _need(pi, "pi", torch.int32, (H, K, N), dev)
+        for t, n in ((D, "D"), (b, "b"), (c, "c")):
+            if self.bf16:
+                _need(t, n, torch.bfloat16, (B, L, H, N, 2), dev)
+            elif self.real:
+                _need(t, n, torch.float32, (B, L, H, N), dev)
+            else:
+                _need(t, n, torch.complex64, (B, L, H, N), dev)
+        for t, n in ((h0, "h0"), (dh_final, "dh_final")):
+            if t is not None:
+                _need(t, n, torch.complex64, (B, H, N), dev)
+        if dy is not None:
+            _need(dy, "dy", torch.float32, (B, L, H), dev)
+
     def prepare(self, pi, stream=None):
+        B, L, H, N, K = self.dims
+        _need(pi, "pi", torch.int32, (H, K, N), pi.device)
         st = load().pdssm_prepare(ctypes.byref(self.d), _p(pi), _p(self.ws), self.ws.numel(),
                                   _p(self.status), _stream(stream))
         if st != OK:
@@ -246,6 +268,7 @@ class Scan:
         self.prepared = True
 
     def fwd(self, idx, pi, D, b, c, h0=None, stream=None):
+        self._check(idx, pi, D, b, c, h0=h0)
         st = load().pdssm_scan_fwd(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
                                    _p(h0), _p(self.y), _p(self.h_final), _p(self.saved),
                                    _p(self.ws), self.ws.numel(), _p(self.status), _stream(stream))
@@ -254,6 +277,7 @@ class Scan:
         return self.y, self.h_final, self.saved
 
     def bwd(self, idx, pi, D, b, c, dy, dh_final=None, stream=None):
+        self._check(idx, pi, D, b, c, dy=dy, dh_final=dh_final)
         st = load().pdssm_scan_bwd(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
                                    _p(self.saved), _p(dy), _p(dh_final), _p(self.dD), _p(self.db),
                                    _p(self.dc), _p(self.dh0), _p(self.ws), self.ws.numel(),
@@ -264,6 +288,7 @@ class Scan:
 
     def bwd_ste(self, idx, pi, D, b, c, dy, dh_final=None, stream=None):
         """bwd() plus the scaled states z (Scan(..., ste=True))."""
+        self._check(idx, pi, D, b, c, dy=dy, dh_final=dh_final)
         st = load().pdssm_scan_bwd_ste(self._desc(), _p(idx), _p(pi), _p(D), _p(b), _p(c),
                                        _p(self.saved), _p(dy), _p(dh_final), _p(self.dD), _p(self.db),
                                        _p(self.dc), _p(self.dh0), _p(self.z), _p(self.ws),
@@ -276,6 +301,9 @@ class Scan:
         """Scores q [B,L,H,K] and dictionary gradient G [H,K,N,N] from the db
         and z of the last bwd_ste() (each None when not asked for)."""
         qq, GG = (self.q if q else None), (self.G if G else None)
+        B, L, H, N, K = self.dims
+        _need(idx, "idx", torch.int32, (B, L, H), self.db.device)
+        _need(pi, "pi", torch.int32, (H, K, N), self.db.device)
         st = load().pdssm_ste_grads(ctypes.byref(self.d), _p(idx), _p(pi), _p(self.db), _p(self.z), _p(qq),
                                     _p(GG), _p(self.ws_ste), self.ws_ste.numel(), _p(self.status),
                                     _stream(stream))

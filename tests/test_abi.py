@@ -196,6 +196,34 @@ def test_fwd_rejects_aliasing_and_misalignment(lib):
     assert _fwd_call(lib, d, {"D": ctypes.c_void_p(shared.value + 4)}) == pdssm.ERR_INVALID_ARG
 
 
+def test_word_arrays_must_be_4_byte_aligned(lib):
+    """idx, y and dy are read and written as 4-byte words: a pointer off a
+    4-byte boundary is rejected on the host (forward, backward, decode)."""
+    d = pdssm.desc(2, 40, 2, 64, 4)
+    f = FakeBufs()
+    idx, y = f(2 * 40 * 2 * 4), f(2 * 40 * 2 * 4)
+    assert _fwd_call(lib, d, {"idx": ctypes.c_void_p(idx.value + 2)}) == pdssm.ERR_INVALID_ARG
+    assert _fwd_call(lib, d, {"y": ctypes.c_void_p(y.value + 1)}) == pdssm.ERR_INVALID_ARG
+    st = 2 * 40 * 2 * 64 * 8
+    args = [f(2 * 40 * 2 * 4), f(2 * 4 * 64 * 4)] + [f(st) for _ in range(3)] + [f(2 * 2 * 5 * 64 * 8)]
+    dy = f(2 * 40 * 2 * 4)
+    outs = [f(st) for _ in range(3)] + [None]
+    need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
+    ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
+    assert lib.pdssm_scan_bwd(ctypes.byref(d), *args, ctypes.c_void_p(dy.value + 2), None, *outs, ws, need,
+                              None, None) == pdssm.ERR_INVALID_ARG
+    a2 = list(args)
+    a2[0] = ctypes.c_void_p(args[0].value + 1)
+    assert lib.pdssm_scan_bwd(ctypes.byref(d), *a2, dy, None, *outs, ws, need, None, None) == pdssm.ERR_INVALID_ARG
+    dd = pdssm.desc(2, 1, 3, 64, 4)
+    row = 2 * 3 * 64 * 8
+    di, dpi, D, b, c, h, dyy = f(2 * 3 * 4), f(3 * 4 * 64 * 4), f(row), f(row), f(row), f(row), f(2 * 3 * 4)
+    assert lib.pdssm_decode_step(ctypes.byref(dd), ctypes.c_void_p(di.value + 2), dpi, D, b, c, None, h, dyy,
+                                 None, None) == pdssm.ERR_INVALID_ARG
+    assert lib.pdssm_decode_step(ctypes.byref(dd), di, dpi, D, b, c, None, h, ctypes.c_void_p(dyy.value + 2),
+                                 None, None) == pdssm.ERR_INVALID_ARG
+
+
 def test_bwd_and_compose_reject_null(lib):
     d = pdssm.desc(2, 40, 2, 64, 4)
     P = ctypes.c_void_p(1 << 40)

@@ -85,3 +85,44 @@ def test_largest_problem_automaton():
         assert_close("dD tail", s.dD[:, t0:, hh:hh + 1].cpu().numpy(), rdD)
     del s, D, b, c, idx_d, pi_d, h0, dy_d
     torch.cuda.empty_cache()
+
+
+def test_longest_single_sequence_automaton():
+    """One sequence of the longest length the ABI accepts at N = 128
+    (B*L*H*N just below 2^31): cut into 8 segments whose aggregate pass folds
+    runs of ~37,000 chunks per wave, so the frontier waits ~0.1 s for each
+    run.  The waits must keep going while the runs progress (status 0), and
+    the forward stays exact on the automaton embedding of App. D."""
+    B, H, N, K = 1, 1, 128, 16
+    L = (2**31 - 1) // (B * H * N)  # 16777215 steps
+    d = pdssm.desc(B, L, H, N, K)
+    nseg = pdssm.scan_segments(d)
+    print("longest sequence: L=%d N=%d, %d chunks, %d segments" % (L, N, pdssm.num_chunks(d), nseg), flush=True)
+    assert nseg == 8 and pdssm.uses_fused(d) == 1
+    rng = np.random.default_rng(11)
+    idx = rng.integers(0, K, size=(B, L, H), dtype=np.int32)
+    pi = rng.integers(0, N, size=(H, K, N)).astype(np.int32)
+    start = int(rng.integers(0, N))
+    acc = (rng.random(N) < 0.5).astype(np.float32)
+
+    idx_d = torch.from_numpy(idx).to(DEV)
+    pi_d = torch.from_numpy(pi).to(DEV)
+    shape = (B, L, H, N)
+    D = torch.ones(shape, dtype=torch.complex64, device=DEV)
+    b = torch.zeros(shape, dtype=torch.complex64, device=DEV)
+    c = torch.from_numpy(acc).to(DEV).to(torch.complex64).expand(shape).contiguous()
+    h0 = torch.zeros((B, H, N), dtype=torch.complex64, device=DEV)
+    h0[0, 0, start] = 1.0
+
+    s = pdssm.Scan(B, L, H, N, K)
+    s.prepare(pi_d)
+    s.fwd(idx_d, pi_d, D, b, c, h0=h0)
+    s.check_status()  # raises on PDSSM_ERR_HIP from a wait that gave up
+    print("longest sequence: forward done", flush=True)
+    st = _simulate(pi[0], idx[0, :, 0], start)
+    np.testing.assert_array_equal(s.y[0, :, 0].cpu().numpy(), acc[st])
+    ref = np.zeros(N, np.complex64)
+    ref[st[-1]] = 1.0
+    np.testing.assert_array_equal(s.h_final[0, 0].cpu().numpy(), ref)
+    del s, D, b, c, idx_d, pi_d, h0
+    torch.cuda.empty_cache()

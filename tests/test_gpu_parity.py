@@ -114,11 +114,62 @@ def test_mixed_degenerate_and_regular_entries():
     check_all(inp, got, eff_chunk(inp))
 
 
+def _force_sorted_entries(inp, N):
+    """Entries with a row of more than seven sources (stored in sorted form):
+    in-degree exactly 8 in head 0, all-to-one in head 1, two rows of 12 and
+    9 sources in head 2 (if present); steps choose them often."""
+    H, K = inp["pi"].shape[:2]
+    inp["pi"][0, 1, :8] = 5
+    inp["pi"][1 % H, 0, :] = N - 1
+    if H > 2:
+        inp["pi"][2, 3, :12] = 0
+        inp["pi"][2, 3, 12:21] = N // 2
+    inp["idx"][:, ::2, 0] = 1
+    inp["idx"][:, 1::3, 1 % H] = 0
+
+
+@pytest.mark.parametrize("N,chunk", [(16, 8), (32, 16), (64, 4), (64, 8), (64, 16), (128, 4), (128, 8),
+                                     (256, 4)])
+def test_sorted_form_entries(N, chunk):
+    """Heads whose dictionary has entries of in-degree > 7 next to regular
+    ones: those steps sum each row's run by a segmented scan inside the
+    pipelined chunk pass (and in the backward's state recompute)."""
+    inp = make_inputs(B=2, L=300, H=3, N=N, K=6, seed=N + chunk, with_h0=True, with_dhf=True)
+    _force_sorted_entries(inp, N)
+    got = run_gpu(inp, chunk=chunk)
+    check_all(inp, got, chunk)
+
+
+@pytest.mark.parametrize("N,L", [(64, 1500), (128, 2000)])
+def test_segmented_scan_with_sorted_form_entries(N, L):
+    """One long sequence cut into segments (aggregate pass, then one
+    workgroup per segment) where some dictionary entries are in sorted form:
+    the run folds of the aggregate pass and the frontier's composition of
+    such runs, forward and backward."""
+    K = 5
+    d = pdssm.desc(1, L, 1, N, K)
+    assert pdssm.scan_segments(d) > 1
+    inp = make_inputs(B=1, L=L, H=1, N=N, K=K, seed=L + 3, with_h0=True, with_dhf=True)
+    inp["pi"][0, 1, :9] = 5
+    inp["pi"][0, 3, :] = 0
+    inp["idx"][:, ::4, 0] = 1
+    inp["idx"][:, 2::5, 0] = 3
+    got = run_gpu(inp)
+    check_all(inp, got, eff_chunk(inp))
+
+
 @pytest.mark.parametrize("N,K", [(128, 128), (256, 64)])
 def test_large_dictionary_chunked_path(N, K):
     """A head's dictionary tables too large for LDS: the chunked three-pass
-    kernels run instead, with the same saved-state layout."""
+    kernels run instead, with the same saved-state layout.  Some entries have
+    a row of more than seven sources (the sorted form), and steps choose them
+    often."""
     inp = make_inputs(B=2, L=90, H=2, N=N, K=K, seed=N + K, with_h0=True, with_dhf=True)
+    assert pdssm.uses_fused(pdssm.desc(2, 90, 2, N, K)) == 0
+    inp["pi"][0, 1, :8] = 3          # in-degree exactly 8
+    inp["pi"][1, 2, :] = N - 1       # all to one row
+    inp["idx"][:, ::3, 0] = 1
+    inp["idx"][:, 1::4, 1] = 2
     got = run_gpu(inp)
     check_all(inp, got, eff_chunk(inp))
 
@@ -247,15 +298,52 @@ def test_segment_protocol_from_entry_points(N, pi_kind):
     assert_close("h_final by segments", hfin.cpu().numpy(), rhf)
 
 
-@pytest.mark.parametrize("N,B,L,H", [(64, 2, 300, 4), (128, 2, 300, 4), (256, 2, 300, 4), (128, 1, 2000, 1)])
-def test_deterministic(N, B, L, H):
-    """Two runs give the same bits: colliding sources are added in a fixed
-    order (uniform maps; the last case runs in segments)."""
-    inp = make_inputs(B=B, L=L, H=H, N=N, K=8, seed=5, with_dhf=True)
+@pytest.mark.parametrize("N,B,L,H,K,sorted_form", [
+    (64, 2, 300, 4, 8, False), (128, 2, 300, 4, 8, False), (256, 2, 300, 4, 8, False),
+    (128, 1, 2000, 1, 8, False), (64, 2, 300, 3, 8, True), (128, 1, 2000, 3, 8, True),
+    (256, 2, 300, 3, 16, True), (128, 2, 90, 3, 128, True), (256, 2, 90, 3, 64, True)])
+def test_deterministic(N, B, L, H, K, sorted_form):
+    """Two runs give the same bits: colliding sources are added in an order
+    fixed by the map (uniform maps; with sorted_form also entries of
+    in-degree > 7; segmented sequences; the multi-pass kernels at K = 128
+    (N = 128) and K = 64 (N = 256))."""
+    inp = make_inputs(B=B, L=L, H=H, N=N, K=K, seed=5, with_h0=True, with_dhf=True)
+    if sorted_form:
+        _force_sorted_entries(inp, N)
     a = run_gpu(inp)
     b = run_gpu(inp)
     for k in a:
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def test_deterministic_full_size_manyone():
+    """The many-to-one workload at full size (B16 L2048 H16 N64 K16, Markov
+    map choices), whose head 4 has an entry of in-degree 9: two runs give the
+    same bits in every output."""
+    w = WORKLOADS[3]
+    inp = workload(3)
+    assert _max_in_degree(inp["pi"]) > 7
+    T = to_dev(inp)
+    outs = []
+    for _ in range(2):
+        s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K)
+        s.prepare(T["pi"])
+        s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
+        s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
+        s.check_status()
+        outs.append({k: getattr(s, k).clone() for k in ("y", "h_final", "saved", "dD", "db", "dc", "dh0")})
+        del s
+    for k in outs[0]:
+        assert torch.equal(outs[0][k], outs[1][k]), k
+
+
+def _max_in_degree(pi):
+    H, K, N = pi.shape
+    m = 0
+    for h in range(H):
+        for k in range(K):
+            m = max(m, int(np.bincount(pi[h, k], minlength=N).max()))
+    return m
 
 
 @pytest.mark.parametrize("N,K,pi_kind", [(64, 16, "perm"), (64, 16, "uniform"), (128, 64, "uniform"),
@@ -393,9 +481,13 @@ def test_workload1_tiny_full():
 
 
 @pytest.mark.parametrize("wi", [2, 3, 4, 5])
-def test_workload_full_size_sampled(wi):
-    """Full-size run in the benchmark's launch configuration; the oracle checks
-    a sample of whole sequences (first, last and two in between)."""
+def test_workload_full_size_every_sequence(wi):
+    """Full-size run in the benchmark's launch configuration (prepared
+    tables, the same chunk and segments); every sequence is checked against
+    the oracle on its own (a pool of host threads runs the float64 oracle one
+    sequence per task): y, h_final, saved states, dD, db, dc and dh0."""
+    from concurrent.futures import ThreadPoolExecutor
+
     w = WORKLOADS[wi]
     print("workload %d: %s" % (wi, w.name), flush=True)
     inp = workload(wi)
@@ -405,17 +497,24 @@ def test_workload_full_size_sampled(wi):
     s.fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"])
     s.bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], T["dy"])
     s.check_status()
-    picks = sorted({(0, 0), (w.B - 1, w.H - 1), (w.B // 2, 1 % w.H), (1 % w.B, w.H // 2)})
-    for bb, hh in picks:
+    del T
+    host = {k: getattr(s, k).cpu().numpy() for k in ("y", "h_final", "saved", "dD", "db", "dc", "dh0")}
+    del s
+    print("workload %d: outputs on the host, checking %d sequences" % (wi, w.B * w.H), flush=True)
+
+    def one(bh):
+        bb, hh = bh
         sub = sub_sequence(inp, bb, hh)
-        got = dict(y=s.y[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
-                   h_final=s.h_final[bb:bb + 1, hh:hh + 1].cpu().numpy(),
-                   saved=s.saved[bb:bb + 1, hh:hh + 1].cpu().numpy(),
-                   dD=s.dD[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
-                   db=s.db[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
-                   dc=s.dc[bb:bb + 1, :, hh:hh + 1].cpu().numpy(),
-                   dh0=s.dh0[bb:bb + 1, hh:hh + 1].cpu().numpy())
-        check_all(sub, got, s.chunk)
-    # properties over every sequence: finite outputs
-    for t in (s.y, s.h_final, s.dD, s.db, s.dc, s.dh0):
-        assert torch.isfinite(torch.view_as_real(t) if t.is_complex() else t).all()
+        got = dict(y=host["y"][bb:bb + 1, :, hh:hh + 1], h_final=host["h_final"][bb:bb + 1, hh:hh + 1],
+                   saved=host["saved"][bb:bb + 1, hh:hh + 1], dD=host["dD"][bb:bb + 1, :, hh:hh + 1],
+                   db=host["db"][bb:bb + 1, :, hh:hh + 1], dc=host["dc"][bb:bb + 1, :, hh:hh + 1],
+                   dh0=host["dh0"][bb:bb + 1, hh:hh + 1])
+        try:
+            check_all(sub, got, pdssm.chunk_len(pdssm.desc(w.B, w.L, w.H, w.N, w.K)))
+        except AssertionError as e:
+            return "sequence (b=%d, h=%d): %s" % (bb, hh, e)
+        return None
+
+    with ThreadPoolExecutor(max_workers=16) as pool:
+        errs = [e for e in pool.map(one, [(bb, hh) for bb in range(w.B) for hh in range(w.H)]) if e]
+    assert not errs, "%d sequences differ; first: %s" % (len(errs), errs[0])
