@@ -57,7 +57,12 @@
  *     per-wave buffers, are staged in the 160 KiB LDS of a workgroup; larger
  *     dictionaries run slower multi-pass kernels with the same results.
  *   - Calls on different streams may run concurrently if their outputs and
- *     workspaces do not overlap; the library keeps no mutable global state.
+ *     workspaces do not overlap; the library keeps no mutable global state
+ *     apart from the device array of pdssm_scan_fwd_noalloc.
+ *   - Waits between the waves of a workgroup are bounded: a wait that sees no
+ *     progress for a long window (a fault, not a slow input) stores
+ *     PDSSM_ERR_HIP to *dev_status and releases every wave, so the kernel
+ *     always ends.
  */
 #ifndef PDSSM_H
 #define PDSSM_H
@@ -120,7 +125,7 @@ typedef enum pdssm_status {
     PDSSM_ERR_INVALID_ARG = -1, /* NULL required pointer, bad size, overlap, unknown flags */
     PDSSM_ERR_UNSUPPORTED = -2, /* N, K or chunk outside the supported set */
     PDSSM_ERR_WORKSPACE = -3,   /* ws NULL or smaller than pdssm_workspace_size */
-    PDSSM_ERR_HIP = -4,         /* a HIP launch reported an error */
+    PDSSM_ERR_HIP = -4,         /* a HIP call reported an error; in *dev_status: a wait gave up */
     PDSSM_ERR_INDEX = -5        /* written to *dev_status by kernels only */
 } pdssm_status;
 
@@ -191,6 +196,30 @@ int pdssm_scan_fwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi
                    const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
                    const pdssm_c64* h0, float* y, pdssm_c64* h_final, pdssm_c64* saved,
                    void* ws, size_t ws_bytes, int* dev_status, void* stream);
+
+/*
+ * pdssm_scan_fwd for callers that cannot allocate device memory or pass a
+ * workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  Same arguments and results as pdssm_scan_fwd
+ * without ws / ws_bytes; the workspace is a device array inside the library,
+ * PDSSM_NOALLOC_SCRATCH_BYTES bytes per GPU, held from the first call on a
+ * GPU until the process ends.  The call uses the array of the current device
+ * (hipGetDevice); the stream must belong to that device.  It allocates and
+ * frees nothing.
+ *   - PDSSM_ERR_WORKSPACE when pdssm_workspace_size(desc, PDSSM_OP_FWD)
+ *     exceeds the array (every workload of up to 256 dictionary entries of
+ *     N = 128 per head, and segmented long sequences, fit).
+ *   - PDSSM_ERR_INVALID_ARG with PDSSM_FLAG_PREPARED (the tables are built
+ *     in the array by every call).
+ * Every call on one GPU shares that GPU's array, which keeps the last
+ * call's contents (each call rebuilds everything it reads there): calls that
+ * overlap in time on one GPU (different streams, or host threads) race.
+ */
+#define PDSSM_NOALLOC_SCRATCH_BYTES (16u << 20)
+int pdssm_scan_fwd_noalloc(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
+                           const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
+                           const pdssm_c64* h0, float* y, pdssm_c64* h_final, pdssm_c64* saved,
+                           int* dev_status, void* stream);
 
 /*
  * Backward scan: the vector-Jacobian product of pdssm_scan_fwd (the paper

@@ -18,6 +18,7 @@ SOURCES = [("pdssm_fused.hip", ["-DPDSSM_N=%d" % n], "pdssm_fused_n%d" % n)
     ("pdssm_ste.hip", [], "pdssm_ste"),
     ("pdssm_decode.hip", [], "pdssm_decode"),
     ("pdssm_select.hip", [], "pdssm_select"),
+    ("pdssm_noalloc.hip", [], "pdssm_noalloc"),
     ("pdssm_api.cpp", [], "pdssm_api"),
 ]
 

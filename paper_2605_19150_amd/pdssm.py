@@ -46,7 +46,7 @@ class Desc(ctypes.Structure):
 
 
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
-           "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd",
+           "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd", "pdssm_scan_fwd_noalloc",
            "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_ste_grads",
            "pdssm_softmax_vjp", "pdssm_decode_step", "pdssm_dict_argmax", "pdssm_route")
 
@@ -75,6 +75,8 @@ def load():
     L.pdssm_prepare.argtypes, L.pdssm_prepare.restype = [D, P, P, Z, P, P], I
     L.pdssm_scan_fwd.argtypes = [D] + [P] * 10 + [Z, P, P]
     L.pdssm_scan_fwd.restype = I
+    L.pdssm_scan_fwd_noalloc.argtypes = [D] + [P] * 11
+    L.pdssm_scan_fwd_noalloc.restype = I
     L.pdssm_scan_bwd.argtypes = [D] + [P] * 13 + [Z, P, P]
     L.pdssm_scan_bwd.restype = I
     L.pdssm_compose_chunks.argtypes = [D] + [P] * 7
@@ -339,6 +341,30 @@ def scan_fwd(idx, pi, D, b, c, h0=None, chunk=0, stream=None):
     s.fwd(idx, pi, D, b, c, h0, stream)
     s.check_status()
     return s.y, s.h_final, s.saved
+
+
+def scan_fwd_noalloc(idx, pi, D, b, c, h0=None, chunk=0, y=None, h_final=None, saved=None, stream=None):
+    """pdssm_scan_fwd_noalloc: the forward with the library's own device
+    workspace (no workspace argument).  Outputs may be passed in (y, h_final,
+    saved); the call then allocates nothing.  Returns (y, h_final, saved)."""
+    B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
+    h0 = _state_arg(h0, "h0", is_real_io(D), (B, H, N), dev)
+    d = desc(B, L, H, N, K, chunk)
+    d.flags = (FLAG_BF16_IO if is_bf16_io(D) else 0) | (FLAG_REAL_IO if is_real_io(D) else 0)
+    C = num_chunks(d)
+    if C < 0:
+        raise PdssmError(C, "num_chunks")
+    y = torch.empty((B, L, H), dtype=torch.float32, device=dev) if y is None else y
+    h_final = torch.empty((B, H, N), dtype=torch.complex64, device=dev) if h_final is None else h_final
+    saved = torch.empty((B, H, C, N), dtype=torch.complex64, device=dev) if saved is None else saved
+    _need(y, "y", torch.float32, (B, L, H), dev)
+    _need(h_final, "h_final", torch.complex64, (B, H, N), dev)
+    _need(saved, "saved", torch.complex64, (B, H, C, N), dev)
+    st = load().pdssm_scan_fwd_noalloc(ctypes.byref(d), _p(idx), _p(pi), _p(D), _p(b), _p(c), _p(h0), _p(y),
+                                       _p(h_final), _p(saved), None, _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_scan_fwd_noalloc")
+    return y, h_final, saved
 
 
 def scan_bwd(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
