@@ -37,9 +37,10 @@
 // rounded up), so the step has no branches: unused record slots point at a
 // row that stays zero.  An entry with a row of in-degree above 7 (rare for
 // random maps, e.g. an all-to-one map) is stored in sorted form instead and
-// its steps sum each row's run with a segmented scan across lanes, behind one
-// scalar branch per step; heads without such entries never test for it.  No
-// sum uses float atomics, so results are deterministic.
+// its steps sum each row's run with a segmented scan across lanes; a head
+// with such entries runs the step-by-step chunk pass, whose steps test their
+// map's class (heads without them never test for it).  No sum uses float
+// atomics, so results are deterministic.
 //
 // The last chunk of a sequence may be short; its missing steps run as exact
 // no-ops (D = 1, b = 0, an identity dictionary entry at index K), so no step
@@ -556,6 +557,15 @@ struct Work {
     int sbm;  // saved-state rows the forward stages in LDS (0: stored as computed)
 };
 
+// The chunk waves a forward workgroup uses: w.wa in a wide kernel (a head of
+// permutations may run fewer), else W itself as a compile-time constant (so
+// that slot numbers and buffer offsets fold into the instructions).
+template <int W>
+__device__ __forceinline__ int active_waves(const Work& w) {
+    if constexpr (W > kPermWaves) return w.wa;
+    else return W;
+}
+
 __device__ __forceinline__ Work work_of(const FusedArgs& a, int nseg, int first_sg) {
     Work w;
     const int u = xcd_seq(a.B * a.H * nseg);
@@ -669,7 +679,8 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     const int ch = w.c0 + lc;
     const Stage st = stage_of<N>(s, wv);
     float2* CS = s.cs + wv * N;  // buffer 0; buffer 1 is Wa*N further (the layout's wave count)
-    const int csb = w.wa * N;
+    const int WA = active_waves<W>(w);
+    const int csb = WA * N;
     finish_chunk<N, TAU>(a, s, lane, q, bad);
 
     // ---- 2. one pass: local state B, chunk operator (Pi, Delta), w_t, local readout
@@ -687,14 +698,14 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     }
     CV<SL> wt[TAU];
     float yl[TAU];
-    if constexpr (Sentinel<N>::kZeroRow) {
+    if constexpr (!FB && Sentinel<N>::kZeroRow) {
         // Pipelined form: every step's gather records are read at chunk start;
         // step t then issues one batch of LDS reads -- its gathers, D_t and
         // pi_t at Pi_{t-1}, and c_{t-1} at Pi_{t-1} for w_{t-1} (c staged in
         // two alternating buffers) -- so each step waits for one round trip.
-        // FB: a step whose map is in sorted form (scalar test) stores its
-        // values at their sorted positions and reads its own positions back
-        // in that batch instead of the gathers, then sums the runs.
+        // (Heads with entries in sorted form take the step-by-step form
+        // below: their steps in this pass measured 13% slower at N = 128,
+        // hybrid-lm 622 -> 703 us, and no faster at N = 64.)
         uint64_t rec[TAU][SL];
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
@@ -705,7 +716,6 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
             const int k = readlane_i(q.kv, t), gk = readlane_i(q.mv, t);
-            const bool fbs = FB && gk == (int)kFallback;
             float2* CSt = CS + (t & 1) * csb;
             const float2* CSp = CS + ((t + 1) & 1) * csb;
             const CV<SL> Dv = Dt(q, t);
@@ -715,61 +725,34 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                 for (int r = 0; r < SL; ++r) {
                     if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
                     const float2 v = cmul(Dv.v[r], Bm.v[r]);
-                    st.V[fbs ? srt_pos(rec[t][r]) : lane * SL + r] = v;
+                    st.V[lane * SL + r] = v;
                     st.Z[lane * SL + r] = Dv.v[r];
                 }
             }
             wave_sync();
             float part = 0.f;
-            // the first GM sources of every row with the step's other
-            // reads in one batch; the 7-source class reads the rest only
-            // at steps whose map has a row with more than GM sources
-            constexpr int GM = G > 4 ? 4 : G;
-            float2 acc[SL], Dp[SL], Cp[SL];
-            int np[SL];
-            if constexpr (FB) {
-                // the run sums below take every lane's values
-#pragma unroll
-                for (int r = 0; r < SL; ++r) acc[r] = make_float2(0.f, 0.f);
-            }
             if (act) {
+                // the first GM sources of every row with the step's other
+                // reads in one batch; the 7-source class reads the rest only
+                // at steps whose map has a row with more than GM sources
+                constexpr int GM = G > 4 ? 4 : G;
+                float2 acc[SL], Dp[SL], Cp[SL];
+                int np[SL];
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
-                    if (fbs) {
-                        acc[r] = st.V[lane * SL + r];
-                    } else {
-                        acc[r] = q.b[t].v[r];
-                        gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
-                    }
+                    acc[r] = q.b[t].v[r];
+                    gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
                     const int p = pm.v[r];
                     Dp[r] = st.Z[p];
                     np[r] = s.dict[k * N + p];
                     if constexpr (!AGG) Cp[r] = CSp[p];
                 }
                 if constexpr (G > GM) {
-                    if (gk > GM && !fbs) {
+                    if (gk > GM) {
 #pragma unroll
                         for (int r = 0; r < SL; ++r) gather_rec_range<GM, G>(st.V, rec[t][r], acc[r]);
                     }
                 }
-            }
-            if constexpr (FB) {
-                if (fbs) {
-                    CV<SL> u;
-                    bool sf[SL];
-                    int e[SL];
-#pragma unroll
-                    for (int r = 0; r < SL; ++r) {
-                        u.v[r] = acc[r];
-                        sf[r] = srt_start(rec[t][r]);
-                        e[r] = srt_end(rec[t][r]);
-                    }
-                    const CV<SL> tot = run_totals<N>(st.V, u, sf, e, lane, act);
-#pragma unroll
-                    for (int r = 0; r < SL; ++r) acc[r] = cadd(q.b[t].v[r], tot.v[r]);
-                }
-            }
-            if (act) {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
                     if constexpr (!AGG) {
@@ -843,14 +826,14 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
         return;
     }
     {
-        const int slot = lc % (2 * w.wa);
-        if constexpr (AGG) wait_ready(s.ready, lc - 2 * w.wa + 1, a.status, s.ready, 1 + 2 * w.wa, s.prog);
-        publish_op<N, G, FB, AGG>(s, w.wa, wv, slot, lc, pm, dm, Bm, lane, act);
+        const int slot = lc % (2 * WA);
+        if constexpr (AGG) wait_ready(s.ready, lc - 2 * WA + 1, a.status, s.ready, 1 + 2 * WA, s.prog);
+        publish_op<N, G, FB, AGG>(s, WA, wv, slot, lc, pm, dm, Bm, lane, act);
     }
     if constexpr (AGG) return;
-    wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * w.wa, s.prog);
+    wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * WA, s.prog);
     CV<SL> carry = cv_zero<SL>();
-    if (act) carry = ld_cv<SL>(s.ring + (lc % (w.wa + 1)) * N, lane);
+    if (act) carry = ld_cv<SL>(s.ring + (lc % (WA + 1)) * N, lane);
     if (act && a.saved && w.sbm == 0) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
 
     // ---- 4. readout correction with the true carry, then one store per chunk
@@ -948,9 +931,10 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     constexpr bool kPerm = G == 1 && !FB;
     const int lane = lane_id();
     const bool act = lane < LANES;
-    float2* X = s.x + w.wa * N;
+    const int WA = active_waves<W>(w);
+    float2* X = s.x + WA * N;
     int* flags = s.ready;
-    const int nflags = 1 + 2 * w.wa;
+    const int nflags = 1 + 2 * WA;
     // The aggregate pass folds the segment from zero and composes its map;
     // the scan starts from the state entering its segment.
     CV<SL> carry = AGG ? cv_zero<SL>() : seg_enter_fwd<N>(a, w, lane, act);
@@ -967,7 +951,7 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     const int M = AGG || !a.saved ? 0 : w.sbm;
     // slot indices c % (Wa + 1) (carry ring) and c % (2 Wa) (operators),
     // advanced by one per chunk
-    const int nring = w.wa + 1, nops = 2 * w.wa;
+    const int nring = WA + 1, nops = 2 * WA;
     int rslot = 0, oslot = 0;
     for (int c = 0; c < w.nc; ++c) {
         wave_sync();
@@ -1101,7 +1085,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
                 fwd_chunk<N, TAU, W, G, FB, true, true>(a, s, w, lc, q, bad, &rs);
             }
         }
-        publish_op<N, G, FB, true>(s, w.wa, wv, wv, wv, rs.pm, rs.dm, rs.Bm, lane, act);
+        publish_op<N, G, FB, true>(s, active_waves<W>(w), wv, wv, wv, rs.pm, rs.dm, rs.Bm, lane, act);
         if (bad) report_index_error(a.status);
         return;
     }
@@ -1109,7 +1093,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
         fwd_frontier<N, W, G, FB, AGG>(a, s, w);
         return;
     }
-    const int WA = w.wa;
+    const int WA = active_waves<W>(w);
     if (wv >= WA) return;
     if constexpr (PREFETCH) {
         Chunk<N, TAU> qa, qb;

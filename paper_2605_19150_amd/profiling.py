@@ -133,6 +133,56 @@ def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, com
     return "\n".join(lines) + "\n"
 
 
+def _counter_means(d, kernel_substr):
+    """Mean per-dispatch value of every counter of the dispatches whose
+    kernel name contains kernel_substr: {counter: (mean, dispatches)}."""
+    vals = collections.defaultdict(lambda: collections.defaultdict(float))
+    for r in _rows(d, "*counter_collection.csv"):
+        if kernel_substr in r["Kernel_Name"]:
+            vals[r["Counter_Name"]][r["Dispatch_Id"]] += float(r["Counter_Value"])
+    return {k: (sum(v.values()) / len(v), len(v)) for k, v in vals.items()}
+
+
+# Counters the occupancy / LDS / VALU summaries explain.
+COUNTER_NOTES = {
+    "LDSBankConflict": "% of GPU time the LDS is stalled by bank conflicts (100 SQ_LDS_BANK_CONFLICT / GRBM_GUI_ACTIVE / CUs)",
+    "VALUBusy": "% of GPU time the vector ALUs process instructions (100 SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE)",
+    "OccupancyPercent": "waves resident as % of the maximum (400 SQ_WAVE_CYCLES / GRBM_GUI_ACTIVE / CUs / 32)",
+    "SQ_INSTS_LDS": "LDS instructions issued",
+    "SQ_INSTS_VALU": "VALU instructions issued",
+    "SQ_LDS_IDX_ACTIVE": "cycles the LDS serves indexed accesses",
+    "SQ_LDS_BANK_CONFLICT": "cycles the LDS is stalled by bank conflicts",
+    "SQ_WAVES": "waves launched",
+    "SQ_WAIT_INST_LDS": "wave-cycles (x4) waiting to issue an LDS instruction",
+    "SQ_ACTIVE_INST_LDS": "wave-cycles (x4) spent on LDS instructions",
+    "SQ_WAIT_ANY": "wave-cycles (x4) waiting for anything",
+    "SQ_ACTIVE_INST_ANY": "wave-cycles (x4) spent on any instruction",
+    "SQ_BUSY_CYCLES": "cycles with active waves in a shader engine",
+    "GRBM_GUI_ACTIVE": "GPU busy cycles",
+}
+
+
+def counters_markdown(kernel, workload, dirs, command, match=None, state_updates=None):
+    """Summary of counter runs (one directory per pass) of one kernel: mean
+    per dispatch of every counter, per state update for the instruction
+    counts when state_updates is given."""
+    match = match or kernel
+    rows = []
+    for d in dirs:
+        for name, (mean, n) in sorted(_counter_means(d, match).items()):
+            rows.append((name, mean, n))
+    out = ["# Occupancy, LDS and VALU counters: %s, workload %s" % (kernel, workload), "",
+           "kernel: %s" % kernel, "dispatches: %s" % match, "workload: %s" % workload,
+           "source-hash: %s" % source_hash(kernel), "",
+           "| counter | mean per dispatch | per state update | dispatches | meaning |", "|---|---|---|---|---|"]
+    for name, mean, n in rows:
+        per = ("%.2f" % (mean / state_updates)) if state_updates and name.startswith("SQ_INSTS") else ""
+        out.append("| %s | %.6g | %s | %d | %s |" % (name, mean, per, n, COUNTER_NOTES.get(name, "")))
+    out += ["", "Commands (from the repository root, one MI355X, one pass per run):", ""]
+    out += ["    " + c for c in command.split(" ;; ")]
+    return "\n".join(out) + "\n"
+
+
 def read_traffic_summary(profiles_dir, kernel, workload):
     """traffic-bytes-per-launch of the matching summary in profiles_dir, or
     None (no summary, or taken on other kernel sources)."""
@@ -162,10 +212,18 @@ def main(argv=None):
     for k in ("kernel", "workload", "fetch", "write", "copy_fetch", "copy_write", "command"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     t.add_argument("--match", default=None, help="substring of the dispatches' kernel name (default: --kernel)")
+    c = sub.add_parser("counters")
+    for k in ("kernel", "workload", "command"):
+        c.add_argument("--" + k, dest=k, required=True)
+    c.add_argument("--dirs", nargs="+", required=True)
+    c.add_argument("--match", default=None)
+    c.add_argument("--state-updates", dest="state_updates", type=float, default=None)
     sub.add_parser("hash")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         sys.stdout.write(stats_markdown(a.dir, a.title, a.command))
+    elif a.cmd == "counters":
+        sys.stdout.write(counters_markdown(a.kernel, a.workload, a.dirs, a.command, a.match, a.state_updates))
     elif a.cmd == "traffic":
         sys.stdout.write(traffic_markdown(a.kernel, a.workload, a.fetch, a.write, a.copy_fetch,
                                           a.copy_write, a.command, a.match))
