@@ -21,6 +21,7 @@ from .oracle import (  # noqa: F401
     oracle_surrogate_grads,
     oracle_dict_argmax,
     oracle_route,
+    oracle_project,
     oracle_num_chunks,
     oracle_lib_path,
 )

@@ -189,3 +189,38 @@ def oracle_route(u, S):
     S = np.asarray(S, np.float64)
     logits = np.einsum("bld,hkd->blhk", u, S)
     return logits, np.argmax(logits, axis=3).astype(np.int32)
+
+
+def oracle_project(u, S=None, Wb=None, Wc=None, Wd=None):
+    """The per-token projections of one layer, in float64 on the exact input
+    values (e.g. widened bf16).  u [B,L,Dm]; per-head weights [H,2N,Dm] whose
+    rows 2n and 2n+1 give the real and imaginary part of entry n:
+      - b[b,t,h,n] = sum_d u W_b[h,2n,d] + i sum_d u W_b[h,2n+1,d], the input
+        term b_t = B(u_t) u_t of the recurrence (App. E.2; Sec. 2.1 eq. (1));
+      - c[b,t,h,n] likewise from W_c, the readout vector C(u_t);
+      - D[b,t,h,n] = sigmoid(a) * exp(i theta), a = sum_d u W_d[h,2n,d],
+        theta = sum_d u W_d[h,2n+1,d]: the diagonal generator D(u_t) (App.
+        E.2.1 computes b and this generator as plain matrix products; the
+        paper leaves the nonlinearity open: a magnitude in (0, 1) and a free
+        phase);
+      - with S [H,K,Dm]: the routing logits and choices of oracle_route.
+    Returns a dict with the keys of the weights given (logits and idx for S)."""
+    u = np.asarray(u, np.float64)
+    out = {}
+    if S is not None:
+        out["logits"], out["idx"] = oracle_route(u, S)
+
+    def proj(W):
+        P = np.einsum("bld,hrd->blhr", u, np.asarray(W, np.float64))  # [B,L,H,2N]
+        return P[..., 0::2], P[..., 1::2]
+
+    if Wb is not None:
+        re, im = proj(Wb)
+        out["b"] = re + 1j * im
+    if Wc is not None:
+        re, im = proj(Wc)
+        out["c"] = re + 1j * im
+    if Wd is not None:
+        a, theta = proj(Wd)
+        out["D"] = (1.0 / (1.0 + np.exp(-a))) * np.exp(1j * theta)
+    return out
