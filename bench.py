@@ -243,10 +243,12 @@ def decode_bench(args, w, dev):
 
 
 def front_bench(args, w, dev):
-    """Selection front end for the workload's layer: the maps of a dense
-    dictionary [H,K,N,N] (pdssm_dict_argmax) and the routing of every token
-    with d_model = H*N (pdssm_route: bf16 product on the matrix cores, fp32
-    logits written, argmax fused)."""
+    """Selection front end and token projections for the workload's layer:
+    the maps of a dense dictionary [H,K,N,N] (pdssm_dict_argmax), the routing
+    of every token with d_model = H*N (pdssm_route: bf16 product on the
+    matrix cores, fp32 logits written, argmax fused), and the whole
+    projection (pdssm_project: routing, b, c and the diagonal generator in one
+    product, u read once)."""
     import torch
     from paper_2605_19150_amd import pdssm
 
@@ -254,28 +256,40 @@ def front_bench(args, w, dev):
     g = torch.Generator(device="cpu").manual_seed(0)
     u = torch.randn((w.B, w.L, Dm), generator=g).to(torch.bfloat16).to(dev)
     S = (torch.randn((w.H, w.K, Dm), generator=g) / Dm ** 0.5).to(torch.bfloat16).to(dev)
+    Wp = [(torch.randn((w.H, 2 * w.N, Dm), generator=g) / Dm ** 0.5).to(torch.bfloat16).to(dev) for _ in range(3)]
     M = torch.randn((w.H, w.K, w.N, w.N), generator=g).to(dev)
     lg = torch.empty((w.B, w.L, w.H, w.K), dtype=torch.float32, device=dev)
     idx = torch.empty((w.B, w.L, w.H), dtype=torch.int32, device=dev)
     pi = torch.empty((w.H, w.K, w.N), dtype=torch.int32, device=dev)
+    outs = [torch.empty((w.B, w.L, w.H, w.N), dtype=torch.complex64, device=dev) for _ in range(3)]
     L = pdssm.load()
     st = pdssm._stream(None)
     flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    P = pdssm._p
 
     def step(ev=None):
         if ev is not None:
             ev[0].record()
-        assert L.pdssm_dict_argmax(w.H, w.K, w.N, pdssm._p(M), pdssm._p(pi), st) == pdssm.OK
+        assert L.pdssm_dict_argmax(w.H, w.K, w.N, P(M), P(pi), st) == pdssm.OK
         if ev is not None:
             ev[1].record()
-        assert L.pdssm_route(T, Dm, w.H, w.K, pdssm._p(u), pdssm._p(S), pdssm._p(lg), pdssm._p(idx), st) == pdssm.OK
+        assert L.pdssm_route(T, Dm, w.H, w.K, P(u), P(S), P(lg), P(idx), st) == pdssm.OK
         if ev is not None:
             ev[2].record()
+        assert L.pdssm_project(T, Dm, w.H, w.K, w.N, P(u), P(S), P(Wp[0]), P(Wp[1]), P(Wp[2]), P(lg), P(idx),
+                               P(outs[0]), P(outs[1]), P(outs[2]), st) == pdssm.OK
+        if ev is not None:
+            ev[3].record()
 
+    t_settle = time.perf_counter()
+    while time.perf_counter() - t_settle < SETTLE_S:
+        flush.fill_(1.0)
+        step()
+        torch.cuda.synchronize()
     for _ in range(args.warmup):
         flush.fill_(1.0)
         step()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     for i in range(args.steps):
         flush.fill_(float(i))
@@ -283,18 +297,29 @@ def front_bench(args, w, dev):
     torch.cuda.synchronize()
     am_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     rt_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    pj_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
     rt_bytes = T * Dm * 2 + w.H * w.K * Dm * 2 + T * w.H * w.K * 4 + T * w.H * 4
     rt_flops = 2.0 * T * w.H * w.K * Dm
+    cols = w.H * w.K + 3 * 2 * w.H * w.N
+    pj_flops = 2.0 * T * cols * Dm
+    pj_bytes = T * Dm * 2 + cols * Dm * 2 + T * w.H * w.K * 4 + T * w.H * 4 + 3 * T * w.H * w.N * 8
     am_bytes = w.H * w.K * w.N * w.N * 4 + w.H * w.K * w.N * 4
+    tf = pj_flops / (pj_ms * 1e-3) / 1e12
     print(json.dumps({
-        "metric": "PD-SSM routing tokens/s (routing product + argmax over the K maps of every head)",
-        "value": T / (rt_ms * 1e-3), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": am_ms + rt_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "metric": "PD-SSM layer projections TFLOP/s (routing, b, c and the diagonal generator in one product)",
+        "value": tf, "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": am_ms + rt_ms + pj_ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16 operands, f32 accumulation", "data": "synthetic (seeded)",
-        "config": {"workload": w.name + " front end", "tokens": T, "d_model": Dm, "H": w.H, "K": w.K, "N": w.N,
-                   "step": "dict_argmax+route", "parallelism": "single-gpu"},
-        "route": {"kernel": "k_route", "ms": rt_ms, "alg_bytes": rt_bytes, "alg_GBps": rt_bytes / (rt_ms * 1e-3) / 1e9,
-                  "flops": rt_flops, "TFLOPs": rt_flops / (rt_ms * 1e-3) / 1e12,
+        "config": {"workload": w.name + " layer front end", "tokens": T, "d_model": Dm, "H": w.H, "K": w.K,
+                   "N": w.N, "step": "dict_argmax+route+project", "parallelism": "single-gpu"},
+        "roofline": {"bound": "mfma", "kernel": "k_project_dma", "achieved": tf, "peak": 2500.0,
+                     "unit": "TFLOP/s", "frac": tf / 2500.0, "traffic": None},
+        "project": {"kernel": "k_project_dma", "ms": pj_ms, "flops": pj_flops, "TFLOPs": tf,
+                    "frac_mfma_bf16": tf / 2500.0, "alg_bytes": pj_bytes,
+                    "alg_GBps": pj_bytes / (pj_ms * 1e-3) / 1e9, "columns": cols},
+        "route": {"kernel": "k_project_dma (routing tiles only)", "ms": rt_ms, "alg_bytes": rt_bytes,
+                  "alg_GBps": rt_bytes / (rt_ms * 1e-3) / 1e9, "flops": rt_flops,
+                  "TFLOPs": rt_flops / (rt_ms * 1e-3) / 1e12,
                   "frac_mfma_bf16": rt_flops / (rt_ms * 1e-3) / 1e12 / 2500.0},
         "dict_argmax": {"kernel": "k_dict_argmax", "ms": am_ms, "alg_bytes": am_bytes,
                         "alg_GBps": am_bytes / (am_ms * 1e-3) / 1e9},

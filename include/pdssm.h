@@ -309,6 +309,32 @@ int pdssm_route(int32_t T, int32_t Dm, int32_t H, int32_t K, const uint16_t* u, 
                 float* logits, int32_t* idx, void* stream);
 
 /*
+ * pdssm_project: everything a layer derives from its tokens u_t in one
+ * product on the matrix cores (bf16 operands, fp32 accumulation), u read from
+ * memory once:
+ *   - the routing of pdssm_route (S non-NULL: logits optional, idx required);
+ *   - b[t,h,n] = P_b[t,h,2n] + i P_b[t,h,2n+1], the input term b_t = B(u_t)
+ *     u_t of the recurrence (App. E.2; Sec. 2.1 eq. (1)), and likewise
+ *     c[t,h,n] from P_c, the readout vector C(u_t);
+ *   - D[t,h,n] = sigmoid(P_d[t,h,2n]) * exp(i P_d[t,h,2n+1]), the diagonal
+ *     generator D(u_t) (App. E.2.1 computes b and this generator as plain
+ *     matrix products; the paper leaves its nonlinearity open: this one keeps
+ *     |D| < 1 with a free phase),
+ * where P_x[t,h,r] = sum_d u[t,d] W_x[h,r,d].  u [T,Dm] bf16; W_b, W_c, W_d
+ * [H,2N,Dm] bf16 (rows 2n and 2n+1 of a head: real and imaginary part, or
+ * magnitude logit and phase, of entry n); b, c, D [T,H,N] complex64 = the
+ * scans' [B,L,H,N] layout with T = B*L.  Each of W_b, W_c, W_d and its
+ * output is given or NULL together; at least one of S, W_b, W_c, W_d.
+ * Dm a multiple of 32; N in {8,...,256}; K <= 256; u, S, W and the complex
+ * outputs 16-byte aligned, logits and idx 4-byte aligned; row offsets of
+ * (T + 256) rows of u and (H*2N + 256) rows of W below 2^32 bytes
+ * (else PDSSM_ERR_UNSUPPORTED).  Needs no workspace.
+ */
+int pdssm_project(int32_t T, int32_t Dm, int32_t H, int32_t K, int32_t N, const uint16_t* u,
+                  const uint16_t* S, const uint16_t* Wb, const uint16_t* Wc, const uint16_t* Wd, float* logits,
+                  int32_t* idx, pdssm_c64* b, pdssm_c64* c, pdssm_c64* D, void* stream);
+
+/*
  * Vector-Jacobian product of the tempered softmax that stands in for a hard
  * argmax in the backward pass (Sec. 3.1, slope-annealed straight-through
  * estimation; Prop. 2): along the middle axis of x [outer, len, inner]

@@ -636,6 +636,53 @@ int pdssm_route(int32_t T, int32_t Dm, int32_t H, int32_t K, const uint16_t* u, 
     return pdssm::launch_route(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }
 
+int pdssm_project(int32_t T, int32_t Dm, int32_t H, int32_t K, int32_t N, const uint16_t* u,
+                  const uint16_t* S, const uint16_t* Wb, const uint16_t* Wc, const uint16_t* Wd, float* logits,
+                  int32_t* idx, pdssm_c64* b, pdssm_c64* c, pdssm_c64* D, void* stream) {
+    if (T < 1 || Dm < 1 || H < 1 || !u) return PDSSM_ERR_INVALID_ARG;
+    if ((!Wb) != (!b) || (!Wc) != (!c) || (!Wd) != (!D)) return PDSSM_ERR_INVALID_ARG;
+    if (!S && !Wb && !Wc && !Wd) return PDSSM_ERR_INVALID_ARG;
+    if (S && (K < 1 || !idx)) return PDSSM_ERR_INVALID_ARG;
+    if ((logits || idx) && !S) return PDSSM_ERR_INVALID_ARG;
+    const bool proj = Wb || Wc || Wd;
+    if (proj && !n_supported(N)) return PDSSM_ERR_UNSUPPORTED;
+    if ((S && K > 256) || Dm % 32 != 0) return PDSSM_ERR_UNSUPPORTED;
+    const long long rows = (S ? (long long)H * K : 0) > (proj ? 2LL * H * N : 0) ? (long long)H * K : 2LL * H * N;
+    if ((long long)(T + 256) * Dm * 2 >= (1LL << 32) || (rows + 256) * Dm * 2 >= (1LL << 32) ||
+        (long long)T * H * (S ? K : 1) >= (1LL << 31) || (proj && 2LL * T * H * N >= (1LL << 31)))
+        return PDSSM_ERR_UNSUPPORTED;
+    for (const void* p : {(const void*)u, (const void*)S, (const void*)Wb, (const void*)Wc, (const void*)Wd,
+                          (const void*)b, (const void*)c, (const void*)D})
+        if (misaligned(p)) return PDSSM_ERR_INVALID_ARG;
+    if (misaligned4(logits) || misaligned4(idx)) return PDSSM_ERR_INVALID_ARG;
+    const size_t nu = (size_t)T * Dm * 2, nS = S ? (size_t)H * K * Dm * 2 : 0, nW = (size_t)H * 2 * N * Dm * 2;
+    const size_t nout = (size_t)T * H * N * 8;
+    if (any_overlap({{logits, S ? (size_t)T * H * K * 4 : 0}, {idx, S ? (size_t)T * H * 4 : 0}, {b, nout},
+                     {c, nout}, {D, nout}},
+                    {{u, nu}, {S, nS}, {Wb, nW}, {Wc, nW}, {Wd, nW}}))
+        return PDSSM_ERR_INVALID_ARG;
+    pdssm::ProjectArgs a = {};
+    a.T = T;
+    a.Dm = Dm;
+    a.H = H;
+    a.K = S ? K : 1;
+    a.N = proj ? N : 8;
+    a.u = u;
+    a.S = S;
+    a.logits = logits;
+    a.idx = idx;
+    const uint16_t* W[3] = {Wb, Wc, Wd};
+    pdssm_c64* out[3] = {b, c, D};
+    for (int i = 0; i < 3; ++i)
+        if (W[i]) {
+            a.W[a.nproj] = W[i];
+            a.out[a.nproj] = reinterpret_cast<float*>(out[i]);
+            a.kind[a.nproj] = i == 2 ? pdssm::kProjGen : pdssm::kProjPlain;
+            ++a.nproj;
+        }
+    return pdssm::launch_project(a, static_cast<hipStream_t>(stream)) == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
+}
+
 int pdssm_softmax_vjp(const float* x, const float* gy, float* gx, int64_t outer, int32_t len, int64_t inner,
                       float temp, void* stream) {
     if (!x || !gy || !gx || outer < 0 || len < 1 || inner < 1) return PDSSM_ERR_INVALID_ARG;

@@ -167,8 +167,10 @@ __global__ __launch_bounds__(256) void k_route(RouteArgs a) {
     }
 }
 
-// ------------------------------------------------------------------ k_route_dma
-// The routing product for contraction sizes that are a multiple of 32, with
+// ------------------------------------------------------------------ k_project_dma
+// The routing product -- and the token projections b, c and the diagonal
+// generator, as further column tiles of the same product -- for contraction
+// sizes that are a multiple of 32, with
 // direct buffer-to-LDS loads (buffer_load_dwordx4 ... lds: every lane of a
 // wave moves 16 bytes to LDS at a wave-uniform base + 16 * lane), so that
 // several slices are in flight without holding them in registers.  Rows past
@@ -233,8 +235,55 @@ __device__ __forceinline__ void barrier_no_fence() {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// Column tiles of the product: first the routing tiles (whole heads of K
+// columns, 256 / K heads each), then for each projection its rows of
+// H*2N in tiles of 256.  All scalar.
+struct ColTile {
+    int kind;   // -1: routing; else the projection's index
+    int r0;     // first weight row of the tile
+    int ncol;   // valid columns
+    int h0, nh; // routing: first head, heads
+};
+
+__device__ __forceinline__ ColTile col_tile(const ProjectArgs& a, int nt, int BN) {
+    ColTile c;
+    const int hpb = a.S ? BN / a.K : 1;
+    const int NTr = a.S ? (a.H + hpb - 1) / hpb : 0;
+    if (nt < NTr) {
+        c.kind = -1;
+        c.h0 = nt * hpb;
+        c.nh = min(hpb, a.H - c.h0);
+        c.r0 = c.h0 * a.K;
+        c.ncol = c.nh * a.K;
+    } else {
+        const int R = 2 * a.H * a.N, NTp = (R + BN - 1) / BN;
+        const int j = nt - NTr;
+        c.kind = j / NTp;
+        c.r0 = (j - c.kind * NTp) * BN;
+        c.ncol = min(BN, R - c.r0);
+        c.h0 = c.nh = 0;
+    }
+    return c;
+}
+
+__device__ __forceinline__ int col_tiles(const ProjectArgs& a, int BN) {
+    const int hpb = a.S ? BN / a.K : 1;
+    const int NTr = a.S ? (a.H + hpb - 1) / hpb : 0;
+    const int R = 2 * a.H * a.N;
+    return NTr + a.nproj * ((R + BN - 1) / BN);
+}
+
+// D = sigmoid(m) exp(i p): the diagonal generator of one entry from its two
+// projected values (magnitude logit m, phase p).
+__device__ __forceinline__ float2 diag_gen(float m, float p) {
+    const float r = 1.f / (1.f + expf(-m));
+    float s, c;
+    sincosf(p, &s, &c);
+    return make_float2(r * c, r * s);
+}
+
 template <int BM>
-__global__ __launch_bounds__(512) void k_route_dma(RouteArgs a) {
+__global__ __launch_bounds__(512) void k_project_dma(ProjectArgs a) {
     using C = RouteDma<BM>;
     constexpr int NT_ = C::NW * 64;
     extern __shared__ __align__(16) unsigned char lds[];
@@ -242,28 +291,28 @@ __global__ __launch_bounds__(512) void k_route_dma(RouteArgs a) {
     // descriptor depend on it
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
     const int wm = wv / C::WGN, wn = wv % C::WGN;
-    const int hpb = C::BN / a.K;  // heads per column tile
-    const int NT = (a.H + hpb - 1) / hpb, MT = (a.T + BM - 1) / BM;
+    const int NT = col_tiles(a, C::BN), MT = (a.T + BM - 1) / BM;
     const int total = NT * MT;
     int t = blockIdx.x;
     if (total % 8 == 0) t = (t % 8) * (total / 8) + t / 8;
     const int nt = t % NT, mt = t / NT;
-    const int h0 = nt * hpb;
-    const int nh = min(hpb, a.H - h0);
-    const int ncol = nh * a.K;
+    const ColTile ct = col_tile(a, nt, C::BN);
+    const int ncol = ct.ncol;
     const int m0 = mt * BM;
     const int HK = a.H * a.K;
+    const int R = 2 * a.H * a.N;
 
     // this lane's byte offset of each of its load instructions: row
     // (wv * PER_WAVE + i) * 16 + lane % 16 of the stage, chunk lane / 16
     const uint32_t row_bytes = (uint32_t)a.Dm * 2;
     const __amdgpu_buffer_rsrc_t ru = row_block(a.u, (uint32_t)a.T * row_bytes);
-    const __amdgpu_buffer_rsrc_t rs = row_block(a.S, (uint32_t)HK * row_bytes);
+    const __amdgpu_buffer_rsrc_t rs =
+        ct.kind < 0 ? row_block(a.S, (uint32_t)HK * row_bytes) : row_block(a.W[ct.kind], (uint32_t)R * row_bytes);
     uint32_t voff[C::PER_WAVE];
 #pragma unroll
     for (int i = 0; i < C::PER_WAVE; ++i) {
         const int row = (wv * C::PER_WAVE + i) * 16 + (lane & 15);
-        const uint32_t r = row < BM ? (uint32_t)(m0 + row) : (uint32_t)(h0 * a.K + row - BM);
+        const uint32_t r = row < BM ? (uint32_t)(m0 + row) : (uint32_t)(ct.r0 + row - BM);
         voff[i] = r * row_bytes + 16u * (uint32_t)(lane >> 4);
     }
     auto issue = [&](int s) {
@@ -347,7 +396,24 @@ __global__ __launch_bounds__(512) void k_route_dma(RouteArgs a) {
         __syncthreads();
         const int mb = m0 + half * HALF;
         const int nm = max(0, min(HALF, a.T - mb));
-        float* lrow = a.logits ? a.logits + (size_t)mb * HK + (size_t)h0 * a.K : nullptr;  // row mb, first column
+        if (ct.kind >= 0) {
+            // a projection: rows of [T, H*2N] floats; R, r0 and ncol are
+            // multiples of 4 (2N >= 16), so every row piece is 16-byte aligned
+            float* orow = a.out[ct.kind] + (size_t)mb * R + ct.r0;
+            const int nq = ncol / 4;
+            const bool gen = a.kind[ct.kind] == kProjGen;
+            for (int e = threadIdx.x; e < nm * nq; e += NT_) {
+                const int m = e / nq, q = e - m * nq;
+                float4 v = *reinterpret_cast<const float4*>(tile + m * C::PITCH + 4 * q);
+                if (gen) {
+                    const float2 d0 = diag_gen(v.x, v.y), d1 = diag_gen(v.z, v.w);
+                    v = make_float4(d0.x, d0.y, d1.x, d1.y);
+                }
+                *reinterpret_cast<float4*>(orow + (size_t)m * R + 4 * q) = v;
+            }
+            continue;
+        }
+        float* lrow = a.logits ? a.logits + (size_t)mb * HK + (size_t)ct.h0 * a.K : nullptr;  // row mb, first column
         if (vec) {
             const int nq = ncol / 4;
             if (lrow)
@@ -364,7 +430,7 @@ __global__ __launch_bounds__(512) void k_route_dma(RouteArgs a) {
         }
         // first maximal index per (token, head); neighbouring lanes take
         // neighbouring tokens
-        for (int e = threadIdx.x; e < HALF * nh; e += NT_) {
+        for (int e = threadIdx.x; e < HALF * ct.nh; e += NT_) {
             const int m = e % HALF, hh = e / HALF;
             if (m >= nm) continue;
             const float* v = tile + m * C::PITCH + hh * a.K;
@@ -382,21 +448,30 @@ __global__ __launch_bounds__(512) void k_route_dma(RouteArgs a) {
                 for (int k = 1; k < a.K; ++k)
                     if (v[k] > bv) bv = v[k], best = k;
             }
-            a.idx[(size_t)(mb + m) * a.H + h0 + hh] = best;
+            a.idx[(size_t)(mb + m) * a.H + ct.h0 + hh] = best;
         }
     }
 }
 
 template <int BM>
-hipError_t route_dma_launch(const RouteArgs& a, hipStream_t st) {
+hipError_t project_dma_launch(const ProjectArgs& a, hipStream_t st) {
     using C = RouteDma<BM>;
-    const int hpb = C::BN / a.K;
-    const int NT = (a.H + hpb - 1) / hpb, MT = (a.T + BM - 1) / BM;
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_route_dma<BM>),
+    const int hpb = a.S ? C::BN / a.K : 1;
+    const int NT = (a.S ? (a.H + hpb - 1) / hpb : 0) + a.nproj * ((2 * a.H * a.N + C::BN - 1) / C::BN);
+    const int MT = (a.T + BM - 1) / BM;
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(k_project_dma<BM>),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)C::LDS);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_route_dma<BM>, dim3((unsigned)(NT * MT)), dim3(C::NW * 64), C::LDS, st, a);
+    hipLaunchKernelGGL(k_project_dma<BM>, dim3((unsigned)(NT * MT)), dim3(C::NW * 64), C::LDS, st, a);
     return hipGetLastError();
+}
+
+// 256-token tiles when they still give every CU two of them
+hipError_t project_dma(const ProjectArgs& a, hipStream_t st) {
+    const int hpb = a.S ? 256 / a.K : 1;
+    const long long NT = (a.S ? (a.H + hpb - 1) / hpb : 0) + (long long)a.nproj * ((2LL * a.H * a.N + 255) / 256);
+    const long long tiles256 = (long long)((a.T + 255) / 256) * NT;
+    return tiles256 >= 512 ? project_dma_launch<256>(a, st) : project_dma_launch<128>(a, st);
 }
 
 // pi[h,k,j] = argmax_i M[h,k,i,j].  A workgroup takes 64 columns of one
@@ -436,15 +511,25 @@ __global__ __launch_bounds__(256) void k_dict_argmax(const float* __restrict__ M
 
 }  // namespace
 
+// byte offsets of the direct-load kernel are 32-bit, rows past the end included
+bool project_fits(long long T, long long rows, long long Dm) {
+    return (T + 256) * Dm * 2 < (1LL << 32) && (rows + 256) * Dm * 2 < (1LL << 32);
+}
+
 hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
-    // byte offsets of the direct-load kernel are 32-bit, rows past the end included
-    const bool fits = (long long)(a.T + 256) * a.Dm * 2 < (1LL << 32) &&
-                      (long long)(a.H * a.K + 256) * a.Dm * 2 < (1LL << 32);
-    if (a.Dm % RouteDma<128>::BK == 0 && fits) {
-        // 256-token tiles when they still give every CU two of them
-        const int NT = (a.H + 256 / a.K - 1) / (256 / a.K);
-        const long long tiles256 = (long long)((a.T + 255) / 256) * NT;
-        return tiles256 >= 512 ? route_dma_launch<256>(a, st) : route_dma_launch<128>(a, st);
+    if (a.Dm % RouteDma<128>::BK == 0 && project_fits(a.T, (long long)a.H * a.K, a.Dm)) {
+        ProjectArgs p = {};
+        p.T = a.T;
+        p.Dm = a.Dm;
+        p.H = a.H;
+        p.K = a.K;
+        p.N = 8;
+        p.u = a.u;
+        p.S = a.S;
+        p.logits = a.logits;
+        p.idx = a.idx;
+        p.nproj = 0;
+        return project_dma(p, st);
     }
     const int hpb = kRouteTN / a.K;
     dim3 grid((a.T + kRouteTM - 1) / kRouteTM, (a.H + hpb - 1) / hpb);
@@ -453,6 +538,13 @@ hipError_t launch_route(const RouteArgs& a, hipStream_t st) {
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_route, grid, dim3(256), kRouteLds, st, a);
     return hipGetLastError();
+}
+
+hipError_t launch_project(const ProjectArgs& a, hipStream_t st) {
+    const long long rows = a.S ? (long long)a.H * a.K : 0;
+    if (a.Dm % RouteDma<128>::BK != 0 || !project_fits(a.T, rows > 2LL * a.H * a.N ? rows : 2LL * a.H * a.N, a.Dm))
+        return hipErrorInvalidValue;
+    return project_dma(a, st);
 }
 
 hipError_t launch_dict_argmax(const float* M, int* pi, int HK, int N, hipStream_t st) {

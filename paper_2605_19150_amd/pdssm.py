@@ -48,7 +48,7 @@ class Desc(ctypes.Structure):
 EXPORTS = ("pdssm_abi_version", "pdssm_chunk_len", "pdssm_num_chunks", "pdssm_workspace_size",
            "pdssm_uses_fused", "pdssm_scan_segments", "pdssm_status_string", "pdssm_prepare", "pdssm_scan_fwd", "pdssm_scan_fwd_noalloc",
            "pdssm_scan_bwd", "pdssm_compose_chunks", "pdssm_scan_bwd_ste", "pdssm_ste_grads",
-           "pdssm_softmax_vjp", "pdssm_decode_step", "pdssm_dict_argmax", "pdssm_route")
+           "pdssm_softmax_vjp", "pdssm_decode_step", "pdssm_dict_argmax", "pdssm_route", "pdssm_project")
 
 
 def lib_path():
@@ -95,6 +95,8 @@ def load():
     L.pdssm_dict_argmax.restype = I
     L.pdssm_route.argtypes = [I32, I32, I32, I32, P, P, P, P, P]
     L.pdssm_route.restype = I
+    L.pdssm_project.argtypes = [I32] * 5 + [P] * 10 + [P]
+    L.pdssm_project.restype = I
     if L.pdssm_abi_version() != 1:
         raise ImportError("libpdssm.so ABI version mismatch")
     _lib = L
@@ -542,3 +544,40 @@ def route(u, S, logits=True, stream=None):
     if st != OK:
         raise PdssmError(st, "pdssm_route")
     return lg, idx
+
+
+def project(u, S=None, Wb=None, Wc=None, Wd=None, logits=True, N=None, stream=None):
+    """pdssm_project: the token projections of a layer in one product.
+    u [B,L,Dm] bf16; S [H,K,Dm] bf16 (routing); Wb, Wc, Wd [H,2N,Dm] bf16
+    (b, c and the diagonal generator).  Returns a dict with logits [B,L,H,K]
+    f32 and idx [B,L,H] int32 (with S), and b, c, D [B,L,H,N] complex64 (each
+    with its weights)."""
+    B, L, Dm = u.shape
+    dev = u.device
+    _need(u, "u", torch.bfloat16, (B, L, Dm), dev)
+    Ws = [w for w in (Wb, Wc, Wd) if w is not None]
+    if S is None and not Ws:
+        raise ValueError("project: nothing to compute")
+    H = S.shape[0] if S is not None else Ws[0].shape[0]
+    K = S.shape[1] if S is not None else 1
+    if Ws:
+        N = Ws[0].shape[1] // 2
+    N = N or 8
+    if S is not None:
+        _need(S, "S", torch.bfloat16, (H, K, Dm), dev)
+    for w, n in ((Wb, "Wb"), (Wc, "Wc"), (Wd, "Wd")):
+        if w is not None:
+            _need(w, n, torch.bfloat16, (H, 2 * N, Dm), dev)
+    out = {}
+    if S is not None:
+        out["logits"] = torch.empty((B, L, H, K), dtype=torch.float32, device=dev) if logits else None
+        out["idx"] = torch.empty((B, L, H), dtype=torch.int32, device=dev)
+    for w, n in ((Wb, "b"), (Wc, "c"), (Wd, "D")):
+        if w is not None:
+            out[n] = torch.empty((B, L, H, N), dtype=torch.complex64, device=dev)
+    st = load().pdssm_project(B * L, Dm, H, K, N, _p(u), _p(S), _p(Wb), _p(Wc), _p(Wd), _p(out.get("logits")),
+                              _p(out.get("idx")), _p(out.get("b")), _p(out.get("c")), _p(out.get("D")),
+                              _stream(stream))
+    if st != OK:
+        raise PdssmError(st, "pdssm_project")
+    return out

@@ -330,3 +330,29 @@ def test_select_host_checks(lib):
     assert lib.pdssm_route(100, 64, 8, 4, u, S, lg, None, None) == pdssm.ERR_INVALID_ARG
     assert lib.pdssm_route(100, 64, 8, 4, u, S, u, idx, None) == pdssm.ERR_INVALID_ARG    # logits over u
     assert lib.pdssm_route(100, 64, 8, 4, ctypes.c_void_p(u.value + 2), S, lg, idx, None) == pdssm.ERR_INVALID_ARG
+
+
+def test_project_host_checks(lib):
+    f = FakeBufs()
+    T, Dm, H, K, N = 100, 64, 4, 8, 16
+    u, S = f(T * Dm * 2), f(H * K * Dm * 2)
+    Wb, Wc, Wd = f(H * 2 * N * Dm * 2), f(H * 2 * N * Dm * 2), f(H * 2 * N * Dm * 2)
+    lg, idx = f(T * H * K * 4), f(T * H * 4)
+    b, c, D = f(T * H * N * 8), f(T * H * N * 8), f(T * H * N * 8)
+    call = lambda *a: lib.pdssm_project(*a, None)  # noqa: E731
+    # nothing asked for; routing without idx; logits without S; weights without output and back
+    assert call(T, Dm, H, K, N, u, None, None, None, None, None, None, None, None, None) == pdssm.ERR_INVALID_ARG
+    assert call(T, Dm, H, K, N, u, S, None, None, None, lg, None, None, None, None) == pdssm.ERR_INVALID_ARG
+    assert call(T, Dm, H, K, N, u, None, Wb, None, None, lg, None, b, None, None) == pdssm.ERR_INVALID_ARG
+    assert call(T, Dm, H, K, N, u, None, Wb, None, None, None, None, None, None, None) == pdssm.ERR_INVALID_ARG
+    assert call(T, Dm, H, K, N, u, None, None, None, None, None, None, None, None, D) == pdssm.ERR_INVALID_ARG
+    # sizes: contraction not a multiple of 32, N and K outside the supported set
+    assert call(T, 48, H, K, N, u, S, Wb, Wc, Wd, lg, idx, b, c, D) == pdssm.ERR_UNSUPPORTED
+    assert call(T, Dm, H, K, 48, u, S, Wb, Wc, Wd, lg, idx, b, c, D) == pdssm.ERR_UNSUPPORTED
+    assert call(T, Dm, H, 257, N, u, S, Wb, Wc, Wd, lg, idx, b, c, D) == pdssm.ERR_UNSUPPORTED
+    assert call(0, Dm, H, K, N, u, S, Wb, Wc, Wd, lg, idx, b, c, D) == pdssm.ERR_INVALID_ARG
+    # alignment and overlap
+    assert call(T, Dm, H, K, N, u, S, Wb, Wc, Wd, lg, idx, ctypes.c_void_p(b.value + 8), c, D) == pdssm.ERR_INVALID_ARG
+    assert call(T, Dm, H, K, N, u, S, Wb, Wc, Wd, lg, ctypes.c_void_p(idx.value + 2), b, c, D) == pdssm.ERR_INVALID_ARG
+    assert call(T, Dm, H, K, N, u, S, Wb, Wc, Wd, lg, idx, b, b, D) == pdssm.ERR_INVALID_ARG        # c over b
+    assert call(T, Dm, H, K, N, u, S, Wb, Wc, Wd, lg, idx, b, c, Wd) == pdssm.ERR_INVALID_ARG       # D over its weights

@@ -1,5 +1,11 @@
 """GPU parity of the selection front end against the float64 oracle.
 
+project: b and c to the same sum-scaled bar as the logits (S = sum_d |u_d W_d|
+of each projected value); the diagonal generator D = sigmoid(a) exp(i theta)
+inherits the bars of a and theta through |d sigmoid| <= 1/4 and
+|exp(i x) - 1| <= |x|: |gpu - ref| <= tol_a / 4 + tol_theta + 1e-6 per
+component (the last term for the fp32 exponential and sine/cosine).
+
 dict_argmax: bit for bit (no arithmetic; ties to the first maximal index).
 route: logits within |gpu - ref| <= 1e-5 + 1e-4*S, S = sum_d |u_d S_d| (an
 fp32 sum of Dm bf16 products, see helpers.assert_close_sum); idx is exactly
@@ -11,7 +17,7 @@ import numpy as np
 import pytest
 
 from helpers import assert_close_sum
-from oracle import oracle_dict_argmax, oracle_route
+from oracle import oracle_dict_argmax, oracle_project, oracle_route
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -106,3 +112,83 @@ def test_route_hybrid_full_size_sampled():
     clear = (top2[..., 1] - top2[..., 0]) > 2 * tol
     np.testing.assert_array_equal(ix[clear], ri[clear])
     assert clear.mean() > 0.9
+
+
+def _check_project(u, S, W, got, rows=None):
+    """got: pdssm.project's outputs (rows: the token rows of u they cover)."""
+    Wb, Wc, Wd = W
+    ref = oracle_project(u, S, Wb, Wc, Wd)
+    au = np.abs(u)
+    for name, w in (("b", Wb), ("c", Wc)):
+        if w is None:
+            continue
+        sc = np.einsum("bld,hrd->blhr", au, np.abs(w))
+        g = got[name]
+        assert_close_sum(name + ".re", g.real, ref[name].real, sc[..., 0::2])
+        assert_close_sum(name + ".im", g.imag, ref[name].imag, sc[..., 1::2])
+    if Wd is not None:
+        sc = np.einsum("bld,hrd->blhr", au, np.abs(Wd))
+        tol = (1e-5 + 1e-4 * sc[..., 0::2]) / 4 + (1e-5 + 1e-4 * sc[..., 1::2]) + 1e-6
+        g, r = got["D"], ref["D"]
+        for part, gp, rp in (("re", g.real, r.real), ("im", g.imag, r.imag)):
+            err = np.abs(gp.astype(np.float64) - rp)
+            bad = err > tol
+            assert not bad.any(), "D.%s: %d out of tolerance, worst %g (tol %g)" % (
+                part, bad.sum(), err.max(), tol[np.unravel_index(np.argmax(err - tol), err.shape)])
+        assert (np.abs(g) < 1 + 1e-6).all()
+    if S is not None:
+        lg, ix = got["logits"], got["idx"]
+        scale = np.einsum("bld,hkd->blhk", au, np.abs(S))
+        assert_close_sum("logits", lg, ref["logits"], scale)
+        np.testing.assert_array_equal(ix, np.argmax(lg, axis=3))
+
+
+def _proj_case(B, L, H, K, N, Dm, seed, kinds="Sbcd"):
+    rng = np.random.default_rng(seed)
+    ut, u = _bf16(rng.standard_normal((B, L, Dm)))
+    S = W = None
+    St, S = _bf16(rng.standard_normal((H, K, Dm)) / np.sqrt(Dm)) if "S" in kinds else (None, None)
+    Ws, Wt = [], []
+    for kch, scale in (("b", 1.0), ("c", 1.0), ("d", 2.0)):
+        if kch in kinds:
+            t, w = _bf16(rng.standard_normal((H, 2 * N, Dm)) * scale / np.sqrt(Dm))
+            Wt.append(t.to(DEV))
+            Ws.append(w)
+        else:
+            Wt.append(None)
+            Ws.append(None)
+    out = pdssm.project(ut.to(DEV), St.to(DEV) if St is not None else None, *Wt, N=N)
+    got = {k: v.cpu().numpy() for k, v in out.items() if v is not None}
+    _check_project(u, S, Ws, got)
+
+
+@pytest.mark.parametrize("B,L,H,K,N,Dm,kinds", [
+    (2, 100, 16, 16, 64, 1024, "Sbcd"),   # a fsa-perm-like layer
+    (1, 70, 3, 5, 8, 64, "Sbcd"),         # ragged tokens, a partial column tile (H*2N = 48), K % 4 != 0
+    (1, 300, 2, 7, 256, 96, "Sbcd"),      # N = 256: four column tiles per projection, three slices
+    (3, 50, 5, 1, 32, 32, "bcd"),         # no routing; H*2N = 320: one whole and one partial tile
+    (8, 2048, 4, 16, 128, 64, "Sbcd"),    # 256-token tiles
+    (2, 77, 6, 9, 16, 128, "b"),          # one projection alone
+    (2, 77, 6, 9, 16, 128, "d"),
+    (2, 77, 6, 9, 16, 128, "Sc"),
+])
+def test_project(B, L, H, K, N, Dm, kinds):
+    print("project B=%d L=%d H=%d K=%d N=%d Dm=%d %s" % (B, L, H, K, N, Dm, kinds), flush=True)
+    _proj_case(B, L, H, K, N, Dm, seed=B * L + H + K + N + Dm, kinds=kinds)
+
+
+@pytest.mark.parametrize("B,L,H,K,N,Dm", [(16, 2048, 16, 16, 64, 1024), (8, 4096, 32, 64, 128, 4096)])
+def test_project_layer_full_size_sampled(B, L, H, K, N, Dm):
+    """The layers of fsa-perm (d = 1024, 16 heads of 64) and hybrid-lm (d =
+    4096, 32 heads of 128) at full size; routing, b, c and D of sampled
+    tokens against the oracle."""
+    print("project layer B=%d L=%d H=%d K=%d N=%d Dm=%d" % (B, L, H, K, N, Dm), flush=True)
+    g = torch.Generator(device="cpu").manual_seed(B + Dm)
+    ut = torch.randn((B, L, Dm), generator=g).to(torch.bfloat16)
+    St = (torch.randn((H, K, Dm), generator=g) / Dm ** 0.5).to(torch.bfloat16)
+    Wt = [(torch.randn((H, 2 * N, Dm), generator=g) * s / Dm ** 0.5).to(torch.bfloat16) for s in (1.0, 1.0, 2.0)]
+    out = pdssm.project(ut.to(DEV), St.to(DEV), *[w.to(DEV) for w in Wt])
+    rows = np.sort(np.random.default_rng(1).choice(B * L, size=64, replace=False))
+    u = ut.reshape(B * L, Dm)[rows].to(torch.float64).numpy()[None]
+    got = {k: v.reshape((B * L,) + v.shape[2:])[rows].cpu().numpy()[None] for k, v in out.items()}
+    _check_project(u, St.to(torch.float64).numpy(), [w.to(torch.float64).numpy() for w in Wt], got)
