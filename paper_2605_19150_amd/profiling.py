@@ -103,8 +103,16 @@ def traffic_markdown(kernel, workload, fetch, write, copy_fetch, copy_write, com
     `match` (default: kernel) selects the dispatches by a substring of their
     demangled name."""
     match = match or kernel
-    f_kib, nf = _counter_mean(fetch, "FETCH_SIZE", match)
-    w_kib, nw = _counter_mean(write, "WRITE_SIZE", match)
+    # several dispatches per call (e.g. an aggregate pass and the scan):
+    # substrings separated by ";;", their per-dispatch means add up
+    f_kib = w_kib = 0.0
+    nf = nw = 0
+    for m in match.split(";;"):
+        fk, n1 = _counter_mean(fetch, "FETCH_SIZE", m)
+        wk, n2 = _counter_mean(write, "WRITE_SIZE", m)
+        f_kib += fk
+        w_kib += wk
+        nf, nw = max(nf, n1), max(nw, n2)
     cf_kib, _ = _counter_mean(copy_fetch, "FETCH_SIZE", "copyBuffer")
     cw_kib, _ = _counter_mean(copy_write, "WRITE_SIZE", "copyBuffer")
     sf = COPY_BYTES / (cf_kib * 1024.0)
@@ -174,6 +182,8 @@ def counters_markdown(kernel, workload, dirs, command, match=None, state_updates
     out = ["# Occupancy, LDS and VALU counters: %s, workload %s" % (kernel, workload), "",
            "kernel: %s" % kernel, "dispatches: %s" % match, "workload: %s" % workload,
            "source-hash: %s" % source_hash(kernel), "",
+           "Instruction counts are wave instructions (one per 64 lanes); the per-state-update column",
+           "divides them by the launch's B*L*H*N state updates.", "",
            "| counter | mean per dispatch | per state update | dispatches | meaning |", "|---|---|---|---|---|"]
     for name, mean, n in rows:
         per = ("%.2f" % (mean / state_updates)) if state_updates and name.startswith("SQ_INSTS") else ""
