@@ -139,13 +139,20 @@ typedef enum pdssm_op {
 /* ABI version of the loaded library (PDSSM_ABI_VERSION at build time). */
 int pdssm_abi_version(void);
 
-/* Effective chunk length of desc (resolves chunk = 0), or a negative status. */
+/* Effective chunk length tau of desc (resolves chunk = 0; the chunk of App.
+ * E.1 Algorithm 1), or a negative status. */
 int pdssm_chunk_len(const pdssm_desc* desc);
 
-/* C = ceil(L / chunk) for the effective chunk, or a negative status. */
+/* C = ceil(L / tau), the number of chunks of App. E.1 Algorithm 1 (the last
+ * one may be short) for the effective chunk: the third extent of `saved`.
+ * Negative status for an invalid desc. */
 int pdssm_num_chunks(const pdssm_desc* desc);
 
-/* Workspace bytes the op needs for desc (0 if none); (size_t)-1 if desc is
+/* Workspace bytes the op needs for desc (0 if none): the per-head dictionary
+ * tables (App. E.2.1: one dictionary serves every step) and, for few long
+ * sequences, the segment aggregates of App. E.1 Algorithm 1 one level up
+ * (PDSSM_OP_FWD / PDSSM_OP_BWD), or the map-grouped partial sums of the
+ * straight-through gradients (PDSSM_OP_STE_GRADS); (size_t)-1 if desc is
  * invalid. */
 size_t pdssm_workspace_size(const pdssm_desc* desc, int op);
 
@@ -162,7 +169,8 @@ int pdssm_uses_fused(const pdssm_desc* desc);
  * structure, one level up).  Negative status for an invalid desc. */
 int pdssm_scan_segments(const pdssm_desc* desc);
 
-/* Human-readable name of a status code (static string, never NULL). */
+/* Human-readable name of a status code (static string, never NULL); the
+ * codes are this library's, not the paper's. */
 const char* pdssm_status_string(int status);
 
 /*
