@@ -349,6 +349,8 @@ def main():
                     help="bf16 (re, im) pairs for D, b, c and the gradients (fp32 arithmetic)")
     ap.add_argument("--real", action="store_true",
                     help="the real-valued model: real fp32 D, b, c and gradients")
+    ap.add_argument("--chunk", type=int, default=0,
+                    help="scan chunk length (4, 8 or 16 steps; 0: the library's default)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="profiling aid: time a plain 1 GiB device copy instead")
     args = ap.parse_args()
@@ -434,7 +436,7 @@ def time_scan(args, wi, dev, flush):
     if args.bf16:
         for k in ("D", "b", "c"):
             T[k] = torch.view_as_real(T[k]).to(torch.bfloat16).contiguous()
-    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, ste=args.ste, bf16=args.bf16, real=args.real)
+    s = pdssm.Scan(w.B, w.L, w.H, w.N, w.K, args.chunk, ste=args.ste, bf16=args.bf16, real=args.real)
     if args.ste:
         from paper_2605_19150_amd.inputs import selection_inputs
         logits, M = selection_inputs(inp["idx"], inp["pi"], seed=0)

@@ -110,10 +110,14 @@ typedef struct pdssm_desc {
  * entry, the recurrence h_t = P_t (D_t .* h_{t-1}) + b_t over the reals and
  * y_t = sum_n c_t[n] h_t[n].  Every other tensor keeps its type: h0, h_final,
  * saved, dh_final and dh0 stay complex64; for the real model h0 and dh_final
- * hold real values (imaginary parts 0, or NULL) and h_final, dh0 then come
- * out with imaginary parts 0.  The arithmetic is the complex64 one on rows
- * whose imaginary parts are 0, so every result equals, bit for bit, the real
- * part of a complex64 call on the same values.  Cannot be combined with
+ * hold real values (their imaginary parts must be 0; or NULL) and h_final,
+ * saved, dh0 come out with imaginary parts 0.  The single-read scan kernels
+ * keep the state real (float arithmetic, half the work of complex64); every
+ * product that feeds a sum is a fused multiply-add in both settings, so every
+ * result still equals, bit for bit, the real part of a complex64 call on the
+ * same values (the multi-pass kernels, for dictionaries beyond LDS, and the
+ * decode step compute the complex64 arithmetic on the real rows).  Cannot be
+ * combined with
  * PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG).  The scans, pdssm_decode_step
  * and the straight-through pair pdssm_scan_bwd_ste / pdssm_ste_grads support
  * it (z, g real fp32 rows); pdssm_compose_chunks returns

@@ -38,6 +38,51 @@ __device__ __forceinline__ float2 cmulc(float2 a, float2 b) {
 }
 __device__ __forceinline__ float2 cadd(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
 
+// The same operations on the real-valued model's float elements.  Each
+// rounds as the complex one does on values whose imaginary parts are 0 (a
+// complex product's real part is then fmaf(a, b, -0), the rounded product),
+// and every product that feeds a sum goes through one of the explicit
+// multiply-adds below in both forms, so the two element types compute the
+// same bits on real data.
+__device__ __forceinline__ float cmul(float a, float b) { return a * b; }
+__device__ __forceinline__ float cmulc(float a, float b) { return a * b; }
+__device__ __forceinline__ float cadd(float a, float b) { return a + b; }
+
+// acc + a b and acc + conj(a) b, real and imaginary parts each as two
+// chained fused multiply-adds (for real data the second adds an exact 0).
+__device__ __forceinline__ float2 cfma(float2 acc, float2 a, float2 b) {
+    return make_float2(fmaf(-a.y, b.y, fmaf(a.x, b.x, acc.x)), fmaf(a.y, b.x, fmaf(a.x, b.y, acc.y)));
+}
+__device__ __forceinline__ float2 cfmac(float2 acc, float2 a, float2 b) {
+    return make_float2(fmaf(a.y, b.y, fmaf(a.x, b.x, acc.x)), fmaf(-a.y, b.x, fmaf(a.x, b.y, acc.y)));
+}
+__device__ __forceinline__ float cfma(float acc, float a, float b) { return fmaf(a, b, acc); }
+__device__ __forceinline__ float cfmac(float acc, float a, float b) { return fmaf(a, b, acc); }
+
+// acc + Re(c h): the readout term c.x h.x - c.y h.y.
+__device__ __forceinline__ float re_fma(float acc, float2 c, float2 h) { return fmaf(-c.y, h.y, fmaf(c.x, h.x, acc)); }
+__device__ __forceinline__ float re_fma(float acc, float c, float h) { return fmaf(c, h, acc); }
+
+// Element constants.
+template <class E>
+__device__ __forceinline__ E ezero() {
+    if constexpr (sizeof(E) == 8) return make_float2(0.f, 0.f);
+    else return 0.f;
+}
+template <class E>
+__device__ __forceinline__ E eone() {
+    if constexpr (sizeof(E) == 8) return make_float2(1.f, 0.f);
+    else return 1.f;
+}
+// g + s conj(c) (the backward's readout term dy_t conj(c_t))
+__device__ __forceinline__ float2 add_sconj(float2 g, float s, float2 c) {
+    return make_float2(fmaf(s, c.x, g.x), fmaf(-s, c.y, g.y));
+}
+__device__ __forceinline__ float add_sconj(float g, float s, float c) { return fmaf(s, c, g); }
+// s conj(h) (the readout gradient dc_t = dy_t conj(h_t))
+__device__ __forceinline__ float2 sconj(float s, float2 h) { return make_float2(s * h.x, -s * h.y); }
+__device__ __forceinline__ float sconj(float s, float h) { return s * h; }
+
 // ------------------------------------------------------------------ wave sync
 // Orders this wave's LDS accesses in the compiler; the hardware already
 // executes one wave's LDS instructions in order.
@@ -58,6 +103,10 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ int readlane_i(int v, int l) { return __builtin_amdgcn_readlane(v, l); }
 __device__ __forceinline__ float readlane_f(float v, int l) {
     return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ float readlane_e(float v, int l) { return readlane_f(v, l); }
+__device__ __forceinline__ float2 readlane_e(float2 v, int l) {
+    return make_float2(readlane_f(v.x, l), readlane_f(v.y, l));
 }
 
 // Sum over the 64 lanes; the total lands in lane 63 (other lanes hold
@@ -84,27 +133,69 @@ __device__ __forceinline__ float wave_sum_last(float v) {
 // sinks work to its first use, which may sit behind a wait on another wave.
 __device__ __forceinline__ void materialize(float v) { asm volatile("" ::"v"(v) : "memory"); }
 __device__ __forceinline__ void materialize(int v) { asm volatile("" ::"v"(v) : "memory"); }
+__device__ __forceinline__ void materialize(float2 v) {
+    materialize(v.x);
+    materialize(v.y);
+}
 
 // Keeps memory operations issued before this point from being moved below it
 // (e.g. a prefetch the compiler would otherwise sink to its first use).
 __device__ __forceinline__ void issue_fence() { asm volatile("" ::: "memory"); }
 
 // ------------------------------------------------------------------ per-lane vectors
-template <int SL>
+template <int SL, class E = float2>
 struct CV {
-    float2 v[SL];
+    E v[SL];
 };
 template <int SL>
 struct IV {
     int v[SL];
 };
 
-template <int SL>
-__device__ __forceinline__ CV<SL> cv_zero() {
-    CV<SL> r;
+template <int SL, class E = float2>
+__device__ __forceinline__ CV<SL, E> cv_zero() {
+    CV<SL, E> r;
 #pragma unroll
-    for (int s = 0; s < SL; ++s) r.v[s] = make_float2(0.f, 0.f);
+    for (int s = 0; s < SL; ++s) r.v[s] = ezero<E>();
     return r;
+}
+
+// This lane's SL consecutive float entries of a row (row + lane*SL), as one
+// vector access.
+template <int SL>
+__device__ __forceinline__ CV<SL, float> ld_cv(const float* __restrict__ row, int lane) {
+    CV<SL, float> r;
+    const float* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        r.v[0] = *p;
+    } else if constexpr (SL == 2) {
+        const float2 q = *reinterpret_cast<const float2*>(p);
+        r.v[0] = q.x;
+        r.v[1] = q.y;
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4) {
+            const float4 q = *reinterpret_cast<const float4*>(p + s);
+            r.v[s] = q.x;
+            r.v[s + 1] = q.y;
+            r.v[s + 2] = q.z;
+            r.v[s + 3] = q.w;
+        }
+    }
+    return r;
+}
+template <int SL>
+__device__ __forceinline__ void st_cv(float* __restrict__ row, int lane, const CV<SL, float>& x) {
+    float* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        *p = x.v[0];
+    } else if constexpr (SL == 2) {
+        *reinterpret_cast<float2*>(p) = make_float2(x.v[0], x.v[1]);
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4)
+            *reinterpret_cast<float4*>(p + s) = make_float4(x.v[s], x.v[s + 1], x.v[s + 2], x.v[s + 3]);
+    }
 }
 
 // Load this lane's SL consecutive complex entries of a row (row + lane*SL).
@@ -156,6 +247,40 @@ __device__ __forceinline__ CV<SL> ld_row(__amdgpu_buffer_rsrc_t r, uint32_t voff
         }
     }
     return out;
+}
+
+// Complex64 rows in memory (states: h0, saved, h_final, dh0, segment
+// aggregates) as elements: the real model keeps the real part and writes
+// imaginary parts 0.
+template <class E, int SL>
+__device__ __forceinline__ CV<SL, E> to_elem(const CV<SL>& x) {
+    if constexpr (sizeof(E) == 8) {
+        return x;
+    } else {
+        CV<SL, E> r;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) r.v[s] = x.v[s].x;
+        return r;
+    }
+}
+template <int SL, class E>
+__device__ __forceinline__ CV<SL> to_c64(const CV<SL, E>& x) {
+    if constexpr (sizeof(E) == 8) {
+        return x;
+    } else {
+        CV<SL> r;
+#pragma unroll
+        for (int s = 0; s < SL; ++s) r.v[s] = make_float2(x.v[s], 0.f);
+        return r;
+    }
+}
+template <class E, int SL>
+__device__ __forceinline__ CV<SL, E> ld_state(const float2* __restrict__ row, int lane) {
+    return to_elem<E>(ld_cv<SL>(row, lane));
+}
+template <int SL, class E>
+__device__ __forceinline__ void st_state(float2* __restrict__ row, int lane, const CV<SL, E>& x) {
+    st_cv<SL>(row, lane, to_c64<SL>(x));
 }
 
 // ------------------------------------------------------------------ bf16 (re, im) pairs
@@ -210,6 +335,49 @@ __device__ __forceinline__ CV<SL> ld_row_w(__amdgpu_buffer_rsrc_t r, uint32_t vo
         }
     }
     return out;
+}
+
+// The real-valued model's rows as float elements (no widening).
+template <int SL, int AUX>
+__device__ __forceinline__ CV<SL, float> ld_row_r(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    CV<SL, float> out;
+    if constexpr (SL == 1) {
+        out.v[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX));
+    } else if constexpr (SL == 2) {
+        const uint2 q = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, AUX));
+        out.v[0] = __uint_as_float(q.x);
+        out.v[1] = __uint_as_float(q.y);
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4) {
+            const uint4 q =
+                __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff + 4 * s, AUX));
+            out.v[s] = __uint_as_float(q.x);
+            out.v[s + 1] = __uint_as_float(q.y);
+            out.v[s + 2] = __uint_as_float(q.z);
+            out.v[s + 3] = __uint_as_float(q.w);
+        }
+    }
+    return out;
+}
+
+// A row of float elements written with the nontemporal hint (the real
+// model's gradient rows).
+template <int SL>
+__device__ __forceinline__ void st_row_r_stream(float* __restrict__ row, int lane, const CV<SL, float>& x) {
+    typedef float f32x2 __attribute__((ext_vector_type(2)));
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    float* p = row + lane * SL;
+    if constexpr (SL == 1) {
+        __builtin_nontemporal_store(x.v[0], p);
+    } else if constexpr (SL == 2) {
+        __builtin_nontemporal_store(f32x2{x.v[0], x.v[1]}, reinterpret_cast<f32x2*>(p));
+    } else {
+#pragma unroll
+        for (int s = 0; s < SL; s += 4)
+            __builtin_nontemporal_store(f32x4{x.v[s], x.v[s + 1], x.v[s + 2], x.v[s + 3]},
+                                        reinterpret_cast<f32x4*>(p + s));
+    }
 }
 
 // This lane's SL entries of a row of 4-byte entries (row + lane*SL), with the
@@ -341,6 +509,8 @@ __device__ __forceinline__ void seg_step(float2& v, bool take) {
     v.y += take ? ty : 0.f;
 }
 
+__device__ __forceinline__ void seg_step1(float& v, float t, bool take) { v += take ? t : 0.f; }
+
 // Inclusive segmented sum over the 64 lanes of a complex value: a lane whose
 // bit is set in `starts` begins a new segment (lane 0 always does).  Row-wise
 // shifts, then the row broadcasts carry row totals across rows, each term
@@ -356,6 +526,23 @@ __device__ __forceinline__ float2 wave_seg_scan(float2 v, uint64_t starts, int l
     seg_step<0x143, 0xc>(v, s0 < 32);
     return v;
 }
+
+// The same for a real value (the real model's elements).
+__device__ __forceinline__ float wave_seg_scan(float v, uint64_t starts, int lane) {
+    const uint64_t le = starts & ((2ull << lane) - 1ull);
+    const int s0 = le ? 63 - __builtin_clzll(le) : 0;
+    seg_step1(v, dpp_fr<0x111, 0xf>(v), lane - 1 >= s0);
+    seg_step1(v, dpp_fr<0x112, 0xf>(v), lane - 2 >= s0);
+    seg_step1(v, dpp_fr<0x114, 0xf>(v), lane - 4 >= s0);
+    seg_step1(v, dpp_fr<0x118, 0xf>(v), lane - 8 >= s0);
+    seg_step1(v, dpp_fr<0x142, 0xa>(v), s0 < (lane & ~15));
+    seg_step1(v, dpp_fr<0x143, 0xc>(v), s0 < 32);
+    return v;
+}
+__device__ __forceinline__ float2 lane_up(float2 C) {  // from lane - 1
+    return make_float2(dpp_fr<0x138, 0xf>(C.x), dpp_fr<0x138, 0xf>(C.y));
+}
+__device__ __forceinline__ float lane_up(float C) { return dpp_fr<0x138, 0xf>(C); }
 
 // ------------------------------------------------------------------ collisions in a fixed order
 // The scatter-add h'[r] = b[r] + sum_{j: pi(j) = r} D[j] h[j] adds every
@@ -392,9 +579,9 @@ __device__ __forceinline__ uint64_t srt_word(int pos, int end, bool has, bool st
 // in-lane pass and a segmented scan across lanes (a fixed order); V is
 // overwritten.  Returns the run total of each of this lane's rows (0 when
 // empty).  All 64 lanes must call it; act = lane holds entries.
-template <int N>
-__device__ __forceinline__ CV<Lay<N>::SL> run_totals(float2* V, CV<Lay<N>::SL> u, const bool (&st)[Lay<N>::SL],
-                                                     const int (&e)[Lay<N>::SL], int lane, bool act) {
+template <int N, class E = float2>
+__device__ __forceinline__ CV<Lay<N>::SL, E> run_totals(E* V, CV<Lay<N>::SL, E> u, const bool (&st)[Lay<N>::SL],
+                                                        const int (&e)[Lay<N>::SL], int lane, bool act) {
     constexpr int SL = Lay<N>::SL;
     bool seen = false;
 #pragma unroll
@@ -403,11 +590,11 @@ __device__ __forceinline__ CV<Lay<N>::SL> run_totals(float2* V, CV<Lay<N>::SL> u
         seen |= st[r];
     }
     const uint64_t starts = __builtin_amdgcn_ballot_w64(act && seen);
-    const float2 C = wave_seg_scan(u.v[SL - 1], starts, lane);
+    const E C = wave_seg_scan(u.v[SL - 1], starts, lane);
     if constexpr (SL == 1) {
         u.v[0] = C;
     } else {
-        const float2 Cp = make_float2(dpp_fr<0x138, 0xf>(C.x), dpp_fr<0x138, 0xf>(C.y));  // from lane - 1
+        const E Cp = lane_up(C);
         bool head = false;
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
@@ -418,12 +605,12 @@ __device__ __forceinline__ CV<Lay<N>::SL> run_totals(float2* V, CV<Lay<N>::SL> u
     wave_sync();
     if (act) st_cv<SL>(V, lane, u);
     wave_sync();
-    CV<SL> tot = cv_zero<SL>();
+    CV<SL, E> tot = cv_zero<SL, E>();
     if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
-            const float2 t = V[e[r] < 0 ? 0 : e[r]];
-            tot.v[r] = e[r] < 0 ? make_float2(0.f, 0.f) : t;
+            const E t = V[e[r] < 0 ? 0 : e[r]];
+            tot.v[r] = e[r] < 0 ? ezero<E>() : t;
         }
     }
     return tot;
@@ -431,9 +618,9 @@ __device__ __forceinline__ CV<Lay<N>::SL> run_totals(float2* V, CV<Lay<N>::SL> u
 
 // h <- bt + P (Dt .* h) for a map given in sorted form (w = this lane's words
 // of the entry).  V: N values of the wave's LDS scratch.
-template <int N>
-__device__ __forceinline__ void sorted_step(float2* V, const uint64_t (&w)[Lay<N>::SL], CV<Lay<N>::SL>& h,
-                                            const CV<Lay<N>::SL>& Dt, const CV<Lay<N>::SL>& bt, int lane,
+template <int N, class E = float2>
+__device__ __forceinline__ void sorted_step(E* V, const uint64_t (&w)[Lay<N>::SL], CV<Lay<N>::SL, E>& h,
+                                            const CV<Lay<N>::SL, E>& Dt, const CV<Lay<N>::SL, E>& bt, int lane,
                                             bool act) {
     constexpr int SL = Lay<N>::SL;
     wave_sync();
@@ -442,7 +629,7 @@ __device__ __forceinline__ void sorted_step(float2* V, const uint64_t (&w)[Lay<N
         for (int r = 0; r < SL; ++r) V[srt_pos(w[r])] = cmul(Dt.v[r], h.v[r]);
     }
     wave_sync();
-    CV<SL> u = cv_zero<SL>();
+    CV<SL, E> u = cv_zero<SL, E>();
     if (act) u = ld_cv<SL>(V, lane);
     bool st[SL];
     int e[SL];
@@ -451,7 +638,7 @@ __device__ __forceinline__ void sorted_step(float2* V, const uint64_t (&w)[Lay<N
         st[r] = srt_start(w[r]);
         e[r] = srt_end(w[r]);
     }
-    const CV<SL> tot = run_totals<N>(V, u, st, e, lane, act);
+    const CV<SL, E> tot = run_totals<N, E>(V, u, st, e, lane, act);
     if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) h.v[r] = cadd(bt.v[r], tot.v[r]);
@@ -584,15 +771,13 @@ __device__ __forceinline__ void table_step(float2* V, int cls, const uint64_t (&
 }
 
 // acc += the sources M0 .. M1-1 of a record (V = the wave's staged values).
-template <int M0, int M1>
-__device__ __forceinline__ void gather_rec_range(const float2* V, uint64_t r, float2& acc) {
+template <int M0, int M1, class E>
+__device__ __forceinline__ void gather_rec_range(const E* V, uint64_t r, E& acc) {
     const unsigned lo = (unsigned)r, hi = (unsigned)(r >> 32);
 #pragma unroll
     for (int m = M0; m < M1; ++m) {
         const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
-        const float2 v = V[src];
-        acc.x += v.x;
-        acc.y += v.y;
+        acc = cadd(acc, V[src]);
     }
 }
 

@@ -45,6 +45,12 @@
 // The last chunk of a sequence may be short; its missing steps run as exact
 // no-ops (D = 1, b = 0, an identity dictionary entry at index K), so no step
 // tests its own index either.
+//
+// Row formats.  D, b, c and the gradients come as complex64, bf16 (re, im)
+// pairs or real fp32 (the real-valued model of App. B).  The first two run
+// complex (float2) arithmetic; the real model runs with float elements
+// throughout (state, LDS staging, published operators), rounding every
+// operation as the complex arithmetic does on zero imaginary parts.
 #include "pdssm_device.h"
 #include "pdssm_fused.h"
 
@@ -165,6 +171,19 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
 }
 
 // ------------------------------------------------------------------ shared pieces
+// Element of the state and of the rows as the kernels compute them: complex
+// (float2) for complex64 and bf16 pairs, float for the real-valued model,
+// whose states stay real (half the arithmetic and LDS bytes).  Every
+// buffer keeps its place in the layout; the real model uses its first half.
+template <int IO>
+struct ElemOf {
+    using T = float2;
+};
+template <>
+struct ElemOf<kIoReal> {
+    using T = float;
+};
+
 struct Smem {
     uint64_t* rec;  // [K+1][N]
     uint8_t* dict;  // [K+1][N]
@@ -211,15 +230,16 @@ __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout&
 // unused gather slots) and a second operand Z[0..N] (D_t, or the backward's
 // diagonal), as two arrays of 8-byte words so that a 64-lane gather from V
 // spreads over all 32 bank pairs.
+template <class E>
 struct Stage {
-    float2* V;
-    float2* Z;
+    E* V;
+    E* Z;
 };
 
-template <int N>
-__device__ __forceinline__ Stage stage_of(const Smem& s, int wv) {
+template <int N, class E = float2>
+__device__ __forceinline__ Stage<E> stage_of(const Smem& s, int wv) {
     float2* base = reinterpret_cast<float2*>(s.vd + wv * (N + 1));
-    return Stage{base, base + N + 1};
+    return Stage<E>{reinterpret_cast<E*>(base), reinterpret_cast<E*>(base + N + 1)};
 }
 
 // Copy head hh's dictionary tables into LDS and append the identity entry
@@ -247,9 +267,9 @@ __device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, 
 }
 
 // Clear the zero row V[N] of the first nw waves' staging rows.
-template <int N>
+template <int N, class E>
 __device__ __forceinline__ void clear_zero_rows(const Smem& s, int nw) {
-    for (int w = threadIdx.x; w < nw; w += blockDim.x) reinterpret_cast<float2*>(s.vd + w * (N + 1))[N] = make_float2(0.f, 0.f);
+    for (int w = threadIdx.x; w < nw; w += blockDim.x) stage_of<N, E>(s, w).V[N] = ezero<E>();
 }
 
 // Gather variant of a head: the smallest of 1, 3, 7 sources covering every
@@ -328,9 +348,8 @@ __device__ __forceinline__ void publish_ready(int* ready, int v) {
 
 // acc[j] += sum of V[src] over the G listed sources of destination row j;
 // V = the wave's staged values.  Straight-line: G reads, no tests.
-template <int N, int G>
-__device__ __forceinline__ void gather_rows(const float2* V, const uint64_t* recrow, int lane,
-                                            CV<Lay<N>::SL>& acc) {
+template <int N, int G, class E>
+__device__ __forceinline__ void gather_rows(const E* V, const uint64_t* recrow, int lane, CV<Lay<N>::SL, E>& acc) {
     constexpr int SL = Lay<N>::SL;
 #pragma unroll
     for (int s = 0; s < SL; ++s) {
@@ -339,22 +358,21 @@ __device__ __forceinline__ void gather_rows(const float2* V, const uint64_t* rec
 #pragma unroll
         for (int m = 0; m < G; ++m) {
             const unsigned src = m < 4 ? (lo >> (8 * m)) & 255u : (hi >> (8 * (m - 4))) & 255u;
-            float2 v = V[src];
+            E v = V[src];
             if constexpr (!Sentinel<N>::kZeroRow) {
                 const bool use = m < (int)(hi >> 24);
-                v = use ? v : make_float2(0.f, 0.f);
+                v = use ? v : ezero<E>();
             }
-            acc.v[s].x += v.x;
-            acc.v[s].y += v.y;
+            acc.v[s] = cadd(acc.v[s], v);
         }
     }
 }
 
 // Per-chunk registers of one wave.
-template <int N, int TAU>
+template <int N, int TAU, class E = float2>
 struct Chunk {
     static constexpr int SL = Lay<N>::SL;
-    CV<SL> D[TAU], b[TAU], c[TAU];
+    CV<SL, E> D[TAU], b[TAU], c[TAU];
     int kv, mv, len;
 };
 
@@ -366,9 +384,9 @@ struct Chunk {
 // need 4 or 5).  The forward's pipelined chunk pass keeps its fixed count:
 // there the branch splits the step's one batch of LDS reads and measured
 // slower.
-template <int N, int G>
-__device__ __forceinline__ void gather_rows_k(const float2* V, const uint64_t* recrow, int lane,
-                                              CV<Lay<N>::SL>& acc, int gk) {
+template <int N, int G, class E>
+__device__ __forceinline__ void gather_rows_k(const E* V, const uint64_t* recrow, int lane, CV<Lay<N>::SL, E>& acc,
+                                              int gk) {
     if constexpr (G <= 3) {
         gather_rows<N, G>(V, recrow, lane, acc);
     } else {
@@ -383,9 +401,10 @@ __device__ __forceinline__ void gather_rows_k(const float2* V, const uint64_t* r
 // in Z for a map composition.  FB: the head has entries in sorted form
 // (a row of more than kMaxSrc sources), tested per step.  M: the step's
 // in-degree class (its map's max in-degree, or kFallback).
-template <int N, int G, bool FB, bool STAGE_D>
-__device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, int lane, bool act, int k, int M,
-                                        CV<Lay<N>::SL>& h, const CV<Lay<N>::SL>& Dt, const CV<Lay<N>::SL>& bt) {
+template <int N, int G, bool FB, bool STAGE_D, class E>
+__device__ __forceinline__ void pd_step(const Smem& s, const Stage<E>& st, int lane, bool act, int k, int M,
+                                        CV<Lay<N>::SL, E>& h, const CV<Lay<N>::SL, E>& Dt,
+                                        const CV<Lay<N>::SL, E>& bt) {
     constexpr int SL = Lay<N>::SL;
     if constexpr (FB) {
         if (M == (int)kFallback) {
@@ -399,7 +418,7 @@ __device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, int lane
                     for (int q = 0; q < SL; ++q) st.Z[lane * SL + q] = Dt.v[q];
                 }
             }
-            sorted_step<N>(st.V, w, h, Dt, bt, lane, act);
+            sorted_step<N, E>(st.V, w, h, Dt, bt, lane, act);
             return;
         }
     }
@@ -407,14 +426,13 @@ __device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, int lane
     if (act) {
 #pragma unroll
         for (int q = 0; q < SL; ++q) {
-            const float2 v = cmul(Dt.v[q], h.v[q]);
-            st.V[lane * SL + q] = v;
+            st.V[lane * SL + q] = cmul(Dt.v[q], h.v[q]);
             if constexpr (STAGE_D) st.Z[lane * SL + q] = Dt.v[q];
         }
     }
     wave_sync();
     if (act) {
-        CV<SL> acc = bt;
+        CV<SL, E> acc = bt;
         gather_rows_k<N, G>(st.V, s.rec + (size_t)k * N, lane, acc, M);
         h = acc;
     }
@@ -432,7 +450,8 @@ __device__ __forceinline__ void pd_step(const Smem& s, const Stage& st, int lane
 // AUX: cache policy of the row loads (the forward streams them, kLoadStream).
 template <int N, int TAU, bool LOAD_B, bool LOAD_C, int AUX = 0, int IO = kIoC64>
 __device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, int ch, int lane, bool act,
-                                            Chunk<N, TAU>& q) {
+                                            Chunk<N, TAU, typename ElemOf<IO>::T>& q) {
+    using E = typename ElemOf<IO>::T;
     constexpr int SL = Lay<N>::SL;
     const int chc = min(ch, a.C - 1);  // addresses stay inside the tensors
     const int s0 = chc * TAU;
@@ -449,7 +468,8 @@ __device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, 
     const __amdgpu_buffer_rsrc_t rnull = row_block(a.D, 0);
     const uint32_t voff = (uint32_t)lane * SL * ESZ;
     auto ld = [&](__amdgpu_buffer_rsrc_t r, uint32_t so) {
-        if constexpr (IO != kIoC64) return ld_row_w<SL, AUX, IO>(r, voff, so);
+        if constexpr (IO == kIoReal) return ld_row_r<SL, AUX>(r, voff, so);
+        else if constexpr (IO == kIoBf16) return ld_row_w<SL, AUX, IO>(r, voff, so);
         else return ld_row<SL, AUX>(r, voff, so);
     };
 #pragma unroll
@@ -461,28 +481,28 @@ __device__ __forceinline__ void issue_chunk(const FusedArgs& a, int bb, int hh, 
             if constexpr (LOAD_B) q.b[t] = ld(in ? rb : rnull, soff);
             if constexpr (LOAD_C) q.c[t] = ld(in ? rc : rnull, soff);
         } else {
-            q.D[t] = cv_zero<SL>();
-            if constexpr (LOAD_B) q.b[t] = cv_zero<SL>();
-            if constexpr (LOAD_C) q.c[t] = cv_zero<SL>();
+            q.D[t] = cv_zero<SL, E>();
+            if constexpr (LOAD_B) q.b[t] = cv_zero<SL, E>();
+            if constexpr (LOAD_C) q.c[t] = cv_zero<SL, E>();
         }
     }
 }
 
 // D row of step t as used by the step: 1 for the padded steps of a short chunk.
-template <int N, int TAU>
-__device__ __forceinline__ CV<Lay<N>::SL> Dt(const Chunk<N, TAU>& q, int t) {
-    CV<Lay<N>::SL> d = q.D[t];
+template <int N, int TAU, class E>
+__device__ __forceinline__ CV<Lay<N>::SL, E> Dt(const Chunk<N, TAU, E>& q, int t) {
+    CV<Lay<N>::SL, E> d = q.D[t];
     const bool in = t < q.len;
 #pragma unroll
-    for (int r = 0; r < Lay<N>::SL; ++r) d.v[r] = in ? d.v[r] : make_float2(1.f, 0.f);
+    for (int r = 0; r < Lay<N>::SL; ++r) d.v[r] = in ? d.v[r] : eone<E>();
     return d;
 }
 
 // Completes an issued chunk: checks the dictionary indices (an index outside
 // [0,K) becomes 0 and is reported) and looks up the steps' in-degree class;
 // padded steps use the identity dictionary entry K.
-template <int N, int TAU>
-__device__ __forceinline__ void finish_chunk(const FusedArgs& a, const Smem& s, int lane, Chunk<N, TAU>& q,
+template <int N, int TAU, class E>
+__device__ __forceinline__ void finish_chunk(const FusedArgs& a, const Smem& s, int lane, Chunk<N, TAU, E>& q,
                                              bool& bad) {
     if (lane < q.len) {
         const bool bk = (unsigned)q.kv >= (unsigned)a.K;
@@ -583,20 +603,20 @@ __device__ __forceinline__ Work work_of(const FusedArgs& a, int nseg, int first_
 // The state entering segment w.sg: h0 (or 0) pushed through the aggregates
 // of segments 0 .. w.sg-1, carry <- B_s + Phi_s carry, each row adding its
 // sources in ascending order (cross-lane values by readlane).
-template <int N>
-__device__ __forceinline__ CV<Lay<N>::SL> seg_enter_fwd(const FusedArgs& a, const Work& w, int lane, bool act) {
+template <int N, class E>
+__device__ __forceinline__ CV<Lay<N>::SL, E> seg_enter_fwd(const FusedArgs& a, const Work& w, int lane, bool act) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    CV<SL> carry = cv_zero<SL>();
-    if (a.h0 && act) carry = ld_cv<SL>(a.h0 + (size_t)w.seq * N, lane);
+    CV<SL, E> carry = cv_zero<SL, E>();
+    if (a.h0 && act) carry = ld_state<E, SL>(a.h0 + (size_t)w.seq * N, lane);
     for (int sp = 0; sp < w.sg; ++sp) {
         const size_t base = ((size_t)w.seq * a.S + sp) * N;
-        CV<SL> acc = cv_zero<SL>(), v = cv_zero<SL>();
+        CV<SL, E> acc = cv_zero<SL, E>(), v = cv_zero<SL, E>();
         IV<SL> P;
 #pragma unroll
         for (int r = 0; r < SL; ++r) P.v[r] = 0;
         if (act) {
-            acc = ld_cv<SL>(a.segA + base, lane);
-            const CV<SL> d = ld_cv<SL>(a.segD + base, lane);
+            acc = ld_state<E, SL>(a.segA + base, lane);
+            const CV<SL, E> d = ld_state<E, SL>(a.segD + base, lane);
             P = ld_iv<SL>(a.segP + base, lane);
 #pragma unroll
             for (int r = 0; r < SL; ++r) v.v[r] = cmul(d.v[r], carry.v[r]);
@@ -605,12 +625,11 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_fwd(const FusedArgs& a, cons
 #pragma unroll
             for (int q = 0; q < SL; ++q) {
                 const int pj = readlane_i(P.v[q], jl);
-                const float vx = readlane_f(v.v[q].x, jl), vy = readlane_f(v.v[q].y, jl);
+                const E vj = readlane_e(v.v[q], jl);
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
                     const bool hit = pj == lane * SL + r;
-                    acc.v[r].x += hit ? vx : 0.f;
-                    acc.v[r].y += hit ? vy : 0.f;
+                    acc.v[r] = cadd(acc.v[r], hit ? vj : ezero<E>());
                 }
             }
         }
@@ -621,27 +640,49 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_fwd(const FusedArgs& a, cons
 
 // A wave's running fold in the aggregate pass: map, diagonal and local state
 // of the chunks it has folded so far (identity and zero at its first one).
-template <int SL>
+template <int SL, class E>
 struct RunState {
     IV<SL> pm;
-    CV<SL> dm, Bm;
+    CV<SL, E> dm, Bm;
 };
+
+// A published operator entry: local state and diagonal side by side (one
+// 16-byte word for complex values, 8 bytes for real ones).
+__device__ __forceinline__ void put_op(float4* agg, int i, float2 B, float2 d) {
+    agg[i] = make_float4(B.x, B.y, d.x, d.y);
+}
+__device__ __forceinline__ void put_op(float4* agg, int i, float B, float d) {
+    reinterpret_cast<float2*>(agg)[i] = make_float2(B, d);
+}
+__device__ __forceinline__ void get_op(const float4* agg, int i, float2& B, float2& d) {
+    const float4 e = agg[i];
+    B = make_float2(e.x, e.y);
+    d = make_float2(e.z, e.w);
+}
+__device__ __forceinline__ void get_op(const float4* agg, int i, float& B, float& d) {
+    const float2 e = reinterpret_cast<const float2*>(agg)[i];
+    B = e.x;
+    d = e.y;
+}
 
 // Writes an operator (local state Bm, diagonal dm, map pm) into operator slot
 // `slot` (and its sorted map, many-to-one heads), then raises the slot's flag
 // to `flag`.  AGG also keeps the plain map for the frontier's composition.
-template <int N, int G, bool FB, bool AGG>
+template <int N, int G, bool FB, bool AGG, class E>
 __device__ __forceinline__ void publish_op(const Smem& s, int wa, int wv, int slot, int flag, const IV<Lay<N>::SL>& pm,
-                                           const CV<Lay<N>::SL>& dm, const CV<Lay<N>::SL>& Bm, int lane, bool act) {
+                                           const CV<Lay<N>::SL, E>& dm, const CV<Lay<N>::SL, E>& Bm, int lane,
+                                           bool act) {
     constexpr int SL = Lay<N>::SL;
-    const Stage st = stage_of<N>(s, wv);
+    // scratch for the sorted map: the wave's buffers in their complex
+    // layout, whatever the element type (no other wave's buffers overlap)
+    const Stage<float2> st = stage_of<N>(s, wv);
     float2* X = s.x + wv * N;
     float2* CS = s.cs + wv * N;
     wave_sync();
     if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
-            s.agg[slot * N + lane * SL + r] = make_float4(Bm.v[r].x, Bm.v[r].y, dm.v[r].x, dm.v[r].y);
+            put_op(s.agg, slot * N + lane * SL + r, Bm.v[r], dm.v[r]);
             if constexpr (G == 1 && !FB) s.agp[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
             if constexpr (AGG) s.agm[slot * N + lane * SL + r] = (uint8_t)pm.v[r];
         }
@@ -669,34 +710,36 @@ __device__ __forceinline__ void publish_op(const Smem& s, int wa, int wv, int sl
 // AGG: the aggregate pass of a segment -- the wave only builds and publishes
 // the chunk operator (c is not loaded, no readout).  RUN (with AGG): the pass
 // starts from and returns to *run instead, and publishes nothing.
-template <int N, int TAU, int W, int G, bool FB, bool AGG, bool RUN = false>
+template <int N, int TAU, int W, int G, bool FB, bool AGG, bool RUN = false, class E>
 __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int lc,
-                                          Chunk<N, TAU>& q, bool& bad, RunState<Lay<N>::SL>* run = nullptr) {
+                                          Chunk<N, TAU, E>& q, bool& bad, RunState<Lay<N>::SL, E>* run = nullptr) {
     static_assert(!RUN || AGG, "a run fold is an aggregate pass");
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     const int ch = w.c0 + lc;
-    const Stage st = stage_of<N>(s, wv);
-    float2* CS = s.cs + wv * N;  // buffer 0; buffer 1 is Wa*N further (the layout's wave count)
+    const Stage<E> st = stage_of<N, E>(s, wv);
     const int WA = active_waves<W>(w);
-    const int csb = WA * N;
+    // c staging buffer 0, and buffer 1 Wa*N complex slots further (the
+    // layout's wave count), in elements
+    E* CS = reinterpret_cast<E*>(s.cs + wv * N);
+    const int csb = WA * N * (int)(sizeof(float2) / sizeof(E));
     finish_chunk<N, TAU>(a, s, lane, q, bad);
 
     // ---- 2. one pass: local state B, chunk operator (Pi, Delta), w_t, local readout
     IV<SL> pm;
-    CV<SL> dm, Bm = cv_zero<SL>();
+    CV<SL, E> dm, Bm = cv_zero<SL, E>();
 #pragma unroll
     for (int r = 0; r < SL; ++r) {
         pm.v[r] = lane * SL + r;
-        dm.v[r] = make_float2(1.f, 0.f);
+        dm.v[r] = eone<E>();
     }
     if constexpr (RUN) {
         pm = run->pm;
         dm = run->dm;
         Bm = run->Bm;
     }
-    CV<SL> wt[TAU];
+    CV<SL, E> wt[TAU];
     float yl[TAU];
     if constexpr (!FB && Sentinel<N>::kZeroRow) {
         // Pipelined form: every step's gather records are read at chunk start;
@@ -716,16 +759,15 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
         for (int t = 0; t < TAU; ++t) {
             const int k = readlane_i(q.kv, t), gk = readlane_i(q.mv, t);
-            float2* CSt = CS + (t & 1) * csb;
-            const float2* CSp = CS + ((t + 1) & 1) * csb;
-            const CV<SL> Dv = Dt(q, t);
+            E* CSt = CS + (t & 1) * csb;
+            const E* CSp = CS + ((t + 1) & 1) * csb;
+            const CV<SL, E> Dv = Dt(q, t);
             wave_sync();
             if (act) {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
                     if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
-                    const float2 v = cmul(Dv.v[r], Bm.v[r]);
-                    st.V[lane * SL + r] = v;
+                    st.V[lane * SL + r] = cmul(Dv.v[r], Bm.v[r]);
                     st.Z[lane * SL + r] = Dv.v[r];
                 }
             }
@@ -736,7 +778,7 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                 // reads in one batch; the 7-source class reads the rest only
                 // at steps whose map has a row with more than GM sources
                 constexpr int GM = G > 4 ? 4 : G;
-                float2 acc[SL], Dp[SL], Cp[SL];
+                E acc[SL], Dp[SL], Cp[SL];
                 int np[SL];
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
@@ -761,21 +803,21 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                     Bm.v[r] = acc[r];
                     dm.v[r] = cmul(Dp[r], dm.v[r]);
                     pm.v[r] = np[r];
-                    if constexpr (!AGG) part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+                    if constexpr (!AGG) part = re_fma(part, q.c[t].v[r], Bm.v[r]);
                 }
             } else if constexpr (!AGG) {
-                if (t > 0) wt[t - 1] = cv_zero<SL>();
+                if (t > 0) wt[t - 1] = cv_zero<SL, E>();
             }
             yl[t] = part;
         }
         if constexpr (!AGG) {
-            const float2* CSl = CS + ((TAU - 1) & 1) * csb;
+            const E* CSl = CS + ((TAU - 1) & 1) * csb;
             wave_sync();
             if (act) {
 #pragma unroll
                 for (int r = 0; r < SL; ++r) wt[TAU - 1].v[r] = cmul(dm.v[r], CSl[pm.v[r]]);
             } else {
-                wt[TAU - 1] = cv_zero<SL>();
+                wt[TAU - 1] = cv_zero<SL, E>();
             }
         }
     } else {
@@ -799,11 +841,11 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
                     pm.v[r] = s.dict[k * N + p];
                     if constexpr (!AGG) {
                         wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
-                        part += q.c[t].v[r].x * Bm.v[r].x - q.c[t].v[r].y * Bm.v[r].y;
+                        part = re_fma(part, q.c[t].v[r], Bm.v[r]);
                     }
                 }
             } else if constexpr (!AGG) {
-                wt[t] = cv_zero<SL>();
+                wt[t] = cv_zero<SL, E>();
             }
             yl[t] = part;
         }
@@ -832,16 +874,15 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     }
     if constexpr (AGG) return;
     wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * WA, s.prog);
-    CV<SL> carry = cv_zero<SL>();
-    if (act) carry = ld_cv<SL>(s.ring + (lc % (WA + 1)) * N, lane);
-    if (act && a.saved && w.sbm == 0) st_cv<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
+    CV<SL, E> carry = cv_zero<SL, E>();
+    if (act) carry = ld_cv<SL>(reinterpret_cast<const E*>(s.ring) + (lc % (WA + 1)) * N, lane);
+    if (act && a.saved && w.sbm == 0) st_state<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
 
     // ---- 4. readout correction with the true carry, then one store per chunk
 #pragma unroll
     for (int t = 0; t < TAU; ++t) {
 #pragma unroll
-        for (int r = 0; r < SL; ++r)
-            yl[t] += wt[t].v[r].x * carry.v[r].x - wt[t].v[r].y * carry.v[r].y;
+        for (int r = 0; r < SL; ++r) yl[t] = re_fma(yl[t], wt[t].v[r], carry.v[r]);
     }
     const float yv = transpose_sum<TAU>(yl, lane);
     const int t = lane / (kWave / TAU);
@@ -853,28 +894,26 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
 // and diagonal d; p = the map (permutation heads) or the sorted position of
 // each source; e, h = run ends per destination and run-start flags per
 // position (many-to-one heads).
-template <int SL>
+template <int SL, class E>
 struct ChunkOp {
-    CV<SL> B, d;
+    CV<SL, E> B, d;
     IV<SL> p, e, h;
 };
 
-template <int N, bool SORTED>
-__device__ __forceinline__ ChunkOp<Lay<N>::SL> read_op(const Smem& s, int slot, int lane, bool act) {
+template <int N, bool SORTED, class E>
+__device__ __forceinline__ ChunkOp<Lay<N>::SL, E> read_op(const Smem& s, int slot, int lane, bool act) {
     constexpr int SL = Lay<N>::SL;
-    ChunkOp<SL> o;
+    ChunkOp<SL, E> o;
 #pragma unroll
     for (int r = 0; r < SL; ++r) {
-        o.B.v[r] = o.d.v[r] = make_float2(0.f, 0.f);
+        o.B.v[r] = o.d.v[r] = ezero<E>();
         o.p.v[r] = o.e.v[r] = o.h.v[r] = 0;
     }
     if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
             const int i = slot * N + lane * SL + r;
-            const float4 e = s.agg[i];
-            o.B.v[r] = make_float2(e.x, e.y);
-            o.d.v[r] = make_float2(e.z, e.w);
+            get_op(s.agg, i, o.B.v[r], o.d.v[r]);
             o.p.v[r] = s.agp[i];
             if constexpr (SORTED) {
                 o.e.v[r] = s.age[i];
@@ -887,11 +926,11 @@ __device__ __forceinline__ ChunkOp<Lay<N>::SL> read_op(const Smem& s, int slot, 
 
 // nxt = B + Pi (Delta .* carry) for a sorted many-to-one operator; X: N
 // complex values of LDS scratch.
-template <int N>
-__device__ __forceinline__ CV<Lay<N>::SL> apply_sorted(const ChunkOp<Lay<N>::SL>& op, const CV<Lay<N>::SL>& carry,
-                                                       float2* X, int lane, bool act) {
+template <int N, class E>
+__device__ __forceinline__ CV<Lay<N>::SL, E> apply_sorted(const ChunkOp<Lay<N>::SL, E>& op,
+                                                          const CV<Lay<N>::SL, E>& carry, E* X, int lane, bool act) {
     constexpr int SL = Lay<N>::SL;
-    CV<SL> u = cv_zero<SL>();
+    CV<SL, E> u = cv_zero<SL, E>();
     wave_sync();
     if (act) {
 #pragma unroll
@@ -906,8 +945,8 @@ __device__ __forceinline__ CV<Lay<N>::SL> apply_sorted(const ChunkOp<Lay<N>::SL>
         st[r] = op.h.v[r] != 0;
         e[r] = op.e.v[r] == kNoRun ? -1 : op.e.v[r];
     }
-    const CV<SL> tot = run_totals<N>(X, u, st, e, lane, act);
-    CV<SL> nxt = cv_zero<SL>();
+    const CV<SL, E> tot = run_totals<N, E>(X, u, st, e, lane, act);
+    CV<SL, E> nxt = cv_zero<SL, E>();
     if (act) {
 #pragma unroll
         for (int r = 0; r < SL; ++r) nxt.v[r] = cadd(op.B.v[r], tot.v[r]);
@@ -925,29 +964,30 @@ __device__ __forceinline__ CV<Lay<N>::SL> apply_sorted(const ChunkOp<Lay<N>::SL>
 // operator's; a flag still behind sends the wave to a bounded wait and a
 // re-read).  The wave runs at raised issue priority: it shares its SIMD with
 // chunk waves whose long arithmetic runs would otherwise delay it.
-template <int N, int W, int G, bool FB, bool AGG>
+template <int N, int W, int G, bool FB, bool AGG, class E>
 __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, const Work& w) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     constexpr bool kPerm = G == 1 && !FB;
     const int lane = lane_id();
     const bool act = lane < LANES;
     const int WA = active_waves<W>(w);
-    float2* X = s.x + WA * N;
+    E* X = reinterpret_cast<E*>(s.x + WA * N);
+    E* ring = reinterpret_cast<E*>(s.ring);
     int* flags = s.ready;
     const int nflags = 1 + 2 * WA;
     // The aggregate pass folds the segment from zero and composes its map;
     // the scan starts from the state entering its segment.
-    CV<SL> carry = AGG ? cv_zero<SL>() : seg_enter_fwd<N>(a, w, lane, act);
+    CV<SL, E> carry = AGG ? cv_zero<SL, E>() : seg_enter_fwd<N, E>(a, w, lane, act);
     IV<SL> accP;
-    CV<SL> accD;
+    CV<SL, E> accD;
 #pragma unroll
     for (int r = 0; r < SL; ++r) {
         accP.v[r] = lane * SL + r;
-        accD.v[r] = make_float2(1.f, 0.f);
+        accD.v[r] = eone<E>();
     }
     __builtin_amdgcn_s_setprio(3);
     wait_ready(s.aflag, 0, a.status, flags, nflags, s.prog);
-    ChunkOp<SL> op = read_op<N, !kPerm>(s, 0, lane, act);
+    ChunkOp<SL, E> op = read_op<N, !kPerm, E>(s, 0, lane, act);
     const int M = AGG || !a.saved ? 0 : w.sbm;
     // slot indices c % (Wa + 1) (carry ring) and c % (2 Wa) (operators),
     // advanced by one per chunk
@@ -955,15 +995,15 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     int rslot = 0, oslot = 0;
     for (int c = 0; c < w.nc; ++c) {
         wave_sync();
-        if (!AGG && act) st_cv<SL>(s.ring + rslot * N, lane, carry);
+        if (!AGG && act) st_cv<SL>(ring + rslot * N, lane, carry);
         rslot = rslot + 1 == nring ? 0 : rslot + 1;
         if (M > 0 && act) {
             // the first M chunk states wait in LDS until the whole workgroup
             // has read its rows; later ones (near the end anyway) go out now
-            if (c < M) st_cv<SL>(s.sb + c * N, lane, carry);
-            else st_cv<SL>(a.saved + ((size_t)w.seq * a.C + w.c0 + c) * N, lane, carry);
+            if (c < M) st_state<SL>(s.sb + c * N, lane, carry);
+            else st_state<SL>(a.saved + ((size_t)w.seq * a.C + w.c0 + c) * N, lane, carry);
         }
-        CV<SL> nxt;
+        CV<SL, E> nxt;
         if constexpr (kPerm) {
             // every entry is a permutation, so is Pi_c: scatter by plain stores
             if (act) {
@@ -976,20 +1016,20 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         const int nslot = oslot + 1 == nops ? 0 : oslot + 1;
         oslot = nslot;
         int seen = 0x7fffffff;
-        ChunkOp<SL> nx;
+        ChunkOp<SL, E> nx;
         if (more) {
             seen = __hip_atomic_load(s.aflag + nslot, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
             issue_fence();
-            nx = read_op<N, !kPerm>(s, nslot, lane, act);
+            nx = read_op<N, !kPerm, E>(s, nslot, lane, act);
         }
         if constexpr (kPerm) {
             wave_sync();
-            nxt = cv_zero<SL>();
+            nxt = cv_zero<SL, E>();
             if (act) nxt = ld_cv<SL>(X, lane);
 #pragma unroll
             for (int r = 0; r < SL; ++r) nxt.v[r] = cadd(nxt.v[r], op.B.v[r]);
         } else {
-            nxt = apply_sorted<N>(op, carry, X, lane, act);
+            nxt = apply_sorted<N, E>(op, carry, X, lane, act);
         }
         if constexpr (AGG) {
             // Phi_acc <- Phi_c Phi_acc: (Pi_c[Pi_acc], Delta_c[Pi_acc] * Delta_acc)
@@ -997,8 +1037,9 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
 #pragma unroll
                 for (int r = 0; r < SL; ++r) {
                     const int p = accP.v[r];
-                    const float4 e = s.agg[slot * N + p];
-                    accD.v[r] = cmul(make_float2(e.z, e.w), accD.v[r]);
+                    E Bc, dc;
+                    get_op(s.agg, slot * N + p, Bc, dc);
+                    accD.v[r] = cmul(dc, accD.v[r]);
                     accP.v[r] = s.agm[slot * N + p];
                 }
             }
@@ -1009,7 +1050,7 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         if (more) {
             if (__builtin_amdgcn_readfirstlane(seen) < c + 1) {
                 wait_ready(s.aflag + nslot, c + 1, a.status, flags, nflags, s.prog);
-                nx = read_op<N, !kPerm>(s, nslot, lane, act);
+                nx = read_op<N, !kPerm, E>(s, nslot, lane, act);
             }
             op = nx;
         }
@@ -1018,12 +1059,12 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
     if constexpr (AGG) {
         const size_t base = ((size_t)w.seq * a.S + w.sg) * N;
         if (act) {
-            st_cv<SL>(a.segA + base, lane, carry);
-            st_cv<SL>(a.segD + base, lane, accD);
+            st_state<SL>(a.segA + base, lane, carry);
+            st_state<SL>(a.segD + base, lane, accD);
             st_iv<SL>(a.segP + base, lane, accP);
         }
     } else if (act && a.hfinal && w.sg == a.S - 1) {
-        st_cv<SL>(a.hfinal + (size_t)w.seq * N, lane, carry);
+        st_state<SL>(a.hfinal + (size_t)w.seq * N, lane, carry);
     }
 }
 
@@ -1032,10 +1073,11 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
 // buffers).  A local chunk past the range issues an empty chunk.
 template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, int IO>
 __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
+    using E = typename ElemOf<IO>::T;
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
-    auto issue = [&](int lc, Chunk<N, TAU>& q) {
+    auto issue = [&](int lc, Chunk<N, TAU, E>& q) {
         issue_chunk<N, TAU, true, !AGG, kLoadStream, IO>(a, w.bb, w.hh, lc < w.nc ? w.c0 + lc : a.C, lane, act, q);
     };
     bool bad = false;
@@ -1054,20 +1096,20 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
         if (wv == W) {
             Work wr = w;
             wr.nc = runs;
-            fwd_frontier<N, W, G, FB, true>(a, s, wr);
+            fwd_frontier<N, W, G, FB, true, E>(a, s, wr);
             return;
         }
         if (wv >= runs) return;
         const int r0 = wv * per, r1 = min(w.nc, r0 + per);
-        RunState<SL> rs;
+        RunState<SL, E> rs;
 #pragma unroll
         for (int r = 0; r < SL; ++r) {
             rs.pm.v[r] = lane * SL + r;
-            rs.dm.v[r] = make_float2(1.f, 0.f);
-            rs.Bm.v[r] = make_float2(0.f, 0.f);
+            rs.dm.v[r] = eone<E>();
+            rs.Bm.v[r] = ezero<E>();
         }
         if constexpr (PREFETCH) {
-            Chunk<N, TAU> qa, qb;
+            Chunk<N, TAU, E> qa, qb;
             issue(r0, qa);
             for (int lc = r0; lc < r1; lc += 2) {
                 issue(lc + 1 < r1 ? lc + 1 : w.nc, qb);
@@ -1080,7 +1122,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
             }
         } else {
             for (int lc = r0; lc < r1; ++lc) {
-                Chunk<N, TAU> q;
+                Chunk<N, TAU, E> q;
                 issue(lc, q);
                 fwd_chunk<N, TAU, W, G, FB, true, true>(a, s, w, lc, q, bad, &rs);
             }
@@ -1090,13 +1132,13 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
         return;
     }
     if (wv == W) {
-        fwd_frontier<N, W, G, FB, AGG>(a, s, w);
+        fwd_frontier<N, W, G, FB, AGG, E>(a, s, w);
         return;
     }
     const int WA = active_waves<W>(w);
     if (wv >= WA) return;
     if constexpr (PREFETCH) {
-        Chunk<N, TAU> qa, qb;
+        Chunk<N, TAU, E> qa, qb;
         issue(wv, qa);
         for (int lc = wv; lc < w.nc; lc += 2 * WA) {
             issue(lc + WA, qb);
@@ -1109,7 +1151,7 @@ __device__ __forceinline__ void fwd_body(const FusedArgs& a, const Smem& s, cons
         }
     } else {
         for (int lc = wv; lc < w.nc; lc += WA) {
-            Chunk<N, TAU> q;
+            Chunk<N, TAU, E> q;
             issue(lc, q);
             fwd_chunk<N, TAU, W, G, FB, AGG>(a, s, w, lc, q, bad);
         }
@@ -1136,7 +1178,7 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     w.wa = narrow ? kPermWaves : W;
     w.sbm = narrow ? a.sbM_perm : a.sbM;
     if (narrow) s = carve_smem(lds, a.lds_perm);
-    clear_zero_rows<N>(s, w.wa);
+    clear_zero_rows<N, typename ElemOf<IO>::T>(s, w.wa);
     if (threadIdx.x == 0) {
         *s.ready = 0;
         *s.prog = 0;
@@ -1168,16 +1210,18 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
 // ================================================================== backward
 // The backward streams its inputs and its gradient rows (each byte is read
 // or written once): nontemporal loads and stores.
-template <int SL>
-__device__ __forceinline__ void st_out(float2* row, int lane, const CV<SL>& x) {
-    st_cv_stream<SL>(row, lane, x);
+template <int IO, int SL, class E>
+__device__ __forceinline__ void st_out(void* rows, size_t off, int lane, const CV<SL, E>& x) {
+    if constexpr (IO == kIoReal) st_row_r_stream<SL>(reinterpret_cast<float*>(rows) + off, lane, x);
+    else if constexpr (IO == kIoBf16) st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(rows) + off, lane, x);
+    else st_cv_stream<SL>(reinterpret_cast<float2*>(rows) + off, lane, x);
 }
 // Per-chunk registers of the backward: the chunk's rows, the saved state
 // entering it and its dy values (lane t holds dy of step t).
-template <int N, int TAU>
+template <int N, int TAU, class E>
 struct BwdChunk {
-    Chunk<N, TAU> q;
-    CV<Lay<N>::SL> hs;
+    Chunk<N, TAU, E> q;
+    CV<Lay<N>::SL, E> hs;
     float dyv;
 };
 
@@ -1186,7 +1230,8 @@ struct BwdChunk {
 // does.  The aggregate pass needs neither b nor the saved states.
 template <int N, int TAU, bool AGG, int IO>
 __device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int r, int lane, bool act,
-                                          BwdChunk<N, TAU>& u) {
+                                          BwdChunk<N, TAU, typename ElemOf<IO>::T>& u) {
+    using E = typename ElemOf<IO>::T;
     constexpr int SL = Lay<N>::SL;
     const int ch = r < w.nc ? w.c0 + w.nc - 1 - r : a.C;
     issue_chunk<N, TAU, !AGG, true, kLoadStream, IO>(a, w.bb, w.hh, ch, lane, act, u.q);
@@ -1194,36 +1239,39 @@ __device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int
     const int s0 = chc * TAU;
     const int lenc = min(TAU, a.L - s0);
     u.dyv = a.dy[((size_t)w.bb * a.L + s0 + min(lane, lenc - 1)) * a.H + w.hh];
-    if constexpr (!AGG) u.hs = act ? ld_cv<SL>(a.saved + ((size_t)w.seq * a.C + chc) * N, lane) : cv_zero<SL>();
+    if constexpr (!AGG)
+        u.hs = act ? ld_state<E, SL>(a.saved + ((size_t)w.seq * a.C + chc) * N, lane) : cv_zero<SL, E>();
 }
 
 // AGG: the aggregate pass of a segment -- each chunk's adjoint operator is
 // composed into the running aggregate passed from wave to wave.
 template <int N, int TAU, int W, int G, bool FB, bool AGG, bool STE, int IO>
 __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, const Work& w, int r,
-                                          BwdChunk<N, TAU>& u, bool& bad) {
+                                          BwdChunk<N, TAU, typename ElemOf<IO>::T>& u, bool& bad) {
+    using E = typename ElemOf<IO>::T;
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
-    const Stage st = stage_of<N>(s, wv);
+    const Stage<E> st = stage_of<N, E>(s, wv);
+    E* ringe = reinterpret_cast<E*>(s.ring);
     uint8_t* PA = s.pa + wv * N;
     const size_t stride = (size_t)a.H * N;
     const int ch = w.c0 + w.nc - 1 - r;
     const int s0 = ch * TAU;
     const size_t base = (((size_t)w.bb * a.L + s0) * a.H + w.hh) * N;
     const int seq = w.seq;
-    Chunk<N, TAU>& q = u.q;
+    Chunk<N, TAU, E>& q = u.q;
     finish_chunk<N, TAU>(a, s, lane, q, bad);
     const float dyv = lane < q.len ? u.dyv : 0.f;
 
     // ---- local adjoint from zero and the chunk operator, reverse time:
     // Phi <- Phi A_t: pa(j) <- pa[pi_t(j)], da(j) <- da[pi_t(j)] D_t(j)
-    CV<SL> g = cv_zero<SL>(), da;
+    CV<SL, E> g = cv_zero<SL, E>(), da;
     IV<SL> pa;
 #pragma unroll
     for (int i = 0; i < SL; ++i) {
         pa.v[i] = lane * SL + i;
-        da.v[i] = make_float2(1.f, 0.f);
+        da.v[i] = eone<E>();
     }
 #pragma unroll
     for (int t = TAU - 1; t >= 0; --t) {
@@ -1235,8 +1283,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
                 pt.v[i] = s.dict[k * N + lane * SL + i];
-                g.v[i].x += dyt * q.c[t].v[i].x;
-                g.v[i].y -= dyt * q.c[t].v[i].y;
+                g.v[i] = add_sconj(g.v[i], dyt, q.c[t].v[i]);
                 st.V[lane * SL + i] = g.v[i];
                 st.Z[lane * SL + i] = da.v[i];
                 PA[lane * SL + i] = (uint8_t)pa.v[i];
@@ -1246,7 +1293,7 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
         if (act) {
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
-                const float2 gv = st.V[pt.v[i]], dz = st.Z[pt.v[i]];
+                const E gv = st.V[pt.v[i]], dz = st.Z[pt.v[i]];
                 pa.v[i] = PA[pt.v[i]];
                 da.v[i] = cmul(dz, Dt(q, t).v[i]);
                 g.v[i] = cmulc(Dt(q, t).v[i], gv);
@@ -1258,31 +1305,29 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
 #pragma unroll
     for (int i = 0; i < SL; ++i) {
         materialize(pa.v[i]);
-        materialize(da.v[i].x);
-        materialize(da.v[i].y);
-        materialize(g.v[i].x);
-        materialize(g.v[i].y);
+        materialize(da.v[i]);
+        materialize(g.v[i]);
     }
     wait_ready(s.ready, r, a.status, s.ready, 1, s.prog);
     if constexpr (AGG) {
         // (Gamma, Pi, Delta)_acc <- (gamma_c + Phi_c^H Gamma_acc, Pi_acc[Pi_c], Delta_acc[Pi_c] Delta_c):
         // the aggregate of chunks c .. c1-1, mapping the gradient entering
         // the segment's last chunk to the one leaving chunk c.
-        const float2* GA = s.ring + (r & 1) * N;
-        const float2* DA = s.ring + (2 + (r & 1)) * N;
+        const E* GA = ringe + (r & 1) * N;
+        const E* DA = ringe + (2 + (r & 1)) * N;
         const uint8_t* PAc = s.agp + (r & 1) * N;
-        CV<SL> Gn, Dn;
+        CV<SL, E> Gn, Dn;
         IV<SL> Pn;
         if (act) {
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
                 const int p = pa.v[i];
-                Gn.v[i] = cadd(g.v[i], cmulc(da.v[i], GA[p]));
+                Gn.v[i] = cfmac(g.v[i], da.v[i], GA[p]);
                 Dn.v[i] = cmul(DA[p], da.v[i]);
                 Pn.v[i] = PAc[p];
             }
-            st_cv<SL>(s.ring + ((r + 1) & 1) * N, lane, Gn);
-            st_cv<SL>(s.ring + (2 + ((r + 1) & 1)) * N, lane, Dn);
+            st_cv<SL>(ringe + ((r + 1) & 1) * N, lane, Gn);
+            st_cv<SL>(ringe + (2 + ((r + 1) & 1)) * N, lane, Dn);
 #pragma unroll
             for (int i = 0; i < SL; ++i) s.agp[((r + 1) & 1) * N + lane * SL + i] = (uint8_t)Pn.v[i];
         }
@@ -1290,27 +1335,27 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
         if (lane == 0) publish_ready(s.ready, r + 1);
         if (r == w.nc - 1 && act) {
             const size_t sb = ((size_t)seq * a.S + w.sg) * N;
-            st_cv<SL>(a.segA + sb, lane, Gn);
-            st_cv<SL>(a.segD + sb, lane, Dn);
+            st_state<SL>(a.segA + sb, lane, Gn);
+            st_state<SL>(a.segD + sb, lane, Dn);
             st_iv<SL>(a.segP + sb, lane, Pn);
         }
         return;
     }
-    CV<SL> U = cv_zero<SL>(), Up;
+    CV<SL, E> U = cv_zero<SL, E>(), Up;
     if (act) {
-        const float2* ring = s.ring + (r & 1) * N;
+        const E* ring = ringe + (r & 1) * N;
         U = ld_cv<SL>(ring, lane);
 #pragma unroll
-        for (int i = 0; i < SL; ++i) Up.v[i] = cadd(g.v[i], cmulc(da.v[i], ring[pa.v[i]]));
-        st_cv<SL>(s.ring + ((r + 1) & 1) * N, lane, Up);
+        for (int i = 0; i < SL; ++i) Up.v[i] = cfmac(g.v[i], da.v[i], ring[pa.v[i]]);
+        st_cv<SL>(ringe + ((r + 1) & 1) * N, lane, Up);
     }
     wave_sync();
     if (lane == 0) publish_ready(s.ready, r + 1);
-    if (ch == 0 && a.dh0 && act) st_cv<SL>(a.dh0 + (size_t)seq * N, lane, Up);
+    if (ch == 0 && a.dh0 && act) st_state<SL>(a.dh0 + (size_t)seq * N, lane, Up);
 
     // ---- recompute the chunk's states from the saved entering state
-    CV<SL> Hs[TAU + 1];
-    CV<SL> hs = u.hs;
+    CV<SL, E> Hs[TAU + 1];
+    CV<SL, E> hs = u.hs;
     Hs[0] = hs;
 #pragma unroll
     for (int t = 0; t < TAU; ++t) {
@@ -1327,51 +1372,41 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
         const int k = readlane_i(q.kv, t);
         const float dyt = readlane_f(dyv, t);
         IV<SL> pt;
-        CV<SL> dct;
+        CV<SL, E> dct;
         wave_sync();
         if (act) {
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
                 pt.v[i] = s.dict[k * N + lane * SL + i];
-                g.v[i].x += dyt * q.c[t].v[i].x;
-                g.v[i].y -= dyt * q.c[t].v[i].y;
-                dct.v[i] = make_float2(dyt * Hs[t + 1].v[i].x, -dyt * Hs[t + 1].v[i].y);
+                g.v[i] = add_sconj(g.v[i], dyt, q.c[t].v[i]);
+                dct.v[i] = sconj(dyt, Hs[t + 1].v[i]);
                 st.V[lane * SL + i] = g.v[i];
             }
         }
         const bool in = t < q.len;
         const size_t off = base + (size_t)t * stride;
         if (act && in) {
-            if constexpr (IO != kIoC64) {
-                st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.db) + off, lane, g);
-                st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.dc) + off, lane, dct);
-            } else {
-                st_out<SL>(a.db + off, lane, g);
-                st_out<SL>(a.dc + off, lane, dct);
-            }
+            st_out<IO, SL>(a.db, off, lane, g);
+            st_out<IO, SL>(a.dc, off, lane, dct);
         }
         wave_sync();
         if (act) {
-            CV<SL> dDt;
+            CV<SL, E> dDt;
 #pragma unroll
             for (int i = 0; i < SL; ++i) {
-                const float2 gp = st.V[pt.v[i]];
+                const E gp = st.V[pt.v[i]];
                 dDt.v[i] = cmulc(Hs[t].v[i], gp);
                 g.v[i] = cmulc(Dt(q, t).v[i], gp);
             }
-            if (in) {
-                if constexpr (IO != kIoC64) st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.dD) + off, lane, dDt);
-                else st_out<SL>(a.dD + off, lane, dDt);
-            }
+            if (in) st_out<IO, SL>(a.dD, off, lane, dDt);
         }
         if constexpr (STE) {
             // the scaled state z_t = D_t .* h_{t-1} for the straight-through gradients
             if (act && in) {
-                CV<SL> zt;
+                CV<SL, E> zt;
 #pragma unroll
                 for (int i = 0; i < SL; ++i) zt.v[i] = cmul(Dt(q, t).v[i], Hs[t].v[i]);
-                if constexpr (IO != kIoC64) st_row_w_stream<SL, IO>(reinterpret_cast<uint32_t*>(a.z) + off, lane, zt);
-                else st_out<SL>(a.z + off, lane, zt);
+                st_out<IO, SL>(a.z, off, lane, zt);
             }
         }
     }
@@ -1381,12 +1416,13 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
 // load of its next chunk is in flight while it computes the current one.
 template <int N, int TAU, int W, int G, bool FB, bool PREFETCH, bool AGG, bool STE, int IO>
 __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, const Work& w) {
+    using E = typename ElemOf<IO>::T;
     constexpr int LANES = Lay<N>::LANES;
     const int wv = wave_id(), lane = lane_id();
     const bool act = lane < LANES;
     bool bad = false;
     if constexpr (PREFETCH) {
-        BwdChunk<N, TAU> ua, ub;
+        BwdChunk<N, TAU, E> ua, ub;
         issue_bwd<N, TAU, AGG, IO>(a, w, wv, lane, act, ua);
         for (int r = wv; r < w.nc; r += 2 * W) {
             issue_bwd<N, TAU, AGG, IO>(a, w, r + W, lane, act, ub);
@@ -1399,7 +1435,7 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, cons
         }
     } else {
         for (int r = wv; r < w.nc; r += W) {
-            BwdChunk<N, TAU> u;
+            BwdChunk<N, TAU, E> u;
             issue_bwd<N, TAU, AGG, IO>(a, w, r, lane, act, u);
             bwd_chunk<N, TAU, W, G, FB, AGG, STE, IO>(a, s, w, r, u, bad);
         }
@@ -1410,24 +1446,24 @@ __device__ __forceinline__ void bwd_body(const FusedArgs& a, const Smem& s, cons
 // The gradient entering segment w.sg from the right: dh_final (or 0) pulled
 // back through the aggregates of segments S-1 .. w.sg+1,
 // U <- Gamma_s + Phi_s^H U (a gather through the wave's LDS buffer X).
-template <int N>
-__device__ __forceinline__ CV<Lay<N>::SL> seg_enter_bwd(const FusedArgs& a, const Work& w, float2* X, int lane,
-                                                        bool act) {
+template <int N, class E>
+__device__ __forceinline__ CV<Lay<N>::SL, E> seg_enter_bwd(const FusedArgs& a, const Work& w, E* X, int lane,
+                                                           bool act) {
     constexpr int SL = Lay<N>::SL;
-    CV<SL> U = cv_zero<SL>();
-    if (a.dhf && act) U = ld_cv<SL>(a.dhf + (size_t)w.seq * N, lane);
+    CV<SL, E> U = cv_zero<SL, E>();
+    if (a.dhf && act) U = ld_state<E, SL>(a.dhf + (size_t)w.seq * N, lane);
     for (int sp = a.S - 1; sp > w.sg; --sp) {
         const size_t base = ((size_t)w.seq * a.S + sp) * N;
-        CV<SL> Un = cv_zero<SL>();
+        CV<SL, E> Un = cv_zero<SL, E>();
         wave_sync();
         if (act) st_cv<SL>(X, lane, U);
         wave_sync();
         if (act) {
-            const CV<SL> G = ld_cv<SL>(a.segA + base, lane);
-            const CV<SL> d = ld_cv<SL>(a.segD + base, lane);
+            const CV<SL, E> G = ld_state<E, SL>(a.segA + base, lane);
+            const CV<SL, E> d = ld_state<E, SL>(a.segD + base, lane);
             const IV<SL> P = ld_iv<SL>(a.segP + base, lane);
 #pragma unroll
-            for (int i = 0; i < SL; ++i) Un.v[i] = cadd(G.v[i], cmulc(d.v[i], X[P.v[i]]));
+            for (int i = 0; i < SL; ++i) Un.v[i] = cfmac(G.v[i], d.v[i], X[P.v[i]]);
         }
         U = Un;
     }
@@ -1436,6 +1472,7 @@ __device__ __forceinline__ CV<Lay<N>::SL> seg_enter_bwd(const FusedArgs& a, cons
 
 template <int N, int TAU, int W, bool AGG, bool STE, int IO>
 __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
+    using E = typename ElemOf<IO>::T;
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
     extern __shared__ __align__(16) unsigned char lds[];
     const Smem s = carve_smem(lds, a.lds);
@@ -1444,23 +1481,24 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     const Work w = AGG ? work_of(a, a.S - 1, 1) : work_of(a, a.S, 0);
 
     stage_tables<N>(a, s, w.hh);
-    clear_zero_rows<N>(s, W);
+    clear_zero_rows<N, E>(s, W);
+    E* ring = reinterpret_cast<E*>(s.ring);
     if (wv == 0) {
         if constexpr (AGG) {
             // identity aggregate: Gamma = 0, Pi = id, Delta = 1
             if (act) {
-                st_cv<SL>(s.ring, lane, cv_zero<SL>());
-                CV<SL> one;
+                st_cv<SL>(ring, lane, cv_zero<SL, E>());
+                CV<SL, E> one;
 #pragma unroll
                 for (int i = 0; i < SL; ++i) {
-                    one.v[i] = make_float2(1.f, 0.f);
+                    one.v[i] = eone<E>();
                     s.agp[lane * SL + i] = (uint8_t)(lane * SL + i);
                 }
-                st_cv<SL>(s.ring + 2 * N, lane, one);
+                st_cv<SL>(ring + 2 * N, lane, one);
             }
         } else {
-            const CV<SL> u = seg_enter_bwd<N>(a, w, s.x, lane, act);
-            if (act) st_cv<SL>(s.ring, lane, u);
+            const CV<SL, E> u = seg_enter_bwd<N, E>(a, w, reinterpret_cast<E*>(s.x), lane, act);
+            if (act) st_cv<SL>(ring, lane, u);
         }
         if (lane == 0) {
             *s.ready = 0;
@@ -1516,24 +1554,32 @@ hipError_t bwd_launch_io(const FusedArgs& a, hipStream_t st) {
     return hipGetLastError();
 }
 
-// the row format (complex64, bf16 pairs, real fp32) picks the instantiation
-template <int N, int TAU, int W>
-hipError_t fwd_launch(const FusedArgs& a, hipStream_t st) {
-    switch (a.io) {
-        case kIoC64: return fwd_launch_io<N, TAU, W, kIoC64>(a, st);
-        case kIoBf16: return fwd_launch_io<N, TAU, W, kIoBf16>(a, st);
-        case kIoReal: return fwd_launch_io<N, TAU, W, kIoReal>(a, st);
-        default: return hipErrorInvalidValue;
+// The chunk-wave count of a call: fused_waves(N, TAU), or kFusedWavesWide
+// for the prefetching kernels when the caller's layout was built for it, or
+// at N = 256 kFusedWavesNarrow / kFusedWavesNarrowest.
+template <int N, int TAU, int IO>
+hipError_t fwd_dispatch_io(const FusedArgs& a, hipStream_t st) {
+    if constexpr (fused_prefetch(N, TAU)) {
+        if (a.W == kFusedWavesWide) return fwd_launch_io<N, TAU, kFusedWavesWide, IO>(a, st);
     }
+    if constexpr (N == 256) {
+        if (a.W == kFusedWavesNarrow) return fwd_launch_io<N, TAU, kFusedWavesNarrow, IO>(a, st);
+        if (a.W == kFusedWavesNarrowest) return fwd_launch_io<N, TAU, kFusedWavesNarrowest, IO>(a, st);
+    }
+    if (a.W != fused_waves(N, TAU)) return hipErrorInvalidValue;
+    return fwd_launch_io<N, TAU, fused_waves(N, TAU), IO>(a, st);
 }
-template <int N, int TAU, int W>
-hipError_t bwd_launch(const FusedArgs& a, hipStream_t st) {
-    switch (a.io) {
-        case kIoC64: return bwd_launch_io<N, TAU, W, kIoC64>(a, st);
-        case kIoBf16: return bwd_launch_io<N, TAU, W, kIoBf16>(a, st);
-        case kIoReal: return bwd_launch_io<N, TAU, W, kIoReal>(a, st);
-        default: return hipErrorInvalidValue;
+
+// The backward's: fused_waves_bwd(N, TAU), or at N = 256 kFusedWavesNarrow
+// or kFusedWavesNarrowest.
+template <int N, int TAU, int IO>
+hipError_t bwd_dispatch_io(const FusedArgs& a, hipStream_t st) {
+    if constexpr (N == 256) {
+        if (a.W == kFusedWavesNarrow) return bwd_launch_io<N, TAU, kFusedWavesNarrow, IO>(a, st);
+        if (a.W == kFusedWavesNarrowest) return bwd_launch_io<N, TAU, kFusedWavesNarrowest, IO>(a, st);
     }
+    if (a.W != fused_waves_bwd(N, TAU)) return hipErrorInvalidValue;
+    return bwd_launch_io<N, TAU, fused_waves_bwd(N, TAU), IO>(a, st);
 }
 
 template <int N>
@@ -1542,33 +1588,26 @@ hipError_t prep_launch(const PrepArgs& p, hipStream_t st) {
     return hipGetLastError();
 }
 
+// The row format (complex64, bf16 pairs, real fp32) picks the instantiation.
 // Chunk lengths compiled per N: TAU * max(1, N/64) <= 16 keeps a chunk's
 // D, b, c rows (and the backward's recomputed states) in registers.
-// The forward's chunk-wave count: fused_waves(N, TAU), or kFusedWavesWide
-// for the prefetching kernels when the caller's layout was built for it.
 template <int N, int TAU>
 hipError_t fwd_dispatch_waves(const FusedArgs& a, hipStream_t st) {
-    if constexpr (fused_prefetch(N, TAU)) {
-        if (a.W == kFusedWavesWide) return fwd_launch<N, TAU, kFusedWavesWide>(a, st);
+    switch (a.io) {
+        case kIoC64: return fwd_dispatch_io<N, TAU, kIoC64>(a, st);
+        case kIoBf16: return fwd_dispatch_io<N, TAU, kIoBf16>(a, st);
+        case kIoReal: return fwd_dispatch_io<N, TAU, kIoReal>(a, st);
+        default: return hipErrorInvalidValue;
     }
-    if constexpr (N == 256) {
-        if (a.W == kFusedWavesNarrow) return fwd_launch<N, TAU, kFusedWavesNarrow>(a, st);
-        if (a.W == kFusedWavesNarrowest) return fwd_launch<N, TAU, kFusedWavesNarrowest>(a, st);
-    }
-    if (a.W != fused_waves(N, TAU)) return hipErrorInvalidValue;
-    return fwd_launch<N, TAU, fused_waves(N, TAU)>(a, st);
 }
-
-// The backward's: fused_waves_bwd(N, TAU), or at N = 256 kFusedWavesNarrow or
-// kFusedWavesNarrowest.
 template <int N, int TAU>
 hipError_t bwd_dispatch_waves(const FusedArgs& a, hipStream_t st) {
-    if constexpr (N == 256) {
-        if (a.W == kFusedWavesNarrow) return bwd_launch<N, TAU, kFusedWavesNarrow>(a, st);
-        if (a.W == kFusedWavesNarrowest) return bwd_launch<N, TAU, kFusedWavesNarrowest>(a, st);
+    switch (a.io) {
+        case kIoC64: return bwd_dispatch_io<N, TAU, kIoC64>(a, st);
+        case kIoBf16: return bwd_dispatch_io<N, TAU, kIoBf16>(a, st);
+        case kIoReal: return bwd_dispatch_io<N, TAU, kIoReal>(a, st);
+        default: return hipErrorInvalidValue;
     }
-    if (a.W != fused_waves_bwd(N, TAU)) return hipErrorInvalidValue;
-    return bwd_launch<N, TAU, fused_waves_bwd(N, TAU)>(a, st);
 }
 
 template <int N, bool FWD>
