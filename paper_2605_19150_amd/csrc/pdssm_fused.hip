@@ -741,113 +741,129 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     }
     CV<SL, E> wt[TAU];
     float yl[TAU];
-    if constexpr (!FB && Sentinel<N>::kZeroRow) {
-        // Pipelined form: every step's gather records are read at chunk start;
-        // step t then issues one batch of LDS reads -- its gathers, D_t and
-        // pi_t at Pi_{t-1}, and c_{t-1} at Pi_{t-1} for w_{t-1} (c staged in
-        // two alternating buffers) -- so each step waits for one round trip.
-        // (Heads with entries in sorted form take the step-by-step form
-        // below: their steps in this pass measured 13% slower at N = 128,
-        // hybrid-lm 622 -> 703 us, and no faster at N = 64.)
-        uint64_t rec[TAU][SL];
+    // Pipelined form (no step of the chunk may use a sorted-form entry):
+    // every step's gather records are read at chunk start; step t then issues
+    // one batch of LDS reads -- its gathers, D_t and pi_t at Pi_{t-1}, and
+    // c_{t-1} at Pi_{t-1} for w_{t-1} (c staged in two alternating buffers)
+    // -- so each step waits for one round trip.  Otherwise the step-by-step
+    // form, where each step waits for its own writes and reads.
+    //
+    // With real elements a head with sorted-form entries runs the pipelined
+    // pass on every chunk none of whose steps uses one (one ballot over the
+    // steps' classes per chunk; measured hybrid-lm 413.7 -> 385.7 us, within
+    // 1% of the same maps without the entry).  With complex elements the two
+    // passes in one kernel cost registers (measured: hybrid-lm in bf16 pairs
+    // 580 -> 1209 us), so those heads keep the step-by-step form; a per-step
+    // test inside the pipelined pass measured 13% slower at N = 128.
+    constexpr bool kPipe = Sentinel<N>::kZeroRow && (!FB || sizeof(E) == sizeof(float));
+    constexpr bool kStep = FB || !Sentinel<N>::kZeroRow;
+    bool pipe = kPipe && !FB;
+    if constexpr (kPipe && FB) pipe = __builtin_amdgcn_ballot_w64(q.mv == (int)kFallback) == 0;
+    if constexpr (kPipe) {
+        if (pipe) {
+            uint64_t rec[TAU][SL];
 #pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t);
+            for (int t = 0; t < TAU; ++t) {
+                const int k = readlane_i(q.kv, t);
 #pragma unroll
-            for (int r = 0; r < SL; ++r) rec[t][r] = act ? s.rec[(size_t)k * N + lane * SL + r] : 0;
-        }
-#pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t), gk = readlane_i(q.mv, t);
-            E* CSt = CS + (t & 1) * csb;
-            const E* CSp = CS + ((t + 1) & 1) * csb;
-            const CV<SL, E> Dv = Dt(q, t);
-            wave_sync();
-            if (act) {
-#pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
-                    st.V[lane * SL + r] = cmul(Dv.v[r], Bm.v[r]);
-                    st.Z[lane * SL + r] = Dv.v[r];
-                }
+                for (int r = 0; r < SL; ++r) rec[t][r] = act ? s.rec[(size_t)k * N + lane * SL + r] : 0;
             }
-            wave_sync();
-            float part = 0.f;
-            if (act) {
-                // the first GM sources of every row with the step's other
-                // reads in one batch; the 7-source class reads the rest only
-                // at steps whose map has a row with more than GM sources
-                constexpr int GM = G > 4 ? 4 : G;
-                E acc[SL], Dp[SL], Cp[SL];
-                int np[SL];
 #pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    acc[r] = q.b[t].v[r];
-                    gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
-                    const int p = pm.v[r];
-                    Dp[r] = st.Z[p];
-                    np[r] = s.dict[k * N + p];
-                    if constexpr (!AGG) Cp[r] = CSp[p];
-                }
-                if constexpr (G > GM) {
-                    if (gk > GM) {
-#pragma unroll
-                        for (int r = 0; r < SL; ++r) gather_rec_range<GM, G>(st.V, rec[t][r], acc[r]);
-                    }
-                }
-#pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    if constexpr (!AGG) {
-                        if (t > 0) wt[t - 1].v[r] = cmul(dm.v[r], Cp[r]);
-                    }
-                    Bm.v[r] = acc[r];
-                    dm.v[r] = cmul(Dp[r], dm.v[r]);
-                    pm.v[r] = np[r];
-                    if constexpr (!AGG) part = re_fma(part, q.c[t].v[r], Bm.v[r]);
-                }
-            } else if constexpr (!AGG) {
-                if (t > 0) wt[t - 1] = cv_zero<SL, E>();
-            }
-            yl[t] = part;
-        }
-        if constexpr (!AGG) {
-            const E* CSl = CS + ((TAU - 1) & 1) * csb;
-            wave_sync();
-            if (act) {
-#pragma unroll
-                for (int r = 0; r < SL; ++r) wt[TAU - 1].v[r] = cmul(dm.v[r], CSl[pm.v[r]]);
-            } else {
-                wt[TAU - 1] = cv_zero<SL, E>();
-            }
-        }
-    } else {
-#pragma unroll
-        for (int t = 0; t < TAU; ++t) {
-            const int k = readlane_i(q.kv, t);
-            const int M = readlane_i(q.mv, t);
-            if (!AGG && act) {
+            for (int t = 0; t < TAU; ++t) {
+                const int k = readlane_i(q.kv, t), gk = readlane_i(q.mv, t);
+                E* CSt = CS + (t & 1) * csb;
+                const E* CSp = CS + ((t + 1) & 1) * csb;
+                const CV<SL, E> Dv = Dt(q, t);
                 wave_sync();
+                if (act) {
 #pragma unroll
-                for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
-            }
-            pd_step<N, G, FB, true>(s, st, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
-            float part = 0.f;
-            if (act) {
-#pragma unroll
-                for (int r = 0; r < SL; ++r) {
-                    // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in Z
-                    const int p = pm.v[r];
-                    dm.v[r] = cmul(st.Z[p], dm.v[r]);
-                    pm.v[r] = s.dict[k * N + p];
-                    if constexpr (!AGG) {
-                        wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
-                        part = re_fma(part, q.c[t].v[r], Bm.v[r]);
+                    for (int r = 0; r < SL; ++r) {
+                        if constexpr (!AGG) CSt[lane * SL + r] = q.c[t].v[r];
+                        st.V[lane * SL + r] = cmul(Dv.v[r], Bm.v[r]);
+                        st.Z[lane * SL + r] = Dv.v[r];
                     }
                 }
-            } else if constexpr (!AGG) {
-                wt[t] = cv_zero<SL, E>();
+                wave_sync();
+                float part = 0.f;
+                if (act) {
+                    // the first GM sources of every row with the step's other
+                    // reads in one batch; the 7-source class reads the rest only
+                    // at steps whose map has a row with more than GM sources
+                    constexpr int GM = G > 4 ? 4 : G;
+                    E acc[SL], Dp[SL], Cp[SL];
+                    int np[SL];
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) {
+                        acc[r] = q.b[t].v[r];
+                        gather_rec_range<0, GM>(st.V, rec[t][r], acc[r]);
+                        const int p = pm.v[r];
+                        Dp[r] = st.Z[p];
+                        np[r] = s.dict[k * N + p];
+                        if constexpr (!AGG) Cp[r] = CSp[p];
+                    }
+                    if constexpr (G > GM) {
+                        if (gk > GM) {
+#pragma unroll
+                            for (int r = 0; r < SL; ++r) gather_rec_range<GM, G>(st.V, rec[t][r], acc[r]);
+                        }
+                    }
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) {
+                        if constexpr (!AGG) {
+                            if (t > 0) wt[t - 1].v[r] = cmul(dm.v[r], Cp[r]);
+                        }
+                        Bm.v[r] = acc[r];
+                        dm.v[r] = cmul(Dp[r], dm.v[r]);
+                        pm.v[r] = np[r];
+                        if constexpr (!AGG) part = re_fma(part, q.c[t].v[r], Bm.v[r]);
+                    }
+                } else if constexpr (!AGG) {
+                    if (t > 0) wt[t - 1] = cv_zero<SL, E>();
+                }
+                yl[t] = part;
             }
-            yl[t] = part;
+            if constexpr (!AGG) {
+                const E* CSl = CS + ((TAU - 1) & 1) * csb;
+                wave_sync();
+                if (act) {
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) wt[TAU - 1].v[r] = cmul(dm.v[r], CSl[pm.v[r]]);
+                } else {
+                    wt[TAU - 1] = cv_zero<SL, E>();
+                }
+            }
+        }
+    }
+    if constexpr (kStep) {
+        if (!pipe) {
+#pragma unroll
+            for (int t = 0; t < TAU; ++t) {
+                const int k = readlane_i(q.kv, t);
+                const int M = readlane_i(q.mv, t);
+                if (!AGG && act) {
+                    wave_sync();
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) CS[lane * SL + r] = q.c[t].v[r];
+                }
+                pd_step<N, G, FB, true>(s, st, lane, act, k, M, Bm, Dt(q, t), q.b[t]);
+                float part = 0.f;
+                if (act) {
+#pragma unroll
+                    for (int r = 0; r < SL; ++r) {
+                        // (Pi, Delta) <- (pi_t[Pi], D_t[Pi] * Delta), D_t staged in Z
+                        const int p = pm.v[r];
+                        dm.v[r] = cmul(st.Z[p], dm.v[r]);
+                        pm.v[r] = s.dict[k * N + p];
+                        if constexpr (!AGG) {
+                            wt[t].v[r] = cmul(dm.v[r], CS[pm.v[r]]);
+                            part = re_fma(part, q.c[t].v[r], Bm.v[r]);
+                        }
+                    }
+                } else if constexpr (!AGG) {
+                    wt[t] = cv_zero<SL, E>();
+                }
+                yl[t] = part;
+            }
         }
     }
 
