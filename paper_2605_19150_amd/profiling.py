@@ -204,6 +204,9 @@ def read_traffic_summary(profiles_dir, kernel, workload):
                 if ": " in line and not line.startswith(("#", " ", "|")):
                     k, v = line.rstrip("\n").split(": ", 1)
                     kv[k.strip()] = v.strip()
+        # traffic summaries only (counter summaries name the same kernel)
+        if "traffic-bytes-per-launch" not in kv:
+            continue
         if kv.get("kernel") == kernel and kv.get("workload") == workload:
             if kv.get("source-hash") != want:
                 return None
