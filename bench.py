@@ -589,6 +589,9 @@ def scan_line(args, w, res):
         out["roofline"]["frac"] = out["roofline"]["achieved"] / HBM_PEAK_GBS
         out["roofline"]["traffic"] = traffic_from_profiles("k_bwd_fused_ste" + suffix, w.name) if fused else None
         out["roofline"]["kernel"] = kern[dom] + (" (+ z)" if dom == "bwd" else "")
+        if dom == "bwd":
+            out["roofline"]["bytes"] = ("algorithmic: idx, dy, D, b, c in; dD, db, dc, z, dh0 out "
+                                        "(%.1f + 8/N bytes per state update)" % (56.0 * esz / 8))
         dg_ms, sm_ms = mean("ste_grads"), mean("softmax")
         gbps = sb["ste_grads"] / (dg_ms * 1e-3) / 1e9
         tfs = sb["ste_grads_flops"] / (dg_ms * 1e-3) / 1e12
