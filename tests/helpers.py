@@ -62,3 +62,18 @@ def ste_scales(pi, idx, g, z):
             if m.any():
                 Gs[h, k] = ag[:, :, h][m].T @ az[:, :, h][m]
     return qs, Gs
+
+
+def force_sorted_entries(inp, N):
+    """Entries with a row of more than seven sources (stored in sorted form):
+    in-degree exactly 8 in head 0, all-to-one in head 1, two rows of 12 and
+    9 sources in head 2 (if present); steps choose them often, and the other
+    entries of those heads keep their maps."""
+    H, K = inp["pi"].shape[:2]
+    inp["pi"][0, 1, :8] = 5
+    inp["pi"][1 % H, 0, :] = N - 1
+    if H > 2:
+        inp["pi"][2, 3, :12] = 0
+        inp["pi"][2, 3, 12:21] = N // 2
+    inp["idx"][:, ::2, 0] = 1
+    inp["idx"][:, 1::3, 1 % H] = 0

@@ -7,7 +7,7 @@ composed integer maps and the automaton case are compared bit for bit.
 import numpy as np
 import pytest
 
-from helpers import assert_close, sub_sequence
+from helpers import assert_close, force_sorted_entries, sub_sequence
 from oracle import oracle_bwd, oracle_compose, oracle_fwd
 from paper_2605_19150_amd.inputs import WORKLOADS, fsa_inputs, make_inputs, workload_inputs
 
@@ -114,20 +114,6 @@ def test_mixed_degenerate_and_regular_entries():
     check_all(inp, got, eff_chunk(inp))
 
 
-def _force_sorted_entries(inp, N):
-    """Entries with a row of more than seven sources (stored in sorted form):
-    in-degree exactly 8 in head 0, all-to-one in head 1, two rows of 12 and
-    9 sources in head 2 (if present); steps choose them often."""
-    H, K = inp["pi"].shape[:2]
-    inp["pi"][0, 1, :8] = 5
-    inp["pi"][1 % H, 0, :] = N - 1
-    if H > 2:
-        inp["pi"][2, 3, :12] = 0
-        inp["pi"][2, 3, 12:21] = N // 2
-    inp["idx"][:, ::2, 0] = 1
-    inp["idx"][:, 1::3, 1 % H] = 0
-
-
 @pytest.mark.parametrize("N,chunk", [(16, 8), (32, 16), (64, 4), (64, 8), (64, 16), (128, 4), (128, 8),
                                      (256, 4)])
 def test_sorted_form_entries(N, chunk):
@@ -135,7 +121,7 @@ def test_sorted_form_entries(N, chunk):
     ones: those steps sum each row's run by a segmented scan inside the
     pipelined chunk pass (and in the backward's state recompute)."""
     inp = make_inputs(B=2, L=300, H=3, N=N, K=6, seed=N + chunk, with_h0=True, with_dhf=True)
-    _force_sorted_entries(inp, N)
+    force_sorted_entries(inp, N)
     got = run_gpu(inp, chunk=chunk)
     check_all(inp, got, chunk)
 
@@ -309,7 +295,7 @@ def test_deterministic(N, B, L, H, K, sorted_form):
     (N = 128) and K = 64 (N = 256))."""
     inp = make_inputs(B=B, L=L, H=H, N=N, K=K, seed=5, with_h0=True, with_dhf=True)
     if sorted_form:
-        _force_sorted_entries(inp, N)
+        force_sorted_entries(inp, N)
     a = run_gpu(inp)
     b = run_gpu(inp)
     for k in a:

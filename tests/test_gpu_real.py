@@ -14,7 +14,7 @@ import ctypes
 import numpy as np
 import pytest
 
-from helpers import assert_close, assert_close_sum, ste_scales, sub_sequence
+from helpers import assert_close, assert_close_sum, force_sorted_entries, ste_scales, sub_sequence
 from oracle import oracle_bwd, oracle_fwd, oracle_ste
 from paper_2605_19150_amd.inputs import make_inputs, workload_inputs
 
@@ -106,6 +106,21 @@ def test_real_io_collisions():
     check_oracle(inp, out)
 
 
+@pytest.mark.parametrize("N,B,L", [(64, 2, 300), (128, 2, 300), (64, 1, 2600), (128, 1, 2600)])
+def test_real_io_sorted_form_mixed(N, B, L):
+    """Heads with sorted-form entries (rows of more than seven sources) next
+    to ordinary ones: with real elements their chunks take the pipelined pass
+    when no step uses such an entry and the step-by-step pass otherwise
+    (head 2 mixes both), also in the aggregate pass of segmented scans
+    (L = 2600).  Bit for bit the complex64 path, and the oracle."""
+    print("real sorted form N=%d B=%d L=%d" % (N, B, L), flush=True)
+    inp = make_inputs(B=B, L=L, H=3, N=N, K=8, seed=N + L, with_h0=True, with_dhf=True, real=True)
+    force_sorted_entries(inp, N)
+    out = run_both(inp)
+    check_bits(out)
+    check_oracle(inp, out)
+
+
 def test_real_io_segmented():
     inp = make_inputs(B=1, L=2600, H=2, N=64, K=16, seed=5, pi_kind="perm", with_h0=True, with_dhf=True,
                       real=True)
@@ -134,15 +149,25 @@ def test_real_io_module_functions():
     assert_close("dh0", dh0.cpu().numpy(), rg[3])
 
 
-@pytest.mark.parametrize("wl", [2, 4])
+# the head of markov-manyone and hybrid-lm with an entry of in-degree > 7
+SORTED_HEAD = {3: 4, 5: 18}
+
+
+@pytest.mark.parametrize("wl", [2, 3, 4, 5])
 def test_real_io_full_size(wl):
+    """Every output of the full-size workload bit for bit against complex64;
+    sampled sequences (including the head with a sorted-form entry) against
+    the oracle."""
     print("real full size workload %d" % wl, flush=True)
     inp = workload_inputs(wl, seed=0, real=True)
     out = run_both(inp)
     check_bits(out)
     r = out["real"]
     B, L, H = inp["idx"].shape
-    for bb, hh in ((0, 0), (B - 1, H - 1), (B // 2, H // 3)):
+    samples = [(0, 0), (B - 1, H - 1), (B // 2, H // 3)]
+    if wl in SORTED_HEAD:
+        samples.append((1, SORTED_HEAD[wl]))
+    for bb, hh in samples:
         sub = sub_sequence(inp, bb, hh)
         ry, rhf, _ = oracle_fwd(sub["idx"], sub["pi"], sub["D"], sub["b"], sub["c"])
         assert_close("y", r["y"][bb:bb + 1, :, hh:hh + 1].cpu().numpy(), ry)
