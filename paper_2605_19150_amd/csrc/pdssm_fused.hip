@@ -61,11 +61,16 @@ namespace {
 // ------------------------------------------------------------------ prep
 // One wave per dictionary entry (h, k): byte dictionary, per-row source
 // records, per-entry max in-degree; an entry with a row of more than kMaxSrc
-// sources gets its sorted form instead of records.
+// sources gets its sorted form instead of records.  Every source finds its
+// rank among the sources of its row (ascending source order) from lane-mask
+// tables (map_ranks), so no lane walks the whole map.
 template <int N>
 __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    __shared__ uint8_t spos[4][N], sstart[4][N];
+    __shared__ uint64_t smt[4][SL][N];  // per wave: lane-mask tables
+    __shared__ uint64_t srec[4][N];     // per wave: the records being filled
+    __shared__ int soff[4][N];          // per wave: sorted form, first position of each row's run
+    __shared__ uint8_t sst[4][N];       // per wave: sorted form, run-start flags by position
     const int wv = wave_id(), lane = lane_id();
     const int e = blockIdx.x * 4 + wv;
     if (e >= a.H * a.K) return;
@@ -80,34 +85,11 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
 #pragma unroll
         for (int s = 0; s < SL; ++s) a.dict[(size_t)e * N + lane * SL + s] = (uint8_t)p.v[s];
     }
-    // Every lane walks the sources j = 0..N-1 in ascending order (the map
-    // value of source j is read from the lane that holds it) and keeps the
-    // ones that land on its rows.
-    uint64_t rec[SL];
-    int cnt[SL];
+    uint64_t* MT[SL];
 #pragma unroll
-    for (int s = 0; s < SL; ++s) {
-        rec[s] = 0;
-#pragma unroll
-        for (int m = 0; m < kMaxSrc; ++m) rec[s] |= (uint64_t)Sentinel<N>::kByte << (8 * m);
-        cnt[s] = 0;
-    }
-    for (int jl = 0; jl < LANES; ++jl) {
-#pragma unroll
-        for (int sj = 0; sj < SL; ++sj) {
-            const int j = jl * SL + sj;
-            const int pj = readlane_i(p.v[sj], jl);
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const bool hit = pj == lane * SL + s;
-                const int c = cnt[s];
-                const int sh = 8 * min(c, kMaxSrc - 1);
-                const uint64_t put = (rec[s] & ~((uint64_t)255 << sh)) | ((uint64_t)j << sh);
-                rec[s] = hit && c < kMaxSrc ? put : rec[s];
-                cnt[s] = c + (hit ? 1 : 0);
-            }
-        }
-    }
+    for (int q = 0; q < SL; ++q) MT[q] = smt[wv][q];
+    int rank[SL], cnt[SL];
+    map_ranks<N>(p, lane, act, MT, rank, cnt);
     int maxdeg = 0;
     if (act) {
 #pragma unroll
@@ -116,54 +98,35 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
     for (int off = 32; off >= 1; off >>= 1) maxdeg = max(maxdeg, __shfl_xor(maxdeg, off));
     uint64_t* out = a.rec + (size_t)e * N;
     if (maxdeg <= kMaxSrc) {
+        // record of row r: its sources in ascending order in bytes 0..6
+        // (unused ones name the sentinel), its in-degree in byte 7; each
+        // source writes its own byte at its rank
+        uint64_t* R = srec[wv];
+        uint64_t empty = 0;
+#pragma unroll
+        for (int m = 0; m < kMaxSrc; ++m) empty |= (uint64_t)Sentinel<N>::kByte << (8 * m);
+        wave_sync();
         if (act) {
 #pragma unroll
-            for (int s = 0; s < SL; ++s) out[lane * SL + s] = rec[s] | (uint64_t)cnt[s] << 56;
+            for (int s = 0; s < SL; ++s) R[lane * SL + s] = empty | (uint64_t)cnt[s] << 56;
+        }
+        wave_sync();
+        if (act) {
+            uint8_t* RB = reinterpret_cast<uint8_t*>(R);
+#pragma unroll
+            for (int s = 0; s < SL; ++s) RB[p.v[s] * 8 + rank[s]] = (uint8_t)(lane * SL + s);
+        }
+        wave_sync();
+        if (act) {
+#pragma unroll
+            for (int s = 0; s < SL; ++s) out[lane * SL + s] = R[lane * SL + s];
         }
     } else {
-        // Sorted form: row r's run starts at the number of sources of rows
-        // below r; source j sits in its row's run at its rank among that
-        // row's sources (a second walk in ascending j, as above).
-        uint8_t* P = spos[wv];
-        uint8_t* S = sstart[wv];
-        int tot = 0;
-#pragma unroll
-        for (int s = 0; s < SL; ++s) tot += act ? cnt[s] : 0;
-        int off = wave_incl_scan_i(tot) - tot;
-        int roff[SL], c2[SL];
-#pragma unroll
-        for (int s = 0; s < SL; ++s) {
-            roff[s] = off;
-            off += act ? cnt[s] : 0;
-            c2[s] = 0;
-        }
-        for (int i = lane; i < N; i += kWave) S[i] = 0;
-        wave_sync();
-        for (int jl = 0; jl < LANES; ++jl) {
-#pragma unroll
-            for (int sj = 0; sj < SL; ++sj) {
-                const int pj = readlane_i(p.v[sj], jl);
-#pragma unroll
-                for (int s = 0; s < SL; ++s) {
-                    if (act && pj == lane * SL + s) {
-                        P[jl * SL + sj] = (uint8_t)(roff[s] + c2[s]);
-                        ++c2[s];
-                    }
-                }
-            }
-        }
+        uint64_t w[SL];
+        map_sorted_words<N>(p, lane, act, MT, soff[wv], sst[wv], w);
         if (act) {
 #pragma unroll
-            for (int s = 0; s < SL; ++s)
-                if (cnt[s] > 0) S[roff[s]] = 1;
-        }
-        wave_sync();
-        if (act) {
-#pragma unroll
-            for (int s = 0; s < SL; ++s) {
-                const int j = lane * SL + s;
-                out[j] = srt_word(P[j], roff[s] + cnt[s] - 1, cnt[s] > 0, S[j] != 0);
-            }
+            for (int s = 0; s < SL; ++s) out[lane * SL + s] = w[s];
         }
     }
     if (lane == 0) a.mtab[e] = (uint8_t)(maxdeg <= kMaxSrc ? maxdeg : kFallback);
