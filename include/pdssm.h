@@ -88,9 +88,7 @@ typedef struct pdssm_desc {
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd: the dictionary tables in
  * ws were built by pdssm_prepare for this desc and the current contents of pi;
- * the scans reuse them instead of rebuilding them (single-read scans of
- * dictionaries of at most 16 entries build their tables in LDS and ignore
- * the flag). */
+ * the scan reuses them instead of rebuilding them. */
 #define PDSSM_FLAG_PREPARED 1u
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd / pdssm_decode_step (and
@@ -184,18 +182,16 @@ const char* pdssm_status_string(int status);
  * shared by every step of a call, so its per-step tables are built once).
  * Builds, in ws, a byte copy of every map pi[h,k,:], per destination row the
  * list of its sources (the gather form of the column-one-hot map) and each
- * map's largest in-degree.  pdssm_scan_fwd and pdssm_scan_bwd build the
- * tables themselves first, unless desc->flags has PDSSM_FLAG_PREPARED: then
- * they use the tables already in ws, which must come from pdssm_prepare with
- * the same desc (flags aside), the same ws and the current contents of pi,
- * enqueued before them on the same stream or ordered before them by the
- * caller.  An entry of pi outside [0,N) is reported through *dev_status here.
- * When the scans of desc run the single-read kernels (pdssm_uses_fused) with
- * at most 16 dictionary entries (K <= 16), every workgroup builds its head's
- * tables in LDS from pi at its start (and reports bad entries itself): the
- * call then checks its arguments and enqueues nothing.
+ * map's largest in-degree.  pdssm_scan_fwd and pdssm_scan_bwd always do this
+ * themselves first, unless desc->flags has PDSSM_FLAG_PREPARED: then they use
+ * the tables already in ws, which must come from pdssm_prepare with the same
+ * desc (flags aside), the same ws and the current contents of pi, enqueued
+ * before them on the same stream or ordered before them by the caller.
+ * An entry of pi outside [0,N) is reported through *dev_status here.
  * ws: at least pdssm_workspace_size(desc, PDSSM_OP_FWD) bytes (the forward and
- * backward sizes are equal), 256-byte aligned, not overlapping pi.
+ * backward sizes are equal), 256-byte aligned, not overlapping pi.  When the
+ * scans of desc run the chunked kernels (dictionaries too large for LDS) no
+ * tables are needed and the call enqueues nothing.
  */
 int pdssm_prepare(const pdssm_desc* desc, const int32_t* pi, void* ws, size_t ws_bytes,
                   int* dev_status, void* stream);

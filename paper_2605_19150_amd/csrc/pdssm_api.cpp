@@ -146,9 +146,6 @@ bool use_fused(const pdssm_desc* d) {
     return fused_layout(d, tau, true).total <= pdssm::kMaxLds && fused_layout(d, tau, false).total <= pdssm::kMaxLds;
 }
 
-// The single-read scans build the dictionary tables themselves.
-bool tables_in_kernel(const pdssm_desc* d) { return d->K <= pdssm::kBuildMaxK && use_fused(d); }
-
 // Segments per sequence of the fused scans.  One workgroup per sequence
 // keeps a CU busy; with fewer sequences than kSegTarget workgroups the
 // sequences are cut along L into up to kMaxSeg segments of at least
@@ -217,8 +214,7 @@ void carve_chunked(ScanArgs& a, void* ws, const Sizes& s, const pdssm_desc* d) {
 
 bool narrow_io(const pdssm_desc* d);
 
-// Dictionary tables at the start of ws (built by the prep kernel for the
-// multi-pass kernels and for single-read scans of large dictionaries).
+// Dictionary tables of the fused kernels at the start of ws.
 pdssm::PrepArgs carve_tables(const pdssm_desc* d, const int32_t* pi, void* ws, const Sizes& s, int* status) {
     char* p = static_cast<char*>(ws);
     pdssm::PrepArgs pa;
@@ -235,16 +231,11 @@ pdssm::PrepArgs carve_tables(const pdssm_desc* d, const int32_t* pi, void* ws, c
     return pa;
 }
 
-// Launch configuration of the single-read kernels: wave counts, LDS layouts,
-// segment aggregates in ws.  With at most kBuildMaxK entries their
-// workgroups build their head's dictionary tables in LDS from pi; larger
-// dictionaries are built in ws by the prep kernel (unless the caller
-// prepared them, PDSSM_FLAG_PREPARED) and copied.
+// Points the fused args at the tables in ws and builds them there unless the
+// caller prepared them (PDSSM_FLAG_PREPARED).
 hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* pi, void* ws,
                       const Sizes& s, int* status, hipStream_t st, bool fwd) {
     const pdssm::PrepArgs pa = carve_tables(d, pi, ws, s, status);
-    f.build = tables_in_kernel(d) ? 1 : 0;
-    f.pi = pi;
     f.dict = pa.dict;
     f.rec = pa.rec;
     f.mtab = pa.mtab;
@@ -274,7 +265,7 @@ hipError_t prep_fused(pdssm::FusedArgs& f, const pdssm_desc* d, const int32_t* p
         p += align_up(s.seqN * g.S * 8);
         f.segP = reinterpret_cast<int*>(p);
     }
-    if (f.build || (d->flags & PDSSM_FLAG_PREPARED)) return hipSuccess;
+    if (d->flags & PDSSM_FLAG_PREPARED) return hipSuccess;
     return pdssm::launch_prep(pa, st);
 }
 
@@ -408,8 +399,6 @@ int pdssm_prepare(const pdssm_desc* d, const int32_t* pi, void* ws, size_t ws_by
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (overlap({ws, need}, {pi, (size_t)d->H * d->K * d->N * 4})) return PDSSM_ERR_INVALID_ARG;
-    // single-read kernels with small dictionaries build their tables in LDS
-    if (tables_in_kernel(d)) return PDSSM_OK;
     const hipError_t e = pdssm::launch_prep(carve_tables(d, pi, ws, s, dev_status), static_cast<hipStream_t>(stream));
     return e == hipSuccess ? PDSSM_OK : PDSSM_ERR_HIP;
 }

@@ -93,12 +93,6 @@ inline LdsLayout fused_lds_add_staging(LdsLayout l, int N, int M) {
 
 constexpr size_t kMaxLds = 163840;  // gfx950: 160 KiB per workgroup
 
-// Dictionaries of at most this many entries are built by the scan kernels
-// themselves (about two entries per wave); larger ones by the prep kernel,
-// whose tables the scans copy: building K = 64 entries in every workgroup
-// measured slower (hybrid-lm forward 628 -> 635 us) than the separate pass.
-constexpr int kBuildMaxK = 16;
-
 // Per-call dictionary tables built by the prep kernel (workspace).
 struct PrepArgs {
     int H, K, N;
@@ -128,11 +122,6 @@ struct FusedArgs {
     float2* db;
     float2* dc;
     float2* dh0;
-    // Dictionary tables: built in LDS from pi by every workgroup (build = 1,
-    // small dictionaries), or copied from the workspace tables of the prep
-    // kernel (build = 0).
-    int build;
-    const int* pi;  // [H][K][N]
     const uint8_t* dict;
     const uint64_t* rec;
     const uint8_t* mtab;

@@ -58,32 +58,36 @@ namespace pdssm {
 
 namespace {
 
-// ------------------------------------------------------------------ dictionary tables
-// Per dictionary entry (h, k): the byte map, per destination row a record of
-// its sources in ascending order (up to kMaxSrc bytes, unused ones naming the
-// sentinel, the in-degree in the top byte), and the entry's in-degree class;
-// an entry with a row of more than kMaxSrc sources gets its sorted form
-// instead of records.  Every source finds its rank among the sources of its
-// row from lane-mask tables (map_ranks) and writes its own byte of the row's
-// record, so no lane walks the whole map.
-
-// Scratch of one wave for entry_tables: SL mask tables of N words, then N
-// ints and N bytes for the sorted form.
+// ------------------------------------------------------------------ prep
+// One wave per dictionary entry (h, k): byte dictionary, per-row source
+// records, per-entry max in-degree; an entry with a row of more than kMaxSrc
+// sources gets its sorted form instead of records.  Every source finds its
+// rank among the sources of its row (ascending source order) from lane-mask
+// tables (map_ranks), so no lane walks the whole map.
 template <int N>
-constexpr uint32_t entry_scratch_bytes() {
-    return (uint32_t)((8 * Lay<N>::SL * N + 5 * N + 15) / 16 * 16);
-}
-
-// The tables of one entry from its (sanitised) map p: records or sorted-form
-// words built in place in R (N words of LDS); returns the in-degree class
-// (the largest in-degree, or kFallback), the same in every lane.
-template <int N>
-__device__ __forceinline__ int entry_tables(const IV<Lay<N>::SL>& p, int lane, bool act, unsigned char* scr,
-                                            uint64_t* R) {
-    constexpr int SL = Lay<N>::SL;
+__global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
+    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
+    __shared__ uint64_t smt[4][SL][N];  // per wave: lane-mask tables
+    __shared__ uint64_t srec[4][N];     // per wave: the records being filled
+    __shared__ int soff[4][N];          // per wave: sorted form, first position of each row's run
+    __shared__ uint8_t sst[4][N];       // per wave: sorted form, run-start flags by position
+    const int wv = wave_id(), lane = lane_id();
+    const int e = blockIdx.x * 4 + wv;
+    if (e >= a.H * a.K) return;
+    const bool act = lane < LANES;
+    bool bad = false;
+    IV<SL> p;
+#pragma unroll
+    for (int s = 0; s < SL; ++s) p.v[s] = 0;
+    if (act) {
+        p = ld_iv<SL>(a.pi + (size_t)e * N, lane);
+        bad = sanitize_map<N, SL>(p);
+#pragma unroll
+        for (int s = 0; s < SL; ++s) a.dict[(size_t)e * N + lane * SL + s] = (uint8_t)p.v[s];
+    }
     uint64_t* MT[SL];
 #pragma unroll
-    for (int q = 0; q < SL; ++q) MT[q] = reinterpret_cast<uint64_t*>(scr) + q * N;
+    for (int q = 0; q < SL; ++q) MT[q] = smt[wv][q];
     int rank[SL], cnt[SL];
     map_ranks<N>(p, lane, act, MT, rank, cnt);
     int maxdeg = 0;
@@ -92,8 +96,12 @@ __device__ __forceinline__ int entry_tables(const IV<Lay<N>::SL>& p, int lane, b
         for (int s = 0; s < SL; ++s) maxdeg = max(maxdeg, cnt[s]);
     }
     for (int off = 32; off >= 1; off >>= 1) maxdeg = max(maxdeg, __shfl_xor(maxdeg, off));
-    maxdeg = __builtin_amdgcn_readfirstlane(maxdeg);
+    uint64_t* out = a.rec + (size_t)e * N;
     if (maxdeg <= kMaxSrc) {
+        // record of row r: its sources in ascending order in bytes 0..6
+        // (unused ones name the sentinel), its in-degree in byte 7; each
+        // source writes its own byte at its rank
+        uint64_t* R = srec[wv];
         uint64_t empty = 0;
 #pragma unroll
         for (int m = 0; m < kMaxSrc; ++m) empty |= (uint64_t)Sentinel<N>::kByte << (8 * m);
@@ -109,47 +117,19 @@ __device__ __forceinline__ int entry_tables(const IV<Lay<N>::SL>& p, int lane, b
             for (int s = 0; s < SL; ++s) RB[p.v[s] * 8 + rank[s]] = (uint8_t)(lane * SL + s);
         }
         wave_sync();
-        return maxdeg;
-    }
-    uint64_t w[SL];
-    map_sorted_words<N>(p, lane, act, MT, reinterpret_cast<int*>(scr + 8 * SL * N),
-                        scr + 8 * SL * N + 4 * N, w);
-    wave_sync();
-    if (act) {
+        if (act) {
 #pragma unroll
-        for (int s = 0; s < SL; ++s) R[lane * SL + s] = w[s];
-    }
-    wave_sync();
-    return (int)kFallback;
-}
-
-// One wave per dictionary entry, into the workspace: the tables of the
-// multi-pass kernels (dictionaries too large for LDS).
-template <int N>
-__global__ __launch_bounds__(256) void k_prep(PrepArgs a) {
-    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    __shared__ __align__(16) unsigned char sscr[4][entry_scratch_bytes<N>()];
-    __shared__ uint64_t srec[4][N];
-    const int wv = wave_id(), lane = lane_id();
-    const int e = blockIdx.x * 4 + wv;
-    if (e >= a.H * a.K) return;
-    const bool act = lane < LANES;
-    bool bad = false;
-    IV<SL> p;
+            for (int s = 0; s < SL; ++s) out[lane * SL + s] = R[lane * SL + s];
+        }
+    } else {
+        uint64_t w[SL];
+        map_sorted_words<N>(p, lane, act, MT, soff[wv], sst[wv], w);
+        if (act) {
 #pragma unroll
-    for (int s = 0; s < SL; ++s) p.v[s] = 0;
-    if (act) {
-        p = ld_iv<SL>(a.pi + (size_t)e * N, lane);
-        bad = sanitize_map<N, SL>(p);
-#pragma unroll
-        for (int s = 0; s < SL; ++s) a.dict[(size_t)e * N + lane * SL + s] = (uint8_t)p.v[s];
+            for (int s = 0; s < SL; ++s) out[lane * SL + s] = w[s];
+        }
     }
-    const int cls = entry_tables<N>(p, lane, act, sscr[wv], srec[wv]);
-    if (act) {
-#pragma unroll
-        for (int s = 0; s < SL; ++s) a.rec[(size_t)e * N + lane * SL + s] = srec[wv][lane * SL + s];
-    }
-    if (lane == 0) a.mtab[e] = (uint8_t)cls;
+    if (lane == 0) a.mtab[e] = (uint8_t)(maxdeg <= kMaxSrc ? maxdeg : kFallback);
     if (bad) report_index_error(a.status);
 }
 
@@ -225,8 +205,9 @@ __device__ __forceinline__ Stage<E> stage_of(const Smem& s, int wv) {
     return Stage<E>{reinterpret_cast<E*>(base), reinterpret_cast<E*>(base + N + 1)};
 }
 
-// Copy head hh's dictionary tables from the workspace into LDS and append
-// the identity entry (all threads; a barrier follows).
+// Copy head hh's dictionary tables into LDS and append the identity entry
+// (all threads; a barrier follows).  The tables sit at the start of every
+// layout of one (N, K), whatever its wave count.
 template <int N>
 __device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, int hh) {
     const int nthr = blockDim.x, tid = threadIdx.x;
@@ -238,59 +219,6 @@ __device__ __forceinline__ void stage_tables(const FusedArgs& a, const Smem& s, 
     uint32_t* ddst = reinterpret_cast<uint32_t*>(s.dict);
     for (int i = tid; i < K * N / 4; i += nthr) ddst[i] = dsrc[i];
     for (int i = tid; i < K; i += nthr) s.mtab[i] = a.mtab[e0 + i];
-}
-
-// Builds the tables of one head's entries from its maps pih [K][N] into LDS
-// (rec, dict, mtab): wave w takes entries w, w + nw, ... (the next entry's
-// map loads while it builds the current one); scr: this wave's scratch.  An
-// entry of pi outside [0,N) becomes 0 and is reported.  Kept out of line: it
-// runs once per workgroup, and inlined into the scan kernels it changed
-// their main loops' code (hybrid-lm 1.6% slower).
-template <int N>
-__device__ __attribute__((noinline)) void build_entries(const int* pih, int K, uint64_t* rec, uint8_t* dict,
-                                                         uint8_t* mtab, unsigned char* scr, int* status) {
-    constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
-    const int wv = wave_id(), lane = lane_id(), nw = __builtin_amdgcn_readfirstlane(blockDim.x / kWave);
-    const bool act = lane < LANES;
-    auto load = [&](int k) {
-        IV<SL> p;
-#pragma unroll
-        for (int r = 0; r < SL; ++r) p.v[r] = 0;
-        if (act && k < K) p = ld_iv<SL>(pih + (size_t)k * N, lane);
-        return p;
-    };
-    bool bad = false;
-    IV<SL> nx = load(wv);
-    for (int k = wv; k < K; k += nw) {
-        IV<SL> p = nx;
-        nx = load(k + nw);
-        if (act) {
-            bad |= sanitize_map<N, SL>(p);
-#pragma unroll
-            for (int r = 0; r < SL; ++r) dict[k * N + lane * SL + r] = (uint8_t)p.v[r];
-        }
-        const int cls = entry_tables<N>(p, lane, act, scr, rec + (size_t)k * N);
-        if (lane == 0) mtab[k] = (uint8_t)cls;
-    }
-    if (bad) report_index_error(status);
-}
-
-// Head hh's dictionary tables in LDS (all threads; a barrier follows): built
-// from pi by every workgroup (a.build), or copied from the workspace tables of
-// the prep kernel; then the identity entry K for the padded steps.  The
-// tables sit at the start of every layout of one (N, K), whatever its wave
-// count; each wave's build scratch lies in the layout from agg on, unused
-// until the scan starts (entry_scratch_bytes per wave, well inside the
-// agg .. sb span of every layout).
-template <int N>
-__device__ __forceinline__ void build_tables(const FusedArgs& a, const Smem& s, unsigned char* lds, int hh) {
-    const int nthr = blockDim.x, tid = threadIdx.x;
-    const int K = a.K;
-    if (a.build)
-        build_entries<N>(a.pi + (size_t)hh * K * N, K, s.rec, s.dict, s.mtab,
-                         lds + a.lds.agg + wave_id() * entry_scratch_bytes<N>(), a.status);
-    else
-        stage_tables<N>(a, s, hh);
     for (int j = tid; j < N; j += nthr) {
         uint64_t rec = (uint64_t)1 << 56 | (uint64_t)j;
 #pragma unroll
@@ -1216,7 +1144,7 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
     Smem s = carve_smem(lds, a.lds);
     Work w = AGG ? work_of(a, a.S - 1, 0) : work_of(a, a.S, 0);
 
-    build_tables<N>(a, s, lds, w.hh);
+    stage_tables<N>(a, s, w.hh);
     __syncthreads();
     bool fb;
     const int G = head_variant(s, a.K, fb);
@@ -1531,8 +1459,7 @@ __global__ __launch_bounds__(W * 64) void k_bwd_fused(FusedArgs a) {
     const bool act = lane < LANES;
     const Work w = AGG ? work_of(a, a.S - 1, 1) : work_of(a, a.S, 0);
 
-    build_tables<N>(a, s, lds, w.hh);
-    __syncthreads();  // the tables' scratch overlaps the staging rows
+    stage_tables<N>(a, s, w.hh);
     clear_zero_rows<N, E>(s, W);
     E* ring = reinterpret_cast<E*>(s.ring);
     if (wv == 0) {
