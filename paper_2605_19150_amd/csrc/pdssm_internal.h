@@ -67,7 +67,7 @@ struct ComposeArgs {
 // is the group's only item, else a partial that a last pass adds up in item
 // order.  All sums run in a fixed order (deterministic results).
 struct DictPlan {
-    int seg, S;      // steps per counting segment, segments per head
+    int seg, S;      // steps per counting segment (a multiple of 256), segments per head (<= 64)
     int P;           // steps per item
     int max_items;   // bound on the number of items (grid size)
     int max_slots;   // bound on the partials of groups with several items
@@ -76,10 +76,20 @@ struct DictPlan {
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// segment counts the dictionary planning kernel holds in LDS (64 KiB)
+constexpr int kDictPlanLds = 16384;
+
 inline DictPlan dict_plan(int B, int L, int H, int N, int K) {
     DictPlan p;
     const size_t BL = (size_t)B * L, total = BL * H;
-    p.seg = 4096;
+    // segments of about 512 steps (two tiles of the scatter), at most 64 per
+    // head and at most kDictPlanLds counts in all: enough workgroups for the
+    // grouping kernels to fill the chip, each with a short serial walk, and
+    // the counts fit the planning kernel's LDS
+    size_t s_want = BL >= 64 * 512 ? 64 : (BL + 511) / 512;
+    const size_t s_lds = (size_t)kDictPlanLds / ((size_t)H * K);
+    if (s_want > s_lds) s_want = s_lds > 0 ? s_lds : 1;
+    p.seg = (int)(((BL + s_want - 1) / s_want + 255) & ~(size_t)255);
     p.S = (int)((BL + p.seg - 1) / p.seg);
     const size_t cell = (size_t)N * N * 4;
     // About 2048 items (fewer idle CUs at the grid's end than with 1024:

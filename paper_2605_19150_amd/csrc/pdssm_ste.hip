@@ -10,7 +10,8 @@
 //     k_dict_hist     per (head, segment of steps): how many steps chose each map
 //     k_dict_plan     one workgroup: per group (h,k) its step count, its first
 //                     position in the grouped order, its first item and, for
-//                     groups of several items, its first partial slot
+//                     groups of several items, its first partial slot; per
+//                     (head, segment, map) the segment's first position
 //     k_dict_scatter  per (head, segment): step ids into the grouped order,
 //                     stable (ranks from ballots over the key bits)
 //     k_ste_gemm      per item (at most P steps of one group): the sum of the
@@ -42,7 +43,8 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 struct SteWs {
     int* order;      // [B*L*H] step ids u = b*L + t, grouped by (head, map)
-    int* hist;       // [H][S][K]
+    int* hist;       // [H][S][K] step counts; k_dict_plan turns them into each
+                     // segment's first position in the grouped order
     int* n;          // [H*K] steps per group
     int* pos;        // [H*K] first position of the group in order
     int* item;       // [H*K + 1] first item of the group; item[H*K] = number of items
@@ -71,8 +73,10 @@ __device__ __forceinline__ int map_key(int k, int K, bool& bad) {
 }
 
 // ------------------------------------------------------------------ grouping
-// Block x = h * S + segment: steps u in [segment*seg, min(+seg, B*L)).
+// Block x = h * S + segment: steps u in [segment*seg, min(+seg, B*L)).  Each
+// thread reads its steps' indices in batches of 8 independent loads.
 __global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
+    constexpr int UB = 8;
     __shared__ int cnt[256];
     const int h = blockIdx.x / a.plan.S, sg = blockIdx.x - h * a.plan.S;
     for (int k = threadIdx.x; k < a.K; k += 256) cnt[k] = 0;
@@ -80,7 +84,17 @@ __global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
     const long BL = (long)a.B * a.L;
     const long u0 = (long)sg * a.plan.seg, u1 = min(u0 + (long)a.plan.seg, BL);
     bool bad = false;
-    for (long u = u0 + threadIdx.x; u < u1; u += 256) atomicAdd(&cnt[map_key(a.idx[u * a.H + h], a.K, bad)], 1);
+    for (long ub = u0 + threadIdx.x; ub < u1; ub += 256 * UB) {
+        int v[UB];
+#pragma unroll
+        for (int e = 0; e < UB; ++e) {
+            const long u = ub + (long)e * 256;
+            v[e] = u < u1 ? a.idx[u * a.H + h] : 0;
+        }
+#pragma unroll
+        for (int e = 0; e < UB; ++e)
+            if (ub + (long)e * 256 < u1) atomicAdd(&cnt[map_key(v[e], a.K, bad)], 1);
+    }
     __syncthreads();
     const SteWs w = ste_ws(a);
     for (int k = threadIdx.x; k < a.K; k += 256) w.hist[((size_t)h * a.plan.S + sg) * a.K + k] = cnt[k];
@@ -89,19 +103,42 @@ __global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
 
 // One workgroup: exclusive prefix sums over the groups gi = h*K + k of their
 // step counts (positions; head h starts at h*B*L), item counts and partial
-// slots.  Thread t owns a contiguous range of groups.
+// slots.  Thread t owns a contiguous range of groups.  Last, each segment
+// count in hist is replaced by the segment's first position in the grouped
+// order (the group's position plus the counts of its earlier segments).  The
+// counts are first copied into LDS when they fit (the plan keeps H*S*K at
+// most kDictPlanLds), so that the walks down the segments read LDS.
 __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
-    constexpr int T = 1024;
+    constexpr int T = 1024, SB = 16;
     __shared__ int sh[3][T];
+    __shared__ int hs[kDictPlanLds];
     const SteWs w = ste_ws(a);
     const int HK = a.H * a.K, t = threadIdx.x, P = a.plan.P, S = a.plan.S;
+    const int nh = HK * S;
+    const bool in_lds = nh <= kDictPlanLds;
+    if (in_lds) {
+#pragma unroll 4
+        for (int e = t; e < nh; e += T) hs[e] = w.hist[e];
+        __syncthreads();
+    }
+    auto count = [&](size_t e) { return in_lds ? hs[e] : w.hist[e]; };
     const int per = (HK + T - 1) / T;
     const int g0 = min(t * per, HK), g1 = min(g0 + per, HK);
+    // entry of segment sg of group gi in hist
+    auto at = [&](int gi, int sg) {
+        const int h = gi / a.K, k = gi - h * a.K;
+        return ((size_t)h * S + sg) * a.K + k;
+    };
     int sn = 0, si = 0, ss = 0;
     for (int gi = g0; gi < g1; ++gi) {
-        const int h = gi / a.K, k = gi - h * a.K;
         int n = 0;
-        for (int sg = 0; sg < S; ++sg) n += w.hist[((size_t)h * S + sg) * a.K + k];
+        for (int s0 = 0; s0 < S; s0 += SB) {
+            int c[SB];
+#pragma unroll
+            for (int e = 0; e < SB; ++e) c[e] = s0 + e < S ? count(at(gi, s0 + e)) : 0;
+#pragma unroll
+            for (int e = 0; e < SB; ++e) n += c[e];
+        }
         w.n[gi] = n;
         const int pieces = (n + P - 1) / P;
         sn += n;
@@ -127,6 +164,17 @@ __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
         w.pos[gi] = pn;
         w.item[gi] = pi;
         w.slot[gi] = pieces >= 2 ? ps : -1;
+        int run = pn;
+        for (int s0 = 0; s0 < S; s0 += SB) {
+            int c[SB];
+#pragma unroll
+            for (int e = 0; e < SB; ++e) c[e] = s0 + e < S ? count(at(gi, s0 + e)) : 0;
+#pragma unroll
+            for (int e = 0; e < SB; ++e) {
+                if (s0 + e < S) w.hist[at(gi, s0 + e)] = run;
+                run += c[e];
+            }
+        }
         pn += n;
         pi += pieces;
         if (pieces >= 2) ps += pieces;
@@ -137,7 +185,8 @@ __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
 // Block x = h * S + segment.  Tiles of 256 steps in order; within a tile a
 // step's rank among the earlier steps with the same map comes from ballots
 // over the key bits (wave) and per-wave counts in LDS (tile), so the grouped
-// order keeps the steps of each group in increasing u.
+// order keeps the steps of each group in increasing u.  The next tile's
+// indices are loaded while a tile is ranked.
 __global__ __launch_bounds__(256) void k_dict_scatter(SteGradArgs a) {
     __shared__ int base[256];
     __shared__ int wc[4][256];
@@ -145,9 +194,7 @@ __global__ __launch_bounds__(256) void k_dict_scatter(SteGradArgs a) {
     const int t = threadIdx.x, wv = t >> 6, lane = t & 63;
     const SteWs w = ste_ws(a);
     for (int k = t; k < a.K; k += 256) {
-        int b = w.pos[h * a.K + k];
-        for (int s2 = 0; s2 < sg; ++s2) b += w.hist[((size_t)h * a.plan.S + s2) * a.K + k];
-        base[k] = b;
+        base[k] = w.hist[((size_t)h * a.plan.S + sg) * a.K + k];  // the segment's first position
         wc[0][k] = wc[1][k] = wc[2][k] = wc[3][k] = 0;
     }
     __syncthreads();
@@ -157,10 +204,13 @@ __global__ __launch_bounds__(256) void k_dict_scatter(SteGradArgs a) {
     while ((1 << nbits) < a.K) ++nbits;
     const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
     bool bad = false;
+    int raw_next = u0 + t < u1 ? a.idx[(u0 + t) * a.H + h] : 0;
     for (long tb = u0; tb < u1; tb += 256) {
         const long u = tb + t;
         const bool valid = u < u1;
-        const int key = valid ? map_key(a.idx[u * a.H + h], a.K, bad) : 0;
+        const int raw = raw_next;
+        if (u + 256 < u1) raw_next = a.idx[(u + 256) * a.H + h];
+        const int key = valid ? map_key(raw, a.K, bad) : 0;
         uint64_t peers = __ballot(valid);
         for (int bit = 0; bit < nbits; ++bit) {
             const bool on = (key >> bit) & 1;
