@@ -456,7 +456,22 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 #pragma unroll
                 for (int u = 0; u < KW; ++u) v[u] = fmaf(g[u].x, zc.x, fmaf(g[u].y, zc.y, v[u]));
             };
-            if constexpr (N < 256 && (KW >= 8 || N == 128)) {
+            if constexpr (N == 128 && KW == 4) {
+                // blocks of 8 columns: their z and map bytes first, then
+                // their gathers (timeseries-like shapes: measured 9% faster
+                // for the whole call than one column ahead; slower at N = 64
+                // and with 8 maps per task)
+                constexpr int JB = 8;
+#pragma unroll 1
+                for (int jb = 0; jb < N; jb += JB) {
+                    uint32_t wc[JB][NW4];
+                    float2 zc[JB];
+#pragma unroll
+                    for (int jj = 0; jj < JB; ++jj) ld_col(jb + jj, wc[jj], zc[jj]);
+#pragma unroll
+                    for (int jj = 0; jj < JB; ++jj) column(wc[jj], zc[jj]);
+                }
+            } else if constexpr (N < 256 && (KW >= 8 || N == 128)) {
                 uint32_t wc[NW4];
                 float2 zc;
                 ld_col(0, wc, zc);
