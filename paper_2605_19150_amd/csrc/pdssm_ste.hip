@@ -585,8 +585,12 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 
 // Block (gi, y): groups of several items add their partials in item order;
 // groups no step chose get zeros; single-item groups were written directly.
+// A thread takes 4 consecutive entries (one 16-byte load per partial when G
+// is 16-byte aligned) and issues the loads of 4 partials before it adds them,
+// in item order.
 template <int N>
 __global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
+    constexpr int PB = 4;
     const SteWs w = ste_ws(a);
     const int gi = blockIdx.x;
     const int pieces = w.item[gi + 1] - w.item[gi];
@@ -594,10 +598,31 @@ __global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
     constexpr int NN = N * N;
     float* dst = a.G + (size_t)gi * NN;
     const float* src = w.partial + (size_t)(pieces ? w.slot[gi] : 0) * NN;
-    for (int e = blockIdx.y * 256 + threadIdx.x; e < NN; e += 256 * gridDim.y) {
-        float sum = 0.f;
-        for (int p = 0; p < pieces; ++p) sum += src[(size_t)p * NN + e];
-        dst[e] = sum;
+    const bool vec = (reinterpret_cast<uintptr_t>(a.G) & 15) == 0;
+    for (int e = 4 * (blockIdx.y * 256 + threadIdx.x); e < NN; e += 4 * 256 * gridDim.y) {
+        float sum[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int p0 = 0; p0 < pieces; p0 += PB) {
+            float4 v[PB];
+#pragma unroll
+            for (int i = 0; i < PB; ++i)
+                v[i] = p0 + i < pieces ? *reinterpret_cast<const float4*>(src + (size_t)(p0 + i) * NN + e)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int i = 0; i < PB; ++i) {
+                if (p0 + i < pieces) {
+                    sum[0] += v[i].x;
+                    sum[1] += v[i].y;
+                    sum[2] += v[i].z;
+                    sum[3] += v[i].w;
+                }
+            }
+        }
+        if (vec) {
+            *reinterpret_cast<float4*>(dst + e) = make_float4(sum[0], sum[1], sum[2], sum[3]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) dst[e + i] = sum[i];
+        }
     }
 }
 
@@ -624,7 +649,7 @@ hipError_t dict_launch(const SteGradArgs& a, hipStream_t st) {
     else if (a.K >= 8 * waves) e = a.G ? gemm_launch<N, KW8, true>(a, st) : gemm_launch<N, KW8, false>(a, st);
     else e = a.G ? gemm_launch<N, 4, true>(a, st) : gemm_launch<N, 4, false>(a, st);
     if (e != hipSuccess || !a.G) return e;
-    const int ys = (N * N + 255) / 256 < 16 ? (N * N + 255) / 256 : 16;
+    const int ys = (N * N + 1023) / 1024 < 64 ? (N * N + 1023) / 1024 : 64;  // one 4-entry piece per thread
     hipLaunchKernelGGL(k_dict_reduce<N>, dim3(a.H * a.K, ys), dim3(256), 0, st, a);
     return hipGetLastError();
 }
