@@ -28,8 +28,9 @@
 //                     s = softmax(x / temp) -- the backward stand-in for a hard
 //                     argmax -- in two passes with an online (max, sums)
 //                     state: k_softmax_rows for a contiguous axis (routing
-//                     logits over k), k_softmax_cols for a strided one (down
-//                     each column of the dense dictionary M[h,k]).
+//                     logits over k), k_softmax_cols / k_softmax_cols4 for a
+//                     strided one (down each column of the dense dictionary
+//                     M[h,k]).
 //
 // Every sum runs in a fixed order, so the results do not change from run to run.
 #include "pdssm_device.h"
@@ -761,6 +762,38 @@ __global__ __launch_bounds__(256) void k_softmax_cols(const float* __restrict__ 
         gx[base + i * inner] = __expf(x[base + i * inner] * it - st.m) * rs * (gy[base + i * inner] - dot) * it;
 }
 
+// inner > 1 with a long axis (the columns of M[h,k] at N >= 32): four
+// threads per fibre, each folding a quarter of the axis; the quarters'
+// states merge in LDS in quarter order and each thread writes its quarter.
+// Neighbouring threads of a wave take neighbouring fibres (coalesced), and
+// the chip gets four times the waves of one thread per fibre.
+__global__ __launch_bounds__(256) void k_softmax_cols4(const float* __restrict__ x, const float* __restrict__ gy,
+                                                       float* __restrict__ gx, int64_t outer, int len, int64_t inner,
+                                                       float it) {
+    __shared__ SoftState part_st[4][64];
+    const int f = threadIdx.x & 63, part = threadIdx.x >> 6;
+    const int64_t id = (int64_t)blockIdx.x * 64 + f;
+    const bool on = id < outer * inner;
+    const int64_t o = on ? id / inner : 0, j = on ? id - o * inner : 0;
+    const int64_t base = o * len * inner + j;
+    const int qn = (len + 3) / 4, i0 = min(len, part * qn), i1 = min(len, i0 + qn);
+    SoftState st = {-INFINITY, 0.f, 0.f};
+    if (on) {
+#pragma unroll 4
+        for (int i = i0; i < i1; ++i) soft_add(st, x[base + i * inner] * it, gy[base + i * inner]);
+    }
+    part_st[part][f] = st;
+    __syncthreads();
+    SoftState m = part_st[0][f];
+#pragma unroll
+    for (int p = 1; p < 4; ++p) soft_merge(m, part_st[p][f]);
+    if (!on) return;
+    const float rs = 1.f / m.s, dot = m.d * rs;
+#pragma unroll 4
+    for (int i = i0; i < i1; ++i)
+        gx[base + i * inner] = __expf(x[base + i * inner] * it - m.m) * rs * (gy[base + i * inner] - dot) * it;
+}
+
 template <int T>
 void softmax_rows4_launch(const float* x, const float* gy, float* gx, int64_t rows, int len, float it,
                           hipStream_t st) {
@@ -818,6 +851,9 @@ hipError_t launch_softmax_vjp(const float* x, const float* gy, float* gx, int64_
         else if (len <= 16) softmax_rows_launch<16>(x, gy, gx, outer, len, inv_temp, st);
         else if (len <= 32) softmax_rows_launch<32>(x, gy, gx, outer, len, inv_temp, st);
         else softmax_rows_launch<64>(x, gy, gx, outer, len, inv_temp, st);
+    } else if (len >= 32) {
+        hipLaunchKernelGGL(k_softmax_cols4, dim3((unsigned)((n + 63) / 64)), dim3(256), 0, st, x, gy, gx, outer, len,
+                           inner, inv_temp);
     } else {
         hipLaunchKernelGGL(k_softmax_cols, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, x, gy, gx, outer, len,
                            inner, inv_temp);

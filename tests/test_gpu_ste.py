@@ -206,6 +206,20 @@ def test_softmax_vjp_row_lengths(length):
         assert_close("len%d" % length, got, oracle_softmax_vjp(xs.cpu().numpy(), gs.cpu().numpy(), 1, 0.7))
 
 
+@pytest.mark.parametrize("shape", [(5, 31, 9), (3, 32, 5), (2, 64, 64), (4, 100, 3), (1, 128, 128),
+                                   (2, 301, 7), (3, 33, 70)])
+def test_softmax_vjp_column_lengths(shape):
+    """Strided axis (the middle one): one thread per column below 32 entries,
+    four threads per column (quarters merged in order) from 32 on, with
+    lengths that leave a short last quarter and column counts that leave
+    a partial block."""
+    rng = np.random.default_rng(sum(shape))
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32) * 3).to(DEV)
+    gy = torch.from_numpy(rng.standard_normal(shape).astype(np.float32)).to(DEV)
+    got = pdssm.softmax_vjp(x, gy, 1, 0.8).cpu().numpy()
+    assert_close("cols%s" % (shape,), got, oracle_softmax_vjp(x.cpu().numpy(), gy.cpu().numpy(), 1, 0.8))
+
+
 @pytest.mark.parametrize("wl", [2, 3])
 def test_full_size_sampled(wl):
     """Workload sizes (B16 L2048 H16 N64 K16): q and z on sampled sequences,
