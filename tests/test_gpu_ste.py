@@ -164,6 +164,27 @@ def test_ste_grads_alone_sizes(N, K):
     assert_close_sum("G", G, rG, Gs)
 
 
+def test_ste_grads_more_groups_than_the_plan_holds_in_lds():
+    """H*K = 66*256 groups exceed the 16384 segment counts the planning
+    kernel stages in LDS (it then walks them in global memory); most groups
+    are empty and get zeros."""
+    rng = np.random.default_rng(66)
+    B, L, H, N, K = 1, 40, 66, 8, 256
+    idx = rng.integers(0, K, size=(B, L, H), dtype=np.int32)
+    pi = rng.integers(0, N, size=(H, K, N), dtype=np.int32)
+    g = (rng.standard_normal((B, L, H, N)) + 1j * rng.standard_normal((B, L, H, N))).astype(np.complex64)
+    z = (rng.standard_normal((B, L, H, N)) + 1j * rng.standard_normal((B, L, H, N))).astype(np.complex64)
+    q, G = (t.cpu().numpy() for t in pdssm.ste_grads(*(torch.from_numpy(a).to(DEV) for a in (idx, pi, g, z))))
+    rq, rG = _dense_ref(idx, pi, g, z)
+    qs, Gs = ste_scales(pi, idx, g.astype(np.complex128), z.astype(np.complex128))
+    assert_close_sum("q", q, rq, qs)
+    assert_close_sum("G", G, rG, Gs)
+    chosen = np.zeros((H, K), dtype=bool)
+    for h in range(H):
+        chosen[h, np.unique(idx[:, :, h])] = True
+    assert not G[~chosen].any()
+
+
 def test_ste_grads_reports_bad_index():
     B, L, H, N, K = 1, 50, 1, 64, 4
     idx = torch.zeros((B, L, H), dtype=torch.int32, device=DEV)
