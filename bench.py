@@ -66,7 +66,8 @@ def alg_bytes(w, C, op, esz=8, ssz=8):
     (design_bytes).  esz = bytes per entry of D, b, c, dD, db, dc (8 for
     complex64, 4 for bf16 pairs or the real model); ssz = bytes per state
     entry of h_final and dh0 (8, or 4 for the real model, whose states are
-    real although the library keeps them as complex64); y and dy are fp32."""
+    real; the library keeps h_final and dh0 as complex64 and the saved states
+    as fp32); y and dy are fp32."""
     B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
     steps = B * L * H
     su = steps * N

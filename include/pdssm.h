@@ -30,7 +30,7 @@
  *       idx [B,L,H] int32 in [0,K)   pi [H,K,N] int32 in [0,N)
  *       D, b, c [B,L,H,N] complex    y, dy [B,L,H] float32
  *       h0, h_final, dh_final, dh0 [B,H,N] complex
- *       saved [B,H,C,N] complex, C = pdssm_num_chunks(desc)
+ *       saved [B,H,C,N] complex (fp32 for the real model), C = pdssm_num_chunks(desc)
  *   - The library never allocates or frees memory and never synchronises.
  *     Scratch memory comes from the caller as `ws` (at least
  *     pdssm_workspace_size(desc, op) bytes, 256-byte aligned).  All work is
@@ -108,15 +108,19 @@ typedef struct pdssm_desc {
  * pdssm_prepare, which ignores it): the real-valued model (App. B, the MAD and time-series
  * setups use it): D, b, c and dD, db, dc are real fp32 [B,L,H,N], 4 bytes per
  * entry, the recurrence h_t = P_t (D_t .* h_{t-1}) + b_t over the reals and
- * y_t = sum_n c_t[n] h_t[n].  Every other tensor keeps its type: h0, h_final,
- * saved, dh_final and dh0 stay complex64; for the real model h0 and dh_final
- * hold real values (their imaginary parts must be 0; or NULL) and h_final,
- * saved, dh0 come out with imaginary parts 0.  The single-read scan kernels
+ * y_t = sum_n c_t[n] h_t[n].  The saved chunk states are real fp32 too:
+ * saved holds B*H*C*N floats (4 bytes per entry, [B,H,C,N]; the pointer is
+ * reinterpreted like those of D, b, c), which pdssm_scan_bwd reads back the
+ * same way.  Every other tensor keeps its type: h0, h_final, dh_final and dh0
+ * stay complex64; for the real model h0 and dh_final hold real values (their
+ * imaginary parts must be 0; or NULL) and h_final, dh0 come out with
+ * imaginary parts 0.  The single-read scan kernels
  * keep the state real (float arithmetic, half the work of complex64); every
  * product that feeds a sum is a fused multiply-add in both settings, so every
  * result still equals, bit for bit, the real part of a complex64 call on the
- * same values (the multi-pass kernels, for dictionaries beyond LDS, and the
- * decode step compute the complex64 arithmetic on the real rows).  Cannot be
+ * same values (saved: the real parts of the complex64 call's saved states;
+ * the multi-pass kernels, for dictionaries beyond LDS, and the decode step
+ * compute the complex64 arithmetic on the real rows).  Cannot be
  * combined with
  * PDSSM_FLAG_BF16_IO (PDSSM_ERR_INVALID_ARG).  The scans, pdssm_decode_step
  * and the straight-through pair pdssm_scan_bwd_ste / pdssm_ste_grads support
@@ -202,7 +206,7 @@ int pdssm_prepare(const pdssm_desc* desc, const int32_t* pi, void* ws, size_t ws
  * In:  idx, pi, D, b, c (required); h0 (NULL = zero initial state).
  * Out: y (required); h_final = h_{L-1} (optional); saved (optional): the state
  *      entering every chunk, saved[b,h,c,:] = h_{c*chunk-1} (h0 for c = 0),
- *      which pdssm_scan_bwd needs.
+ *      which pdssm_scan_bwd needs (fp32 entries with PDSSM_FLAG_REAL_IO).
  */
 int pdssm_scan_fwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
                    const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,

@@ -49,6 +49,10 @@ int check_dims(const pdssm_desc* d) {
     return PDSSM_OK;
 }
 
+// Bytes per entry of the chunk-entering states (saved): complex64, or fp32
+// for the real-valued model.
+int state_bytes(const pdssm_desc* d) { return (d->flags & PDSSM_FLAG_REAL_IO) ? 4 : 8; }
+
 // Effective scan chunk (fwd/bwd) or a negative status.
 int scan_chunk(const pdssm_desc* d) {
     int st = check_dims(d);
@@ -420,7 +424,7 @@ int pdssm_scan_fwd(const pdssm_desc* d, const int32_t* idx, const int32_t* pi,
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
-    if (any_overlap({{y, s.idxN * 4}, {h_final, s.seqN * 8}, {saved, s.perChunk * 8}, {ws, need}},
+    if (any_overlap({{y, s.idxN * 4}, {h_final, s.seqN * 8}, {saved, s.perChunk * state_bytes(d)}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {h0, s.seqN * 8}}))
         return PDSSM_ERR_INVALID_ARG;
     a.idx = idx;
@@ -473,7 +477,7 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     if (z && io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
     if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, nst}, {ws, need}},
-                    {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * 8},
+                    {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * state_bytes(d)},
                      {dy, nidx}, {dh_final, s.seqN * 8}}))
         return PDSSM_ERR_INVALID_ARG;
     a.idx = idx;

@@ -178,6 +178,20 @@ __global__ __launch_bounds__(256) void k_fwd_agg(ScanArgs a) {
     if (bad) report_index_error(a.status);
 }
 
+// The carries (chunk-entering states, the saved states when the caller
+// keeps them): complex64, or their real parts as fp32 for the real model
+// (whose states have imaginary parts 0 here too).
+template <int SL>
+__device__ __forceinline__ void st_carry(const ScanArgs& a, size_t off, int lane, const CV<SL>& h) {
+    if (a.io == kIoReal) st_srow<SL>(a.carry, off, lane, to_elem<float>(h));
+    else st_srow<SL>(a.carry, off, lane, h);
+}
+template <int SL>
+__device__ __forceinline__ CV<SL> ld_carry(const ScanArgs& a, size_t off, int lane) {
+    if (a.io == kIoReal) return to_c64<SL>(ld_srow<SL, float>(a.carry, off, lane));
+    return ld_srow<SL, float2>(a.carry, off, lane);
+}
+
 template <int N>
 __global__ __launch_bounds__(256) void k_fwd_carry(ScanArgs a) {
     constexpr int SL = Lay<N>::SL, LANES = Lay<N>::LANES;
@@ -200,7 +214,7 @@ __global__ __launch_bounds__(256) void k_fwd_carry(ScanArgs a) {
     }
     for (int ch = 0; ch < a.C; ++ch) {
         const size_t o = o0 + (size_t)ch * N;
-        if (act) st_cv<SL>(a.carry + o, lane, h);
+        if (act) st_carry<SL>(a, o, lane, h);
         uint64_t wc[SL];
 #pragma unroll
         for (int s = 0; s < SL; ++s) wc[s] = (uint32_t)pn.v[s];  // sorted form of the chunk map
@@ -236,7 +250,7 @@ __global__ __launch_bounds__(256) void k_fwd_replay(ScanArgs a) {
         kv = (unsigned)kv >= (unsigned)a.K ? 0 : kv;  // reported by k_fwd_agg
     }
     CV<SL> h = cv_zero<SL>();
-    if (act) h = ld_cv<SL>(a.carry + ((size_t)seq * a.C + ch) * N, lane);
+    if (act) h = ld_carry<SL>(a, ((size_t)seq * a.C + ch) * N, lane);
 
     const size_t stride = (size_t)a.H * N;
     const size_t base = (((size_t)bb * a.L + s0) * a.H + hh) * N;
@@ -445,7 +459,7 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
     // ---- forward recompute of the chunk's states
     CV<SL> h = cv_zero<SL>();
     if (act) {
-        h = ld_cv<SL>(a.carry + ((size_t)seq * a.C + ch) * N, lane);
+        h = ld_carry<SL>(a, ((size_t)seq * a.C + ch) * N, lane);
         st_cv<SL>(Hs, lane, h);
     }
     CV<SL> Dn = cv_zero<SL>(), bn = cv_zero<SL>();

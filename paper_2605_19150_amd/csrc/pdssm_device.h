@@ -283,6 +283,20 @@ __device__ __forceinline__ void st_state(float2* __restrict__ row, int lane, con
     st_cv<SL>(row, lane, to_c64<SL>(x));
 }
 
+// Chunk-entering states (the saved states, their LDS staging and the
+// multi-pass carries): complex64 rows, or float32 rows for the real model,
+// whose states are real.  off counts entries from base.
+template <int SL, class E>
+__device__ __forceinline__ CV<SL, E> ld_srow(const float2* base, size_t off, int lane) {
+    if constexpr (sizeof(E) == sizeof(float)) return ld_cv<SL>(reinterpret_cast<const float*>(base) + off, lane);
+    else return ld_cv<SL>(base + off, lane);
+}
+template <int SL, class E>
+__device__ __forceinline__ void st_srow(float2* base, size_t off, int lane, const CV<SL, E>& x) {
+    if constexpr (sizeof(E) == sizeof(float)) st_cv<SL>(reinterpret_cast<float*>(base) + off, lane, x);
+    else st_cv<SL>(base + off, lane, x);
+}
+
 // ------------------------------------------------------------------ bf16 (re, im) pairs
 // A complex value in 32 bits: bf16 real part in the low half, bf16 imaginary
 // part in the high half (torch: view_as_real(x).to(bfloat16)).  Widening is

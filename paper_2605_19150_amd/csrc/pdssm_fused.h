@@ -85,7 +85,8 @@ inline LdsLayout fused_lds_layout(int N, int K, int W) {
 }
 
 // Adds M saved-state rows of staging to a layout (the forward writes chunk
-// states there and flushes them to HBM in bursts of M rows).
+// states there and flushes them to HBM in bursts of M rows; complex64 rows
+// for every row format).
 inline LdsLayout fused_lds_add_staging(LdsLayout l, int N, int M) {
     l.total = l.sb + (uint32_t)((size_t)M * N * 8);
     return l;
@@ -117,7 +118,7 @@ struct FusedArgs {
     const float2* dhf;
     float* y;
     float2* hfinal;
-    float2* saved;  // [B*H][C][N]
+    float2* saved;  // [B*H][C][N]: complex64, or float32 entries for the real model (kIoReal)
     float2* dD;
     float2* db;
     float2* dc;

@@ -164,7 +164,8 @@ struct Smem {
     float2* x;      // [W][N]
     float2* cs;     // [W][2][N] (forward: staged c_t, two steps)
     uint8_t* pa;    // [W][N] (backward)
-    float2* sb;     // [sbM][N] forward: staged saved states
+    float2* sb;     // [sbM][N] forward: staged saved states (complex64 rows; the real model's
+                    // are narrowed to their real parts when written out)
 };
 
 __device__ __forceinline__ Smem carve_smem(unsigned char* base, const LdsLayout& l) {
@@ -855,7 +856,10 @@ __device__ __forceinline__ void fwd_chunk(const FusedArgs& a, const Smem& s, con
     wait_ready(s.ready, lc + 1, a.status, s.ready, 1 + 2 * WA, s.prog);
     CV<SL, E> carry = cv_zero<SL, E>();
     if (act) carry = ld_cv<SL>(reinterpret_cast<const E*>(s.ring) + (lc % (WA + 1)) * N, lane);
-    if (act && a.saved && w.sbm == 0) st_state<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
+    if (act && a.saved && w.sbm == 0) {
+        if constexpr (sizeof(E) == sizeof(float)) st_srow<SL>(a.saved, ((size_t)w.seq * a.C + ch) * N, lane, carry);
+        else st_state<SL>(a.saved + ((size_t)w.seq * a.C + ch) * N, lane, carry);
+    }
 
     // ---- 4. readout correction with the true carry, then one store per chunk
 #pragma unroll
@@ -978,8 +982,12 @@ __device__ __forceinline__ void fwd_frontier(const FusedArgs& a, const Smem& s, 
         rslot = rslot + 1 == nring ? 0 : rslot + 1;
         if (M > 0 && act) {
             // the first M chunk states wait in LDS until the whole workgroup
-            // has read its rows; later ones (near the end anyway) go out now
+            // has read its rows; later ones (near the end anyway) go out now.
+            // (Staging the real model's states as floats measured 2% slower
+            // at markov-manyone: the compiler spills more scalar registers.)
             if (c < M) st_state<SL>(s.sb + c * N, lane, carry);
+            else if constexpr (sizeof(E) == sizeof(float))
+                st_srow<SL>(a.saved, ((size_t)w.seq * a.C + w.c0 + c) * N, lane, carry);
             else st_state<SL>(a.saved + ((size_t)w.seq * a.C + w.c0 + c) * N, lane, carry);
         }
         CV<SL, E> nxt;
@@ -1178,10 +1186,18 @@ __global__ __launch_bounds__((W + 1) * 64) void k_fwd_fused(FusedArgs a) {
             const int lane = lane_id();
             __syncthreads();
             const int rows = min(w.sbm, w.nc);
-            float2* dst = a.saved + ((size_t)w.seq * a.C + w.c0) * N;
-            if (lane < LANES)
-                for (int i = wave_id(); i < rows; i += W + 1)
-                    st_cv<SL>(dst + (size_t)i * N, lane, ld_cv<SL>(s.sb + i * N, lane));
+            if constexpr (IO == kIoReal) {
+                // the real model's states leave as their real parts
+                const size_t dst = ((size_t)w.seq * a.C + w.c0) * N;
+                if (lane < LANES)
+                    for (int i = wave_id(); i < rows; i += W + 1)
+                        st_srow<SL>(a.saved, dst + (size_t)i * N, lane, ld_state<float, SL>(s.sb + (size_t)i * N, lane));
+            } else {
+                float2* dst = a.saved + ((size_t)w.seq * a.C + w.c0) * N;
+                if (lane < LANES)
+                    for (int i = wave_id(); i < rows; i += W + 1)
+                        st_cv<SL>(dst + (size_t)i * N, lane, ld_cv<SL>(s.sb + i * N, lane));
+            }
         }
     }
 }
@@ -1219,7 +1235,7 @@ __device__ __forceinline__ void issue_bwd(const FusedArgs& a, const Work& w, int
     const int lenc = min(TAU, a.L - s0);
     u.dyv = a.dy[((size_t)w.bb * a.L + s0 + min(lane, lenc - 1)) * a.H + w.hh];
     if constexpr (!AGG)
-        u.hs = act ? ld_state<E, SL>(a.saved + ((size_t)w.seq * a.C + chc) * N, lane) : cv_zero<SL, E>();
+        u.hs = act ? ld_srow<SL, E>(a.saved, ((size_t)w.seq * a.C + chc) * N, lane) : cv_zero<SL, E>();  // real: fp32 rows
 }
 
 // AGG: the aggregate pass of a segment -- each chunk's adjoint operator is

@@ -11,9 +11,10 @@ Tensor layouts (all contiguous, on one GPU):
   saved [B,H,C,N] complex64 (C = num_chunks).
 With bf16 I/O (FLAG_BF16_IO), D, b, c and dD, db, dc are bfloat16 tensors
   [B,L,H,N,2] holding (re, im) (torch.view_as_real(x).to(torch.bfloat16)).
-The real-valued model (FLAG_REAL_IO): D, b, c and dD, db, dc are float32
-  [B,L,H,N]; h0, dh_final, h_final, dh0 and saved stay complex64 (scan_fwd and
-  scan_bwd also take a real float32 h0 / dh_final and widen it).
+The real-valued model (FLAG_REAL_IO): D, b, c, dD, db, dc and saved are
+  float32 ([B,L,H,N], saved [B,H,C,N]: the states are real); h0, dh_final,
+  h_final and dh0 stay complex64 (scan_fwd and scan_bwd also take a real
+  float32 h0 / dh_final and widen it).
 Straight-through surrogate gradients (Sec. 3.1 Prop. 2): q [B,L,H,K] float32,
   z [B,L,H,N] complex64, G [H,K,N,N] float32, routing logits [B,L,H,K] and
   dense dictionary M [H,K,N,N] float32.
@@ -220,7 +221,7 @@ class Scan:
         self.ws = torch.empty(nws, dtype=torch.uint8, device=dev)
         self.y = torch.empty((B, L, H), dtype=torch.float32, device=dev)
         self.h_final = torch.empty((B, H, N), dtype=torch.complex64, device=dev)
-        self.saved = torch.empty((B, H, self.C, N), dtype=torch.complex64, device=dev)
+        self.saved = torch.empty((B, H, self.C, N), dtype=torch.float32 if real else torch.complex64, device=dev)
         if bf16:
             self.dD = torch.empty((B, L, H, N, 2), dtype=torch.bfloat16, device=dev)
         elif real:
@@ -336,7 +337,8 @@ def _state_arg(x, name, real, dims, dev):
 
 
 def scan_fwd(idx, pi, D, b, c, h0=None, chunk=0, stream=None):
-    """Returns (y [B,L,H] f32, h_final [B,H,N] c64, saved [B,H,C,N] c64)."""
+    """Returns (y [B,L,H] f32, h_final [B,H,N] c64, saved [B,H,C,N] c64, or
+    f32 for real inputs)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
     h0 = _state_arg(h0, "h0", is_real_io(D), (B, H, N), dev)
     s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D), real=is_real_io(D))
@@ -358,10 +360,11 @@ def scan_fwd_noalloc(idx, pi, D, b, c, h0=None, chunk=0, y=None, h_final=None, s
         raise PdssmError(C, "num_chunks")
     y = torch.empty((B, L, H), dtype=torch.float32, device=dev) if y is None else y
     h_final = torch.empty((B, H, N), dtype=torch.complex64, device=dev) if h_final is None else h_final
-    saved = torch.empty((B, H, C, N), dtype=torch.complex64, device=dev) if saved is None else saved
+    sdt = saved_dtype(D)
+    saved = torch.empty((B, H, C, N), dtype=sdt, device=dev) if saved is None else saved
     _need(y, "y", torch.float32, (B, L, H), dev)
     _need(h_final, "h_final", torch.complex64, (B, H, N), dev)
-    _need(saved, "saved", torch.complex64, (B, H, C, N), dev)
+    _need(saved, "saved", sdt, (B, H, C, N), dev)
     st = load().pdssm_scan_fwd_noalloc(ctypes.byref(d), _p(idx), _p(pi), _p(D), _p(b), _p(c), _p(h0), _p(y),
                                        _p(h_final), _p(saved), None, _stream(stream))
     if st != OK:
@@ -369,12 +372,18 @@ def scan_fwd_noalloc(idx, pi, D, b, c, h0=None, chunk=0, y=None, h_final=None, s
     return y, h_final, saved
 
 
+def saved_dtype(D):
+    """dtype of the saved chunk states for inputs D: float32 for the real
+    model (its states are real), else complex64."""
+    return torch.float32 if is_real_io(D) else torch.complex64
+
+
 def scan_bwd(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
     """Returns (dD, db, dc [B,L,H,N] c64, or [B,L,H,N,2] bf16 for bf16 inputs,
     or [B,L,H,N] f32 for real inputs; dh0 [B,H,N] c64)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
     s = Scan(B, L, H, N, K, chunk, dev, bf16=is_bf16_io(D), real=is_real_io(D))
-    _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
+    _need(saved, "saved", saved_dtype(D), (B, H, s.C, N), dev)
     _need(dy, "dy", torch.float32, (B, L, H), dev)
     dh_final = _state_arg(dh_final, "dh_final", is_real_io(D), (B, H, N), dev)
     s.saved = saved
@@ -412,7 +421,7 @@ def scan_bwd_ste(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=Non
     """Returns (dD, db, dc, dh0, z [B,L,H,N] c64, or f32 for real inputs)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
     s = Scan(B, L, H, N, K, chunk, dev, ste=True, real=is_real_io(D))
-    _need(saved, "saved", torch.complex64, (B, H, s.C, N), dev)
+    _need(saved, "saved", saved_dtype(D), (B, H, s.C, N), dev)
     _need(dy, "dy", torch.float32, (B, L, H), dev)
     dh_final = _state_arg(dh_final, "dh_final", is_real_io(D), (B, H, N), dev)
     s.saved = saved
