@@ -327,6 +327,23 @@ __device__ __forceinline__ void mfma_step(f32x16 (&acc)[DictCfg<N>::TILES][DictC
     }
 }
 
+// Staged score tiles hold complex64 entries, or fp32 for real rows (the
+// real model), whose scores then take one multiply-add per gathered entry:
+// the complex form's second one, 0 * 0 + v, returns v unchanged (v is never
+// -0), so both give the same bits.
+template <int IO>
+struct TileOf {
+    using T = float2;
+};
+template <>
+struct TileOf<kIoReal> {
+    using T = float;
+};
+__device__ __forceinline__ float tile_elem(float2 x, float) { return x.x; }
+__device__ __forceinline__ float2 tile_elem(float2 x, float2) { return x; }
+__device__ __forceinline__ float score_fma(float g, float z, float v) { return fmaf(g, z, v); }
+__device__ __forceinline__ float score_fma(float2 g, float2 z, float v) { return fmaf(g.x, z.x, fmaf(g.y, z.y, v)); }
+
 // Element r of tile (ti, tj) in lane l sits at row 32 ti + 8 (r/4) + 4 (l/32) + r%4,
 // column 32 tj + l%32 of the wave's block.
 __device__ __forceinline__ int acc_row(int ti, int r, int lane) { return 32 * ti + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
@@ -343,8 +360,9 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
     constexpr int NB = Cfg::NB, T = Cfg::TILES, U = Cfg::U, RS = Cfg::RS, GP = Cfg::GP;
     extern __shared__ __align__(16) unsigned char lds[];
     float* red = reinterpret_cast<float*>(lds);
-    float2* Gt = reinterpret_cast<float2*>(lds);
-    float2* Zt = Gt + N * GP;
+    using TE = typename TileOf<IO>::T;
+    TE* Gt = reinterpret_cast<TE*>(lds);
+    TE* Zt = Gt + N * GP;
     uint8_t* dT = lds + Cfg::TILE_BYTES;
     const SteWs w = ste_ws(a);
     const int HK = a.H * a.K, KP = score_kp(a.K);
@@ -403,12 +421,12 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
             const int t = my0 + b * U + u;
             if constexpr (Cfg::SPLIT > 1) {
                 if (lane < N) {
-                    Gt[lane * GP + t] = gq[u];
-                    Zt[lane * GP + t] = zq[u];
+                    Gt[lane * GP + t] = tile_elem(gq[u], TE());
+                    Zt[lane * GP + t] = tile_elem(zq[u], TE());
                 }
             } else {
-                if (bj == 0) Gt[(i0 + lane) * GP + t] = gq[u];
-                if (bi == 0) Zt[(j0 + lane) * GP + t] = zq[u];
+                if (bj == 0) Gt[(i0 + lane) * GP + t] = tile_elem(gq[u], TE());
+                if (bi == 0) Zt[(j0 + lane) * GP + t] = tile_elem(zq[u], TE());
             }
         }
     };
@@ -438,7 +456,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
             // are read with this column's gathers, so each column waits for
             // one LDS round trip
             constexpr int NW4 = KW / 4 > 0 ? KW / 4 : 1;
-            auto ld_col = [&](int j, uint32_t (&wds)[NW4], float2& zt) {
+            auto ld_col = [&](int j, uint32_t (&wds)[NW4], TE& zt) {
                 zt = Zt[j * GP + tt];
                 if constexpr (KW == 16) {
                     const uint4 pk = *reinterpret_cast<const uint4*>(dT + j * KP + kb);
@@ -450,12 +468,12 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
                     wds[0] = *reinterpret_cast<const uint32_t*>(dT + j * KP + kb);
                 }
             };
-            auto column = [&](const uint32_t (&wc)[NW4], float2 zc) {
-                float2 g[KW > 0 ? KW : 1];
+            auto column = [&](const uint32_t (&wc)[NW4], TE zc) {
+                TE g[KW > 0 ? KW : 1];
 #pragma unroll
                 for (int u = 0; u < KW; ++u) g[u] = Gt[((wc[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
 #pragma unroll
-                for (int u = 0; u < KW; ++u) v[u] = fmaf(g[u].x, zc.x, fmaf(g[u].y, zc.y, v[u]));
+                for (int u = 0; u < KW; ++u) v[u] = score_fma(g[u], zc, v[u]);
             };
             if constexpr (N == 128 && KW == 4) {
                 // blocks of 8 columns: their z and map bytes first, then
@@ -466,7 +484,7 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 #pragma unroll 1
                 for (int jb = 0; jb < N; jb += JB) {
                     uint32_t wc[JB][NW4];
-                    float2 zc[JB];
+                    TE zc[JB];
 #pragma unroll
                     for (int jj = 0; jj < JB; ++jj) ld_col(jb + jj, wc[jj], zc[jj]);
 #pragma unroll
@@ -474,12 +492,12 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
                 }
             } else if constexpr (N < 256 && (KW >= 8 || N == 128)) {
                 uint32_t wc[NW4];
-                float2 zc;
+                TE zc;
                 ld_col(0, wc, zc);
 #pragma unroll 2
                 for (int j = 0; j < N; ++j) {
                     uint32_t wn[NW4];
-                    float2 zn;
+                    TE zn;
                     ld_col(min(j + 1, N - 1), wn, zn);
                     column(wc, zc);
 #pragma unroll
@@ -493,12 +511,12 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
 #pragma unroll 2
                 for (int j = 0; j < N; ++j) {
                     uint32_t wc[NW4];
-                    float2 zc;
+                    TE zc;
                     ld_col(j, wc, zc);
 #pragma unroll
                     for (int u = 0; u < KW; ++u) {
-                        const float2 g = Gt[((wc[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
-                        v[u] = fmaf(g.x, zc.x, fmaf(g.y, zc.y, v[u]));
+                        const TE g = Gt[((wc[u >> 2] >> (8 * (u & 3))) & 0xff) * GP + tt];
+                        v[u] = score_fma(g, zc, v[u]);
                     }
                 }
             }
