@@ -41,6 +41,7 @@ namespace pdssm {
 namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x32 __attribute__((ext_vector_type(32)));
 
 struct SteWs {
     int* order;      // [B*L*H] step ids u = b*L + t, grouped by (head, map)
@@ -344,6 +345,20 @@ __device__ __forceinline__ float2 tile_elem(float2 x, float2) { return x; }
 __device__ __forceinline__ float score_fma(float g, float z, float v) { return fmaf(g, z, v); }
 __device__ __forceinline__ float score_fma(float2 g, float2 z, float v) { return fmaf(g.x, z.x, fmaf(g.y, z.y, v)); }
 
+// Real rows (NB = 64): G += g z^T needs no second contraction term, so one
+// v_mfma_f32_32x32x1f32 (two 32 x 32 blocks, K = 1) does the work of two
+// tiles.  accR[tj] holds tiles (0, tj) and (1, tj) as its blocks: lane l
+// supplies A = g[l] (block l/32, row l%32) and B = z of column 32 tj + l%32
+// for both blocks, i.e. the low (tj = 0) or high (tj = 1) half of z in both
+// halves of the wave, which one permlane32 swap of z with itself gives.
+// Block b's registers 16 b .. 16 b + 15 follow the 32x32 single-block
+// layout below, so accR[tj][16 ti + r] is element r of tile (ti, tj).
+__device__ __forceinline__ void mfma_step_real(f32x32 (&accR)[2], float g, float z) {
+    const auto zs = __builtin_amdgcn_permlane32_swap(__float_as_uint(z), __float_as_uint(z), false, false);
+    accR[0] = __builtin_amdgcn_mfma_f32_32x32x1f32(g, __uint_as_float(zs[0]), accR[0], 0, 0, 0);
+    accR[1] = __builtin_amdgcn_mfma_f32_32x32x1f32(g, __uint_as_float(zs[1]), accR[1], 0, 0, 0);
+}
+
 // Element r of tile (ti, tj) in lane l sits at row 32 ti + 8 (r/4) + 4 (l/32) + r%4,
 // column 32 tj + l%32 of the wave's block.
 __device__ __forceinline__ int acc_row(int ti, int r, int lane) { return 32 * ti + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
@@ -404,6 +419,14 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
         for (int tj = 0; tj < T; ++tj)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[ti][tj][r] = 0.f;
+    constexpr bool kRealG = IO == kIoReal && NB == 64;
+    f32x32 accR[2];
+    if constexpr (kRealG) {
+#pragma unroll
+        for (int tj = 0; tj < 2; ++tj)
+#pragma unroll
+            for (int r = 0; r < 32; ++r) accR[tj][r] = 0.f;
+    }
 
     // step ids of run r (lane t: step t; past the item: the item's last step,
     // so every load below stays valid and unconditional)
@@ -433,7 +456,10 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
     auto multiply = [&](const float2 (&gq)[U], const float2 (&zq)[U], int r, int b) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (r * RS + my0 + b * U + u < cnt) mfma_step<N>(acc, gq[u], zq[u], lane);
+            if (r * RS + my0 + b * U + u < cnt) {
+                if constexpr (kRealG) mfma_step_real(accR, gq[u].x, zq[u].x);
+                else mfma_step<N>(acc, gq[u], zq[u], lane);
+            }
     };
     // scores of the run's steps, KW maps per task: lane l takes step l % RS
     // of the run, and the 64 / RS lane groups of a wave take different tasks
@@ -566,6 +592,14 @@ __global__ __launch_bounds__(DictCfg<N>::WAVES * 64) void k_ste_gemm(SteGradArgs
         sidn = sidnn;
     }
     if constexpr (!DO_G) return;
+    if constexpr (kRealG) {
+#pragma unroll
+        for (int ti = 0; ti < 2; ++ti)
+#pragma unroll
+            for (int tj = 0; tj < 2; ++tj)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[ti][tj][r] = accR[tj][16 * ti + r];
+    }
 
     if constexpr (Cfg::SPLIT > 1) {
         __syncthreads();  // red aliases the tiles
