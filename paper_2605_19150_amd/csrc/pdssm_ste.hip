@@ -112,7 +112,7 @@ __global__ __launch_bounds__(256) void k_dict_hist(SteGradArgs a) {
 // most kDictPlanLds), so that the walks down the segments read LDS.
 __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
     constexpr int T = 1024, SB = 16;
-    __shared__ int sh[3][T];
+    __shared__ int sh[3][T / 64];
     __shared__ int hs[kDictPlanLds];
     const SteWs w = ste_ws(a);
     const int HK = a.H * a.K, t = threadIdx.x, P = a.plan.P, S = a.plan.S;
@@ -147,19 +147,31 @@ __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
         si += pieces;
         ss += pieces >= 2 ? pieces : 0;
     }
-    sh[0][t] = sn;
-    sh[1][t] = si;
-    sh[2][t] = ss;
-    __syncthreads();
-    for (int d = 1; d < T; d <<= 1) {
-        const int v0 = t >= d ? sh[0][t - d] : 0, v1 = t >= d ? sh[1][t - d] : 0, v2 = t >= d ? sh[2][t - d] : 0;
-        __syncthreads();
-        sh[0][t] += v0;
-        sh[1][t] += v1;
-        sh[2][t] += v2;
-        __syncthreads();
+    // prefix sums over the threads: within each wave by shuffles, then over
+    // the waves' totals
+    const int lane = t & 63, wv = t >> 6;
+    int x0 = sn, x1 = si, x2 = ss;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        const int y0 = __shfl_up(x0, d), y1 = __shfl_up(x1, d), y2 = __shfl_up(x2, d);
+        if (lane >= d) {
+            x0 += y0;
+            x1 += y1;
+            x2 += y2;
+        }
     }
-    int pn = sh[0][t] - sn, pi = sh[1][t] - si, ps = sh[2][t] - ss;
+    if (lane == 63) {
+        sh[0][wv] = x0;
+        sh[1][wv] = x1;
+        sh[2][wv] = x2;
+    }
+    __syncthreads();
+    for (int v = 0; v < wv; ++v) {
+        x0 += sh[0][v];
+        x1 += sh[1][v];
+        x2 += sh[2][v];
+    }
+    int pn = x0 - sn, pi = x1 - si, ps = x2 - ss;
     for (int gi = g0; gi < g1; ++gi) {
         const int n = w.n[gi];
         const int pieces = (n + P - 1) / P;
@@ -181,7 +193,7 @@ __global__ __launch_bounds__(1024) void k_dict_plan(SteGradArgs a) {
         pi += pieces;
         if (pieces >= 2) ps += pieces;
     }
-    if (t == T - 1) w.item[HK] = sh[1][T - 1];
+    if (t == T - 1) w.item[HK] = x1;  // the inclusive total
 }
 
 // Block x = h * S + segment.  Tiles of 256 steps in order; within a tile a
