@@ -154,6 +154,30 @@ def test_real_io_module_functions():
 SORTED_HEAD = {3: 4, 5: 18}
 
 
+def test_real_io_saved_fp32_through_every_entry():
+    """The real model's saved states are fp32 [B,H,C,N]: scan_fwd and
+    scan_fwd_noalloc (the library's own workspace) give the same bits, on a
+    single-read head mix and on a segmented sequence, and scan_bwd reads them
+    back."""
+    for B, L, H, N, K, seed in ((3, 150, 2, 64, 9, 21), (1, 2600, 1, 128, 8, 22)):
+        print("real saved: B%d L%d H%d N%d K%d" % (B, L, H, N, K), flush=True)
+        inp = make_inputs(B=B, L=L, H=H, N=N, K=K, seed=seed, with_h0=True, real=True)
+        T = {k: torch.from_numpy(np.ascontiguousarray(inp[k])).to(DEV) for k in ("idx", "pi", "D", "b", "c", "dy")}
+        h0r = torch.from_numpy(np.ascontiguousarray(inp["h0"].real)).to(DEV)
+        y0, h0, s0 = (x.clone() for x in pdssm.scan_fwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=h0r))
+        y1, h1, s1 = pdssm.scan_fwd_noalloc(T["idx"], T["pi"], T["D"], T["b"], T["c"], h0=h0r)
+        torch.cuda.synchronize()
+        assert s0.dtype == torch.float32 and s1.dtype == torch.float32
+        assert torch.equal(y0, y1) and torch.equal(h0, h1) and torch.equal(s0, s1)
+        tau = pdssm.chunk_len(pdssm.desc(B, L, H, N, K))
+        _, _, rsaved = oracle_fwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], h0=inp["h0"], chunk=tau)
+        assert_close("saved", s0.cpu().numpy(), rsaved.real)
+        g = pdssm.scan_bwd(T["idx"], T["pi"], T["D"], T["b"], T["c"], s1, T["dy"])
+        rg = oracle_bwd(inp["idx"], inp["pi"], inp["D"], inp["b"], inp["c"], inp["dy"], h0=inp["h0"])
+        for k, v, r in zip(("dD", "db", "dc"), g[:3], rg[:3]):
+            assert_close(k, v.cpu().numpy(), r.real)
+
+
 @pytest.mark.parametrize("wl", [2, 3, 4, 5])
 def test_real_io_full_size(wl):
     """Every output of the full-size workload bit for bit against complex64;
