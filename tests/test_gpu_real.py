@@ -255,3 +255,34 @@ def test_real_ste(N, K, B, L, H, chunk):
     # the module functions take real g and z
     q2, G2 = pdssm.ste_grads(idx, pi, r["db"], r["z"])
     assert torch.equal(q2, r["q"]) and torch.equal(G2, r["G"])
+
+
+@pytest.mark.parametrize("wl", [2, 4])
+def test_real_ste_full_size_matches_complex(wl):
+    """Full-size fsa-perm (N=64) and timeseries (N=128, segmented) with real
+    rows: the straight-through outputs (fp32 score tiles, the two-block
+    K=1 products) equal the complex64 path's on the same values bit for bit."""
+    print("real ste full size workload %d" % wl, flush=True)
+    inp = workload_inputs(wl, seed=0, real=True)
+    B, L, H = inp["idx"].shape
+    _, K, N = inp["pi"].shape
+    idx, pi = torch.from_numpy(inp["idx"]).to(DEV), torch.from_numpy(inp["pi"]).to(DEV)
+    dy = torch.from_numpy(inp["dy"]).to(DEV)
+    real = {k: torch.from_numpy(inp[k]).to(DEV) for k in ("D", "b", "c")}
+    out = {}
+    for tag, re in (("real", True), ("c64", False)):
+        T = real if re else {k: v.to(torch.complex64) for k, v in real.items()}
+        s = pdssm.Scan(B, L, H, N, K, 0, DEV, ste=True, real=re)
+        s.fwd(idx, pi, T["D"], T["b"], T["c"])
+        s.bwd_ste(idx, pi, T["D"], T["b"], T["c"], dy)
+        s.ste_grads(idx, pi)
+        s.check_status()
+        out[tag] = {k: getattr(s, k).clone() for k in ("db", "z", "q", "G")}
+        del s
+        torch.cuda.empty_cache()
+    r, c = out["real"], out["c64"]
+    for k in ("db", "z"):
+        assert torch.equal(r[k], c[k].real), k
+    for k in ("q", "G"):
+        assert bool(torch.isfinite(r[k]).all()), k
+        assert torch.equal(r[k], c[k]), k
