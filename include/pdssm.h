@@ -99,9 +99,10 @@ typedef struct pdssm_desc {
  * arithmetic).  Every other tensor (idx, pi, h0, h_final, saved, y, dy,
  * dh_final, dh0) keeps its type.  The arithmetic is fp32 as without the
  * flag: inputs widen exactly, gradients are rounded to nearest (ties to
- * even) when stored.  pdssm_compose_chunks, pdssm_scan_bwd_ste and
- * pdssm_ste_grads return PDSSM_ERR_UNSUPPORTED (z in bf16 would round the
- * straight-through inputs). */
+ * even) when stored.  The straight-through pair keeps z complex64 (a bf16 z
+ * would round the straight-through inputs): pdssm_scan_bwd_ste writes it so,
+ * and pdssm_ste_grads takes g = db as bf16 pairs with that complex64 z.
+ * pdssm_compose_chunks returns PDSSM_ERR_UNSUPPORTED. */
 #define PDSSM_FLAG_BF16_IO 2u
 
 /* desc->flags bit for pdssm_scan_fwd / pdssm_scan_bwd / pdssm_decode_step (and
@@ -264,8 +265,8 @@ int pdssm_scan_bwd(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi
  * the state entering the map of step t, which pdssm_ste_grads needs together
  * with db (the gradient g_t reaching h_t).  Same workspace as pdssm_scan_bwd
  * (PDSSM_OP_BWD).  z must not overlap any other argument.  With
- * PDSSM_FLAG_REAL_IO z is a real fp32 row like db (PDSSM_FLAG_BF16_IO:
- * PDSSM_ERR_UNSUPPORTED).
+ * PDSSM_FLAG_REAL_IO z is a real fp32 row like db; with PDSSM_FLAG_BF16_IO
+ * it stays complex64 (unrounded) while dD, db, dc are bf16 pairs.
  */
 int pdssm_scan_bwd_ste(const pdssm_desc* desc, const int32_t* idx, const int32_t* pi,
                        const pdssm_c64* D, const pdssm_c64* b, const pdssm_c64* c,
@@ -292,8 +293,9 @@ int pdssm_scan_bwd_ste(const pdssm_desc* desc, const int32_t* idx, const int32_t
  * sort) and every sum runs in a fixed order (deterministic results).
  * In:  idx [B,L,H], pi [H,K,N] (needed for q), g, z [B,L,H,N] complex64, or
  *      real fp32 with PDSSM_FLAG_REAL_IO (the real-valued model: Re(g conj z)
- *      is then g z); desc->chunk is ignored; PDSSM_FLAG_BF16_IO gives
- *      PDSSM_ERR_UNSUPPORTED.
+ *      is then g z), or with PDSSM_FLAG_BF16_IO g as bf16 (re, im) pairs
+ *      (4 bytes per entry, widened exactly) and z complex64, as
+ *      pdssm_scan_bwd_ste writes them; desc->chunk is ignored.
  * ws:  at least pdssm_workspace_size(desc, PDSSM_OP_STE_GRADS) bytes, 256-byte
  *      aligned.  An idx entry outside [0,K) counts as map 0 and is reported
  *      through *dev_status; a pi entry outside [0,N) reads row 0.

@@ -473,10 +473,11 @@ int scan_bwd_impl(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, co
     if (!ws || ws_bytes < need || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
     if (misaligned(z)) return PDSSM_ERR_INVALID_ARG;
-    // z in bf16 pairs would round the straight-through inputs: not offered
-    if (z && io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     const size_t nidx = s.idxN * 4, npi = (size_t)d->H * d->K * d->N * 4, nst = s.stepN * io_bytes(d);
-    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, nst}, {ws, need}},
+    // z: complex64 with bf16 pairs (rounding it would round the
+    // straight-through inputs), else the gradients' row format
+    const size_t nz = s.stepN * (io_format(d) == pdssm::kIoBf16 ? 8 : io_bytes(d));
+    if (any_overlap({{dD, nst}, {db, nst}, {dc, nst}, {dh0, s.seqN * 8}, {z, nz}, {ws, need}},
                     {{idx, nidx}, {pi, npi}, {D, nst}, {b, nst}, {c, nst}, {saved, s.perChunk * state_bytes(d)},
                      {dy, nidx}, {dh_final, s.seqN * 8}}))
         return PDSSM_ERR_INVALID_ARG;
@@ -536,7 +537,6 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
                     void* stream) {
     const int st = check_dims(d);
     if (st != PDSSM_OK) return st;
-    if (io_format(d) == pdssm::kIoBf16) return PDSSM_ERR_UNSUPPORTED;
     if (!idx || !g || !z || (!q && !G) || (q && !pi)) return PDSSM_ERR_INVALID_ARG;
     if (misaligned4(idx)) return PDSSM_ERR_INVALID_ARG;
     if (misaligned(g) || misaligned(z) || misaligned(pi) || (reinterpret_cast<uintptr_t>(G) & 3) != 0 ||
@@ -545,9 +545,12 @@ int pdssm_ste_grads(const pdssm_desc* d, const int32_t* idx, const int32_t* pi, 
     const pdssm::DictPlan plan = pdssm::dict_plan(d->B, d->L, d->H, d->N, d->K);
     if (!ws || ws_bytes < plan.bytes || (reinterpret_cast<uintptr_t>(ws) % kAlign) != 0)
         return PDSSM_ERR_WORKSPACE;
+    // g in the row format (bf16 pairs, real fp32 or complex64); z complex64
+    // with bf16 pairs (as pdssm_scan_bwd_ste writes it), else the same format
     const size_t nidx = (size_t)d->B * d->L * d->H * 4, nst = nidx / 4 * d->N * io_bytes(d);
+    const size_t nz = nidx / 4 * d->N * (io_format(d) == pdssm::kIoBf16 ? 8 : io_bytes(d));
     const size_t nG = (size_t)d->H * d->K * d->N * d->N * 4, npi = (size_t)d->H * d->K * d->N * 4;
-    if (any_overlap({{G, nG}, {q, nidx * d->K}, {ws, plan.bytes}}, {{idx, nidx}, {g, nst}, {z, nst}, {pi, npi}}))
+    if (any_overlap({{G, nG}, {q, nidx * d->K}, {ws, plan.bytes}}, {{idx, nidx}, {g, nst}, {z, nz}, {pi, npi}}))
         return PDSSM_ERR_INVALID_ARG;
     pdssm::SteGradArgs a = {};
     a.B = d->B;

@@ -544,7 +544,7 @@ __global__ __launch_bounds__(64) void k_bwd_emit(ScanArgs a) {
             CV<SL> zt;
 #pragma unroll
             for (int s = 0; s < SL; ++s) zt.v[s] = cmul(Dt.v[s], hp.v[s]);
-            st_io<SL, IO>(a.z, off, lane, zt);
+            st_io<SL, (IO == kIoBf16 ? kIoC64 : IO)>(a.z, off, lane, zt);  // bf16 pairs: z complex64
         }
     }
 }

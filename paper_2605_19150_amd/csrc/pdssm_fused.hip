@@ -1401,7 +1401,9 @@ __device__ __forceinline__ void bwd_chunk(const FusedArgs& a, const Smem& s, con
                 CV<SL, E> zt;
 #pragma unroll
                 for (int i = 0; i < SL; ++i) zt.v[i] = cmul(Dt(q, t).v[i], Hs[t].v[i]);
-                st_out<IO, SL>(a.z, off, lane, zt);
+                // with bf16 pairs z stays complex64 (rounding it would round
+                // the straight-through inputs)
+                st_out<(IO == kIoBf16 ? kIoC64 : IO), SL>(a.z, off, lane, zt);
             }
         }
     }

@@ -14,8 +14,8 @@ struct ScanArgs {
     int B, L, H, N, K;
     int tau;  // chunk length
     int C;    // ceil(L / tau)
-    int io;   // row format of D, b, c, dD, db, dc, z (kIoC64, kIoBf16, kIoReal: pdssm_io.h);
-              // the float2 pointers below are reinterpreted for the 4-byte formats
+    int io;   // row format of D, b, c, dD, db, dc, z (kIoC64, kIoBf16, kIoReal: pdssm_io.h; z stays
+              // complex64 with kIoBf16); the float2 pointers below are reinterpreted for the 4-byte formats
     const int* idx;
     const int* pi;
     const float2* D;
@@ -127,7 +127,8 @@ struct SteGradArgs {
     int B, L, H, N, K;
     const int* idx;    // [B,L,H]
     const int* pi;     // [H,K,N] (scores only)
-    int io;            // row format of g and z: kIoC64 or kIoReal (real fp32, pdssm_io.h)
+    int io;            // row format of g: kIoC64, kIoReal (real fp32; z too) or kIoBf16 (bf16
+                       // pairs; z complex64), pdssm_io.h
     const float2* g;   // [B,L,H,N] gradient reaching h_t (db of the backward)
     const float2* z;   // [B,L,H,N] D_t .* h_{t-1}
     float* q;          // [B,L,H,K] scores of every map, or null

@@ -306,6 +306,13 @@ __device__ __forceinline__ void load_step(const SteGradArgs& a, int u, int h, in
         const float zq = __builtin_nontemporal_load(reinterpret_cast<const float*>(a.z) + row + j0 + r);
         gv = make_float2(gq, 0.f);
         zv = make_float2(zq, 0.f);
+    } else if constexpr (IO == kIoBf16) {
+        // g = db in bf16 (re, im) pairs, widened exactly; z complex64
+        typedef float f32x2 __attribute__((ext_vector_type(2)));
+        const uint32_t gw = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(a.g) + row + i0 + r);
+        const f32x2 zq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.z + row + j0 + r));
+        gv = bf2_to_f2(gw);
+        zv = make_float2(zq.x, zq.y);
     } else {
         typedef float f32x2 __attribute__((ext_vector_type(2)));
         const f32x2 gq = __builtin_nontemporal_load(reinterpret_cast<const f32x2*>(a.g + row + i0 + r));
@@ -693,7 +700,9 @@ __global__ __launch_bounds__(256) void k_dict_reduce(SteGradArgs a) {
 
 template <int N, int KW, bool DO_G>
 hipError_t gemm_launch(const SteGradArgs& a, hipStream_t st) {
-    auto kern = a.io == kIoReal ? k_ste_gemm<N, KW, DO_G, kIoReal> : k_ste_gemm<N, KW, DO_G, kIoC64>;
+    auto kern = a.io == kIoReal   ? k_ste_gemm<N, KW, DO_G, kIoReal>
+                : a.io == kIoBf16 ? k_ste_gemm<N, KW, DO_G, kIoBf16>
+                                  : k_ste_gemm<N, KW, DO_G, kIoC64>;
     const size_t lds = ste_gemm_lds<N>(a.K, KW > 0);
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -418,9 +418,10 @@ def compose_chunks(idx, pi, D, chunk, stream=None):
 
 
 def scan_bwd_ste(idx, pi, D, b, c, saved, dy, dh_final=None, chunk=0, stream=None):
-    """Returns (dD, db, dc, dh0, z [B,L,H,N] c64, or f32 for real inputs)."""
+    """Returns (dD, db, dc, dh0, z [B,L,H,N] c64, or f32 for real inputs;
+    with bf16 inputs dD, db, dc are bf16 pairs and z stays c64)."""
     B, L, H, N, K, dev = _check_inputs(idx, pi, D, b, c)
-    s = Scan(B, L, H, N, K, chunk, dev, ste=True, real=is_real_io(D))
+    s = Scan(B, L, H, N, K, chunk, dev, ste=True, bf16=is_bf16_io(D), real=is_real_io(D))
     _need(saved, "saved", saved_dtype(D), (B, H, s.C, N), dev)
     _need(dy, "dy", torch.float32, (B, L, H), dev)
     dh_final = _state_arg(dh_final, "dh_final", is_real_io(D), (B, H, N), dev)
@@ -434,18 +435,22 @@ def ste_grads(idx, pi, g, z, q=True, G=True, stream=None):
     """(q [B,L,H,K] f32 or None, G [H,K,N,N] f32 or None) from g = db and z
     of scan_bwd_ste: the scores of every map at every step and, per head and
     map, the sum of Re(g_t z_t^H) over the steps that chose the map.  g, z
-    complex64, or float32 for the real-valued model."""
+    complex64; or float32 for the real-valued model; or g as bf16 (re, im)
+    pairs [B,L,H,N,2] (the bf16 setting's db) with z complex64."""
     B, L, H = idx.shape
     N = g.shape[3]
     K = pi.shape[1]
     dev = idx.device
-    real = is_real_io(g)
+    real, bf16 = is_real_io(g), is_bf16_io(g)
     _need(idx, "idx", torch.int32, (B, L, H), dev)
     _need(pi, "pi", torch.int32, (H, K, N), dev)
-    _need(g, "g", torch.float32 if real else torch.complex64, (B, L, H, N), dev)
+    if bf16:
+        _need(g, "g", torch.bfloat16, (B, L, H, N, 2), dev)
+    else:
+        _need(g, "g", torch.float32 if real else torch.complex64, (B, L, H, N), dev)
     _need(z, "z", torch.float32 if real else torch.complex64, (B, L, H, N), dev)
     d = desc(B, L, H, N, K)
-    d.flags = FLAG_REAL_IO if real else 0
+    d.flags = FLAG_REAL_IO if real else (FLAG_BF16_IO if bf16 else 0)
     ws = torch.empty(max(workspace_size(d, OP_STE_GRADS), 1), dtype=torch.uint8, device=dev)
     qq = torch.empty((B, L, H, K), dtype=torch.float32, device=dev) if q else None
     GG = torch.empty((H, K, N, N), dtype=torch.float32, device=dev) if G else None

@@ -109,21 +109,22 @@ def test_flags_known_bits_only(lib):
 def test_narrow_io_only_where_supported(lib, flag):
     f = FakeBufs()
     P = lambda n: f(n)  # noqa: E731
-    # composition takes complex64 only; the straight-through pair takes real
-    # rows but not bf16 pairs (the scans and the decode step take both)
+    # composition takes complex64 only (the scans, the decode step and the
+    # straight-through pair take both narrow formats)
     d = pdssm.desc(2, 40, 2, 64, 4)
     d.flags = getattr(pdssm, flag)
     st = 2 * 40 * 2 * 64 * 8
     assert lib.pdssm_compose_chunks(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), None,
                                     None) == pdssm.ERR_UNSUPPORTED
     if flag == "FLAG_BF16_IO":
-        assert lib.pdssm_ste_grads(ctypes.byref(d), P(640), P(2048), P(st), P(st), P(st), P(st), P(1 << 20),
-                                   1 << 20, None, None) == pdssm.ERR_UNSUPPORTED
-        need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_BWD)
+        # bf16 pairs: g has 4 bytes per entry and z stays complex64 (8), so an
+        # output placed in the second half of z's extent overlaps it
+        need = lib.pdssm_workspace_size(ctypes.byref(d), pdssm.OP_STE_GRADS)
         ws = ctypes.c_void_p(f(need).value // 256 * 256 + 256)
-        args = [P(640), P(2048), P(st), P(st), P(st), P(2 * 2 * 5 * 64 * 8), P(640), None]
-        assert lib.pdssm_scan_bwd_ste(ctypes.byref(d), *args, P(st), P(st), P(st), None, P(st), ws, need, None,
-                                      None) == pdssm.ERR_UNSUPPORTED
+        g, z = f(st // 2), f(2 * st)
+        q_in_z = ctypes.c_void_p(z.value + st // 2 + 256)
+        assert lib.pdssm_ste_grads(ctypes.byref(d), P(640), P(2048), g, z, q_in_z, None, ws, need, None,
+                                   None) == pdssm.ERR_INVALID_ARG
 
 
 def test_prepare_host_checks(lib):

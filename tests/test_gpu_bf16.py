@@ -139,3 +139,49 @@ def test_bf16_io_multi_pass_large_dictionary():
     assert pdssm.load().pdssm_uses_fused(ctypes.byref(pdssm.desc(2, 70, 2, 128, 128))) == 0
     exact, out = run_both(inp)
     check(inp, exact, out)
+
+
+@pytest.mark.parametrize("N,K,L", [(64, 16, 300), (128, 32, 200), (32, 5, 77)])
+def test_bf16_ste(N, K, L):
+    """The straight-through pair with bf16 pairs: z stays complex64 and equals
+    the fp32 path's bit for bit; db is its bf16 rounding; q and G from the
+    bf16 db equal the complex64 ste_grads on the widened db bit for bit, and
+    the oracle's (from the unrounded gradient) within the bf16 rounding."""
+    from helpers import assert_close_sum, ste_scales
+    from oracle import oracle_bwd, oracle_ste
+    print("bf16 ste N=%d K=%d L=%d" % (N, K, L), flush=True)
+    B, H = 2, 3
+    inp = make_inputs(B, L, H, N, K, seed=N + K + L, with_h0=True, with_dhf=True)
+    pairs, exact = {}, {}
+    for k in ("D", "b", "c"):
+        pairs[k], exact[k] = to_bf16_pairs(inp[k])
+    cplx = {k: torch.from_numpy(exact[k].astype(np.complex64)).to(DEV) for k in ("D", "b", "c")}
+    idx, pi = torch.from_numpy(inp["idx"]).to(DEV), torch.from_numpy(inp["pi"]).to(DEV)
+    h0, dhf = torch.from_numpy(inp["h0"]).to(DEV), torch.from_numpy(inp["dh_final"]).to(DEV)
+    dy = torch.from_numpy(inp["dy"]).to(DEV)
+    out = {}
+    for tag, T, bf in (("bf", pairs, True), ("f32", cplx, False)):
+        s = pdssm.Scan(B, L, H, N, K, 0, DEV, ste=True, bf16=bf)
+        s.fwd(idx, pi, T["D"], T["b"], T["c"], h0=h0)
+        s.bwd_ste(idx, pi, T["D"], T["b"], T["c"], dy, dh_final=dhf)
+        s.ste_grads(idx, pi)
+        s.check_status()
+        out[tag] = {k: getattr(s, k).clone() for k in ("db", "z", "q", "G")}
+        del s
+    bf, f32 = out["bf"], out["f32"]
+    assert bf["z"].dtype == torch.complex64
+    assert torch.equal(bf["z"], f32["z"])
+    assert torch.equal(bf["db"], rne_bf16(f32["db"]))
+    g_wide = torch.view_as_complex(bf["db"].to(torch.float32).contiguous())
+    q2, G2 = pdssm.ste_grads(idx, pi, g_wide, bf["z"])
+    assert torch.equal(bf["q"], q2) and torch.equal(bf["G"], G2)
+    q3, G3 = pdssm.ste_grads(idx, pi, bf["db"], bf["z"])  # module function, bf16 g
+    assert torch.equal(bf["q"], q3) and torch.equal(bf["G"], G3)
+    rg = oracle_bwd(inp["idx"], inp["pi"], exact["D"], exact["b"], exact["c"], inp["dy"], h0=inp["h0"],
+                    dh_final=inp["dh_final"])
+    q, G, z = oracle_ste(inp["idx"], inp["pi"], exact["D"], exact["b"], exact["c"], inp["dy"], h0=inp["h0"],
+                         dh_final=inp["dh_final"], want_z=True)
+    assert_close("z", bf["z"].cpu().numpy(), np.asarray(z))
+    qs, Gs = ste_scales(inp["pi"], inp["idx"], rg[1], z)
+    assert_close_sum("q", bf["q"].cpu().numpy(), q, qs, rtol=BF_RTOL)
+    assert_close_sum("G", bf["G"].cpu().numpy(), G, Gs, rtol=BF_RTOL)
