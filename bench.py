@@ -31,7 +31,8 @@ sequence of the workload on the 16-core CPU share of a one-GPU machine.
 prepare, forward, the backward with the scaled states (pdssm_scan_bwd_ste),
 the candidate-map scores and the dictionary gradient (pdssm_ste_grads) and
 the two tempered-softmax products (routing logits, dense dictionary); the
-line then carries an "ste" object with each call's time and roofline.
+line then carries an "ste" object with each call's time and roofline.  It
+combines with --real (real rows) and --bf16 (bf16 pairs, z complex64).
 
 --decode times single-step decode instead (pdssm_decode_step: one recurrence
 step per sequence, state updated in place), back to back on the workload's
@@ -83,18 +84,21 @@ def saved_bytes(w, C, ssz=8):
     return w.B * w.H * C * w.N * ssz
 
 
-def ste_bytes(w, C, real=False):
+def ste_bytes(w, C, real=False, bf16=False):
     """Algorithmic bytes and flops of the straight-through calls (real: the
-    real-valued model, 4-byte rows and real states)."""
+    real-valued model, 4-byte rows and real states; bf16: 4-byte rows, z
+    complex64)."""
     B, L, H, N, K = w.B, w.L, w.H, w.N, w.K
     steps = B * L * H
     su = steps * N
-    esz = 4 if real else 8
+    esz = 4 if (real or bf16) else 8
+    ssz = 4 if real else 8
+    zsz = 4 if real else 8
     return {
         # the plain backward, plus z [B,L,H,N] written
-        "bwd_ste": alg_bytes(w, C, "bwd", esz, esz) + su * esz,
+        "bwd_ste": alg_bytes(w, C, "bwd", esz, ssz) + su * zsz,
         # idx, pi, g (= db) and z read once, q [B,L,H,K] and G [H,K,N,N] f32 written once
-        "ste_grads": steps * 4 + H * K * N * 4 + 2 * su * esz + steps * K * 4 + H * K * N * N * 4,
+        "ste_grads": steps * 4 + H * K * N * 4 + su * (esz + zsz) + steps * K * 4 + H * K * N * N * 4,
         # per step and (i, j): Re(g_i conj z_j) = two real multiply-adds (one when real)
         "ste_grads_flops": (2 if real else 4) * steps * N * N,
         # logits and q in, d logits out; M and G in, dM out
@@ -392,8 +396,6 @@ def main():
         return
     if args.real and args.bf16:
         sys.exit("bench.py: --real and --bf16 do not combine (one row format at a time)")
-    if args.bf16 and args.ste:
-        sys.exit("bench.py: --bf16 and --ste do not combine (the straight-through path is complex64)")
     # Written between timed steps so that no input is still in L2 / MALL.
     flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
     res, inp = time_scan(args, args.workload, dev, flush)
@@ -579,7 +581,7 @@ def scan_line(args, w, res):
         "clock_settle": res["settle"],
     }
     if args.ste:
-        sb = ste_bytes(w, s.C, real=args.real)
+        sb = ste_bytes(w, s.C, real=args.real, bf16=args.bf16)
         out["fwd_bwd"] = None
         out["bwd"]["alg_bytes"] = sb["bwd_ste"]
         out["bwd"]["kernel"] = kern["bwd"] + " (+ z)"
@@ -592,7 +594,8 @@ def scan_line(args, w, res):
         out["roofline"]["kernel"] = kern[dom] + (" (+ z)" if dom == "bwd" else "")
         if dom == "bwd":
             out["roofline"]["bytes"] = ("algorithmic: idx, dy, D, b, c in; dD, db, dc, z, dh0 out "
-                                        "(%.1f + 8/N bytes per state update)" % (56.0 * esz / 8))
+                                        "(%.1f + 8/N bytes per state update)"
+                                        % (48.0 * esz / 8 + (4 if args.real else 8)))
         dg_ms, sm_ms = mean("ste_grads"), mean("softmax")
         gbps = sb["ste_grads"] / (dg_ms * 1e-3) / 1e9
         tfs = sb["ste_grads_flops"] / (dg_ms * 1e-3) / 1e12
